@@ -1,0 +1,480 @@
+"""CPU oracle for the UFP4 hot path -- TEST INFRASTRUCTURE ONLY.
+
+This is a plain, slow and deliberately obvious reference for the data-parallel hot path of the UFP4
+recipe in "Rethinking Shrinkage Bias in LLM FP4 Pretraining" (arXiv 2606.20381):
+
+  * the block-16 Random Hadamard Transform (RHT) of Sec. 2.2, applied along the reduction axis of a GEMM
+    operand;
+  * 1x16 block-scaled quantization (Sec. 2.1) to the uniform 4-bit grid of the recipe (Sec. 4, Table 1:
+    codes -7..7) or to the E2M1 grid of the comparison recipe, with round-to-nearest-even (RTNE) or
+    stochastic rounding (SR);
+  * the quantized training GEMMs fwd_y, bwd_dx and bwd_dw (Sec. 2.2, last display and its closing
+    sentence), evaluated as an fp64 product of the dequantized operands.
+
+Who may use it: the tests, the smoke check and the CPU-baseline leg of the benchmark. The product (the
+HIP library and its Python binding) never imports, links or runs anything here, and nothing here imports
+the product package. Inputs are numpy arrays; bf16 tensors arrive as their raw uint16 bit patterns.
+
+Readings of the paper that this oracle fixes (the paper states exact mathematics only):
+  * RHT arithmetic: y = RN_fp32( (1/4) * sum_j H16[i,j] * eps_j * x_j ), the exact 16-term sum rounded
+    once to fp32 ("correctly rounded"). The sum is evaluated in fp64 through an explicit 16x16 matrix
+    product; this is exact when the nonzero magnitudes of a block span at most 2^41 (checked, see
+    `_check_rht_domain`).
+  * Scale and reciprocal: s = RN32(amax / g), r = RN32(g / amax), v = RN32(y * r); g = 7 (uniform) or
+    6 (E2M1). A block with amax = 0 gets s = 0 and all codes 0.
+  * RTNE tie rule: the level whose magnitude code is even (IEEE round-half-even on the 4-bit encoding).
+  * SR: q = g_b with probability (v - g_a)/(g_b - g_a) over adjacent signed levels g_a <= v < g_b,
+    realised with a 16-bit uniform draw U = u / 2^16: q = g_b iff U < (v - g_a)/(g_b - g_a).
+    The draws come from Philox4x32-10 with key = seed and counter = (block, row, half, stream).
+  * Codes outside the grid are clamped (|v| can exceed g by one fp32 ulp).
+  * Packing: uniform codes as two's-complement nibbles, E2M1 codes as OCP FP4 bit patterns (sign bit 3,
+    canonical +0); element 2j in the low nibble of byte j.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+# ---------------------------------------------------------------------------------------------------
+# Formats, rounding modes, constants (Sec. 2.1; Table 1)
+# ---------------------------------------------------------------------------------------------------
+
+UNIFORM = 0  # E1M2/INT4-style uniform grid, integer codes -7..7 (Sec. 4 recipe; Table 1)
+E2M1 = 1  # FP4 E2M1 grid of the comparison recipe (Sec. 2.1, Fig. 1; Table 1)
+
+RTNE = 0  # round to nearest, deterministic ties (Sec. 2.1)
+SR = 1  # stochastic rounding (Sec. 2.1, second display)
+
+BLOCK = 16  # 1x16 quantization block and RHT block (Table 1)
+
+# Non-negative levels of each grid, in magnitude-code order (Sec. 2.1; Sec. 3.1 lists the E2M1 ones).
+GRID_MAGNITUDES = {
+    UNIFORM: np.arange(8, dtype=np.float64),  # 0..7; the E1M2 levels k/4 scaled by 4
+    E2M1: np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]),
+}
+G_MAX = {UNIFORM: 7.0, E2M1: 6.0}  # g_max of Sec. 2.1
+
+
+# ---------------------------------------------------------------------------------------------------
+# bf16 helpers
+# ---------------------------------------------------------------------------------------------------
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact bf16 -> fp32 widening of raw uint16 bit patterns."""
+    bits = np.asarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round to nearest even (finite inputs)."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    u = u + np.uint64(0x7FFF) + lsb
+    return (u >> np.uint64(16)).astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------------------------------
+# Hadamard matrices and the RHT (Sec. 2.2)
+# ---------------------------------------------------------------------------------------------------
+
+def sylvester_hadamard(n: int) -> np.ndarray:
+    """Normalised Sylvester Hadamard H_n by the recursion of Sec. 2.2 (H_1 = [1], factor 1/sqrt(2))."""
+    if n < 1 or n & (n - 1):
+        raise ValueError("n must be a power of two")
+    h = np.ones((1, 1))
+    while h.shape[0] < n:
+        h = np.block([[h, h], [h, -h]]) / np.sqrt(2.0)
+    return h
+
+
+def hadamard_pm1(n: int = BLOCK) -> np.ndarray:
+    """The same recursion without the 1/sqrt(2) factors: the +-1 matrix, H_n = hadamard_pm1(n)/sqrt(n).
+
+    For n = 16 the collected normalisation is exactly 1/4 (Sec. 2.2 recursion, four levels).
+    """
+    if n < 1 or n & (n - 1):
+        raise ValueError("n must be a power of two")
+    h = np.ones((1, 1))
+    while h.shape[0] < n:
+        h = np.block([[h, h], [h, -h]])
+    return h
+
+
+def sign_vector(sign_mask: int, n: int = BLOCK) -> np.ndarray:
+    """Diagonal of the random sign matrix S_n of Sec. 2.2: eps_j = -1 iff bit j of the mask is set."""
+    return np.array([-1.0 if (int(sign_mask) >> j) & 1 else 1.0 for j in range(n)])
+
+
+def _check_rht_domain(blocks: np.ndarray) -> None:
+    """Check that the fp64 evaluation of every 16-term sum is exact.
+
+    Each term is a bf16 value (8 significant bits). With frexp exponents e_max and e_min over the nonzero
+    entries of a block, the exact sum is a multiple of 2^(e_min - 8) below 2^(e_max + 4) in magnitude, so
+    it fits the 53-bit fp64 significand when e_max - e_min <= 41.
+    """
+    mag = np.abs(blocks)
+    nz = mag > 0
+    _, e = np.frexp(np.where(nz, mag, 1.0))
+    e_max = np.where(nz, e, np.iinfo(np.int32).min).max(axis=-1)
+    e_min = np.where(nz, e, np.iinfo(np.int32).max).min(axis=-1)
+    spread = np.where(nz.any(axis=-1), e_max - e_min, 0)
+    if np.any(spread > 41):
+        raise ValueError("a block spans more than 2^41 in magnitude: the RHT sum is not exact in fp64")
+
+
+def rht_exact_f64(blocks: np.ndarray, sign_mask: int) -> np.ndarray:
+    """Unrounded RHT of 16-element row blocks: each row vector x becomes x S_16 H_16 (Sec. 2.2).
+
+    `blocks` has shape [..., 16]. H_16 is symmetric, so (x S H)_i = (1/4) sum_j H16pm1[i,j] eps_j x_j.
+    Evaluated as an explicit matrix product in fp64; exact under `_check_rht_domain`.
+    """
+    blocks = np.asarray(blocks, dtype=np.float64)
+    eps = sign_vector(sign_mask)
+    return ((blocks * eps) @ hadamard_pm1(BLOCK)) * 0.25
+
+
+def rht_blocks(blocks_f32: np.ndarray, sign_mask: int) -> np.ndarray:
+    """RHT of bf16-valued 16-blocks, correctly rounded to fp32 (one rounding of the exact result)."""
+    b64 = np.asarray(blocks_f32, dtype=np.float64)
+    _check_rht_domain(b64)
+    return rht_exact_f64(b64, sign_mask).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------------------------------
+# Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11)
+# ---------------------------------------------------------------------------------------------------
+
+PHILOX_M0 = 0xD2511F53
+PHILOX_M1 = 0xCD9E8D57
+PHILOX_W0 = 0x9E3779B9
+PHILOX_W1 = 0xBB67AE85
+_MASK32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(c0, c1, c2, c3, k0, k1):
+    """Philox4x32 with 10 rounds on arrays of 32-bit counters; returns the four 32-bit output words.
+
+    One round: (hi0, lo0) = M0 * c0, (hi1, lo1) = M1 * c2 (64-bit products);
+    (c0, c1, c2, c3) <- (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0); then the key is bumped by the Weyl
+    constants (W0, W1) before the next round.
+    """
+    c0 = np.asarray(c0, dtype=np.uint64) & _MASK32
+    c1 = np.asarray(c1, dtype=np.uint64) & _MASK32
+    c2 = np.asarray(c2, dtype=np.uint64) & _MASK32
+    c3 = np.asarray(c3, dtype=np.uint64) & _MASK32
+    k0 = np.uint64(int(k0) & 0xFFFFFFFF)
+    k1 = np.uint64(int(k1) & 0xFFFFFFFF)
+    c0, c1, c2, c3 = np.broadcast_arrays(c0, c1, c2, c3)
+    for _ in range(10):
+        p0 = c0 * np.uint64(PHILOX_M0)
+        p1 = c2 * np.uint64(PHILOX_M1)
+        hi0, lo0 = p0 >> np.uint64(32), p0 & _MASK32
+        hi1, lo1 = p1 >> np.uint64(32), p1 & _MASK32
+        c0, c1, c2, c3 = hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0
+        k0 = (k0 + np.uint64(PHILOX_W0)) & _MASK32
+        k1 = (k1 + np.uint64(PHILOX_W1)) & _MASK32
+    return tuple(w.astype(np.uint32) for w in (c0, c1, c2, c3))
+
+
+def sr_draws(block_idx, row_idx, seed: int, stream: int) -> np.ndarray:
+    """The sixteen 16-bit uniform draws of each quantization block, shape [..., 16] (uint16).
+
+    Block (row r, block b) uses two Philox calls, counter (b, r, h, stream) for h = 0, 1 and key
+    (seed low 32 bits, seed high 32 bits). Element j of the block takes the 16-bit half (j & 1) -- low
+    half first -- of output word (j & 7) >> 1 of call h = j >> 3.
+    """
+    b = np.asarray(block_idx, dtype=np.uint64)
+    r = np.asarray(row_idx, dtype=np.uint64)
+    b, r = np.broadcast_arrays(b, r)
+    k0, k1 = int(seed) & 0xFFFFFFFF, (int(seed) >> 32) & 0xFFFFFFFF
+    out = np.empty(b.shape + (BLOCK,), dtype=np.uint16)
+    for h in range(2):
+        words = philox4x32_10(b, r, np.uint64(h), np.uint64(int(stream) & 0xFFFFFFFF), k0, k1)
+        for w in range(4):
+            out[..., 8 * h + 2 * w] = (words[w] & np.uint32(0xFFFF)).astype(np.uint16)
+            out[..., 8 * h + 2 * w + 1] = (words[w] >> np.uint32(16)).astype(np.uint16)
+    return out
+
+
+# ---------------------------------------------------------------------------------------------------
+# Rounding onto a grid (Sec. 2.1)
+# ---------------------------------------------------------------------------------------------------
+
+def round_nearest_even(v: np.ndarray, fmt: int) -> np.ndarray:
+    """RTNE onto the signed grid: nearest level; on a tie, the level with the even magnitude code.
+
+    Returns signed level *indices* (magnitude code with the sign of v; -0 becomes 0). Values beyond the
+    largest level go to it (the nearest level). Brute force over every level.
+    """
+    mags = GRID_MAGNITUDES[fmt]
+    a = np.abs(np.asarray(v, dtype=np.float64))
+    dist = np.abs(a[..., None] - mags)  # exact: fp32 inputs, small dyadic levels
+    best = dist.min(axis=-1, keepdims=True)
+    cand = dist == best
+    # among the (at most two) nearest levels prefer the even magnitude code
+    even = (np.arange(8) % 2) == 0
+    pick_even = cand & even
+    idx = np.where(pick_even.any(axis=-1), pick_even.argmax(axis=-1), cand.argmax(axis=-1))
+    return np.where(np.asarray(v) < 0, -idx, idx).astype(np.int64)
+
+
+def _signed_levels(fmt: int) -> np.ndarray:
+    mags = GRID_MAGNITUDES[fmt]
+    return np.concatenate([-mags[:0:-1], mags])  # ascending, -g_max .. g_max
+
+
+def round_stochastic(v: np.ndarray, u16: np.ndarray, fmt: int) -> np.ndarray:
+    """SR onto the signed grid with 16-bit draws (Sec. 2.1, second display).
+
+    For g_a <= v < g_b adjacent signed levels, q = g_b iff u/2^16 < (v - g_a)/(g_b - g_a); otherwise g_a.
+    v on a level stays there; |v| beyond the largest level goes to it. Returns signed level indices.
+    """
+    levels = _signed_levels(fmt)
+    v64 = np.asarray(v, dtype=np.float64)
+    vc = np.clip(v64, levels[0], levels[-1])
+    ia = np.searchsorted(levels, vc, side="right") - 1  # levels[ia] <= vc
+    ia = np.clip(ia, 0, len(levels) - 1)
+    ib = np.minimum(ia + 1, len(levels) - 1)
+    ga, gb = levels[ia], levels[ib]
+    width = np.where(ib > ia, gb - ga, 1.0)
+    p_up = np.where(ib > ia, (vc - ga) / width, 0.0)  # exact: dyadic numbers, power-of-two widths
+    u = np.asarray(u16, dtype=np.float64) / 65536.0
+    q = np.where(u < p_up, gb, ga)
+    # back to signed magnitude index
+    mags = GRID_MAGNITUDES[fmt]
+    idx = np.searchsorted(mags, np.abs(q))
+    return np.where(q < 0, -idx, idx).astype(np.int64)
+
+
+def level_values(signed_idx: np.ndarray, fmt: int) -> np.ndarray:
+    """Signed level index -> level value (fp64)."""
+    signed_idx = np.asarray(signed_idx)
+    mags = GRID_MAGNITUDES[fmt]
+    return np.sign(signed_idx) * mags[np.abs(signed_idx)]
+
+
+# ---------------------------------------------------------------------------------------------------
+# The blockwise quantizer Q_G of Sec. 2.1, with the RHT of Sec. 2.2 in front
+# ---------------------------------------------------------------------------------------------------
+
+def _check_block_domain(amax: np.ndarray, g: float) -> None:
+    nz = amax > 0
+    r = np.float32(g) / np.where(nz, amax, np.float32(1.0))
+    if not np.all(np.isfinite(amax)) or not np.all(np.isfinite(r)):
+        raise ValueError("non-finite input, or a block amax so small that g/amax overflows fp32")
+
+
+def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0,
+                  seed: int = 0, stream: int = 0, row_ids=None, block_base: int = 0):
+    """Quantize an operand A [rows, red] along its contiguous (reduction) axis.
+
+    Steps per 1x16 block B (Sec. 2.1 display; RHT of Sec. 2.2 applied first when `rht`):
+      y = RHT(x) or x;  s = RN32(amax/g);  q_i = rho(y_i / s) with y_i/s taken as RN32(y_i * RN32(g/amax)).
+    `row_ids` are the global row numbers used in the SR counters (default 0..rows-1); `block_base` is
+    added to the block number (used for operands cut out of a longer reduction axis).
+    Returns (signed level indices int64 [rows, red], scales fp32 [rows, red/16]).
+    """
+    a = np.asarray(a_f32, dtype=np.float32)
+    rows, red = a.shape
+    if red % BLOCK:
+        raise ValueError("reduction length must be a multiple of 16")
+    nb = red // BLOCK
+    blocks = a.reshape(rows, nb, BLOCK)
+    y = rht_blocks(blocks, sign_mask) if rht else blocks.copy()
+    if not np.all(np.isfinite(y)):
+        raise ValueError("non-finite value after the transform")
+    g = np.float32(G_MAX[fmt])
+    amax = np.abs(y).max(axis=-1)  # fp32
+    _check_block_domain(amax, float(g))
+    nz = amax > 0
+    scale = np.where(nz, amax / g, np.float32(0.0)).astype(np.float32)
+    recip = np.where(nz, g / np.where(nz, amax, np.float32(1.0)), np.float32(0.0)).astype(np.float32)
+    v = (y * recip[..., None]).astype(np.float32)  # one fp32 multiply per element
+    if rounding == RTNE:
+        idx = round_nearest_even(v, fmt)
+    elif rounding == SR:
+        rid = np.arange(rows) if row_ids is None else np.asarray(row_ids)
+        bidx = block_base + np.arange(nb)
+        u = sr_draws(bidx[None, :], rid[:, None], seed, stream)
+        idx = round_stochastic(v, u, fmt)
+    else:
+        raise ValueError("unknown rounding mode")
+    idx = np.where(nz[..., None], idx, 0)
+    return idx.reshape(rows, red), scale
+
+
+# ---------------------------------------------------------------------------------------------------
+# Operand views per GEMM (Sec. 2.2, closing sentence: the RHT axis is the reduction axis)
+# ---------------------------------------------------------------------------------------------------
+
+def operand_rowwise(t_bits: np.ndarray) -> np.ndarray:
+    """Operand whose reduction axis is the contiguous axis of the stored tensor: A = T."""
+    return bf16_bits_to_f32(t_bits)
+
+
+def operand_colwise(t_bits: np.ndarray) -> np.ndarray:
+    """Operand whose reduction axis is the strided axis: A = T^T (rows of A are columns of T)."""
+    return np.ascontiguousarray(bf16_bits_to_f32(t_bits).T)
+
+
+def pad16(n: int) -> int:
+    return -(-int(n) // BLOCK) * BLOCK
+
+
+def operand_colwise_grouped(t_bits: np.ndarray, counts) -> tuple[np.ndarray, np.ndarray]:
+    """Transposed operand of a grouped (MoE) tensor whose rows are split into consecutive groups.
+
+    Group g owns rows [off_g, off_g + counts[g]) of T. Its block of A is T[group]^T with the reduction
+    axis (the group's tokens) zero-padded to a multiple of 16; the padded groups are concatenated along
+    the reduction axis. Zero padding keeps every group's GEMM unchanged ((XH')(WH')^T = XW^T).
+    Returns (A [cols, sum pad16(counts)], padded offsets [G+1]).
+    """
+    t = bf16_bits_to_f32(t_bits)
+    counts = [int(c) for c in counts]
+    if sum(counts) != t.shape[0]:
+        raise ValueError("group counts do not cover the rows")
+    pads = [pad16(c) for c in counts]
+    poff = np.concatenate([[0], np.cumsum(pads)]).astype(np.int64)
+    a = np.zeros((t.shape[1], int(poff[-1])), dtype=np.float32)
+    off = 0
+    for g, c in enumerate(counts):
+        a[:, poff[g]:poff[g] + c] = t[off:off + c].T
+        off += c
+    return a, poff
+
+
+# ---------------------------------------------------------------------------------------------------
+# Packing (codes -> bytes) and dequantization
+# ---------------------------------------------------------------------------------------------------
+
+def code_nibbles(idx: np.ndarray, fmt: int) -> np.ndarray:
+    """4-bit code of each element: two's complement of k for the uniform grid; sign<<3 | magnitude code
+    (OCP FP4 E2M1 bit pattern, canonical +0) for E2M1."""
+    idx = np.asarray(idx, dtype=np.int64)
+    if fmt == UNIFORM:
+        return (idx & 0xF).astype(np.uint8)
+    sign = (idx < 0).astype(np.int64)
+    return ((sign << 3) | np.abs(idx)).astype(np.uint8)
+
+
+def nibbles_to_idx(nib: np.ndarray, fmt: int) -> np.ndarray:
+    nib = np.asarray(nib, dtype=np.int64)
+    if fmt == UNIFORM:
+        return np.where(nib >= 8, nib - 16, nib)
+    mag = nib & 7
+    return np.where(nib & 8, -mag, mag)
+
+
+def pack_codes(idx: np.ndarray, fmt: int) -> np.ndarray:
+    """[rows, red] level indices -> [rows, red/2] bytes; element 2j in the low nibble of byte j."""
+    nib = code_nibbles(idx, fmt)
+    return (nib[:, 0::2] | (nib[:, 1::2] << np.uint8(4))).astype(np.uint8)
+
+
+def unpack_codes(packed: np.ndarray, fmt: int) -> np.ndarray:
+    packed = np.asarray(packed, dtype=np.uint8)
+    rows, half = packed.shape
+    nib = np.empty((rows, 2 * half), dtype=np.uint8)
+    nib[:, 0::2] = packed & np.uint8(0xF)
+    nib[:, 1::2] = packed >> np.uint8(4)
+    return nibbles_to_idx(nib, fmt)
+
+
+def dequantize(idx: np.ndarray, scales: np.ndarray, fmt: int) -> np.ndarray:
+    """Q_G(T) as a numerical tensor (Sec. 2.1 footnote sentence): level value times block scale, fp64."""
+    idx = np.asarray(idx)
+    rows, red = idx.shape
+    vals = level_values(idx, fmt).reshape(rows, red // BLOCK, BLOCK)
+    return (vals * np.asarray(scales, dtype=np.float64)[..., None]).reshape(rows, red)
+
+
+# ---------------------------------------------------------------------------------------------------
+# Quantized GEMMs (Sec. 2.2: Y_hat = Q(XH') Q(WH')^T; all three training GEMMs in the same NT form)
+# ---------------------------------------------------------------------------------------------------
+
+def gemm_nt(a_idx, a_scales, b_idx, b_scales, fmt: int) -> np.ndarray:
+    """C = deq(A) @ deq(B)^T in fp64; A [M, red], B [N, red] share the quantized reduction axis."""
+    return dequantize(a_idx, a_scales, fmt) @ dequantize(b_idx, b_scales, fmt).T
+
+
+def gemm_nt_grouped(a_idx, a_scales, b_idx, b_scales, fmt: int, a_rows=None, b_rows=None,
+                    red_cols=None) -> list[np.ndarray]:
+    """Per-group NT GEMMs. Each of `a_rows`, `b_rows`, `red_cols` is a list of (start, stop) pairs or
+    None (whole axis); group g multiplies A[a_rows[g], red_cols[g]] by B[b_rows[g], red_cols[g]]^T."""
+    da = dequantize(a_idx, a_scales, fmt)
+    db = dequantize(b_idx, b_scales, fmt)
+    n = max(len(x) for x in (a_rows, b_rows, red_cols) if x is not None)
+    out = []
+    for g in range(n):
+        ar = slice(*a_rows[g]) if a_rows is not None else slice(None)
+        br = slice(*b_rows[g]) if b_rows is not None else slice(None)
+        rc = slice(*red_cols[g]) if red_cols is not None else slice(None)
+        out.append(da[ar, rc] @ db[br, rc].T)
+    return out
+
+
+# ---------------------------------------------------------------------------------------------------
+# One linear layer's three quantized GEMMs under a recipe (Sec. 4, Table 1; Sec. 2.2 closing sentence)
+# ---------------------------------------------------------------------------------------------------
+
+RECIPES = {
+    # format, RHT on (fwd_y, bwd_dx, bwd_dw), SR on dY only (Table 1)
+    "ufp4": dict(fmt=UNIFORM, rht=(True, True, True)),
+    "e2m1": dict(fmt=E2M1, rht=(False, False, True)),
+}
+
+
+def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 0, seed: int = 0):
+    """Quantize the six operands of one linear layer and run fwd_y, bwd_dx and bwd_dw.
+
+    X [M, K], W [N, K], dY [M, N] (bf16 bit patterns). Operands:
+      fwd_y : X, W rowwise along K (RTNE)              -> Y  [M, N]
+      bwd_dx: dY rowwise along N (SR, stream 0),  W^T along N (RTNE)  -> dX [M, K]
+      bwd_dw: dY^T along M (SR, stream 1),       X^T along M (RTNE)  -> dW [N, K]
+    Returns a dict with the quantized operands (idx, scales) and the three fp64 outputs.
+    """
+    cfg = RECIPES[recipe]
+    fmt = cfg["fmt"]
+    r_y, r_dx, r_dw = cfg["rht"]
+    q = {}
+    q["x"] = quantize_rows(operand_rowwise(x_bits), fmt, RTNE, r_y, sign_mask)
+    q["w"] = quantize_rows(operand_rowwise(w_bits), fmt, RTNE, r_y, sign_mask)
+    q["dy"] = quantize_rows(operand_rowwise(dy_bits), fmt, SR, r_dx, sign_mask, seed, 0)
+    q["wt"] = quantize_rows(operand_colwise(w_bits), fmt, RTNE, r_dx, sign_mask)
+    q["dyt"] = quantize_rows(operand_colwise(dy_bits), fmt, SR, r_dw, sign_mask, seed, 1)
+    q["xt"] = quantize_rows(operand_colwise(x_bits), fmt, RTNE, r_dw, sign_mask)
+    out = {
+        "y": gemm_nt(*q["x"], *q["w"], fmt),
+        "dx": gemm_nt(*q["dy"], *q["wt"], fmt),
+        "dw": gemm_nt(*q["dyt"], *q["xt"], fmt),
+    }
+    return q, out
+
+
+# ---------------------------------------------------------------------------------------------------
+# Quality diagnostics (Sec. 3.2): SQNR, operand projection alpha, bucket entropy / effective ratio
+# ---------------------------------------------------------------------------------------------------
+
+def nmse(q: np.ndarray, ref: np.ndarray) -> float:
+    """||Q - T||_F^2 / ||T||_F^2 (Sec. 3.2, NMSE)."""
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.sum((np.asarray(q, dtype=np.float64) - ref) ** 2) / np.sum(ref ** 2))
+
+
+def sqnr_db(q: np.ndarray, ref: np.ndarray) -> float:
+    return float(-10.0 * np.log10(nmse(q, ref)))
+
+
+def operand_projection(q: np.ndarray, ref: np.ndarray) -> float:
+    """alpha_A = <A_hat, A>_F / ||A||_F^2 (Sec. 3.2, operand projection)."""
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.sum(np.asarray(q, dtype=np.float64) * ref) / np.sum(ref * ref))
+
+
+def effective_bucket_ratio(idx: np.ndarray, fmt: int, eps: float = 1e-12) -> float:
+    """B_eff = exp(E)/K with E = -sum p_i log(p_i + eps) over the K magnitude buckets (Sec. 3.2)."""
+    k = len(GRID_MAGNITUDES[fmt])
+    mag = np.abs(np.asarray(idx)).ravel()
+    p = np.bincount(mag, minlength=k)[:k] / mag.size
+    ent = -np.sum(p * np.log(p + eps))
+    return float(np.exp(ent) / k)

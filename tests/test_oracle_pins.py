@@ -1,0 +1,507 @@
+"""Pins for the CPU oracle: each test ties the oracle to something other than itself -- a value the paper
+prints, a closed form, an invariant, a library routine or brute force on tiny inputs."""
+
+import os
+import shutil
+import subprocess
+import tempfile
+from fractions import Fraction
+from math import floor
+
+import numpy as np
+import pytest
+
+from oracle import ufp4_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _read_table(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+def _rand_bf16_bits(rng, shape, scale=1.0):
+    x = (rng.standard_normal(shape) * scale).astype(np.float32)
+    return O.f32_to_bf16_bits(x)
+
+
+# ------------------------------------------------------------------------------------------------
+# Hadamard / RHT (Sec. 2.2)
+# ------------------------------------------------------------------------------------------------
+
+def test_sylvester_recursion_equals_popcount_closed_form():
+    h = O.hadamard_pm1(16)
+    for i in range(16):
+        for j in range(16):
+            assert h[i, j] == (-1) ** bin(i & j).count("1")
+
+
+@pytest.mark.parametrize("n", [2, 4, 8, 16, 32, 64])
+def test_hadamard_orthogonality(n):
+    h = O.hadamard_pm1(n)
+    assert np.array_equal(h @ h.T, n * np.eye(n))
+    hn = O.sylvester_hadamard(n)
+    assert np.abs(hn.T @ hn - np.eye(n)).max() < 1e-14
+    assert np.abs(hn - h / np.sqrt(n)).max() < 1e-15
+
+
+@pytest.mark.parametrize("mask", [0, 1, 0x8000, 0xA5C3, 0xFFFF])
+def test_rht_orthogonal_and_invertible(mask):
+    eps = O.sign_vector(mask)
+    m = np.diag(eps) @ O.hadamard_pm1(16)
+    assert np.array_equal(m @ m.T, 16 * np.eye(16))
+    rng = np.random.default_rng(mask)
+    x = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (50, 16))).astype(np.float64)
+    y = O.rht_exact_f64(x, mask)
+    # x S H / 4 = y  =>  x = 4 y H S / 16 = y H S / 4 (H symmetric, H H = 16 I)
+    back = (y @ O.hadamard_pm1(16)) * eps * 0.25
+    assert np.array_equal(back, x)
+
+
+def test_sign_mask_bit_order():
+    # bit j of the mask flips element j: a unit vector at j maps to eps_j * (row j of H) / 4
+    for j in range(16):
+        e = np.zeros((1, 16))
+        e[0, j] = 1.0
+        y_flip = O.rht_exact_f64(e, 1 << j)
+        y_keep = O.rht_exact_f64(e, 0xFFFF ^ (1 << j))
+        assert np.array_equal(y_flip[0], -O.hadamard_pm1(16)[j] / 4)
+        assert np.array_equal(y_keep[0], O.hadamard_pm1(16)[j] / 4)
+
+
+def test_rotation_invariance_all_three_gemms():
+    """Sec. 2.2: Y = X W^T = (X H')(W H')^T along the shared dimension, for fwd_y, bwd_dx and bwd_dw."""
+    rng = np.random.default_rng(7)
+    m, n, k = 48, 32, 64
+    x = rng.standard_normal((m, k))
+    w = rng.standard_normal((n, k))
+    dy = rng.standard_normal((m, n))
+    mask = 0x3C5A
+
+    def rot(a):  # rotate rows of a (reduction axis contiguous) blockwise
+        r, c = a.shape
+        return O.rht_exact_f64(a.reshape(r, c // 16, 16), mask).reshape(r, c)
+
+    for a, b, ref in [(x, w, x @ w.T), (dy, w.T, dy @ w), (dy.T, x.T, dy.T @ x)]:
+        got = rot(np.ascontiguousarray(a)) @ rot(np.ascontiguousarray(b)).T
+        assert np.linalg.norm(got - ref) / np.linalg.norm(ref) < 1e-13
+
+
+def _round_fraction_f32(q: Fraction) -> np.float32:
+    """Correct IEEE binary32 round-half-even of an exact rational (independent of any float path)."""
+    if q == 0:
+        return np.float32(0.0)
+    sign = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    ulp_e = max(e - 23, -149)
+    scaled = a / Fraction(2) ** ulp_e
+    n = floor(scaled)
+    rem = scaled - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    val = Fraction(n) * Fraction(2) ** ulp_e
+    assert val < Fraction(2) ** 128
+    return np.float32(sign * float(val))  # n < 2^25: exact in fp64 and in fp32
+
+
+def test_rht_correctly_rounded_bruteforce():
+    """y_i = RN32(1/4 sum_j H[i,j] eps_j x_j) against exact rational arithmetic, including blocks whose
+    magnitudes span up to 2^41 and subnormal-range results."""
+    rng = np.random.default_rng(11)
+    blocks = []
+    for t in range(300):
+        mant = rng.integers(-255, 256, size=16)
+        spread = int(rng.integers(0, 42))
+        base = int(rng.integers(-120, 100))
+        expo = base - rng.integers(0, spread + 1, size=16)
+        vals = np.array([float(Fraction(int(mm)) * Fraction(2) ** int(ee - 7)) for mm, ee in zip(mant, expo)])
+        if t % 7 == 0:
+            vals[rng.integers(0, 16, size=5)] = 0.0
+        blocks.append(O.bf16_bits_to_f32(O.f32_to_bf16_bits(vals.astype(np.float32))))
+    blocks = np.array(blocks)
+    # keep only blocks inside the exactness domain after the bf16 rounding
+    mask = 0x9E37
+    got = None
+    keep = []
+    for b in blocks:
+        try:
+            O._check_rht_domain(b[None].astype(np.float64))
+            keep.append(b)
+        except ValueError:
+            pass
+    keep = np.array(keep)
+    assert len(keep) > 250
+    got = O.rht_blocks(keep, mask)
+    h = O.hadamard_pm1(16)
+    eps = O.sign_vector(mask)
+    for bi, b in enumerate(keep):
+        xs = [Fraction(float(v)) for v in b]
+        for i in range(16):
+            s = sum(Fraction(int(h[i, j] * eps[j])) * xs[j] for j in range(16)) / 4
+            want = _round_fraction_f32(s)
+            assert got[bi, i].view(np.uint32) == want.view(np.uint32), (bi, i)
+
+
+def test_rht_domain_is_enforced():
+    b = np.zeros((1, 16))
+    b[0, 0] = 2.0 ** 20
+    b[0, 1] = 2.0 ** -22  # spread 42
+    with pytest.raises(ValueError):
+        O.rht_blocks(b.astype(np.float32), 0)
+    b[0, 1] = 2.0 ** -21  # spread 41: allowed
+    O.rht_blocks(b.astype(np.float32), 0)
+
+
+# ------------------------------------------------------------------------------------------------
+# Rounding rules (Sec. 2.1) and Shrinkage Bias (Sec. 3.1)
+# ------------------------------------------------------------------------------------------------
+
+def test_uniform_rtne_is_rint_and_clip():
+    rng = np.random.default_rng(3)
+    v = np.concatenate([rng.uniform(-7.6, 7.6, 100000).astype(np.float32),
+                        np.arange(-15, 16, dtype=np.float32) / 2,  # every tie
+                        np.float32([7.0000005, -7.0000005, 0.0, -0.0])])
+    got = O.round_nearest_even(v, O.UNIFORM)
+    want = np.clip(np.rint(v.astype(np.float64)), -7, 7).astype(np.int64)
+    assert np.array_equal(got, want)
+
+
+def test_e2m1_rtne_ties_golden():
+    rows = _read_table("e2m1_ties.txt")
+    v = np.array([float(r[0]) for r in rows], dtype=np.float32)
+    want = np.array([float(r[1]) for r in rows])
+    got = O.level_values(O.round_nearest_even(v, O.E2M1), O.E2M1)
+    assert np.array_equal(got, want)
+
+
+def test_e2m1_rtne_matches_threshold_search():
+    """Nearest level by searching the bin edges (midpoints) -- a different algorithm from the oracle's
+    distance argmin; ties resolved by the golden tie table above."""
+    mags = np.array([0, .5, 1, 1.5, 2, 3, 4, 6])
+    mids = (mags[:-1] + mags[1:]) / 2
+    rng = np.random.default_rng(5)
+    v = rng.uniform(-7, 7, 200000).astype(np.float32)
+    v = v[~np.isin(np.abs(v), mids)]
+    idx = np.searchsorted(mids, np.abs(v.astype(np.float64)))
+    want = np.where(v < 0, -mags[idx], mags[idx])
+    got = O.level_values(O.round_nearest_even(v, O.E2M1), O.E2M1)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("row", _read_table("shrinkage_bias_bins.txt"))
+def test_shrinkage_bias_per_bin(row):
+    """Eq. (eq:bin-asymmetry-bias) by dense enumeration of a locally uniform density inside each bin."""
+    fmt = O.E2M1 if row[0] == "e2m1" else O.UNIFORM
+    lo, hi, want = float(row[2]), float(row[3]), float(row[4])
+    n = 1 << 20
+    t = lo + (hi - lo) * (np.arange(n) + 0.5) / n  # midpoint rule: strictly inside the open bin
+    q = O.level_values(O.round_nearest_even(t, fmt), fmt)
+    assert np.all(q == float(row[1]))
+    assert abs(np.mean(q - t) - want) < 1e-9
+
+
+def test_shrinkage_bias_uniform_inputs():
+    """Uniform inputs over a range ending inside a bin: E2M1 shows a negative mean error, the uniform grid
+    none. Over the full range [0, g_max] every grid has zero mean error (trapezoid identity), so the
+    range stops at 5: the upper edge of E2M1's (3.5, 5) bin and the middle of the uniform (4.5, 5.5) bin."""
+    n = 1 << 21
+    t = 5.0 * (np.arange(n) + 0.5) / n
+    b_e2m1 = np.mean(O.level_values(O.round_nearest_even(t, O.E2M1), O.E2M1) - t)
+    b_uni = np.mean(O.level_values(O.round_nearest_even(t, O.UNIFORM), O.UNIFORM) - t)
+    # closed form: the integral of (rho(t) - t) over each bin piece inside [0, 5], divided by 5
+    pieces = [(0, 0.25, 0), (0.25, 0.75, .5), (0.75, 1.25, 1), (1.25, 1.75, 1.5), (1.75, 2.5, 2),
+              (2.5, 3.5, 3), (3.5, 5.0, 4)]
+    want_e2m1 = sum(q * (b - a) - (b * b - a * a) / 2 for a, b, q in pieces) / 5.0
+    pieces_u = [(0, .5, 0), (.5, 1.5, 1), (1.5, 2.5, 2), (2.5, 3.5, 3), (3.5, 4.5, 4), (4.5, 5.0, 5)]
+    want_uni = sum(q * (b - a) - (b * b - a * a) / 2 for a, b, q in pieces_u) / 5.0
+    assert abs(want_uni) < 1e-15
+    assert want_e2m1 < -0.05
+    # the sample grid straddles bin edges (discontinuities), so the midpoint rule is accurate to ~1e-7
+    assert abs(b_e2m1 - want_e2m1) < 1e-6
+    assert abs(b_uni - want_uni) < 1e-6
+
+
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+def test_sr_exact_expectation(fmt):
+    """Sec. 2.1: SR is unbiased. Enumerating all 65536 draws gives E[q] - v in [0, 2^-16 * width)."""
+    rng = np.random.default_rng(9)
+    g = O.G_MAX[fmt]
+    # random values, values whose fraction f makes f * 2^16 an integer (the bias bound is tight there),
+    # and tiny values around zero
+    v = np.concatenate([rng.uniform(-g, g, 64), [0.3, -0.3, 1e-7, -1e-7, 0.5, -0.5, 0.25, 2.75, -3.125,
+                                                 5.5, 1.0 + 2 ** -16]]).astype(np.float32)
+    u = np.arange(65536, dtype=np.uint16)
+    levels = O._signed_levels(fmt)
+    for vi in v:
+        q = O.level_values(O.round_stochastic(np.full(65536, vi, np.float32), u, fmt), fmt)
+        ia = np.searchsorted(levels, float(vi), side="right") - 1
+        ib = min(ia + 1, len(levels) - 1)
+        width = levels[ib] - levels[ia] if ib > ia else 1.0
+        assert set(np.unique(q)) <= {levels[ia], levels[ib]}
+        bias = q.mean() - float(vi)
+        assert 0.0 <= bias < width / 65536, (vi, bias)
+
+
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+def test_sr_keeps_grid_values(fmt):
+    """A value already on the grid has probability 0 of moving (Sec. 2.1: Pr[q = g_b] = 0 at g_a)."""
+    u = np.arange(65536, dtype=np.uint16)
+    for lv in O._signed_levels(fmt):
+        q = O.level_values(O.round_stochastic(np.full(65536, lv, np.float32), u, fmt), fmt)
+        assert np.all(q == lv)
+
+
+def test_philox_draw_bits_balanced():
+    """Every bit of every draw position is a fair coin over many blocks (catches a lost or swapped bit
+    in the extraction of 16-bit draws from the Philox words)."""
+    u = O.sr_draws(np.arange(1 << 14)[:, None], np.arange(2)[None, :], seed=0x0123456789ABCDEF, stream=0)
+    u = u.reshape(-1, 16).astype(np.uint32)
+    n = u.shape[0]
+    for bit in range(16):
+        frac = ((u >> np.uint32(bit)) & np.uint32(1)).mean(axis=0)
+        assert np.all(np.abs(frac - 0.5) < 5 * 0.5 / np.sqrt(n)), bit
+
+
+def test_sr_statistical_mean_with_philox_draws():
+    rng = np.random.default_rng(1)
+    v = rng.uniform(-7, 7, 8).astype(np.float32)
+    n_blocks = 1 << 13
+    u = O.sr_draws(np.arange(n_blocks)[:, None], np.zeros((1, 1), np.int64), seed=1234, stream=3)
+    u = u.reshape(-1)  # 131072 draws
+    for vi in v:
+        q = O.level_values(O.round_stochastic(np.full(u.size, vi, np.float32), u, O.UNIFORM), O.UNIFORM)
+        f = float(vi) - np.floor(float(vi))
+        sigma = np.sqrt(f * (1 - f) / u.size) + 1e-12
+        assert abs(q.mean() - float(vi)) < 4.5 * sigma + 2 ** -16
+
+
+def test_philox_draws_uniform_histogram():
+    u = O.sr_draws(np.arange(4096)[:, None], np.arange(8)[None, :], seed=0xDEADBEEF12345678, stream=1)
+    hist = np.bincount((u.reshape(-1) >> 12).astype(np.int64), minlength=16)
+    expected = u.size / 16
+    chi2 = np.sum((hist - expected) ** 2 / expected)
+    assert chi2 < 60  # 15 degrees of freedom; p ~ 1e-7
+
+
+def _build_rocrand_philox(tmp):
+    src = os.path.join(tmp, "philox_ref.cpp")
+    exe = os.path.join(tmp, "philox_ref")
+    with open(src, "w") as f:
+        f.write(
+            "#include <hip/hip_runtime.h>\n#include <rocrand/rocrand_philox4x32_10.h>\n#include <cstdio>\n"
+            "struct E : rocrand_device::philox4x32_10_engine {\n"
+            "  uint4 raw(uint4 c, uint2 k) { return ten_rounds(c, k); } };\n"
+            "int main() { E e; unsigned a[6];\n"
+            "  while (scanf(\"%x %x %x %x %x %x\", a, a+1, a+2, a+3, a+4, a+5) == 6) {\n"
+            "    uint4 o = e.raw(make_uint4(a[0], a[1], a[2], a[3]), make_uint2(a[4], a[5]));\n"
+            "    printf(\"%08x %08x %08x %08x\\n\", o.x, o.y, o.z, o.w); } return 0; }\n")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    subprocess.run(["g++", "-O1", "-D__HIP_PLATFORM_AMD__", f"-I{rocm}/include", src, "-o", exe],
+                   check=True, capture_output=True)
+    return exe
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or not os.path.exists("/opt/rocm/include/rocrand"),
+                    reason="needs g++ and the rocRAND headers")
+def test_philox_matches_rocrand():
+    """Philox4x32-10 against rocRAND's independent implementation (its engine's ten-round function)."""
+    rng = np.random.default_rng(2024)
+    ctr = rng.integers(0, 2 ** 32, size=(500, 4), dtype=np.uint64)
+    key = rng.integers(0, 2 ** 32, size=(500, 2), dtype=np.uint64)
+    ctr[0] = 0
+    key[0] = 0
+    ctr[1] = 0xFFFFFFFF
+    key[1] = 0xFFFFFFFF
+    with tempfile.TemporaryDirectory() as tmp:
+        exe = _build_rocrand_philox(tmp)
+        inp = "\n".join(" ".join(f"{int(v):x}" for v in list(c) + list(k)) for c, k in zip(ctr, key))
+        out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout.split()
+    ref = np.array([int(w, 16) for w in out], dtype=np.uint64).reshape(-1, 4)
+    for i in range(len(ctr)):
+        got = O.philox4x32_10(ctr[i, 0], ctr[i, 1], ctr[i, 2], ctr[i, 3], key[i, 0], key[i, 1])
+        assert [int(w) for w in got] == [int(w) for w in ref[i]], i
+
+
+# ------------------------------------------------------------------------------------------------
+# Quantizer (Sec. 2.1 display) -- invariants and brute force
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+@pytest.mark.parametrize("rht", [False, True])
+def test_quantizer_invariants(fmt, rht):
+    rng = np.random.default_rng(17)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (64, 256)))
+    a[3, 16:32] = 0.0  # a zero block
+    idx, s = O.quantize_rows(a, fmt, O.RTNE, rht, 0x1234)
+    g = O.G_MAX[fmt]
+    y = O.rht_blocks(a.reshape(64, 16, 16), 0x1234) if rht else a.reshape(64, 16, 16)
+    amax = np.abs(y).max(-1)
+    assert np.array_equal(s, (amax / np.float32(g)).astype(np.float32))
+    assert s[3, 1] == 0 and np.all(idx[3, 16:32] == 0)
+    blocks = idx.reshape(64, 16, 16)
+    lv = O.level_values(blocks, fmt)
+    nz = amax > 0
+    # the amax element carries the top level, with its sign
+    am = np.abs(y).argmax(-1)
+    top = np.take_along_axis(lv, am[..., None], -1)[..., 0]
+    sgn = np.sign(np.take_along_axis(y, am[..., None], -1)[..., 0])
+    assert np.all(top[nz] == g * sgn[nz])
+    if fmt == O.UNIFORM:
+        err = np.abs(lv * s[..., None].astype(np.float64) - y.astype(np.float64))
+        assert np.all(err <= s[..., None] * (0.5 + 2 ** -20) + 1e-30)
+
+
+def test_quantizer_bruteforce_tiny_blocks():
+    """Every element's level is the nearest of all 15 signed levels to y/s, found with exact rationals."""
+    rng = np.random.default_rng(23)
+    for fmt in (O.UNIFORM, O.E2M1):
+        levels = [Fraction(float(x)) for x in O._signed_levels(fmt)]
+        mags = list(O.GRID_MAGNITUDES[fmt])
+        for trial in range(40):
+            a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (1, 16), scale=10.0 ** rng.uniform(-3, 3)))
+            idx, s = O.quantize_rows(a, fmt, O.RTNE, trial % 2 == 1, trial * 977)
+            y = O.rht_blocks(a.reshape(1, 1, 16), trial * 977)[0, 0] if trial % 2 else a[0]
+            g = np.float32(O.G_MAX[fmt])
+            r = g / np.abs(y).max()
+            for i in range(16):
+                v = Fraction(float(np.float32(y[i] * r)))
+                d = [abs(v - L) for L in levels]
+                best = min(d)
+                cands = [L for L, dd in zip(levels, d) if dd == best]
+                if len(cands) > 1:  # tie: even magnitude code
+                    cands = [L for L in cands if mags.index(abs(float(L))) % 2 == 0]
+                assert O.level_values(idx[0, i], fmt) == float(cands[0])
+
+
+def test_sr_quantizer_uses_counter_draws_and_is_reproducible():
+    rng = np.random.default_rng(29)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (8, 64)))
+    i1, s1 = O.quantize_rows(a, O.UNIFORM, O.SR, True, 0x55, seed=99, stream=0)
+    i2, s2 = O.quantize_rows(a, O.UNIFORM, O.SR, True, 0x55, seed=99, stream=0)
+    i3, _ = O.quantize_rows(a, O.UNIFORM, O.SR, True, 0x55, seed=99, stream=1)
+    assert np.array_equal(i1, i2) and np.array_equal(s1, s2)
+    assert not np.array_equal(i1, i3)
+    # rows quantized alone, with their global row ids, give the same codes (counters are global)
+    i4, _ = O.quantize_rows(a[5:7], O.UNIFORM, O.SR, True, 0x55, seed=99, stream=0, row_ids=[5, 6])
+    assert np.array_equal(i4, i1[5:7])
+
+
+def test_pack_unpack_roundtrip_and_bit_patterns():
+    rng = np.random.default_rng(31)
+    for fmt in (O.UNIFORM, O.E2M1):
+        idx = rng.integers(-7, 8, size=(5, 32))
+        p = O.pack_codes(idx, fmt)
+        assert p.shape == (5, 16)
+        assert np.array_equal(O.unpack_codes(p, fmt), idx)
+    one = np.array([[-1, 7, -7, 0]])
+    assert list(O.pack_codes(one, O.UNIFORM)[0]) == [0x7F, 0x09]  # -1 -> 0xF, 7 -> 0x7, -7 -> 0x9
+    e = np.array([[-7, 7, -1, 0]])  # E2M1: -6 -> 0xF, 6 -> 0x7, -0.5 -> 0x9, 0 -> 0x0
+    assert list(O.pack_codes(e, O.E2M1)[0]) == [0x7F, 0x09]
+
+
+def test_colwise_is_rowwise_of_transpose():
+    rng = np.random.default_rng(37)
+    t = _rand_bf16_bits(rng, (64, 48))
+    a = O.operand_colwise(t)
+    b = O.bf16_bits_to_f32(np.ascontiguousarray(t.T))
+    assert np.array_equal(a, b)
+    i1, s1 = O.quantize_rows(a, O.UNIFORM, O.SR, True, 7, seed=5, stream=1)
+    i2, s2 = O.quantize_rows(b, O.UNIFORM, O.SR, True, 7, seed=5, stream=1)
+    assert np.array_equal(i1, i2) and np.array_equal(s1, s2)
+
+
+# ------------------------------------------------------------------------------------------------
+# GEMMs (Sec. 2.2)
+# ------------------------------------------------------------------------------------------------
+
+def test_gemm_integer_special_case():
+    """Power-of-two scales: the dequantized product is an exactly representable integer matmul."""
+    rng = np.random.default_rng(41)
+    a = rng.integers(-7, 8, size=(24, 64))
+    b = rng.integers(-7, 8, size=(40, 64))
+    sa = (2.0 ** rng.integers(-6, 6, size=(24, 4))).astype(np.float32)
+    sb = (2.0 ** rng.integers(-6, 6, size=(40, 4))).astype(np.float32)
+    got = O.gemm_nt(a, sa, b, sb, O.UNIFORM)
+    want = np.zeros((24, 40))
+    for kb in range(4):
+        blk = slice(16 * kb, 16 * kb + 16)
+        want += (a[:, blk] @ b[:, blk].T) * np.outer(sa[:, kb], sb[:, kb])
+    assert np.array_equal(got, want)
+
+
+def test_gemm_bruteforce_fractions():
+    rng = np.random.default_rng(43)
+    for fmt in (O.UNIFORM, O.E2M1):
+        a = rng.integers(-7, 8, size=(3, 32))
+        b = rng.integers(-7, 8, size=(4, 32))
+        sa = rng.uniform(0.01, 2, size=(3, 2)).astype(np.float32)
+        sb = rng.uniform(0.01, 2, size=(4, 2)).astype(np.float32)
+        got = O.gemm_nt(a, sa, b, sb, fmt)
+        lv = {i: Fraction(float(O.level_values(np.array(i), fmt))) for i in range(-7, 8)}
+        for i in range(3):
+            for j in range(4):
+                acc = sum(lv[a[i, k]] * Fraction(float(sa[i, k // 16])) * lv[b[j, k]] * Fraction(float(sb[j, k // 16]))
+                          for k in range(32))
+                assert abs(got[i, j] - float(acc)) <= 1e-14 * max(1.0, abs(float(acc)))
+
+
+def test_grouped_padding_keeps_products():
+    """Zero-padding each group's token axis to a multiple of 16 leaves X_g^T dY_g unchanged, with and
+    without the rotation (Sec. 2.2 invariance)."""
+    rng = np.random.default_rng(47)
+    counts = [5, 16, 33, 0, 19]
+    mtot = sum(counts)
+    x = _rand_bf16_bits(rng, (mtot, 32))
+    dy = _rand_bf16_bits(rng, (mtot, 24))
+    ax, poff = O.operand_colwise_grouped(x, counts)
+    ad, poff2 = O.operand_colwise_grouped(dy, counts)
+    assert np.array_equal(poff, poff2) and list(np.diff(poff)) == [16, 16, 48, 0, 32]
+    xf, df = O.bf16_bits_to_f32(x).astype(np.float64), O.bf16_bits_to_f32(dy).astype(np.float64)
+
+    def rot(a):
+        r, c = a.shape
+        return O.rht_exact_f64(a.reshape(r, c // 16, 16).astype(np.float64), 0xBEEF).reshape(r, c)
+
+    rx, rd = rot(ax), rot(ad)
+    off = 0
+    for gi, c in enumerate(counts):
+        cols = slice(int(poff[gi]), int(poff[gi + 1]))
+        ref = df[off:off + c].T @ xf[off:off + c]
+        assert np.allclose(ad[:, cols].astype(np.float64) @ ax[:, cols].T.astype(np.float64), ref, rtol=0, atol=1e-12)
+        if c:
+            assert np.linalg.norm(rd[:, cols] @ rx[:, cols].T - ref) <= 1e-13 * np.linalg.norm(ref)
+        off += c
+
+
+@pytest.mark.parametrize("recipe", ["ufp4", "e2m1"])
+def test_layer_gemms_approximate_exact_products(recipe):
+    rng = np.random.default_rng(53)
+    x = _rand_bf16_bits(rng, (64, 128))
+    w = _rand_bf16_bits(rng, (96, 128))
+    dy = _rand_bf16_bits(rng, (64, 96))
+    q, out = O.layer_gemms(x, w, dy, recipe, sign_mask=0x2F1D, seed=3)
+    xf, wf, df = (O.bf16_bits_to_f32(t).astype(np.float64) for t in (x, w, dy))
+    for key, ref in (("y", xf @ wf.T), ("dx", df @ wf), ("dw", df.T @ xf)):
+        assert out[key].shape == ref.shape
+        assert O.sqnr_db(out[key], ref) > 12.0, key
+    assert q["wt"][0].shape == (128, 96) and q["dyt"][0].shape == (96, 64) and q["xt"][0].shape == (128, 64)
+
+
+def test_diagnostics_closed_forms():
+    a = np.array([[1.0, 2.0], [3.0, 4.0]])
+    assert O.operand_projection(0.9 * a, a) == pytest.approx(0.9)
+    assert O.sqnr_db(1.1 * a, a) == pytest.approx(20.0)
+    idx = np.array([[0, 1, 2, 3, 4, 5, 6, 7]])
+    assert O.effective_bucket_ratio(idx, O.UNIFORM) == pytest.approx(1.0, abs=1e-9)
+    assert O.effective_bucket_ratio(np.zeros((1, 8), np.int64), O.UNIFORM) == pytest.approx(1 / 8, abs=1e-9)
