@@ -1,0 +1,286 @@
+"""Benchmark of the UFP4 hot path on one MI355X.
+
+One step = the whole hot path of one linear layer's training step under the UFP4 recipe: six fused
+RHT + quantize calls (X, W rowwise along K; dY rowwise along N with SR; W^T along N; dY^T along M with SR;
+X^T along M) and the three block-scaled 4-bit GEMMs fwd_y, bwd_dx, bwd_dw. Inputs are resident in HBM before
+the timed region; every output buffer is allocated before it, so the timed loop only launches kernels.
+
+Prints one JSON line. `value` is the step's GEMM work (3 x 2MNK) divided by the step time, in TFLOP/s;
+`breakdown` has every kernel's average duration and its own GB/s (quantizers, 2.75 algorithmic bytes per
+element) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel, the dominant one; `cpu_baseline` times the CPU
+oracle on a bounded sample of the same layer.
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2606_20381_amd import ufp4 as U  # noqa: E402
+from paper_2606_20381_amd import workloads as WL  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+INT8_PEAK_TOPS = 5000.0  # dense int8 MFMA, MI355X
+QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
+METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
+
+
+class Timeline:
+    """HIP events around every launch of the timed region, on the stream the kernels run on."""
+
+    def __init__(self):
+        self.events = {}
+
+    def run(self, label, fn, record):
+        if not record:
+            return fn()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        r = fn()
+        e.record()
+        self.events.setdefault(label, []).append((s, e))
+        return r
+
+    def mean_us(self, label):
+        v = [s.elapsed_time(e) * 1e3 for s, e in self.events[label]]
+        return float(np.mean(v))
+
+
+# ---------------------------------------------------------------------------------------------------
+# step builders: each returns (step(record) -> None, kernel table)
+# kernel table: label -> ("quant", elements) or ("gemm", flops)
+# ---------------------------------------------------------------------------------------------------
+
+def dense_step(wl, tl: Timeline):
+    m, s = wl.sign_mask, wl.seed
+    x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
+    M, K = x.shape
+    N = w.shape[0]
+    q = {
+        "x": U.empty_qtensor(M, K), "w": U.empty_qtensor(N, K), "dy": U.empty_qtensor(M, N),
+        "wt": U.empty_qtensor(K, N), "dyt": U.empty_qtensor(N, M), "xt": U.empty_qtensor(K, M),
+    }
+    y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
+    dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
+
+    def step(rec):
+        tl.run("quant_x", lambda: U.rht_quantize(x, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: U.rht_quantize(w, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: U.rht_quantize(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
+                                                     out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: U.rht_quantize(w, transpose=True, sign_mask=m, out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: U.rht_quantize(dy, transpose=True, sign_mask=m, rounding=U.SR, seed=s,
+                                                      stream_id=1, out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: U.rht_quantize(x, transpose=True, sign_mask=m, out=q["xt"]), rec)
+        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y(q["x"], q["w"], out=y), rec)
+        tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
+        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
+
+    kern = {
+        "quant_x": ("quant", M * K), "quant_w": ("quant", N * K), "quant_dy_sr": ("quant", M * N),
+        "quant_wt": ("quant", N * K), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
+        "gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
+        "gemm_bwd_dw": ("gemm", 2 * M * N * K),
+    }
+    return step, kern
+
+
+def moe_step(wl, tl: Timeline):
+    m, s = wl.sign_mask, wl.seed
+    E, N, K = wl.w.shape
+    x, dy = wl.x.cuda(), wl.dy.cuda()
+    w2 = wl.w.reshape(E * N, K).cuda()
+    M = x.shape[0]
+    off, poff, red = U.group_offsets(wl.counts)
+    eoff, epoff, ered = U.group_offsets([N] * E)
+    q = {
+        "x": U.empty_qtensor(M, K), "w": U.empty_qtensor(E * N, K), "dy": U.empty_qtensor(M, N),
+        "wt": U.empty_qtensor(K, E * N), "dyt": U.empty_qtensor(N, red), "xt": U.empty_qtensor(K, red),
+    }
+    y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
+    dw = torch.empty(E, N, K, dtype=torch.float32, device="cuda")
+
+    def step(rec):
+        tl.run("quant_x", lambda: U.rht_quantize(x, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: U.rht_quantize(w2, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: U.rht_quantize(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
+                                                     out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, sign_mask=m, out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, poff, red, sign_mask=m, rounding=U.SR, seed=s,
+                                                            stream_id=1, out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, poff, red, sign_mask=m, out=q["xt"]), rec)
+        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y_grouped(q["x"], q["w"], off, N, out=y), rec)
+        tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx_grouped(q["dy"], q["wt"], off, out=dx), rec)
+        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw_grouped(q["dyt"], q["xt"], poff, out=dw), rec)
+
+    flops = 2 * M * N * K
+    kern = {
+        "quant_x": ("quant", M * K), "quant_w": ("quant", E * N * K), "quant_dy_sr": ("quant", M * N),
+        "quant_wt": ("quant", E * N * K), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
+        "gemm_fwd_y": ("gemm", flops), "gemm_bwd_dx": ("gemm", flops), "gemm_bwd_dw": ("gemm", flops),
+    }
+    return step, kern
+
+
+def quant1g_step(tl: Timeline):
+    t = WL.quantizer_tensor().cuda()
+    R, C = t.shape
+    q = U.empty_qtensor(R, C)
+
+    def step(rec):
+        tl.run("quant_rows_rtne", lambda: U.rht_quantize(t, sign_mask=0x6A09, out=q), rec)
+
+    return step, {"quant_rows_rtne": ("quant", R * C)}
+
+
+# ---------------------------------------------------------------------------------------------------
+# CPU oracle baseline: the same layer step on a bounded sample of tokens
+# ---------------------------------------------------------------------------------------------------
+
+def cpu_baseline(wl, tokens: int = 128):
+    from oracle import ufp4_oracle as O
+    from threadpoolctl import threadpool_info
+
+    x = WL.bf16_bits(wl.x[:tokens].contiguous())
+    dy = WL.bf16_bits(wl.dy[:tokens].contiguous())
+    w = WL.bf16_bits(wl.w)
+    M, K = x.shape
+    N = w.shape[0]
+    t0 = time.perf_counter()
+    O.layer_gemms(x, w, dy, "ufp4", sign_mask=wl.sign_mask, seed=wl.seed)
+    dt = time.perf_counter() - t0
+    flops = 3 * 2 * M * N * K
+    blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(blas),
+        "kind": "oracle",
+        "sample": (f"whole UFP4 layer step (6 quantizations + 3 fp64 GEMMs) on {tokens} of {wl.x.shape[0]} "
+                   f"tokens, full {N}x{K} weight; {dt:.1f} s; elementwise numpy on 1 thread, fp64 matmul on "
+                   f"{blas} BLAS threads; host {platform.processor() or platform.machine()}, "
+                   f"os.cpu_count()={os.cpu_count()}"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="dense",
+                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU layout "
+              f"is described in DESIGN.md but not run", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    U.lib()
+
+    tl = Timeline()
+    wl = None
+    if args.workload == "quant1g":
+        step, kern = quant1g_step(tl)
+        wname = "standalone quantizer: 32768x16384 bf16 (1 GiB), rowwise RTNE with RHT"
+    else:
+        wl = WL.CONFIGS[args.workload]()
+        step, kern = (moe_step if wl.grouped else dense_step)(wl, tl)
+        wname = wl.name
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step(True)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    breakdown = {}
+    gemm_flops = 0
+    quant_bytes = 0.0
+    for label, (kind, work) in kern.items():
+        us = tl.mean_us(label)
+        if kind == "quant":
+            gbps = work * QUANT_BYTES_PER_ELEM / (us * 1e-6) / 1e9
+            breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
+            quant_bytes += work * QUANT_BYTES_PER_ELEM
+        else:
+            tf = work / (us * 1e-6) / 1e12
+            breakdown[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_int8": round(tf / INT8_PEAK_TOPS, 4)}
+            gemm_flops += work
+
+    gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
+    quant_labels = [k for k, (kind, _) in kern.items() if kind == "quant"]
+    if gemm_labels:
+        value = gemm_flops / (ms_per_step * 1e-3) / 1e12
+        unit = "TFLOP/s"
+        per_launch = np.mean([kern[k][1] for k in gemm_labels])
+        avg_us = np.mean([tl.mean_us(k) for k in gemm_labels])
+        ach = per_launch / (avg_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "kernel": "gemm_kernel (int8 MFMA 32x32x16 + fp32 scale epilogue)",
+                "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": None}
+    else:
+        value = quant_bytes / (ms_per_step * 1e-3) / 1e9
+        unit = "GB/s"
+        label = quant_labels[0]
+        us = tl.mean_us(label)
+        ach = kern[label][1] * QUANT_BYTES_PER_ELEM / (us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "kernel": "quant_rows_kernel", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None}
+    if quant_labels and gemm_labels:
+        qus = sum(tl.mean_us(k) for k in quant_labels)
+        breakdown["quant_all"] = {"us": round(qus, 2), "GB/s": round(quant_bytes / (qus * 1e-6) / 1e9, 1)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8" if gemm_labels else "f64+f32",
+        "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
+        "config": {"workload": wname, "recipe": "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY",
+                   "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",
+                   "wall_s": round(wall, 3)},
+        "roofline": roof,
+        "breakdown": breakdown,
+    }
+    if wl is not None and not args.no_cpu_baseline and not wl.grouped:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * ufp4.h -- C ABI of the UFP4 hot path on MI355X (gfx950).
+ *
+ * Implements the two data-parallel pieces of the UFP4 4-bit training recipe of "Rethinking Shrinkage
+ * Bias in LLM FP4 Pretraining" (arXiv 2606.20381):
+ *
+ *   1. block-16 Random Hadamard Transform (Sec. 2.2) fused with 1x16 block-scaled quantization
+ *      (Sec. 2.1) to the uniform 4-bit grid of the recipe (Sec. 4, Table 1), along the reduction axis
+ *      of a GEMM operand -- rowwise (reduction axis contiguous) or transposed (reduction axis strided);
+ *   2. the block-scaled 4-bit GEMMs fwd_y (Y = X W^T), bwd_dx (dX = dY W) and bwd_dw (dW = dY^T X) that
+ *      consume those operands (Sec. 2.2, quantized GEMM display; RHT axis per GEMM in its last sentence).
+ *
+ * An E2M1 quantizer and the same GEMMs on E2M1 codes form the comparison baseline (Table 1).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - All pointers named *_dev are device pointers (HBM). Host pointers are named *_host. The caller owns
+ *    every buffer; the library allocates, frees and synchronizes nothing.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls are asynchronous on it.
+ *  - bf16 tensors are row-major with a leading dimension `ld` in elements (ld >= cols, ld % 8 == 0,
+ *    base 16-byte aligned).
+ *  - A quantized operand Q is [rows, red] with the reduction axis `red` contiguous, red % 16 == 0:
+ *      codes : uint8 [rows, red/2], row stride `code_ld` bytes; element 2j of a 16-block in the low
+ *              nibble of byte j. Uniform grid: two's-complement code k in -7..7. E2M1: OCP FP4 bit
+ *              pattern (sign in bit 3, canonical +0).
+ *      scales: fp32 [rows, red/16], row stride `scale_ld` floats; block b of row r dequantizes as
+ *              level(code) * scales[r, b]. Uniform grid: s = RN(amax/7); E2M1: s = RN(amax/6).
+ *  - Quantizer arithmetic, per 16-block x (bf16):
+ *      y_i  = RN_fp32( 1/4 * sum_j H16[i,j] * eps_j * x_j )  with the exact sum (rht != 0), else y = x;
+ *             H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
+ *             Exact when the nonzero |x_j| of a block span at most 2^41.
+ *      amax = max |y_i|;  s = RN(amax/g);  r = RN(g/amax);  v_i = RN(y_i * r);  amax == 0 -> s = 0, codes 0.
+ *      RTNE (Sec. 2.1): nearest level, ties to the level with the even magnitude code.
+ *      SR   (Sec. 2.1): adjacent signed levels g_a <= v < g_b; q = g_b iff u/2^16 < (v - g_a)/(g_b - g_a),
+ *             u a 16-bit Philox4x32-10 draw: key = (seed lo32, seed hi32), counter = (block, row, half,
+ *             stream), element j takes 16-bit half (j & 1) of word (j & 7) >> 1 of call half = j >> 3.
+ *             `block` is the block index along the reduction axis, `row` the operand row.
+ *      |v| beyond the top level is clamped to it.
+ *  - GEMMs: C[i, j] = sum_b sA[i,b] sB[j,b] sum_{k in block b} level(A[i,k]) level(B[j,k]) with fp32
+ *    accumulation; output fp32 or bf16 (RNE), row-major with leading dimension ldc (elements).
+ *
+ * Errors: every call validates its arguments on the host before launching anything and returns
+ * UFP4_OK or an error code (no launch happens on error). Device faults surface at the caller's next
+ * synchronization. Inputs must be finite.
+ */
+#ifndef UFP4_H
+#define UFP4_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    UFP4_OK = 0,
+    UFP4_ERR_INVALID_ARG = 1, /* null pointer, negative size, unknown enum value                     */
+    UFP4_ERR_SHAPE = 2,       /* reduction length not a multiple of 16, leading dimension too small  */
+    UFP4_ERR_ALIGN = 3,       /* pointer or leading dimension not aligned as required                 */
+    UFP4_ERR_UNSUPPORTED = 5, /* valid request this build does not implement                          */
+    UFP4_ERR_HIP = 6          /* kernel launch failed                                                 */
+} ufp4_status;
+
+enum { UFP4_FMT_UNIFORM = 0, UFP4_FMT_E2M1 = 1 };
+enum { UFP4_ROUND_RTNE = 0, UFP4_ROUND_SR = 1 };
+enum { UFP4_OUT_F32 = 0, UFP4_OUT_BF16 = 1 };
+
+/* Human-readable name of a status code (static string). */
+const char *ufp4_status_string(int status);
+
+/* Library version, "major.minor.patch". */
+const char *ufp4_version(void);
+
+/*
+ * ufp4_rht_quantize -- fused RHT + uniform-grid quantization of one GEMM operand (Sec. 2.1, Sec. 2.2;
+ * recipe of Sec. 4 / Table 1). Uniform grid, codes -7..7, g = 7.
+ *
+ *   x_dev      bf16 [rows, cols], leading dimension ld (elements).
+ *   transpose  0: operand A = X, reduction along cols (cols % 16 == 0); Q is [rows, cols].
+ *              1: operand A = X^T, reduction along rows (rows % 16 == 0); Q is [cols, rows].
+ *   rht        nonzero: apply the block-16 RHT with sign_mask (bits 0..15) before quantizing.
+ *   rounding   UFP4_ROUND_RTNE or UFP4_ROUND_SR (seed, stream select the Philox draws; ignored for RTNE).
+ *   codes_dev  uint8 [Q rows, Q red / 2], row stride code_ld bytes (code_ld >= red/2, code_ld % 8 == 0).
+ *   scales_dev fp32 [Q rows, Q red / 16], row stride scale_ld floats (scale_ld >= red/16).
+ */
+int ufp4_rht_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                      uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
+                      int64_t code_ld, float *scales_dev, int64_t scale_ld, void *stream);
+
+/* ufp4_e2m1_quantize -- the same operation on the E2M1 grid (g = 6, levels 0, .5, 1, 1.5, 2, 3, 4, 6),
+ * the comparison baseline of Table 1. Arguments as ufp4_rht_quantize. */
+int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
+                       int64_t code_ld, float *scales_dev, int64_t scale_ld, void *stream);
+
+/*
+ * ufp4_quantize_grouped_t -- transposed quantization of an expert-grouped tensor (MoE), either grid.
+ *
+ *   x_dev              bf16 [rows, cols] (ld elements); rows are split into num_groups consecutive groups.
+ *   group_offsets_dev  int64 [num_groups + 1] device array, 0 = off_0 <= ... <= off_G = rows.
+ *   padded_offsets_dev int64 [num_groups + 1] device array, pad_0 = 0, pad_{g+1} = pad_g +
+ *                      16 * ceil((off_{g+1} - off_g) / 16): the group's column range in Q.
+ *   Q is [cols, red_total] with red_total = pad_G; group g's block of Q is X[off_g:off_{g+1}]^T with its
+ *   reduction (token) axis zero-padded to a multiple of 16. Block numbers in the SR counters count along
+ *   the padded concatenated axis. Used for bwd_dw's dY^T and X^T and, with equal groups, for the
+ *   per-expert W^T of bwd_dx.
+ *   red_total          pad_G as known to the caller (sizes the output); must match the device array.
+ */
+int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld,
+                            const int64_t *group_offsets_dev, const int64_t *padded_offsets_dev,
+                            int32_t num_groups, int64_t red_total, int rht, uint32_t sign_mask, int rounding,
+                            uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_ld,
+                            float *scales_dev, int64_t scale_ld, void *stream);
+
+/*
+ * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that
+ * share their reduction axis (the axis the RHT was applied along):
+ *
+ *   ufp4_gemm_fwd_y : Y  [M, N] = Q(X H')   [M, K] . Q(W H')   [N, K]^T
+ *   ufp4_gemm_bwd_dx: dX [M, K] = Q(dY H')  [M, N] . Q(W^T H') [K, N]^T
+ *   ufp4_gemm_bwd_dw: dW [N, K] = Q(dY^T H')[N, M] . Q(X^T H') [K, M]^T
+ *
+ * Arguments: (a_codes, a_scales) is the left operand, (b_codes, b_scales) the right one, with row
+ * strides (code_ld bytes, scale_ld floats) each; `format` is the grid both operands were quantized to
+ * (UFP4_FMT_UNIFORM or UFP4_FMT_E2M1); out_dtype UFP4_OUT_F32 or UFP4_OUT_BF16; out_dev row-major with
+ * leading dimension ldc (elements). Both operands must come from quantizations with the same rht
+ * setting and sign mask (the library cannot check this).
+ */
+int ufp4_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_ld, const float *x_scales_dev, int64_t x_scale_ld,
+                    const void *w_codes_dev, int64_t w_code_ld, const float *w_scales_dev, int64_t w_scale_ld,
+                    int64_t M, int64_t N, int64_t K, int format, void *y_dev, int64_t ldc, int out_dtype,
+                    void *stream);
+int ufp4_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_ld, const float *dy_scales_dev,
+                     int64_t dy_scale_ld, const void *wt_codes_dev, int64_t wt_code_ld,
+                     const float *wt_scales_dev, int64_t wt_scale_ld, int64_t M, int64_t N, int64_t K,
+                     int format, void *dx_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_ld, const float *dyt_scales_dev,
+                     int64_t dyt_scale_ld, const void *xt_codes_dev, int64_t xt_code_ld,
+                     const float *xt_scales_dev, int64_t xt_scale_ld, int64_t M, int64_t N, int64_t K,
+                     int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+
+/*
+ * Grouped (MoE) forms: num_groups experts, token rows expert-contiguous.
+ *
+ *   fwd_y : Y_g  [m_g, N] = Qx[off_g:off_{g+1}, :K] . Qw[g*N:(g+1)*N, :K]^T        (Y  [M_total, N])
+ *   bwd_dx: dX_g [m_g, K] = Qdy[off_g:off_{g+1}, :N] . Qwt[:K, g*N:(g+1)*N]^T       (dX [M_total, K])
+ *           where Qwt [K, G*N] is the grouped-transposed quantization of W [G*N, K] with equal groups.
+ *   bwd_dw: dW_g [N, K]  = Qdyt[:N, pad_g:pad_{g+1}] . Qxt[:K, pad_g:pad_{g+1}]^T   (dW [G, N, K])
+ *
+ * group_offsets_dev / padded_offsets_dev as in ufp4_quantize_grouped_t; M_total = off_G; red_total = pad_G is
+ * the reduction length of Qdyt and Qxt. Offsets are read on the device: rows past M_total and reduction
+ * positions past red_total are ignored, groups with no tokens give dW_g = 0.
+ */
+int ufp4_gemm_fwd_y_grouped(const void *x_codes_dev, int64_t x_code_ld, const float *x_scales_dev,
+                            int64_t x_scale_ld, const void *w_codes_dev, int64_t w_code_ld,
+                            const float *w_scales_dev, int64_t w_scale_ld, const int64_t *group_offsets_dev,
+                            int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format, void *y_dev,
+                            int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dx_grouped(const void *dy_codes_dev, int64_t dy_code_ld, const float *dy_scales_dev,
+                             int64_t dy_scale_ld, const void *wt_codes_dev, int64_t wt_code_ld,
+                             const float *wt_scales_dev, int64_t wt_scale_ld, const int64_t *group_offsets_dev,
+                             int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format,
+                             void *dx_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dw_grouped(const void *dyt_codes_dev, int64_t dyt_code_ld, const float *dyt_scales_dev,
+                             int64_t dyt_scale_ld, const void *xt_codes_dev, int64_t xt_code_ld,
+                             const float *xt_scales_dev, int64_t xt_scale_ld,
+                             const int64_t *padded_offsets_dev, int32_t num_groups, int64_t red_total, int64_t N,
+                             int64_t K, int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UFP4_H */

@@ -1,0 +1,316 @@
+// Block-scaled 4-bit NT GEMM on CDNA4 int8 MFMA (Sec. 2.2: Y_hat = Q(XH') Q(WH')^T; the three training
+// GEMMs fwd_y, bwd_dx, bwd_dw all take this form once both operands are stored reduction-contiguous).
+//
+//   C[i, j] = sum_b  sA[i,b] * sB[j,b] * D_b[i, j],   D_b[i, j] = sum_{k in block b} A[i,k] * B[j,k]
+//
+// Every 16-element K-block has its own fp32 scale on both sides, so D_b is formed per block by one
+// v_mfma_i32_32x32x16_i8 (K = 16 exactly) and folded into an fp32 accumulator by the VALU:
+// acc += float(D_b) * (sA * sB). Codes are expanded to int8 with the nibble trick: for a packed byte
+// (lo | hi << 4) of two's-complement nibbles, (byte & 0xF0) is 16*hi and ((byte & 0x0F) << 4) is 16*lo as
+// int8, so D_b comes out scaled by 256 (undone once at the end). E2M1 codes are expanded through a
+// byte-permute table to 2 * level (exact in int8), scaled by 4.
+//
+// Work split: 128 x 128 output tile per workgroup, 4 waves in 2 x 2, each wave 64 x 64 = 2 x 2 MFMA
+// tiles. K is staged through LDS 8 blocks (128 codes) at a time, double-buffered: the next stage's
+// global loads are in flight while the current one is computed. LDS holds codes as planes
+// [block][half][row] (one dword = 8 codes per row and half), so the MFMA operand reads of a half-wave
+// are 32 consecutive dwords; scales as planes [block][row].
+//
+// Grouped (MoE) problems: ragged M (fwd_y, bwd_dx: token rows split into groups) resolves its group
+// from the tile index with a wave-wide prefix sum over the group sizes; ragged K (bwd_dw: the reduction
+// runs over each group's padded token range) takes the group from blockIdx.z.
+
+#include "ufp4_device.h"
+#include "ufp4_internal.h"
+
+namespace ufp4 {
+
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128, BN = 128;
+constexpr int SKB = 8;         // K-blocks per LDS stage
+constexpr int CPL = BM + 2;    // dwords per code plane (row stride offset of 2 banks between planes)
+constexpr int SPL = BM + 4;    // floats per scale plane
+static_assert(BM == BN, "one plane stride for both operands");
+
+struct alignas(16) GemmSmem {
+    uint32_t a[2][SKB * 2 * CPL];
+    uint32_t b[2][SKB * 2 * CPL];
+    float as[2][SKB * SPL];
+    float bs[2][SKB * SPL];
+    int32_t grp[2];
+};
+
+// 8 packed uniform codes (one dword) -> 8 int8 lanes holding 16 * code (even codes first, then odd).
+__device__ __forceinline__ long expand_uniform(uint32_t d) {
+    const uint32_t lo = (d & 0x0F0F0F0Fu) << 4;
+    const uint32_t hi = d & 0xF0F0F0F0u;
+    return (long)(((uint64_t)hi << 32) | lo);
+}
+
+// 4 E2M1 nibbles, one per byte (low 4 bits) -> 4 int8 holding 2 * level.
+__device__ __forceinline__ uint32_t e2m1_bytes_to_i8x2(uint32_t nib) {
+    const uint32_t sel = nib & 0x07070707u;
+    // magnitudes * 2: 0 1 2 3 4 6 8 12 and their negations
+    const uint32_t pos = __builtin_amdgcn_perm(0x0C080604u, 0x03020100u, sel);
+    const uint32_t neg = __builtin_amdgcn_perm(0xF4F8FAFCu, 0xFDFEFF00u, sel);
+    const uint32_t m = ((nib >> 3) & 0x01010101u) * 0xFFu;
+    return (pos & ~m) | (neg & m);
+}
+
+__device__ __forceinline__ long expand_e2m1(uint32_t d) {
+    const uint32_t lo = e2m1_bytes_to_i8x2(d & 0x0F0F0F0Fu);
+    const uint32_t hi = e2m1_bytes_to_i8x2((d >> 4) & 0x0F0F0F0Fu);
+    return (long)(((uint64_t)hi << 32) | lo);
+}
+
+template <int FMT>
+__device__ __forceinline__ long expand(uint32_t d) {
+    if constexpr (FMT == kFmtUniform) return expand_uniform(d);
+    else return expand_e2m1(d);
+}
+
+struct GemmArgs {
+    GemmJob j;
+};
+
+// The problem one workgroup works on, with pointers already advanced to its tile / group.
+struct Tile {
+    const uint8_t* a;
+    const float* as;
+    const uint8_t* b;
+    const float* bs;
+    int mrows, nrows;  // valid rows of the tile in A and B
+    int64_t nkb;       // reduction blocks
+    int64_t c_off;     // element offset of the tile's (0, 0) in C
+};
+
+// Ragged-M: find the group owning global m-tile t. Wave 0 runs a prefix sum over per-group tile counts,
+// 64 groups at a time; the result goes through LDS. Returns false for tiles past the last group.
+__device__ bool resolve_ragged_m(const GemmJob& j, GemmSmem& sm, int64_t t, int& g_out, int64_t& local_tile) {
+    const int tid = threadIdx.x;
+    if (tid == 0) sm.grp[0] = -1;
+    __syncthreads();
+    if (tid < 64) {
+        int64_t base = 0;
+        for (int g0 = 0; g0 < j.G; g0 += 64) {
+            const int g = g0 + tid;
+            int64_t cnt = 0;
+            if (g < j.G) cnt = (j.offsets[g + 1] - j.offsets[g] + BM - 1) / BM;
+            int64_t incl = cnt;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int64_t v = __shfl_up(incl, d, 64);
+                if (tid >= d) incl += v;
+            }
+            const int64_t excl = incl - cnt;
+            if (cnt > 0 && base + excl <= t && t < base + incl) {
+                sm.grp[0] = g;
+                sm.grp[1] = (int32_t)(t - base - excl);
+            }
+            base += __shfl(incl, 63, 64);
+        }
+    }
+    __syncthreads();
+    g_out = sm.grp[0];
+    local_tile = sm.grp[1];
+    return g_out >= 0;
+}
+
+template <int FMT, int OUT>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
+    __shared__ GemmSmem sm;
+    const GemmJob& j = args.j;
+    const int tid = threadIdx.x;
+
+    // ---- resolve this workgroup's tile --------------------------------------------------------
+    Tile tl;
+    const int64_t tn = blockIdx.x;
+    if (j.mode == kGemmRaggedM) {
+        int g;
+        int64_t lt;
+        if (!resolve_ragged_m(j, sm, blockIdx.y, g, lt)) return;
+        const int64_t r0 = j.offsets[g] + lt * BM;
+        const int64_t end = j.offsets[g + 1] < j.M ? j.offsets[g + 1] : j.M;  // offsets past M_total: ignored
+        const int64_t rows_g = end - r0;
+        if (rows_g <= 0) return;
+        tl.a = j.a + r0 * j.lda;
+        tl.as = j.as + r0 * j.ldas;
+        const int64_t brow = g * j.b_group_rows + tn * BN;
+        const int64_t bkb = g * j.b_group_kb;
+        tl.b = j.b + brow * j.ldb + bkb * 8;
+        tl.bs = j.bs + brow * j.ldbs + bkb;
+        tl.mrows = (int)(rows_g < BM ? rows_g : BM);
+        const int64_t nr = j.N - tn * BN;
+        tl.nrows = (int)(nr < BN ? nr : BN);
+        tl.nkb = j.nkb;
+        tl.c_off = r0 * j.ldc + tn * BN;
+    } else {
+        const int64_t tm = blockIdx.y;
+        int64_t kb0 = 0, c_base = 0;
+        tl.nkb = j.nkb;
+        if (j.mode == kGemmRaggedK) {
+            const int g = blockIdx.z;
+            // the group's padded token range, clamped to the operands' reduction length
+            const int64_t p0 = j.offsets[g] < j.red_total ? j.offsets[g] : j.red_total;
+            const int64_t p1 = j.offsets[g + 1] < j.red_total ? j.offsets[g + 1] : j.red_total;
+            kb0 = p0 / 16;
+            tl.nkb = p1 > p0 ? (p1 - p0) / 16 : 0;
+            c_base = (int64_t)g * j.M * j.ldc;
+        }
+        tl.a = j.a + tm * BM * j.lda + kb0 * 8;
+        tl.as = j.as + tm * BM * j.ldas + kb0;
+        tl.b = j.b + tn * BN * j.ldb + kb0 * 8;
+        tl.bs = j.bs + tn * BN * j.ldbs + kb0;
+        const int64_t mr = j.M - tm * BM, nr = j.N - tn * BN;
+        tl.mrows = (int)(mr < BM ? mr : BM);
+        tl.nrows = (int)(nr < BN ? nr : BN);
+        tl.c_off = c_base + tm * BM * j.ldc + tn * BN;
+    }
+
+    // ---- main loop ----------------------------------------------------------------------------
+    const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+
+    float acc[2][2][16];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
+
+    uint2 ra[4], rb[4];
+    float rsa[4], rsb[4];
+    const int64_t nstages = (tl.nkb + SKB - 1) / SKB;
+
+    auto load_stage = [&](int64_t s) {
+        const int64_t ks = s * SKB;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = tid + 256 * q;
+            const int row = e >> 3, kb = e & 7;
+            const bool kok = ks + kb < tl.nkb;
+            const bool aok = kok && row < tl.mrows, bok = kok && row < tl.nrows;
+            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + row * j.lda + (ks + kb) * 8) : make_uint2(0, 0);
+            rsa[q] = aok ? tl.as[row * j.ldas + ks + kb] : 0.0f;
+            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + row * j.ldb + (ks + kb) * 8) : make_uint2(0, 0);
+            rsb[q] = bok ? tl.bs[row * j.ldbs + ks + kb] : 0.0f;
+        }
+    };
+    auto store_stage = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = tid + 256 * q;
+            const int row = e >> 3, kb = e & 7;
+            sm.a[buf][(kb * 2 + 0) * CPL + row] = ra[q].x;
+            sm.a[buf][(kb * 2 + 1) * CPL + row] = ra[q].y;
+            sm.b[buf][(kb * 2 + 0) * CPL + row] = rb[q].x;
+            sm.b[buf][(kb * 2 + 1) * CPL + row] = rb[q].y;
+            sm.as[buf][kb * SPL + row] = rsa[q];
+            sm.bs[buf][kb * SPL + row] = rsb[q];
+        }
+    };
+
+    if (nstages > 0) {
+        load_stage(0);
+        store_stage(0);
+    }
+    __syncthreads();
+
+    for (int64_t s = 0; s < nstages; ++s) {
+        const int buf = (int)(s & 1);
+        if (s + 1 < nstages) load_stage(s + 1);
+        const int64_t left = tl.nkb - s * SKB;
+        const int kbn = (int)(left < SKB ? left : SKB);
+#pragma unroll
+        for (int kb = 0; kb < SKB; ++kb) {
+            if (kb < kbn) {
+                long aop[2], bop[2];
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    aop[t2] = expand<FMT>(sm.a[buf][(kb * 2 + h) * CPL + wm * 64 + t2 * 32 + l32]);
+                    bop[t2] = expand<FMT>(sm.b[buf][(kb * 2 + h) * CPL + wn * 64 + t2 * 32 + l32]);
+                }
+                v16i d[2][2];
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        const v16i z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+                        d[a][b] = __builtin_amdgcn_mfma_i32_32x32x16_i8(aop[a], bop[b], z, 0, 0, 0);
+                    }
+                float sb[2];
+#pragma unroll
+                for (int b = 0; b < 2; ++b) sb[b] = sm.bs[buf][kb * SPL + wn * 64 + b * 32 + l32];
+#pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    float sa[16];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float4 v =
+                            *reinterpret_cast<const float4*>(&sm.as[buf][kb * SPL + wm * 64 + a * 32 + 8 * q + 4 * h]);
+                        sa[4 * q + 0] = v.x;
+                        sa[4 * q + 1] = v.y;
+                        sa[4 * q + 2] = v.z;
+                        sa[4 * q + 3] = v.w;
+                    }
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            acc[a][b][i] = __builtin_fmaf((float)d[a][b][i], sa[i] * sb[b], acc[a][b][i]);
+                }
+            }
+        }
+        if (s + 1 < nstages) store_stage(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: undo the int8 expansion factor and store -----------------------------------
+    constexpr float kUndo = FMT == kFmtUniform ? 1.0f / 256.0f : 0.25f;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int col = wn * 64 + b * 32 + l32;
+            if (col >= tl.nrows) continue;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                if (row >= tl.mrows) continue;
+                const float v = acc[a][b][i] * kUndo;
+                const int64_t off = tl.c_off + (int64_t)row * j.ldc + col;
+                if constexpr (OUT == kOutF32) {
+                    static_cast<float*>(j.c)[off] = v;
+                } else {
+                    static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
+                }
+            }
+        }
+    }
+}
+
+template <int FMT, int OUT>
+static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
+    dim3 grid((unsigned)((j.N + BN - 1) / BN), 1, 1);
+    if (j.mode == kGemmRaggedM) {
+        grid.y = (unsigned)((j.M + BM - 1) / BM + j.G);
+    } else {
+        grid.y = (unsigned)((j.M + BM - 1) / BM);
+        if (j.mode == kGemmRaggedK) grid.z = (unsigned)j.G;
+    }
+    if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
+    GemmArgs args{j};
+    gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmJob& j, hipStream_t s) {
+    if (j.format == kFmtE2M1) {
+        return j.out_dtype == kOutBF16 ? launch_t<kFmtE2M1, kOutBF16>(j, s) : launch_t<kFmtE2M1, kOutF32>(j, s);
+    }
+    return j.out_dtype == kOutBF16 ? launch_t<kFmtUniform, kOutBF16>(j, s) : launch_t<kFmtUniform, kOutF32>(j, s);
+}
+
+}  // namespace ufp4

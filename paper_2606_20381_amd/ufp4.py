@@ -1,0 +1,253 @@
+"""Python binding of libufp4 (ctypes). Argument marshalling only: every step runs in the HIP library.
+
+Tensors are torch tensors on the GPU; torch supplies device memory and the current stream. The library
+must be built (``python -m paper_2606_20381_amd.build``); without it every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+UNIFORM = 0
+E2M1 = 1
+RTNE = 0
+SR = 1
+OUT_F32 = 0
+OUT_BF16 = 1
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libufp4.so")
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_INT = ctypes.c_int
+_U32 = ctypes.c_uint32
+_U64 = ctypes.c_uint64
+
+_QUANT_ARGS = [_P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, _P, _I64, _P, _I64, _P]
+_GEMM_ARGS = [_P, _I64, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I64, _INT, _P, _I64, _INT, _P]
+SIGNATURES = {
+    "ufp4_status_string": ([_INT], ctypes.c_char_p),
+    "ufp4_version": ([], ctypes.c_char_p),
+    "ufp4_rht_quantize": (_QUANT_ARGS, _INT),
+    "ufp4_e2m1_quantize": (_QUANT_ARGS, _INT),
+    "ufp4_quantize_grouped_t": ([_INT, _P, _I64, _I64, _I64, _P, _P, _I32, _I64, _INT, _U32, _INT, _U64, _U32, _P,
+                                 _I64, _P, _I64, _P], _INT),
+    "ufp4_gemm_fwd_y": (_GEMM_ARGS, _INT),
+    "ufp4_gemm_bwd_dx": (_GEMM_ARGS, _INT),
+    "ufp4_gemm_bwd_dw": (_GEMM_ARGS, _INT),
+    "ufp4_gemm_fwd_y_grouped": ([_P, _I64, _P, _I64, _P, _I64, _P, _I64, _P, _I32, _I64, _I64, _I64, _INT, _P, _I64,
+                                 _INT, _P], _INT),
+    "ufp4_gemm_bwd_dx_grouped": ([_P, _I64, _P, _I64, _P, _I64, _P, _I64, _P, _I32, _I64, _I64, _I64, _INT, _P, _I64,
+                                  _INT, _P], _INT),
+    "ufp4_gemm_bwd_dw_grouped": ([_P, _I64, _P, _I64, _P, _I64, _P, _I64, _P, _I32, _I64, _I64, _I64, _INT, _P, _I64,
+                                  _INT, _P], _INT),
+}
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libufp4.so (once) and declare the C signatures. Raises if the library is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is not built; run `python -m paper_2606_20381_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (args, res) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+class UFP4Error(RuntimeError):
+    def __init__(self, status: int, call: str):
+        msg = lib().ufp4_status_string(status).decode()
+        super().__init__(f"{call}: {msg} (status {status})")
+        self.status = status
+
+
+def _check(status: int, call: str) -> None:
+    if status != 0:
+        raise UFP4Error(status, call)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+@dataclass
+class QTensor:
+    """A quantized operand [rows, red] (reduction contiguous): packed codes and fp32 block scales."""
+
+    codes: torch.Tensor  # uint8 [rows, >= red/2]
+    scales: torch.Tensor  # float32 [rows, >= red/16]
+    fmt: int
+    rows: int
+    red: int
+
+    @property
+    def code_ld(self) -> int:
+        return self.codes.stride(0)
+
+    @property
+    def scale_ld(self) -> int:
+        return self.scales.stride(0)
+
+
+def empty_qtensor(rows: int, red: int, fmt: int = UNIFORM, device="cuda") -> QTensor:
+    code_ld = max(8, -(-(red // 2) // 16) * 16)  # 16-byte row stride
+    codes = torch.empty((rows, code_ld), dtype=torch.uint8, device=device)[:, : red // 2]
+    scales = torch.empty((rows, red // 16), dtype=torch.float32, device=device)
+    return QTensor(codes, scales, fmt, rows, red)
+
+
+def _quantize_call(name, fmt, x, transpose, rht, sign_mask, rounding, seed, stream_id, out):
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    qrows, red = (cols, rows) if transpose else (rows, cols)
+    q = out if out is not None else empty_qtensor(qrows, red, fmt, x.device)
+    st = getattr(lib(), name)(x.data_ptr(), rows, cols, x.stride(0), int(transpose), int(rht), sign_mask, rounding,
+                              seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_ld,
+                              q.scales.data_ptr(), q.scale_ld, _stream())
+    _check(st, name)
+    return q
+
+
+def rht_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = True, sign_mask: int = 0,
+                 rounding: int = RTNE, seed: int = 0, stream_id: int = 0, out: QTensor | None = None) -> QTensor:
+    """Fused RHT + uniform-grid quantization (ufp4_rht_quantize)."""
+    return _quantize_call("ufp4_rht_quantize", UNIFORM, x, transpose, rht, sign_mask, rounding, seed, stream_id, out)
+
+
+def e2m1_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = False, sign_mask: int = 0,
+                  rounding: int = RTNE, seed: int = 0, stream_id: int = 0, out: QTensor | None = None) -> QTensor:
+    """Fused (optional) RHT + E2M1 quantization (ufp4_e2m1_quantize), the comparison baseline."""
+    return _quantize_call("ufp4_e2m1_quantize", E2M1, x, transpose, rht, sign_mask, rounding, seed, stream_id, out)
+
+
+def group_offsets(counts, device="cuda"):
+    """(token offsets, padded offsets, padded total) for per-group row counts; offsets as int64 device
+    tensors of length G + 1."""
+    off = [0]
+    poff = [0]
+    for c in counts:
+        off.append(off[-1] + int(c))
+        poff.append(poff[-1] + -(-int(c) // 16) * 16)
+    return (torch.tensor(off, dtype=torch.int64, device=device), torch.tensor(poff, dtype=torch.int64, device=device),
+            poff[-1])
+
+
+def quantize_grouped_t(x: torch.Tensor, offsets: torch.Tensor, padded_offsets: torch.Tensor, red_total: int, *,
+                       fmt: int = UNIFORM, rht: bool = True, sign_mask: int = 0, rounding: int = RTNE, seed: int = 0,
+                       stream_id: int = 0, out: QTensor | None = None) -> QTensor:
+    """Grouped transposed quantization (ufp4_quantize_grouped_t): Q [cols, red_total]."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    G = offsets.numel() - 1
+    q = out if out is not None else empty_qtensor(cols, red_total, fmt, x.device)
+    st = lib().ufp4_quantize_grouped_t(fmt, x.data_ptr(), rows, cols, x.stride(0), offsets.data_ptr(),
+                                       padded_offsets.data_ptr(), G, red_total, int(rht), sign_mask, rounding,
+                                       seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_ld,
+                                       q.scales.data_ptr(), q.scale_ld, _stream())
+    _check(st, "ufp4_quantize_grouped_t")
+    return q
+
+
+def _out(rows, cols, out_dtype, device, out):
+    if out is not None:
+        return out
+    return torch.empty((rows, cols), dtype=out_dtype, device=device)
+
+
+def _odt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return OUT_F32
+    if t.dtype == torch.bfloat16:
+        return OUT_BF16
+    raise ValueError("output must be float32 or bfloat16")
+
+
+def _gemm(name, a: QTensor, b: QTensor, M, N, K, c: torch.Tensor):
+    if a.fmt != b.fmt:
+        raise ValueError("operands quantized to different grids")
+    st = getattr(lib(), name)(a.codes.data_ptr(), a.code_ld, a.scales.data_ptr(), a.scale_ld, b.codes.data_ptr(),
+                              b.code_ld, b.scales.data_ptr(), b.scale_ld, M, N, K, a.fmt, c.data_ptr(), c.stride(0),
+                              _odt(c), _stream())
+    _check(st, name)
+    return c
+
+
+def gemm_fwd_y(xq: QTensor, wq: QTensor, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """Y [M, N] = Q(X H') Q(W H')^T (ufp4_gemm_fwd_y)."""
+    M, K, N = xq.rows, xq.red, wq.rows
+    return _gemm("ufp4_gemm_fwd_y", xq, wq, M, N, K, _out(M, N, out_dtype, xq.codes.device, out))
+
+
+def gemm_bwd_dx(dyq: QTensor, wtq: QTensor, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """dX [M, K] = Q(dY H') Q(W^T H')^T (ufp4_gemm_bwd_dx)."""
+    M, N, K = dyq.rows, dyq.red, wtq.rows
+    return _gemm("ufp4_gemm_bwd_dx", dyq, wtq, M, N, K, _out(M, K, out_dtype, dyq.codes.device, out))
+
+
+def gemm_bwd_dw(dytq: QTensor, xtq: QTensor, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """dW [N, K] = Q(dY^T H') Q(X^T H')^T (ufp4_gemm_bwd_dw)."""
+    N, M, K = dytq.rows, dytq.red, xtq.rows
+    return _gemm("ufp4_gemm_bwd_dw", dytq, xtq, M, N, K, _out(N, K, out_dtype, dytq.codes.device, out))
+
+
+def gemm_fwd_y_grouped(xq: QTensor, wq: QTensor, offsets: torch.Tensor, n_per_group: int, out_dtype=torch.float32,
+                       out=None) -> torch.Tensor:
+    """Y_g = Qx[group g rows] Qw[g*N:(g+1)*N]^T, Y [M_total, N] (ufp4_gemm_fwd_y_grouped)."""
+    G = offsets.numel() - 1
+    M, K, N = xq.rows, xq.red, n_per_group
+    c = _out(M, N, out_dtype, xq.codes.device, out)
+    st = lib().ufp4_gemm_fwd_y_grouped(xq.codes.data_ptr(), xq.code_ld, xq.scales.data_ptr(), xq.scale_ld,
+                                       wq.codes.data_ptr(), wq.code_ld, wq.scales.data_ptr(), wq.scale_ld,
+                                       offsets.data_ptr(), G, M, N, K, xq.fmt, c.data_ptr(), c.stride(0), _odt(c),
+                                       _stream())
+    _check(st, "ufp4_gemm_fwd_y_grouped")
+    return c
+
+
+def gemm_bwd_dx_grouped(dyq: QTensor, wtq: QTensor, offsets: torch.Tensor, out_dtype=torch.float32,
+                        out=None) -> torch.Tensor:
+    """dX_g = Qdy[group g rows] Qwt[:, g*N:(g+1)*N]^T, dX [M_total, K] (ufp4_gemm_bwd_dx_grouped)."""
+    G = offsets.numel() - 1
+    M, N, K = dyq.rows, dyq.red, wtq.rows
+    c = _out(M, K, out_dtype, dyq.codes.device, out)
+    st = lib().ufp4_gemm_bwd_dx_grouped(dyq.codes.data_ptr(), dyq.code_ld, dyq.scales.data_ptr(), dyq.scale_ld,
+                                        wtq.codes.data_ptr(), wtq.code_ld, wtq.scales.data_ptr(), wtq.scale_ld,
+                                        offsets.data_ptr(), G, M, N, K, dyq.fmt, c.data_ptr(), c.stride(0), _odt(c),
+                                        _stream())
+    _check(st, "ufp4_gemm_bwd_dx_grouped")
+    return c
+
+
+def gemm_bwd_dw_grouped(dytq: QTensor, xtq: QTensor, padded_offsets: torch.Tensor, out_dtype=torch.float32,
+                        out=None) -> torch.Tensor:
+    """dW_g = Qdyt[:, pad_g:pad_{g+1}] Qxt[:, pad_g:pad_{g+1}]^T, dW [G, N, K] (ufp4_gemm_bwd_dw_grouped)."""
+    G = padded_offsets.numel() - 1
+    N, K = dytq.rows, xtq.rows
+    c = out if out is not None else torch.empty((G, N, K), dtype=out_dtype, device=dytq.codes.device)
+    st = lib().ufp4_gemm_bwd_dw_grouped(dytq.codes.data_ptr(), dytq.code_ld, dytq.scales.data_ptr(), dytq.scale_ld,
+                                        xtq.codes.data_ptr(), xtq.code_ld, xtq.scales.data_ptr(), xtq.scale_ld,
+                                        padded_offsets.data_ptr(), G, dytq.red, N, K, dytq.fmt, c.data_ptr(), c.stride(-2),
+                                        _odt(c), _stream())
+    _check(st, "ufp4_gemm_bwd_dw_grouped")
+    return c

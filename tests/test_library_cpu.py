@@ -1,0 +1,122 @@
+"""CPU checks of the C ABI library: it loads, exports every function include/ufp4.h declares, and rejects
+bad arguments on the host before any GPU call (no compute runs here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_20381_amd import ufp4 as U
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ufp4.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ufp4_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(U.library_path()):
+        pytest.skip("libufp4.so not built")
+    return U.lib()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for required in ("ufp4_rht_quantize", "ufp4_e2m1_quantize", "ufp4_gemm_fwd_y", "ufp4_gemm_bwd_dx",
+                     "ufp4_gemm_bwd_dw"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    raw = ctypes.CDLL(U.library_path())
+    for name in _declared():
+        assert hasattr(raw, name), name
+        assert name in U.SIGNATURES, f"binding lacks a signature for {name}"
+
+
+def test_status_strings(lib):
+    assert lib.ufp4_status_string(0) == b"ok"
+    assert lib.ufp4_status_string(3).startswith(b"misaligned")
+    assert lib.ufp4_version() == b"0.1.0"
+
+
+FAKE = 1 << 20  # a 1 MiB-aligned non-null address that is never dereferenced: every call below fails validation
+
+
+@pytest.mark.parametrize("args,status", [
+    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream_id, codes, code_ld, scales, scale_ld)
+    ((None, 16, 16, 16, 0, 1, 0, 0, 0, 0, FAKE, 8, FAKE, 1), 1),          # null input
+    ((FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # cols % 16
+    ((FAKE, 24, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # transposed: rows % 16
+    ((FAKE, 16, 32, 30, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # ld < cols
+    ((FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # ld % 8
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 8, FAKE, 2), 2),          # code_ld < red/2
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 1), 2),         # scale_ld < red/16
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 20, FAKE, 2), 3),         # code_ld % 8
+    ((FAKE + 2, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 3),     # input alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, 16, FAKE, 2), 1),         # rounding enum
+    ((FAKE, 16, 32, 32, 2, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 1),         # transpose flag
+    ((FAKE, 16, 32, 32, 0, 1, 0x10000, 0, 0, 0, FAKE, 16, FAKE, 2), 1),   # sign mask > 16 bits
+    ((FAKE, -1, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 1),         # negative size
+])
+def test_quantize_validation(lib, args, status):
+    for fn in (lib.ufp4_rht_quantize, lib.ufp4_e2m1_quantize):
+        assert fn(*args, None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    # (a, lda, as, ldas, b, ldb, bs, ldbs, M, N, K, fmt, c, ldc, out)
+    ((None, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 16, 0, FAKE, 16, 0), 1),
+    ((FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 24, 0, FAKE, 16, 0), 2),    # K % 16
+    ((FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 32, 0, FAKE, 16, 0), 2),    # lda < K/2
+    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE, 8, 0), 2),   # ldc < N
+    ((FAKE, 12, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 16, 0, FAKE, 16, 0), 3),  # lda % 8
+    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 3, FAKE, 16, 0), 1),  # format enum
+    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE, 16, 5), 1),  # out dtype enum
+    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE + 1, 16, 0), 3),  # output alignment
+])
+def test_gemm_validation(lib, args, status):
+    # the dense entry points map (M, N, K) onto (rows_a, rows_b, reduction) differently; pick the layout each
+    # expects so the same failure shows up
+    assert lib.ufp4_gemm_fwd_y(*args, None) == status
+
+
+def test_gemm_validation_per_pass_layout(lib):
+    # bwd_dx: dY [M, N] . Wt [K, N]^T -> dX [M, K]; the reduction is N
+    assert lib.ufp4_gemm_bwd_dx(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 24, 16, 0, FAKE, 16, 0, None) == 2
+    # bwd_dw: dYt [N, M] . Xt [K, M]^T -> dW [N, K]; the reduction is M
+    assert lib.ufp4_gemm_bwd_dw(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 24, 16, 16, 0, FAKE, 16, 0, None) == 2
+
+
+def test_grouped_validation(lib):
+    # null offsets
+    assert lib.ufp4_quantize_grouped_t(0, FAKE, 32, 16, 16, None, FAKE, 2, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
+                                       None) == 1
+    # too many groups for one launch
+    assert lib.ufp4_quantize_grouped_t(0, FAKE, 32, 16, 16, FAKE, FAKE, 5000, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
+                                       None) == 5
+    # padded total smaller than the rows
+    assert lib.ufp4_quantize_grouped_t(0, FAKE, 64, 16, 16, FAKE, FAKE, 2, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
+                                       None) == 2
+    assert lib.ufp4_gemm_fwd_y_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, None, 2, 16, 16, 16, 0, FAKE, 16, 0,
+                                       None) == 1
+    assert lib.ufp4_gemm_bwd_dx_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, FAKE, 0, 16, 16, 16, 0, FAKE, 16, 0,
+                                        None) == 1
+    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, FAKE, 2, 32, 16, 16, 3, FAKE, 16, 0,
+                                        None) == 1
+    # red_total wider than the operands' code rows
+    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, 8, FAKE, 2, FAKE, 8, FAKE, 2, FAKE, 2, 32, 16, 16, 0, FAKE, 16, 0,
+                                        None) == 2
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(U, "_lib", None)
+    monkeypatch.setattr(U, "_LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        U.lib()
