@@ -20,6 +20,9 @@
 // from the tile index with a wave-wide prefix sum over the group sizes; ragged K (bwd_dw: the reduction
 // runs over each group's padded token range) takes the group from blockIdx.z.
 
+#include <cstdlib>
+#include <cstring>
+
 #include "ufp4_device.h"
 #include "ufp4_internal.h"
 
@@ -87,9 +90,9 @@ struct Tile {
 
 // Ragged-M: find the group owning global m-tile t. Wave 0 runs a prefix sum over per-group tile counts,
 // 64 groups at a time; the result goes through LDS. Returns false for tiles past the last group.
-__device__ bool resolve_ragged_m(const GemmJob& j, GemmSmem& sm, int64_t t, int& g_out, int64_t& local_tile) {
+__device__ bool resolve_ragged_m(const GemmJob& j, int32_t* grp, int64_t t, int& g_out, int64_t& local_tile) {
     const int tid = threadIdx.x;
-    if (tid == 0) sm.grp[0] = -1;
+    if (tid == 0) grp[0] = -1;
     __syncthreads();
     if (tid < 64) {
         int64_t base = 0;
@@ -105,35 +108,57 @@ __device__ bool resolve_ragged_m(const GemmJob& j, GemmSmem& sm, int64_t t, int&
             }
             const int64_t excl = incl - cnt;
             if (cnt > 0 && base + excl <= t && t < base + incl) {
-                sm.grp[0] = g;
-                sm.grp[1] = (int32_t)(t - base - excl);
+                grp[0] = g;
+                grp[1] = (int32_t)(t - base - excl);
             }
             base += __shfl(incl, 63, 64);
         }
     }
     __syncthreads();
-    g_out = sm.grp[0];
-    local_tile = sm.grp[1];
+    g_out = grp[0];
+    local_tile = grp[1];
     return g_out >= 0;
 }
 
-template <int FMT, int OUT>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
-    __shared__ GemmSmem sm;
-    const GemmJob& j = args.j;
-    const int tid = threadIdx.x;
+// Write a workgroup's 128 x 128 fp32 accumulator tile (four waves, 2 x 2 MFMA tiles of 32 x 32 each; output
+// row of register i in lane l: 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32), scaled by `mul`.
+template <int OUT>
+__device__ __forceinline__ void store_tile(const GemmJob& j, const Tile& tl, const float (&acc)[2][2][16], float mul,
+                                           int wm, int wn, int h, int l32) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int col = wn * 64 + b * 32 + l32;
+            if (col >= tl.nrows) continue;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                if (row >= tl.mrows) continue;
+                const float v = acc[a][b][i] * mul;
+                const int64_t off = tl.c_off + (int64_t)row * j.ldc + col;
+                if constexpr (OUT == kOutF32) {
+                    static_cast<float*>(j.c)[off] = v;
+                } else {
+                    static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
+                }
+            }
+        }
+    }
+}
 
-    // ---- resolve this workgroup's tile --------------------------------------------------------
-    Tile tl;
+// Resolve the workgroup's output tile (dense, ragged-M group or ragged-K group). Returns false when the
+// workgroup has nothing to do (a ragged-M tile index past the last group); all threads agree.
+__device__ bool resolve_tile(const GemmJob& j, int32_t* grp, Tile& tl) {
     const int64_t tn = blockIdx.x;
     if (j.mode == kGemmRaggedM) {
         int g;
         int64_t lt;
-        if (!resolve_ragged_m(j, sm, blockIdx.y, g, lt)) return;
+        if (!resolve_ragged_m(j, grp, blockIdx.y, g, lt)) return false;
         const int64_t r0 = j.offsets[g] + lt * BM;
         const int64_t end = j.offsets[g + 1] < j.M ? j.offsets[g + 1] : j.M;  // offsets past M_total: ignored
         const int64_t rows_g = end - r0;
-        if (rows_g <= 0) return;
+        if (rows_g <= 0) return false;
         tl.a = j.a + r0 * j.lda;
         tl.as = j.as + r0 * j.ldas;
         const int64_t brow = g * j.b_group_rows + tn * BN;
@@ -167,6 +192,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
         tl.nrows = (int)(nr < BN ? nr : BN);
         tl.c_off = c_base + tm * BM * j.ldc + tn * BN;
     }
+
+    return true;
+}
+
+template <int FMT, int OUT>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
+    __shared__ GemmSmem sm;
+    const GemmJob& j = args.j;
+    const int tid = threadIdx.x;
+
+    Tile tl;
+    if (!resolve_tile(j, sm.grp, tl)) return;
 
     // ---- main loop ----------------------------------------------------------------------------
     const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
@@ -267,28 +304,192 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
         __syncthreads();
     }
 
-    // ---- epilogue: undo the int8 expansion factor and store -----------------------------------
     constexpr float kUndo = FMT == kFmtUniform ? 1.0f / 256.0f : 0.25f;
+    store_tile<OUT>(j, tl, acc, kUndo, wm, wn, h, l32);
+}
+
+// ================================================================================================
+// fp32-output variant (the default).
+//
+// The per-block dot product D_b comes out of the MFMA already in fp32, and a second fp32 MFMA forms the
+// outer product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and
+// block: acc += D_b * (sA sB)_b. The outer products use the two-block v_mfma_f32_32x32x1_2b_f32 (two 32 x 32
+// tiles per instruction). Uniform codes are converted to fp8 e4m3 (integers -7..7 are exact) while
+// a stage is copied into LDS, and D_b is a v_mfma_f32_32x32x16_fp8_fp8. E2M1 codes go straight into the
+// scaled f8f6f4 MFMA as FP4 operands (neutral E8M0 scales), the 16 codes of a block occupying 16 of its
+// 64 K slots and the rest zero.
+// ================================================================================================
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v32f __attribute__((ext_vector_type(32)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+
+constexpr int SKB2 = 4;          // K-blocks per LDS stage
+constexpr int CPL2 = BM + 1;     // code plane stride in 8-byte entries
+constexpr int SPL2 = BM + 4;     // scale plane stride in floats
+
+// Per-byte sign masks: byte i of the result is 0xFF when bit 7 of byte i of x is set, else 0x00. The byte
+// permute's selectors 8..11 replicate bits 15, 31, 47 and 63 of {x << 8, x}, i.e. bits 15, 31, 7, 23 of x.
+__device__ __forceinline__ uint32_t byte_sign_mask(uint32_t x) {
+    return __builtin_amdgcn_perm(x << 8, x, 0x090B080Au);
+}
+
+// Two's-complement nibbles -> fp8 e4m3 bytes, four at a time. sel holds the low three bits of each nibble
+// (one per byte), m is 0xFF in the bytes whose nibble is negative.
+__device__ __forceinline__ uint32_t e4m3_from_nibbles(uint32_t sel, uint32_t m) {
+    // |k| = 0..7 -> 00 38 40 44 48 4A 4C 4E ; k = -8..-1 (index k & 7 = 0..7) -> -8(unused) -7 .. -1
+    const uint32_t pos = __builtin_amdgcn_perm(0x4E4C4A48u, 0x44403800u, sel);
+    const uint32_t ngt = __builtin_amdgcn_perm(0xB8C0C4C8u, 0xCACCCE00u, sel);
+    return (ngt & m) | (pos & ~m);
+}
+
+// 8 uniform codes (one packed dword) -> 8 fp8 bytes: even codes in the low dword, odd codes in the high one.
+__device__ __forceinline__ uint2 uniform_to_e4m3(uint32_t d) {
+    const uint32_t lo = e4m3_from_nibbles(d & 0x07070707u, byte_sign_mask(d << 4));
+    const uint32_t hi = e4m3_from_nibbles((d >> 4) & 0x07070707u, byte_sign_mask(d));
+    return make_uint2(lo, hi);
+}
+
+template <int FMT>
+struct alignas(16) GemmSmem2 {
+    // uniform: fp8 bytes (8 per row, block and half); E2M1: the raw packed codes in .x
+    uint2 a[2][SKB2 * 2 * CPL2];
+    uint2 b[2][SKB2 * 2 * CPL2];
+    float as[2][SKB2 * SPL2];
+    float bs[2][SKB2 * SPL2];
+    int32_t grp[2];
+};
+
+template <int FMT>
+__device__ __forceinline__ v16f block_dot(uint2 a, uint2 b) {
+    const v16f z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    if constexpr (FMT == kFmtUniform) {
+        const long av = (long)(((uint64_t)a.y << 32) | a.x);
+        const long bv = (long)(((uint64_t)b.y << 32) | b.x);
+        return __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(av, bv, z, 0, 0, 0);
+    } else {
+        const v8i av = {(int)a.x, 0, 0, 0, 0, 0, 0, 0};
+        const v8i bv = {(int)b.x, 0, 0, 0, 0, 0, 0, 0};
+        // A and B as FP4 E2M1 (format 4), E8M0 scales 127 = 2^0
+        return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, z, 4, 4, 0, 127, 0, 127);
+    }
+}
+
+template <int FMT, int OUT>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
+    __shared__ GemmSmem2<FMT> sm;
+    const GemmJob& j = args.j;
+    const int tid = threadIdx.x;
+
+    Tile tl;
+    if (!resolve_tile(j, sm.grp, tl)) return;
+
+    const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+
+    float acc[2][2][16];
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            const int col = wn * 64 + b * 32 + l32;
-            if (col >= tl.nrows) continue;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                if (row >= tl.mrows) continue;
-                const float v = acc[a][b][i] * kUndo;
-                const int64_t off = tl.c_off + (int64_t)row * j.ldc + col;
-                if constexpr (OUT == kOutF32) {
-                    static_cast<float*>(j.c)[off] = v;
-                } else {
-                    static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
+            for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
+
+    uint2 ra[2], rb[2];
+    float rsa[2], rsb[2];
+    const int64_t nstages = (tl.nkb + SKB2 - 1) / SKB2;
+
+    auto load_stage = [&](int64_t s) {
+        const int64_t ks = s * SKB2;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int e = tid + 256 * q;
+            const int row = e >> 2, kb = e & 3;
+            const bool kok = ks + kb < tl.nkb;
+            const bool aok = kok && row < tl.mrows, bok = kok && row < tl.nrows;
+            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + row * j.lda + (ks + kb) * 8) : make_uint2(0, 0);
+            rsa[q] = aok ? tl.as[row * j.ldas + ks + kb] : 0.0f;
+            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + row * j.ldb + (ks + kb) * 8) : make_uint2(0, 0);
+            rsb[q] = bok ? tl.bs[row * j.ldbs + ks + kb] : 0.0f;
+        }
+    };
+    auto store_stage = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int e = tid + 256 * q;
+            const int row = e >> 2, kb = e & 3;
+            if constexpr (FMT == kFmtUniform) {
+                sm.a[buf][(kb * 2 + 0) * CPL2 + row] = uniform_to_e4m3(ra[q].x);
+                sm.a[buf][(kb * 2 + 1) * CPL2 + row] = uniform_to_e4m3(ra[q].y);
+                sm.b[buf][(kb * 2 + 0) * CPL2 + row] = uniform_to_e4m3(rb[q].x);
+                sm.b[buf][(kb * 2 + 1) * CPL2 + row] = uniform_to_e4m3(rb[q].y);
+            } else {
+                sm.a[buf][(kb * 2 + 0) * CPL2 + row] = make_uint2(ra[q].x, 0);
+                sm.a[buf][(kb * 2 + 1) * CPL2 + row] = make_uint2(ra[q].y, 0);
+                sm.b[buf][(kb * 2 + 0) * CPL2 + row] = make_uint2(rb[q].x, 0);
+                sm.b[buf][(kb * 2 + 1) * CPL2 + row] = make_uint2(rb[q].y, 0);
+            }
+            sm.as[buf][kb * SPL2 + row] = rsa[q];
+            sm.bs[buf][kb * SPL2 + row] = rsb[q];
+        }
+    };
+
+    if (nstages > 0) {
+        load_stage(0);
+        store_stage(0);
+    }
+    __syncthreads();
+
+    const v32f z32 = {};
+    for (int64_t s = 0; s < nstages; ++s) {
+        const int buf = (int)(s & 1);
+        if (s + 1 < nstages) load_stage(s + 1);
+        const int64_t left = tl.nkb - s * SKB2;
+        const int kbn = (int)(left < SKB2 ? left : SKB2);
+#pragma unroll
+        for (int kb = 0; kb < SKB2; ++kb) {
+            if (kb < kbn) {
+                uint2 av[2], bv[2];
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    av[t2] = sm.a[buf][(kb * 2 + h) * CPL2 + wm * 64 + t2 * 32 + l32];
+                    bv[t2] = sm.b[buf][(kb * 2 + h) * CPL2 + wn * 64 + t2 * 32 + l32];
+                }
+                // Outer products sA x sB with the two-block f32 MFMA: lanes 0-31 feed block 0, lanes 32-63
+                // block 1. X = {tile (0,0), tile (1,1)}, Y = {tile (0,1), tile (1,0)}: every lane supplies the
+                // A scale of tile row h, and the B scale of tile column h (X) or 1 - h (Y).
+                const float sa = sm.as[buf][kb * SPL2 + wm * 64 + h * 32 + l32];
+                const float sbx = sm.bs[buf][kb * SPL2 + wn * 64 + h * 32 + l32];
+                const float sby = sm.bs[buf][kb * SPL2 + wn * 64 + (1 - h) * 32 + l32];
+                v16f d[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) d[t] = block_dot<FMT>(av[t >> 1], bv[t & 1]);
+                const v32f wx = __builtin_amdgcn_mfma_f32_32x32x1f32(sa, sbx, z32, 0, 0, 0);
+                const v32f wy = __builtin_amdgcn_mfma_f32_32x32x1f32(sa, sby, z32, 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    acc[0][0][i] = __builtin_fmaf(d[0][i], wx[i], acc[0][0][i]);
+                    acc[1][1][i] = __builtin_fmaf(d[3][i], wx[16 + i], acc[1][1][i]);
+                    acc[0][1][i] = __builtin_fmaf(d[1][i], wy[i], acc[0][1][i]);
+                    acc[1][0][i] = __builtin_fmaf(d[2][i], wy[16 + i], acc[1][0][i]);
                 }
             }
         }
+        if (s + 1 < nstages) store_stage(buf ^ 1);
+        __syncthreads();
     }
+
+    store_tile<OUT>(j, tl, acc, 1.0f, wm, wn, h, l32);
+}
+
+// UFP4_GEMM_MFMA=i8 selects the int8-MFMA kernel (cvt + scale product + fma per output and block) instead of
+// the default fp32-output kernel; both compute the same sums exactly up to fp32 accumulation order.
+static bool use_i8_mfma() {
+    static const bool v = [] {
+        const char* e = getenv("UFP4_GEMM_MFMA");
+        return e != nullptr && strcmp(e, "i8") == 0;
+    }();
+    return v;
 }
 
 template <int FMT, int OUT>
@@ -302,7 +503,11 @@ static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
     }
     if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
     GemmArgs args{j};
-    gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+    if (use_i8_mfma()) {
+        gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+    } else {
+        gemm_f32_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+    }
     return hipGetLastError();
 }
 
