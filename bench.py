@@ -137,6 +137,17 @@ def moe_step(wl, tl: Timeline):
     return step, kern
 
 
+def copy1g_step(tl: Timeline):
+    """Plain device copy of the 1 GiB quantizer tensor: the calibration kernel for HBM byte counters."""
+    t = WL.quantizer_tensor().cuda()
+    dst = torch.empty_like(t)
+
+    def step(rec):
+        tl.run("copy", lambda: dst.copy_(t), rec)
+
+    return step, {"copy": ("copy", t.numel() * t.element_size())}
+
+
 def quant1g_step(tl: Timeline):
     t = WL.quantizer_tensor().cuda()
     R, C = t.shape
@@ -152,7 +163,7 @@ def quant1g_step(tl: Timeline):
 # CPU oracle baseline: the same layer step on a bounded sample of tokens
 # ---------------------------------------------------------------------------------------------------
 
-def cpu_baseline(wl, tokens: int = 128):
+def cpu_baseline(wl, tokens: int = 512):
     from oracle import ufp4_oracle as O
     from threadpoolctl import threadpool_info
 
@@ -184,7 +195,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dense",
-                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g"])
+                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "copy1g"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -202,6 +213,9 @@ def main():
     if args.workload == "quant1g":
         step, kern = quant1g_step(tl)
         wname = "standalone quantizer: 32768x16384 bf16 (1 GiB), rowwise RTNE with RHT"
+    elif args.workload == "copy1g":
+        step, kern = copy1g_step(tl)
+        wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
         step, kern = (moe_step if wl.grouped else dense_step)(wl, tl)
@@ -226,7 +240,11 @@ def main():
     quant_bytes = 0.0
     for label, (kind, work) in kern.items():
         us = tl.mean_us(label)
-        if kind == "quant":
+        if kind == "copy":
+            gbps = 2 * work / (us * 1e-6) / 1e9
+            breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
+            quant_bytes += 2 * work
+        elif kind == "quant":
             gbps = work * QUANT_BYTES_PER_ELEM / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += work * QUANT_BYTES_PER_ELEM
@@ -236,7 +254,7 @@ def main():
             gemm_flops += work
 
     gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
-    quant_labels = [k for k, (kind, _) in kern.items() if kind == "quant"]
+    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "copy")]
     if gemm_labels:
         value = gemm_flops / (ms_per_step * 1e-3) / 1e12
         unit = "TFLOP/s"
@@ -251,8 +269,9 @@ def main():
         unit = "GB/s"
         label = quant_labels[0]
         us = tl.mean_us(label)
-        ach = kern[label][1] * QUANT_BYTES_PER_ELEM / (us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "kernel": "quant_rows_kernel", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+        per_launch = kern[label][1] * (QUANT_BYTES_PER_ELEM if kern[label][0] == "quant" else 2)
+        ach = per_launch / (us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "kernel": "quant_rows_kernel" if kern[label][0] == "quant" else "copy", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None}
     if quant_labels and gemm_labels:
         qus = sum(tl.mean_us(k) for k in quant_labels)

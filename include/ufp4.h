@@ -21,8 +21,9 @@
  *    base 16-byte aligned).
  *  - A quantized operand Q is [rows, red] with the reduction axis `red` contiguous, red % 16 == 0:
  *      codes : uint8 [rows, red/2], row stride `code_ld` bytes; element 2j of a 16-block in the low
- *              nibble of byte j. Uniform grid: two's-complement code k in -7..7. E2M1: OCP FP4 bit
- *              pattern (sign in bit 3, canonical +0).
+ *              nibble of byte j. Each nibble is sign-magnitude: sign in bit 3, magnitude code in bits
+ *              0-2, zero always +0. Uniform grid: magnitude |k| of the code k in -7..7. E2M1: index of the
+ *              magnitude in 0, .5, 1, 1.5, 2, 3, 4, 6 (the OCP FP4 bit pattern).
  *      scales: fp32 [rows, red/16], row stride `scale_ld` floats; block b of row r dequantizes as
  *              level(code) * scales[r, b]. Uniform grid: s = RN(amax/7); E2M1: s = RN(amax/6).
  *  - Quantizer arithmetic, per 16-block x (bf16):

@@ -27,8 +27,8 @@ Readings of the paper that this oracle fixes (the paper states exact mathematics
     realised with a 16-bit uniform draw U = u / 2^16: q = g_b iff U < (v - g_a)/(g_b - g_a).
     The draws come from Philox4x32-10 with key = seed and counter = (block, row, half, stream).
   * Codes outside the grid are clamped (|v| can exceed g by one fp32 ulp).
-  * Packing: uniform codes as two's-complement nibbles, E2M1 codes as OCP FP4 bit patterns (sign bit 3,
-    canonical +0); element 2j in the low nibble of byte j.
+  * Packing: sign-magnitude nibbles for both grids -- sign in bit 3, magnitude code in bits 0-2 (for E2M1
+    this is the OCP FP4 bit pattern), zero always encoded as +0; element 2j in the low nibble of byte j.
 """
 
 from __future__ import annotations
@@ -348,19 +348,15 @@ def operand_colwise_grouped(t_bits: np.ndarray, counts) -> tuple[np.ndarray, np.
 # ---------------------------------------------------------------------------------------------------
 
 def code_nibbles(idx: np.ndarray, fmt: int) -> np.ndarray:
-    """4-bit code of each element: two's complement of k for the uniform grid; sign<<3 | magnitude code
-    (OCP FP4 E2M1 bit pattern, canonical +0) for E2M1."""
+    """4-bit code of each element: sign << 3 | magnitude code, zero as +0. For the uniform grid the
+    magnitude code is |k|; for E2M1 it is the index of the magnitude, so the nibble is the OCP FP4 pattern."""
     idx = np.asarray(idx, dtype=np.int64)
-    if fmt == UNIFORM:
-        return (idx & 0xF).astype(np.uint8)
     sign = (idx < 0).astype(np.int64)
     return ((sign << 3) | np.abs(idx)).astype(np.uint8)
 
 
 def nibbles_to_idx(nib: np.ndarray, fmt: int) -> np.ndarray:
     nib = np.asarray(nib, dtype=np.int64)
-    if fmt == UNIFORM:
-        return np.where(nib >= 8, nib - 16, nib)
     mag = nib & 7
     return np.where(nib & 8, -mag, mag)
 

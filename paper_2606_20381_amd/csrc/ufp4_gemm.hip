@@ -5,10 +5,8 @@
 //
 // Every 16-element K-block has its own fp32 scale on both sides, so D_b is formed per block by one
 // v_mfma_i32_32x32x16_i8 (K = 16 exactly) and folded into an fp32 accumulator by the VALU:
-// acc += float(D_b) * (sA * sB). Codes are expanded to int8 with the nibble trick: for a packed byte
-// (lo | hi << 4) of two's-complement nibbles, (byte & 0xF0) is 16*hi and ((byte & 0x0F) << 4) is 16*lo as
-// int8, so D_b comes out scaled by 256 (undone once at the end). E2M1 codes are expanded through a
-// byte-permute table to 2 * level (exact in int8), scaled by 4.
+// acc += float(D_b) * (sA * sB). Codes are expanded to int8 through byte-permute tables: uniform codes to k,
+// E2M1 codes to 2 * level (exact in int8; the factor 4 on D_b is undone at the end).
 //
 // Work split: 128 x 128 output tile per workgroup, 4 waves in 2 x 2, each wave 64 x 64 = 2 x 2 MFMA
 // tiles. K is staged through LDS 8 blocks (128 codes) at a time, double-buffered: the next stage's
@@ -44,10 +42,24 @@ struct alignas(16) GemmSmem {
     int32_t grp[2];
 };
 
-// 8 packed uniform codes (one dword) -> 8 int8 lanes holding 16 * code (even codes first, then odd).
+// Per-byte sign masks: byte i of the result is 0xFF when bit 7 of byte i of x is set, else 0x00. The byte
+// permute's selectors 8..11 replicate bits 15, 31, 47 and 63 of {x << 8, x}, i.e. bits 15, 31, 7, 23 of x.
+__device__ __forceinline__ uint32_t byte_sign_mask(uint32_t x) {
+    return __builtin_amdgcn_perm(x << 8, x, 0x090B080Au);
+}
+
+// 4 uniform sign-magnitude nibbles, one per byte (low 4 bits) -> 4 int8 holding the code k.
+__device__ __forceinline__ uint32_t uniform_bytes_to_i8(uint32_t nib) {
+    const uint32_t mag = nib & 0x07070707u;
+    const uint32_t neg = __builtin_amdgcn_perm(0xF9FAFBFCu, 0xFDFEFF00u, mag);  // 0 -1 -2 .. -7
+    const uint32_t m = byte_sign_mask(nib << 4);
+    return (neg & m) | (mag & ~m);
+}
+
+// 8 packed uniform codes (one dword) -> 8 int8 lanes (even codes first, then odd).
 __device__ __forceinline__ long expand_uniform(uint32_t d) {
-    const uint32_t lo = (d & 0x0F0F0F0Fu) << 4;
-    const uint32_t hi = d & 0xF0F0F0F0u;
+    const uint32_t lo = uniform_bytes_to_i8(d & 0x0F0F0F0Fu);
+    const uint32_t hi = uniform_bytes_to_i8((d >> 4) & 0x0F0F0F0Fu);
     return (long)(((uint64_t)hi << 32) | lo);
 }
 
@@ -304,50 +316,77 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
         __syncthreads();
     }
 
-    constexpr float kUndo = FMT == kFmtUniform ? 1.0f / 256.0f : 0.25f;
+    constexpr float kUndo = FMT == kFmtUniform ? 1.0f : 0.25f;
     store_tile<OUT>(j, tl, acc, kUndo, wm, wn, h, l32);
 }
 
 // ================================================================================================
 // fp32-output variant (the default).
 //
-// The per-block dot product D_b comes out of the MFMA already in fp32, and a second fp32 MFMA forms the
-// outer product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and
-// block: acc += D_b * (sA sB)_b. The outer products use the two-block v_mfma_f32_32x32x1_2b_f32 (two 32 x 32
-// tiles per instruction). Uniform codes are converted to fp8 e4m3 (integers -7..7 are exact) while
-// a stage is copied into LDS, and D_b is a v_mfma_f32_32x32x16_fp8_fp8. E2M1 codes go straight into the
-// scaled f8f6f4 MFMA as FP4 operands (neutral E8M0 scales), the 16 codes of a block occupying 16 of its
-// 64 K slots and the rest zero.
+// The per-block dot product D_b comes out of the MFMA already in fp32 and a second MFMA forms the outer
+// product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and block:
+// acc += D_b * (sA sB)_b.
+//
+//  * D_b: uniform codes become fp8 e4m3 subnormals (code k -> k * 2^-9, exact) while a stage is copied into
+//    LDS and go through v_mfma_f32_32x32x16_fp8_fp8; E2M1 codes go straight into the scaled f8f6f4 MFMA as
+//    FP4 operands (neutral E8M0 scales), the 16 codes of a block occupying 16 of its 64 K slots.
+//  * (sA sB)_b: every fp32 scale is split exactly into three bf16 pieces s = s0 + s1 + s2 (top, middle and
+//    low 8 significand bits) when staged; a v_mfma_f32_32x32x16_bf16 whose 16 K slots hold the nine
+//    products a_i b_j (exact in fp32) sums them, i.e. sA sB up to fp32 accumulation rounding. The bf16
+//    MFMA co-executes with the VALU FMAs; an fp32 MFMA would not.
+//  * The MFMAs of one half of the wave's four tiles run while the VALU folds the other half (software
+//    pipeline across K-blocks and stages).
 // ================================================================================================
 
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef float v32f __attribute__((ext_vector_type(32)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int SKB2 = 4;          // K-blocks per LDS stage
 constexpr int CPL2 = BM + 1;     // code plane stride in 8-byte entries
-constexpr int SPL2 = BM + 4;     // scale plane stride in floats
+constexpr int SPL2 = BM + 2;     // scale plane stride in 8-byte entries
 
-// Per-byte sign masks: byte i of the result is 0xFF when bit 7 of byte i of x is set, else 0x00. The byte
-// permute's selectors 8..11 replicate bits 15, 31, 47 and 63 of {x << 8, x}, i.e. bits 15, 31, 7, 23 of x.
-__device__ __forceinline__ uint32_t byte_sign_mask(uint32_t x) {
-    return __builtin_amdgcn_perm(x << 8, x, 0x090B080Au);
-}
-
-// Two's-complement nibbles -> fp8 e4m3 bytes, four at a time. sel holds the low three bits of each nibble
-// (one per byte), m is 0xFF in the bytes whose nibble is negative.
-__device__ __forceinline__ uint32_t e4m3_from_nibbles(uint32_t sel, uint32_t m) {
-    // |k| = 0..7 -> 00 38 40 44 48 4A 4C 4E ; k = -8..-1 (index k & 7 = 0..7) -> -8(unused) -7 .. -1
-    const uint32_t pos = __builtin_amdgcn_perm(0x4E4C4A48u, 0x44403800u, sel);
-    const uint32_t ngt = __builtin_amdgcn_perm(0xB8C0C4C8u, 0xCACCCE00u, sel);
-    return (ngt & m) | (pos & ~m);
-}
-
-// 8 uniform codes (one packed dword) -> 8 fp8 bytes: even codes in the low dword, odd codes in the high one.
+// 8 uniform codes (one packed dword of sign-magnitude nibbles) -> 8 fp8 e4m3 bytes. The byte s000 0mmm is an
+// e4m3 subnormal worth (-1)^s * m * 2^-9, so the code k becomes k * 2^-9 exactly (the product of two codes
+// carries 2^-18, undone once at the store). Even codes go to the low dword, odd codes to the high one.
 __device__ __forceinline__ uint2 uniform_to_e4m3(uint32_t d) {
-    const uint32_t lo = e4m3_from_nibbles(d & 0x07070707u, byte_sign_mask(d << 4));
-    const uint32_t hi = e4m3_from_nibbles((d >> 4) & 0x07070707u, byte_sign_mask(d));
+    const uint32_t lo = (d & 0x07070707u) | ((d << 4) & 0x80808080u);
+    const uint32_t hi = ((d >> 4) & 0x07070707u) | (d & 0x80808080u);
     return make_uint2(lo, hi);
+}
+
+// Exact split of an fp32 value into three bf16 pieces x = s0 + s1 + s2 (truncations of the top, middle and
+// low 8 significand bits; each difference is exact in fp32). Returned as {s0 | s1 << 16, s2}.
+__device__ __forceinline__ uint2 split_bf16x3(float x) {
+    const uint32_t hi = __float_as_uint(x) & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(hi);
+    const uint32_t mid = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(mid);
+    return make_uint2((hi >> 16) | mid, __float_as_uint(r2) >> 16);
+}
+
+// K-slot layout of the outer-product MFMA (slot t holds a_i * b_j): lanes 0-31 carry slots 0-7 =
+// (0,0) (1,0) (2,0) (0,1) (1,1) (2,1) (0,2) (1,2), lanes 32-63 slot 8 = (2,2) and zeros. The byte-permute
+// selectors pick each operand dword from the staged pair {s0 | s1 << 16, s2} (bytes 0-3 and 4-7).
+struct SplitSel {
+    uint32_t a[4], b[4];
+};
+__device__ __forceinline__ SplitSel make_split_sel(int h) {
+    SplitSel s;
+    if (h == 0) {
+        s.a[0] = 0x03020100u; s.a[1] = 0x01000504u; s.a[2] = 0x05040302u; s.a[3] = 0x03020100u;  // a0a1 a2a0 a1a2 a0a1
+        s.b[0] = 0x01000100u; s.b[1] = 0x03020100u; s.b[2] = 0x03020302u; s.b[3] = 0x05040504u;  // b0b0 b0b1 b1b1 b2b2
+    } else {
+        s.a[0] = s.b[0] = 0x07060504u;                                                              // s2 | 0
+        s.a[1] = s.a[2] = s.a[3] = s.b[1] = s.b[2] = s.b[3] = 0x0C0C0C0Cu;                          // zeros
+    }
+    return s;
+}
+__device__ __forceinline__ v8bf split_operand(uint2 c, const uint32_t (&sel)[4]) {
+    uint32_t d[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) d[i] = __builtin_amdgcn_perm(c.y, c.x, sel[i]);
+    return __builtin_bit_cast(v8bf, d);
 }
 
 template <int FMT>
@@ -355,8 +394,8 @@ struct alignas(16) GemmSmem2 {
     // uniform: fp8 bytes (8 per row, block and half); E2M1: the raw packed codes in .x
     uint2 a[2][SKB2 * 2 * CPL2];
     uint2 b[2][SKB2 * 2 * CPL2];
-    float as[2][SKB2 * SPL2];
-    float bs[2][SKB2 * SPL2];
+    uint2 as[2][SKB2 * SPL2];  // split scales
+    uint2 bs[2][SKB2 * SPL2];
     int32_t grp[2];
 };
 
@@ -375,8 +414,21 @@ __device__ __forceinline__ v16f block_dot(uint2 a, uint2 b) {
     }
 }
 
-template <int FMT, int OUT>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
+__device__ __forceinline__ v16f scale_outer(v8bf a, v8bf b) {
+    const v16f z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, z, 0, 0, 0);
+}
+
+// VEC: the operands' rows are 16-byte aligned at every stage start (code row stride % 16 == 0, scale row
+// stride % 4 == 0, first block % 4 == 0), so stages are fetched with 16-byte loads.
+//
+// Work split: 8 waves per 128 x 128 tile; wave (wm, wn) owns rows 64 wm .. +64 and columns 32 wn .. +32, i.e.
+// two 32 x 32 MFMA tiles. At <= 128 VGPRs two workgroups share a CU (four waves per SIMD), which is what
+// lets MFMAs and VALU FMAs of different waves overlap: a single wave issues neither back to back.
+constexpr int kWaves2 = 8;
+
+template <int FMT, int OUT, bool VEC>
+__global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     __shared__ GemmSmem2<FMT> sm;
     const GemmJob& j = args.j;
     const int tid = threadIdx.x;
@@ -385,93 +437,107 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
     if (!resolve_tile(j, sm.grp, tl)) return;
 
     const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
-    const int wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+    const int wave = tid >> 6, wm = wave >> 2, wn = wave & 3;
+    const SplitSel sel = make_split_sel(h);
 
-    float acc[2][2][16];
+    float acc[2][16];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
+        for (int i = 0; i < 16; ++i) acc[a][i] = 0.0f;
 
-    uint2 ra[2], rb[2];
-    float rsa[2], rsb[2];
-    const int64_t nstages = (tl.nkb + SKB2 - 1) / SKB2;
+    const int64_t nkb = tl.nkb;
+    const int64_t nstages = (nkb + SKB2 - 1) / SKB2;
+
+    // staging: threads 0-255 fetch A codes, 256-511 B codes (two threads per row, 16 bytes = two blocks
+    // each); threads 0-127 fetch A scales, 128-255 B scales (one row, four blocks each)
+    const bool c_is_a = tid < 256;
+    const int crow = (tid & 255) >> 1, chalf = tid & 1;
+    const bool has_s = tid < 256;
+    const bool s_is_a = tid < 128;
+    const int srow = tid & 127;
+    uint4 qc, qs;
 
     auto load_stage = [&](int64_t s) {
         const int64_t ks = s * SKB2;
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            const int e = tid + 256 * q;
-            const int row = e >> 2, kb = e & 3;
-            const bool kok = ks + kb < tl.nkb;
-            const bool aok = kok && row < tl.mrows, bok = kok && row < tl.nrows;
-            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + row * j.lda + (ks + kb) * 8) : make_uint2(0, 0);
-            rsa[q] = aok ? tl.as[row * j.ldas + ks + kb] : 0.0f;
-            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + row * j.ldb + (ks + kb) * 8) : make_uint2(0, 0);
-            rsb[q] = bok ? tl.bs[row * j.ldbs + ks + kb] : 0.0f;
+        {
+            const uint8_t* base = c_is_a ? tl.a : tl.b;
+            const int64_t ld = c_is_a ? j.lda : j.ldb;
+            const int rows = c_is_a ? tl.mrows : tl.nrows;
+            const int64_t kb = ks + 2 * chalf;
+            qc = make_uint4(0, 0, 0, 0);
+            if (crow < rows) {
+                const uint8_t* p = base + crow * ld + kb * 8;
+                if (VEC && kb + 1 < nkb) {
+                    qc = *reinterpret_cast<const uint4*>(p);
+                } else {
+                    const uint2 u0 = kb < nkb ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+                    const uint2 u1 = kb + 1 < nkb ? *reinterpret_cast<const uint2*>(p + 8) : make_uint2(0, 0);
+                    qc = make_uint4(u0.x, u0.y, u1.x, u1.y);
+                }
+            }
         }
+        qs = make_uint4(0, 0, 0, 0);
+        if (has_s) {
+            const float* base = s_is_a ? tl.as : tl.bs;
+            const int64_t ld = s_is_a ? j.ldas : j.ldbs;
+            const int rows = s_is_a ? tl.mrows : tl.nrows;
+            if (srow < rows) {
+                const float* p = base + srow * ld + ks;
+                if (VEC && ks + 3 < nkb) {
+                    qs = *reinterpret_cast<const uint4*>(p);
+                } else {
+                    uint32_t v[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) v[q] = ks + q < nkb ? __float_as_uint(p[q]) : 0u;
+                    qs = make_uint4(v[0], v[1], v[2], v[3]);
+                }
+            }
+        }
+    };
+    auto put_codes = [&](uint2* plane, uint32_t c, int kb, int half) {
+        if constexpr (FMT == kFmtUniform) plane[(kb * 2 + half) * CPL2 + crow] = uniform_to_e4m3(c);
+        else plane[(kb * 2 + half) * CPL2 + crow] = make_uint2(c, 0);
     };
     auto store_stage = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            const int e = tid + 256 * q;
-            const int row = e >> 2, kb = e & 3;
-            if constexpr (FMT == kFmtUniform) {
-                sm.a[buf][(kb * 2 + 0) * CPL2 + row] = uniform_to_e4m3(ra[q].x);
-                sm.a[buf][(kb * 2 + 1) * CPL2 + row] = uniform_to_e4m3(ra[q].y);
-                sm.b[buf][(kb * 2 + 0) * CPL2 + row] = uniform_to_e4m3(rb[q].x);
-                sm.b[buf][(kb * 2 + 1) * CPL2 + row] = uniform_to_e4m3(rb[q].y);
-            } else {
-                sm.a[buf][(kb * 2 + 0) * CPL2 + row] = make_uint2(ra[q].x, 0);
-                sm.a[buf][(kb * 2 + 1) * CPL2 + row] = make_uint2(ra[q].y, 0);
-                sm.b[buf][(kb * 2 + 0) * CPL2 + row] = make_uint2(rb[q].x, 0);
-                sm.b[buf][(kb * 2 + 1) * CPL2 + row] = make_uint2(rb[q].y, 0);
-            }
-            sm.as[buf][kb * SPL2 + row] = rsa[q];
-            sm.bs[buf][kb * SPL2 + row] = rsb[q];
+        uint2* cp = c_is_a ? sm.a[buf] : sm.b[buf];
+        const int kb0 = 2 * chalf;
+        put_codes(cp, qc.x, kb0, 0);
+        put_codes(cp, qc.y, kb0, 1);
+        put_codes(cp, qc.z, kb0 + 1, 0);
+        put_codes(cp, qc.w, kb0 + 1, 1);
+        if (has_s) {
+            uint2* sp = s_is_a ? sm.as[buf] : sm.bs[buf];
+            sp[0 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.x));
+            sp[1 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.y));
+            sp[2 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.z));
+            sp[3 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.w));
         }
     };
 
-    if (nstages > 0) {
-        load_stage(0);
-        store_stage(0);
-    }
-    __syncthreads();
-
-    const v32f z32 = {};
     for (int64_t s = 0; s < nstages; ++s) {
         const int buf = (int)(s & 1);
+        if (s == 0) {
+            load_stage(0);
+            store_stage(0);
+            __syncthreads();
+        }
         if (s + 1 < nstages) load_stage(s + 1);
-        const int64_t left = tl.nkb - s * SKB2;
+        const int64_t left = nkb - s * SKB2;
         const int kbn = (int)(left < SKB2 ? left : SKB2);
 #pragma unroll
         for (int kb = 0; kb < SKB2; ++kb) {
             if (kb < kbn) {
-                uint2 av[2], bv[2];
+                const int pl = (kb * 2 + h) * CPL2;
+                const uint2 b0 = sm.b[buf][pl + wn * 32 + l32];
+                const v8bf vb = split_operand(sm.bs[buf][kb * SPL2 + wn * 32 + l32], sel.b);
 #pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2) {
-                    av[t2] = sm.a[buf][(kb * 2 + h) * CPL2 + wm * 64 + t2 * 32 + l32];
-                    bv[t2] = sm.b[buf][(kb * 2 + h) * CPL2 + wn * 64 + t2 * 32 + l32];
-                }
-                // Outer products sA x sB with the two-block f32 MFMA: lanes 0-31 feed block 0, lanes 32-63
-                // block 1. X = {tile (0,0), tile (1,1)}, Y = {tile (0,1), tile (1,0)}: every lane supplies the
-                // A scale of tile row h, and the B scale of tile column h (X) or 1 - h (Y).
-                const float sa = sm.as[buf][kb * SPL2 + wm * 64 + h * 32 + l32];
-                const float sbx = sm.bs[buf][kb * SPL2 + wn * 64 + h * 32 + l32];
-                const float sby = sm.bs[buf][kb * SPL2 + wn * 64 + (1 - h) * 32 + l32];
-                v16f d[4];
+                for (int a = 0; a < 2; ++a) {
+                    const int ra = wm * 64 + a * 32 + l32;
+                    const v16f d = block_dot<FMT>(sm.a[buf][pl + ra], b0);
+                    const v16f w = scale_outer(split_operand(sm.as[buf][kb * SPL2 + ra], sel.a), vb);
 #pragma unroll
-                for (int t = 0; t < 4; ++t) d[t] = block_dot<FMT>(av[t >> 1], bv[t & 1]);
-                const v32f wx = __builtin_amdgcn_mfma_f32_32x32x1f32(sa, sbx, z32, 0, 0, 0);
-                const v32f wy = __builtin_amdgcn_mfma_f32_32x32x1f32(sa, sby, z32, 0, 0, 0);
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    acc[0][0][i] = __builtin_fmaf(d[0][i], wx[i], acc[0][0][i]);
-                    acc[1][1][i] = __builtin_fmaf(d[3][i], wx[16 + i], acc[1][1][i]);
-                    acc[0][1][i] = __builtin_fmaf(d[1][i], wy[i], acc[0][1][i]);
-                    acc[1][0][i] = __builtin_fmaf(d[2][i], wy[16 + i], acc[1][0][i]);
+                    for (int i = 0; i < 16; ++i) acc[a][i] = __builtin_fmaf(d[i], w[i], acc[a][i]);
                 }
             }
         }
@@ -479,7 +545,25 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
         __syncthreads();
     }
 
-    store_tile<OUT>(j, tl, acc, 1.0f, wm, wn, h, l32);
+    // uniform: the fp8 subnormal encoding scaled every product by 2^-18
+    const float mul = FMT == kFmtUniform ? 262144.0f : 1.0f;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const int col = wn * 32 + l32;
+        if (col >= tl.nrows) continue;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int row = wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+            if (row >= tl.mrows) continue;
+            const float v = acc[a][i] * mul;
+            const int64_t off = tl.c_off + (int64_t)row * j.ldc + col;
+            if constexpr (OUT == kOutF32) {
+                static_cast<float*>(j.c)[off] = v;
+            } else {
+                static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
+            }
+        }
+    }
 }
 
 // UFP4_GEMM_MFMA=i8 selects the int8-MFMA kernel (cvt + scale product + fma per output and block) instead of
@@ -503,10 +587,18 @@ static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
     }
     if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
     GemmArgs args{j};
+    // 16-byte staging loads need every stage start of every row aligned; the ragged-K groups start at
+    // arbitrary blocks, so they take the guarded 8-byte path.
+    const bool vec = j.mode != kGemmRaggedK && j.lda % 16 == 0 && j.ldb % 16 == 0 && j.ldas % 4 == 0 &&
+                     j.ldbs % 4 == 0 && (uintptr_t)j.a % 16 == 0 && (uintptr_t)j.b % 16 == 0 &&
+                     (uintptr_t)j.as % 16 == 0 && (uintptr_t)j.bs % 16 == 0 &&
+                     (j.mode != kGemmRaggedM || j.b_group_kb % 4 == 0);
     if (use_i8_mfma()) {
         gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+    } else if (vec) {
+        gemm_f32_kernel<FMT, OUT, true><<<grid, 64 * kWaves2, 0, s>>>(args);
     } else {
-        gemm_f32_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
+        gemm_f32_kernel<FMT, OUT, false><<<grid, 64 * kWaves2, 0, s>>>(args);
     }
     return hipGetLastError();
 }

@@ -24,13 +24,17 @@ namespace ufp4 {
 // Per-element rounding onto the grid; returns the 4-bit code in the low bits.
 // ------------------------------------------------------------------------------------------------
 
-// 1.5 * 2^23: adding it to |x| <= 2^22 rounds x to an integer (round-half-even in the current rounding
-// mode) and leaves that integer, in two's complement, in the low mantissa bits.
+// 1.5 * 2^23: adding it to 0 <= x <= 2^22 rounds x to an integer (round-half-even in the current rounding
+// mode) and leaves that integer in the low mantissa bits.
 constexpr float kMagic = 12582912.0f;
 
+// Codes are sign-magnitude nibbles: sign in bit 3, |k| in bits 0-2, zero as +0.
+//
+// RTNE: rounding is symmetric, so |k| = rint(|v|); k < 0 exactly when v < -1/2. No clamp is needed:
+// |v| = RN(|y| * RN(7/amax)) <= 7 (1 + 2^-23), which still rounds to 7.
 __device__ __forceinline__ uint32_t uniform_rtne(float v) {
-    const float vc = __builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f);
-    return __float_as_uint(vc + kMagic) & 0xFu;
+    const uint32_t mag = __float_as_uint(__builtin_fabsf(v) + kMagic) & 0x7u;
+    return mag | (v < -0.5f ? 8u : 0u);
 }
 
 // Stochastic rounding between the integers lo = floor(v) and lo + 1: up iff lo + u/2^16 < v. Both sides
@@ -40,7 +44,8 @@ __device__ __forceinline__ uint32_t uniform_sr(float v, uint32_t u16) {
     const float lo = floorf(vc);
     const float t = __builtin_fmaf((float)u16, 1.0f / 65536.0f, lo);
     const float k = (t < vc) ? lo + 1.0f : lo;
-    return __float_as_uint(k + kMagic) & 0xFu;
+    const uint32_t mag = __float_as_uint(__builtin_fabsf(k) + kMagic) & 0x7u;
+    return mag | (k < 0.0f ? 8u : 0u);
 }
 
 // E2M1 magnitude code of the nearest level, ties to the even code (levels 0,.5,1,1.5,2,3,4,6; the bin

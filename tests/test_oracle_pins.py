@@ -405,7 +405,7 @@ def test_pack_unpack_roundtrip_and_bit_patterns():
         assert p.shape == (5, 16)
         assert np.array_equal(O.unpack_codes(p, fmt), idx)
     one = np.array([[-1, 7, -7, 0]])
-    assert list(O.pack_codes(one, O.UNIFORM)[0]) == [0x7F, 0x09]  # -1 -> 0xF, 7 -> 0x7, -7 -> 0x9
+    assert list(O.pack_codes(one, O.UNIFORM)[0]) == [0x79, 0x0F]  # -1 -> 0x9, 7 -> 0x7, -7 -> 0xF, 0 -> 0x0
     e = np.array([[-7, 7, -1, 0]])  # E2M1: -6 -> 0xF, 6 -> 0x7, -0.5 -> 0x9, 0 -> 0x0
     assert list(O.pack_codes(e, O.E2M1)[0]) == [0x7F, 0x09]
 
