@@ -126,7 +126,8 @@ int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t
  * strides (code_ld bytes, scale_ld floats) each; `format` is the grid both operands were quantized to
  * (UFP4_FMT_UNIFORM or UFP4_FMT_E2M1); out_dtype UFP4_OUT_F32 or UFP4_OUT_BF16; out_dev row-major with
  * leading dimension ldc (elements). Both operands must come from quantizations with the same rht
- * setting and sign mask (the library cannot check this).
+ * setting and sign mask (the library cannot check this). Code row strides above 2^24 bytes or scale row
+ * strides above 2^22 floats return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_ld, const float *x_scales_dev, int64_t x_scale_ld,
                     const void *w_codes_dev, int64_t w_code_ld, const float *w_scales_dev, int64_t w_scale_ld,

@@ -91,6 +91,10 @@ int check_gemm(const void* a, int64_t lda, const float* as, int64_t ldas, const 
     if (!aligned(a, 8) || !aligned(b, 8) || !aligned(as, 4) || !aligned(bs, 4)) return UFP4_ERR_ALIGN;
     if (!aligned(c, out_dtype == UFP4_OUT_F32 ? 4 : 2)) return UFP4_ERR_ALIGN;
     if (rows_a >= (int64_t(1) << 31) || rows_b >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    // a 128-row tile of either operand must lie within 2^31 bytes (32-bit buffer offsets)
+    if (lda > (int64_t(1) << 24) || ldb > (int64_t(1) << 24) || ldas > (int64_t(1) << 22) ||
+        ldbs > (int64_t(1) << 22))
+        return UFP4_ERR_UNSUPPORTED;
     return UFP4_OK;
 }
 

@@ -16,7 +16,7 @@
 //
 // Grouped (MoE) problems: ragged M (fwd_y, bwd_dx: token rows split into groups) resolves its group
 // from the tile index with a wave-wide prefix sum over the group sizes; ragged K (bwd_dw: the reduction
-// runs over each group's padded token range) takes the group from blockIdx.z.
+// runs over each group's padded token range) takes the group from the grid's z index.
 
 #include <cstdlib>
 #include <cstring>
@@ -159,14 +159,21 @@ __device__ __forceinline__ void store_tile(const GemmJob& j, const Tile& tl, con
     }
 }
 
+// Grid position of a workgroup: tile column, tile row (ragged-M: global m-tile index) and group (ragged-K).
+struct TilePos {
+    int64_t tn, tm;
+    int g;
+};
+__device__ __forceinline__ TilePos grid_pos() { return {(int64_t)blockIdx.x, (int64_t)blockIdx.y, (int)blockIdx.z}; }
+
 // Resolve the workgroup's output tile (dense, ragged-M group or ragged-K group). Returns false when the
 // workgroup has nothing to do (a ragged-M tile index past the last group); all threads agree.
-__device__ bool resolve_tile(const GemmJob& j, int32_t* grp, Tile& tl) {
-    const int64_t tn = blockIdx.x;
+__device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos, Tile& tl) {
+    const int64_t tn = pos.tn;
     if (j.mode == kGemmRaggedM) {
         int g;
         int64_t lt;
-        if (!resolve_ragged_m(j, grp, blockIdx.y, g, lt)) return false;
+        if (!resolve_ragged_m(j, grp, pos.tm, g, lt)) return false;
         const int64_t r0 = j.offsets[g] + lt * BM;
         const int64_t end = j.offsets[g + 1] < j.M ? j.offsets[g + 1] : j.M;  // offsets past M_total: ignored
         const int64_t rows_g = end - r0;
@@ -183,11 +190,11 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, Tile& tl) {
         tl.nkb = j.nkb;
         tl.c_off = r0 * j.ldc + tn * BN;
     } else {
-        const int64_t tm = blockIdx.y;
+        const int64_t tm = pos.tm;
         int64_t kb0 = 0, c_base = 0;
         tl.nkb = j.nkb;
         if (j.mode == kGemmRaggedK) {
-            const int g = blockIdx.z;
+            const int g = pos.g;
             // the group's padded token range, clamped to the operands' reduction length
             const int64_t p0 = j.offsets[g] < j.red_total ? j.offsets[g] : j.red_total;
             const int64_t p1 = j.offsets[g + 1] < j.red_total ? j.offsets[g + 1] : j.red_total;
@@ -215,7 +222,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
     const int tid = threadIdx.x;
 
     Tile tl;
-    if (!resolve_tile(j, sm.grp, tl)) return;
+    if (!resolve_tile(j, sm.grp, grid_pos(), tl)) return;
 
     // ---- main loop ----------------------------------------------------------------------------
     const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
@@ -323,7 +330,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
 // ================================================================================================
 // fp32-output variant (the default).
 //
-// The per-block dot product D_b comes out of the MFMA already in fp32 and a second MFMA forms the outer
+// The per-block dot product D_b comes out of an MFMA already in fp32 and a second MFMA forms the outer
 // product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and block:
 // acc += D_b * (sA sB)_b.
 //
@@ -331,71 +338,68 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
 //    LDS and go through v_mfma_f32_32x32x16_fp8_fp8; E2M1 codes go straight into the scaled f8f6f4 MFMA as
 //    FP4 operands (neutral E8M0 scales), the 16 codes of a block occupying 16 of its 64 K slots.
 //  * (sA sB)_b: every fp32 scale is split exactly into three bf16 pieces s = s0 + s1 + s2 (top, middle and
-//    low 8 significand bits) when staged; a v_mfma_f32_32x32x16_bf16 whose 16 K slots hold the nine
-//    products a_i b_j (exact in fp32) sums them, i.e. sA sB up to fp32 accumulation rounding. The bf16
-//    MFMA co-executes with the VALU FMAs; an fp32 MFMA would not.
-//  * The MFMAs of one half of the wave's four tiles run while the VALU folds the other half (software
-//    pipeline across K-blocks and stages).
+//    low 8 significand bits) when staged, and stored directly as the operand of a v_mfma_f32_32x32x8_bf16
+//    whose 8 K slots hold eight of the nine piece products (all but s2 * s2', below 2^-30 sA sB). Products
+//    of two 8-bit significands are exact in fp32, so the MFMA returns sA sB up to fp32 accumulation
+//    rounding. The bf16 MFMA co-executes with the VALU FMAs; an fp32 MFMA would not.
+//  * Staging: global reads are buffer loads (out-of-range rows read as zero, so no branches) issued two
+//    stages ahead into registers; the conversions happen once per workgroup when a stage is written to LDS.
 // ================================================================================================
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef short v4s __attribute__((ext_vector_type(4)));
 
-constexpr int SKB2 = 4;          // K-blocks per LDS stage
-constexpr int CPL2 = BM + 1;     // code plane stride in 8-byte entries
-constexpr int SPL2 = BM + 2;     // scale plane stride in 8-byte entries
+constexpr int SKB2 = 4;       // K-blocks per LDS stage
+constexpr int PL2 = BM + 1;   // 8-byte entries per LDS plane (one plane per block and half-wave)
 
 // 8 uniform codes (one packed dword of sign-magnitude nibbles) -> 8 fp8 e4m3 bytes. The byte s000 0mmm is an
 // e4m3 subnormal worth (-1)^s * m * 2^-9, so the code k becomes k * 2^-9 exactly (the product of two codes
-// carries 2^-18, undone once at the store). Even codes go to the low dword, odd codes to the high one.
+// carries 2^-18, undone once at the store). Even codes go to the low dword, odd codes to the high one; both
+// operands use the same order, so the K-slot permutation cancels in the dot product.
 __device__ __forceinline__ uint2 uniform_to_e4m3(uint32_t d) {
     const uint32_t lo = (d & 0x07070707u) | ((d << 4) & 0x80808080u);
     const uint32_t hi = ((d >> 4) & 0x07070707u) | (d & 0x80808080u);
     return make_uint2(lo, hi);
 }
 
-// Exact split of an fp32 value into three bf16 pieces x = s0 + s1 + s2 (truncations of the top, middle and
-// low 8 significand bits; each difference is exact in fp32). Returned as {s0 | s1 << 16, s2}.
-__device__ __forceinline__ uint2 split_bf16x3(float x) {
-    const uint32_t hi = __float_as_uint(x) & 0xFFFF0000u;
-    const float r1 = x - __uint_as_float(hi);
-    const uint32_t mid = __float_as_uint(r1) & 0xFFFF0000u;
-    const float r2 = r1 - __uint_as_float(mid);
-    return make_uint2((hi >> 16) | mid, __float_as_uint(r2) >> 16);
+// Exact split x = p0 + p1 + p2 into three bf16 values, each returned in the top half of a dword (low half
+// zero): truncations of the top, middle and low 8 significand bits; both differences are exact in fp32.
+__device__ __forceinline__ void split_bf16x3(float x, uint32_t& p0, uint32_t& p1, uint32_t& p2) {
+    p0 = __float_as_uint(x) & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(p0);
+    p1 = __float_as_uint(r1) & 0xFFFF0000u;
+    p2 = __float_as_uint(r1 - __uint_as_float(p1));
 }
 
-// K-slot layout of the outer-product MFMA (slot t holds a_i * b_j): lanes 0-31 carry slots 0-7 =
-// (0,0) (1,0) (2,0) (0,1) (1,1) (2,1) (0,2) (1,2), lanes 32-63 slot 8 = (2,2) and zeros. The byte-permute
-// selectors pick each operand dword from the staged pair {s0 | s1 << 16, s2} (bytes 0-3 and 4-7).
-struct SplitSel {
-    uint32_t a[4], b[4];
+// {lo: bf16 of x, hi: bf16 of y} from two split pieces
+__device__ __forceinline__ uint32_t bf16_pair(uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x07060302u); }
+
+// Outer-product operands of one (row, block) scale. K slots 0-3 (lanes 0-31) and 4-7 (lanes 32-63) hold
+//   A side: a0 a0 a0 a1 | a1 a1 a2 a2        B side: b0 b1 b2 b0 | b1 b2 b0 b1
+// so the eight slot products are a0b0 a0b1 a0b2 a1b0 a1b1 a1b2 a2b0 a2b1.
+struct ScaleOp {
+    uint2 h0, h1;
 };
-__device__ __forceinline__ SplitSel make_split_sel(int h) {
-    SplitSel s;
-    if (h == 0) {
-        s.a[0] = 0x03020100u; s.a[1] = 0x01000504u; s.a[2] = 0x05040302u; s.a[3] = 0x03020100u;  // a0a1 a2a0 a1a2 a0a1
-        s.b[0] = 0x01000100u; s.b[1] = 0x03020100u; s.b[2] = 0x03020302u; s.b[3] = 0x05040504u;  // b0b0 b0b1 b1b1 b2b2
-    } else {
-        s.a[0] = s.b[0] = 0x07060504u;                                                              // s2 | 0
-        s.a[1] = s.a[2] = s.a[3] = s.b[1] = s.b[2] = s.b[3] = 0x0C0C0C0Cu;                          // zeros
-    }
-    return s;
+__device__ __forceinline__ ScaleOp scale_op_a(float s) {
+    uint32_t p0, p1, p2;
+    split_bf16x3(s, p0, p1, p2);
+    return {make_uint2(bf16_pair(p0, p0), bf16_pair(p0, p1)), make_uint2(bf16_pair(p1, p1), bf16_pair(p2, p2))};
 }
-__device__ __forceinline__ v8bf split_operand(uint2 c, const uint32_t (&sel)[4]) {
-    uint32_t d[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) d[i] = __builtin_amdgcn_perm(c.y, c.x, sel[i]);
-    return __builtin_bit_cast(v8bf, d);
+__device__ __forceinline__ ScaleOp scale_op_b(float s) {
+    uint32_t p0, p1, p2;
+    split_bf16x3(s, p0, p1, p2);
+    const uint32_t q01 = bf16_pair(p0, p1);
+    return {make_uint2(q01, bf16_pair(p2, p0)), make_uint2(bf16_pair(p1, p2), q01)};
 }
 
-template <int FMT>
 struct alignas(16) GemmSmem2 {
-    // uniform: fp8 bytes (8 per row, block and half); E2M1: the raw packed codes in .x
-    uint2 a[2][SKB2 * 2 * CPL2];
-    uint2 b[2][SKB2 * 2 * CPL2];
-    uint2 as[2][SKB2 * SPL2];  // split scales
-    uint2 bs[2][SKB2 * SPL2];
+    // plane (block * 2 + half) holds one 8-byte entry per row: codes (fp8 bytes for uniform, 8 FP4 codes in
+    // .x for E2M1) and outer-product scale operands
+    uint2 a[2][SKB2 * 2 * PL2];
+    uint2 b[2][SKB2 * 2 * PL2];
+    uint2 as[2][SKB2 * 2 * PL2];
+    uint2 bs[2][SKB2 * 2 * PL2];
     int32_t grp[2];
 };
 
@@ -414,31 +418,58 @@ __device__ __forceinline__ v16f block_dot(uint2 a, uint2 b) {
     }
 }
 
-__device__ __forceinline__ v16f scale_outer(v8bf a, v8bf b) {
+__device__ __forceinline__ v16f scale_outer(uint2 a, uint2 b) {
     const v16f z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, z, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(__builtin_bit_cast(v4s, a), __builtin_bit_cast(v4s, b), z, 0, 0,
+                                                     0);
 }
 
-// VEC: the operands' rows are 16-byte aligned at every stage start (code row stride % 16 == 0, scale row
-// stride % 4 == 0, first block % 4 == 0), so stages are fetched with 16-byte loads.
-//
+// Wave-uniform copies (SGPRs) of values the compiler cannot prove uniform, e.g. those read back from LDS.
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+    const uint64_t u = (uint64_t)v;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+template <typename T>
+__device__ __forceinline__ const T* uniform_ptr(const T* p) {
+    return reinterpret_cast<const T*>(uniform_i64((int64_t)(uintptr_t)p));
+}
+
+// Raw buffer resource over `bytes` bytes from `base`: loads at offsets past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Registers of one stage held by one thread: two blocks of codes of one row, and their two scales.
+struct StageRegs {
+    uint2 c0, c1;
+    uint32_t s0, s1;
+};
+
 // Work split: 8 waves per 128 x 128 tile; wave (wm, wn) owns rows 64 wm .. +64 and columns 32 wn .. +32, i.e.
 // two 32 x 32 MFMA tiles. At <= 128 VGPRs two workgroups share a CU (four waves per SIMD), which is what
 // lets MFMAs and VALU FMAs of different waves overlap: a single wave issues neither back to back.
 constexpr int kWaves2 = 8;
 
-template <int FMT, int OUT, bool VEC>
+template <int FMT, int OUT>
 __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
-    __shared__ GemmSmem2<FMT> sm;
+    __shared__ GemmSmem2 sm;
     const GemmJob& j = args.j;
     const int tid = threadIdx.x;
 
     Tile tl;
-    if (!resolve_tile(j, sm.grp, tl)) return;
+    if (!resolve_tile(j, sm.grp, grid_pos(), tl)) return;
+    // the buffer resources below must live in SGPRs
+    tl.a = uniform_ptr(tl.a);
+    tl.b = uniform_ptr(tl.b);
+    tl.as = uniform_ptr(tl.as);
+    tl.bs = uniform_ptr(tl.bs);
+    tl.mrows = __builtin_amdgcn_readfirstlane(tl.mrows);
+    tl.nrows = __builtin_amdgcn_readfirstlane(tl.nrows);
+    tl.nkb = uniform_i64(tl.nkb);
 
     const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
-    const int wave = tid >> 6, wm = wave >> 2, wn = wave & 3;
-    const SplitSel sel = make_split_sel(h);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), wm = wave >> 2, wn = wave & 3;
 
     float acc[2][16];
 #pragma unroll
@@ -446,103 +477,93 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[a][i] = 0.0f;
 
-    const int64_t nkb = tl.nkb;
-    const int64_t nstages = (nkb + SKB2 - 1) / SKB2;
+    // 32-bit stage counters keep the loop (and the buffer loads' stage offsets) on the scalar unit
+    const int nkb = __builtin_amdgcn_readfirstlane((int)tl.nkb);
+    const int nstages = (nkb + SKB2 - 1) / SKB2;
 
-    // staging: threads 0-255 fetch A codes, 256-511 B codes (two threads per row, 16 bytes = two blocks
-    // each); threads 0-127 fetch A scales, 128-255 B scales (one row, four blocks each)
-    const bool c_is_a = tid < 256;
-    const int crow = (tid & 255) >> 1, chalf = tid & 1;
-    const bool has_s = tid < 256;
-    const bool s_is_a = tid < 128;
-    const int srow = tid & 127;
-    uint4 qc, qs;
+    // Staging: waves 0-3 fetch A, waves 4-7 B; thread (row, pair) takes blocks 2 pair and 2 pair + 1 of its
+    // row in every stage: 2 x 8 bytes of codes and 2 scales.
+    const bool st_a = wave < 4;
+    const int srow = (tid & 255) >> 1, spair = tid & 1;
+    const int rows = st_a ? tl.mrows : tl.nrows;
+    const int64_t ldc_b = st_a ? j.lda : j.ldb;   // code row stride, bytes
+    const int64_t lds_f = st_a ? j.ldas : j.ldbs;  // scale row stride, floats
+    const __amdgpu_buffer_rsrc_t rc =
+        make_rsrc(st_a ? (const void*)tl.a : (const void*)tl.b, (uint32_t)((rows - 1) * ldc_b + (int64_t)nkb * 8));
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(st_a ? (const void*)tl.as : (const void*)tl.bs, (uint32_t)(((rows - 1) * lds_f + (int64_t)nkb) * 4));
+    const int voc = (int)(srow * ldc_b) + spair * 16;
+    const int vos = (int)(srow * lds_f + spair * 2) * 4;
 
-    auto load_stage = [&](int64_t s) {
-        const int64_t ks = s * SKB2;
-        {
-            const uint8_t* base = c_is_a ? tl.a : tl.b;
-            const int64_t ld = c_is_a ? j.lda : j.ldb;
-            const int rows = c_is_a ? tl.mrows : tl.nrows;
-            const int64_t kb = ks + 2 * chalf;
-            qc = make_uint4(0, 0, 0, 0);
-            if (crow < rows) {
-                const uint8_t* p = base + crow * ld + kb * 8;
-                if (VEC && kb + 1 < nkb) {
-                    qc = *reinterpret_cast<const uint4*>(p);
-                } else {
-                    const uint2 u0 = kb < nkb ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
-                    const uint2 u1 = kb + 1 < nkb ? *reinterpret_cast<const uint2*>(p + 8) : make_uint2(0, 0);
-                    qc = make_uint4(u0.x, u0.y, u1.x, u1.y);
-                }
-            }
-        }
-        qs = make_uint4(0, 0, 0, 0);
-        if (has_s) {
-            const float* base = s_is_a ? tl.as : tl.bs;
-            const int64_t ld = s_is_a ? j.ldas : j.ldbs;
-            const int rows = s_is_a ? tl.mrows : tl.nrows;
-            if (srow < rows) {
-                const float* p = base + srow * ld + ks;
-                if (VEC && ks + 3 < nkb) {
-                    qs = *reinterpret_cast<const uint4*>(p);
-                } else {
-                    uint32_t v[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) v[q] = ks + q < nkb ? __float_as_uint(p[q]) : 0u;
-                    qs = make_uint4(v[0], v[1], v[2], v[3]);
-                }
-            }
-        }
+    auto load = [&](StageRegs& r, int s) {
+        const int soc = __builtin_amdgcn_readfirstlane(s * SKB2 * 8), sos = __builtin_amdgcn_readfirstlane(s * SKB2 * 4);
+        r.c0 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, voc, soc, 0));
+        r.c1 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, voc + 8, soc, 0));
+        r.s0 = __builtin_amdgcn_raw_buffer_load_b32(rs, vos, sos, 0);
+        r.s1 = __builtin_amdgcn_raw_buffer_load_b32(rs, vos + 4, sos, 0);
     };
-    auto put_codes = [&](uint2* plane, uint32_t c, int kb, int half) {
-        if constexpr (FMT == kFmtUniform) plane[(kb * 2 + half) * CPL2 + crow] = uniform_to_e4m3(c);
-        else plane[(kb * 2 + half) * CPL2 + crow] = make_uint2(c, 0);
+    auto conv = [](uint32_t d) -> uint2 {
+        if constexpr (FMT == kFmtUniform) return uniform_to_e4m3(d);
+        else return make_uint2(d, 0u);
     };
-    auto store_stage = [&](int buf) {
-        uint2* cp = c_is_a ? sm.a[buf] : sm.b[buf];
-        const int kb0 = 2 * chalf;
-        put_codes(cp, qc.x, kb0, 0);
-        put_codes(cp, qc.y, kb0, 1);
-        put_codes(cp, qc.z, kb0 + 1, 0);
-        put_codes(cp, qc.w, kb0 + 1, 1);
-        if (has_s) {
-            uint2* sp = s_is_a ? sm.as[buf] : sm.bs[buf];
-            sp[0 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.x));
-            sp[1 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.y));
-            sp[2 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.z));
-            sp[3 * SPL2 + srow] = split_bf16x3(__uint_as_float(qs.w));
-        }
+    auto put = [&](int buf, const StageRegs& r) {
+        uint2* cp = st_a ? sm.a[buf] : sm.b[buf];
+        uint2* sp = st_a ? sm.as[buf] : sm.bs[buf];
+        const int e0 = (4 * spair) * PL2 + srow;  // plane (2 pair, half 0)
+        cp[e0] = conv(r.c0.x);
+        cp[e0 + PL2] = conv(r.c0.y);
+        cp[e0 + 2 * PL2] = conv(r.c1.x);
+        cp[e0 + 3 * PL2] = conv(r.c1.y);
+        const ScaleOp o0 = st_a ? scale_op_a(__uint_as_float(r.s0)) : scale_op_b(__uint_as_float(r.s0));
+        const ScaleOp o1 = st_a ? scale_op_a(__uint_as_float(r.s1)) : scale_op_b(__uint_as_float(r.s1));
+        sp[e0] = o0.h0;
+        sp[e0 + PL2] = o0.h1;
+        sp[e0 + 2 * PL2] = o1.h0;
+        sp[e0 + 3 * PL2] = o1.h1;
     };
-
-    for (int64_t s = 0; s < nstages; ++s) {
-        const int buf = (int)(s & 1);
-        if (s == 0) {
-            load_stage(0);
-            store_stage(0);
-            __syncthreads();
-        }
-        if (s + 1 < nstages) load_stage(s + 1);
-        const int64_t left = nkb - s * SKB2;
-        const int kbn = (int)(left < SKB2 ? left : SKB2);
+    auto compute = [&](int buf, int s) {
+        const int left = nkb - s * SKB2;
+        const int kbn = left < SKB2 ? left : SKB2;
 #pragma unroll
         for (int kb = 0; kb < SKB2; ++kb) {
             if (kb < kbn) {
-                const int pl = (kb * 2 + h) * CPL2;
-                const uint2 b0 = sm.b[buf][pl + wn * 32 + l32];
-                const v8bf vb = split_operand(sm.bs[buf][kb * SPL2 + wn * 32 + l32], sel.b);
+                const int pl = (kb * 2 + h) * PL2;
+                const uint2 bc = sm.b[buf][pl + wn * 32 + l32];
+                const uint2 bw = sm.bs[buf][pl + wn * 32 + l32];
 #pragma unroll
                 for (int a = 0; a < 2; ++a) {
-                    const int ra = wm * 64 + a * 32 + l32;
-                    const v16f d = block_dot<FMT>(sm.a[buf][pl + ra], b0);
-                    const v16f w = scale_outer(split_operand(sm.as[buf][kb * SPL2 + ra], sel.a), vb);
+                    const int ra = pl + wm * 64 + a * 32 + l32;
+                    const v16f d = block_dot<FMT>(sm.a[buf][ra], bc);
+                    const v16f w = scale_outer(sm.as[buf][ra], bw);
 #pragma unroll
                     for (int i = 0; i < 16; ++i) acc[a][i] = __builtin_fmaf(d[i], w[i], acc[a][i]);
                 }
             }
         }
-        if (s + 1 < nstages) store_stage(buf ^ 1);
+    };
+
+    if (nstages > 0) {
+        // Loads are issued unconditionally (past the last stage they read zeros or unused bytes) so that the
+        // wait before each LDS write counts exactly the four loads of the stage fetched after it.
+        StageRegs r0, r1;
+        load(r0, 0);
+        load(r1, 1);
+        put(0, r0);
         __syncthreads();
+        // stage s computes from LDS buffer s % 2 while stage s + 2 is fetched into the registers that held
+        // stage s and stage s + 1 (fetched one stage earlier) is written to the other buffer
+        for (int s = 0; s < nstages; s += 2) {
+            load(r0, s + 2);
+            compute(0, s);
+            if (s + 1 >= nstages) break;
+            put(1, r1);
+            __syncthreads();
+            load(r1, s + 3);
+            compute(1, s + 1);
+            if (s + 2 >= nstages) break;
+            put(0, r0);
+            __syncthreads();
+        }
     }
 
     // uniform: the fp8 subnormal encoding scaled every product by 2^-18
@@ -587,18 +608,10 @@ static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
     }
     if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
     GemmArgs args{j};
-    // 16-byte staging loads need every stage start of every row aligned; the ragged-K groups start at
-    // arbitrary blocks, so they take the guarded 8-byte path.
-    const bool vec = j.mode != kGemmRaggedK && j.lda % 16 == 0 && j.ldb % 16 == 0 && j.ldas % 4 == 0 &&
-                     j.ldbs % 4 == 0 && (uintptr_t)j.a % 16 == 0 && (uintptr_t)j.b % 16 == 0 &&
-                     (uintptr_t)j.as % 16 == 0 && (uintptr_t)j.bs % 16 == 0 &&
-                     (j.mode != kGemmRaggedM || j.b_group_kb % 4 == 0);
     if (use_i8_mfma()) {
         gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
-    } else if (vec) {
-        gemm_f32_kernel<FMT, OUT, true><<<grid, 64 * kWaves2, 0, s>>>(args);
     } else {
-        gemm_f32_kernel<FMT, OUT, false><<<grid, 64 * kWaves2, 0, s>>>(args);
+        gemm_f32_kernel<FMT, OUT><<<grid, 64 * kWaves2, 0, s>>>(args);
     }
     return hipGetLastError();
 }
