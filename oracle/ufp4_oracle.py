@@ -133,11 +133,22 @@ def rht_exact_f64(blocks: np.ndarray, sign_mask: int) -> np.ndarray:
     return ((blocks * eps) @ hadamard_pm1(BLOCK)) * 0.25
 
 
+FP32_MIN_NORMAL = 2.0 ** -126
+
+
 def rht_blocks(blocks_f32: np.ndarray, sign_mask: int) -> np.ndarray:
-    """RHT of bf16-valued 16-blocks, correctly rounded to fp32 (one rounding of the exact result)."""
+    """RHT of bf16-valued 16-blocks, correctly rounded to fp32 (one rounding of the exact result).
+
+    Domain: besides `_check_rht_domain`, every nonzero output must be a normal fp32 number (reading of the
+    paper's silence on subnormals: scaling by the RHT's factor 1/4 is then exact in any order).
+    """
     b64 = np.asarray(blocks_f32, dtype=np.float64)
     _check_rht_domain(b64)
-    return rht_exact_f64(b64, sign_mask).astype(np.float32)
+    y = rht_exact_f64(b64, sign_mask).astype(np.float32)
+    mag = np.abs(y)
+    if np.any((mag > 0) & (mag < FP32_MIN_NORMAL)):
+        raise ValueError("an RHT output is a subnormal fp32 number: outside the supported domain")
+    return y
 
 
 # ---------------------------------------------------------------------------------------------------
@@ -258,10 +269,13 @@ def level_values(signed_idx: np.ndarray, fmt: int) -> np.ndarray:
 # ---------------------------------------------------------------------------------------------------
 
 def _check_block_domain(amax: np.ndarray, g: float) -> None:
+    """Supported blocks: finite, and either all zero or with a scale amax/g that is a normal fp32 number."""
     nz = amax > 0
     r = np.float32(g) / np.where(nz, amax, np.float32(1.0))
     if not np.all(np.isfinite(amax)) or not np.all(np.isfinite(r)):
         raise ValueError("non-finite input, or a block amax so small that g/amax overflows fp32")
+    if np.any(nz & (amax.astype(np.float64) < g * FP32_MIN_NORMAL)):
+        raise ValueError("a block amax below g * 2^-126 (subnormal scale): outside the supported domain")
 
 
 def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0,

@@ -130,13 +130,14 @@ def test_rht_correctly_rounded_bruteforce():
             vals[rng.integers(0, 16, size=5)] = 0.0
         blocks.append(O.bf16_bits_to_f32(O.f32_to_bf16_bits(vals.astype(np.float32))))
     blocks = np.array(blocks)
-    # keep only blocks inside the exactness domain after the bf16 rounding
+    # keep only blocks inside the supported domain after the bf16 rounding (sum exact in fp64, no subnormal
+    # fp32 output)
     mask = 0x9E37
     got = None
     keep = []
     for b in blocks:
         try:
-            O._check_rht_domain(b[None].astype(np.float64))
+            O.rht_blocks(b[None], mask)
             keep.append(b)
         except ValueError:
             pass
@@ -161,6 +162,24 @@ def test_rht_domain_is_enforced():
         O.rht_blocks(b.astype(np.float32), 0)
     b[0, 1] = 2.0 ** -21  # spread 41: allowed
     O.rht_blocks(b.astype(np.float32), 0)
+
+
+def test_subnormal_outputs_and_scales_are_outside_the_domain():
+    # RHT output 2^-127 (x0 / 4): subnormal fp32 -> rejected; 2^-126 is the smallest accepted magnitude
+    b = np.zeros((1, 16), dtype=np.float32)
+    b[0, 0] = np.float32(2.0 ** -125)
+    with pytest.raises(ValueError):
+        O.rht_blocks(b, 0)
+    b[0, 0] = np.float32(2.0 ** -124)
+    assert np.all(np.abs(O.rht_blocks(b, 0)) == np.float32(2.0 ** -126))
+    # block scale amax / g must be normal: amax = 2^-124 < 7 * 2^-126 is rejected, 2^-123 accepted (g = 7)
+    a = np.zeros((1, 16), dtype=np.float32)
+    a[0, 3] = np.float32(2.0 ** -124)
+    with pytest.raises(ValueError):
+        O.quantize_rows(a, O.UNIFORM, O.RTNE, False)
+    a[0, 3] = np.float32(2.0 ** -123)
+    idx, sc = O.quantize_rows(a, O.UNIFORM, O.RTNE, False)
+    assert idx[0, 3] == 7 and sc[0, 0] == np.float32(2.0 ** -123 / 7)
 
 
 # ------------------------------------------------------------------------------------------------
