@@ -10,7 +10,10 @@ Prints one JSON line. `value` is the step's GEMM work (3 x 2MNK) divided by the 
 element) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel, the dominant one; `cpu_baseline` times the CPU
 oracle on a bounded sample of the same layer.
 
-Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g]
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g]
+
+Without --warmup the untimed warmup runs whole steps until at least WARMUP_SECONDS have passed: the GPU's clock
+takes tens of milliseconds of load to settle, and a few milliseconds of warmup would time the ramp.
 """
 
 from __future__ import annotations
@@ -33,7 +36,13 @@ from paper_2606_20381_amd import ufp4 as U  # noqa: E402
 from paper_2606_20381_amd import workloads as WL  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
-INT8_PEAK_TOPS = 5000.0  # dense int8 MFMA, MI355X
+INT8_PEAK_TOPS = 5000.0  # dense int8 / fp8 MFMA, MI355X
+# Bound of an exact per-16-block fp32-scale GEMM: one VALU FMA per output and block, i.e. 2MNK / (MNK/16) = 32
+# ops per FMA, at 256 CUs x 4 SIMDs x 16 fp32 FMA lanes per clock x 2.4 GHz = 39.3 T FMA/s (non-packed).
+ATTAINABLE_TOPS = 32 * 256 * 4 * 16 * 2.4e9 / 1e12
+GEMM_KERNEL = "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+WARMUP_SECONDS = 0.5
 QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
 METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
 
@@ -160,6 +169,36 @@ def quant1g_step(tl: Timeline):
 
 
 # ---------------------------------------------------------------------------------------------------
+# measured HBM traffic (rocprofv3 FETCH_SIZE / WRITE_SIZE runs, scaled by a 1 GiB copy), valid only for the
+# kernel source it was measured on
+# ---------------------------------------------------------------------------------------------------
+
+TRAFFIC_SOURCES = {"gemm": "ufp4_gemm.hip", "quant": "ufp4_quant.hip"}
+
+
+def _source_digest(name: str) -> str:
+    import hashlib
+
+    path = os.path.join(ROOT, "paper_2606_20381_amd", "csrc", name)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kind: str, workload: str):
+    """HBM bytes per launch of the dominant kernel from profiles/traffic.json, or None when there is no
+    entry for this workload or the kernel source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            table = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = table.get(kind, {}).get(workload)
+    if not entry or entry.get("source_sha256") != _source_digest(TRAFFIC_SOURCES[kind]):
+        return None
+    return entry["bytes_per_launch"]
+
+
+# ---------------------------------------------------------------------------------------------------
 # CPU oracle baseline: the same layer step on a bounded sample of tokens
 # ---------------------------------------------------------------------------------------------------
 
@@ -193,7 +232,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
     ap.add_argument("--workload", default="dense",
                     choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "copy1g"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -222,8 +261,17 @@ def main():
         wname = wl.name
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
-        step(False)
+    if args.warmup is None:
+        # whole untimed steps until the clock has settled
+        warm, tw = 0, time.perf_counter()
+        while warm < 3 or time.perf_counter() - tw < WARMUP_SECONDS:
+            step(False)
+            torch.cuda.synchronize()
+            warm += 1
+        args.warmup = warm
+    else:
+        for _ in range(args.warmup):
+            step(False)
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -261,9 +309,11 @@ def main():
         per_launch = np.mean([kern[k][1] for k in gemm_labels])
         avg_us = np.mean([tl.mean_us(k) for k in gemm_labels])
         ach = per_launch / (avg_us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "kernel": "gemm_kernel (int8 MFMA 32x32x16 + fp32 scale epilogue)",
+        roof = {"bound": "mfma", "kernel": GEMM_KERNEL,
                 "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": None}
+                "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": measured_traffic("gemm", wname),
+                "attainable": {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
+                               "why": "one fp32 VALU FMA per output and 16-block"}}
     else:
         value = quant_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"
@@ -271,8 +321,10 @@ def main():
         us = tl.mean_us(label)
         per_launch = kern[label][1] * (QUANT_BYTES_PER_ELEM if kern[label][0] == "quant" else 2)
         ach = per_launch / (us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "kernel": "quant_rows_kernel" if kern[label][0] == "quant" else "copy", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None}
+        kname = "quant_rows_kernel" if kern[label][0] == "quant" else "copy"
+        roof = {"bound": "hbm", "kernel": kname, "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic("quant", wname) if kname != "copy" else None}
     if quant_labels and gemm_labels:
         qus = sum(tl.mean_us(k) for k in quant_labels)
         breakdown["quant_all"] = {"us": round(qus, 2), "GB/s": round(quant_bytes / (qus * 1e-6) / 1e9, 1)}
@@ -288,7 +340,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i8" if gemm_labels else "f64+f32",
+        "dtype": "f32" if gemm_labels else "f64+f32",
         "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
         "config": {"workload": wname, "recipe": "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY",
                    "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",

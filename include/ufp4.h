@@ -19,13 +19,21 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls are asynchronous on it.
  *  - bf16 tensors are row-major with a leading dimension `ld` in elements (ld >= cols, ld % 8 == 0,
  *    base 16-byte aligned).
- *  - A quantized operand Q is [rows, red] with the reduction axis `red` contiguous, red % 16 == 0:
- *      codes : uint8 [rows, red/2], row stride `code_ld` bytes; element 2j of a 16-block in the low
- *              nibble of byte j. Each nibble is sign-magnitude: sign in bit 3, magnitude code in bits
- *              0-2, zero always +0. Uniform grid: magnitude |k| of the code k in -7..7. E2M1: index of the
- *              magnitude in 0, .5, 1, 1.5, 2, 3, 4, 6 (the OCP FP4 bit pattern).
- *      scales: fp32 [rows, red/16], row stride `scale_ld` floats; block b of row r dequantizes as
- *              level(code) * scales[r, b]. Uniform grid: s = RN(amax/7); E2M1: s = RN(amax/6).
+ *  - A quantized operand Q is [rows, red] (red % 16 == 0, nkb = red/16 blocks of 16 along the reduction
+ *    axis), stored in panels: rows 128p .. 128p+127 form panel p, and within a panel the data of block b
+ *    of all 128 rows is contiguous -- the order in which the GEMMs stage K-blocks.
+ *      codes : panel p at codes_dev + p * code_panel_ld bytes; block b of row 128p + i at
+ *              + b * 1024 + i * 8 (8 bytes). Element 2j of the block is the low nibble of byte j. Each
+ *              nibble is sign-magnitude: sign in bit 3, magnitude code in bits 0-2, zero always +0.
+ *              Uniform grid: magnitude |k| of the code k in -7..7. E2M1: index of the magnitude in
+ *              0, .5, 1, 1.5, 2, 3, 4, 6 (the OCP FP4 bit pattern).
+ *      scales: fp32; panel p at scales_dev + p * scale_panel_ld floats; block b of row 128p + i at
+ *              + b * 128 + i. Block b of row r dequantizes as level(code) * scale. Uniform grid:
+ *              s = RN(amax/7); E2M1: s = RN(amax/6).
+ *      code_panel_ld >= 1024 * nkb and a multiple of 16, scale_panel_ld >= 128 * nkb and a multiple of 4;
+ *      both base pointers 16-byte aligned; buffers hold ceil(rows / 128) whole panels. The quantizers
+ *      write rows past `rows` in the last panel as zero codes and zero scales. Panel strides above 2^29
+ *      bytes (codes) or 2^27 floats (scales) return UFP4_ERR_UNSUPPORTED.
  *  - Quantizer arithmetic, per 16-block x (bf16):
  *      y_i  = RN_fp32( 1/4 * sum_j H16[i,j] * eps_j * x_j )  with the exact sum (rht != 0), else y = x;
  *             H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
@@ -82,18 +90,18 @@ const char *ufp4_version(void);
  *              1: operand A = X^T, reduction along rows (rows % 16 == 0); Q is [cols, rows].
  *   rht        nonzero: apply the block-16 RHT with sign_mask (bits 0..15) before quantizing.
  *   rounding   UFP4_ROUND_RTNE or UFP4_ROUND_SR (seed, stream select the Philox draws; ignored for RTNE).
- *   codes_dev  uint8 [Q rows, Q red / 2], row stride code_ld bytes (code_ld >= red/2, code_ld % 8 == 0).
- *   scales_dev fp32 [Q rows, Q red / 16], row stride scale_ld floats (scale_ld >= red/16).
+ *   codes_dev, code_panel_ld, scales_dev, scale_panel_ld: Q in the panel layout above.
+ * Rowwise operands (transpose = 0) of more than 2097120 rows return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_rht_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
-                      int64_t code_ld, float *scales_dev, int64_t scale_ld, void *stream);
+                      int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld, void *stream);
 
 /* ufp4_e2m1_quantize -- the same operation on the E2M1 grid (g = 6, levels 0, .5, 1, 1.5, 2, 3, 4, 6),
  * the comparison baseline of Table 1. Arguments as ufp4_rht_quantize. */
 int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                        uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
-                       int64_t code_ld, float *scales_dev, int64_t scale_ld, void *stream);
+                       int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld, void *stream);
 
 /*
  * ufp4_quantize_grouped_t -- transposed quantization of an expert-grouped tensor (MoE), either grid.
@@ -111,8 +119,8 @@ int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld
 int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld,
                             const int64_t *group_offsets_dev, const int64_t *padded_offsets_dev,
                             int32_t num_groups, int64_t red_total, int rht, uint32_t sign_mask, int rounding,
-                            uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_ld,
-                            float *scales_dev, int64_t scale_ld, void *stream);
+                            uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_panel_ld,
+                            float *scales_dev, int64_t scale_panel_ld, void *stream);
 
 /*
  * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that
@@ -122,24 +130,24 @@ int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t
  *   ufp4_gemm_bwd_dx: dX [M, K] = Q(dY H')  [M, N] . Q(W^T H') [K, N]^T
  *   ufp4_gemm_bwd_dw: dW [N, K] = Q(dY^T H')[N, M] . Q(X^T H') [K, M]^T
  *
- * Arguments: (a_codes, a_scales) is the left operand, (b_codes, b_scales) the right one, with row
- * strides (code_ld bytes, scale_ld floats) each; `format` is the grid both operands were quantized to
+ * Arguments: (a_codes, a_scales) is the left operand, (b_codes, b_scales) the right one, each in the panel
+ * layout with its panel strides (code_panel_ld bytes, scale_panel_ld floats); `format` is the grid both
+ * operands were quantized to
  * (UFP4_FMT_UNIFORM or UFP4_FMT_E2M1); out_dtype UFP4_OUT_F32 or UFP4_OUT_BF16; out_dev row-major with
  * leading dimension ldc (elements). Both operands must come from quantizations with the same rht
- * setting and sign mask (the library cannot check this). Code row strides above 2^24 bytes or scale row
- * strides above 2^22 floats return UFP4_ERR_UNSUPPORTED.
+ * setting and sign mask (the library cannot check this).
  */
-int ufp4_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_ld, const float *x_scales_dev, int64_t x_scale_ld,
-                    const void *w_codes_dev, int64_t w_code_ld, const float *w_scales_dev, int64_t w_scale_ld,
+int ufp4_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_panel_ld, const float *x_scales_dev, int64_t x_scale_panel_ld,
+                    const void *w_codes_dev, int64_t w_code_panel_ld, const float *w_scales_dev, int64_t w_scale_panel_ld,
                     int64_t M, int64_t N, int64_t K, int format, void *y_dev, int64_t ldc, int out_dtype,
                     void *stream);
-int ufp4_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_ld, const float *dy_scales_dev,
-                     int64_t dy_scale_ld, const void *wt_codes_dev, int64_t wt_code_ld,
-                     const float *wt_scales_dev, int64_t wt_scale_ld, int64_t M, int64_t N, int64_t K,
+int ufp4_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_panel_ld, const float *dy_scales_dev,
+                     int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
+                     const float *wt_scales_dev, int64_t wt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
                      int format, void *dx_dev, int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_ld, const float *dyt_scales_dev,
-                     int64_t dyt_scale_ld, const void *xt_codes_dev, int64_t xt_code_ld,
-                     const float *xt_scales_dev, int64_t xt_scale_ld, int64_t M, int64_t N, int64_t K,
+int ufp4_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const float *dyt_scales_dev,
+                     int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
+                     const float *xt_scales_dev, int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
                      int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
 
 /*
@@ -154,19 +162,19 @@ int ufp4_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_ld, const float
  * the reduction length of Qdyt and Qxt. Offsets are read on the device: rows past M_total and reduction
  * positions past red_total are ignored, groups with no tokens give dW_g = 0.
  */
-int ufp4_gemm_fwd_y_grouped(const void *x_codes_dev, int64_t x_code_ld, const float *x_scales_dev,
-                            int64_t x_scale_ld, const void *w_codes_dev, int64_t w_code_ld,
-                            const float *w_scales_dev, int64_t w_scale_ld, const int64_t *group_offsets_dev,
+int ufp4_gemm_fwd_y_grouped(const void *x_codes_dev, int64_t x_code_panel_ld, const float *x_scales_dev,
+                            int64_t x_scale_panel_ld, const void *w_codes_dev, int64_t w_code_panel_ld,
+                            const float *w_scales_dev, int64_t w_scale_panel_ld, const int64_t *group_offsets_dev,
                             int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format, void *y_dev,
                             int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dx_grouped(const void *dy_codes_dev, int64_t dy_code_ld, const float *dy_scales_dev,
-                             int64_t dy_scale_ld, const void *wt_codes_dev, int64_t wt_code_ld,
-                             const float *wt_scales_dev, int64_t wt_scale_ld, const int64_t *group_offsets_dev,
+int ufp4_gemm_bwd_dx_grouped(const void *dy_codes_dev, int64_t dy_code_panel_ld, const float *dy_scales_dev,
+                             int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
+                             const float *wt_scales_dev, int64_t wt_scale_panel_ld, const int64_t *group_offsets_dev,
                              int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format,
                              void *dx_dev, int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dw_grouped(const void *dyt_codes_dev, int64_t dyt_code_ld, const float *dyt_scales_dev,
-                             int64_t dyt_scale_ld, const void *xt_codes_dev, int64_t xt_code_ld,
-                             const float *xt_scales_dev, int64_t xt_scale_ld,
+int ufp4_gemm_bwd_dw_grouped(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const float *dyt_scales_dev,
+                             int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
+                             const float *xt_scales_dev, int64_t xt_scale_panel_ld,
                              const int64_t *padded_offsets_dev, int32_t num_groups, int64_t red_total, int64_t N,
                              int64_t K, int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
 

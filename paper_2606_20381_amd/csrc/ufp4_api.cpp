@@ -21,10 +21,23 @@ void fill_sign_xor(uint32_t mask, uint32_t (&sx)[8]) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? UFP4_OK : UFP4_ERR_HIP; }
 
+constexpr int64_t kMaxCodePanelLd = int64_t(1) << 29;   // bytes
+constexpr int64_t kMaxScalePanelLd = int64_t(1) << 27;  // floats
+
+// Panel-layout strides of a quantized operand with reduction length `red`.
+int check_panels(const void* codes, int64_t code_pld, const float* scales, int64_t scale_pld, int64_t red) {
+    const int64_t nkb = red / 16;
+    if (code_pld < nkb * kPanelBlockBytes || scale_pld < nkb * kPanelBlockScales) return UFP4_ERR_SHAPE;
+    if (code_pld % 16 != 0 || scale_pld % 4 != 0) return UFP4_ERR_ALIGN;
+    if (!aligned(codes, 16) || !aligned(scales, 16)) return UFP4_ERR_ALIGN;
+    if (code_pld > kMaxCodePanelLd || scale_pld > kMaxScalePanelLd) return UFP4_ERR_UNSUPPORTED;
+    return UFP4_OK;
+}
+
 // Checks shared by the plain and grouped quantizers. `red` is the operand's reduction length, `qrows` its
 // row count.
 int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, int64_t ld, int rht, uint32_t sign_mask,
-                       int rounding, const void* codes, int64_t code_ld, const float* scales, int64_t scale_ld,
+                       int rounding, const void* codes, int64_t code_pld, const float* scales, int64_t scale_pld,
                        int64_t red, int64_t qrows) {
     if (format != UFP4_FMT_UNIFORM && format != UFP4_FMT_E2M1) return UFP4_ERR_INVALID_ARG;
     if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
@@ -34,23 +47,24 @@ int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, in
     if (!x || !codes || !scales) return UFP4_ERR_INVALID_ARG;
     if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
     if (red % 16 != 0) return UFP4_ERR_SHAPE;
-    if (code_ld < red / 2 || scale_ld < red / 16) return UFP4_ERR_SHAPE;
-    if (code_ld % 8 != 0) return UFP4_ERR_ALIGN;
-    if (!aligned(x, 16) || !aligned(codes, 8) || !aligned(scales, 4)) return UFP4_ERR_ALIGN;
-    if (qrows >= (int64_t(1) << 32) || red / 16 >= (int64_t(1) << 32)) return UFP4_ERR_UNSUPPORTED;
+    if (!aligned(x, 16)) return UFP4_ERR_ALIGN;
+    const int st = check_panels(codes, code_pld, scales, scale_pld, red);
+    if (st != UFP4_OK) return st;
+    if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     return UFP4_OK;
 }
 
 int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
-                  uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes, int64_t code_ld,
-                  float* scales, int64_t scale_ld, void* stream) {
+                  uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes, int64_t code_pld,
+                  float* scales, int64_t scale_pld, void* stream) {
     if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
     const int64_t red = transpose ? rows : cols;
     const int64_t qrows = transpose ? cols : rows;
-    const int st = check_quant_common(format, x, rows, cols, ld, rht, sign_mask, rounding, codes, code_ld, scales,
-                                      scale_ld, red, qrows);
+    const int st = check_quant_common(format, x, rows, cols, ld, rht, sign_mask, rounding, codes, code_pld, scales,
+                                      scale_pld, red, qrows);
     if (st != UFP4_OK) return st;
-    if (!transpose && qrows * (red / 16) >= (int64_t(1) << 32)) return UFP4_ERR_UNSUPPORTED;
+    // rowwise: one workgroup per 32 padded rows along the grid's y dimension
+    if (!transpose && padded_rows(qrows) / 32 > 65535) return UFP4_ERR_UNSUPPORTED;
     if (rows == 0 || cols == 0) return UFP4_OK;
     QuantJob j{};
     j.format = format;
@@ -70,49 +84,45 @@ int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t
     j.qa.key1 = (uint32_t)(seed >> 32);
     j.qa.stream = stream_id;
     j.codes = codes;
-    j.code_ld = code_ld;
+    j.code_pld = code_pld;
     j.scales = scales;
-    j.scale_ld = scale_ld;
+    j.scale_pld = scale_pld;
     return status_of(launch_quantize(j, static_cast<hipStream_t>(stream)));
 }
 
 // Shared checks of the GEMM entry points. A is [rows_a, red], B is [rows_b, red] (reduction contiguous).
-int check_gemm(const void* a, int64_t lda, const float* as, int64_t ldas, const void* b, int64_t ldb, const float* bs,
-               int64_t ldbs, int64_t rows_a, int64_t rows_b, int64_t red_a, int64_t red_b, int format, const void* c,
-               int64_t ldc, int64_t c_cols, int out_dtype) {
+int check_gemm(const void* a, int64_t a_pld, const float* as, int64_t as_pld, const void* b, int64_t b_pld,
+               const float* bs, int64_t bs_pld, int64_t rows_a, int64_t rows_b, int64_t red_a, int64_t red_b, int format,
+               const void* c, int64_t ldc, int64_t c_cols, int out_dtype) {
     if (format != UFP4_FMT_UNIFORM && format != UFP4_FMT_E2M1) return UFP4_ERR_INVALID_ARG;
     if (out_dtype != UFP4_OUT_F32 && out_dtype != UFP4_OUT_BF16) return UFP4_ERR_INVALID_ARG;
     if (rows_a < 0 || rows_b < 0 || red_a < 0 || red_b < 0) return UFP4_ERR_INVALID_ARG;
     if (!a || !as || !b || !bs || !c) return UFP4_ERR_INVALID_ARG;
     if (red_a % 16 != 0 || red_b % 16 != 0) return UFP4_ERR_SHAPE;
-    if (lda < red_a / 2 || ldb < red_b / 2 || ldas < red_a / 16 || ldbs < red_b / 16) return UFP4_ERR_SHAPE;
     if (ldc < c_cols) return UFP4_ERR_SHAPE;
-    if (lda % 8 != 0 || ldb % 8 != 0) return UFP4_ERR_ALIGN;
-    if (!aligned(a, 8) || !aligned(b, 8) || !aligned(as, 4) || !aligned(bs, 4)) return UFP4_ERR_ALIGN;
+    int st = check_panels(a, a_pld, as, as_pld, red_a);
+    if (st == UFP4_OK) st = check_panels(b, b_pld, bs, bs_pld, red_b);
+    if (st != UFP4_OK) return st;
     if (!aligned(c, out_dtype == UFP4_OUT_F32 ? 4 : 2)) return UFP4_ERR_ALIGN;
     if (rows_a >= (int64_t(1) << 31) || rows_b >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
-    // a 128-row tile of either operand must lie within 2^31 bytes (32-bit buffer offsets)
-    if (lda > (int64_t(1) << 24) || ldb > (int64_t(1) << 24) || ldas > (int64_t(1) << 22) ||
-        ldbs > (int64_t(1) << 22))
-        return UFP4_ERR_UNSUPPORTED;
     return UFP4_OK;
 }
 
-GemmJob make_job(int mode, const void* a, int64_t lda, const float* as, int64_t ldas, const void* b, int64_t ldb,
-                 const float* bs, int64_t ldbs, int64_t M, int64_t N, int64_t nkb, int format, void* c, int64_t ldc,
-                 int out_dtype) {
+GemmJob make_job(int mode, const void* a, int64_t a_pld, const float* as, int64_t as_pld, const void* b,
+                 int64_t b_pld, const float* bs, int64_t bs_pld, int64_t M, int64_t N, int64_t nkb, int format, void* c,
+                 int64_t ldc, int out_dtype) {
     GemmJob j{};
     j.format = format;
     j.out_dtype = out_dtype;
     j.mode = mode;
     j.a = static_cast<const uint8_t*>(a);
-    j.lda = lda;
+    j.a_pld = a_pld;
     j.as = as;
-    j.ldas = ldas;
+    j.as_pld = as_pld;
     j.b = static_cast<const uint8_t*>(b);
-    j.ldb = ldb;
+    j.b_pld = b_pld;
     j.bs = bs;
-    j.ldbs = ldbs;
+    j.bs_pld = bs_pld;
     j.M = M;
     j.N = N;
     j.nkb = nkb;
@@ -123,15 +133,15 @@ GemmJob make_job(int mode, const void* a, int64_t lda, const float* as, int64_t 
     return j;
 }
 
-int gemm_dense(const void* a, int64_t lda, const float* as, int64_t ldas, const void* b, int64_t ldb, const float* bs,
-               int64_t ldbs, int64_t rows_a, int64_t rows_b, int64_t red, int format, void* c, int64_t ldc,
-               int out_dtype, void* stream) {
-    const int st =
-        check_gemm(a, lda, as, ldas, b, ldb, bs, ldbs, rows_a, rows_b, red, red, format, c, ldc, rows_b, out_dtype);
+int gemm_dense(const void* a, int64_t a_pld, const float* as, int64_t as_pld, const void* b, int64_t b_pld,
+               const float* bs, int64_t bs_pld, int64_t rows_a, int64_t rows_b, int64_t red, int format, void* c,
+               int64_t ldc, int out_dtype, void* stream) {
+    const int st = check_gemm(a, a_pld, as, as_pld, b, b_pld, bs, bs_pld, rows_a, rows_b, red, red, format, c, ldc,
+                              rows_b, out_dtype);
     if (st != UFP4_OK) return st;
     if (rows_a == 0 || rows_b == 0) return UFP4_OK;
-    const GemmJob j = make_job(kGemmDense, a, lda, as, ldas, b, ldb, bs, ldbs, rows_a, rows_b, red / 16, format, c, ldc,
-                               out_dtype);
+    const GemmJob j = make_job(kGemmDense, a, a_pld, as, as_pld, b, b_pld, bs, bs_pld, rows_a, rows_b, red / 16, format,
+                               c, ldc, out_dtype);
     return status_of(launch_gemm(j, static_cast<hipStream_t>(stream)));
 }
 
@@ -155,29 +165,29 @@ const char* ufp4_version(void) { return "0.1.0"; }
 
 int ufp4_rht_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes_dev,
-                      int64_t code_ld, float* scales_dev, int64_t scale_ld, void* stream) {
+                      int64_t code_panel_ld, float* scales_dev, int64_t scale_panel_ld, void* stream) {
     return quantize_impl(UFP4_FMT_UNIFORM, x_dev, rows, cols, ld, transpose, rht, sign_mask, rounding, seed, stream_id,
-                         codes_dev, code_ld, scales_dev, scale_ld, stream);
+                         codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream);
 }
 
 int ufp4_e2m1_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                        uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes_dev,
-                       int64_t code_ld, float* scales_dev, int64_t scale_ld, void* stream) {
+                       int64_t code_panel_ld, float* scales_dev, int64_t scale_panel_ld, void* stream) {
     return quantize_impl(UFP4_FMT_E2M1, x_dev, rows, cols, ld, transpose, rht, sign_mask, rounding, seed, stream_id,
-                         codes_dev, code_ld, scales_dev, scale_ld, stream);
+                         codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream);
 }
 
 int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t cols, int64_t ld,
                             const int64_t* group_offsets_dev, const int64_t* padded_offsets_dev, int32_t num_groups,
                             int64_t red_total, int rht, uint32_t sign_mask, int rounding, uint64_t seed,
-                            uint32_t stream_id, void* codes_dev, int64_t code_ld, float* scales_dev, int64_t scale_ld,
-                            void* stream) {
+                            uint32_t stream_id, void* codes_dev, int64_t code_panel_ld, float* scales_dev,
+                            int64_t scale_panel_ld, void* stream) {
     if (!group_offsets_dev || !padded_offsets_dev) return UFP4_ERR_INVALID_ARG;
     if (num_groups < 1 || num_groups > max_groups_quantize()) return num_groups < 1 ? UFP4_ERR_INVALID_ARG
                                                                                     : UFP4_ERR_UNSUPPORTED;
     if (red_total < rows) return UFP4_ERR_SHAPE;
-    const int st = check_quant_common(format, x_dev, rows, cols, ld, rht, sign_mask, rounding, codes_dev, code_ld,
-                                      scales_dev, scale_ld, red_total, cols);
+    const int st = check_quant_common(format, x_dev, rows, cols, ld, rht, sign_mask, rounding, codes_dev, code_panel_ld,
+                                      scales_dev, scale_panel_ld, red_total, cols);
     if (st != UFP4_OK) return st;
     if (red_total == 0 || cols == 0) return UFP4_OK;
     QuantJob j{};
@@ -198,49 +208,49 @@ int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t
     j.qa.key1 = (uint32_t)(seed >> 32);
     j.qa.stream = stream_id;
     j.codes = codes_dev;
-    j.code_ld = code_ld;
+    j.code_pld = code_panel_ld;
     j.scales = scales_dev;
-    j.scale_ld = scale_ld;
+    j.scale_pld = scale_panel_ld;
     return status_of(launch_quantize(j, static_cast<hipStream_t>(stream)));
 }
 
-int ufp4_gemm_fwd_y(const void* x_codes_dev, int64_t x_code_ld, const float* x_scales_dev, int64_t x_scale_ld,
-                    const void* w_codes_dev, int64_t w_code_ld, const float* w_scales_dev, int64_t w_scale_ld,
+int ufp4_gemm_fwd_y(const void* x_codes_dev, int64_t x_code_panel_ld, const float* x_scales_dev, int64_t x_scale_panel_ld,
+                    const void* w_codes_dev, int64_t w_code_panel_ld, const float* w_scales_dev, int64_t w_scale_panel_ld,
                     int64_t M, int64_t N, int64_t K, int format, void* y_dev, int64_t ldc, int out_dtype,
                     void* stream) {
-    return gemm_dense(x_codes_dev, x_code_ld, x_scales_dev, x_scale_ld, w_codes_dev, w_code_ld, w_scales_dev,
-                      w_scale_ld, M, N, K, format, y_dev, ldc, out_dtype, stream);
+    return gemm_dense(x_codes_dev, x_code_panel_ld, x_scales_dev, x_scale_panel_ld, w_codes_dev, w_code_panel_ld, w_scales_dev,
+                      w_scale_panel_ld, M, N, K, format, y_dev, ldc, out_dtype, stream);
 }
 
-int ufp4_gemm_bwd_dx(const void* dy_codes_dev, int64_t dy_code_ld, const float* dy_scales_dev, int64_t dy_scale_ld,
-                     const void* wt_codes_dev, int64_t wt_code_ld, const float* wt_scales_dev, int64_t wt_scale_ld,
+int ufp4_gemm_bwd_dx(const void* dy_codes_dev, int64_t dy_code_panel_ld, const float* dy_scales_dev, int64_t dy_scale_panel_ld,
+                     const void* wt_codes_dev, int64_t wt_code_panel_ld, const float* wt_scales_dev, int64_t wt_scale_panel_ld,
                      int64_t M, int64_t N, int64_t K, int format, void* dx_dev, int64_t ldc, int out_dtype,
                      void* stream) {
     // dX [M, K] = dY [M, N] . (W^T [K, N])^T
-    return gemm_dense(dy_codes_dev, dy_code_ld, dy_scales_dev, dy_scale_ld, wt_codes_dev, wt_code_ld, wt_scales_dev,
-                      wt_scale_ld, M, K, N, format, dx_dev, ldc, out_dtype, stream);
+    return gemm_dense(dy_codes_dev, dy_code_panel_ld, dy_scales_dev, dy_scale_panel_ld, wt_codes_dev, wt_code_panel_ld, wt_scales_dev,
+                      wt_scale_panel_ld, M, K, N, format, dx_dev, ldc, out_dtype, stream);
 }
 
-int ufp4_gemm_bwd_dw(const void* dyt_codes_dev, int64_t dyt_code_ld, const float* dyt_scales_dev,
-                     int64_t dyt_scale_ld, const void* xt_codes_dev, int64_t xt_code_ld, const float* xt_scales_dev,
-                     int64_t xt_scale_ld, int64_t M, int64_t N, int64_t K, int format, void* dw_dev, int64_t ldc,
+int ufp4_gemm_bwd_dw(const void* dyt_codes_dev, int64_t dyt_code_panel_ld, const float* dyt_scales_dev,
+                     int64_t dyt_scale_panel_ld, const void* xt_codes_dev, int64_t xt_code_panel_ld, const float* xt_scales_dev,
+                     int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K, int format, void* dw_dev, int64_t ldc,
                      int out_dtype, void* stream) {
     // dW [N, K] = dY^T [N, M] . (X^T [K, M])^T
-    return gemm_dense(dyt_codes_dev, dyt_code_ld, dyt_scales_dev, dyt_scale_ld, xt_codes_dev, xt_code_ld,
-                      xt_scales_dev, xt_scale_ld, N, K, M, format, dw_dev, ldc, out_dtype, stream);
+    return gemm_dense(dyt_codes_dev, dyt_code_panel_ld, dyt_scales_dev, dyt_scale_panel_ld, xt_codes_dev, xt_code_panel_ld,
+                      xt_scales_dev, xt_scale_panel_ld, N, K, M, format, dw_dev, ldc, out_dtype, stream);
 }
 
-int ufp4_gemm_fwd_y_grouped(const void* x_codes_dev, int64_t x_code_ld, const float* x_scales_dev, int64_t x_scale_ld,
-                            const void* w_codes_dev, int64_t w_code_ld, const float* w_scales_dev, int64_t w_scale_ld,
+int ufp4_gemm_fwd_y_grouped(const void* x_codes_dev, int64_t x_code_panel_ld, const float* x_scales_dev, int64_t x_scale_panel_ld,
+                            const void* w_codes_dev, int64_t w_code_panel_ld, const float* w_scales_dev, int64_t w_scale_panel_ld,
                             const int64_t* group_offsets_dev, int32_t num_groups, int64_t M_total, int64_t N, int64_t K,
                             int format, void* y_dev, int64_t ldc, int out_dtype, void* stream) {
     if (!group_offsets_dev || num_groups < 1) return UFP4_ERR_INVALID_ARG;
-    const int st = check_gemm(x_codes_dev, x_code_ld, x_scales_dev, x_scale_ld, w_codes_dev, w_code_ld, w_scales_dev,
-                              w_scale_ld, M_total, N * num_groups, K, K, format, y_dev, ldc, N, out_dtype);
+    const int st = check_gemm(x_codes_dev, x_code_panel_ld, x_scales_dev, x_scale_panel_ld, w_codes_dev, w_code_panel_ld, w_scales_dev,
+                              w_scale_panel_ld, M_total, N * num_groups, K, K, format, y_dev, ldc, N, out_dtype);
     if (st != UFP4_OK) return st;
     if (M_total == 0 || N == 0) return UFP4_OK;
-    GemmJob j = make_job(kGemmRaggedM, x_codes_dev, x_code_ld, x_scales_dev, x_scale_ld, w_codes_dev, w_code_ld,
-                         w_scales_dev, w_scale_ld, M_total, N, K / 16, format, y_dev, ldc, out_dtype);
+    GemmJob j = make_job(kGemmRaggedM, x_codes_dev, x_code_panel_ld, x_scales_dev, x_scale_panel_ld, w_codes_dev, w_code_panel_ld,
+                         w_scales_dev, w_scale_panel_ld, M_total, N, K / 16, format, y_dev, ldc, out_dtype);
     j.offsets = group_offsets_dev;
     j.G = num_groups;
     j.b_group_rows = N;
@@ -248,20 +258,20 @@ int ufp4_gemm_fwd_y_grouped(const void* x_codes_dev, int64_t x_code_ld, const fl
     return status_of(launch_gemm(j, static_cast<hipStream_t>(stream)));
 }
 
-int ufp4_gemm_bwd_dx_grouped(const void* dy_codes_dev, int64_t dy_code_ld, const float* dy_scales_dev,
-                             int64_t dy_scale_ld, const void* wt_codes_dev, int64_t wt_code_ld,
-                             const float* wt_scales_dev, int64_t wt_scale_ld, const int64_t* group_offsets_dev,
+int ufp4_gemm_bwd_dx_grouped(const void* dy_codes_dev, int64_t dy_code_panel_ld, const float* dy_scales_dev,
+                             int64_t dy_scale_panel_ld, const void* wt_codes_dev, int64_t wt_code_panel_ld,
+                             const float* wt_scales_dev, int64_t wt_scale_panel_ld, const int64_t* group_offsets_dev,
                              int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format, void* dx_dev,
                              int64_t ldc, int out_dtype, void* stream) {
     if (!group_offsets_dev || num_groups < 1) return UFP4_ERR_INVALID_ARG;
     // A = dY [M_total, N]; B = W^T [K, G*N], group g uses reduction columns [g*N, (g+1)*N)
-    const int st = check_gemm(dy_codes_dev, dy_code_ld, dy_scales_dev, dy_scale_ld, wt_codes_dev, wt_code_ld,
-                              wt_scales_dev, wt_scale_ld, M_total, K, N, N * num_groups, format, dx_dev, ldc, K,
+    const int st = check_gemm(dy_codes_dev, dy_code_panel_ld, dy_scales_dev, dy_scale_panel_ld, wt_codes_dev, wt_code_panel_ld,
+                              wt_scales_dev, wt_scale_panel_ld, M_total, K, N, N * num_groups, format, dx_dev, ldc, K,
                               out_dtype);
     if (st != UFP4_OK) return st;
     if (M_total == 0 || K == 0) return UFP4_OK;
-    GemmJob j = make_job(kGemmRaggedM, dy_codes_dev, dy_code_ld, dy_scales_dev, dy_scale_ld, wt_codes_dev, wt_code_ld,
-                         wt_scales_dev, wt_scale_ld, M_total, K, N / 16, format, dx_dev, ldc, out_dtype);
+    GemmJob j = make_job(kGemmRaggedM, dy_codes_dev, dy_code_panel_ld, dy_scales_dev, dy_scale_panel_ld, wt_codes_dev, wt_code_panel_ld,
+                         wt_scales_dev, wt_scale_panel_ld, M_total, K, N / 16, format, dx_dev, ldc, out_dtype);
     j.offsets = group_offsets_dev;
     j.G = num_groups;
     j.b_group_rows = 0;
@@ -269,21 +279,21 @@ int ufp4_gemm_bwd_dx_grouped(const void* dy_codes_dev, int64_t dy_code_ld, const
     return status_of(launch_gemm(j, static_cast<hipStream_t>(stream)));
 }
 
-int ufp4_gemm_bwd_dw_grouped(const void* dyt_codes_dev, int64_t dyt_code_ld, const float* dyt_scales_dev,
-                             int64_t dyt_scale_ld, const void* xt_codes_dev, int64_t xt_code_ld,
-                             const float* xt_scales_dev, int64_t xt_scale_ld, const int64_t* padded_offsets_dev,
+int ufp4_gemm_bwd_dw_grouped(const void* dyt_codes_dev, int64_t dyt_code_panel_ld, const float* dyt_scales_dev,
+                             int64_t dyt_scale_panel_ld, const void* xt_codes_dev, int64_t xt_code_panel_ld,
+                             const float* xt_scales_dev, int64_t xt_scale_panel_ld, const int64_t* padded_offsets_dev,
                              int32_t num_groups, int64_t red_total, int64_t N, int64_t K, int format, void* dw_dev,
                              int64_t ldc, int out_dtype, void* stream) {
     if (!padded_offsets_dev || num_groups < 1) return UFP4_ERR_INVALID_ARG;
     if (num_groups > 65535) return UFP4_ERR_UNSUPPORTED;
     // A = dY^T [N, red_total], B = X^T [K, red_total]; group g reduces over [pad_g, pad_{g+1}) of that axis
-    const int st = check_gemm(dyt_codes_dev, dyt_code_ld, dyt_scales_dev, dyt_scale_ld, xt_codes_dev, xt_code_ld,
-                              xt_scales_dev, xt_scale_ld, N, K, red_total, red_total, format, dw_dev, ldc, K,
+    const int st = check_gemm(dyt_codes_dev, dyt_code_panel_ld, dyt_scales_dev, dyt_scale_panel_ld, xt_codes_dev, xt_code_panel_ld,
+                              xt_scales_dev, xt_scale_panel_ld, N, K, red_total, red_total, format, dw_dev, ldc, K,
                               out_dtype);
     if (st != UFP4_OK) return st;
     if (N == 0 || K == 0) return UFP4_OK;
-    GemmJob j = make_job(kGemmRaggedK, dyt_codes_dev, dyt_code_ld, dyt_scales_dev, dyt_scale_ld, xt_codes_dev,
-                         xt_code_ld, xt_scales_dev, xt_scale_ld, N, K, 0, format, dw_dev, ldc, out_dtype);
+    GemmJob j = make_job(kGemmRaggedK, dyt_codes_dev, dyt_code_panel_ld, dyt_scales_dev, dyt_scale_panel_ld, xt_codes_dev,
+                         xt_code_panel_ld, xt_scales_dev, xt_scale_panel_ld, N, K, 0, format, dw_dev, ldc, out_dtype);
     j.offsets = padded_offsets_dev;
     j.G = num_groups;
     j.red_total = red_total;

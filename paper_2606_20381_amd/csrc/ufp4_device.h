@@ -36,26 +36,6 @@ __device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint3
 }
 
 // ------------------------------------------------------------------------------------------------
-// Unsigned 32-bit division by a run-time constant d >= 1 (Granlund-Montgomery round-up method):
-// q = (umulhi(n, m) + n) >> s with s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1.
-// ------------------------------------------------------------------------------------------------
-struct FastDiv {
-    uint32_t d, m, s;
-};
-
-inline FastDiv make_fastdiv(uint32_t d) {
-    uint32_t s = 0;
-    while ((1ull << s) < d) ++s;
-    const uint64_t m = ((1ull << 32) * ((1ull << s) - d)) / d + 1;
-    return {d, (uint32_t)m, s};
-}
-
-__device__ __forceinline__ uint32_t fastdiv(uint32_t n, const FastDiv& f) {
-    const uint64_t t = (uint64_t)__umulhi(n, f.m) + n;
-    return (uint32_t)(t >> f.s);
-}
-
-// ------------------------------------------------------------------------------------------------
 // bf16 <-> fp32
 // ------------------------------------------------------------------------------------------------
 __device__ __forceinline__ float bf16_lo(uint32_t pair) { return __uint_as_float(pair << 16); }

@@ -29,6 +29,17 @@ namespace ufp4 {
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128;
+static_assert(BM == kPanelRows && BN == kPanelRows, "a dense tile is one operand panel");
+
+// Offsets of (row, block) in the panel layout, the row counted from a tile's first row (row0 within its panel).
+__device__ __forceinline__ int64_t code_off(int row0, int row, int64_t kb, int64_t pld) {
+    const int r = row0 + row;
+    return (int64_t)(r / kPanelRows) * pld + kb * kPanelBlockBytes + (int64_t)(r % kPanelRows) * 8;
+}
+__device__ __forceinline__ int64_t scale_off(int row0, int row, int64_t kb, int64_t pld) {
+    const int r = row0 + row;
+    return (int64_t)(r / kPanelRows) * pld + kb * kPanelBlockScales + (r % kPanelRows);
+}
 constexpr int SKB = 8;         // K-blocks per LDS stage
 constexpr int CPL = BM + 2;    // dwords per code plane (row stride offset of 2 banks between planes)
 constexpr int SPL = BM + 4;    // floats per scale plane
@@ -90,11 +101,16 @@ struct GemmArgs {
 };
 
 // The problem one workgroup works on, with pointers already advanced to its tile / group.
+// A workgroup's operand tiles. Operands are in the panel layout (panels of 128 rows, block b of a panel at
+// b * 1024 bytes / b * 128 floats); a/as (b/bs) point at the panel holding the tile's first row, already
+// advanced to the tile's first K-block, and a_row0 (b_row0) is that row's index within its panel (nonzero
+// only for ragged-M groups, whose tiles start anywhere).
 struct Tile {
     const uint8_t* a;
     const float* as;
     const uint8_t* b;
     const float* bs;
+    int a_row0, b_row0;
     int mrows, nrows;  // valid rows of the tile in A and B
     int64_t nkb;       // reduction blocks
     int64_t c_off;     // element offset of the tile's (0, 0) in C
@@ -178,12 +194,14 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos,
         const int64_t end = j.offsets[g + 1] < j.M ? j.offsets[g + 1] : j.M;  // offsets past M_total: ignored
         const int64_t rows_g = end - r0;
         if (rows_g <= 0) return false;
-        tl.a = j.a + r0 * j.lda;
-        tl.as = j.as + r0 * j.ldas;
+        tl.a = j.a + (r0 / kPanelRows) * j.a_pld;
+        tl.as = j.as + (r0 / kPanelRows) * j.as_pld;
+        tl.a_row0 = (int)(r0 % kPanelRows);
         const int64_t brow = g * j.b_group_rows + tn * BN;
         const int64_t bkb = g * j.b_group_kb;
-        tl.b = j.b + brow * j.ldb + bkb * 8;
-        tl.bs = j.bs + brow * j.ldbs + bkb;
+        tl.b = j.b + (brow / kPanelRows) * j.b_pld + bkb * kPanelBlockBytes;
+        tl.bs = j.bs + (brow / kPanelRows) * j.bs_pld + bkb * kPanelBlockScales;
+        tl.b_row0 = (int)(brow % kPanelRows);
         tl.mrows = (int)(rows_g < BM ? rows_g : BM);
         const int64_t nr = j.N - tn * BN;
         tl.nrows = (int)(nr < BN ? nr : BN);
@@ -202,10 +220,12 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos,
             tl.nkb = p1 > p0 ? (p1 - p0) / 16 : 0;
             c_base = (int64_t)g * j.M * j.ldc;
         }
-        tl.a = j.a + tm * BM * j.lda + kb0 * 8;
-        tl.as = j.as + tm * BM * j.ldas + kb0;
-        tl.b = j.b + tn * BN * j.ldb + kb0 * 8;
-        tl.bs = j.bs + tn * BN * j.ldbs + kb0;
+        // BM = BN = 128: dense tiles are whole panels
+        tl.a = j.a + tm * j.a_pld + kb0 * kPanelBlockBytes;
+        tl.as = j.as + tm * j.as_pld + kb0 * kPanelBlockScales;
+        tl.b = j.b + tn * j.b_pld + kb0 * kPanelBlockBytes;
+        tl.bs = j.bs + tn * j.bs_pld + kb0 * kPanelBlockScales;
+        tl.a_row0 = tl.b_row0 = 0;
         const int64_t mr = j.M - tm * BM, nr = j.N - tn * BN;
         tl.mrows = (int)(mr < BM ? mr : BM);
         tl.nrows = (int)(nr < BN ? nr : BN);
@@ -248,10 +268,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
             const int row = e >> 3, kb = e & 7;
             const bool kok = ks + kb < tl.nkb;
             const bool aok = kok && row < tl.mrows, bok = kok && row < tl.nrows;
-            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + row * j.lda + (ks + kb) * 8) : make_uint2(0, 0);
-            rsa[q] = aok ? tl.as[row * j.ldas + ks + kb] : 0.0f;
-            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + row * j.ldb + (ks + kb) * 8) : make_uint2(0, 0);
-            rsb[q] = bok ? tl.bs[row * j.ldbs + ks + kb] : 0.0f;
+            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + code_off(tl.a_row0, row, ks + kb, j.a_pld))
+                        : make_uint2(0, 0);
+            rsa[q] = aok ? tl.as[scale_off(tl.a_row0, row, ks + kb, j.as_pld)] : 0.0f;
+            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + code_off(tl.b_row0, row, ks + kb, j.b_pld))
+                        : make_uint2(0, 0);
+            rsb[q] = bok ? tl.bs[scale_off(tl.b_row0, row, ks + kb, j.bs_pld)] : 0.0f;
         }
     };
     auto store_stage = [&](int buf) {
@@ -464,6 +486,8 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     tl.b = uniform_ptr(tl.b);
     tl.as = uniform_ptr(tl.as);
     tl.bs = uniform_ptr(tl.bs);
+    tl.a_row0 = __builtin_amdgcn_readfirstlane(tl.a_row0);
+    tl.b_row0 = __builtin_amdgcn_readfirstlane(tl.b_row0);
     tl.mrows = __builtin_amdgcn_readfirstlane(tl.mrows);
     tl.nrows = __builtin_amdgcn_readfirstlane(tl.nrows);
     tl.nkb = uniform_i64(tl.nkb);
@@ -482,25 +506,32 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     const int nstages = (nkb + SKB2 - 1) / SKB2;
 
     // Staging: waves 0-3 fetch A, waves 4-7 B; thread (row, pair) takes blocks 2 pair and 2 pair + 1 of its
-    // row in every stage: 2 x 8 bytes of codes and 2 scales.
+    // row in every stage (2 x 8 bytes of codes and 2 scales). A wave covers 64 consecutive rows of one block,
+    // i.e. contiguous runs of the panel layout.
     const bool st_a = wave < 4;
-    const int srow = (tid & 255) >> 1, spair = tid & 1;
+    const int srow = tid & 127, spair = (tid >> 7) & 1;
     const int rows = st_a ? tl.mrows : tl.nrows;
-    const int64_t ldc_b = st_a ? j.lda : j.ldb;   // code row stride, bytes
-    const int64_t lds_f = st_a ? j.ldas : j.ldbs;  // scale row stride, floats
-    const __amdgpu_buffer_rsrc_t rc =
-        make_rsrc(st_a ? (const void*)tl.a : (const void*)tl.b, (uint32_t)((rows - 1) * ldc_b + (int64_t)nkb * 8));
+    const int row0 = st_a ? tl.a_row0 : tl.b_row0;
+    const int64_t cpld = st_a ? j.a_pld : j.b_pld;   // bytes
+    const int64_t spld = st_a ? j.as_pld : j.bs_pld;  // floats
+    // the resources end at the last valid byte of the tile: loads of rows past it, or of blocks past the end
+    // in the last panel, read zeros
+    const int64_t last_panel = (row0 + rows - 1) / kPanelRows;
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(st_a ? (const void*)tl.a : (const void*)tl.b,
+                                                (uint32_t)(last_panel * cpld + (int64_t)nkb * kPanelBlockBytes));
     const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc(st_a ? (const void*)tl.as : (const void*)tl.bs, (uint32_t)(((rows - 1) * lds_f + (int64_t)nkb) * 4));
-    const int voc = (int)(srow * ldc_b) + spair * 16;
-    const int vos = (int)(srow * lds_f + spair * 2) * 4;
+        make_rsrc(st_a ? (const void*)tl.as : (const void*)tl.bs,
+                  (uint32_t)((last_panel * spld + (int64_t)nkb * kPanelBlockScales) * 4));
+    const int voc = (int)code_off(row0, srow, 2 * spair, cpld);
+    const int vos = (int)scale_off(row0, srow, 2 * spair, spld) * 4;
 
     auto load = [&](StageRegs& r, int s) {
-        const int soc = __builtin_amdgcn_readfirstlane(s * SKB2 * 8), sos = __builtin_amdgcn_readfirstlane(s * SKB2 * 4);
+        const int soc = __builtin_amdgcn_readfirstlane(s * SKB2 * (int)kPanelBlockBytes);
+        const int sos = __builtin_amdgcn_readfirstlane(s * SKB2 * (int)kPanelBlockScales * 4);
         r.c0 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, voc, soc, 0));
-        r.c1 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, voc + 8, soc, 0));
+        r.c1 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rc, voc + (int)kPanelBlockBytes, soc, 0));
         r.s0 = __builtin_amdgcn_raw_buffer_load_b32(rs, vos, sos, 0);
-        r.s1 = __builtin_amdgcn_raw_buffer_load_b32(rs, vos + 4, sos, 0);
+        r.s1 = __builtin_amdgcn_raw_buffer_load_b32(rs, vos + (int)kPanelBlockScales * 4, sos, 0);
     };
     auto conv = [](uint32_t d) -> uint2 {
         if constexpr (FMT == kFmtUniform) return uniform_to_e4m3(d);

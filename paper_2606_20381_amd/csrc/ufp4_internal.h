@@ -7,6 +7,13 @@
 namespace ufp4 {
 
 enum { kFmtUniform = 0, kFmtE2M1 = 1 };
+
+// Quantized operands are stored in panels of kPanelRows rows; within a panel, block b of every row sits at
+// b * 1024 bytes (codes, 8 per row) and b * 128 floats (scales, 1 per row).
+constexpr int64_t kPanelRows = 128;
+constexpr int64_t kPanelBlockBytes = kPanelRows * 8;
+constexpr int64_t kPanelBlockScales = kPanelRows;
+__host__ __device__ constexpr int64_t padded_rows(int64_t rows) { return (rows + kPanelRows - 1) / kPanelRows * kPanelRows; }
 enum { kRoundRTNE = 0, kRoundSR = 1 };
 enum { kOutF32 = 0, kOutBF16 = 1 };
 
@@ -29,9 +36,9 @@ struct QuantJob {
     int32_t num_groups;
     QuantArgs qa;
     void* codes;
-    int64_t code_ld;
+    int64_t code_pld;  // bytes between panels
     float* scales;
-    int64_t scale_ld;
+    int64_t scale_pld;  // floats between panels
 };
 
 hipError_t launch_quantize(const QuantJob& job, hipStream_t stream);
@@ -42,14 +49,14 @@ enum GemmMode { kGemmDense = 0, kGemmRaggedM = 1, kGemmRaggedK = 2 };
 
 struct GemmJob {
     int format, out_dtype, mode;
-    const uint8_t* a;  // codes of the left operand, row stride lda bytes
-    int64_t lda;
-    const float* as;  // its scales, row stride ldas floats
-    int64_t ldas;
+    const uint8_t* a;  // codes of the left operand (panel layout), panel stride a_pld bytes
+    int64_t a_pld;
+    const float* as;  // its scales, panel stride as_pld floats
+    int64_t as_pld;
     const uint8_t* b;
-    int64_t ldb;
+    int64_t b_pld;
     const float* bs;
-    int64_t ldbs;
+    int64_t bs_pld;
     int64_t M;    // rows of A: dense and ragged-K per problem; ragged-M the total over groups
     int64_t N;    // rows of B per problem
     int64_t nkb;  // reduction blocks (dense, ragged-M); unused for ragged-K (from the offsets)

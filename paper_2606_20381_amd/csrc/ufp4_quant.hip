@@ -5,12 +5,19 @@
 //   y    = RN32( x S_16 H_16 )            exact 16-term sum in fp64 (Sylvester butterfly), one rounding
 //   s    = RN32(amax / g),  r = RN32(g / amax),  v = RN32(y * r)
 //   code = RTNE(v) or SR(v; Philox draw)  onto the grid, clamped to +-g
+// The RHT's factor 1/4 is a power of two: the kernel keeps y' = 4y = RN32(unscaled sum), so amax' = 4 amax,
+// RN32(g / amax') = RN32(g / amax) / 4 and y' * RN32(g / amax') = y * r exactly, and s = RN32(amax' / g) / 4.
+// These identities hold while y and s are normal fp32 numbers, the supported input domain.
 //
-// Two layouts: rowwise (reduction axis contiguous, one thread per block, 32-byte loads) and transposed
-// (reduction axis strided: a 128x64 tile is staged through LDS, each thread builds two column blocks
-// from LDS, and the packed codes are restaged so that every output row is written in 64-byte runs).
-// The transposed kernel also serves grouped (MoE) tensors whose token axis is cut into groups that are
-// zero-padded to a multiple of 16.
+// Two input layouts: rowwise (reduction axis contiguous, one thread per block, 32-byte loads) and
+// transposed (reduction axis strided: a 128x64 tile is staged through LDS, each thread builds two column
+// blocks from LDS). The transposed kernel also serves grouped (MoE) tensors whose token axis is cut into
+// groups that are zero-padded to a multiple of 16.
+//
+// Output layout (panels): the quantized operand's rows are cut into panels of 128; within a panel, block b
+// of all 128 rows is stored contiguously (codes: 128 x 8 bytes at b * 1024; scales: 128 floats at b * 128).
+// Rows past the operand's last one in the final panel are written as zero codes and zero scales. This is the
+// order in which the GEMM stages K-blocks, so its loads are contiguous runs.
 //
 // This translation unit is compiled with -ffp-contract=off: every fp32/fp64 operation above must round
 // exactly once, as written.
@@ -24,28 +31,37 @@ namespace ufp4 {
 // Per-element rounding onto the grid; returns the 4-bit code in the low bits.
 // ------------------------------------------------------------------------------------------------
 
-// 1.5 * 2^23: adding it to 0 <= x <= 2^22 rounds x to an integer (round-half-even in the current rounding
-// mode) and leaves that integer in the low mantissa bits.
-constexpr float kMagic = 12582912.0f;
-
 // Codes are sign-magnitude nibbles: sign in bit 3, |k| in bits 0-2, zero as +0.
 //
-// RTNE: rounding is symmetric, so |k| = rint(|v|); k < 0 exactly when v < -1/2. No clamp is needed:
-// |v| = RN(|y| * RN(7/amax)) <= 7 (1 + 2^-23), which still rounds to 7.
-__device__ __forceinline__ uint32_t uniform_rtne(float v) {
-    const uint32_t mag = __float_as_uint(__builtin_fabsf(v) + kMagic) & 0x7u;
-    return mag | (v < -0.5f ? 8u : 0u);
-}
+// Uniform grid. 1.5 * 2^23 + 8 is an even integer with ulp 1: adding it to v (|v| <= 7.5) rounds v to the
+// nearest integer k, ties to the even one (RTNE), and leaves the nibble k + 8 in bits 0-3 of the sum with
+// bits 4-21 clear. No clamp is needed for RTNE: |v| = RN(|y| * RN(7/amax)) <= 7 (1 + 2^-23) rounds to 7.
+constexpr float kMagic8 = 12582920.0f;
 
 // Stochastic rounding between the integers lo = floor(v) and lo + 1: up iff lo + u/2^16 < v. Both sides
-// are exact in fp32 (lo + u/2^16 needs at most 20 significant bits), so the decision is exact.
-__device__ __forceinline__ uint32_t uniform_sr(float v, uint32_t u16) {
+// are exact in fp32 (lo + u/2^16 needs at most 20 significant bits), so the decision is exact. Returns the
+// chosen integer.
+__device__ __forceinline__ float uniform_sr_level(float v, uint32_t u16) {
     const float vc = __builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f);
     const float lo = floorf(vc);
     const float t = __builtin_fmaf((float)u16, 1.0f / 65536.0f, lo);
-    const float k = (t < vc) ? lo + 1.0f : lo;
-    const uint32_t mag = __float_as_uint(__builtin_fabsf(k) + kMagic) & 0x7u;
-    return mag | (k < 0.0f ? 8u : 0u);
+    return (t < vc) ? lo + 1.0f : lo;
+}
+
+// Eight words whose bits 0-3 hold a nibble and bits 4-21 are clear (higher bits arbitrary) -> one dword,
+// element i in bits 4i .. 4i+3. Shifts by 12 and more push the arbitrary bits out of the word.
+__device__ __forceinline__ uint32_t pack_nibbles(const uint32_t* t) {
+    const uint32_t low = t[0] | (t[1] << 4) | (t[2] << 8);
+    const uint32_t high = (t[3] << 12) | (t[4] << 16) | (t[5] << 20) | (t[6] << 24) | (t[7] << 28);
+    return (low & 0xFFFu) | high;
+}
+
+// Offset nibbles n = k + 8 (k in -7..7, so n >= 1) -> sign-magnitude nibbles: n >= 8 gives n ^ 8 = k, n < 8
+// gives (n ^ 15) + 1 = 16 - n = 8 | -k. Per nibble, without carries between nibbles.
+__device__ __forceinline__ uint32_t offset_to_sign_magnitude(uint32_t x) {
+    const uint32_t t = ~x & 0x88888888u;  // 8 in the nibbles with n < 8
+    const uint32_t one = t >> 3;
+    return (x ^ 0x88888888u ^ (t - one)) + one;
 }
 
 // E2M1 magnitude code of the nearest level, ties to the even code (levels 0,.5,1,1.5,2,3,4,6; the bin
@@ -86,15 +102,10 @@ __device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t u16) {
     return e2m1_code_of_level(q);
 }
 
-template <int FMT, int ROUND>
-__device__ __forceinline__ uint32_t round_code(float v, uint32_t u16) {
-    if constexpr (FMT == kFmtUniform) {
-        if constexpr (ROUND == kRoundSR) return uniform_sr(v, u16);
-        else return uniform_rtne(v);
-    } else {
-        if constexpr (ROUND == kRoundSR) return e2m1_sr(v, u16);
-        else return e2m1_rtne(v);
-    }
+template <int ROUND>
+__device__ __forceinline__ uint32_t e2m1_code(float v, uint32_t u16) {
+    if constexpr (ROUND == kRoundSR) return e2m1_sr(v, u16);
+    else return e2m1_rtne(v);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -124,8 +135,9 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
                 }
             }
         }
+        // y' = 4 y (see the file header)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) y[i] = (float)(d[i] * 0.25);
+        for (int i = 0; i < 16; ++i) y[i] = (float)d[i];
     } else {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -137,8 +149,14 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
 #pragma unroll
     for (int i = 0; i < 16; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
     constexpr float g = FMT == kFmtUniform ? 7.0f : 6.0f;
-    scale = amax / g;                               // IEEE-correct fp32 division
-    const float r = amax > 0.0f ? g / amax : 0.0f;  // zero block: all v = 0, codes 0
+    // RN(amax / g) as RN(amax * c) with c = RN(1/g), corrected by one FMA residual step: equal to the correctly
+    // rounded quotient for every fp32 amax when g = 7 and for every normal quotient when g = 6 (both checked
+    // over all fp32 inputs); amax = 0 gives 0.
+    constexpr float c = 1.0f / g;
+    const float q0 = amax * c;
+    const float sc = __builtin_fmaf(__builtin_fmaf(-q0, g, amax), c, q0);
+    scale = RHT ? sc * 0.25f : sc;
+    const float r = amax > 0.0f ? g / amax : 0.0f;  // IEEE division; zero block: all v = 0, codes 0
 
     uint32_t u[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if constexpr (ROUND == kRoundSR) {
@@ -147,39 +165,96 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
         u[0] = p0.x; u[1] = p0.y; u[2] = p0.z; u[3] = p0.w;
         u[4] = p1.x; u[5] = p1.y; u[6] = p1.z; u[7] = p1.w;
     }
-    uint32_t lo = 0, hi = 0;
+    if constexpr (FMT == kFmtUniform) {
+        uint32_t t[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const float v = __fmul_rn(y[i], r);
-        const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-        const uint32_t c = round_code<FMT, ROUND>(v, u16);
-        if (i < 8) lo |= c << (4 * i);
-        else hi |= c << (4 * (i - 8));
+        for (int i = 0; i < 16; ++i) {
+            const float v = __fmul_rn(y[i], r);
+            if constexpr (ROUND == kRoundSR) {
+                const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
+                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);  // exact: an integer plus the constant
+            } else {
+                t[i] = __float_as_uint(v + kMagic8);  // the rounding itself
+            }
+        }
+        code_lo = offset_to_sign_magnitude(pack_nibbles(t));
+        code_hi = offset_to_sign_magnitude(pack_nibbles(t + 8));
+    } else {
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float v = __fmul_rn(y[i], r);
+            const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
+            const uint32_t c = e2m1_code<ROUND>(v, u16);
+            if (i < 8) lo |= c << (4 * i);
+            else hi |= c << (4 * (i - 8));
+        }
+        code_lo = lo;
+        code_hi = hi;
     }
-    code_lo = lo;
-    code_hi = hi;
 }
 
 // ------------------------------------------------------------------------------------------------
-// Rowwise: reduction axis contiguous. One thread per 16-block.
+// Rowwise: reduction axis contiguous. A workgroup of 512 threads quantizes a tile of 32 rows x 16 blocks
+// through LDS: a wave reads 4 rows x 512 contiguous bytes, each thread quantizes one block, and the tile is
+// written in panel order, each half-wave storing 32 rows x 8 bytes of one block. Consecutive workgroups take
+// consecutive block tiles of the same rows. Padding rows of the last panel are written as zeros.
 // ------------------------------------------------------------------------------------------------
+constexpr int kRR = 32;    // tile rows
+constexpr int kRB = 16;    // tile blocks
+constexpr int kRT = 512;   // threads
+constexpr int kRI = kRR * kRB / kRT;  // blocks per thread
+
 template <int FMT, int ROUND, bool RHT>
-__global__ __launch_bounds__(256) void quant_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, uint32_t total,
-                                                         FastDiv nb, QuantArgs qa, uint8_t* __restrict__ codes,
-                                                         int64_t code_ld, float* __restrict__ scales, int64_t scale_ld) {
-    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
-    if (i >= total) return;
-    const uint32_t r = fastdiv(i, nb);
-    const uint32_t b = i - r * nb.d;
-    const uint4* src = reinterpret_cast<const uint4*>(x + (int64_t)r * ld + (int64_t)b * kBlock);
-    const uint4 v0 = src[0];
-    const uint4 v1 = src[1];
-    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    uint32_t lo, hi;
-    float s;
-    quant_block16<FMT, ROUND, RHT>(w, qa, b, r, lo, hi, s);
-    *reinterpret_cast<uint2*>(codes + (int64_t)r * code_ld + (int64_t)b * 8) = make_uint2(lo, hi);
-    scales[(int64_t)r * scale_ld + b] = s;
+__global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, int64_t qrows,
+                                                         int64_t nb, QuantArgs qa, uint8_t* __restrict__ codes,
+                                                         int64_t code_pld, float* __restrict__ scales,
+                                                         int64_t scale_pld) {
+    __shared__ uint2 s_codes[kRB][kRR];
+    __shared__ float s_scales[kRB][kRR];
+    const int t = threadIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.y * kRR;
+    const int64_t b0 = (int64_t)blockIdx.x * kRB;
+
+    // item k = t + kRT q: row k / 16, block k % 16 of the tile
+    uint4 v[kRI][2];
+#pragma unroll
+    for (int q = 0; q < kRI; ++q) {
+        const int k = t + kRT * q;
+        const int64_t r = r0 + (k >> 4), b = b0 + (k & 15);
+        v[q][0] = v[q][1] = make_uint4(0, 0, 0, 0);
+        if (r < qrows && b < nb) {
+            const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kBlock);
+            v[q][0] = src[0];
+            v[q][1] = src[1];
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < kRI; ++q) {
+        const int k = t + kRT * q;
+        const int64_t r = r0 + (k >> 4), b = b0 + (k & 15);
+        uint32_t lo = 0, hi = 0;
+        float sc = 0.0f;
+        if (r < qrows && b < nb) {
+            const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
+                                   v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
+            quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+        }
+        s_codes[k & 15][k >> 4] = make_uint2(lo, hi);
+        s_scales[k & 15][k >> 4] = sc;
+    }
+    __syncthreads();
+    // item k: block k / 32, row k % 32 (the 32 rows lie in one panel: r0 is a multiple of 32)
+#pragma unroll
+    for (int q = 0; q < kRI; ++q) {
+        const int k = t + kRT * q;
+        const int64_t r = r0 + (k % kRR), b = b0 + (k / kRR);
+        if (b < nb) {
+            const int64_t P = r >> 7, ri = r & 127;
+            *reinterpret_cast<uint2*>(codes + P * code_pld + b * 1024 + ri * 8) = s_codes[k / kRR][k % kRR];
+            scales[P * scale_pld + b * 128 + ri] = s_scales[k / kRR][k % kRR];
+        }
+    }
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -199,13 +274,13 @@ struct TGroups {
 
 template <int FMT, int ROUND, bool RHT, bool GROUPED>
 __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
-                                                         int64_t ld, int64_t red_total, TGroups grp, QuantArgs qa,
-                                                         uint8_t* __restrict__ codes, int64_t code_ld,
-                                                         float* __restrict__ scales, int64_t scale_ld) {
+                                                         int64_t prows, int64_t ld, int64_t red_total, TGroups grp,
+                                                         QuantArgs qa, uint8_t* __restrict__ codes, int64_t code_pld,
+                                                         float* __restrict__ scales, int64_t scale_pld) {
     __shared__ uint32_t tile[kTR * kTStride];
     __shared__ int64_t src_row[kTR];
-    __shared__ uint2 out_codes[kTC][kTR / kBlock + 1];
-    __shared__ float out_scales[kTC][kTR / kBlock + 1];
+    __shared__ uint2 out_codes[kTR / kBlock][kTC];
+    __shared__ float out_scales[kTR / kBlock][kTC];
     __shared__ int64_t s_off[GROUPED ? kMaxGroupsLds + 1 : 1];
     __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
 
@@ -290,27 +365,32 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
             const int64_t ca = c0 + 2 * p, cb = ca + 1;
             if (blk_ok && ca < cols) {
                 quant_block16<FMT, ROUND, RHT>(col_lo, qa, gblk, (uint32_t)ca, lo, hi, s);
-                out_codes[2 * p][bl] = make_uint2(lo, hi);
-                out_scales[2 * p][bl] = s;
+                out_codes[bl][2 * p] = make_uint2(lo, hi);
+                out_scales[bl][2 * p] = s;
             }
             if (blk_ok && cb < cols) {
                 quant_block16<FMT, ROUND, RHT>(col_hi, qa, gblk, (uint32_t)cb, lo, hi, s);
-                out_codes[2 * p + 1][bl] = make_uint2(lo, hi);
-                out_scales[2 * p + 1][bl] = s;
+                out_codes[bl][2 * p + 1] = make_uint2(lo, hi);
+                out_scales[bl][2 * p + 1] = s;
             }
         }
         __syncthreads();
 
-        // 4. write out: 64 operand rows x 8 blocks; 8 consecutive threads cover one row's 64 bytes
+        // 4. write out: 8 blocks x 64 operand rows (all in one panel, c0 being a multiple of 64); consecutive
+        //    threads take consecutive rows of a block, so each block goes out as 64 x 8 contiguous bytes.
+        //    Rows past the operand (panel padding) are written as zeros.
         const int64_t b0 = p0 / kBlock;
 #pragma unroll
         for (int pass = 0; pass < 2; ++pass) {
             const int e = t + 256 * pass;
-            const int cl = e >> 3, bl = e & 7;
+            const int cl = e & (kTC - 1), bl = e / kTC;
             const int64_t c = c0 + cl;
-            if (c < cols && p0 + bl * kBlock < red_total) {
-                *reinterpret_cast<uint2*>(codes + c * code_ld + (b0 + bl) * 8) = out_codes[cl][bl];
-                scales[c * scale_ld + b0 + bl] = out_scales[cl][bl];
+            if (c < prows && p0 + bl * kBlock < red_total) {
+                const bool valid = c < cols;
+                const int64_t P = c >> 7, ri = c & 127;
+                *reinterpret_cast<uint2*>(codes + P * code_pld + (b0 + bl) * 1024 + ri * 8) =
+                    valid ? out_codes[bl][cl] : make_uint2(0u, 0u);
+                scales[P * scale_pld + (b0 + bl) * 128 + ri] = valid ? out_scales[bl][cl] : 0.0f;
             }
         }
         __syncthreads();
@@ -322,23 +402,26 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
 // ------------------------------------------------------------------------------------------------
 template <int FMT, int ROUND, bool RHT>
 static hipError_t launch_rows_t(const QuantJob& j, hipStream_t s) {
-    const uint32_t nb = (uint32_t)(j.red / kBlock);
-    const uint32_t total = (uint32_t)(j.qrows * nb);
-    const dim3 grid((total + 255) / 256);
-    quant_rows_kernel<FMT, ROUND, RHT><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, total,
-                                                           make_fastdiv(nb), j.qa, static_cast<uint8_t*>(j.codes),
-                                                           j.code_ld, j.scales, j.scale_ld);
+    const int64_t nb = j.red / kBlock;
+    const int64_t prows = padded_rows(j.qrows);
+    if (nb == 0 || prows == 0) return hipSuccess;
+    const dim3 grid((unsigned)((nb + kRB - 1) / kRB), (unsigned)(prows / kRR));
+    quant_rows_kernel<FMT, ROUND, RHT><<<grid, kRT, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, j.qrows, nb, j.qa,
+                                                           static_cast<uint8_t*>(j.codes), j.code_pld, j.scales,
+                                                           j.scale_pld);
     return hipGetLastError();
 }
 
 template <int FMT, int ROUND, bool RHT, bool GROUPED>
 static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
+    const int64_t prows = padded_rows(j.qrows);
     const int64_t gy = (j.red + kTR - 1) / kTR;
-    const dim3 grid((unsigned)((j.qrows + kTC - 1) / kTC), (unsigned)(gy < 65535 ? gy : 65535));
+    if (prows == 0 || gy == 0) return hipSuccess;
+    const dim3 grid((unsigned)(prows / kTC), (unsigned)(gy < 65535 ? gy : 65535));
     TGroups grp{j.group_off, j.group_poff, j.num_groups};
     quant_cols_kernel<FMT, ROUND, RHT, GROUPED><<<grid, 256, 0, s>>>(
-        static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, j.ld, j.red, grp, j.qa, static_cast<uint8_t*>(j.codes),
-        j.code_ld, j.scales, j.scale_ld);
+        static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, prows, j.ld, j.red, grp, j.qa,
+        static_cast<uint8_t*>(j.codes), j.code_pld, j.scales, j.scale_pld);
     return hipGetLastError();
 }
 

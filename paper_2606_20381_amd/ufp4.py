@@ -89,29 +89,54 @@ def _ptr(t: torch.Tensor | None) -> int | None:
     return None if t is None else t.data_ptr()
 
 
+PANEL_ROWS = 128  # rows per panel of a quantized operand
+
+
 @dataclass
 class QTensor:
-    """A quantized operand [rows, red] (reduction contiguous): packed codes and fp32 block scales."""
+    """A quantized operand [rows, red] in the library's panel layout.
 
-    codes: torch.Tensor  # uint8 [rows, >= red/2]
-    scales: torch.Tensor  # float32 [rows, >= red/16]
+    Rows are grouped in panels of 128; within a panel, block b (16 reduction positions) of all 128 rows is
+    contiguous: 128 x 8 bytes of codes at b * 1024 and 128 fp32 scales at b * 128. Rows past ``rows`` in the
+    last panel hold zeros. ``codes_rows()`` / ``scales_rows()`` give the plain row-major views.
+    """
+
+    codes: torch.Tensor  # uint8 [panels, >= 1024 * red/16]
+    scales: torch.Tensor  # float32 [panels, >= 128 * red/16]
     fmt: int
     rows: int
     red: int
 
     @property
-    def code_ld(self) -> int:
+    def code_panel_ld(self) -> int:
         return self.codes.stride(0)
 
     @property
-    def scale_ld(self) -> int:
+    def scale_panel_ld(self) -> int:
         return self.scales.stride(0)
+
+    @property
+    def panels(self) -> int:
+        return self.codes.shape[0]
+
+    def codes_rows(self) -> torch.Tensor:
+        """Codes as uint8 [rows, red/2], row-major (a copy)."""
+        nkb = self.red // 16
+        v = self.codes[:, : nkb * 1024].reshape(self.panels, nkb, PANEL_ROWS, 8).permute(0, 2, 1, 3)
+        return v.reshape(self.panels * PANEL_ROWS, nkb * 8)[: self.rows]
+
+    def scales_rows(self) -> torch.Tensor:
+        """Scales as float32 [rows, red/16], row-major (a copy)."""
+        nkb = self.red // 16
+        v = self.scales[:, : nkb * PANEL_ROWS].reshape(self.panels, nkb, PANEL_ROWS).permute(0, 2, 1)
+        return v.reshape(self.panels * PANEL_ROWS, nkb)[: self.rows]
 
 
 def empty_qtensor(rows: int, red: int, fmt: int = UNIFORM, device="cuda") -> QTensor:
-    code_ld = max(8, -(-(red // 2) // 16) * 16)  # 16-byte row stride
-    codes = torch.empty((rows, code_ld), dtype=torch.uint8, device=device)[:, : red // 2]
-    scales = torch.empty((rows, red // 16), dtype=torch.float32, device=device)
+    panels = max(1, -(-rows // PANEL_ROWS))
+    nkb = red // 16
+    codes = torch.empty((panels, max(16, nkb * 1024)), dtype=torch.uint8, device=device)
+    scales = torch.empty((panels, max(4, nkb * PANEL_ROWS)), dtype=torch.float32, device=device)
     return QTensor(codes, scales, fmt, rows, red)
 
 
@@ -122,8 +147,8 @@ def _quantize_call(name, fmt, x, transpose, rht, sign_mask, rounding, seed, stre
     qrows, red = (cols, rows) if transpose else (rows, cols)
     q = out if out is not None else empty_qtensor(qrows, red, fmt, x.device)
     st = getattr(lib(), name)(x.data_ptr(), rows, cols, x.stride(0), int(transpose), int(rht), sign_mask, rounding,
-                              seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_ld,
-                              q.scales.data_ptr(), q.scale_ld, _stream())
+                              seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_panel_ld,
+                              q.scales.data_ptr(), q.scale_panel_ld, _stream())
     _check(st, name)
     return q
 
@@ -163,8 +188,8 @@ def quantize_grouped_t(x: torch.Tensor, offsets: torch.Tensor, padded_offsets: t
     q = out if out is not None else empty_qtensor(cols, red_total, fmt, x.device)
     st = lib().ufp4_quantize_grouped_t(fmt, x.data_ptr(), rows, cols, x.stride(0), offsets.data_ptr(),
                                        padded_offsets.data_ptr(), G, red_total, int(rht), sign_mask, rounding,
-                                       seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_ld,
-                                       q.scales.data_ptr(), q.scale_ld, _stream())
+                                       seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_panel_ld,
+                                       q.scales.data_ptr(), q.scale_panel_ld, _stream())
     _check(st, "ufp4_quantize_grouped_t")
     return q
 
@@ -186,8 +211,8 @@ def _odt(t: torch.Tensor) -> int:
 def _gemm(name, a: QTensor, b: QTensor, M, N, K, c: torch.Tensor):
     if a.fmt != b.fmt:
         raise ValueError("operands quantized to different grids")
-    st = getattr(lib(), name)(a.codes.data_ptr(), a.code_ld, a.scales.data_ptr(), a.scale_ld, b.codes.data_ptr(),
-                              b.code_ld, b.scales.data_ptr(), b.scale_ld, M, N, K, a.fmt, c.data_ptr(), c.stride(0),
+    st = getattr(lib(), name)(a.codes.data_ptr(), a.code_panel_ld, a.scales.data_ptr(), a.scale_panel_ld, b.codes.data_ptr(),
+                              b.code_panel_ld, b.scales.data_ptr(), b.scale_panel_ld, M, N, K, a.fmt, c.data_ptr(), c.stride(0),
                               _odt(c), _stream())
     _check(st, name)
     return c
@@ -217,8 +242,8 @@ def gemm_fwd_y_grouped(xq: QTensor, wq: QTensor, offsets: torch.Tensor, n_per_gr
     G = offsets.numel() - 1
     M, K, N = xq.rows, xq.red, n_per_group
     c = _out(M, N, out_dtype, xq.codes.device, out)
-    st = lib().ufp4_gemm_fwd_y_grouped(xq.codes.data_ptr(), xq.code_ld, xq.scales.data_ptr(), xq.scale_ld,
-                                       wq.codes.data_ptr(), wq.code_ld, wq.scales.data_ptr(), wq.scale_ld,
+    st = lib().ufp4_gemm_fwd_y_grouped(xq.codes.data_ptr(), xq.code_panel_ld, xq.scales.data_ptr(), xq.scale_panel_ld,
+                                       wq.codes.data_ptr(), wq.code_panel_ld, wq.scales.data_ptr(), wq.scale_panel_ld,
                                        offsets.data_ptr(), G, M, N, K, xq.fmt, c.data_ptr(), c.stride(0), _odt(c),
                                        _stream())
     _check(st, "ufp4_gemm_fwd_y_grouped")
@@ -231,8 +256,8 @@ def gemm_bwd_dx_grouped(dyq: QTensor, wtq: QTensor, offsets: torch.Tensor, out_d
     G = offsets.numel() - 1
     M, N, K = dyq.rows, dyq.red, wtq.rows
     c = _out(M, K, out_dtype, dyq.codes.device, out)
-    st = lib().ufp4_gemm_bwd_dx_grouped(dyq.codes.data_ptr(), dyq.code_ld, dyq.scales.data_ptr(), dyq.scale_ld,
-                                        wtq.codes.data_ptr(), wtq.code_ld, wtq.scales.data_ptr(), wtq.scale_ld,
+    st = lib().ufp4_gemm_bwd_dx_grouped(dyq.codes.data_ptr(), dyq.code_panel_ld, dyq.scales.data_ptr(), dyq.scale_panel_ld,
+                                        wtq.codes.data_ptr(), wtq.code_panel_ld, wtq.scales.data_ptr(), wtq.scale_panel_ld,
                                         offsets.data_ptr(), G, M, N, K, dyq.fmt, c.data_ptr(), c.stride(0), _odt(c),
                                         _stream())
     _check(st, "ufp4_gemm_bwd_dx_grouped")
@@ -245,8 +270,8 @@ def gemm_bwd_dw_grouped(dytq: QTensor, xtq: QTensor, padded_offsets: torch.Tenso
     G = padded_offsets.numel() - 1
     N, K = dytq.rows, xtq.rows
     c = out if out is not None else torch.empty((G, N, K), dtype=out_dtype, device=dytq.codes.device)
-    st = lib().ufp4_gemm_bwd_dw_grouped(dytq.codes.data_ptr(), dytq.code_ld, dytq.scales.data_ptr(), dytq.scale_ld,
-                                        xtq.codes.data_ptr(), xtq.code_ld, xtq.scales.data_ptr(), xtq.scale_ld,
+    st = lib().ufp4_gemm_bwd_dw_grouped(dytq.codes.data_ptr(), dytq.code_panel_ld, dytq.scales.data_ptr(), dytq.scale_panel_ld,
+                                        xtq.codes.data_ptr(), xtq.code_panel_ld, xtq.scales.data_ptr(), xtq.scale_panel_ld,
                                         padded_offsets.data_ptr(), G, dytq.red, N, K, dytq.fmt, c.data_ptr(), c.stride(-2),
                                         _odt(c), _stream())
     _check(st, "ufp4_gemm_bwd_dw_grouped")

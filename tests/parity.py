@@ -52,12 +52,12 @@ def gpu_operand(t_dev: torch.Tensor, layout: str, fmt: int, rounding: int, rht: 
 
 
 def gpu_rows(q: U.QTensor, rows=None):
-    """(packed codes, scales) of the GPU operand on the host, restricted to `rows`."""
-    codes = q.codes.cpu().numpy()
-    scales = q.scales.cpu().numpy()
+    """(packed codes, scales) of the GPU operand as row-major host arrays, restricted to `rows`."""
+    codes, scales = q.codes_rows(), q.scales_rows()
     if rows is not None:
-        codes, scales = codes[rows], scales[rows]
-    return codes, scales
+        idx = torch.as_tensor(np.asarray(rows), dtype=torch.int64, device=codes.device)
+        codes, scales = codes[idx], scales[idx]
+    return codes.cpu().numpy(), scales.cpu().numpy()
 
 
 def assert_codes_equal(gpu_codes, gpu_scales, idx, sc, fmt, what=""):

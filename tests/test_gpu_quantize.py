@@ -115,6 +115,34 @@ def test_ragged_transposed(shape):
     _check_operand(t, "xt", O.E2M1, True, 0x2468, 11, rounding=O.SR, stream=2)
 
 
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+def test_panel_layout_padding_and_strides(fmt):
+    """Panel layout: 200 rows -> 2 panels whose last 56 rows are zero; wider panel strides than needed are
+    honoured (the gap is left untouched); both input layouts."""
+    g = torch.Generator().manual_seed(17)
+    t = torch.randn(200, 48, generator=g).bfloat16()
+    bits = WL.bf16_bits(t)
+    fn = U.rht_quantize if fmt == O.UNIFORM else U.e2m1_quantize
+    for layout, src in (("rows", t), ("cols", t.t().contiguous())):
+        qrows, red = 200, 48
+        nkb = red // 16
+        codes = torch.full((2, nkb * 1024 + 96), 0xAB, dtype=torch.uint8, device="cuda")
+        scales = torch.full((2, nkb * 128 + 12), -5.0, dtype=torch.float32, device="cuda")
+        q = U.QTensor(codes, scales, fmt, qrows, red)
+        print(f"panel layout fmt={fmt} layout={layout}", flush=True)
+        fn(src.cuda(), transpose=(layout == "cols"), rht=True, sign_mask=0x1111, rounding=O.RTNE, seed=1, out=q)
+        torch.cuda.synchronize()
+        gc, gs = P.gpu_rows(q)
+        idx, sc = P.oracle_operand(bits, "rows", fmt, O.RTNE, True, 0x1111, 1, 0)  # both give the operand t
+        P.assert_codes_equal(gc, gs, idx, sc, fmt, f"panel layout {layout}")
+        c = codes.cpu().numpy()
+        sv = scales.cpu().numpy()
+        pad = c[1, : nkb * 1024].reshape(nkb, 128, 8)[:, 200 - 128:, :]
+        assert np.all(pad == 0), "padding rows of the last panel must be zero codes"
+        assert np.all(sv[1, : nkb * 128].reshape(nkb, 128)[:, 200 - 128:] == 0.0)
+        assert np.all(c[:, nkb * 1024:] == 0xAB) and np.all(sv[:, nkb * 128:] == -5.0), "gap between panels written"
+
+
 def test_strided_input_rows_and_cols():
     g = torch.Generator().manual_seed(5)
     big = torch.randn(96, 200, generator=g).bfloat16().cuda()
@@ -144,20 +172,20 @@ def test_empty_and_invalid_calls():
     q = U.empty_qtensor(32, 32)
     s = torch.cuda.current_stream().cuda_stream
     # empty tensor: no launch, OK
-    assert L.ufp4_rht_quantize(x.data_ptr(), 0, 32, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_ld,
-                               q.scales.data_ptr(), q.scale_ld, s) == 0
+    assert L.ufp4_rht_quantize(x.data_ptr(), 0, 32, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
+                               q.scales.data_ptr(), q.scale_panel_ld, s) == 0
     # reduction length not a multiple of 16
-    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 24, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_ld,
-                               q.scales.data_ptr(), q.scale_ld, s) == 2
-    # code row stride too small
+    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 24, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
+                               q.scales.data_ptr(), q.scale_panel_ld, s) == 2
+    # code panel stride too small
     assert L.ufp4_rht_quantize(x.data_ptr(), 32, 32, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), 8,
-                               q.scales.data_ptr(), q.scale_ld, s) == 2
+                               q.scales.data_ptr(), q.scale_panel_ld, s) == 2
     # misaligned input
-    assert L.ufp4_rht_quantize(x.data_ptr() + 2, 32, 16, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_ld,
-                               q.scales.data_ptr(), q.scale_ld, s) == 3
+    assert L.ufp4_rht_quantize(x.data_ptr() + 2, 32, 16, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
+                               q.scales.data_ptr(), q.scale_panel_ld, s) == 3
     # bad enum
-    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 32, 32, 0, 1, 0, 7, 0, 0, q.codes.data_ptr(), q.code_ld,
-                               q.scales.data_ptr(), q.scale_ld, s) == 1
+    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 32, 32, 0, 1, 0, 7, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
+                               q.scales.data_ptr(), q.scale_panel_ld, s) == 1
     torch.cuda.synchronize()
 
 

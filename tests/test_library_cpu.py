@@ -49,21 +49,31 @@ def test_status_strings(lib):
 FAKE = 1 << 20  # a 1 MiB-aligned non-null address that is never dereferenced: every call below fails validation
 
 
+# panel strides for one and two 16-blocks of reduction
+C1, S1, C2, S2 = 1024, 128, 2048, 256
+
+
 @pytest.mark.parametrize("args,status", [
-    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream_id, codes, code_ld, scales, scale_ld)
-    ((None, 16, 16, 16, 0, 1, 0, 0, 0, 0, FAKE, 8, FAKE, 1), 1),          # null input
-    ((FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # cols % 16
-    ((FAKE, 24, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # transposed: rows % 16
-    ((FAKE, 16, 32, 30, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # ld < cols
-    ((FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 2),         # ld % 8
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 8, FAKE, 2), 2),          # code_ld < red/2
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 1), 2),         # scale_ld < red/16
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 20, FAKE, 2), 3),         # code_ld % 8
-    ((FAKE + 2, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 3),     # input alignment
-    ((FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, 16, FAKE, 2), 1),         # rounding enum
-    ((FAKE, 16, 32, 32, 2, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 1),         # transpose flag
-    ((FAKE, 16, 32, 32, 0, 1, 0x10000, 0, 0, 0, FAKE, 16, FAKE, 2), 1),   # sign mask > 16 bits
-    ((FAKE, -1, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2), 1),         # negative size
+    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream_id, codes, code_panel_ld, scales,
+    #  scale_panel_ld)
+    ((None, 16, 16, 16, 0, 1, 0, 0, 0, 0, FAKE, C1, FAKE, S1), 1),          # null input
+    ((FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # cols % 16
+    ((FAKE, 24, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # transposed: rows % 16
+    ((FAKE, 16, 32, 30, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # ld < cols
+    ((FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # ld % 8
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C1, FAKE, S2), 2),          # code panel stride < 1024 nkb
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S1), 2),          # scale panel stride < 128 nkb
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2 + 8, FAKE, S2), 3),      # code panel stride % 16
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2 + 2), 3),      # scale panel stride % 4
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE + 8, C2, FAKE, S2), 3),      # codes alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE + 4, S2), 3),      # scales alignment
+    ((FAKE + 2, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 3),      # input alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, C2, FAKE, S2), 1),          # rounding enum
+    ((FAKE, 16, 32, 32, 2, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 1),          # transpose flag
+    ((FAKE, 16, 32, 32, 0, 1, 0x10000, 0, 0, 0, FAKE, C2, FAKE, S2), 1),    # sign mask > 16 bits
+    ((FAKE, -1, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 1),          # negative size
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 1 << 30, FAKE, S2), 5),     # code panel stride > 2^29
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, 1 << 28), 5),     # scale panel stride > 2^27
 ])
 def test_quantize_validation(lib, args, status):
     for fn in (lib.ufp4_rht_quantize, lib.ufp4_e2m1_quantize):
@@ -71,15 +81,18 @@ def test_quantize_validation(lib, args, status):
 
 
 @pytest.mark.parametrize("args,status", [
-    # (a, lda, as, ldas, b, ldb, bs, ldbs, M, N, K, fmt, c, ldc, out)
-    ((None, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 16, 0, FAKE, 16, 0), 1),
-    ((FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 24, 0, FAKE, 16, 0), 2),    # K % 16
-    ((FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 16, 32, 0, FAKE, 16, 0), 2),    # lda < K/2
-    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE, 8, 0), 2),   # ldc < N
-    ((FAKE, 12, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 16, 0, FAKE, 16, 0), 3),  # lda % 8
-    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 3, FAKE, 16, 0), 1),  # format enum
-    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE, 16, 5), 1),  # out dtype enum
-    ((FAKE, 16, FAKE, 2, FAKE, 16, FAKE, 2, 16, 16, 32, 0, FAKE + 1, 16, 0), 3),  # output alignment
+    # (a, a_panel_ld, as, as_panel_ld, b, b_panel_ld, bs, bs_panel_ld, M, N, K, fmt, c, ldc, out)
+    ((None, C1, FAKE, S1, FAKE, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 1),
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 24, 0, FAKE, 16, 0), 2),      # K % 16
+    ((FAKE, C1, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 0), 2),      # A panel stride < 1024 K/16
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S1, 16, 16, 32, 0, FAKE, 16, 0), 2),      # B scale stride < 128 K/16
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 8, 0), 2),       # ldc < N
+    ((FAKE, C1 + 8, FAKE, S1, FAKE, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 3),  # A panel stride % 16
+    ((FAKE, C1, FAKE, S1, FAKE + 4, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 3),  # B codes alignment
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 3, FAKE, 16, 0), 1),      # format enum
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 5), 1),      # out dtype enum
+    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE + 1, 16, 0), 3),  # output alignment
+    ((FAKE, C2, FAKE, S2, FAKE, 1 << 30, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 0), 5), # B panel stride > 2^29
 ])
 def test_gemm_validation(lib, args, status):
     # the dense entry points map (M, N, K) onto (rows_a, rows_b, reduction) differently; pick the layout each
@@ -89,9 +102,9 @@ def test_gemm_validation(lib, args, status):
 
 def test_gemm_validation_per_pass_layout(lib):
     # bwd_dx: dY [M, N] . Wt [K, N]^T -> dX [M, K]; the reduction is N
-    assert lib.ufp4_gemm_bwd_dx(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 16, 24, 16, 0, FAKE, 16, 0, None) == 2
+    assert lib.ufp4_gemm_bwd_dx(FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 24, 16, 0, FAKE, 16, 0, None) == 2
     # bwd_dw: dYt [N, M] . Xt [K, M]^T -> dW [N, K]; the reduction is M
-    assert lib.ufp4_gemm_bwd_dw(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, 24, 16, 16, 0, FAKE, 16, 0, None) == 2
+    assert lib.ufp4_gemm_bwd_dw(FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 24, 16, 16, 0, FAKE, 16, 0, None) == 2
 
 
 def test_grouped_validation(lib):
@@ -110,9 +123,9 @@ def test_grouped_validation(lib):
                                         None) == 1
     assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, FAKE, 2, 32, 16, 16, 3, FAKE, 16, 0,
                                         None) == 1
-    # red_total wider than the operands' code rows
-    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, 8, FAKE, 2, FAKE, 8, FAKE, 2, FAKE, 2, 32, 16, 16, 0, FAKE, 16, 0,
-                                        None) == 2
+    # red_total wider than the operands' panels
+    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, C1, FAKE, S1, FAKE, C1, FAKE, S1, FAKE, 2, 32, 16, 16, 0, FAKE, 16,
+                                        0, None) == 2
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
