@@ -37,10 +37,14 @@ from paper_2606_20381_amd import workloads as WL  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
 INT8_PEAK_TOPS = 5000.0  # dense int8 / fp8 MFMA, MI355X
+FP4_PEAK_TFLOPS = 10100.0  # dense fp4 MFMA (the E2M1 baseline's block products)
 # Bound of an exact per-16-block fp32-scale GEMM: one VALU FMA per output and block, i.e. 2MNK / (MNK/16) = 32
 # ops per FMA, at 256 CUs x 4 SIMDs x 16 fp32 FMA lanes per clock x 2.4 GHz = 39.3 T FMA/s (non-packed).
 ATTAINABLE_TOPS = 32 * 256 * 4 * 16 * 2.4e9 / 1e12
-GEMM_KERNEL = "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)"
+GEMM_KERNEL = {
+    "ufp4": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
+    "e2m1": "gemm_f32_kernel (FP4 f8f6f4 MFMA per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
+}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 WARMUP_SECONDS = 0.5
 QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
@@ -73,28 +77,43 @@ class Timeline:
 # kernel table: label -> ("quant", elements) or ("gemm", flops)
 # ---------------------------------------------------------------------------------------------------
 
-def dense_step(wl, tl: Timeline):
+# Per recipe: the quantizer and, for fwd_y / bwd_dx / bwd_dw, whether the RHT is applied to that GEMM's
+# operands (Table 1: UFP4 rotates all three; the E2M1 baseline only bwd_dw's).
+RECIPES = {
+    "ufp4": (U.UNIFORM, (True, True, True), "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY"),
+    "e2m1": (U.E2M1, (False, False, True), "e2m1 baseline: E2M1 grid, RHT16 on bwd_dw only, SR on dY"),
+}
+
+
+def _quantizers(recipe: str):
+    fmt, (r_y, r_dx, r_dw), _ = RECIPES[recipe]
+    fn = U.rht_quantize if fmt == U.UNIFORM else U.e2m1_quantize
+    return fmt, fn, r_y, r_dx, r_dw
+
+
+def dense_step(wl, tl: Timeline, recipe: str = "ufp4"):
     m, s = wl.sign_mask, wl.seed
+    fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
     M, K = x.shape
     N = w.shape[0]
     q = {
-        "x": U.empty_qtensor(M, K), "w": U.empty_qtensor(N, K), "dy": U.empty_qtensor(M, N),
-        "wt": U.empty_qtensor(K, N), "dyt": U.empty_qtensor(N, M), "xt": U.empty_qtensor(K, M),
+        "x": U.empty_qtensor(M, K, fmt), "w": U.empty_qtensor(N, K, fmt), "dy": U.empty_qtensor(M, N, fmt),
+        "wt": U.empty_qtensor(K, N, fmt), "dyt": U.empty_qtensor(N, M, fmt), "xt": U.empty_qtensor(K, M, fmt),
     }
     y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
     dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
     dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
 
     def step(rec):
-        tl.run("quant_x", lambda: U.rht_quantize(x, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: U.rht_quantize(w, sign_mask=m, out=q["w"]), rec)
-        tl.run("quant_dy_sr", lambda: U.rht_quantize(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
-                                                     out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: U.rht_quantize(w, transpose=True, sign_mask=m, out=q["wt"]), rec)
-        tl.run("quant_dyt_sr", lambda: U.rht_quantize(dy, transpose=True, sign_mask=m, rounding=U.SR, seed=s,
-                                                      stream_id=1, out=q["dyt"]), rec)
-        tl.run("quant_xt", lambda: U.rht_quantize(x, transpose=True, sign_mask=m, out=q["xt"]), rec)
+        tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: Q(w, rht=r_y, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
+                                        out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: Q(w, transpose=True, rht=r_dx, sign_mask=m, out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: Q(dy, transpose=True, rht=r_dw, sign_mask=m, rounding=U.SR, seed=s,
+                                         stream_id=1, out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: Q(x, transpose=True, rht=r_dw, sign_mask=m, out=q["xt"]), rec)
         tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y(q["x"], q["w"], out=y), rec)
         tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
         tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
@@ -108,8 +127,9 @@ def dense_step(wl, tl: Timeline):
     return step, kern
 
 
-def moe_step(wl, tl: Timeline):
+def moe_step(wl, tl: Timeline, recipe: str = "ufp4"):
     m, s = wl.sign_mask, wl.seed
+    fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     E, N, K = wl.w.shape
     x, dy = wl.x.cuda(), wl.dy.cuda()
     w2 = wl.w.reshape(E * N, K).cuda()
@@ -117,22 +137,24 @@ def moe_step(wl, tl: Timeline):
     off, poff, red = U.group_offsets(wl.counts)
     eoff, epoff, ered = U.group_offsets([N] * E)
     q = {
-        "x": U.empty_qtensor(M, K), "w": U.empty_qtensor(E * N, K), "dy": U.empty_qtensor(M, N),
-        "wt": U.empty_qtensor(K, E * N), "dyt": U.empty_qtensor(N, red), "xt": U.empty_qtensor(K, red),
+        "x": U.empty_qtensor(M, K, fmt), "w": U.empty_qtensor(E * N, K, fmt), "dy": U.empty_qtensor(M, N, fmt),
+        "wt": U.empty_qtensor(K, E * N, fmt), "dyt": U.empty_qtensor(N, red, fmt), "xt": U.empty_qtensor(K, red, fmt),
     }
     y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
     dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
     dw = torch.empty(E, N, K, dtype=torch.float32, device="cuda")
 
     def step(rec):
-        tl.run("quant_x", lambda: U.rht_quantize(x, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: U.rht_quantize(w2, sign_mask=m, out=q["w"]), rec)
-        tl.run("quant_dy_sr", lambda: U.rht_quantize(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
-                                                     out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, sign_mask=m, out=q["wt"]), rec)
-        tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, poff, red, sign_mask=m, rounding=U.SR, seed=s,
-                                                            stream_id=1, out=q["dyt"]), rec)
-        tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, poff, red, sign_mask=m, out=q["xt"]), rec)
+        tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: Q(w2, rht=r_y, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
+                                        out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, fmt=fmt, rht=r_dx, sign_mask=m,
+                                                        out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
+                                                            rounding=U.SR, seed=s, stream_id=1, out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
+                                                        out=q["xt"]), rec)
         tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y_grouped(q["x"], q["w"], off, N, out=y), rec)
         tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx_grouped(q["dy"], q["wt"], off, out=dx), rec)
         tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw_grouped(q["dyt"], q["xt"], poff, out=dw), rec)
@@ -202,7 +224,7 @@ def measured_traffic(kind: str, workload: str):
 # CPU oracle baseline: the same layer step on a bounded sample of tokens
 # ---------------------------------------------------------------------------------------------------
 
-def cpu_baseline(wl, tokens: int = 512):
+def cpu_baseline(wl, tokens: int = 512, recipe: str = "ufp4"):
     from oracle import ufp4_oracle as O
     from threadpoolctl import threadpool_info
 
@@ -212,7 +234,7 @@ def cpu_baseline(wl, tokens: int = 512):
     M, K = x.shape
     N = w.shape[0]
     t0 = time.perf_counter()
-    O.layer_gemms(x, w, dy, "ufp4", sign_mask=wl.sign_mask, seed=wl.seed)
+    O.layer_gemms(x, w, dy, recipe, sign_mask=wl.sign_mask, seed=wl.seed)
     dt = time.perf_counter() - t0
     flops = 3 * 2 * M * N * K
     blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
@@ -235,6 +257,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
     ap.add_argument("--workload", default="dense",
                     choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "copy1g"])
+    ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPES),
+                    help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -257,7 +281,7 @@ def main():
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
-        step, kern = (moe_step if wl.grouped else dense_step)(wl, tl)
+        step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe)
         wname = wl.name
     torch.cuda.synchronize()
 
@@ -309,9 +333,10 @@ def main():
         per_launch = np.mean([kern[k][1] for k in gemm_labels])
         avg_us = np.mean([tl.mean_us(k) for k in gemm_labels])
         ach = per_launch / (avg_us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "kernel": GEMM_KERNEL,
-                "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": measured_traffic("gemm", wname),
+        peak = INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS
+        roof = {"bound": "mfma", "kernel": GEMM_KERNEL[args.recipe],
+                "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": measured_traffic("gemm", wname + "/" + args.recipe),
                 "attainable": {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
                                "why": "one fp32 VALU FMA per output and 16-block"}}
     else:
@@ -342,14 +367,14 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if gemm_labels else "f64+f32",
         "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
-        "config": {"workload": wname, "recipe": "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY",
+        "config": {"workload": wname, "recipe": RECIPES[args.recipe][2],
                    "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",
                    "wall_s": round(wall, 3)},
         "roofline": roof,
         "breakdown": breakdown,
     }
     if wl is not None and not args.no_cpu_baseline and not wl.grouped:
-        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"] = cpu_baseline(wl, recipe=args.recipe)
     print(json.dumps(out), flush=True)
 
 

@@ -612,7 +612,7 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
             if constexpr (OUT == kOutF32) {
                 static_cast<float*>(j.c)[off] = v;
             } else {
-                static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
+                static_cast<uint16_t*>(j.c)[off] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
             }
         }
     }
