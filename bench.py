@@ -10,7 +10,7 @@ Prints one JSON line. `value` is the step's GEMM work (3 x 2MNK) divided by the 
 element) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel, the dominant one; `cpu_baseline` times the CPU
 oracle on a bounded sample of the same layer.
 
-Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g]
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|copy1g]
 
 Without --warmup the untimed warmup runs whole steps until at least WARMUP_SECONDS have passed: the GPU's clock
 takes tens of milliseconds of load to settle, and a few milliseconds of warmup would time the ramp.
@@ -179,15 +179,18 @@ def copy1g_step(tl: Timeline):
     return step, {"copy": ("copy", t.numel() * t.element_size())}
 
 
-def quant1g_step(tl: Timeline):
+def quant1g_step(tl: Timeline, transpose: bool):
+    """The quantizer alone on a 1 GiB bf16 tensor, rowwise (reduction along its 16384 columns) or transposed
+    (operand X^T, reduction along its 32768 rows)."""
     t = WL.quantizer_tensor().cuda()
     R, C = t.shape
-    q = U.empty_qtensor(R, C)
+    q = U.empty_qtensor(C, R) if transpose else U.empty_qtensor(R, C)
+    label = "quant_cols_rtne" if transpose else "quant_rows_rtne"
 
     def step(rec):
-        tl.run("quant_rows_rtne", lambda: U.rht_quantize(t, sign_mask=0x6A09, out=q), rec)
+        tl.run(label, lambda: U.rht_quantize(t, transpose=transpose, sign_mask=0x6A09, out=q), rec)
 
-    return step, {"quant_rows_rtne": ("quant", R * C)}
+    return step, {label: ("quant", R * C)}
 
 
 # ---------------------------------------------------------------------------------------------------
@@ -256,7 +259,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
     ap.add_argument("--workload", default="dense",
-                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "copy1g"])
+                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "copy1g"])
     ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPES),
                     help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -273,9 +276,11 @@ def main():
 
     tl = Timeline()
     wl = None
-    if args.workload == "quant1g":
-        step, kern = quant1g_step(tl)
-        wname = "standalone quantizer: 32768x16384 bf16 (1 GiB), rowwise RTNE with RHT"
+    if args.workload in ("quant1g", "quant1g-t"):
+        transpose = args.workload == "quant1g-t"
+        step, kern = quant1g_step(tl, transpose)
+        wname = (f"standalone quantizer: 32768x16384 bf16 (1 GiB), {'transposed' if transpose else 'rowwise'} "
+                 f"RTNE with RHT")
     elif args.workload == "copy1g":
         step, kern = copy1g_step(tl)
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
@@ -346,7 +351,7 @@ def main():
         us = tl.mean_us(label)
         per_launch = kern[label][1] * (QUANT_BYTES_PER_ELEM if kern[label][0] == "quant" else 2)
         ach = per_launch / (us * 1e-6) / 1e9
-        kname = "quant_rows_kernel" if kern[label][0] == "quant" else "copy"
+        kname = {"quant_rows_rtne": "quant_rows_kernel", "quant_cols_rtne": "quant_cols_kernel"}.get(label, "copy")
         roof = {"bound": "hbm", "kernel": kname, "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic("quant", wname) if kname != "copy" else None}

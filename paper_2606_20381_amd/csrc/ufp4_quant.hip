@@ -258,12 +258,15 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restr
 }
 
 // ------------------------------------------------------------------------------------------------
-// Transposed (and grouped-transposed): operand A = X^T, reduction along X's rows.
-// Tile: 128 padded reduction positions (8 blocks) x 64 columns of X. 256 threads.
+// Transposed (and grouped-transposed): operand A = X^T, reduction along X's rows. A thread loads a
+// 16-row x kXC-column bf16 sub-tile (one load of 2 kXC bytes per row) and quantizes its kXC column blocks
+// from registers, so no LDS transposition and no barrier is needed. It then writes the kXC consecutive
+// operand rows of its block, 8 kXC contiguous bytes of codes. A workgroup of 256 threads covers 64 columns
+// x (256 / (64 / kXC)) blocks; the threads of one block read 128 contiguous bytes of each row. (Measured:
+// 4 columns per thread performs within a few percent of 8; an LDS-transposed 128 x 64 tile was 12-20%
+// slower.)
 // ------------------------------------------------------------------------------------------------
-constexpr int kTR = 128;               // tile rows (reduction positions), 8 blocks
-constexpr int kTC = 64;                // tile columns (operand rows of A)
-constexpr int kTStride = kTC / 2 + 4;  // LDS tile row stride in dwords (bf16 pairs), padded
+constexpr int kXC = 8;                     // columns (operand rows) per thread
 constexpr int kMaxGroupsLds = 1024;
 
 struct TGroups {
@@ -272,21 +275,19 @@ struct TGroups {
     int32_t G;
 };
 
+constexpr int kXG = 64 / kXC;              // column groups per workgroup
+constexpr int kXB = 256 / kXG;             // blocks per workgroup
+static_assert(kXC == 8 || kXC == 4, "columns per thread");
+
 template <int FMT, int ROUND, bool RHT, bool GROUPED>
-__global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
-                                                         int64_t prows, int64_t ld, int64_t red_total, TGroups grp,
-                                                         QuantArgs qa, uint8_t* __restrict__ codes, int64_t code_pld,
-                                                         float* __restrict__ scales, int64_t scale_pld) {
-    __shared__ uint32_t tile[kTR * kTStride];
-    __shared__ int64_t src_row[kTR];
-    __shared__ uint2 out_codes[kTR / kBlock][kTC];
-    __shared__ float out_scales[kTR / kBlock][kTC];
+__global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restrict__ x, int64_t rows,
+                                                             int64_t cols, int64_t prows, int64_t ld,
+                                                             int64_t red_total, TGroups grp, QuantArgs qa,
+                                                             uint8_t* __restrict__ codes, int64_t code_pld,
+                                                             float* __restrict__ scales, int64_t scale_pld) {
     __shared__ int64_t s_off[GROUPED ? kMaxGroupsLds + 1 : 1];
     __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
-
     const int t = threadIdx.x;
-    const int64_t c0 = (int64_t)blockIdx.x * kTC;
-
     if constexpr (GROUPED) {
         for (int g = t; g <= grp.G; g += 256) {
             s_off[g] = grp.off[g];
@@ -294,106 +295,76 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         }
         __syncthreads();
     }
+    const int cg = t % kXG, rb = t / kXG;
+    const int64_t cbase = (int64_t)blockIdx.x * 64 + cg * kXC;  // first operand row of the thread
+    if (cbase >= prows) return;
+    const int ncol = cols - cbase < kXC ? (int)(cols - cbase) : kXC;  // valid columns of the thread (<= 0: none)
+    const int64_t nblk = red_total / kBlock;
+    constexpr int kW = kXC / 2;  // dwords per row
 
-    for (int64_t p0 = (int64_t)blockIdx.y * kTR; p0 < red_total; p0 += (int64_t)gridDim.y * kTR) {
-        // 1. source row of every tile row (-1: zero padding or past the end)
-        if (t < kTR) {
-            const int64_t P = p0 + t;
-            int64_t sr = -1;
-            if (P < red_total) {
-                if constexpr (GROUPED) {
-                    int lo = 0, hi = grp.G - 1;  // last group with poff[g] <= P
-                    while (lo < hi) {
-                        const int mid = (lo + hi + 1) >> 1;
-                        if (s_poff[mid] <= P) lo = mid;
-                        else hi = mid - 1;
+    for (int64_t gb = (int64_t)blockIdx.y * kXB + rb; gb < nblk; gb += (int64_t)gridDim.y * kXB) {
+        const int64_t P0 = gb * kBlock;
+        // the 16 positions of a block lie in one group (group lengths are padded to multiples of 16): rows
+        // src0 .. src0 + nvalid - 1 of X, the rest padding
+        int64_t src0, nvalid;
+        if constexpr (GROUPED) {
+            int lo = 0, hi = grp.G - 1;  // last group with poff[g] <= P0
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_poff[mid] <= P0) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t local0 = P0 - s_poff[lo];
+            src0 = s_off[lo] + local0;
+            nvalid = (s_off[lo + 1] - s_off[lo]) - local0;
+        } else {
+            src0 = P0;
+            nvalid = kBlock;
+        }
+        if (src0 + nvalid > rows) nvalid = rows - src0;  // offsets beyond X are treated as padding
+        if (src0 < 0 || nvalid < 0) nvalid = 0;
+
+        uint32_t v[kBlock][kW];
+#pragma unroll
+        for (int j = 0; j < kBlock; ++j) {
+#pragma unroll
+            for (int k = 0; k < kW; ++k) v[j][k] = 0;
+            if (j < nvalid) {
+                const uint16_t* src = x + (src0 + j) * ld + cbase;
+                if (ncol == kXC) {
+                    if constexpr (kXC == 8) {
+                        const uint4 l = *reinterpret_cast<const uint4*>(src);
+                        v[j][0] = l.x; v[j][1] = l.y; v[j][2] = l.z; v[j][3] = l.w;
+                    } else {
+                        const uint2 l = *reinterpret_cast<const uint2*>(src);
+                        v[j][0] = l.x; v[j][1] = l.y;
                     }
-                    const int64_t local = P - s_poff[lo];
-                    // rows past the group's tokens are padding; offsets beyond X are treated as padding too
-                    if (local < s_off[lo + 1] - s_off[lo] && s_off[lo] + local < rows) sr = s_off[lo] + local;
-                } else {
-                    sr = P;
+                } else if (ncol > 0) {  // ragged last columns: no read past column cols - 1
+#pragma unroll
+                    for (int k = 0; k < kXC; ++k)
+                        if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
                 }
             }
-            src_row[t] = sr;
         }
-        __syncthreads();
-
-        // 2. load the 128 x 64 bf16 tile (16 bytes per thread and pass, 8 threads per tile row)
-        const bool full_cols = c0 + kTC <= cols;
+        uint32_t clo[kXC], chi[kXC];
+        float sc[kXC];
 #pragma unroll
-        for (int pass = 0; pass < 4; ++pass) {
-            const int chunk = t + 256 * pass;
-            const int row = chunk >> 3, c8 = chunk & 7;
-            const int64_t sr = src_row[row];
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (sr >= 0) {
-                const uint16_t* src = x + sr * ld + c0 + c8 * 8;
-                if (full_cols) {
-                    v = *reinterpret_cast<const uint4*>(src);
-                } else {
-                    uint16_t e[8];
+        for (int q = 0; q < kXC; ++q) {
+            const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;  // high or low bf16 of each dword
+            uint32_t w[8];
 #pragma unroll
-                    for (int k = 0; k < 8; ++k) e[k] = (c0 + c8 * 8 + k < cols) ? src[k] : (uint16_t)0;
-                    v = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
-                                   e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
-                }
-            }
-            uint32_t* dst = &tile[row * kTStride + c8 * 4];
-            dst[0] = v.x;
-            dst[1] = v.y;
-            dst[2] = v.z;
-            dst[3] = v.w;
+            for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
+            clo[q] = chi[q] = 0;
+            sc[q] = 0.0f;
+            if (q < ncol) quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
         }
-        __syncthreads();
-
-        // 3. each thread: column pair (2p, 2p+1), block bl of the tile
-        {
-            const int p = t & 31, bl = t >> 5;
-            uint32_t col_lo[8], col_hi[8];
+        const int64_t P = cbase >> 7, ri = cbase & 127;  // the kXC rows lie in one panel
+        uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + ri * 8);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t a = tile[(bl * kBlock + 2 * j) * kTStride + p];
-                const uint32_t b = tile[(bl * kBlock + 2 * j + 1) * kTStride + p];
-                col_lo[j] = (a & 0xFFFFu) | (b << 16);
-                col_hi[j] = (a >> 16) | (b & 0xFFFF0000u);
-            }
-            const uint32_t gblk = (uint32_t)(p0 / kBlock) + bl;
-            const bool blk_ok = p0 + bl * kBlock < red_total;
-            uint32_t lo, hi;
-            float s;
-            const int64_t ca = c0 + 2 * p, cb = ca + 1;
-            if (blk_ok && ca < cols) {
-                quant_block16<FMT, ROUND, RHT>(col_lo, qa, gblk, (uint32_t)ca, lo, hi, s);
-                out_codes[bl][2 * p] = make_uint2(lo, hi);
-                out_scales[bl][2 * p] = s;
-            }
-            if (blk_ok && cb < cols) {
-                quant_block16<FMT, ROUND, RHT>(col_hi, qa, gblk, (uint32_t)cb, lo, hi, s);
-                out_codes[bl][2 * p + 1] = make_uint2(lo, hi);
-                out_scales[bl][2 * p + 1] = s;
-            }
-        }
-        __syncthreads();
-
-        // 4. write out: 8 blocks x 64 operand rows (all in one panel, c0 being a multiple of 64); consecutive
-        //    threads take consecutive rows of a block, so each block goes out as 64 x 8 contiguous bytes.
-        //    Rows past the operand (panel padding) are written as zeros.
-        const int64_t b0 = p0 / kBlock;
+        for (int q = 0; q < kXC / 2; ++q) dc[q] = make_uint4(clo[2 * q], chi[2 * q], clo[2 * q + 1], chi[2 * q + 1]);
+        float4* ds = reinterpret_cast<float4*>(scales + P * scale_pld + gb * 128 + ri);
 #pragma unroll
-        for (int pass = 0; pass < 2; ++pass) {
-            const int e = t + 256 * pass;
-            const int cl = e & (kTC - 1), bl = e / kTC;
-            const int64_t c = c0 + cl;
-            if (c < prows && p0 + bl * kBlock < red_total) {
-                const bool valid = c < cols;
-                const int64_t P = c >> 7, ri = c & 127;
-                *reinterpret_cast<uint2*>(codes + P * code_pld + (b0 + bl) * 1024 + ri * 8) =
-                    valid ? out_codes[bl][cl] : make_uint2(0u, 0u);
-                scales[P * scale_pld + (b0 + bl) * 128 + ri] = valid ? out_scales[bl][cl] : 0.0f;
-            }
-        }
-        __syncthreads();
+        for (int q = 0; q < kXC / 4; ++q) ds[q] = make_float4(sc[4 * q], sc[4 * q + 1], sc[4 * q + 2], sc[4 * q + 3]);
     }
 }
 
@@ -415,9 +386,10 @@ static hipError_t launch_rows_t(const QuantJob& j, hipStream_t s) {
 template <int FMT, int ROUND, bool RHT, bool GROUPED>
 static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
     const int64_t prows = padded_rows(j.qrows);
-    const int64_t gy = (j.red + kTR - 1) / kTR;
+    const int64_t nblk = j.red / kBlock;
+    const int64_t gy = (nblk + kXB - 1) / kXB;
     if (prows == 0 || gy == 0) return hipSuccess;
-    const dim3 grid((unsigned)(prows / kTC), (unsigned)(gy < 65535 ? gy : 65535));
+    const dim3 grid((unsigned)((prows + 63) / 64), (unsigned)(gy < 65535 ? gy : 65535));
     TGroups grp{j.group_off, j.group_poff, j.num_groups};
     quant_cols_kernel<FMT, ROUND, RHT, GROUPED><<<grid, 256, 0, s>>>(
         static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, prows, j.ld, j.red, grp, j.qa,
