@@ -331,6 +331,18 @@ def operand_colwise(t_bits: np.ndarray) -> np.ndarray:
     return np.ascontiguousarray(bf16_bits_to_f32(t_bits).T)
 
 
+def quantize_both(t_bits: np.ndarray, fmt: int, rounding: int, rht_rows: bool, rht_cols: bool,
+                  sign_mask_rows: int = 0, sign_mask_cols: int = 0, seed: int = 0, stream_rows: int = 0,
+                  stream_cols: int = 0):
+    """The two operands one stored tensor T [rows, cols] supplies to a training step (Sec. 2.2: the RHT and
+    the quantization run along each GEMM's reduction axis, and T is reduced along its columns in one GEMM and
+    along its rows in another): (Q(T) along cols, Q(T^T) along rows), two independent quantizations with
+    their own RHT flag, sign mask and SR stream. Returns ((idx, scales) rowwise, (idx, scales) transposed).
+    """
+    return (quantize_rows(operand_rowwise(t_bits), fmt, rounding, rht_rows, sign_mask_rows, seed, stream_rows),
+            quantize_rows(operand_colwise(t_bits), fmt, rounding, rht_cols, sign_mask_cols, seed, stream_cols))
+
+
 def pad16(n: int) -> int:
     return -(-int(n) // BLOCK) * BLOCK
 

@@ -440,6 +440,31 @@ def test_colwise_is_rowwise_of_transpose():
     assert np.array_equal(i1, i2) and np.array_equal(s1, s2)
 
 
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+def test_both_operands_of_one_tensor(fmt):
+    """quantize_both: a symmetric tensor gives the same operand both ways, and the transposed output of T
+    is the rowwise output of T^T (with the settings swapped)."""
+    rng = np.random.default_rng(41)
+    a = rng.standard_normal((48, 48)).astype(np.float32)
+    sym = O.f32_to_bf16_bits(a + a.T)
+    (ir, sr), (ic, scol) = O.quantize_both(sym, fmt, O.SR, True, True, 0x1234, 0x1234, seed=9, stream_rows=3,
+                                           stream_cols=3)
+    assert np.array_equal(ir, ic) and np.array_equal(sr, scol)
+    t = _rand_bf16_bits(rng, (32, 80))
+    (ir, sr), (ic, scol) = O.quantize_both(t, fmt, O.SR, False, True, 0x00F0, 0xBEEF, seed=4, stream_rows=0,
+                                           stream_cols=1)
+    assert ir.shape == (32, 80) and ic.shape == (80, 32)
+    tt = np.ascontiguousarray(t.T)
+    (jr, tr), (jc, tc) = O.quantize_both(tt, fmt, O.SR, True, False, 0xBEEF, 0x00F0, seed=4, stream_rows=1,
+                                         stream_cols=0)
+    assert np.array_equal(ic, jr) and np.array_equal(scol, tr)
+    assert np.array_equal(ir, jc) and np.array_equal(sr, tc)
+    # different streams give different SR draws: the two outputs of a symmetric tensor then differ
+    (ir, _), (ic, _) = O.quantize_both(sym, fmt, O.SR, True, True, 0x1234, 0x1234, seed=9, stream_rows=0,
+                                       stream_cols=1)
+    assert not np.array_equal(ir, ic)
+
+
 # ------------------------------------------------------------------------------------------------
 # GEMMs (Sec. 2.2)
 # ------------------------------------------------------------------------------------------------
