@@ -1,16 +1,22 @@
 """Benchmark of the UFP4 hot path on one MI355X.
 
-One step = the whole hot path of one linear layer's training step under the UFP4 recipe: six fused
-RHT + quantize calls (X, W rowwise along K; dY rowwise along N with SR; W^T along N; dY^T along M with SR;
-X^T along M) and the three block-scaled 4-bit GEMMs fwd_y, bwd_dx, bwd_dw. Inputs are resident in HBM before
-the timed region; every output buffer is allocated before it, so the timed loop only launches kernels.
+One step = the whole hot path of one linear layer's training step under the UFP4 recipe: the six fused
+RHT + quantized operands (X, W rowwise along K; dY rowwise along N with SR; W^T along N; dY^T along M with SR;
+X^T along M) and the three block-scaled 4-bit GEMMs fwd_y, bwd_dx, bwd_dw. By default X and W each go through
+the two-operand quantizer (one read, both operands) and dY through the two single-output kernels (faster for
+SR); --quant separate uses six single-output calls. Inputs are resident in HBM before the timed region; every
+output buffer is allocated before it, so the timed loop only launches kernels.
 
 Prints one JSON line. `value` is the step's GEMM work (3 x 2MNK) divided by the step time, in TFLOP/s;
-`breakdown` has every kernel's average duration and its own GB/s (quantizers, 2.75 algorithmic bytes per
-element) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel, the dominant one; `cpu_baseline` times the CPU
-oracle on a bounded sample of the same layer.
+`breakdown` has every kernel's average duration and its own GB/s (algorithmic bytes: 2.75 per element for a
+single-output quantizer, 3.5 for the two-operand one) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel,
+the dominant one; `cpu_baseline` times the CPU oracle on a bounded sample of the same layer.
 
-Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|copy1g]
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--quant dual|separate]
+                       [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|quant1g-dual|copy1g]
+
+The quant1g workloads time one quantizer on a 1 GiB bf16 tensor; they also time the same kernel without the
+RHT (plain block quantization) and report the ratio, the quantity the paper gives for its own fused kernel.
 
 Without --warmup the untimed warmup runs whole steps until at least WARMUP_SECONDS have passed: the GPU's clock
 takes tens of milliseconds of load to settle, and a few milliseconds of warmup would time the ramp.
@@ -48,6 +54,8 @@ GEMM_KERNEL = {
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 WARMUP_SECONDS = 0.5
 QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
+DUAL_BYTES_PER_ELEM = 3.5  # two-operand quantizer: 2 B in, 2 x 0.75 B out
+BYTES_PER_ELEM = {"quant": QUANT_BYTES_PER_ELEM, "quant2": DUAL_BYTES_PER_ELEM, "copy": 2.0}
 METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
 
 
@@ -91,7 +99,7 @@ def _quantizers(recipe: str):
     return fmt, fn, r_y, r_dx, r_dw
 
 
-def dense_step(wl, tl: Timeline, recipe: str = "ufp4"):
+def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     m, s = wl.sign_mask, wl.seed
     fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
@@ -105,29 +113,45 @@ def dense_step(wl, tl: Timeline, recipe: str = "ufp4"):
     dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
     dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
 
-    def step(rec):
-        tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: Q(w, rht=r_y, sign_mask=m, out=q["w"]), rec)
+    def quant_dy(rec):
         tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
                                         out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: Q(w, transpose=True, rht=r_dx, sign_mask=m, out=q["wt"]), rec)
         tl.run("quant_dyt_sr", lambda: Q(dy, transpose=True, rht=r_dw, sign_mask=m, rounding=U.SR, seed=s,
                                          stream_id=1, out=q["dyt"]), rec)
+
+    def step_separate(rec):
+        tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: Q(w, rht=r_y, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_wt", lambda: Q(w, transpose=True, rht=r_dx, sign_mask=m, out=q["wt"]), rec)
         tl.run("quant_xt", lambda: Q(x, transpose=True, rht=r_dw, sign_mask=m, out=q["xt"]), rec)
+        quant_dy(rec)
+        gemms(rec)
+
+    def step_dual(rec):
+        tl.run("quant_x_xt", lambda: U.quantize_dual(x, fmt=fmt, rht_rows=r_y, rht_cols=r_dw, sign_mask_rows=m,
+                                                     sign_mask_cols=m, out_rows=q["x"], out_cols=q["xt"]), rec)
+        tl.run("quant_w_wt", lambda: U.quantize_dual(w, fmt=fmt, rht_rows=r_y, rht_cols=r_dx, sign_mask_rows=m,
+                                                     sign_mask_cols=m, out_rows=q["w"], out_cols=q["wt"]), rec)
+        quant_dy(rec)
+        gemms(rec)
+
+    def gemms(rec):
         tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y(q["x"], q["w"], out=y), rec)
         tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
         tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
 
-    kern = {
-        "quant_x": ("quant", M * K), "quant_w": ("quant", N * K), "quant_dy_sr": ("quant", M * N),
-        "quant_wt": ("quant", N * K), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
-        "gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
-        "gemm_bwd_dw": ("gemm", 2 * M * N * K),
-    }
-    return step, kern
+    kern = {"quant_dy_sr": ("quant", M * N), "quant_dyt_sr": ("quant", M * N)}
+    if dual:
+        kern.update({"quant_x_xt": ("quant2", M * K), "quant_w_wt": ("quant2", N * K)})
+    else:
+        kern.update({"quant_x": ("quant", M * K), "quant_w": ("quant", N * K), "quant_wt": ("quant", N * K),
+                     "quant_xt": ("quant", M * K)})
+    kern.update({"gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
+                 "gemm_bwd_dw": ("gemm", 2 * M * N * K)})
+    return (step_dual if dual else step_separate), kern
 
 
-def moe_step(wl, tl: Timeline, recipe: str = "ufp4"):
+def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     m, s = wl.sign_mask, wl.seed
     fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     E, N, K = wl.w.shape
@@ -146,11 +170,15 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4"):
 
     def step(rec):
         tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: Q(w2, rht=r_y, sign_mask=m, out=q["w"]), rec)
+        if dual:  # W^T's expert groups are N rows each (N % 16 == 0): no padding, the plain transposed operand
+            tl.run("quant_w_wt", lambda: U.quantize_dual(w2, fmt=fmt, rht_rows=r_y, rht_cols=r_dx, sign_mask_rows=m,
+                                                         sign_mask_cols=m, out_rows=q["w"], out_cols=q["wt"]), rec)
+        else:
+            tl.run("quant_w", lambda: Q(w2, rht=r_y, sign_mask=m, out=q["w"]), rec)
+            tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, fmt=fmt, rht=r_dx, sign_mask=m,
+                                                            out=q["wt"]), rec)
         tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
                                         out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, fmt=fmt, rht=r_dx, sign_mask=m,
-                                                        out=q["wt"]), rec)
         tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
                                                             rounding=U.SR, seed=s, stream_id=1, out=q["dyt"]), rec)
         tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
@@ -160,11 +188,15 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4"):
         tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw_grouped(q["dyt"], q["xt"], poff, out=dw), rec)
 
     flops = 2 * M * N * K
-    kern = {
-        "quant_x": ("quant", M * K), "quant_w": ("quant", E * N * K), "quant_dy_sr": ("quant", M * N),
-        "quant_wt": ("quant", E * N * K), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
+    kern = {"quant_x": ("quant", M * K)}
+    if dual:
+        kern["quant_w_wt"] = ("quant2", E * N * K)
+    else:
+        kern.update({"quant_w": ("quant", E * N * K), "quant_wt": ("quant", E * N * K)})
+    kern.update({
+        "quant_dy_sr": ("quant", M * N), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
         "gemm_fwd_y": ("gemm", flops), "gemm_bwd_dx": ("gemm", flops), "gemm_bwd_dw": ("gemm", flops),
-    }
+    })
     return step, kern
 
 
@@ -179,18 +211,36 @@ def copy1g_step(tl: Timeline):
     return step, {"copy": ("copy", t.numel() * t.element_size())}
 
 
-def quant1g_step(tl: Timeline, transpose: bool):
-    """The quantizer alone on a 1 GiB bf16 tensor, rowwise (reduction along its 16384 columns) or transposed
-    (operand X^T, reduction along its 32768 rows)."""
+def quant1g_step(tl: Timeline, mode: str):
+    """One quantizer on a 1 GiB bf16 tensor: rowwise (reduction along its 16384 columns), transposed (operand
+    X^T, reduction along its 32768 rows) or both operands in one pass. Returns (step, kernel table, plain step):
+    the plain step runs the same kernel without the RHT."""
     t = WL.quantizer_tensor().cuda()
     R, C = t.shape
-    q = U.empty_qtensor(C, R) if transpose else U.empty_qtensor(R, C)
-    label = "quant_cols_rtne" if transpose else "quant_rows_rtne"
+    if mode == "dual":
+        qr, qc = U.empty_qtensor(R, C), U.empty_qtensor(C, R)
+
+        def run(rht):
+            return U.quantize_dual(t, rht_rows=rht, rht_cols=rht, sign_mask_rows=0x6A09, sign_mask_cols=0x6A09,
+                                   out_rows=qr, out_cols=qc)
+
+        label, kind = "quant_dual_rtne", "quant2"
+    else:
+        transpose = mode == "cols"
+        q = U.empty_qtensor(C, R) if transpose else U.empty_qtensor(R, C)
+
+        def run(rht):
+            return U.rht_quantize(t, transpose=transpose, rht=rht, sign_mask=0x6A09, out=q)
+
+        label, kind = ("quant_cols_rtne" if transpose else "quant_rows_rtne"), "quant"
 
     def step(rec):
-        tl.run(label, lambda: U.rht_quantize(t, transpose=transpose, sign_mask=0x6A09, out=q), rec)
+        tl.run(label, lambda: run(True), rec)
 
-    return step, {label: ("quant", R * C)}
+    def plain(rec):
+        tl.run(label + "_plain", lambda: run(False), rec)
+
+    return step, {label: (kind, R * C)}, plain
 
 
 # ---------------------------------------------------------------------------------------------------
@@ -259,9 +309,13 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
     ap.add_argument("--workload", default="dense",
-                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "copy1g"])
+                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "quant1g-dual",
+                             "copy1g"])
     ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPES),
                     help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
+    ap.add_argument("--quant", default="dual", choices=["dual", "separate"],
+                    help="dual: X and W quantized to both operands in one pass (dY, SR, uses the single-output "
+                         "kernels, measured faster); separate: six single-output quantizations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -276,17 +330,18 @@ def main():
 
     tl = Timeline()
     wl = None
-    if args.workload in ("quant1g", "quant1g-t"):
-        transpose = args.workload == "quant1g-t"
-        step, kern = quant1g_step(tl, transpose)
-        wname = (f"standalone quantizer: 32768x16384 bf16 (1 GiB), {'transposed' if transpose else 'rowwise'} "
-                 f"RTNE with RHT")
+    plain = None
+    if args.workload in ("quant1g", "quant1g-t", "quant1g-dual"):
+        mode = {"quant1g": "rows", "quant1g-t": "cols", "quant1g-dual": "dual"}[args.workload]
+        step, kern, plain = quant1g_step(tl, mode)
+        what = {"rows": "rowwise", "cols": "transposed", "dual": "rowwise + transposed in one pass"}[mode]
+        wname = f"standalone quantizer: 32768x16384 bf16 (1 GiB), {what} RTNE with RHT"
     elif args.workload == "copy1g":
         step, kern = copy1g_step(tl)
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
-        step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe)
+        step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe, args.quant == "dual")
         wname = wl.name
     torch.cuda.synchronize()
 
@@ -311,6 +366,19 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = start.elapsed_time(end) / args.steps
+    context = None
+    if plain is not None:
+        # the same kernel without the RHT, timed after the measured steps (not part of `value`)
+        for _ in range(args.warmup):
+            plain(False)
+        for _ in range(args.steps):
+            plain(True)
+        torch.cuda.synchronize()
+        (label,) = kern
+        fused_us, plain_us = tl.mean_us(label), tl.mean_us(label + "_plain")
+        context = {"plain_quant_us": round(plain_us, 2), "fused_us": round(fused_us, 2),
+                   "fused_over_plain": round(fused_us / plain_us, 3),
+                   "paper": "fused / plain quantization latency ~1.06x (SM90), ~1.07x (SM100); Sec. 5 Q5"}
 
     breakdown = {}
     gemm_flops = 0
@@ -321,17 +389,17 @@ def main():
             gbps = 2 * work / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += 2 * work
-        elif kind == "quant":
-            gbps = work * QUANT_BYTES_PER_ELEM / (us * 1e-6) / 1e9
+        elif kind in ("quant", "quant2"):
+            gbps = work * BYTES_PER_ELEM[kind] / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
-            quant_bytes += work * QUANT_BYTES_PER_ELEM
+            quant_bytes += work * BYTES_PER_ELEM[kind]
         else:
             tf = work / (us * 1e-6) / 1e12
             breakdown[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_int8": round(tf / INT8_PEAK_TOPS, 4)}
             gemm_flops += work
 
     gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
-    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "copy")]
+    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "quant2", "copy")]
     if gemm_labels:
         value = gemm_flops / (ms_per_step * 1e-3) / 1e12
         unit = "TFLOP/s"
@@ -349,9 +417,10 @@ def main():
         unit = "GB/s"
         label = quant_labels[0]
         us = tl.mean_us(label)
-        per_launch = kern[label][1] * (QUANT_BYTES_PER_ELEM if kern[label][0] == "quant" else 2)
+        per_launch = kern[label][1] * BYTES_PER_ELEM[kern[label][0]]
         ach = per_launch / (us * 1e-6) / 1e9
-        kname = {"quant_rows_rtne": "quant_rows_kernel", "quant_cols_rtne": "quant_cols_kernel"}.get(label, "copy")
+        kname = {"quant_rows_rtne": "quant_rows_kernel", "quant_cols_rtne": "quant_cols_kernel",
+                 "quant_dual_rtne": "quant_dual_kernel"}.get(label, "copy")
         roof = {"bound": "hbm", "kernel": kname, "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic("quant", wname) if kname != "copy" else None}
@@ -378,6 +447,10 @@ def main():
         "roofline": roof,
         "breakdown": breakdown,
     }
+    if context is not None:
+        out["rht_cost"] = context
+    if wl is not None:
+        out["config"]["quant"] = args.quant
     if wl is not None and not args.no_cpu_baseline and not wl.grouped:
         out["cpu_baseline"] = cpu_baseline(wl, recipe=args.recipe)
     print(json.dumps(out), flush=True)

@@ -123,6 +123,28 @@ int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t
                             float *scales_dev, int64_t scale_panel_ld, void *stream);
 
 /*
+ * ufp4_quantize_dual -- both quantized operands of one tensor from a single read of it (either grid):
+ * Q_r = Q(X H') [rows, cols] along cols (transpose 0) and Q_c = Q(X^T H') [cols, rows] along rows
+ * (transpose 1), as the fused RHT + quantize of Sec. 2.2 needs them for the two GEMMs a training step runs
+ * on X (fwd_y and bwd_dw for X; bwd_dx and bwd_dw for dY; fwd_y and bwd_dx for W). Each output has its own
+ * RHT flag, sign mask and SR stream; the results equal, bit for bit, ufp4_rht_quantize /
+ * ufp4_e2m1_quantize called with transpose 0 and 1 and those arguments. The input is read from HBM once
+ * (2 bytes per element instead of 4).
+ *
+ *   format             UFP4_FMT_UNIFORM or UFP4_FMT_E2M1.
+ *   x_dev              bf16 [rows, cols], leading dimension ld; rows % 16 == 0 and cols % 16 == 0.
+ *   rht_rows, sign_mask_rows, stream_rows   RHT and SR stream of Q_r; *_cols the same for Q_c.
+ *   rounding, seed     as ufp4_rht_quantize, for both outputs.
+ *   codes_r_dev ... scale_panel_ld_r   Q_r in the panel layout (reduction cols); *_c: Q_c (reduction rows).
+ * The two outputs must not overlap each other or the input.
+ */
+int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int rht_rows,
+                       uint32_t sign_mask_rows, uint32_t stream_rows, int rht_cols, uint32_t sign_mask_cols,
+                       uint32_t stream_cols, int rounding, uint64_t seed, void *codes_r_dev, int64_t code_panel_ld_r,
+                       float *scales_r_dev, int64_t scale_panel_ld_r, void *codes_c_dev, int64_t code_panel_ld_c,
+                       float *scales_c_dev, int64_t scale_panel_ld_c, void *stream);
+
+/*
  * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that
  * share their reduction axis (the axis the RHT was applied along):
  *

@@ -214,6 +214,47 @@ int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t
     return status_of(launch_quantize(j, static_cast<hipStream_t>(stream)));
 }
 
+int ufp4_quantize_dual(int format, const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int rht_rows,
+                       uint32_t sign_mask_rows, uint32_t stream_rows, int rht_cols, uint32_t sign_mask_cols,
+                       uint32_t stream_cols, int rounding, uint64_t seed, void* codes_r_dev, int64_t code_panel_ld_r,
+                       float* scales_r_dev, int64_t scale_panel_ld_r, void* codes_c_dev, int64_t code_panel_ld_c,
+                       float* scales_c_dev, int64_t scale_panel_ld_c, void* stream) {
+    // Q_r = X [rows, cols] along cols; Q_c = X^T [cols, rows] along rows
+    int st = check_quant_common(format, x_dev, rows, cols, ld, rht_rows, sign_mask_rows, rounding, codes_r_dev,
+                                code_panel_ld_r, scales_r_dev, scale_panel_ld_r, cols, rows);
+    if (st == UFP4_OK)
+        st = check_quant_common(format, x_dev, rows, cols, ld, rht_cols, sign_mask_cols, rounding, codes_c_dev,
+                                code_panel_ld_c, scales_c_dev, scale_panel_ld_c, rows, cols);
+    if (st != UFP4_OK) return st;
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    // grid: x over 64-column tiles of the padded columns, y over 32 groups of 16 rows (grid-stride beyond)
+    if (padded_rows(cols) / 64 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    DualJob j{};
+    j.format = format;
+    j.rounding = rounding;
+    j.rht_r = rht_rows;
+    j.rht_c = rht_cols;
+    j.x = x_dev;
+    j.rows = rows;
+    j.cols = cols;
+    j.ld = ld;
+    fill_sign_xor(sign_mask_rows, j.qr.sign_xor);
+    fill_sign_xor(sign_mask_cols, j.qc.sign_xor);
+    j.qr.key0 = j.qc.key0 = (uint32_t)seed;
+    j.qr.key1 = j.qc.key1 = (uint32_t)(seed >> 32);
+    j.qr.stream = stream_rows;
+    j.qc.stream = stream_cols;
+    j.codes_r = codes_r_dev;
+    j.code_pld_r = code_panel_ld_r;
+    j.scales_r = scales_r_dev;
+    j.scale_pld_r = scale_panel_ld_r;
+    j.codes_c = codes_c_dev;
+    j.code_pld_c = code_panel_ld_c;
+    j.scales_c = scales_c_dev;
+    j.scale_pld_c = scale_panel_ld_c;
+    return status_of(launch_quantize_dual(j, static_cast<hipStream_t>(stream)));
+}
+
 int ufp4_gemm_fwd_y(const void* x_codes_dev, int64_t x_code_panel_ld, const float* x_scales_dev, int64_t x_scale_panel_ld,
                     const void* w_codes_dev, int64_t w_code_panel_ld, const float* w_scales_dev, int64_t w_scale_panel_ld,
                     int64_t M, int64_t N, int64_t K, int format, void* y_dev, int64_t ldc, int out_dtype,

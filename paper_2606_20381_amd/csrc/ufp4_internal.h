@@ -44,6 +44,25 @@ struct QuantJob {
 hipError_t launch_quantize(const QuantJob& job, hipStream_t stream);
 int max_groups_quantize();
 
+// Both quantized operands of one tensor X [rows, cols] (rows, cols multiples of 16) from one read: Q_r = X
+// along cols ([rows, cols]) and Q_c = X^T along rows ([cols, rows]). Already validated.
+struct DualJob {
+    int format, rounding, rht_r, rht_c;
+    const void* x;
+    int64_t rows, cols, ld;
+    QuantArgs qr, qc;  // sign masks and SR streams of Q_r and Q_c (same key)
+    void* codes_r;
+    int64_t code_pld_r;
+    float* scales_r;
+    int64_t scale_pld_r;
+    void* codes_c;
+    int64_t code_pld_c;
+    float* scales_c;
+    int64_t scale_pld_c;
+};
+
+hipError_t launch_quantize_dual(const DualJob& job, hipStream_t stream);
+
 // Block-scaled NT GEMM: C[i, j] = sum_b sA[i,b] sB[j,b] sum_{k in b} A[i,k] B[j,k] over `nkb` 16-blocks.
 enum GemmMode { kGemmDense = 0, kGemmRaggedM = 1, kGemmRaggedK = 2 };
 

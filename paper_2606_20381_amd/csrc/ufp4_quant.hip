@@ -10,9 +10,10 @@
 // These identities hold while y and s are normal fp32 numbers, the supported input domain.
 //
 // Two input layouts: rowwise (reduction axis contiguous, one thread per block, 32-byte loads) and
-// transposed (reduction axis strided: a 128x64 tile is staged through LDS, each thread builds two column
-// blocks from LDS). The transposed kernel also serves grouped (MoE) tensors whose token axis is cut into
-// groups that are zero-padded to a multiple of 16.
+// transposed (reduction axis strided: each thread loads a 16-row x 8-column sub-tile and builds its eight
+// column blocks in registers). The transposed kernel also serves grouped (MoE) tensors whose token axis is
+// cut into groups that are zero-padded to a multiple of 16. A third kernel produces both operands of one
+// tensor (rowwise and transposed) from a single read of it.
 //
 // Output layout (panels): the quantized operand's rows are cut into panels of 128; within a panel, block b
 // of all 128 rows is stored contiguously (codes: 128 x 8 bytes at b * 1024; scales: 128 floats at b * 128).
@@ -266,6 +267,18 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restr
 // 4 columns per thread performs within a few percent of 8; an LDS-transposed 128 x 64 tile was 12-20%
 // slower.)
 // ------------------------------------------------------------------------------------------------
+// One row's kXC consecutive bf16 (kXC / 2 dwords) with a single 16- or 8-byte load.
+template <int C>
+__device__ __forceinline__ void load_row_chunk(const uint16_t* src, uint32_t (&d)[C / 2]) {
+    if constexpr (C == 8) {
+        const uint4 l = *reinterpret_cast<const uint4*>(src);
+        d[0] = l.x; d[1] = l.y; d[2] = l.z; d[3] = l.w;
+    } else {
+        const uint2 l = *reinterpret_cast<const uint2*>(src);
+        d[0] = l.x; d[1] = l.y;
+    }
+}
+
 constexpr int kXC = 8;                     // columns (operand rows) per thread
 constexpr int kMaxGroupsLds = 1024;
 
@@ -325,27 +338,28 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         if (src0 < 0 || nvalid < 0) nvalid = 0;
 
         uint32_t v[kBlock][kW];
+        if (ncol == kXC && nvalid == kBlock) {  // the common case: a full 16 x kXC sub-tile, no per-row tests
 #pragma unroll
-        for (int j = 0; j < kBlock; ++j) {
+            for (int j = 0; j < kBlock; ++j) load_row_chunk<kXC>(x + (src0 + j) * ld + cbase, v[j]);
+        } else {
 #pragma unroll
-            for (int k = 0; k < kW; ++k) v[j][k] = 0;
-            if (j < nvalid) {
-                const uint16_t* src = x + (src0 + j) * ld + cbase;
-                if (ncol == kXC) {
-                    if constexpr (kXC == 8) {
-                        const uint4 l = *reinterpret_cast<const uint4*>(src);
-                        v[j][0] = l.x; v[j][1] = l.y; v[j][2] = l.z; v[j][3] = l.w;
-                    } else {
-                        const uint2 l = *reinterpret_cast<const uint2*>(src);
-                        v[j][0] = l.x; v[j][1] = l.y;
+            for (int j = 0; j < kBlock; ++j) {
+#pragma unroll
+                for (int k = 0; k < kW; ++k) v[j][k] = 0;
+                if (j < nvalid) {
+                    const uint16_t* src = x + (src0 + j) * ld + cbase;
+                    if (ncol == kXC) {
+                        load_row_chunk<kXC>(src, v[j]);
+                    } else if (ncol > 0) {  // ragged last columns: no read past column cols - 1
+#pragma unroll
+                        for (int k = 0; k < kXC; ++k)
+                            if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
                     }
-                } else if (ncol > 0) {  // ragged last columns: no read past column cols - 1
-#pragma unroll
-                    for (int k = 0; k < kXC; ++k)
-                        if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
                 }
             }
         }
+        // Columns past `cols` and rows past a group's tokens hold zeros: such a block quantizes to zero codes
+        // and a +0 scale, the padding value, so every block is quantized unconditionally.
         uint32_t clo[kXC], chi[kXC];
         float sc[kXC];
 #pragma unroll
@@ -354,9 +368,7 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
             uint32_t w[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
-            clo[q] = chi[q] = 0;
-            sc[q] = 0.0f;
-            if (q < ncol) quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+            quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
         }
         const int64_t P = cbase >> 7, ri = cbase & 127;  // the kXC rows lie in one panel
         uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + ri * 8);
@@ -365,6 +377,107 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         float4* ds = reinterpret_cast<float4*>(scales + P * scale_pld + gb * 128 + ri);
 #pragma unroll
         for (int q = 0; q < kXC / 4; ++q) ds[q] = make_float4(sc[4 * q], sc[4 * q + 1], sc[4 * q + 2], sc[4 * q + 3]);
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Both operands of one tensor X [rows, cols] from one read of X: Q_r = Q(X) along cols (rowwise) and
+// Q_c = Q(X^T) along rows (transposed), each with its own RHT flag, sign mask and SR stream; bit for bit the
+// results of the two separate kernels. rows and cols are multiples of 16.
+//
+// The lanes l and l + 32 of a wave form a pair that owns a 16 x 16 sub-tile: rows 16 gb .. 16 gb + 15,
+// columns col0 .. col0 + 15; lane l loads columns col0 .. col0 + 7 of all 16 rows, lane l + 32 the other
+// eight. Each lane first quantizes its eight column blocks as the transposed kernel does. One
+// v_permlane32_swap per dword then exchanges half of the sub-tile between the two lanes (lanes 0-31 give up
+// rows 8-15 and receive columns 8-15 of rows 0-7, lanes 32-63 the converse), after which registers v[i]
+// and v[8 + i] hold row 8h + i's full 16-column block in both lanes (h = l / 32). Each lane then quantizes
+// eight row blocks and writes them as 64 contiguous bytes (eight consecutive rows of one block).
+// Zero codes and scales fill the padding rows of both operands' last panels.
+// ------------------------------------------------------------------------------------------------
+template <int FMT, int ROUND, bool RHT_R, bool RHT_C>
+__global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                         int64_t ld, QuantArgs qr, QuantArgs qc,
+                                                         uint8_t* __restrict__ codes_r, int64_t code_pld_r,
+                                                         float* __restrict__ scales_r, int64_t scale_pld_r,
+                                                         uint8_t* __restrict__ codes_c, int64_t code_pld_c,
+                                                         float* __restrict__ scales_c, int64_t scale_pld_c) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int h = lane >> 5, chunk = lane & 3, rbl = (lane >> 2) & 7;
+    const int64_t col0 = (int64_t)blockIdx.x * 64 + chunk * 16;  // first column of the pair's sub-tile
+    const int64_t cbase = col0 + h * 8;                          // first column of this lane
+    const bool chunk_ok = col0 < cols;  // cols % 16 == 0: the 16 columns are all real or all padding
+    const int64_t nblk = rows / kBlock;                 // reduction blocks of Q_c = 16-row groups of X
+    const int64_t ngrp = padded_rows(rows) / kBlock;    // 16-row groups including Q_r's padding rows
+
+    for (int64_t gb = (int64_t)blockIdx.y * 32 + wave * 8 + rbl; gb < ngrp; gb += (int64_t)gridDim.y * 32) {
+        const int64_t r0 = gb * kBlock + h * 8;  // first Q_r row of this lane
+        const int64_t Pr = r0 >> 7, rir = r0 & 127;
+        const int64_t bcol = col0 / kBlock;
+        if (gb >= nblk) {  // padding rows of Q_r only
+            if (chunk_ok) {
+                uint4* dc = reinterpret_cast<uint4*>(codes_r + Pr * code_pld_r + bcol * 1024 + rir * 8);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) dc[q] = make_uint4(0, 0, 0, 0);
+                float4* ds = reinterpret_cast<float4*>(scales_r + Pr * scale_pld_r + bcol * 128 + rir);
+                ds[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+                ds[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            continue;
+        }
+        uint32_t v[kBlock][4];
+        if (chunk_ok) {
+#pragma unroll
+            for (int j = 0; j < kBlock; ++j) load_row_chunk<8>(x + (gb * kBlock + j) * ld + cbase, v[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < kBlock; ++j) v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0;
+        }
+        // Q_c: the eight column blocks of this lane (operand rows cbase .. cbase + 7). Past `cols` the data is
+        // zero, which quantizes to the padding value (zero codes, +0 scale).
+        {
+            uint32_t clo[8], chi[8];
+            float sc[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+                uint32_t w[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
+                quant_block16<FMT, ROUND, RHT_C>(w, qc, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+            }
+            const int64_t P = cbase >> 7, ri = cbase & 127;
+            uint4* dc = reinterpret_cast<uint4*>(codes_c + P * code_pld_c + gb * 1024 + ri * 8);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) dc[q] = make_uint4(clo[2 * q], chi[2 * q], clo[2 * q + 1], chi[2 * q + 1]);
+            float4* ds = reinterpret_cast<float4*>(scales_c + P * scale_pld_c + gb * 128 + ri);
+            ds[0] = make_float4(sc[0], sc[1], sc[2], sc[3]);
+            ds[1] = make_float4(sc[4], sc[5], sc[6], sc[7]);
+        }
+        if (!chunk_ok) continue;  // no Q_r block for padding columns (the partner lane takes the same branch)
+        __builtin_amdgcn_sched_barrier(0);  // keep the two phases apart: their temporaries would add up
+        // exchange: afterwards v[i] = columns 0-7 and v[8 + i] = columns 8-15 of row 8h + i
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const auto r = __builtin_amdgcn_permlane32_swap(v[i][k], v[8 + i][k], false, false);
+                v[i][k] = r[0];
+                v[8 + i][k] = r[1];
+            }
+        }
+        uint32_t rlo[8], rhi[8];
+        float rs[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t w[8] = {v[i][0], v[i][1], v[i][2], v[i][3], v[8 + i][0], v[8 + i][1], v[8 + i][2], v[8 + i][3]};
+            quant_block16<FMT, ROUND, RHT_R>(w, qr, (uint32_t)bcol, (uint32_t)(r0 + i), rlo[i], rhi[i], rs[i]);
+        }
+        uint4* dc = reinterpret_cast<uint4*>(codes_r + Pr * code_pld_r + bcol * 1024 + rir * 8);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dc[q] = make_uint4(rlo[2 * q], rhi[2 * q], rlo[2 * q + 1], rhi[2 * q + 1]);
+        float4* ds = reinterpret_cast<float4*>(scales_r + Pr * scale_pld_r + bcol * 128 + rir);
+        ds[0] = make_float4(rs[0], rs[1], rs[2], rs[3]);
+        ds[1] = make_float4(rs[4], rs[5], rs[6], rs[7]);
     }
 }
 
@@ -414,6 +527,34 @@ static hipError_t dispatch_fmt(const QuantJob& j, hipStream_t s) {
 
 hipError_t launch_quantize(const QuantJob& j, hipStream_t s) {
     return j.format == kFmtE2M1 ? dispatch_fmt<kFmtE2M1>(j, s) : dispatch_fmt<kFmtUniform>(j, s);
+}
+
+template <int FMT, int ROUND, bool RHT_R, bool RHT_C>
+static hipError_t launch_dual_t(const DualJob& j, hipStream_t s) {
+    const int64_t gx = padded_rows(j.cols) / 64;
+    const int64_t gy = (padded_rows(j.rows) / kBlock + 31) / 32;
+    if (gx == 0 || gy == 0) return hipSuccess;
+    const dim3 grid((unsigned)gx, (unsigned)(gy < 65535 ? gy : 65535));
+    quant_dual_kernel<FMT, ROUND, RHT_R, RHT_C><<<grid, 256, 0, s>>>(
+        static_cast<const uint16_t*>(j.x), j.rows, j.cols, j.ld, j.qr, j.qc, static_cast<uint8_t*>(j.codes_r),
+        j.code_pld_r, j.scales_r, j.scale_pld_r, static_cast<uint8_t*>(j.codes_c), j.code_pld_c, j.scales_c,
+        j.scale_pld_c);
+    return hipGetLastError();
+}
+
+template <int FMT, int ROUND>
+static hipError_t dispatch_dual_rht(const DualJob& j, hipStream_t s) {
+    if (j.rht_r) return j.rht_c ? launch_dual_t<FMT, ROUND, true, true>(j, s) : launch_dual_t<FMT, ROUND, true, false>(j, s);
+    return j.rht_c ? launch_dual_t<FMT, ROUND, false, true>(j, s) : launch_dual_t<FMT, ROUND, false, false>(j, s);
+}
+
+template <int FMT>
+static hipError_t dispatch_dual_fmt(const DualJob& j, hipStream_t s) {
+    return j.rounding == kRoundSR ? dispatch_dual_rht<FMT, kRoundSR>(j, s) : dispatch_dual_rht<FMT, kRoundRTNE>(j, s);
+}
+
+hipError_t launch_quantize_dual(const DualJob& j, hipStream_t s) {
+    return j.format == kFmtE2M1 ? dispatch_dual_fmt<kFmtE2M1>(j, s) : dispatch_dual_fmt<kFmtUniform>(j, s);
 }
 
 int max_groups_quantize() { return kMaxGroupsLds; }

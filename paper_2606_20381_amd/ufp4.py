@@ -38,6 +38,8 @@ SIGNATURES = {
     "ufp4_e2m1_quantize": (_QUANT_ARGS, _INT),
     "ufp4_quantize_grouped_t": ([_INT, _P, _I64, _I64, _I64, _P, _P, _I32, _I64, _INT, _U32, _INT, _U64, _U32, _P,
                                  _I64, _P, _I64, _P], _INT),
+    "ufp4_quantize_dual": ([_INT, _P, _I64, _I64, _I64, _INT, _U32, _U32, _INT, _U32, _U32, _INT, _U64, _P, _I64, _P,
+                            _I64, _P, _I64, _P, _I64, _P], _INT),
     "ufp4_gemm_fwd_y": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dx": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dw": (_GEMM_ARGS, _INT),
@@ -163,6 +165,26 @@ def e2m1_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = False
                   rounding: int = RTNE, seed: int = 0, stream_id: int = 0, out: QTensor | None = None) -> QTensor:
     """Fused (optional) RHT + E2M1 quantization (ufp4_e2m1_quantize), the comparison baseline."""
     return _quantize_call("ufp4_e2m1_quantize", E2M1, x, transpose, rht, sign_mask, rounding, seed, stream_id, out)
+
+
+def quantize_dual(x: torch.Tensor, *, fmt: int = UNIFORM, rht_rows: bool = True, rht_cols: bool = True,
+                  sign_mask_rows: int = 0, sign_mask_cols: int = 0, rounding: int = RTNE, seed: int = 0,
+                  stream_rows: int = 0, stream_cols: int = 0, out_rows: QTensor | None = None,
+                  out_cols: QTensor | None = None) -> tuple[QTensor, QTensor]:
+    """Both operands of x [rows, cols] from one read (ufp4_quantize_dual): (Q_r [rows, cols] along cols,
+    Q_c [cols, rows] along rows)."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    qr = out_rows if out_rows is not None else empty_qtensor(rows, cols, fmt, x.device)
+    qc = out_cols if out_cols is not None else empty_qtensor(cols, rows, fmt, x.device)
+    st = lib().ufp4_quantize_dual(fmt, x.data_ptr(), rows, cols, x.stride(0), int(rht_rows), sign_mask_rows,
+                                  stream_rows, int(rht_cols), sign_mask_cols, stream_cols, rounding,
+                                  seed & 0xFFFFFFFFFFFFFFFF, qr.codes.data_ptr(), qr.code_panel_ld,
+                                  qr.scales.data_ptr(), qr.scale_panel_ld, qc.codes.data_ptr(), qc.code_panel_ld,
+                                  qc.scales.data_ptr(), qc.scale_panel_ld, _stream())
+    _check(st, "ufp4_quantize_dual")
+    return qr, qc
 
 
 def group_offsets(counts, device="cuda"):

@@ -107,6 +107,37 @@ def test_gemm_validation_per_pass_layout(lib):
     assert lib.ufp4_gemm_bwd_dw(FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 24, 16, 16, 0, FAKE, 16, 0, None) == 2
 
 
+def _dual_args(rows=32, cols=48, ld=48, fmt=0, rht_r=1, mask_r=0, rht_c=1, mask_c=0, rnd=0, x=FAKE, cr=FAKE,
+               cr_ld=3 * 1024, sr=FAKE, sr_ld=3 * 128, cc=FAKE, cc_ld=2 * 1024, sc=FAKE, sc_ld=2 * 128):
+    # (fmt, x, rows, cols, ld, rht_r, mask_r, stream_r, rht_c, mask_c, stream_c, rounding, seed,
+    #  codes_r, code_panel_ld_r, scales_r, scale_panel_ld_r, codes_c, ..., stream)
+    return (fmt, x, rows, cols, ld, rht_r, mask_r, 0, rht_c, mask_c, 1, rnd, 0, cr, cr_ld, sr, sr_ld, cc, cc_ld, sc,
+            sc_ld, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), 1),                          # null input
+    (dict(cc=None), 1),                         # null transposed codes
+    (dict(fmt=2), 1),                           # format enum
+    (dict(rnd=2), 1),                           # rounding enum
+    (dict(rht_c=3), 1),                         # rht flag
+    (dict(mask_r=0x10000), 1),                  # sign mask > 16 bits
+    (dict(rows=-16), 1),                        # negative size
+    (dict(rows=24), 2),                         # rows % 16 (the transposed output's reduction)
+    (dict(cols=40, ld=40), 2),                  # cols % 16 (the rowwise output's reduction)
+    (dict(ld=40), 2),                           # ld < cols
+    (dict(ld=52), 2),                           # ld % 8
+    (dict(cr_ld=2 * 1024), 2),                  # rowwise code panel stride < 1024 cols/16
+    (dict(sc_ld=128), 2),                       # transposed scale panel stride < 128 rows/16
+    (dict(cc_ld=2 * 1024 + 8), 3),              # panel stride % 16
+    (dict(x=FAKE + 2), 3),                      # input alignment
+    (dict(sr=FAKE + 4), 3),                     # scales alignment
+    (dict(cc_ld=1 << 30), 5),                   # panel stride > 2^29
+])
+def test_dual_validation(lib, kw, status):
+    assert lib.ufp4_quantize_dual(*_dual_args(**kw)) == status
+
+
 def test_grouped_validation(lib):
     # null offsets
     assert lib.ufp4_quantize_grouped_t(0, FAKE, 32, 16, 16, None, FAKE, 2, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
