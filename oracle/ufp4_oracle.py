@@ -439,10 +439,126 @@ def gemm_nt_grouped(a_idx, a_scales, b_idx, b_scales, fmt: int, a_rows=None, b_r
 # One linear layer's three quantized GEMMs under a recipe (Sec. 4, Table 1; Sec. 2.2 closing sentence)
 # ---------------------------------------------------------------------------------------------------
 
+# ---------------------------------------------------------------------------------------------------
+# The uniform grid with power-of-two block scales (Sec. 4: the scale hierarchy is orthogonal to the grid
+# and may follow the hardware). Quantization blocks of 32 along the reduction axis share one scale 2^E,
+# stored as an E8M0 byte E + 127; the RHT stays block-16 (two RHT blocks per scale block) and the codes are
+# the uniform levels -7..7, stored as FP6 E2M3 numbers (every integer up to 7 is exact in E2M3).
+# ---------------------------------------------------------------------------------------------------
+
+MX_BLOCK = 32
+E8M0_BIAS = 127
+
+
+def mx_scale_exponent(amax) -> np.ndarray:
+    """Per block, the smallest integer E with amax <= 7 * 2^E: the power-of-two scale that keeps every
+    |y / 2^E| within the top level 7 (no clipping). amax = 0 gives E = -127 (E8M0 byte 0); a zero block's
+    codes are all 0 whatever the scale."""
+    a = np.asarray(amax, dtype=np.float64)
+    m, e = np.frexp(a)  # a = m * 2^e with 0.5 <= m < 1; 7 * 2^E >= a  <=>  2^(E - e) >= m / 7
+    E = np.where(m <= 0.875, e - 3, e - 2)  # m / 7 <= 1/8  <=>  m <= 7/8
+    return np.where(a > 0, E, -E8M0_BIAS).astype(np.int64)
+
+
+def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int = 0, seed: int = 0,
+                     stream: int = 0, row_ids=None):
+    """Quantize an operand A [rows, red] (red % 32 == 0) along its contiguous axis with power-of-two scales.
+
+    Per 1x32 block: y = RHT16(x) on each half (or x); E = mx_scale_exponent(amax |y|); v = y * 2^-E (exact);
+    codes -7..7 by RTNE or SR with the draws of the two 16-blocks it contains (the SR counters number
+    16-blocks, as in `quantize_rows`). Returns (signed codes int64 [rows, red], E8M0 bytes uint8
+    [rows, red/32]).
+    """
+    a = np.asarray(a_f32, dtype=np.float32)
+    rows, red = a.shape
+    if red % MX_BLOCK:
+        raise ValueError("reduction length must be a multiple of 32")
+    n16, n32 = red // BLOCK, red // MX_BLOCK
+    y16 = a.reshape(rows, n16, BLOCK)
+    y16 = rht_blocks(y16, sign_mask) if rht else y16.copy()
+    if not np.all(np.isfinite(y16)):
+        raise ValueError("non-finite value after the transform")
+    y = y16.reshape(rows, n32, MX_BLOCK)
+    amax = np.abs(y).max(axis=-1)
+    _check_block_domain(amax, 7.0)
+    E = mx_scale_exponent(amax)
+    v = y.astype(np.float64) * np.ldexp(1.0, -E)[..., None]  # a power of two: exact
+    if rounding == RTNE:
+        idx = round_nearest_even(v, UNIFORM)
+    elif rounding == SR:
+        rid = np.arange(rows) if row_ids is None else np.asarray(row_ids)
+        u = sr_draws(np.arange(n16)[None, :], rid[:, None], seed, stream).reshape(rows, n32, MX_BLOCK)
+        idx = round_stochastic(v, u, UNIFORM)
+    else:
+        raise ValueError("unknown rounding mode")
+    return idx.reshape(rows, red), (E + E8M0_BIAS).astype(np.uint8)
+
+
+def e2m3_value(bits) -> np.ndarray:
+    """Value of a 6-bit FP6 E2M3 pattern (OCP MX formats): sign, 2 exponent bits (bias 1), 3 mantissa bits;
+    exponent 0 is subnormal (m/8)."""
+    b = np.asarray(bits, dtype=np.int64)
+    s, e, m = (b >> 5) & 1, (b >> 3) & 3, b & 7
+    mag = np.where(e == 0, m / 8.0, np.ldexp(1.0 + m / 8.0, e - 1))
+    return np.where(s == 1, -mag, mag)
+
+
+_E2M3_OF_INT = {int(e2m3_value(b)): b for b in range(32) if float(e2m3_value(b)).is_integer()}
+
+
+def e2m3_codes(idx: np.ndarray) -> np.ndarray:
+    """Signed integer codes -7..7 -> their E2M3 bit patterns (zero as +0), by search over the format."""
+    idx = np.asarray(idx, dtype=np.int64)
+    mag = np.vectorize(lambda k: _E2M3_OF_INT[int(k)])(np.abs(idx)) if idx.size else np.zeros(idx.shape, np.int64)
+    return np.where(idx < 0, mag | 0x20, mag).astype(np.int64)
+
+
+def pack_fp6(idx: np.ndarray) -> np.ndarray:
+    """[rows, red] codes -> uint8 [rows, red * 3 / 4]: each 32-block as 24 bytes, element j of the block in
+    bits 6j .. 6j + 5 of its little-endian 192-bit string (the operand layout of the scaled f8f6f4 MFMA)."""
+    c = e2m3_codes(idx)
+    rows, red = c.shape
+    blocks = c.reshape(rows, red // MX_BLOCK, MX_BLOCK)
+    out = np.zeros((rows, red // MX_BLOCK, 24), dtype=np.uint8)
+    for j in range(MX_BLOCK):
+        for bit in range(6):
+            pos = 6 * j + bit
+            out[..., pos // 8] |= (((blocks[..., j] >> bit) & 1) << (pos % 8)).astype(np.uint8)
+    return out.reshape(rows, red // MX_BLOCK * 24)
+
+
+def unpack_fp6(packed: np.ndarray) -> np.ndarray:
+    """Inverse of pack_fp6: signed integer codes."""
+    p = np.asarray(packed, dtype=np.uint8)
+    rows, nbytes = p.shape
+    blocks = p.reshape(rows, nbytes // 24, 24).astype(np.int64)
+    bits = np.zeros((rows, nbytes // 24, MX_BLOCK), dtype=np.int64)
+    for j in range(MX_BLOCK):
+        for bit in range(6):
+            pos = 6 * j + bit
+            bits[..., j] |= ((blocks[..., pos // 8] >> (pos % 8)) & 1) << bit
+    return e2m3_value(bits).astype(np.int64).reshape(rows, nbytes // 24 * MX_BLOCK)
+
+
+def dequantize_mx(idx: np.ndarray, e8m0: np.ndarray) -> np.ndarray:
+    """Codes and E8M0 block scales -> fp64 values k * 2^(e8m0 - 127)."""
+    idx = np.asarray(idx, dtype=np.float64)
+    rows, red = idx.shape
+    sc = np.ldexp(1.0, np.asarray(e8m0, dtype=np.int64) - E8M0_BIAS)
+    return (idx.reshape(rows, red // MX_BLOCK, MX_BLOCK) * sc[..., None]).reshape(rows, red)
+
+
+def gemm_nt_mx(a_idx, a_e8m0, b_idx, b_e8m0) -> np.ndarray:
+    """C = deq(A) @ deq(B)^T in fp64 for operands with power-of-two block scales."""
+    return dequantize_mx(a_idx, a_e8m0) @ dequantize_mx(b_idx, b_e8m0).T
+
+
 RECIPES = {
     # format, RHT on (fwd_y, bwd_dx, bwd_dw), SR on dY only (Table 1)
     "ufp4": dict(fmt=UNIFORM, rht=(True, True, True)),
     "e2m1": dict(fmt=E2M1, rht=(False, False, True)),
+    # the UFP4 recipe with 1x32 power-of-two (E8M0) scales instead of 1x16 fp32 scales
+    "mxufp4": dict(fmt=UNIFORM, rht=(True, True, True), scales="e8m0x32"),
 }
 
 
@@ -459,6 +575,17 @@ def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 
     fmt = cfg["fmt"]
     r_y, r_dx, r_dw = cfg["rht"]
     q = {}
+    if cfg.get("scales") == "e8m0x32":
+        Q = quantize_rows_mx
+        q["x"] = Q(operand_rowwise(x_bits), RTNE, r_y, sign_mask)
+        q["w"] = Q(operand_rowwise(w_bits), RTNE, r_y, sign_mask)
+        q["dy"] = Q(operand_rowwise(dy_bits), SR, r_dx, sign_mask, seed, 0)
+        q["wt"] = Q(operand_colwise(w_bits), RTNE, r_dx, sign_mask)
+        q["dyt"] = Q(operand_colwise(dy_bits), SR, r_dw, sign_mask, seed, 1)
+        q["xt"] = Q(operand_colwise(x_bits), RTNE, r_dw, sign_mask)
+        out = {"y": gemm_nt_mx(*q["x"], *q["w"]), "dx": gemm_nt_mx(*q["dy"], *q["wt"]),
+               "dw": gemm_nt_mx(*q["dyt"], *q["xt"])}
+        return q, out
     q["x"] = quantize_rows(operand_rowwise(x_bits), fmt, RTNE, r_y, sign_mask)
     q["w"] = quantize_rows(operand_rowwise(w_bits), fmt, RTNE, r_y, sign_mask)
     q["dy"] = quantize_rows(operand_rowwise(dy_bits), fmt, SR, r_dx, sign_mask, seed, 0)

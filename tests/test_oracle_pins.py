@@ -549,3 +549,124 @@ def test_diagnostics_closed_forms():
     idx = np.array([[0, 1, 2, 3, 4, 5, 6, 7]])
     assert O.effective_bucket_ratio(idx, O.UNIFORM) == pytest.approx(1.0, abs=1e-9)
     assert O.effective_bucket_ratio(np.zeros((1, 8), np.int64), O.UNIFORM) == pytest.approx(1 / 8, abs=1e-9)
+
+
+# ------------------------------------------------------------------------------------------------
+# Uniform grid with power-of-two block scales (Sec. 4: scale hierarchy chosen for the hardware)
+# ------------------------------------------------------------------------------------------------
+
+def test_mx_scale_exponent_is_the_smallest_covering_power_of_two():
+    rng = np.random.default_rng(51)
+    amax = np.concatenate([
+        (rng.standard_normal(4000) * 10.0 ** rng.integers(-30, 30, 4000)).astype(np.float32),
+        np.float32([7.0, 3.5, 14.0, 1.0, 0.875, 7 * 2.0 ** -100, 3.4e38]),
+        np.nextafter(np.float32([7.0, 3.5, 14.0]), np.float32(np.inf)),
+        np.nextafter(np.float32([7.0, 3.5, 14.0]), np.float32(0)),
+    ])
+    amax = np.abs(amax)
+    amax = amax[amax > 0]
+    E = O.mx_scale_exponent(amax)
+    for a, e in zip(amax.tolist(), E.tolist()):
+        fa = Fraction(a)
+        two_e = Fraction(2) ** e
+        assert 7 * two_e >= fa, (a, e)
+        assert 7 * two_e / 2 < fa, (a, e)
+    assert O.mx_scale_exponent(np.float32([0.0]))[0] == -127
+
+
+def test_e2m3_format_against_the_ocp_definition():
+    # values fixed by the OCP Microscaling formats specification for FP6 E2M3
+    assert O.e2m3_value(0b011111) == 7.5  # largest normal
+    assert O.e2m3_value(0b001000) == 1.0
+    assert O.e2m3_value(0b000001) == 0.125  # smallest subnormal
+    assert O.e2m3_value(0b111111) == -7.5
+    assert O.e2m3_value(0b010000) == 2.0
+    k = np.arange(-7, 8)
+    assert np.array_equal(O.e2m3_value(O.e2m3_codes(k)), k)
+    assert O.e2m3_codes(np.array([0]))[0] == 0  # zero as +0
+
+
+def test_fp6_packing_bit_positions_and_roundtrip():
+    rng = np.random.default_rng(52)
+    idx = rng.integers(-7, 8, size=(5, 96))
+    p = O.pack_fp6(idx)
+    assert p.shape == (5, 72)
+    assert np.array_equal(O.unpack_fp6(p), idx)
+    one = np.zeros((1, 32), dtype=np.int64)
+    for j in (0, 1, 5, 21, 31):
+        one[:] = 0
+        one[0, j] = -1  # E2M3 -1 = 0b101000
+        bits = int.from_bytes(O.pack_fp6(one)[0].tobytes(), "little")
+        assert bits == 0b101000 << (6 * j)
+
+
+def _mx_reference_block(y, u=None):
+    """One 32-block by exact rationals: the smallest 2^E with 7 * 2^E >= amax, v = y / 2^E, then the
+    nearest integer (ties to even) or the SR rule with 16-bit draws."""
+    ys = [Fraction(float(t)) for t in y]
+    amax = max(abs(t) for t in ys)
+    if amax == 0:
+        return [0] * len(ys), 0
+    e = 0
+    while 7 * Fraction(2) ** e < amax:
+        e += 1
+    while 7 * Fraction(2) ** (e - 1) >= amax:
+        e -= 1
+    codes = []
+    for i, t in enumerate(ys):
+        v = t / Fraction(2) ** e
+        lo = floor(v)
+        if u is None:
+            frac = v - lo
+            k = lo + 1 if frac > Fraction(1, 2) or (frac == Fraction(1, 2) and lo % 2 == 1) else lo
+        else:
+            k = lo + 1 if Fraction(int(u[i]), 65536) < v - lo else lo
+        codes.append(max(-7, min(7, k)))
+    return codes, e + 127
+
+
+@pytest.mark.parametrize("rounding", [O.RTNE, O.SR])
+def test_mx_quantizer_against_exact_rationals(rounding):
+    rng = np.random.default_rng(53 + rounding)
+    rows = 6
+    a = (rng.standard_normal((rows, 64)) * np.exp(rng.standard_normal((rows, 1)) * 3)).astype(np.float32)
+    a[1, :32] = 0.0  # a zero block
+    a[2, 5] = 7.0 * 2.0 ** -3  # an exact top level
+    a = O.bf16_bits_to_f32(O.f32_to_bf16_bits(a))
+    idx, e8 = O.quantize_rows_mx(a, rounding, False, seed=7, stream=2)
+    u = O.sr_draws(np.arange(4)[None, :], np.arange(rows)[:, None], 7, 2).reshape(rows, 2, 32)
+    for r in range(rows):
+        for b in range(2):
+            codes, e = _mx_reference_block(a[r, 32 * b:32 * b + 32], None if rounding == O.RTNE else u[r, b])
+            assert list(idx[r, 32 * b:32 * b + 32]) == codes, (r, b)
+            if e:
+                assert e8[r, b] == e
+
+
+def test_mx_quantizer_invariants_with_rht():
+    rng = np.random.default_rng(54)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (16, 128), 3.0))
+    idx, e8 = O.quantize_rows_mx(a, O.RTNE, True, sign_mask=0x5A5A)
+    y = O.rht_blocks(a.reshape(16, 8, 16), 0x5A5A).reshape(16, 4, 32).astype(np.float64)
+    s = np.ldexp(1.0, e8.astype(np.int64) - 127)
+    top = np.abs(idx.reshape(16, 4, 32)).max(axis=-1)
+    assert np.all((top >= 4) & (top <= 7))  # amax / 2^E lies in (3.5, 7]: the top code is 4..7, no clipping
+    err = np.abs(idx.reshape(16, 4, 32) * s[..., None] - y)
+    assert np.all(err <= s[..., None] / 2)  # RTNE: within half a step
+
+
+def test_mx_gemm_special_cases():
+    rng = np.random.default_rng(55)
+    a = rng.integers(-7, 8, size=(5, 64))
+    b = rng.integers(-7, 8, size=(3, 64))
+    ones_a = np.full((5, 2), 127, np.uint8)
+    ones_b = np.full((3, 2), 127, np.uint8)
+    assert np.array_equal(O.gemm_nt_mx(a, ones_a, b, ones_b), (a @ b.T).astype(np.float64))
+    ea = rng.integers(120, 135, size=(5, 2)).astype(np.uint8)
+    eb = rng.integers(120, 135, size=(3, 2)).astype(np.uint8)
+    c = O.gemm_nt_mx(a, ea, b, eb)
+    for i in range(5):
+        for j in range(3):
+            want = sum(Fraction(int(a[i, k])) * Fraction(2) ** (int(ea[i, k // 32]) - 127) * int(b[j, k])
+                       * Fraction(2) ** (int(eb[j, k // 32]) - 127) for k in range(64))
+            assert c[i, j] == float(want)
