@@ -48,6 +48,7 @@ FP4_PEAK_TFLOPS = 10100.0  # dense fp4 MFMA (the E2M1 baseline's block products)
 # ops per FMA, at 256 CUs x 4 SIMDs x 16 fp32 FMA lanes per clock x 2.4 GHz = 39.3 T FMA/s (non-packed).
 ATTAINABLE_TOPS = 32 * 256 * 4 * 16 * 2.4e9 / 1e12
 GEMM_KERNEL = {
+    "mxufp4": "gemm_mx_kernel (scaled f8f6f4 MFMA 32x32x64, FP6 E2M3 operands, E8M0 scales applied in the matrix core)",
     "ufp4": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
     "e2m1": "gemm_f32_kernel (FP4 f8f6f4 MFMA per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
 }
@@ -55,7 +56,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 WARMUP_SECONDS = 0.5
 QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
 DUAL_BYTES_PER_ELEM = 3.5  # two-operand quantizer: 2 B in, 2 x 0.75 B out
-BYTES_PER_ELEM = {"quant": QUANT_BYTES_PER_ELEM, "quant2": DUAL_BYTES_PER_ELEM, "copy": 2.0}
+BYTES_PER_ELEM = {"quant": QUANT_BYTES_PER_ELEM, "quant2": DUAL_BYTES_PER_ELEM, "copy": 2.0,
+                  "quantmx": 2.0 + 0.75 + 1.0 / 32}
 METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
 
 
@@ -90,6 +92,9 @@ class Timeline:
 RECIPES = {
     "ufp4": (U.UNIFORM, (True, True, True), "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY"),
     "e2m1": (U.E2M1, (False, False, True), "e2m1 baseline: E2M1 grid, RHT16 on bwd_dw only, SR on dY"),
+    "mxufp4": (U.UNIFORM, (True, True, True),
+               "mxufp4: uniform -7..7 with power-of-two 1x32 (E8M0) scales, FP6 E2M3 codes, RHT16 on all GEMMs, "
+               "SR on dY"),
 }
 
 
@@ -99,7 +104,44 @@ def _quantizers(recipe: str):
     return fmt, fn, r_y, r_dx, r_dw
 
 
+def dense_step_mx(wl, tl: Timeline):
+    """The layer step with power-of-two 1x32 scales: six quantizations (RHT16 everywhere, SR on dY) and the
+    three passes on the scaled FP6 matrix-core instruction."""
+    m, s = wl.sign_mask, wl.seed
+    x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
+    M, K = x.shape
+    N = w.shape[0]
+    E = U.empty_qtensor_mx
+    q = {"x": E(M, K), "w": E(N, K), "dy": E(M, N), "wt": E(K, N), "dyt": E(N, M), "xt": E(K, M)}
+    y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
+    dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
+    Q = U.mx_quantize
+
+    def step(rec):
+        tl.run("quant_x", lambda: Q(x, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: Q(w, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: Q(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0, out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: Q(w, transpose=True, sign_mask=m, out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: Q(dy, transpose=True, sign_mask=m, rounding=U.SR, seed=s, stream_id=1,
+                                         out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: Q(x, transpose=True, sign_mask=m, out=q["xt"]), rec)
+        tl.run("gemm_fwd_y", lambda: U.mx_gemm_fwd_y(q["x"], q["w"], out=y), rec)
+        tl.run("gemm_bwd_dx", lambda: U.mx_gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
+        tl.run("gemm_bwd_dw", lambda: U.mx_gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
+
+    kern = {
+        "quant_x": ("quantmx", M * K), "quant_w": ("quantmx", N * K), "quant_dy_sr": ("quantmx", M * N),
+        "quant_wt": ("quantmx", N * K), "quant_dyt_sr": ("quantmx", M * N), "quant_xt": ("quantmx", M * K),
+        "gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
+        "gemm_bwd_dw": ("gemm", 2 * M * N * K),
+    }
+    return step, kern
+
+
 def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
+    if recipe == "mxufp4":
+        return dense_step_mx(wl, tl)
     m, s = wl.sign_mask, wl.seed
     fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
@@ -341,6 +383,9 @@ def main():
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
+        if wl.grouped and args.recipe == "mxufp4":
+            print("bench.py: the power-of-two-scale recipe has no grouped (MoE) kernels in this build", file=sys.stderr)
+            sys.exit(2)
         step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe, args.quant == "dual")
         wname = wl.name
     torch.cuda.synchronize()
@@ -389,29 +434,31 @@ def main():
             gbps = 2 * work / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += 2 * work
-        elif kind in ("quant", "quant2"):
+        elif kind in ("quant", "quant2", "quantmx"):
             gbps = work * BYTES_PER_ELEM[kind] / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += work * BYTES_PER_ELEM[kind]
         else:
             tf = work / (us * 1e-6) / 1e12
-            breakdown[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_int8": round(tf / INT8_PEAK_TOPS, 4)}
+            breakdown[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1),
+                                "frac_peak": round(tf / (INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS), 4)}
             gemm_flops += work
 
     gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
-    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "quant2", "copy")]
+    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "quant2", "quantmx", "copy")]
     if gemm_labels:
         value = gemm_flops / (ms_per_step * 1e-3) / 1e12
         unit = "TFLOP/s"
         per_launch = np.mean([kern[k][1] for k in gemm_labels])
         avg_us = np.mean([tl.mean_us(k) for k in gemm_labels])
         ach = per_launch / (avg_us * 1e-6) / 1e12
-        peak = INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS
+        peak = INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS  # fp6 and fp4 share the peak
         roof = {"bound": "mfma", "kernel": GEMM_KERNEL[args.recipe],
                 "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": measured_traffic("gemm", wname + "/" + args.recipe),
-                "attainable": {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
-                               "why": "one fp32 VALU FMA per output and 16-block"}}
+                "frac": round(ach / peak, 4), "traffic": measured_traffic("gemm", wname + "/" + args.recipe)}
+        if args.recipe != "mxufp4":  # the per-16 fp32 scales need one VALU FMA per output and block
+            roof["attainable"] = {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
+                                  "why": "one fp32 VALU FMA per output and 16-block"}
     else:
         value = quant_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"
@@ -439,7 +486,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if gemm_labels else "f64+f32",
+        "dtype": ("fp6+f32" if args.recipe == "mxufp4" else "f32") if gemm_labels else "f64+f32",
         "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
         "config": {"workload": wname, "recipe": RECIPES[args.recipe][2],
                    "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",

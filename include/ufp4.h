@@ -145,6 +145,49 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
                        float *scales_c_dev, int64_t scale_panel_ld_c, void *stream);
 
 /*
+ * Power-of-two block scales. The paper leaves the scale hierarchy open (Sec. 4: single-level, two-level or
+ * block scales, chosen for the hardware); these calls pair the same uniform grid and RHT with one scale per
+ * 1x32 block that gfx950's scaled matrix-core instruction applies itself.
+ *
+ * ufp4_mx_quantize -- fused RHT + quantization with power-of-two scales. Per 1x32 block along the reduction
+ *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = the smallest integer with
+ *   amax |y| <= 7 * 2^E; v = y * 2^-E (exact); codes -7..7 by RTNE or SR (same rules and Philox draws, the
+ *   counters numbering 16-blocks). Arguments as ufp4_rht_quantize, except:
+ *     red % 32 == 0 (cols when transpose = 0, rows when transpose = 1);
+ *     codes: FP6 E2M3 numbers (the integers -7..7 are exact), 32 per block in 24 bytes, element j in bits
+ *            6j .. 6j + 5 of the block's little-endian 192-bit string;
+ *     scales_dev: uint8 E8M0 bytes E + 127 (0 for an all-zero block).
+ *   Layout (panels of 128 rows, 32-blocks): codes of block b of row 128p + i at codes_dev + p * code_panel_ld
+ *   + b * 3072 + i * 24; its scale at scales_dev + p * scale_panel_ld + b * 128 + i. code_panel_ld >=
+ *   3072 * red/32 and scale_panel_ld >= 128 * red/32, both multiples of 16; both pointers 16-byte aligned.
+ *   Padding rows of the last panel are written as zero codes and scale byte 0. Rowwise operands of more than
+ *   4194240 rows return UFP4_ERR_UNSUPPORTED.
+ */
+int ufp4_mx_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                     uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
+                     int64_t code_panel_ld, void *scales_dev, int64_t scale_panel_ld, void *stream);
+
+/*
+ * ufp4_mx_gemm_fwd_y / _bwd_dx / _bwd_dw -- the three passes (shapes and operand roles as the ufp4_gemm_*
+ *   calls below) on operands from ufp4_mx_quantize: C[i, j] = sum_k A[i,k] 2^(eA - 127) B[j,k] 2^(eB - 127)
+ *   with the scales of each element's 32-block, accumulated in fp32 by the matrix core; output fp32 or bf16
+ *   (RNE) with leading dimension ldc. K % 32 == 0. A left operand of more than 8388480 rows returns
+ *   UFP4_ERR_UNSUPPORTED.
+ */
+int ufp4_mx_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_panel_ld, const void *x_scales_dev,
+                       int64_t x_scale_panel_ld, const void *w_codes_dev, int64_t w_code_panel_ld,
+                       const void *w_scales_dev, int64_t w_scale_panel_ld, int64_t M, int64_t N, int64_t K, void *y_dev,
+                       int64_t ldc, int out_dtype, void *stream);
+int ufp4_mx_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_panel_ld, const void *dy_scales_dev,
+                        int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
+                        const void *wt_scales_dev, int64_t wt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
+                        void *dx_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_mx_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const void *dyt_scales_dev,
+                        int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
+                        const void *xt_scales_dev, int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
+                        void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+
+/*
  * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that
  * share their reduction axis (the axis the RHT was applied along):
  *

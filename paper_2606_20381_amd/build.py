@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libufp4.so")
 INCLUDE = os.path.join(os.path.dirname(PKG), "include")
 
-SOURCES = ["ufp4_quant.hip", "ufp4_gemm.hip", "ufp4_api.cpp"]
+SOURCES = ["ufp4_quant.hip", "ufp4_gemm.hip", "ufp4_gemm_mx.hip", "ufp4_api.cpp"]
 
 ARCH = "gfx950"
 FLAGS = [

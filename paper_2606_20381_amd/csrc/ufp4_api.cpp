@@ -90,6 +90,88 @@ int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t
     return status_of(launch_quantize(j, static_cast<hipStream_t>(stream)));
 }
 
+// Panel layout of an operand with power-of-two 1x32 scales (reduction length `red`, a multiple of 32).
+int check_panels_mx(const void* codes, int64_t code_pld, const void* scales, int64_t scale_pld, int64_t red) {
+    const int64_t nkb = red / 32;
+    if (code_pld < nkb * kMxPanelBlockBytes || scale_pld < nkb * kMxPanelBlockScales) return UFP4_ERR_SHAPE;
+    if (code_pld % 16 != 0 || scale_pld % 16 != 0) return UFP4_ERR_ALIGN;
+    if (!aligned(codes, 16) || !aligned(scales, 16)) return UFP4_ERR_ALIGN;
+    if (code_pld > kMaxCodePanelLd || scale_pld > kMaxCodePanelLd) return UFP4_ERR_UNSUPPORTED;
+    return UFP4_OK;
+}
+
+int mx_quantize_impl(const void* x, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht, uint32_t sign_mask,
+                     int rounding, uint64_t seed, uint32_t stream_id, void* codes, int64_t code_pld, void* scales,
+                     int64_t scale_pld, void* stream) {
+    if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
+    if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
+    if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
+    if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    if (!x || !codes || !scales) return UFP4_ERR_INVALID_ARG;
+    const int64_t red = transpose ? rows : cols;
+    const int64_t qrows = transpose ? cols : rows;
+    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
+    if (red % 32 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x, 16)) return UFP4_ERR_ALIGN;
+    const int st = check_panels_mx(codes, code_pld, scales, scale_pld, red);
+    if (st != UFP4_OK) return st;
+    if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    if (!transpose && padded_rows(qrows) / 64 > 65535) return UFP4_ERR_UNSUPPORTED;  // one workgroup row per 64
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    MxQuantJob j{};
+    j.rounding = rounding;
+    j.rht = rht;
+    j.transpose = transpose;
+    j.x = x;
+    j.xrows = rows;
+    j.ld = ld;
+    j.qrows = qrows;
+    j.red = red;
+    fill_sign_xor(sign_mask, j.qa.sign_xor);
+    j.qa.key0 = (uint32_t)seed;
+    j.qa.key1 = (uint32_t)(seed >> 32);
+    j.qa.stream = stream_id;
+    j.codes = codes;
+    j.code_pld = code_pld;
+    j.scales = scales;
+    j.scale_pld = scale_pld;
+    return status_of(launch_quantize_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+// NT product of two operands with power-of-two scales: A [rows_a, red], B [rows_b, red].
+int mx_gemm_impl(const void* a, int64_t a_pld, const void* as, int64_t as_pld, const void* b, int64_t b_pld,
+                 const void* bs, int64_t bs_pld, int64_t rows_a, int64_t rows_b, int64_t red, void* c, int64_t ldc,
+                 int out_dtype, void* stream) {
+    if (out_dtype != UFP4_OUT_F32 && out_dtype != UFP4_OUT_BF16) return UFP4_ERR_INVALID_ARG;
+    if (rows_a < 0 || rows_b < 0 || red < 0) return UFP4_ERR_INVALID_ARG;
+    if (!a || !as || !b || !bs || !c) return UFP4_ERR_INVALID_ARG;
+    if (red % 32 != 0) return UFP4_ERR_SHAPE;
+    int st = check_panels_mx(a, a_pld, as, as_pld, red);
+    if (st == UFP4_OK) st = check_panels_mx(b, b_pld, bs, bs_pld, red);
+    if (st != UFP4_OK) return st;
+    if (ldc < rows_b) return UFP4_ERR_SHAPE;
+    if (!aligned(c, out_dtype == UFP4_OUT_F32 ? 4 : 2)) return UFP4_ERR_ALIGN;
+    if ((rows_a + 127) / 128 > 65535 || red / 32 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    if (rows_a == 0 || rows_b == 0) return UFP4_OK;
+    MxGemmJob j{};
+    j.out_dtype = out_dtype;
+    j.a = static_cast<const uint8_t*>(a);
+    j.a_pld = a_pld;
+    j.as = static_cast<const uint8_t*>(as);
+    j.as_pld = as_pld;
+    j.b = static_cast<const uint8_t*>(b);
+    j.b_pld = b_pld;
+    j.bs = static_cast<const uint8_t*>(bs);
+    j.bs_pld = bs_pld;
+    j.M = rows_a;
+    j.N = rows_b;
+    j.nkb = red / 32;
+    j.c = c;
+    j.ldc = ldc;
+    return status_of(launch_gemm_mx(j, static_cast<hipStream_t>(stream)));
+}
+
 // Shared checks of the GEMM entry points. A is [rows_a, red], B is [rows_b, red] (reduction contiguous).
 int check_gemm(const void* a, int64_t a_pld, const float* as, int64_t as_pld, const void* b, int64_t b_pld,
                const float* bs, int64_t bs_pld, int64_t rows_a, int64_t rows_b, int64_t red_a, int64_t red_b, int format,
@@ -253,6 +335,39 @@ int ufp4_quantize_dual(int format, const void* x_dev, int64_t rows, int64_t cols
     j.scales_c = scales_c_dev;
     j.scale_pld_c = scale_panel_ld_c;
     return status_of(launch_quantize_dual(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                     uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes_dev,
+                     int64_t code_panel_ld, void* scales_dev, int64_t scale_panel_ld, void* stream) {
+    return mx_quantize_impl(x_dev, rows, cols, ld, transpose, rht, sign_mask, rounding, seed, stream_id, codes_dev,
+                            code_panel_ld, scales_dev, scale_panel_ld, stream);
+}
+
+int ufp4_mx_gemm_fwd_y(const void* x_codes_dev, int64_t x_code_panel_ld, const void* x_scales_dev,
+                       int64_t x_scale_panel_ld, const void* w_codes_dev, int64_t w_code_panel_ld,
+                       const void* w_scales_dev, int64_t w_scale_panel_ld, int64_t M, int64_t N, int64_t K, void* y_dev,
+                       int64_t ldc, int out_dtype, void* stream) {
+    return mx_gemm_impl(x_codes_dev, x_code_panel_ld, x_scales_dev, x_scale_panel_ld, w_codes_dev, w_code_panel_ld,
+                        w_scales_dev, w_scale_panel_ld, M, N, K, y_dev, ldc, out_dtype, stream);
+}
+
+int ufp4_mx_gemm_bwd_dx(const void* dy_codes_dev, int64_t dy_code_panel_ld, const void* dy_scales_dev,
+                        int64_t dy_scale_panel_ld, const void* wt_codes_dev, int64_t wt_code_panel_ld,
+                        const void* wt_scales_dev, int64_t wt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
+                        void* dx_dev, int64_t ldc, int out_dtype, void* stream) {
+    // dX [M, K] = dY [M, N] . (W^T [K, N])^T
+    return mx_gemm_impl(dy_codes_dev, dy_code_panel_ld, dy_scales_dev, dy_scale_panel_ld, wt_codes_dev, wt_code_panel_ld,
+                        wt_scales_dev, wt_scale_panel_ld, M, K, N, dx_dev, ldc, out_dtype, stream);
+}
+
+int ufp4_mx_gemm_bwd_dw(const void* dyt_codes_dev, int64_t dyt_code_panel_ld, const void* dyt_scales_dev,
+                        int64_t dyt_scale_panel_ld, const void* xt_codes_dev, int64_t xt_code_panel_ld,
+                        const void* xt_scales_dev, int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
+                        void* dw_dev, int64_t ldc, int out_dtype, void* stream) {
+    // dW [N, K] = dY^T [N, M] . (X^T [K, M])^T
+    return mx_gemm_impl(dyt_codes_dev, dyt_code_panel_ld, dyt_scales_dev, dyt_scale_panel_ld, xt_codes_dev,
+                        xt_code_panel_ld, xt_scales_dev, xt_scale_panel_ld, N, K, M, dw_dev, ldc, out_dtype, stream);
 }
 
 int ufp4_gemm_fwd_y(const void* x_codes_dev, int64_t x_code_panel_ld, const float* x_scales_dev, int64_t x_scale_panel_ld,

@@ -63,6 +63,45 @@ struct DualJob {
 
 hipError_t launch_quantize_dual(const DualJob& job, hipStream_t stream);
 
+// Power-of-two block scales: the uniform grid with one E8M0 scale per 1x32 block and FP6 E2M3 codes.
+// Operand [rows, red] (red % 32 == 0) in panels of 128 rows; within a panel, 32-block b of all 128 rows is
+// contiguous: codes 128 x 24 bytes at b * 3072, scales 128 bytes at b * 128.
+constexpr int64_t kMxPanelBlockBytes = kPanelRows * 24;
+constexpr int64_t kMxPanelBlockScales = kPanelRows;
+
+struct MxQuantJob {
+    int rounding, rht, transpose;
+    const void* x;
+    int64_t xrows, ld;  // X rows and leading dimension (elements)
+    int64_t qrows;      // rows of the quantized operand
+    int64_t red;        // its reduction length (multiple of 32)
+    QuantArgs qa;
+    void* codes;
+    int64_t code_pld;  // bytes between panels
+    void* scales;
+    int64_t scale_pld;  // bytes between panels
+};
+
+hipError_t launch_quantize_mx(const MxQuantJob& job, hipStream_t stream);
+
+// NT GEMM on two such operands: C[i, j] = sum_k A[i,k] 2^(eA[i,k/32]-127) B[j,k] 2^(eB[j,k/32]-127).
+struct MxGemmJob {
+    int out_dtype;
+    const uint8_t* a;
+    int64_t a_pld;
+    const uint8_t* as;
+    int64_t as_pld;
+    const uint8_t* b;
+    int64_t b_pld;
+    const uint8_t* bs;
+    int64_t bs_pld;
+    int64_t M, N, nkb;  // rows of A, rows of B, 32-blocks of the reduction
+    void* c;
+    int64_t ldc;
+};
+
+hipError_t launch_gemm_mx(const MxGemmJob& job, hipStream_t stream);
+
 // Block-scaled NT GEMM: C[i, j] = sum_b sA[i,b] sB[j,b] sum_{k in b} A[i,k] B[j,k] over `nkb` 16-blocks.
 enum GemmMode { kGemmDense = 0, kGemmRaggedM = 1, kGemmRaggedK = 2 };
 

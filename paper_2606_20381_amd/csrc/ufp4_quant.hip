@@ -112,10 +112,9 @@ __device__ __forceinline__ uint32_t e2m1_code(float v, uint32_t u16) {
 // ------------------------------------------------------------------------------------------------
 // One 16-block: eight bf16 pairs in (element 2j in the low half of w[j]), packed codes + scale out.
 // ------------------------------------------------------------------------------------------------
-template <int FMT, int ROUND, bool RHT>
-__device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
-                                              uint32_t& code_lo, uint32_t& code_hi, float& scale) {
-    float y[16];
+// The RHT of one 16-block: y' = 4y = RN32( sum_j H16[i,j] eps_j x_j ) (see the file header), or y = x.
+template <bool RHT>
+__device__ __forceinline__ void rht16_unscaled(const uint32_t* w, const QuantArgs& qa, float* y) {
     if constexpr (RHT) {
         double d[16];
 #pragma unroll
@@ -136,7 +135,6 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
                 }
             }
         }
-        // y' = 4 y (see the file header)
 #pragma unroll
         for (int i = 0; i < 16; ++i) y[i] = (float)d[i];
     } else {
@@ -146,6 +144,13 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
             y[2 * j + 1] = bf16_hi(w[j]);
         }
     }
+}
+
+template <int FMT, int ROUND, bool RHT>
+__device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
+                                              uint32_t& code_lo, uint32_t& code_hi, float& scale) {
+    float y[16];
+    rht16_unscaled<RHT>(w, qa, y);
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
@@ -482,6 +487,175 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
 }
 
 // ------------------------------------------------------------------------------------------------
+// Power-of-two block scales (the scale hierarchy is free, Sec. 4): blocks of 32 along the reduction axis
+// share one scale 2^E, E the smallest integer with amax <= 7 * 2^E, stored as the E8M0 byte E + 127; the
+// RHT stays block-16; codes are the uniform levels -7..7 stored as FP6 E2M3 numbers, 32 of them in 24 bytes
+// (element j in bits 6j .. 6j + 5): the A/B operand format of v_mfma_scale_f32_32x32x64_f8f6f4.
+// ------------------------------------------------------------------------------------------------
+constexpr int kMxBlock = 32;
+
+// Sign-magnitude nibbles of 8 consecutive codes (nibble i = code i) -> E2M3 bytes: b0 = codes 0-3, b1 = 4-7.
+// E2M3 magnitudes of 0..7 are 0, 8, 16, 20, 24, 26, 28, 30 (a byte-permute lookup); the sign goes to bit 5.
+__device__ __forceinline__ void sm_nibbles_to_e2m3(uint32_t p, uint32_t& b0, uint32_t& b1) {
+    const uint32_t ev = p & 0x0F0F0F0Fu;         // nibbles 0, 2, 4, 6
+    const uint32_t od = (p >> 4) & 0x0F0F0F0Fu;  // nibbles 1, 3, 5, 7
+    const uint32_t n0 = __builtin_amdgcn_perm(od, ev, 0x05010400u);  // nibbles 0 1 2 3, one per byte
+    const uint32_t n1 = __builtin_amdgcn_perm(od, ev, 0x07030602u);  // nibbles 4 5 6 7
+    b0 = __builtin_amdgcn_perm(0x1E1C1A18u, 0x14100800u, n0 & 0x07070707u) | ((n0 & 0x08080808u) << 2);
+    b1 = __builtin_amdgcn_perm(0x1E1C1A18u, 0x14100800u, n1 & 0x07070707u) | ((n1 & 0x08080808u) << 2);
+}
+
+// Four 6-bit values, one per byte -> 24 bits c0 | c1 << 6 | c2 << 12 | c3 << 18.
+__device__ __forceinline__ uint32_t pack6x4(uint32_t b) {
+    const uint32_t p = (b & 0x003F003Fu) | ((b >> 2) & 0x0FC00FC0u);
+    return (p & 0xFFFu) | ((p >> 4) & 0xFFF000u);
+}
+
+// One 32-block: sixteen bf16 pairs in (element 2j in the low half of w[j]); 24 bytes of E2M3 codes and the
+// E8M0 scale byte out. `blk16` numbers the block's first 16-block along the reduction axis (the SR counters
+// count 16-blocks).
+template <int ROUND, bool RHT>
+__device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const QuantArgs& qa, uint32_t blk16,
+                                                 uint32_t row, uint32_t (&out)[6], uint32_t& e8m0) {
+    float y[32];
+    rht16_unscaled<RHT>(w, qa, y);
+    rht16_unscaled<RHT>(w + 8, qa, y + 16);
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
+    // amax = 1.f * 2^(eb - 127): the smallest E with amax <= 7 * 2^E is eb - 129, plus one when 1.f > 1.75
+    const uint32_t ab = __float_as_uint(amax);
+    const int e8 = (int)(ab >> 23) - 2 + ((ab & 0x7FFFFFu) > 0x600000u ? 1 : 0);  // E + 127 for this amax
+    // y' = 4y with the RHT: the scale of y is 2^(E - 2); v = y' * 2^-E either way (exact, a power of two)
+    e8m0 = amax > 0.0f ? (uint32_t)(RHT ? e8 - 2 : e8) : 0u;
+    const float mult = amax > 0.0f ? __uint_as_float((uint32_t)(254 - e8) << 23) : 0.0f;
+    uint32_t p[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        uint32_t u[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if constexpr (ROUND == kRoundSR) {
+            const Philox4 p0 = philox4x32_10(blk16 + h, row, 0u, qa.stream, qa.key0, qa.key1);
+            const Philox4 p1 = philox4x32_10(blk16 + h, row, 1u, qa.stream, qa.key0, qa.key1);
+            u[0] = p0.x; u[1] = p0.y; u[2] = p0.z; u[3] = p0.w;
+            u[4] = p1.x; u[5] = p1.y; u[6] = p1.z; u[7] = p1.w;
+        }
+        uint32_t t[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float v = y[16 * h + i] * mult;  // |v| <= 7
+            if constexpr (ROUND == kRoundSR) {
+                const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
+                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);
+            } else {
+                t[i] = __float_as_uint(v + kMagic8);
+            }
+        }
+        p[2 * h] = offset_to_sign_magnitude(pack_nibbles(t));
+        p[2 * h + 1] = offset_to_sign_magnitude(pack_nibbles(t + 8));
+    }
+    uint32_t g[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        uint32_t b0, b1;
+        sm_nibbles_to_e2m3(p[k], b0, b1);
+        g[2 * k] = pack6x4(b0);
+        g[2 * k + 1] = pack6x4(b1);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {  // four 24-bit groups -> three words
+        out[3 * k] = g[4 * k] | (g[4 * k + 1] << 24);
+        out[3 * k + 1] = (g[4 * k + 1] >> 8) | (g[4 * k + 2] << 16);
+        out[3 * k + 2] = (g[4 * k + 2] >> 16) | (g[4 * k + 3] << 8);
+    }
+}
+
+// Rowwise: wave w of a workgroup takes 32-block blockIdx.x * 4 + w of 64 consecutive operand rows (lane =
+// row), so the four waves read 256 contiguous bytes of each row and every wave writes 64 x 24 contiguous
+// bytes of codes and 64 scale bytes. Rows past the operand's last one (panel padding) get zeros.
+template <int ROUND, bool RHT>
+__global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, int64_t qrows,
+                                                      int64_t nb32, QuantArgs qa, uint8_t* __restrict__ codes,
+                                                      int64_t code_pld, uint8_t* __restrict__ scales,
+                                                      int64_t scale_pld) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t b = (int64_t)blockIdx.x * 4 + wave;
+    if (b >= nb32) return;
+    const int64_t r = (int64_t)blockIdx.y * 64 + lane;
+    uint32_t out[6] = {0, 0, 0, 0, 0, 0};
+    uint32_t e8 = 0;
+    if (r < qrows) {
+        const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kMxBlock);
+        uint32_t w[16];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint4 l = src[q];
+            w[4 * q] = l.x; w[4 * q + 1] = l.y; w[4 * q + 2] = l.z; w[4 * q + 3] = l.w;
+        }
+        quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * b), (uint32_t)r, out, e8);
+    }
+    const int64_t P = r >> 7, ri = r & 127;
+    uint2* dc = reinterpret_cast<uint2*>(codes + P * code_pld + b * 3072 + ri * 24);
+    dc[0] = make_uint2(out[0], out[1]);
+    dc[1] = make_uint2(out[2], out[3]);
+    dc[2] = make_uint2(out[4], out[5]);
+    scales[P * scale_pld + b * 128 + ri] = (uint8_t)e8;
+}
+
+// Transposed: a thread loads 32 rows x 4 columns of X (one 8-byte load per row) and quantizes the four
+// column blocks from registers; sixteen threads cover 64 columns, a workgroup 16 row blocks. The four
+// operand rows of a block leave as 96 contiguous bytes of codes and one word of scales. Columns past `cols`
+// (panel padding) hold zeros and quantize to zero codes and scale byte 0.
+template <int ROUND, bool RHT>
+__global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                      int64_t ld, QuantArgs qa, uint8_t* __restrict__ codes,
+                                                      int64_t code_pld, uint8_t* __restrict__ scales,
+                                                      int64_t scale_pld) {
+    const int t = threadIdx.x, cg = t & 15, rb = t >> 4;
+    const int64_t cbase = (int64_t)blockIdx.x * 64 + cg * 4;
+    const int ncol = cols - cbase < 4 ? (int)(cols - cbase) : 4;
+    const int64_t nblk = rows / kMxBlock;
+    for (int64_t gb = (int64_t)blockIdx.y * 16 + rb; gb < nblk; gb += (int64_t)gridDim.y * 16) {
+        uint32_t v[kMxBlock][2];
+        if (ncol == 4) {
+#pragma unroll
+            for (int j = 0; j < kMxBlock; ++j) {
+                const uint2 l = *reinterpret_cast<const uint2*>(x + (gb * kMxBlock + j) * ld + cbase);
+                v[j][0] = l.x;
+                v[j][1] = l.y;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kMxBlock; ++j) {
+                v[j][0] = v[j][1] = 0;
+                const uint16_t* src = x + (gb * kMxBlock + j) * ld + cbase;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
+            }
+        }
+        uint32_t out[4][6], e8[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+            uint32_t w[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
+            quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * gb), (uint32_t)(cbase + q), out[q], e8[q]);
+        }
+        const int64_t P = cbase >> 7, ri = cbase & 127;
+        uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 3072 + ri * 24);  // 96 bytes
+        dc[0] = make_uint4(out[0][0], out[0][1], out[0][2], out[0][3]);
+        dc[1] = make_uint4(out[0][4], out[0][5], out[1][0], out[1][1]);
+        dc[2] = make_uint4(out[1][2], out[1][3], out[1][4], out[1][5]);
+        dc[3] = make_uint4(out[2][0], out[2][1], out[2][2], out[2][3]);
+        dc[4] = make_uint4(out[2][4], out[2][5], out[3][0], out[3][1]);
+        dc[5] = make_uint4(out[3][2], out[3][3], out[3][4], out[3][5]);
+        *reinterpret_cast<uint32_t*>(scales + P * scale_pld + gb * 128 + ri) =
+            e8[0] | (e8[1] << 8) | (e8[2] << 16) | (e8[3] << 24);
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
 // Host-side launchers
 // ------------------------------------------------------------------------------------------------
 template <int FMT, int ROUND, bool RHT>
@@ -551,6 +725,32 @@ static hipError_t dispatch_dual_rht(const DualJob& j, hipStream_t s) {
 template <int FMT>
 static hipError_t dispatch_dual_fmt(const DualJob& j, hipStream_t s) {
     return j.rounding == kRoundSR ? dispatch_dual_rht<FMT, kRoundSR>(j, s) : dispatch_dual_rht<FMT, kRoundRTNE>(j, s);
+}
+
+template <int ROUND, bool RHT>
+static hipError_t launch_mx_t(const MxQuantJob& j, hipStream_t s) {
+    const int64_t prows = padded_rows(j.qrows);
+    if (!j.transpose) {
+        const int64_t nb32 = j.red / kMxBlock;
+        const dim3 grid((unsigned)((nb32 + 3) / 4), (unsigned)(prows / 64));
+        if (grid.x == 0 || grid.y == 0) return hipSuccess;
+        mx_rows_kernel<ROUND, RHT><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, j.qrows, nb32, j.qa,
+                                                        static_cast<uint8_t*>(j.codes), j.code_pld,
+                                                        static_cast<uint8_t*>(j.scales), j.scale_pld);
+    } else {
+        const int64_t gy = (j.red / kMxBlock + 15) / 16;
+        const dim3 grid((unsigned)(prows / 64), (unsigned)(gy < 65535 ? gy : 65535));
+        if (grid.x == 0 || grid.y == 0) return hipSuccess;
+        mx_cols_kernel<ROUND, RHT><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, j.ld,
+                                                        j.qa, static_cast<uint8_t*>(j.codes), j.code_pld,
+                                                        static_cast<uint8_t*>(j.scales), j.scale_pld);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_mx(const MxQuantJob& j, hipStream_t s) {
+    if (j.rounding == kRoundSR) return j.rht ? launch_mx_t<kRoundSR, true>(j, s) : launch_mx_t<kRoundSR, false>(j, s);
+    return j.rht ? launch_mx_t<kRoundRTNE, true>(j, s) : launch_mx_t<kRoundRTNE, false>(j, s);
 }
 
 hipError_t launch_quantize_dual(const DualJob& j, hipStream_t s) {

@@ -31,6 +31,7 @@ _U64 = ctypes.c_uint64
 
 _QUANT_ARGS = [_P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, _P, _I64, _P, _I64, _P]
 _GEMM_ARGS = [_P, _I64, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I64, _INT, _P, _I64, _INT, _P]
+_GEMM_MX_ARGS = [_P, _I64, _P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I64, _P, _I64, _INT, _P]
 SIGNATURES = {
     "ufp4_status_string": ([_INT], ctypes.c_char_p),
     "ufp4_version": ([], ctypes.c_char_p),
@@ -40,6 +41,10 @@ SIGNATURES = {
                                  _I64, _P, _I64, _P], _INT),
     "ufp4_quantize_dual": ([_INT, _P, _I64, _I64, _I64, _INT, _U32, _U32, _INT, _U32, _U32, _INT, _U64, _P, _I64, _P,
                             _I64, _P, _I64, _P, _I64, _P], _INT),
+    "ufp4_mx_quantize": (_QUANT_ARGS, _INT),
+    "ufp4_mx_gemm_fwd_y": (_GEMM_MX_ARGS, _INT),
+    "ufp4_mx_gemm_bwd_dx": (_GEMM_MX_ARGS, _INT),
+    "ufp4_mx_gemm_bwd_dw": (_GEMM_MX_ARGS, _INT),
     "ufp4_gemm_fwd_y": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dx": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dw": (_GEMM_ARGS, _INT),
@@ -185,6 +190,92 @@ def quantize_dual(x: torch.Tensor, *, fmt: int = UNIFORM, rht_rows: bool = True,
                                   qc.scales.data_ptr(), qc.scale_panel_ld, _stream())
     _check(st, "ufp4_quantize_dual")
     return qr, qc
+
+
+@dataclass
+class QTensorMX:
+    """An operand quantized with power-of-two 1x32 scales, [rows, red] in panels of 128 rows: 32-block b of the
+    panel's rows is contiguous, 128 x 24 bytes of FP6 E2M3 codes at b * 3072 and 128 E8M0 bytes at b * 128."""
+
+    codes: torch.Tensor  # uint8 [panels, >= 3072 * red/32]
+    scales: torch.Tensor  # uint8 [panels, >= 128 * red/32]
+    rows: int
+    red: int
+
+    @property
+    def code_panel_ld(self) -> int:
+        return self.codes.stride(0)
+
+    @property
+    def scale_panel_ld(self) -> int:
+        return self.scales.stride(0)
+
+    @property
+    def panels(self) -> int:
+        return self.codes.shape[0]
+
+    def codes_rows(self) -> torch.Tensor:
+        """Codes as uint8 [rows, red * 3/4] (24 bytes per 32-block), row-major (a copy)."""
+        nkb = self.red // 32
+        v = self.codes[:, : nkb * 3072].reshape(self.panels, nkb, PANEL_ROWS, 24).permute(0, 2, 1, 3)
+        return v.reshape(self.panels * PANEL_ROWS, nkb * 24)[: self.rows]
+
+    def scales_rows(self) -> torch.Tensor:
+        """E8M0 scale bytes as uint8 [rows, red/32], row-major (a copy)."""
+        nkb = self.red // 32
+        v = self.scales[:, : nkb * PANEL_ROWS].reshape(self.panels, nkb, PANEL_ROWS).permute(0, 2, 1)
+        return v.reshape(self.panels * PANEL_ROWS, nkb)[: self.rows]
+
+
+def empty_qtensor_mx(rows: int, red: int, device="cuda") -> QTensorMX:
+    panels = max(1, -(-rows // PANEL_ROWS))
+    nkb = red // 32
+    codes = torch.empty((panels, max(16, nkb * 3072)), dtype=torch.uint8, device=device)
+    scales = torch.empty((panels, max(16, nkb * PANEL_ROWS)), dtype=torch.uint8, device=device)
+    return QTensorMX(codes, scales, rows, red)
+
+
+def mx_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = True, sign_mask: int = 0,
+                rounding: int = RTNE, seed: int = 0, stream_id: int = 0, out: QTensorMX | None = None) -> QTensorMX:
+    """Fused RHT + uniform-grid quantization with power-of-two 1x32 scales (ufp4_mx_quantize)."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    qrows, red = (cols, rows) if transpose else (rows, cols)
+    q = out if out is not None else empty_qtensor_mx(qrows, red, x.device)
+    st = lib().ufp4_mx_quantize(x.data_ptr(), rows, cols, x.stride(0), int(transpose), int(rht), sign_mask, rounding,
+                                seed & 0xFFFFFFFFFFFFFFFF, stream_id, q.codes.data_ptr(), q.code_panel_ld,
+                                q.scales.data_ptr(), q.scale_panel_ld, _stream())
+    _check(st, "ufp4_mx_quantize")
+    return q
+
+
+def _gemm_mx_call(name, a: QTensorMX, b: QTensorMX, M, N, K, c: torch.Tensor):
+    if c.dim() != 2 or c.stride(1) != 1:
+        raise ValueError("output must be a 2-D row-major tensor")
+    st = getattr(lib(), name)(a.codes.data_ptr(), a.code_panel_ld, a.scales.data_ptr(), a.scale_panel_ld,
+                              b.codes.data_ptr(), b.code_panel_ld, b.scales.data_ptr(), b.scale_panel_ld, M, N, K,
+                              c.data_ptr(), c.stride(0), _odt(c), _stream())
+    _check(st, name)
+    return c
+
+
+def mx_gemm_fwd_y(xq: QTensorMX, wq: QTensorMX, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """Y [M, N] = Q(X H') Q(W H')^T with power-of-two scales (ufp4_mx_gemm_fwd_y)."""
+    M, K, N = xq.rows, xq.red, wq.rows
+    return _gemm_mx_call("ufp4_mx_gemm_fwd_y", xq, wq, M, N, K, _out(M, N, out_dtype, xq.codes.device, out))
+
+
+def mx_gemm_bwd_dx(dyq: QTensorMX, wtq: QTensorMX, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """dX [M, K] = Q(dY H') Q(W^T H')^T (ufp4_mx_gemm_bwd_dx)."""
+    M, N, K = dyq.rows, dyq.red, wtq.rows
+    return _gemm_mx_call("ufp4_mx_gemm_bwd_dx", dyq, wtq, M, N, K, _out(M, K, out_dtype, dyq.codes.device, out))
+
+
+def mx_gemm_bwd_dw(dytq: QTensorMX, xtq: QTensorMX, out_dtype=torch.float32, out=None) -> torch.Tensor:
+    """dW [N, K] = Q(dY^T H') Q(X^T H')^T (ufp4_mx_gemm_bwd_dw)."""
+    N, M, K = dytq.rows, dytq.red, xtq.rows
+    return _gemm_mx_call("ufp4_mx_gemm_bwd_dw", dytq, xtq, M, N, K, _out(N, K, out_dtype, dytq.codes.device, out))
 
 
 def group_offsets(counts, device="cuda"):

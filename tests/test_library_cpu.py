@@ -164,3 +164,30 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(U, "_LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         U.lib()
+
+
+def test_mx_validation(lib):
+    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, codes, code_pld, scales, scale_pld)
+    C32, S32 = 3072, 128  # panel strides for one 32-block
+    q = lib.ufp4_mx_quantize
+    assert q(FAKE, 16, 48, 48, 0, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, 2 * S32, None) == 2   # cols % 32
+    assert q(FAKE, 48, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, 2 * S32, None) == 2   # transposed: rows % 32
+    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, 2 * S32, None) == 2       # code stride < 3072 nkb
+    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, S32, None) == 2       # scale stride < 128 nkb
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, S32 + 4, None) == 3       # scale stride % 16
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE + 8, S32, None) == 3       # scales alignment
+    assert q(None, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, S32, None) == 1           # null input
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, C32, FAKE, S32, None) == 1           # rounding enum
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 1 << 30, FAKE, S32, None) == 5       # stride > 2^29
+    g = lib.ufp4_mx_gemm_fwd_y
+    # (a, a_pld, as, as_pld, b, b_pld, bs, bs_pld, M, N, K, c, ldc, out)
+    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 48, FAKE, 16, 0, None) == 2  # K % 32
+    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 64, FAKE, 16, 0, None) == 2  # strides < 2 blocks
+    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 8, 0, None) == 2   # ldc < N
+    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 16, 4, None) == 1  # out dtype
+    assert g(None, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 16, 0, None) == 1  # null operand
+    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE + 2, 16, 0, None) == 3  # out alignment
+    assert lib.ufp4_mx_gemm_bwd_dx(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 48, 16, FAKE, 16, 0,
+                                   None) == 2  # reduction N % 32
+    assert lib.ufp4_mx_gemm_bwd_dw(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 48, 16, 16, FAKE, 16, 0,
+                                   None) == 2  # reduction M % 32
