@@ -157,8 +157,9 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
  *     codes: FP6 E2M3 numbers (the integers -7..7 are exact), 32 per block in 24 bytes, element j in bits
  *            6j .. 6j + 5 of the block's little-endian 192-bit string;
  *     scales_dev: uint8 E8M0 bytes E + 127 (0 for an all-zero block).
- *   Layout (panels of 128 rows, 32-blocks): codes of block b of row 128p + i at codes_dev + p * code_panel_ld
- *   + b * 3072 + i * 24; its scale at scales_dev + p * scale_panel_ld + b * 128 + i. code_panel_ld >=
+ *   Layout (panels of 128 rows, 32-blocks): the 24 code bytes of block b of row 128p + i are three 8-byte
+ *   units, unit u (bytes 8u .. 8u + 7 of the string) at codes_dev + p * code_panel_ld + b * 3072 + u * 1024
+ *   + i * 8; its scale at scales_dev + p * scale_panel_ld + b * 128 + i. code_panel_ld >=
  *   3072 * red/32 and scale_panel_ld >= 128 * red/32, both multiples of 16; both pointers 16-byte aligned.
  *   Padding rows of the last panel are written as zero codes and scale byte 0. Rowwise operands of more than
  *   4194240 rows return UFP4_ERR_UNSUPPORTED.

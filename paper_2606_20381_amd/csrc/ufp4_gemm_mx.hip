@@ -10,8 +10,10 @@
 //
 // Tiling: a 128 x 128 output tile per 256-thread workgroup (4 waves of 64 x 64, 2 x 2 MFMA tiles of 32 x 32).
 // K advances 128 (four 32-blocks) per stage. A stage of one operand is a contiguous 12 KiB run of its panel
-// (the panel layout puts the 128 rows of a 32-block together) plus 512 scale bytes; it is fetched with 16-byte
-// loads one stage ahead into registers and copied unchanged into double-buffered LDS.
+// (the panel layout puts the 128 rows of a 32-block together, each row's 24 bytes as three 8-byte units in
+// three planes of 128 rows) plus 512 scale bytes; it is fetched with 16-byte loads one stage ahead into
+// registers and copied unchanged into double-buffered LDS, where a lane's operand is three 8-byte reads that
+// 32 consecutive rows make contiguous.
 
 #include "ufp4_internal.h"
 
@@ -23,34 +25,49 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 constexpr int kMxTile = 128;                    // rows of A and of B per tile (one panel each)
 constexpr int kMxStageBlocks = 4;               // 32-blocks per stage
 constexpr int kMxStageBytes = kMxStageBlocks * 3072;
-constexpr int kMxStageChunks = kMxStageBytes / 16;  // 768 chunks of 16 bytes per operand
 constexpr int kMxThreads = 256;
-constexpr int kMxChunksPerThread = kMxStageChunks / kMxThreads;  // 3
-static_assert(kMxStageChunks % kMxThreads == 0, "stage chunks");
+constexpr int kMxBufs = 3;                      // stages in LDS: the one computed and two in flight
+constexpr int kMxLoadsPerStage = 7;             // per wave: 3 of A, 3 of B, 1 of scales (16 bytes per lane)
 
-struct MxSmem {
-    uint8_t a[2][kMxStageBytes];
-    uint8_t b[2][kMxStageBytes];
-    uint32_t as[2][kMxStageBlocks * 32];  // 128 scale bytes per block
-    uint32_t bs[2][kMxStageBlocks * 32];
+struct MxStageSmem {
+    uint8_t a[kMxStageBytes];
+    uint8_t b[kMxStageBytes];
+    uint8_t s[2 * kMxStageBlocks * 128];  // scale bytes of A (512) then of B (512)
 };
 
-struct MxStage {
-    uint4 a[kMxChunksPerThread], b[kMxChunksPerThread];
-    uint32_t s;  // one scale word: of A for threads 0-127, of B for threads 128-255
-};
-
-__device__ __forceinline__ v8i load_fp6_operand(const uint8_t* p) {  // 24 bytes, 8-byte aligned
+// The 24 bytes of one row's 32-block: three 8-byte units 1024 bytes apart (planar layout, see the file
+// header), so 32 lanes reading consecutive rows touch 256 contiguous bytes per unit.
+__device__ __forceinline__ v8i load_fp6_operand(const uint8_t* p) {
     const uint2 x0 = *reinterpret_cast<const uint2*>(p);
-    const uint2 x1 = *reinterpret_cast<const uint2*>(p + 8);
-    const uint2 x2 = *reinterpret_cast<const uint2*>(p + 16);
+    const uint2 x1 = *reinterpret_cast<const uint2*>(p + 1024);
+    const uint2 x2 = *reinterpret_cast<const uint2*>(p + 2048);
     const v8i v = {(int)x0.x, (int)x0.y, (int)x1.x, (int)x1.y, (int)x2.x, (int)x2.y, 0, 0};
     return v;
 }
 
+// 16 bytes per lane from global memory straight into LDS: lane i's bytes land at lds_base + 16 i (lds_base
+// wave-uniform, in M0). Written as inline assembly so that the compiler, which does not see these LDS
+// writes, does not make every later LDS read wait for all of them; the kernel orders them itself (vmcnt
+// waits and barriers).
+__device__ __forceinline__ void dma16(const void* src, const void* lds_base) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(lds_base));
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "memory", "m0");
+}
+
+// s_waitcnt immediates (gfx9 encoding): wait until at most n vector-memory operations are outstanding,
+// and additionally for all LDS operations.
+__device__ __forceinline__ void wait_vm_lgkm(int n) {
+    switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0x0070); break;
+        default: __builtin_amdgcn_s_waitcnt(0x0070 | kMxLoadsPerStage); break;
+    }
+}
+
 template <int OUT>
 __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
-    __shared__ MxSmem sm;
+    // three separate LDS objects (not an array): the compiler then knows that loads in flight into one buffer
+    // do not alias reads of another and does not make the reads wait for them
+    __shared__ MxStageSmem sm0, sm1, sm2;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h = lane >> 5, l32 = lane & 31;
     const int wm = wave >> 1, wn = wave & 1;
@@ -62,29 +79,35 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     const int nkb = (int)j.nkb;
     const int nst = (nkb + kMxStageBlocks - 1) / kMxStageBlocks;
 
-    // Blocks past the reduction's end (last stage) are zero-filled: zero codes contribute nothing.
-    auto load = [&](MxStage& r, int s) {
+    // Stage s into buffer s % 3 with direct global-to-LDS loads: each wave instruction moves 64 x 16 bytes
+    // to 1024 contiguous LDS bytes. Wave w copies chunks (i * 256 + w * 64 + lane) of A and of B, i < 3, and
+    // scale chunk 16 w + lane (lanes 0-15; chunks 0-31 are A's 512 scale bytes, 32-63 B's). In a partial
+    // last stage the blocks past the end are written as zeros instead (codes 0, scale byte 0).
+    auto issue = [&](int s, MxStageSmem& d) {
         const int kb0 = s * kMxStageBlocks;
+        const int valid = nkb - kb0 < kMxStageBlocks ? nkb - kb0 : kMxStageBlocks;
 #pragma unroll
-        for (int i = 0; i < kMxChunksPerThread; ++i) {
-            const int c = tid + kMxThreads * i;
-            const bool ok = kb0 + c / 192 < nkb;  // 192 chunks per 32-block
-            r.a[i] = ok ? reinterpret_cast<const uint4*>(ga + (int64_t)kb0 * 3072)[c] : make_uint4(0, 0, 0, 0);
-            r.b[i] = ok ? reinterpret_cast<const uint4*>(gb + (int64_t)kb0 * 3072)[c] : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < 3; ++i) {
+            const int c0 = i * 256 + wave * 64;  // first chunk of this wave's instruction
+            const int c = c0 + lane;
+            if (c / 192 < valid) {
+                dma16(reinterpret_cast<const uint4*>(ga + (int64_t)kb0 * 3072) + c, reinterpret_cast<uint4*>(d.a) + c0);
+                dma16(reinterpret_cast<const uint4*>(gb + (int64_t)kb0 * 3072) + c, reinterpret_cast<uint4*>(d.b) + c0);
+            } else {
+                reinterpret_cast<uint4*>(d.a)[c] = make_uint4(0, 0, 0, 0);
+                reinterpret_cast<uint4*>(d.b)[c] = make_uint4(0, 0, 0, 0);
+            }
         }
-        const int w = tid & 127;  // scale word w of the stage: block w / 32
-        const uint8_t* src = tid < 128 ? gas : gbs;
-        r.s = kb0 + w / 32 < nkb ? reinterpret_cast<const uint32_t*>(src + (int64_t)kb0 * 128)[w] : 0u;
-    };
-    auto put = [&](int buf, const MxStage& r) {
-#pragma unroll
-        for (int i = 0; i < kMxChunksPerThread; ++i) {
-            const int c = tid + kMxThreads * i;
-            reinterpret_cast<uint4*>(sm.a[buf])[c] = r.a[i];
-            reinterpret_cast<uint4*>(sm.b[buf])[c] = r.b[i];
+        if (lane < 16) {
+            const int c = wave * 16 + lane;  // 0-31: A scales, 32-63: B scales; 8 chunks per block
+            const int blk = (c & 31) / 8;
+            if (blk < valid) {
+                const uint8_t* src = (c < 32 ? gas : gbs) + (int64_t)kb0 * 128 + (c & 31) * 16;
+                dma16(src, reinterpret_cast<uint4*>(d.s) + wave * 16);
+            } else {
+                reinterpret_cast<uint4*>(d.s)[c] = make_uint4(0, 0, 0, 0);
+            }
         }
-        if (tid < 128) sm.as[buf][tid] = r.s;
-        else sm.bs[buf][tid - 128] = r.s;
     };
 
     v16f acc[2][2];
@@ -95,9 +118,7 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
 
-    auto compute = [&](int buf) {
-        const uint8_t* sas = reinterpret_cast<const uint8_t*>(sm.as[buf]);
-        const uint8_t* sbs = reinterpret_cast<const uint8_t*>(sm.bs[buf]);
+    auto compute = [&](const MxStageSmem& d) {
 #pragma unroll
         for (int ks = 0; ks < kMxStageBlocks / 2; ++ks) {
             const int kk = 2 * ks + h;  // this lane's 32-block: lanes 0-31 hold K 0-31 of the step, 32-63 K 32-63
@@ -106,14 +127,14 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 #pragma unroll
             for (int a = 0; a < 2; ++a) {
                 const int row = wm * 64 + a * 32 + l32;
-                av[a] = load_fp6_operand(sm.a[buf] + kk * 3072 + row * 24);
-                sa[a] = sas[kk * 128 + row];
+                av[a] = load_fp6_operand(d.a + kk * 3072 + row * 8);
+                sa[a] = d.s[kk * 128 + row];
             }
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int col = wn * 64 + b * 32 + l32;
-                bv[b] = load_fp6_operand(sm.b[buf] + kk * 3072 + col * 24);
-                sb[b] = sbs[kk * 128 + col];
+                bv[b] = load_fp6_operand(d.b + kk * 3072 + col * 8);
+                sb[b] = d.s[512 + kk * 128 + col];
             }
 #pragma unroll
             for (int a = 0; a < 2; ++a)
@@ -125,18 +146,25 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
         }
     };
 
-    if (nst > 0) {
-        MxStage r;
-        load(r, 0);
-        put(0, r);
-        __syncthreads();
-        for (int s = 0; s < nst; ++s) {
-            const bool more = s + 1 < nst;
-            if (more) load(r, s + 1);
-            compute(s & 1);
-            if (more) put((s + 1) & 1, r);
-            __syncthreads();
-        }
+    // Stage s is computed from buffer s % 3 while stages s + 1 and s + 2 are in flight. A wave's own loads
+    // of stage s are complete once at most the 7 of stage s + 1 are outstanding; the barrier then makes every
+    // wave's part visible, and it also orders the previous stage's reads of buffer (s + 2) % 3 before the
+    // loads into it are issued.
+    // A partial last stage issues fewer loads (blocks past the end are zero-filled), so before it every
+    // wave waits for all of its loads instead of counting.
+    const bool last_full = nkb % kMxStageBlocks == 0;
+    auto step = [&](int s, MxStageSmem& cur, MxStageSmem& next2) {
+        wait_vm_lgkm(s + 1 < nst && (last_full || s + 2 < nst) ? kMxLoadsPerStage : 0);
+        __builtin_amdgcn_s_barrier();
+        if (s + 2 < nst) issue(s + 2, next2);
+        compute(cur);
+    };
+    if (nst > 0) issue(0, sm0);
+    if (nst > 1) issue(1, sm1);
+    for (int s = 0; s < nst; s += 3) {
+        step(s, sm0, sm2);
+        if (s + 1 < nst) step(s + 1, sm1, sm0);
+        if (s + 2 < nst) step(s + 2, sm2, sm1);
     }
 
 #pragma unroll

@@ -490,7 +490,9 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
 // Power-of-two block scales (the scale hierarchy is free, Sec. 4): blocks of 32 along the reduction axis
 // share one scale 2^E, E the smallest integer with amax <= 7 * 2^E, stored as the E8M0 byte E + 127; the
 // RHT stays block-16; codes are the uniform levels -7..7 stored as FP6 E2M3 numbers, 32 of them in 24 bytes
-// (element j in bits 6j .. 6j + 5): the A/B operand format of v_mfma_scale_f32_32x32x64_f8f6f4.
+// (element j in bits 6j .. 6j + 5): the A/B operand format of v_mfma_scale_f32_32x32x64_f8f6f4. In a panel
+// the 24 bytes of row i's block b are three 8-byte units, unit u at b * 3072 + u * 1024 + i * 8, so that
+// consecutive rows' units are contiguous (conflict-free 8-byte LDS reads in the GEMM).
 // ------------------------------------------------------------------------------------------------
 constexpr int kMxBlock = 32;
 
@@ -570,7 +572,7 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
 }
 
 // Rowwise: wave w of a workgroup takes 32-block blockIdx.x * 4 + w of 64 consecutive operand rows (lane =
-// row), so the four waves read 256 contiguous bytes of each row and every wave writes 64 x 24 contiguous
+// row), so the four waves read 256 contiguous bytes of each row and every wave writes three runs of 64 x 8
 // bytes of codes and 64 scale bytes. Rows past the operand's last one (panel padding) get zeros.
 template <int ROUND, bool RHT>
 __global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, int64_t qrows,
@@ -594,16 +596,15 @@ __global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict
         quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * b), (uint32_t)r, out, e8);
     }
     const int64_t P = r >> 7, ri = r & 127;
-    uint2* dc = reinterpret_cast<uint2*>(codes + P * code_pld + b * 3072 + ri * 24);
-    dc[0] = make_uint2(out[0], out[1]);
-    dc[1] = make_uint2(out[2], out[3]);
-    dc[2] = make_uint2(out[4], out[5]);
+    uint8_t* dc = codes + P * code_pld + b * 3072 + ri * 8;  // three planes of 8-byte units
+#pragma unroll
+    for (int q = 0; q < 3; ++q) *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
     scales[P * scale_pld + b * 128 + ri] = (uint8_t)e8;
 }
 
 // Transposed: a thread loads 32 rows x 4 columns of X (one 8-byte load per row) and quantizes the four
 // column blocks from registers; sixteen threads cover 64 columns, a workgroup 16 row blocks. The four
-// operand rows of a block leave as 96 contiguous bytes of codes and one word of scales. Columns past `cols`
+// operand rows of a block leave as three runs of 32 bytes of codes and one word of scales. Columns past `cols`
 // (panel padding) hold zeros and quantize to zero codes and scale byte 0.
 template <int ROUND, bool RHT>
 __global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
@@ -643,13 +644,13 @@ __global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict
             quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * gb), (uint32_t)(cbase + q), out[q], e8[q]);
         }
         const int64_t P = cbase >> 7, ri = cbase & 127;
-        uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 3072 + ri * 24);  // 96 bytes
-        dc[0] = make_uint4(out[0][0], out[0][1], out[0][2], out[0][3]);
-        dc[1] = make_uint4(out[0][4], out[0][5], out[1][0], out[1][1]);
-        dc[2] = make_uint4(out[1][2], out[1][3], out[1][4], out[1][5]);
-        dc[3] = make_uint4(out[2][0], out[2][1], out[2][2], out[2][3]);
-        dc[4] = make_uint4(out[2][4], out[2][5], out[3][0], out[3][1]);
-        dc[5] = make_uint4(out[3][2], out[3][3], out[3][4], out[3][5]);
+        uint8_t* dc = codes + P * code_pld + gb * 3072 + ri * 8;  // per plane, 4 rows x 8 bytes = 32 bytes
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            uint4* d = reinterpret_cast<uint4*>(dc + q * 1024);
+            d[0] = make_uint4(out[0][2 * q], out[0][2 * q + 1], out[1][2 * q], out[1][2 * q + 1]);
+            d[1] = make_uint4(out[2][2 * q], out[2][2 * q + 1], out[3][2 * q], out[3][2 * q + 1]);
+        }
         *reinterpret_cast<uint32_t*>(scales + P * scale_pld + gb * 128 + ri) =
             e8[0] | (e8[1] << 8) | (e8[2] << 16) | (e8[3] << 24);
     }

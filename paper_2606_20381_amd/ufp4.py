@@ -195,7 +195,8 @@ def quantize_dual(x: torch.Tensor, *, fmt: int = UNIFORM, rht_rows: bool = True,
 @dataclass
 class QTensorMX:
     """An operand quantized with power-of-two 1x32 scales, [rows, red] in panels of 128 rows: 32-block b of the
-    panel's rows is contiguous, 128 x 24 bytes of FP6 E2M3 codes at b * 3072 and 128 E8M0 bytes at b * 128."""
+    panel's rows is contiguous, 3072 bytes of FP6 E2M3 codes at b * 3072 (three planes of 128 x 8 bytes: row
+    i's 24-byte string is plane 0, 1, 2 at i * 8) and 128 E8M0 bytes at b * 128."""
 
     codes: torch.Tensor  # uint8 [panels, >= 3072 * red/32]
     scales: torch.Tensor  # uint8 [panels, >= 128 * red/32]
@@ -217,7 +218,7 @@ class QTensorMX:
     def codes_rows(self) -> torch.Tensor:
         """Codes as uint8 [rows, red * 3/4] (24 bytes per 32-block), row-major (a copy)."""
         nkb = self.red // 32
-        v = self.codes[:, : nkb * 3072].reshape(self.panels, nkb, PANEL_ROWS, 24).permute(0, 2, 1, 3)
+        v = self.codes[:, : nkb * 3072].reshape(self.panels, nkb, 3, PANEL_ROWS, 8).permute(0, 3, 1, 2, 4)
         return v.reshape(self.panels * PANEL_ROWS, nkb * 24)[: self.rows]
 
     def scales_rows(self) -> torch.Tensor:

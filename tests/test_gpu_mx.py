@@ -76,7 +76,7 @@ def _check(t_cpu, layout, rounding, rht, mask, seed, stream, what=""):
     tail = q.panels * U.PANEL_ROWS - q.rows  # padding rows of the last panel are zero
     if tail:
         nkb = red // 32
-        lc = q.codes[-1, : nkb * 3072].reshape(nkb, U.PANEL_ROWS, 24)[:, U.PANEL_ROWS - tail:]
+        lc = q.codes[-1, : nkb * 3072].reshape(nkb, 3, U.PANEL_ROWS, 8)[:, :, U.PANEL_ROWS - tail:]
         ls = q.scales[-1, : nkb * U.PANEL_ROWS].reshape(nkb, U.PANEL_ROWS)[:, U.PANEL_ROWS - tail:]
         assert int(lc.count_nonzero()) == 0 and int(ls.count_nonzero()) == 0, f"{what}: padding not zero"
 
