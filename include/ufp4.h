@@ -172,7 +172,7 @@ int ufp4_mx_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, 
  * ufp4_mx_gemm_fwd_y / _bwd_dx / _bwd_dw -- the three passes (shapes and operand roles as the ufp4_gemm_*
  *   calls below) on operands from ufp4_mx_quantize: C[i, j] = sum_k A[i,k] 2^(eA - 127) B[j,k] 2^(eB - 127)
  *   with the scales of each element's 32-block, accumulated in fp32 by the matrix core; output fp32 or bf16
- *   (RNE) with leading dimension ldc. K % 32 == 0. A left operand of more than 8388480 rows returns
+ *   (RNE) with leading dimension ldc. K % 32 == 0. Outputs of 2^31 or more 128 x 128 tiles return
  *   UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_mx_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_panel_ld, const void *x_scales_dev,

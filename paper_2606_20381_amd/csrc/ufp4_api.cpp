@@ -152,7 +152,9 @@ int mx_gemm_impl(const void* a, int64_t a_pld, const void* as, int64_t as_pld, c
     if (st != UFP4_OK) return st;
     if (ldc < rows_b) return UFP4_ERR_SHAPE;
     if (!aligned(c, out_dtype == UFP4_OUT_F32 ? 4 : 2)) return UFP4_ERR_ALIGN;
-    if ((rows_a + 127) / 128 > 65535 || red / 32 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    // one workgroup per 128 x 128 output tile on a one-dimensional grid
+    if (((rows_a + 127) / 128) * ((rows_b + 127) / 128) >= (int64_t(1) << 31) || red / 32 >= (int64_t(1) << 31))
+        return UFP4_ERR_UNSUPPORTED;
     if (rows_a == 0 || rows_b == 0) return UFP4_OK;
     MxGemmJob j{};
     j.out_dtype = out_dtype;

@@ -63,6 +63,22 @@ __device__ __forceinline__ void wait_vm_lgkm(int n) {
     }
 }
 
+// Workgroup -> output tile. Workgroups are dealt to the 8 XCDs round robin (workgroup L to XCD L % 8) and each
+// XCD has its own L2, so the first 8 * floor(T / 8) workgroups are renumbered to give XCD k the contiguous
+// range of tiles [k T/8, (k + 1) T/8); tiles are then ordered in bands of kGroupRows tile rows, column by
+// column within a band, so that the workgroups running together on one XCD share a few A and B panels.
+constexpr int kGroupRows = 8;
+__device__ __forceinline__ void tile_of(int64_t L, int64_t gy, int64_t gx, int64_t& tm, int64_t& tn) {
+    const int64_t T = gx * gy, per = T / 8;
+    const int64_t t = L < 8 * per ? (L % 8) * per + L / 8 : L;
+    const int64_t band = t / (kGroupRows * gx);
+    const int64_t first = band * kGroupRows;
+    const int64_t rows = gy - first < kGroupRows ? gy - first : kGroupRows;
+    const int64_t r = t - band * kGroupRows * gx;
+    tm = first + r % rows;
+    tn = r / rows;
+}
+
 template <int OUT>
 __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     // three separate LDS objects (not an array): the compiler then knows that loads in flight into one buffer
@@ -71,7 +87,8 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h = lane >> 5, l32 = lane & 31;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t tm = blockIdx.y, tn = blockIdx.x;  // tile index = panel index of A and of B
+    int64_t tm, tn;  // tile index = panel index of A and of B
+    tile_of(blockIdx.x, (j.M + kMxTile - 1) / kMxTile, (j.N + kMxTile - 1) / kMxTile, tm, tn);
     const uint8_t* ga = j.a + tm * j.a_pld;
     const uint8_t* gas = j.as + tm * j.as_pld;
     const uint8_t* gb = j.b + tn * j.b_pld;
@@ -189,8 +206,9 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 }
 
 hipError_t launch_gemm_mx(const MxGemmJob& j, hipStream_t s) {
-    const dim3 grid((unsigned)((j.N + kMxTile - 1) / kMxTile), (unsigned)((j.M + kMxTile - 1) / kMxTile));
-    if (grid.x == 0 || grid.y == 0) return hipSuccess;
+    const int64_t tiles = ((j.N + kMxTile - 1) / kMxTile) * ((j.M + kMxTile - 1) / kMxTile);
+    if (tiles == 0) return hipSuccess;
+    const dim3 grid((unsigned)tiles);
     if (j.out_dtype == kOutBF16) gemm_mx_kernel<kOutBF16><<<grid, kMxThreads, 0, s>>>(j);
     else gemm_mx_kernel<kOutF32><<<grid, kMxThreads, 0, s>>>(j);
     return hipGetLastError();
