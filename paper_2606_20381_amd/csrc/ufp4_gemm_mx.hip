@@ -45,13 +45,14 @@ __device__ __forceinline__ v8i load_fp6_operand(const uint8_t* p) {
     return v;
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane i's bytes land at lds_base + 16 i (lds_base
-// wave-uniform, in M0). Written as inline assembly so that the compiler, which does not see these LDS
-// writes, does not make every later LDS read wait for all of them; the kernel orders them itself (vmcnt
-// waits and barriers).
-__device__ __forceinline__ void dma16(const void* src, const void* lds_base) {
+// 16 bytes per lane from global memory straight into LDS: lane i reads sbase + voff_i and its bytes land at
+// lds_base + 16 i (sbase and lds_base wave-uniform, lds_base in M0). Written as inline assembly so that the
+// compiler, which does not see these LDS writes, does not make every later LDS read wait for all of them; the
+// kernel orders them itself (vmcnt waits and barriers).
+__device__ __forceinline__ void dma16(uint32_t voff, const void* sbase, const void* lds_base) {
     const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(lds_base));
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(m0) : "memory", "m0");
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(m0)
+                 : "memory", "m0");
 }
 
 // s_waitcnt immediates (gfx9 encoding): wait until at most n vector-memory operations are outstanding,
@@ -84,46 +85,42 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     // three separate LDS objects (not an array): the compiler then knows that loads in flight into one buffer
     // do not alias reads of another and does not make the reads wait for them
     __shared__ MxStageSmem sm0, sm1, sm2;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: load addresses stay scalar
     const int h = lane >> 5, l32 = lane & 31;
     const int wm = wave >> 1, wn = wave & 1;
     int64_t tm, tn;  // tile index = panel index of A and of B
     tile_of(blockIdx.x, (j.M + kMxTile - 1) / kMxTile, (j.N + kMxTile - 1) / kMxTile, tm, tn);
-    const uint8_t* ga = j.a + tm * j.a_pld;
-    const uint8_t* gas = j.as + tm * j.as_pld;
-    const uint8_t* gb = j.b + tn * j.b_pld;
-    const uint8_t* gbs = j.bs + tn * j.bs_pld;
+    const uint8_t* const ga = j.a + tm * j.a_pld;
+    const uint8_t* const gb = j.b + tn * j.b_pld;
+    // this wave's scale run: waves 0, 1 load A's 512 scale bytes, waves 2, 3 B's
+    const uint8_t* const gs = wave < 2 ? j.as + tm * j.as_pld : j.bs + tn * j.bs_pld;
     const int nkb = (int)j.nkb;
     const int nst = (nkb + kMxStageBlocks - 1) / kMxStageBlocks;
+    const int kb_last = nkb - 1;
 
-    // Stage s into buffer s % 3 with direct global-to-LDS loads: each wave instruction moves 64 x 16 bytes
-    // to 1024 contiguous LDS bytes. Wave w copies chunks (i * 256 + w * 64 + lane) of A and of B, i < 3, and
-    // scale chunk 16 w + lane (lanes 0-15; chunks 0-31 are A's 512 scale bytes, 32-63 B's). In a partial
-    // last stage the blocks past the end are written as zeros instead (codes 0, scale byte 0).
+    // Stage s into a buffer with direct global-to-LDS loads: each wave instruction moves 64 x 16 bytes to
+    // 1024 contiguous LDS bytes. Wave w copies chunks (i * 256 + w * 64 + lane) of A and of B, i < 3, and scale
+    // chunk 16 w + lane (lanes 0-15; chunks 0-31 are A's 512 scale bytes, 32-63 B's). Every wave issues the
+    // same 7 loads for every stage: blocks past the end of the reduction (partial last stage) are read from the
+    // last block instead, and compute() gives them zero scales.
+    const uint32_t voff = (uint32_t)lane * 16;
     auto issue = [&](int s, MxStageSmem& d) {
         const int kb0 = s * kMxStageBlocks;
-        const int valid = nkb - kb0 < kMxStageBlocks ? nkb - kb0 : kMxStageBlocks;
 #pragma unroll
         for (int i = 0; i < 3; ++i) {
-            const int c0 = i * 256 + wave * 64;  // first chunk of this wave's instruction
-            const int c = c0 + lane;
-            if (c / 192 < valid) {
-                dma16(reinterpret_cast<const uint4*>(ga + (int64_t)kb0 * 3072) + c, reinterpret_cast<uint4*>(d.a) + c0);
-                dma16(reinterpret_cast<const uint4*>(gb + (int64_t)kb0 * 3072) + c, reinterpret_cast<uint4*>(d.b) + c0);
-            } else {
-                reinterpret_cast<uint4*>(d.a)[c] = make_uint4(0, 0, 0, 0);
-                reinterpret_cast<uint4*>(d.b)[c] = make_uint4(0, 0, 0, 0);
-            }
+            const int c0 = i * 256 + wave * 64;  // 64-chunk groups never straddle a block (192 chunks)
+            const int blk = c0 / 192;
+            const int kb = kb0 + blk < kb_last ? kb0 + blk : kb_last;
+            const int64_t off = (int64_t)kb * 3072 + (c0 - blk * 192) * 16;
+            dma16(voff, ga + off, reinterpret_cast<uint4*>(d.a) + c0);
+            dma16(voff, gb + off, reinterpret_cast<uint4*>(d.b) + c0);
         }
         if (lane < 16) {
-            const int c = wave * 16 + lane;  // 0-31: A scales, 32-63: B scales; 8 chunks per block
-            const int blk = (c & 31) / 8;
-            if (blk < valid) {
-                const uint8_t* src = (c < 32 ? gas : gbs) + (int64_t)kb0 * 128 + (c & 31) * 16;
-                dma16(src, reinterpret_cast<uint4*>(d.s) + wave * 16);
-            } else {
-                reinterpret_cast<uint4*>(d.s)[c] = make_uint4(0, 0, 0, 0);
-            }
+            // chunks 16 w + lane: within the operand's run, chunk (w & 1) * 16 + lane of block chunk / 8
+            const int cc = (wave & 1) * 16 + lane, blk = cc >> 3;
+            const int kb = kb0 + blk < kb_last ? kb0 + blk : kb_last;
+            dma16((uint32_t)(kb * 128 + (cc & 7) * 16), gs, reinterpret_cast<uint4*>(d.s) + wave * 16);
         }
     };
 
@@ -135,23 +132,24 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
 
-    auto compute = [&](const MxStageSmem& d) {
+    auto compute = [&](const MxStageSmem& d, int valid) {
 #pragma unroll
         for (int ks = 0; ks < kMxStageBlocks / 2; ++ks) {
             const int kk = 2 * ks + h;  // this lane's 32-block: lanes 0-31 hold K 0-31 of the step, 32-63 K 32-63
+            const bool live = kk < valid;  // blocks past the end get scale 2^-127 on both sides: products 0
             v8i av[2], bv[2];
             int sa[2], sb[2];
 #pragma unroll
             for (int a = 0; a < 2; ++a) {
                 const int row = wm * 64 + a * 32 + l32;
                 av[a] = load_fp6_operand(d.a + kk * 3072 + row * 8);
-                sa[a] = d.s[kk * 128 + row];
+                sa[a] = live ? d.s[kk * 128 + row] : 0;
             }
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int col = wn * 64 + b * 32 + l32;
                 bv[b] = load_fp6_operand(d.b + kk * 3072 + col * 8);
-                sb[b] = d.s[512 + kk * 128 + col];
+                sb[b] = live ? d.s[512 + kk * 128 + col] : 0;
             }
 #pragma unroll
             for (int a = 0; a < 2; ++a)
@@ -167,14 +165,12 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     // of stage s are complete once at most the 7 of stage s + 1 are outstanding; the barrier then makes every
     // wave's part visible, and it also orders the previous stage's reads of buffer (s + 2) % 3 before the
     // loads into it are issued.
-    // A partial last stage issues fewer loads (blocks past the end are zero-filled), so before it every
-    // wave waits for all of its loads instead of counting.
-    const bool last_full = nkb % kMxStageBlocks == 0;
     auto step = [&](int s, MxStageSmem& cur, MxStageSmem& next2) {
-        wait_vm_lgkm(s + 1 < nst && (last_full || s + 2 < nst) ? kMxLoadsPerStage : 0);
+        wait_vm_lgkm(s + 1 < nst ? kMxLoadsPerStage : 0);
         __builtin_amdgcn_s_barrier();
         if (s + 2 < nst) issue(s + 2, next2);
-        compute(cur);
+        const int left = nkb - s * kMxStageBlocks;
+        compute(cur, left < kMxStageBlocks ? left : kMxStageBlocks);
     };
     if (nst > 0) issue(0, sm0);
     if (nst > 1) issue(1, sm1);
