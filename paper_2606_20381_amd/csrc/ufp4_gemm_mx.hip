@@ -8,12 +8,12 @@
 // per-16 scales of the main recipe, so the kernel is bound by the matrix cores and by how fast operand tiles
 // reach them.
 //
-// Tiling: a 128 x 128 output tile per 256-thread workgroup (4 waves of 64 x 64, 2 x 2 MFMA tiles of 32 x 32).
-// K advances 128 (four 32-blocks) per stage. A stage of one operand is a contiguous 12 KiB run of its panel
-// (the panel layout puts the 128 rows of a 32-block together, each row's 24 bytes as three 8-byte units in
-// three planes of 128 rows) plus 512 scale bytes; it is fetched with 16-byte loads one stage ahead into
-// registers and copied unchanged into double-buffered LDS, where a lane's operand is three 8-byte reads that
-// 32 consecutive rows make contiguous.
+// Tiling: a 256 x 256 output tile per 512-thread workgroup (8 waves of 128 x 64, 4 x 2 MFMA tiles of 32 x 32,
+// two waves per SIMD, one workgroup per CU). K advances 128 (four 32-blocks) per stage. A stage of one panel
+// is a contiguous 12 KiB run (the panel layout puts the 128 rows of a 32-block together, each row's 24 bytes
+// as three 8-byte units in three planes of 128 rows) plus 512 scale bytes; stages are copied unchanged from
+// global memory into a three-deep LDS ring by direct-to-LDS loads issued two stages ahead, and a lane's
+// operand is three 8-byte LDS reads that 32 consecutive rows make contiguous.
 
 #include "ufp4_internal.h"
 
@@ -22,17 +22,17 @@ namespace ufp4 {
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 
-constexpr int kMxTile = 128;                    // rows of A and of B per tile (one panel each)
+constexpr int kMxTile = 256;                    // rows of A and of B per workgroup tile (two panels each)
 constexpr int kMxStageBlocks = 4;               // 32-blocks per stage
-constexpr int kMxStageBytes = kMxStageBlocks * 3072;
-constexpr int kMxThreads = 256;
+constexpr int kMxStageBytes = kMxStageBlocks * 3072;  // one panel's codes per stage
+constexpr int kMxThreads = 512;                 // 8 waves, two per SIMD, each a 128 x 64 tile
 constexpr int kMxBufs = 3;                      // stages in LDS: the one computed and two in flight
 constexpr int kMxLoadsPerStage = 7;             // per wave: 3 of A, 3 of B, 1 of scales (16 bytes per lane)
 
 struct MxStageSmem {
-    uint8_t a[kMxStageBytes];
-    uint8_t b[kMxStageBytes];
-    uint8_t s[2 * kMxStageBlocks * 128];  // scale bytes of A (512) then of B (512)
+    uint8_t a[2][kMxStageBytes];  // the tile's two panels of A
+    uint8_t b[2][kMxStageBytes];
+    uint8_t s[2][2][kMxStageBlocks * 128];  // scale bytes: [A, B][panel][block * 128 + row]
 };
 
 // The 24 bytes of one row's 32-block: three 8-byte units 1024 bytes apart (planar layout, see the file
@@ -88,45 +88,54 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: load addresses stay scalar
     const int h = lane >> 5, l32 = lane & 31;
-    const int wm = wave >> 1, wn = wave & 1;
-    int64_t tm, tn;  // tile index = panel index of A and of B
+    const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows wm * 128 .. + 127, cols wn * 64 .. + 63
+    int64_t tm, tn;
     tile_of(blockIdx.x, (j.M + kMxTile - 1) / kMxTile, (j.N + kMxTile - 1) / kMxTile, tm, tn);
-    const uint8_t* const ga = j.a + tm * j.a_pld;
-    const uint8_t* const gb = j.b + tn * j.b_pld;
-    // this wave's scale run: waves 0, 1 load A's 512 scale bytes, waves 2, 3 B's
-    const uint8_t* const gs = wave < 2 ? j.as + tm * j.as_pld : j.bs + tn * j.bs_pld;
+    // The tile's two panels of each operand. A panel past the operand's last one (a tile over the edge) is
+    // replaced by the last panel: those rows only feed outputs that are not stored.
+    const int64_t pa_last = (j.M - 1) / 128, pb_last = (j.N - 1) / 128;
+    const int64_t pa1 = 2 * tm + 1 < pa_last ? 2 * tm + 1 : pa_last;
+    const int64_t pb1 = 2 * tn + 1 < pb_last ? 2 * tn + 1 : pb_last;
+    const uint8_t* const ga0 = j.a + 2 * tm * j.a_pld;
+    const uint8_t* const ga1 = j.a + pa1 * j.a_pld;
+    const uint8_t* const gb0 = j.b + 2 * tn * j.b_pld;
+    const uint8_t* const gb1 = j.b + pb1 * j.b_pld;
+    // this wave's scale run: chunks 16 w .. 16 w + 15 of [A panel 0, A panel 1, B panel 0, B panel 1] x 32
+    const int sop = wave >> 2, sp = (wave >> 1) & 1;
+    const uint8_t* const gs = sop == 0 ? j.as + (sp ? pa1 : 2 * tm) * j.as_pld : j.bs + (sp ? pb1 : 2 * tn) * j.bs_pld;
+    const int64_t M = j.M, N = j.N, ldc = j.ldc;
+    void* const cptr = j.c;
     const int nkb = (int)j.nkb;
     const int nst = (nkb + kMxStageBlocks - 1) / kMxStageBlocks;
     const int kb_last = nkb - 1;
 
     // Stage s into a buffer with direct global-to-LDS loads: each wave instruction moves 64 x 16 bytes to
-    // 1024 contiguous LDS bytes. Wave w copies chunks (i * 256 + w * 64 + lane) of A and of B, i < 3, and scale
-    // chunk 16 w + lane (lanes 0-15; chunks 0-31 are A's 512 scale bytes, 32-63 B's). Every wave issues the
-    // same 7 loads for every stage: blocks past the end of the reduction (partial last stage) are read from the
-    // last block instead, and compute() gives them zero scales.
+    // 1024 contiguous LDS bytes. Per operand a stage is 2 panels x 768 chunks; wave w copies chunks
+    // i * 512 + w * 64 + lane (i < 3) of the pair, panel = chunk / 768, and scale chunks 16 w + lane (lanes
+    // 0-15). Every wave issues the same 7 loads for every stage: blocks past the end of the reduction
+    // (partial last stage) are read from the last block instead, and compute() gives them zero scales.
     const uint32_t voff = (uint32_t)lane * 16;
     auto issue = [&](int s, MxStageSmem& d) {
         const int kb0 = s * kMxStageBlocks;
 #pragma unroll
         for (int i = 0; i < 3; ++i) {
-            const int c0 = i * 256 + wave * 64;  // 64-chunk groups never straddle a block (192 chunks)
-            const int blk = c0 / 192;
+            const int c0 = i * 512 + wave * 64;  // 64-chunk groups never straddle a panel or a block
+            const int p = c0 / 768, cp0 = c0 - p * 768, blk = cp0 / 192;
             const int kb = kb0 + blk < kb_last ? kb0 + blk : kb_last;
-            const int64_t off = (int64_t)kb * 3072 + (c0 - blk * 192) * 16;
-            dma16(voff, ga + off, reinterpret_cast<uint4*>(d.a) + c0);
-            dma16(voff, gb + off, reinterpret_cast<uint4*>(d.b) + c0);
+            const int64_t off = (int64_t)kb * 3072 + (cp0 - blk * 192) * 16;
+            dma16(voff, (p ? ga1 : ga0) + off, reinterpret_cast<uint4*>(d.a[p]) + cp0);
+            dma16(voff, (p ? gb1 : gb0) + off, reinterpret_cast<uint4*>(d.b[p]) + cp0);
         }
         if (lane < 16) {
-            // chunks 16 w + lane: within the operand's run, chunk (w & 1) * 16 + lane of block chunk / 8
-            const int cc = (wave & 1) * 16 + lane, blk = cc >> 3;
+            const int cc = (wave & 1) * 16 + lane, blk = cc >> 3;  // chunk within the 32-chunk run
             const int kb = kb0 + blk < kb_last ? kb0 + blk : kb_last;
-            dma16((uint32_t)(kb * 128 + (cc & 7) * 16), gs, reinterpret_cast<uint4*>(d.s) + wave * 16);
+            dma16((uint32_t)(kb * 128 + (cc & 7) * 16), gs, reinterpret_cast<uint4*>(&d.s[0][0][0]) + wave * 16);
         }
     };
 
-    v16f acc[2][2];
+    v16f acc[4][2];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -137,27 +146,25 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
         for (int ks = 0; ks < kMxStageBlocks / 2; ++ks) {
             const int kk = 2 * ks + h;  // this lane's 32-block: lanes 0-31 hold K 0-31 of the step, 32-63 K 32-63
             const bool live = kk < valid;  // blocks past the end get scale 2^-127 on both sides: products 0
-            v8i av[2], bv[2];
-            int sa[2], sb[2];
-#pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                const int row = wm * 64 + a * 32 + l32;
-                av[a] = load_fp6_operand(d.a + kk * 3072 + row * 8);
-                sa[a] = live ? d.s[kk * 128 + row] : 0;
-            }
+            v8i av[4], bv[2];
+            int sa[4], sb[2];
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
-                const int col = wn * 64 + b * 32 + l32;
-                bv[b] = load_fp6_operand(d.b + kk * 3072 + col * 8);
-                sb[b] = live ? d.s[512 + kk * 128 + col] : 0;
+                const int col = wn * 64 + b * 32 + l32, p = col >> 7, r = col & 127;
+                bv[b] = load_fp6_operand(d.b[p] + kk * 3072 + r * 8);
+                sb[b] = live ? d.s[1][p][kk * 128 + r] : 0;
             }
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < 4; ++a) {
+                const int r = a * 32 + l32;  // row within panel wm
+                av[a] = load_fp6_operand(d.a[wm] + kk * 3072 + r * 8);
+                sa[a] = live ? d.s[0][wm][kk * 128 + r] : 0;
 #pragma unroll
                 for (int b = 0; b < 2; ++b)
                     // formats 2 = FP6 E2M3 for both operands; the scale bytes sit in byte 0 of sa / sb
                     acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[a], bv[b], acc[a][b], 2, 2, 0,
                                                                                 sa[a], 0, sb[b]);
+            }
         }
     };
 
@@ -181,20 +188,20 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     }
 
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
+    for (int a = 0; a < 4; ++a) {
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const int64_t col = tn * kMxTile + wn * 64 + b * 32 + l32;
-            if (col >= j.N) continue;
+            if (col >= N) continue;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int64_t row = tm * kMxTile + wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                if (row >= j.M) continue;
+                const int64_t row = tm * kMxTile + wm * 128 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                if (row >= M) continue;
                 const float v = acc[a][b][i];
                 if constexpr (OUT == kOutF32) {
-                    static_cast<float*>(j.c)[row * j.ldc + col] = v;
+                    static_cast<float*>(cptr)[row * ldc + col] = v;
                 } else {
-                    static_cast<uint16_t*>(j.c)[row * j.ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
+                    static_cast<uint16_t*>(cptr)[row * ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
                 }
             }
         }
