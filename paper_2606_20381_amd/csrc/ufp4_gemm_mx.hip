@@ -187,21 +187,30 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
         if (s + 2 < nst) step(s + 2, sm2, sm1);
     }
 
+    // Epilogue: lane (l32, h) holds rows 8q + 4h + t (q, t < 4) of column l32 of each 32 x 32 tile; a store
+    // instruction writes two runs of 32 consecutive outputs. Tiles inside the output skip the bounds tests.
+    const bool inside = (tm + 1) * kMxTile <= M && (tn + 1) * kMxTile <= N;
+    auto store = [&](int64_t row, int64_t col, float v) {
+        if constexpr (OUT == kOutF32) {
+            static_cast<float*>(cptr)[row * ldc + col] = v;
+        } else {
+            static_cast<uint16_t*>(cptr)[row * ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
+        }
+    };
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const int64_t col = tn * kMxTile + wn * 64 + b * 32 + l32;
-            if (col >= N) continue;
+            const int64_t row0 = tm * kMxTile + wm * 128 + a * 32 + 4 * h;
+            if (inside) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int64_t row = tm * kMxTile + wm * 128 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                if (row >= M) continue;
-                const float v = acc[a][b][i];
-                if constexpr (OUT == kOutF32) {
-                    static_cast<float*>(cptr)[row * ldc + col] = v;
-                } else {
-                    static_cast<uint16_t*>(cptr)[row * ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
+                for (int i = 0; i < 16; ++i) store(row0 + 8 * (i >> 2) + (i & 3), col, acc[a][b][i]);
+            } else if (col < N) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int64_t row = row0 + 8 * (i >> 2) + (i & 3);
+                    if (row < M) store(row, col, acc[a][b][i]);
                 }
             }
         }
