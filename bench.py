@@ -338,7 +338,7 @@ def cpu_baseline(wl, tokens: int = 512, recipe: str = "ufp4"):
         "unit": "TFLOP/s",
         "cores": int(blas),
         "kind": "oracle",
-        "sample": (f"whole UFP4 layer step (6 quantizations + 3 fp64 GEMMs) on {tokens} of {wl.x.shape[0]} "
+        "sample": (f"whole {recipe} layer step (6 quantizations + 3 fp64 GEMMs) on {tokens} of {wl.x.shape[0]} "
                    f"tokens, full {N}x{K} weight; {dt:.1f} s; elementwise numpy on 1 thread, fp64 matmul on "
                    f"{blas} BLAS threads; host {platform.processor() or platform.machine()}, "
                    f"os.cpu_count()={os.cpu_count()}"),

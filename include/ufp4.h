@@ -150,9 +150,10 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
  * 1x32 block that gfx950's scaled matrix-core instruction applies itself.
  *
  * ufp4_mx_quantize -- fused RHT + quantization with power-of-two scales. Per 1x32 block along the reduction
- *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = the smallest integer with
- *   amax |y| <= 7 * 2^E; v = y * 2^-E (exact); codes -7..7 by RTNE or SR (same rules and Philox draws, the
- *   counters numbering 16-blocks). Arguments as ufp4_rht_quantize, except:
+ *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = floor(log2 amax |y|) - 2 (the OCP
+ *   Microscaling shared-exponent rule, the levels read as FP6 E2M3 numbers); v = y * 2^-E (exact, |v| < 8);
+ *   codes -7..7 by RTNE or SR (same rules and Philox draws, the counters numbering 16-blocks), |v| > 7
+ *   clamped to the top level. Arguments as ufp4_rht_quantize, except:
  *     red % 32 == 0 (cols when transpose = 0, rows when transpose = 1);
  *     codes: FP6 E2M3 numbers (the integers -7..7 are exact), 32 per block in 24 bytes, element j in bits
  *            6j .. 6j + 5 of the block's little-endian 192-bit string;

@@ -441,9 +441,10 @@ def gemm_nt_grouped(a_idx, a_scales, b_idx, b_scales, fmt: int, a_rows=None, b_r
 
 # ---------------------------------------------------------------------------------------------------
 # The uniform grid with power-of-two block scales (Sec. 4: the scale hierarchy is orthogonal to the grid
-# and may follow the hardware). Quantization blocks of 32 along the reduction axis share one scale 2^E,
-# stored as an E8M0 byte E + 127; the RHT stays block-16 (two RHT blocks per scale block) and the codes are
-# the uniform levels -7..7, stored as FP6 E2M3 numbers (every integer up to 7 is exact in E2M3).
+# and may follow the hardware). Quantization blocks of 32 along the reduction axis share one scale 2^E
+# (OCP Microscaling rule), stored as an E8M0 byte E + 127; the RHT stays block-16 (two RHT blocks per scale
+# block) and the codes are the uniform levels -7..7, stored as FP6 E2M3 numbers (every integer up to 7 is
+# exact in E2M3).
 # ---------------------------------------------------------------------------------------------------
 
 MX_BLOCK = 32
@@ -451,23 +452,24 @@ E8M0_BIAS = 127
 
 
 def mx_scale_exponent(amax) -> np.ndarray:
-    """Per block, the smallest integer E with amax <= 7 * 2^E: the power-of-two scale that keeps every
-    |y / 2^E| within the top level 7 (no clipping). amax = 0 gives E = -127 (E8M0 byte 0); a zero block's
-    codes are all 0 whatever the scale."""
+    """Per block, E = floor(log2 amax) - 2: the shared-exponent rule of the OCP Microscaling formats
+    (floor(log2 amax) minus the exponent of the element format's largest binade) with the integer levels
+    -7..7 read as FP6 E2M3 numbers, whose largest binade is [4, 8). Then amax / 2^E lies in [4, 8): the
+    top element may exceed the top level 7 and is clamped to it (the rounding clamps, as for the fp32
+    scales). amax = 0 gives E = -127 (E8M0 byte 0); a zero block's codes are all 0 whatever the scale."""
     a = np.asarray(amax, dtype=np.float64)
-    m, e = np.frexp(a)  # a = m * 2^e with 0.5 <= m < 1; 7 * 2^E >= a  <=>  2^(E - e) >= m / 7
-    E = np.where(m <= 0.875, e - 3, e - 2)  # m / 7 <= 1/8  <=>  m <= 7/8
-    return np.where(a > 0, E, -E8M0_BIAS).astype(np.int64)
+    m, e = np.frexp(a)  # a = m * 2^e with 0.5 <= m < 1, so floor(log2 a) = e - 1
+    return np.where(a > 0, e - 3, -E8M0_BIAS).astype(np.int64)
 
 
 def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int = 0, seed: int = 0,
                      stream: int = 0, row_ids=None):
     """Quantize an operand A [rows, red] (red % 32 == 0) along its contiguous axis with power-of-two scales.
 
-    Per 1x32 block: y = RHT16(x) on each half (or x); E = mx_scale_exponent(amax |y|); v = y * 2^-E (exact);
-    codes -7..7 by RTNE or SR with the draws of the two 16-blocks it contains (the SR counters number
-    16-blocks, as in `quantize_rows`). Returns (signed codes int64 [rows, red], E8M0 bytes uint8
-    [rows, red/32]).
+    Per 1x32 block: y = RHT16(x) on each half (or x); E = mx_scale_exponent(amax |y|); v = y * 2^-E (exact,
+    |v| < 8); codes -7..7 by RTNE or SR with the draws of the two 16-blocks it contains (the SR counters
+    number 16-blocks, as in `quantize_rows`), |v| > 7 clamped to the top level. Returns (signed codes int64
+    [rows, red], E8M0 bytes uint8 [rows, red/32]).
     """
     a = np.asarray(a_f32, dtype=np.float32)
     rows, red = a.shape

@@ -488,7 +488,9 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
 
 // ------------------------------------------------------------------------------------------------
 // Power-of-two block scales (the scale hierarchy is free, Sec. 4): blocks of 32 along the reduction axis
-// share one scale 2^E, E the smallest integer with amax <= 7 * 2^E, stored as the E8M0 byte E + 127; the
+// share one scale 2^E, E = floor(log2 amax) - 2 (the OCP Microscaling shared-exponent rule with the levels
+// read as E2M3 numbers; |y| / 2^E < 8 and values past the top level are clamped to it), stored as the E8M0
+// byte E + 127; the
 // RHT stays block-16; codes are the uniform levels -7..7 stored as FP6 E2M3 numbers, 32 of them in 24 bytes
 // (element j in bits 6j .. 6j + 5): the A/B operand format of v_mfma_scale_f32_32x32x64_f8f6f4. In a panel
 // the 24 bytes of row i's block b are three 8-byte units, unit u at b * 3072 + u * 1024 + i * 8, so that
@@ -525,9 +527,10 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
-    // amax = 1.f * 2^(eb - 127): the smallest E with amax <= 7 * 2^E is eb - 129, plus one when 1.f > 1.75
+    // amax = 1.f * 2^(eb - 127): E = floor(log2 amax) - 2 = eb - 129 (the OCP shared-exponent rule with the
+    // levels read as E2M3 numbers), so amax * 2^-E lies in [4, 8)
     const uint32_t ab = __float_as_uint(amax);
-    const int e8 = (int)(ab >> 23) - 2 + ((ab & 0x7FFFFFu) > 0x600000u ? 1 : 0);  // E + 127 for this amax
+    const int e8 = (int)(ab >> 23) - 2;  // E + 127 for this amax
     // y' = 4y with the RHT: the scale of y is 2^(E - 2); v = y' * 2^-E either way (exact, a power of two)
     e8m0 = amax > 0.0f ? (uint32_t)(RHT ? e8 - 2 : e8) : 0u;
     const float mult = amax > 0.0f ? __uint_as_float((uint32_t)(254 - e8) << 23) : 0.0f;
@@ -544,12 +547,12 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
         uint32_t t[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float v = y[16 * h + i] * mult;  // |v| <= 7
+            const float v = y[16 * h + i] * mult;  // |v| < 8: the top level 7 is the clamp
             if constexpr (ROUND == kRoundSR) {
                 const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);
+                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);  // clamps itself
             } else {
-                t[i] = __float_as_uint(v + kMagic8);
+                t[i] = __float_as_uint(__builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f) + kMagic8);
             }
         }
         p[2 * h] = offset_to_sign_magnitude(pack_nibbles(t));

@@ -555,13 +555,14 @@ def test_diagnostics_closed_forms():
 # Uniform grid with power-of-two block scales (Sec. 4: scale hierarchy chosen for the hardware)
 # ------------------------------------------------------------------------------------------------
 
-def test_mx_scale_exponent_is_the_smallest_covering_power_of_two():
+def test_mx_scale_exponent_follows_the_ocp_shared_exponent_rule():
+    """E = floor(log2 amax) - 2, checked with exact rationals: 4 * 2^E <= amax < 8 * 2^E."""
     rng = np.random.default_rng(51)
     amax = np.concatenate([
         (rng.standard_normal(4000) * 10.0 ** rng.integers(-30, 30, 4000)).astype(np.float32),
-        np.float32([7.0, 3.5, 14.0, 1.0, 0.875, 7 * 2.0 ** -100, 3.4e38]),
-        np.nextafter(np.float32([7.0, 3.5, 14.0]), np.float32(np.inf)),
-        np.nextafter(np.float32([7.0, 3.5, 14.0]), np.float32(0)),
+        np.float32([7.0, 3.5, 14.0, 1.0, 0.875, 4.0, 8.0, 7 * 2.0 ** -100, 3.4e38]),
+        np.nextafter(np.float32([4.0, 8.0, 1.0]), np.float32(np.inf)),
+        np.nextafter(np.float32([4.0, 8.0, 1.0]), np.float32(0)),
     ])
     amax = np.abs(amax)
     amax = amax[amax > 0]
@@ -569,8 +570,7 @@ def test_mx_scale_exponent_is_the_smallest_covering_power_of_two():
     for a, e in zip(amax.tolist(), E.tolist()):
         fa = Fraction(a)
         two_e = Fraction(2) ** e
-        assert 7 * two_e >= fa, (a, e)
-        assert 7 * two_e / 2 < fa, (a, e)
+        assert 4 * two_e <= fa < 8 * two_e, (a, e)
     assert O.mx_scale_exponent(np.float32([0.0]))[0] == -127
 
 
@@ -601,20 +601,20 @@ def test_fp6_packing_bit_positions_and_roundtrip():
 
 
 def _mx_reference_block(y, u=None):
-    """One 32-block by exact rationals: the smallest 2^E with 7 * 2^E >= amax, v = y / 2^E, then the
-    nearest integer (ties to even) or the SR rule with 16-bit draws."""
+    """One 32-block by exact rationals: 2^E with 4 * 2^E <= amax < 8 * 2^E found by search, v = y / 2^E,
+    then the nearest integer (ties to even) or the SR rule with 16-bit draws, clamped to [-7, 7]."""
     ys = [Fraction(float(t)) for t in y]
     amax = max(abs(t) for t in ys)
     if amax == 0:
         return [0] * len(ys), 0
     e = 0
-    while 7 * Fraction(2) ** e < amax:
+    while 8 * Fraction(2) ** e <= amax:
         e += 1
-    while 7 * Fraction(2) ** (e - 1) >= amax:
+    while 4 * Fraction(2) ** e > amax:
         e -= 1
     codes = []
     for i, t in enumerate(ys):
-        v = t / Fraction(2) ** e
+        v = min(max(t / Fraction(2) ** e, Fraction(-7)), Fraction(7))
         lo = floor(v)
         if u is None:
             frac = v - lo
@@ -650,9 +650,11 @@ def test_mx_quantizer_invariants_with_rht():
     y = O.rht_blocks(a.reshape(16, 8, 16), 0x5A5A).reshape(16, 4, 32).astype(np.float64)
     s = np.ldexp(1.0, e8.astype(np.int64) - 127)
     top = np.abs(idx.reshape(16, 4, 32)).max(axis=-1)
-    assert np.all((top >= 4) & (top <= 7))  # amax / 2^E lies in (3.5, 7]: the top code is 4..7, no clipping
+    assert np.all((top >= 4) & (top <= 7))  # amax / 2^E lies in [4, 8): the top code is 4..7
     err = np.abs(idx.reshape(16, 4, 32) * s[..., None] - y)
-    assert np.all(err <= s[..., None] / 2)  # RTNE: within half a step
+    clipped = np.abs(y) > 7.5 * s[..., None]
+    assert np.all(err[~clipped] <= s[..., None].repeat(32, -1)[~clipped] / 2)  # RTNE: within half a step
+    assert np.all(err[clipped] <= s[..., None].repeat(32, -1)[clipped])  # clamped top values: within a step
 
 
 def test_mx_gemm_special_cases():
