@@ -54,6 +54,25 @@ GRID_MAGNITUDES = {
 }
 G_MAX = {UNIFORM: 7.0, E2M1: 6.0}  # g_max of Sec. 2.1
 
+# Range-restricted E2M1 (Sec. 5 Q4, the max_fpx ablation; Appendix search space): keep only the levels up to
+# max_fpx and use g = max_fpx. The kept levels are a prefix of the E2M1 list, so magnitude codes are unchanged.
+E2M1_MAX_FPX = (2.0, 4.0, 6.0)
+
+
+def grid_magnitudes(fmt: int, max_fpx=None) -> np.ndarray:
+    """Non-negative levels of a grid in magnitude-code order; E2M1 optionally cut at max_fpx."""
+    mags = GRID_MAGNITUDES[fmt]
+    if max_fpx is None:
+        return mags
+    if fmt != E2M1 or float(max_fpx) not in E2M1_MAX_FPX:
+        raise ValueError("max_fpx applies to E2M1 only and must be one of 2, 4, 6")
+    return mags[mags <= float(max_fpx)]
+
+
+def grid_gmax(fmt: int, max_fpx=None) -> float:
+    """g of the scale s = amax/g: the top level of the (possibly restricted) grid."""
+    return float(grid_magnitudes(fmt, max_fpx)[-1])
+
 
 # ---------------------------------------------------------------------------------------------------
 # bf16 helpers
@@ -211,36 +230,37 @@ def sr_draws(block_idx, row_idx, seed: int, stream: int) -> np.ndarray:
 # Rounding onto a grid (Sec. 2.1)
 # ---------------------------------------------------------------------------------------------------
 
-def round_nearest_even(v: np.ndarray, fmt: int) -> np.ndarray:
+def round_nearest_even(v: np.ndarray, fmt: int, max_fpx=None) -> np.ndarray:
     """RTNE onto the signed grid: nearest level; on a tie, the level with the even magnitude code.
 
     Returns signed level *indices* (magnitude code with the sign of v; -0 becomes 0). Values beyond the
-    largest level go to it (the nearest level). Brute force over every level.
+    largest level go to it (the nearest level). Brute force over every level of the grid (E2M1 cut at
+    max_fpx when given).
     """
-    mags = GRID_MAGNITUDES[fmt]
+    mags = grid_magnitudes(fmt, max_fpx)
     a = np.abs(np.asarray(v, dtype=np.float64))
     dist = np.abs(a[..., None] - mags)  # exact: fp32 inputs, small dyadic levels
     best = dist.min(axis=-1, keepdims=True)
     cand = dist == best
     # among the (at most two) nearest levels prefer the even magnitude code
-    even = (np.arange(8) % 2) == 0
+    even = (np.arange(len(mags)) % 2) == 0
     pick_even = cand & even
     idx = np.where(pick_even.any(axis=-1), pick_even.argmax(axis=-1), cand.argmax(axis=-1))
     return np.where(np.asarray(v) < 0, -idx, idx).astype(np.int64)
 
 
-def _signed_levels(fmt: int) -> np.ndarray:
-    mags = GRID_MAGNITUDES[fmt]
+def _signed_levels(fmt: int, max_fpx=None) -> np.ndarray:
+    mags = grid_magnitudes(fmt, max_fpx)
     return np.concatenate([-mags[:0:-1], mags])  # ascending, -g_max .. g_max
 
 
-def round_stochastic(v: np.ndarray, u16: np.ndarray, fmt: int) -> np.ndarray:
+def round_stochastic(v: np.ndarray, u16: np.ndarray, fmt: int, max_fpx=None) -> np.ndarray:
     """SR onto the signed grid with 16-bit draws (Sec. 2.1, second display).
 
     For g_a <= v < g_b adjacent signed levels, q = g_b iff u/2^16 < (v - g_a)/(g_b - g_a); otherwise g_a.
     v on a level stays there; |v| beyond the largest level goes to it. Returns signed level indices.
     """
-    levels = _signed_levels(fmt)
+    levels = _signed_levels(fmt, max_fpx)
     v64 = np.asarray(v, dtype=np.float64)
     vc = np.clip(v64, levels[0], levels[-1])
     ia = np.searchsorted(levels, vc, side="right") - 1  # levels[ia] <= vc
@@ -252,7 +272,7 @@ def round_stochastic(v: np.ndarray, u16: np.ndarray, fmt: int) -> np.ndarray:
     u = np.asarray(u16, dtype=np.float64) / 65536.0
     q = np.where(u < p_up, gb, ga)
     # back to signed magnitude index
-    mags = GRID_MAGNITUDES[fmt]
+    mags = grid_magnitudes(fmt, max_fpx)
     idx = np.searchsorted(mags, np.abs(q))
     return np.where(q < 0, -idx, idx).astype(np.int64)
 
@@ -279,13 +299,14 @@ def _check_block_domain(amax: np.ndarray, g: float) -> None:
 
 
 def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0,
-                  seed: int = 0, stream: int = 0, row_ids=None, block_base: int = 0):
+                  seed: int = 0, stream: int = 0, row_ids=None, block_base: int = 0, max_fpx=None):
     """Quantize an operand A [rows, red] along its contiguous (reduction) axis.
 
     Steps per 1x16 block B (Sec. 2.1 display; RHT of Sec. 2.2 applied first when `rht`):
       y = RHT(x) or x;  s = RN32(amax/g);  q_i = rho(y_i / s) with y_i/s taken as RN32(y_i * RN32(g/amax)).
     `row_ids` are the global row numbers used in the SR counters (default 0..rows-1); `block_base` is
-    added to the block number (used for operands cut out of a longer reduction axis).
+    added to the block number (used for operands cut out of a longer reduction axis). `max_fpx` (E2M1
+    only) restricts the grid to the levels up to it, with g = max_fpx.
     Returns (signed level indices int64 [rows, red], scales fp32 [rows, red/16]).
     """
     a = np.asarray(a_f32, dtype=np.float32)
@@ -297,7 +318,7 @@ def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_ma
     y = rht_blocks(blocks, sign_mask) if rht else blocks.copy()
     if not np.all(np.isfinite(y)):
         raise ValueError("non-finite value after the transform")
-    g = np.float32(G_MAX[fmt])
+    g = np.float32(grid_gmax(fmt, max_fpx))
     amax = np.abs(y).max(axis=-1)  # fp32
     _check_block_domain(amax, float(g))
     nz = amax > 0
@@ -305,12 +326,12 @@ def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_ma
     recip = np.where(nz, g / np.where(nz, amax, np.float32(1.0)), np.float32(0.0)).astype(np.float32)
     v = (y * recip[..., None]).astype(np.float32)  # one fp32 multiply per element
     if rounding == RTNE:
-        idx = round_nearest_even(v, fmt)
+        idx = round_nearest_even(v, fmt, max_fpx)
     elif rounding == SR:
         rid = np.arange(rows) if row_ids is None else np.asarray(row_ids)
         bidx = block_base + np.arange(nb)
         u = sr_draws(bidx[None, :], rid[:, None], seed, stream)
-        idx = round_stochastic(v, u, fmt)
+        idx = round_stochastic(v, u, fmt, max_fpx)
     else:
         raise ValueError("unknown rounding mode")
     idx = np.where(nz[..., None], idx, 0)
@@ -629,3 +650,50 @@ def effective_bucket_ratio(idx: np.ndarray, fmt: int, eps: float = 1e-12) -> flo
     p = np.bincount(mag, minlength=k)[:k] / mag.size
     ent = -np.sum(p * np.log(p + eps))
     return float(np.exp(ent) / k)
+
+
+def quant_stats(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0, seed: int = 0,
+                stream: int = 0, max_fpx=None) -> dict:
+    """Sums behind the Sec. 3.2 diagnostics for one quantization of an operand A [rows, red].
+
+    The reference is the tensor the quantizer rounds: ref = y, the RHT output rounded to fp32 (rht) or x
+    itself; q = Q_G(ref) dequantized (level * scale, fp64). Returns
+      err2 = ||q - ref||_F^2,  ref2 = ||ref||_F^2,  cross = <q, ref>_F,
+      hist[m] = number of elements whose magnitude code is m (m = 0..7; bucket 0 is zero).
+    NMSE = err2 / ref2 and alpha = cross / ref2 (Sec. 3.2); B_eff follows from hist.
+    """
+    a = np.asarray(a_f32, dtype=np.float32)
+    rows, red = a.shape
+    blocks = a.reshape(rows, red // BLOCK, BLOCK)
+    y = rht_blocks(blocks, sign_mask) if rht else blocks
+    ref = np.asarray(y, dtype=np.float64).reshape(rows, red)
+    idx, sc = quantize_rows(a, fmt, rounding, rht, sign_mask, seed, stream, max_fpx=max_fpx)
+    q = dequantize(idx, sc, fmt)
+    return {
+        "err2": float(np.sum((q - ref) ** 2)),
+        "ref2": float(np.sum(ref * ref)),
+        "cross": float(np.sum(q * ref)),
+        "hist": np.bincount(np.abs(idx).ravel(), minlength=8)[:8].astype(np.int64),
+    }
+
+
+def stats_metrics(st: dict, fmt: int, max_fpx=None, eps: float = 1e-12) -> dict:
+    """NMSE, SQNR (dB), alpha and B_eff (K = levels of the grid, zero included) from `quant_stats` sums."""
+    k = len(grid_magnitudes(fmt, max_fpx))
+    hist = np.asarray(st["hist"], dtype=np.float64)[:k]
+    n = hist.sum()
+    p = hist / n if n > 0 else hist
+    ent = -np.sum(p * np.log(p + eps))
+    ref2 = st["ref2"]
+    nm = st["err2"] / ref2 if ref2 > 0 else float("nan")
+    return {
+        "nmse": nm,
+        "sqnr_db": float(-10.0 * np.log10(nm)) if nm > 0 else float("inf"),
+        "alpha": st["cross"] / ref2 if ref2 > 0 else float("nan"),
+        "beff": float(np.exp(ent) / k),
+    }
+
+
+def delta_sqnr_db(nmse_raw: float, nmse_rht: float) -> float:
+    """Delta SQNR = 10 log10(NMSE_I / NMSE_H16) (Sec. 3.2): positive when the rotation helps."""
+    return float(10.0 * np.log10(nmse_raw / nmse_rht))

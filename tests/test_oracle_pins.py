@@ -551,6 +551,116 @@ def test_diagnostics_closed_forms():
     assert O.effective_bucket_ratio(np.zeros((1, 8), np.int64), O.UNIFORM) == pytest.approx(1 / 8, abs=1e-9)
 
 
+def _one_block(vals):
+    row = np.zeros((1, 16), np.float32)
+    row[0, :len(vals)] = vals
+    return row
+
+
+def test_quant_stats_hand_computed_blocks():
+    """Sums worked out by hand for single 16-blocks (no RHT, scale 1 so that v = x)."""
+    # uniform: 7, 3.375, -1.625 -> codes 7, 3, -2 (s = 7/7 = 1)
+    st = O.quant_stats(_one_block([7.0, 3.375, -1.625]), O.UNIFORM, O.RTNE, False)
+    assert st["err2"] == 0.28125 and st["ref2"] == 63.03125 and st["cross"] == 62.375
+    assert st["hist"].tolist() == [13, 0, 1, 1, 0, 0, 0, 1]
+    # E2M1: 6, 2.5, -0.75 -> 6, 2 (tie to the even code 4), -1 (tie to the even code 2)
+    st = O.quant_stats(_one_block([6.0, 2.5, -0.75]), O.E2M1, O.RTNE, False)
+    assert st["err2"] == 0.3125 and st["ref2"] == 42.8125 and st["cross"] == 41.75
+    assert st["hist"].tolist() == [13, 0, 1, 0, 1, 0, 0, 1]
+    # E2M1 cut at max_fpx = 2: s = 3, v = 2, 0.8333334, -0.25 -> 2 (code 4), 1 (code 2), 0 (tie to code 0)
+    st = O.quant_stats(_one_block([6.0, 2.5, -0.75]), O.E2M1, O.RTNE, False, max_fpx=2)
+    assert st["err2"] == 0.8125 and st["cross"] == 43.5
+    assert st["hist"].tolist() == [14, 0, 1, 0, 1, 0, 0, 0]
+
+
+def test_quant_stats_on_grid_input_is_lossless():
+    """Blocks whose values are k * 2^e with max |k| = 7 quantize exactly: NMSE 0, alpha 1 (RTNE and SR)."""
+    rng = np.random.default_rng(61)
+    k = rng.integers(-7, 8, size=(24, 64)).astype(np.float64)
+    k[:, ::16] = 7.0  # every block reaches the top level
+    a = (k * np.exp2(rng.integers(-6, 7, size=(24, 4)).repeat(16, axis=1))).astype(np.float32)
+    for rnd in (O.RTNE, O.SR):
+        st = O.quant_stats(a, O.UNIFORM, rnd, False, seed=5)
+        m = O.stats_metrics(st, O.UNIFORM)
+        assert st["err2"] == 0.0 and m["alpha"] == 1.0
+        assert st["hist"].tolist() == np.bincount(np.abs(k).astype(np.int64).ravel(), minlength=8).tolist()
+
+
+def test_quant_stats_sums_are_consistent():
+    """||q - r||^2 = ||q||^2 - 2 <q, r> + ||r||^2 with ||q||^2 taken from the dequantized operand; counts add up."""
+    rng = np.random.default_rng(62)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (48, 96)))
+    for fmt, mf in ((O.UNIFORM, None), (O.E2M1, None), (O.E2M1, 4.0)):
+        for rht in (False, True):
+            st = O.quant_stats(a, fmt, O.SR, rht, 0x5A5A, seed=9, stream=1, max_fpx=mf)
+            idx, sc = O.quantize_rows(a, fmt, O.SR, rht, 0x5A5A, 9, 1, max_fpx=mf)
+            q2 = float(np.sum(O.dequantize(idx, sc, fmt) ** 2))
+            assert st["err2"] == pytest.approx(q2 - 2 * st["cross"] + st["ref2"], rel=1e-9)
+            assert int(st["hist"].sum()) == a.size
+
+
+def test_stats_metrics_closed_forms():
+    st = {"err2": 1.0, "ref2": 100.0, "cross": 90.0, "hist": np.array([4, 4, 4, 4, 4, 4, 4, 4])}
+    m = O.stats_metrics(st, O.UNIFORM)
+    assert m["nmse"] == 0.01 and m["sqnr_db"] == pytest.approx(20.0) and m["alpha"] == 0.9
+    assert m["beff"] == pytest.approx(1.0, abs=1e-9)
+    # the cut grid has K = 5 buckets; all mass in one of them gives 1/5
+    st = {"err2": 0.0, "ref2": 1.0, "cross": 1.0, "hist": np.array([0, 0, 7, 0, 0, 0, 0, 0])}
+    assert O.stats_metrics(st, O.E2M1, max_fpx=2)["beff"] == pytest.approx(1 / 5, abs=1e-9)
+    assert O.delta_sqnr_db(0.01, 0.001) == pytest.approx(10.0)
+
+
+# ------------------------------------------------------------------------------------------------
+# Range-restricted E2M1 (Sec. 5 Q4: max_fpx in {2, 4, 6})
+# ------------------------------------------------------------------------------------------------
+
+def test_max_fpx_six_is_the_plain_e2m1_grid():
+    rng = np.random.default_rng(63)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (16, 64)))
+    for rnd in (O.RTNE, O.SR):
+        i0, s0 = O.quantize_rows(a, O.E2M1, rnd, True, 0x0F0F, 4, 0)
+        i1, s1 = O.quantize_rows(a, O.E2M1, rnd, True, 0x0F0F, 4, 0, max_fpx=6)
+        assert np.array_equal(i0, i1) and np.array_equal(s0, s1)
+
+
+def test_max_fpx_levels_and_ties():
+    assert O.grid_magnitudes(O.E2M1, 2).tolist() == [0.0, 0.5, 1.0, 1.5, 2.0]
+    assert O.grid_magnitudes(O.E2M1, 4).tolist() == [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0]
+    v = np.array([1.25, 1.75, -0.25, 2.6, 3.5, 5.0, -7.0], np.float32)
+    assert O.round_nearest_even(v, O.E2M1, 2).tolist() == [2, 4, 0, 4, 4, 4, -4]
+    assert O.round_nearest_even(v, O.E2M1, 4).tolist() == [2, 4, 0, 5, 6, 6, -6]
+    assert O.round_nearest_even(v, O.E2M1).tolist() == [2, 4, 0, 5, 6, 6, -7]
+    with pytest.raises(ValueError):
+        O.grid_magnitudes(O.UNIFORM, 4)
+    with pytest.raises(ValueError):
+        O.grid_magnitudes(O.E2M1, 3)
+
+
+def test_max_fpx_sr_is_exhaustively_unbiased_and_stays_on_the_cut_grid():
+    """Over all 2^16 draws: the mean of SR equals v (v a multiple of 2^-16 of the bin), and no draw leaves
+    the restricted grid, also 1 ulp above its top level."""
+    u = np.arange(65536, dtype=np.uint32)
+    for mf, v in ((4.0, 3.25), (4.0, -3.75), (2.0, 1.125), (2.0, -0.375)):
+        q = O.level_values(O.round_stochastic(np.full(65536, v, np.float32), u, O.E2M1, mf), O.E2M1)
+        assert q.mean() == v
+    for mf in (2.0, 4.0):
+        top = np.nextafter(np.float32(mf), np.float32(10.0))
+        q = O.level_values(O.round_stochastic(np.full(65536, top, np.float32), u, O.E2M1, mf), O.E2M1)
+        assert set(q.tolist()) == {mf}
+
+
+def test_max_fpx_on_grid_block_is_reproduced():
+    """A block on the cut grid with |x| reaching max_fpx * 2^e quantizes exactly with s = 2^e."""
+    for mf in (2.0, 4.0):
+        lv = O.grid_magnitudes(O.E2M1, mf)
+        vals = np.concatenate([lv, -lv[1:]])[:16]
+        row = np.zeros((1, 16), np.float32)
+        row[0, :len(vals)] = vals * 0.125
+        idx, sc = O.quantize_rows(row, O.E2M1, O.RTNE, False, max_fpx=mf)
+        assert sc[0, 0] == np.float32(0.125)
+        assert np.array_equal(O.dequantize(idx, sc, O.E2M1), row.astype(np.float64))
+
+
 # ------------------------------------------------------------------------------------------------
 # Uniform grid with power-of-two block scales (Sec. 4: scale hierarchy chosen for the hardware)
 # ------------------------------------------------------------------------------------------------
