@@ -13,10 +13,13 @@ single-output quantizer, 3.5 for the two-operand one) or TFLOP/s (GEMMs); `roofl
 the dominant one; `cpu_baseline` times the CPU oracle on a bounded sample of the same layer.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--quant dual|separate]
-                       [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|quant1g-dual|copy1g]
+                       [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|quant1g-dual|copy1g|
+                                   quality-dense|quality-moe124b]
 
 The quant1g workloads time one quantizer on a 1 GiB bf16 tensor; they also time the same kernel without the
 RHT (plain block quantization) and report the ratio, the quantity the paper gives for its own fused kernel.
+The quality workloads print the Sec. 3.2 diagnostics of every GEMM operand of the layer (four grids, without
+and with the RHT), computed on the GPU at full size by the statistics kernel, and that kernel's throughput.
 
 Without --warmup the untimed warmup runs whole steps until at least WARMUP_SECONDS have passed: the GPU's clock
 takes tens of milliseconds of load to settle, and a few milliseconds of warmup would time the ramp.
@@ -282,7 +285,76 @@ def quant1g_step(tl: Timeline, mode: str):
     def plain(rec):
         tl.run(label + "_plain", lambda: run(False), rec)
 
-    return step, {label: (kind, R * C)}, plain
+    unfused = None
+    if mode == "rows":
+        # the unfused form: standalone RHT into an fp32 tensor, then the fp32-input quantizer (same codes)
+        y = torch.empty((R, C), dtype=torch.float32, device="cuda")
+        qu = U.empty_qtensor(R, C)
+
+        def unfused(rec):
+            tl.run(label + "_unfused_rht", lambda: U.rht(t, sign_mask=0x6A09, out=y), rec)
+            tl.run(label + "_unfused_quant", lambda: U.quantize_f32(y, out=qu), rec)
+
+    return step, {label: (kind, R * C)}, plain, unfused
+
+
+# ---------------------------------------------------------------------------------------------------
+# quality diagnostics (Sec. 3.2) on the layer's tensors at full size, from ufp4_quant_stats
+# ---------------------------------------------------------------------------------------------------
+
+QUALITY_GRIDS = [("uniform", U.UNIFORM, 0.0), ("e2m1", U.E2M1, 0.0), ("e2m1 max_fpx=4", U.E2M1, 4.0),
+                 ("e2m1 max_fpx=2", U.E2M1, 2.0)]
+
+
+def quality_report(wl, steps: int):
+    """NMSE / SQNR / alpha / B_eff of every GEMM operand of the layer, per grid, without and with the RHT,
+    Delta SQNR (Sec. 3.2), and the coherent attenuation eta = alpha_A alpha_B of each GEMM; plus the
+    statistics kernel's own throughput on the first operand."""
+    x, dy = wl.x.cuda(), wl.dy.cuda()
+    w = wl.w.reshape(-1, wl.w.shape[-1]).cuda()  # experts stacked along N (multiples of 16)
+    # operand: (tensor, transpose, rounding, SR stream), as in the layer step
+    ops = {"X (fwd_y)": (x, False, U.RTNE, 0), "W (fwd_y)": (w, False, U.RTNE, 0),
+           "dY (bwd_dx)": (dy, False, U.SR, 0), "W^T (bwd_dx)": (w, True, U.RTNE, 0),
+           "dY^T (bwd_dw)": (dy, True, U.SR, 1), "X^T (bwd_dw)": (x, True, U.RTNE, 0)}
+    table = {}
+    for gname, fmt, mf in QUALITY_GRIDS:
+        rows = {}
+        for oname, (t, tr, rnd, st) in ops.items():
+            r = {}
+            for rht in (False, True):
+                q = U.quant_stats(t, fmt, max_fpx=mf, transpose=tr, rht=rht, sign_mask=wl.sign_mask, rounding=rnd,
+                                  seed=wl.seed, stream_id=st)
+                r["rht" if rht else "raw"] = {"nmse": q.nmse, "sqnr_db": round(q.sqnr_db, 3),
+                                              "alpha": round(q.alpha, 6), "beff": round(q.beff, 4)}
+                r["_nmse_" + ("rht" if rht else "raw")] = q.nmse
+            r["delta_sqnr_db"] = round(10.0 * np.log10(r.pop("_nmse_raw") / r.pop("_nmse_rht")), 3)
+            rows[oname] = r
+        eta = {}
+        for gemm, (a, b) in {"fwd_y": ("X (fwd_y)", "W (fwd_y)"), "bwd_dx": ("dY (bwd_dx)", "W^T (bwd_dx)"),
+                             "bwd_dw": ("dY^T (bwd_dw)", "X^T (bwd_dw)")}.items():
+            eta[gemm] = {k: round(rows[a][k]["alpha"] * rows[b][k]["alpha"], 6) for k in ("raw", "rht")}
+        table[gname] = {"operands": rows, "eta": eta}
+    # timing of the statistics kernel (uniform grid, RHT, X rowwise)
+    rec = torch.empty(U.STATS_BYTES // 8, dtype=torch.float64, device="cuda")
+    lib = U.lib()
+
+    def launch():
+        return lib.ufp4_quant_stats(U.UNIFORM, 0.0, x.data_ptr(), x.shape[0], x.shape[1], x.stride(0), 0, 1,
+                                    wl.sign_mask, U.RTNE, 0, 0, rec.data_ptr(), U._stream())
+
+    for _ in range(3):
+        launch()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        launch()
+    e.record()
+    torch.cuda.synchronize()
+    us = s.elapsed_time(e) * 1e3 / steps
+    gbps = x.numel() * 2 / (us * 1e-6) / 1e9
+    return table, {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4),
+                   "work": f"quant_stats_kernel + record clear on X {tuple(x.shape)} (reads 2 B per element)"}
 
 
 # ---------------------------------------------------------------------------------------------------
@@ -352,7 +424,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
     ap.add_argument("--workload", default="dense",
                     choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "quant1g-dual",
-                             "copy1g"])
+                             "copy1g", "quality-dense", "quality-moe124b"])
     ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPES),
                     help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
     ap.add_argument("--quant", default="dual", choices=["dual", "separate"],
@@ -370,12 +442,26 @@ def main():
     torch.cuda.set_device(0)
     U.lib()
 
+    if args.workload.startswith("quality"):
+        wl = WL.CONFIGS["dense" if args.workload == "quality-dense" else "moe124b"]()
+        table, kern_time = quality_report(wl, args.steps)
+        print(json.dumps({
+            "metric": "quantization quality of the layer's GEMM operands (Sec. 3.2): NMSE, SQNR, alpha, B_eff, "
+                      "Delta SQNR; eta = alpha_A alpha_B per GEMM",
+            "value": kern_time["GB/s"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "higher_is_better": True, "vs_baseline": None, "dtype": "f64+f32",
+            "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
+            "config": {"workload": wl.name, "note": "transposed operands of grouped tensors are taken along the "
+                       "concatenated token axis, without the per-expert padding of the grouped quantizer"},
+            "stats_kernel": kern_time, "quality": table}), flush=True)
+        return
+
     tl = Timeline()
     wl = None
-    plain = None
+    plain = unfused = None
     if args.workload in ("quant1g", "quant1g-t", "quant1g-dual"):
         mode = {"quant1g": "rows", "quant1g-t": "cols", "quant1g-dual": "dual"}[args.workload]
-        step, kern, plain = quant1g_step(tl, mode)
+        step, kern, plain, unfused = quant1g_step(tl, mode)
         what = {"rows": "rowwise", "cols": "transposed", "dual": "rowwise + transposed in one pass"}[mode]
         wname = f"standalone quantizer: 32768x16384 bf16 (1 GiB), {what} RTNE with RHT"
     elif args.workload == "copy1g":
@@ -424,6 +510,19 @@ def main():
         context = {"plain_quant_us": round(plain_us, 2), "fused_us": round(fused_us, 2),
                    "fused_over_plain": round(fused_us / plain_us, 3),
                    "paper": "fused / plain quantization latency ~1.06x (SM90), ~1.07x (SM100); Sec. 5 Q5"}
+        if unfused is not None:
+            for _ in range(args.warmup):
+                unfused(False)
+            for _ in range(args.steps):
+                unfused(True)
+            torch.cuda.synchronize()
+            r_us, q_us = tl.mean_us(label + "_unfused_rht"), tl.mean_us(label + "_unfused_quant")
+            context.update({
+                "unfused_rht_us": round(r_us, 2), "unfused_quant_us": round(q_us, 2),
+                "unfused_over_fused": round((r_us + q_us) / fused_us, 3),
+                "unfused_form": "standalone RHT writing fp32 y (2 B in, 4 B out per element), then the fp32-input "
+                                "quantizer (4 B in, 0.75 B out); same codes as the fused kernel",
+                "paper_unfused": "unfused / fused latency 1.62x (SM90), 1.41x (SM100); Sec. 5 Q5"})
 
     breakdown = {}
     gemm_flops = 0

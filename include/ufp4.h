@@ -104,6 +104,68 @@ int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld
                        int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld, void *stream);
 
 /*
+ * ufp4_e2m1_quantize_range -- ufp4_e2m1_quantize on the E2M1 grid cut at max_fpx (Sec. 5 Q4, the
+ * range-restricted E2M1 ablation): only the levels up to max_fpx are kept and g = max_fpx, so s = RN(amax /
+ * max_fpx). max_fpx = 2 keeps 0, .5, 1, 1.5, 2; 4 keeps 0 .. 4; 6 is the full grid. The codes are the
+ * E2M1 codes of the kept levels, so the E2M1 GEMMs consume the result unchanged. Other max_fpx values
+ * (0 included) return UFP4_ERR_INVALID_ARG. Remaining arguments as ufp4_rht_quantize.
+ */
+int ufp4_e2m1_quantize_range(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                             uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, float max_fpx,
+                             void *codes_dev, int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld,
+                             void *stream);
+
+/*
+ * ufp4_quant_stats -- quality statistics of one quantization, the sums behind the diagnostics of Sec. 3.2
+ * (NMSE_A(G, T), SQNR, the operand projection alpha, the bucket entropy behind B_eff). The operand is
+ * quantized exactly as ufp4_rht_quantize / ufp4_e2m1_quantize(_range) would quantize it, but nothing is
+ * stored except the record below. For every element, ref is the value the quantizer rounds (the fp32 RHT
+ * output y when rht != 0, else x) and q = level(code) * scale its dequantized value.
+ *
+ *   format, max_fpx  UFP4_FMT_UNIFORM with max_fpx = 0, or UFP4_FMT_E2M1 with max_fpx 0 (full grid), 2, 4, 6.
+ *   stats_dev        device pointer (8-byte aligned) to one ufp4_quant_stats_t record, overwritten (zero for
+ *                    an empty operand, whose x_dev may be NULL). fp64 sums are accumulated with atomics: their last bits may
+ *                    differ between calls; the counts are exact.
+ *   Other arguments as ufp4_rht_quantize. NMSE = err2 / ref2, alpha = cross / ref2, bucket fractions
+ *   p_m = hist[m] / (rows * cols).
+ */
+typedef struct {
+    double err2;           /* sum of (q - ref)^2 */
+    double ref2;           /* sum of ref^2 */
+    double cross;          /* sum of q * ref */
+    uint64_t hist[8];      /* elements whose magnitude code is m = 0..7 (m = 0: zero) */
+} ufp4_quant_stats_t;
+
+int ufp4_quant_stats(int format, float max_fpx, const void *x_dev, int64_t rows, int64_t cols, int64_t ld,
+                     int transpose, int rht, uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id,
+                     ufp4_quant_stats_t *stats_dev, void *stream);
+
+/*
+ * The unfused form of RHT + quantization (Sec. 5 Q5 measures it against the fused kernel): a standalone
+ * transform that writes the rotated tensor, then a plain quantization of it. The intermediate is fp32, which
+ * holds y exactly, so ufp4_quantize_f32(ufp4_rht(x)) produces the same codes and scales as
+ * ufp4_rht_quantize(x, rht = 1) (rowwise) bit for bit.
+ *
+ * ufp4_rht -- y = RN_fp32( x S_16 H_16 ) for every 16-block along the rows of x (Sec. 2.2; the arithmetic
+ *   of the quantizer's transform, see the conventions above). x_dev bf16 [rows, cols] (cols % 16 == 0, ld as
+ *   for the quantizers); y_dev fp32 [rows, cols] with leading dimension ldy (ldy >= cols, ldy % 4 == 0,
+ *   16-byte aligned). sign_mask as for ufp4_rht_quantize.
+ */
+int ufp4_rht(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t sign_mask, float *y_dev,
+             int64_t ldy, void *stream);
+
+/*
+ * ufp4_quantize_f32 -- rowwise quantization of an fp32 tensor without a transform (the second half of the
+ *   unfused form): operand A = X [rows, cols] along cols, the arithmetic of ufp4_rht_quantize with rht = 0
+ *   applied to fp32 values. format UFP4_FMT_UNIFORM or UFP4_FMT_E2M1 (full grid); ld >= cols, ld % 4 == 0,
+ *   x_dev 16-byte aligned. Inputs must be finite with every nonzero block amax at least g * 2^-126.
+ *   Remaining arguments as ufp4_rht_quantize.
+ */
+int ufp4_quantize_f32(int format, const float *x_dev, int64_t rows, int64_t cols, int64_t ld, int rounding,
+                      uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_panel_ld, float *scales_dev,
+                      int64_t scale_panel_ld, void *stream);
+
+/*
  * ufp4_quantize_grouped_t -- transposed quantization of an expert-grouped tensor (MoE), either grid.
  *
  *   x_dev              bf16 [rows, cols] (ld elements); rows are split into num_groups consecutive groups.

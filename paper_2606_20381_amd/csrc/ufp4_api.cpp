@@ -9,6 +9,8 @@
 
 using namespace ufp4;
 
+static_assert(sizeof(ufp4_quant_stats_t) == sizeof(QuantStats), "statistics record layout");
+
 namespace {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -20,6 +22,18 @@ void fill_sign_xor(uint32_t mask, uint32_t (&sx)[8]) {
 }
 
 int status_of(hipError_t e) { return e == hipSuccess ? UFP4_OK : UFP4_ERR_HIP; }
+
+// Top level of the E2M1 grid: max_fpx 0 (the full grid, 6) or 2, 4, 6; the uniform grid takes 0 only.
+bool valid_max_fpx(int format, float max_fpx) {
+    if (max_fpx == 0.0f) return true;
+    return format == UFP4_FMT_E2M1 && (max_fpx == 2.0f || max_fpx == 4.0f || max_fpx == 6.0f);
+}
+
+void fill_grid(float max_fpx, QuantArgs& qa) {
+    const float g = max_fpx == 0.0f ? 6.0f : max_fpx;
+    qa.e2m1_g = g;
+    qa.e2m1_ginv = 1.0f / g;  // RN(1/g), as the kernels' constant for the uniform grid
+}
 
 constexpr int64_t kMaxCodePanelLd = int64_t(1) << 29;   // bytes
 constexpr int64_t kMaxScalePanelLd = int64_t(1) << 27;  // floats
@@ -56,8 +70,9 @@ int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, in
 
 int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                   uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes, int64_t code_pld,
-                  float* scales, int64_t scale_pld, void* stream) {
+                  float* scales, int64_t scale_pld, void* stream, float max_fpx = 0.0f) {
     if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
+    if (!valid_max_fpx(format, max_fpx)) return UFP4_ERR_INVALID_ARG;
     const int64_t red = transpose ? rows : cols;
     const int64_t qrows = transpose ? cols : rows;
     const int st = check_quant_common(format, x, rows, cols, ld, rht, sign_mask, rounding, codes, code_pld, scales,
@@ -80,6 +95,7 @@ int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t
     j.group_poff = nullptr;
     j.num_groups = 1;
     fill_sign_xor(sign_mask, j.qa.sign_xor);
+    fill_grid(max_fpx, j.qa);
     j.qa.key0 = (uint32_t)seed;
     j.qa.key1 = (uint32_t)(seed >> 32);
     j.qa.stream = stream_id;
@@ -261,6 +277,109 @@ int ufp4_e2m1_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld
                          codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream);
 }
 
+int ufp4_e2m1_quantize_range(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
+                             uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, float max_fpx,
+                             void* codes_dev, int64_t code_panel_ld, float* scales_dev, int64_t scale_panel_ld,
+                             void* stream) {
+    if (max_fpx == 0.0f) return UFP4_ERR_INVALID_ARG;  // the full grid is ufp4_e2m1_quantize
+    return quantize_impl(UFP4_FMT_E2M1, x_dev, rows, cols, ld, transpose, rht, sign_mask, rounding, seed, stream_id,
+                         codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream, max_fpx);
+}
+
+int ufp4_quant_stats(int format, float max_fpx, const void* x_dev, int64_t rows, int64_t cols, int64_t ld,
+                     int transpose, int rht, uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id,
+                     ufp4_quant_stats_t* stats_dev, void* stream) {
+    if (format != UFP4_FMT_UNIFORM && format != UFP4_FMT_E2M1) return UFP4_ERR_INVALID_ARG;
+    if (!valid_max_fpx(format, max_fpx)) return UFP4_ERR_INVALID_ARG;
+    if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
+    if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
+    if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
+    if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    const bool empty = rows == 0 || cols == 0;
+    if ((!x_dev && !empty) || !stats_dev) return UFP4_ERR_INVALID_ARG;  // an empty operand may have no storage
+    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
+    const int64_t red = transpose ? rows : cols;
+    const int64_t qrows = transpose ? cols : rows;
+    if (red % 16 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x_dev, 16) || !aligned(stats_dev, 8)) return UFP4_ERR_ALIGN;
+    if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    StatsJob j{};
+    j.format = format;
+    j.rounding = rounding;
+    j.rht = rht;
+    j.transpose = transpose;
+    j.x = x_dev;
+    j.ld = ld;
+    j.qrows = empty ? 0 : qrows;
+    j.red = red;
+    fill_sign_xor(sign_mask, j.qa.sign_xor);
+    fill_grid(max_fpx, j.qa);
+    j.qa.key0 = (uint32_t)seed;
+    j.qa.key1 = (uint32_t)(seed >> 32);
+    j.qa.stream = stream_id;
+    j.stats = reinterpret_cast<QuantStats*>(stats_dev);
+    return status_of(launch_quant_stats(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_rht(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t sign_mask, float* y_dev, int64_t ldy,
+             void* stream) {
+    if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    if (!x_dev || !y_dev) return UFP4_ERR_INVALID_ARG;
+    if (cols % 16 != 0 || ld < cols || ld % 8 != 0 || ldy < cols || ldy % 4 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x_dev, 16) || !aligned(y_dev, 16)) return UFP4_ERR_ALIGN;
+    if (cols / 16 / 256 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    RhtJob j{};
+    j.x = x_dev;
+    j.rows = rows;
+    j.cols = cols;
+    j.ld = ld;
+    fill_sign_xor(sign_mask, j.qa.sign_xor);
+    fill_grid(0.0f, j.qa);
+    j.y = y_dev;
+    j.ldy = ldy;
+    return status_of(launch_rht(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_quantize_f32(int format, const float* x_dev, int64_t rows, int64_t cols, int64_t ld, int rounding,
+                      uint64_t seed, uint32_t stream_id, void* codes_dev, int64_t code_panel_ld, float* scales_dev,
+                      int64_t scale_panel_ld, void* stream) {
+    if (format != UFP4_FMT_UNIFORM && format != UFP4_FMT_E2M1) return UFP4_ERR_INVALID_ARG;
+    if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    if (!x_dev || !codes_dev || !scales_dev) return UFP4_ERR_INVALID_ARG;
+    if (cols % 16 != 0 || ld < cols || ld % 4 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    const int st = check_panels(codes_dev, code_panel_ld, scales_dev, scale_panel_ld, cols);
+    if (st != UFP4_OK) return st;
+    if (rows >= (int64_t(1) << 31) || padded_rows(rows) / 32 > 65535) return UFP4_ERR_UNSUPPORTED;
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    QuantJob j{};
+    j.format = format;
+    j.rounding = rounding;
+    j.rht = 0;
+    j.transpose = 0;
+    j.input_f32 = 1;
+    j.x = x_dev;
+    j.xrows = rows;
+    j.ld = ld;
+    j.qrows = rows;
+    j.red = cols;
+    j.num_groups = 1;
+    fill_sign_xor(0, j.qa.sign_xor);
+    fill_grid(0.0f, j.qa);
+    j.qa.key0 = (uint32_t)seed;
+    j.qa.key1 = (uint32_t)(seed >> 32);
+    j.qa.stream = stream_id;
+    j.codes = codes_dev;
+    j.code_pld = code_panel_ld;
+    j.scales = scales_dev;
+    j.scale_pld = scale_panel_ld;
+    return status_of(launch_quantize(j, static_cast<hipStream_t>(stream)));
+}
+
 int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t cols, int64_t ld,
                             const int64_t* group_offsets_dev, const int64_t* padded_offsets_dev, int32_t num_groups,
                             int64_t red_total, int rht, uint32_t sign_mask, int rounding, uint64_t seed,
@@ -288,6 +407,7 @@ int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t
     j.group_poff = padded_offsets_dev;
     j.num_groups = num_groups;
     fill_sign_xor(sign_mask, j.qa.sign_xor);
+    fill_grid(0.0f, j.qa);
     j.qa.key0 = (uint32_t)seed;
     j.qa.key1 = (uint32_t)(seed >> 32);
     j.qa.stream = stream_id;
@@ -324,6 +444,8 @@ int ufp4_quantize_dual(int format, const void* x_dev, int64_t rows, int64_t cols
     j.ld = ld;
     fill_sign_xor(sign_mask_rows, j.qr.sign_xor);
     fill_sign_xor(sign_mask_cols, j.qc.sign_xor);
+    fill_grid(0.0f, j.qr);
+    fill_grid(0.0f, j.qc);
     j.qr.key0 = j.qc.key0 = (uint32_t)seed;
     j.qr.key1 = j.qc.key1 = (uint32_t)(seed >> 32);
     j.qr.stream = stream_rows;

@@ -22,11 +22,14 @@ struct QuantArgs {
     uint32_t sign_xor[8];  // XOR mask per bf16 pair: 0x8000 / 0x80000000 where eps_j = -1
     uint32_t key0, key1;   // Philox key = seed
     uint32_t stream;       // Philox counter word 3
+    float e2m1_g;          // E2M1 top level max_fpx (2, 4 or 6) and RN(1 / max_fpx); unused by the uniform grid
+    float e2m1_ginv;
 };
 
 // One quantization request, already validated.
 struct QuantJob {
     int format, rounding, rht, transpose;
+    int input_f32;  // x is fp32 (rowwise, rht = 0): the quantizing half of the unfused form
     const void* x;
     int64_t xrows, ld;  // X rows and leading dimension (elements)
     int64_t qrows;      // rows of the quantized operand
@@ -43,6 +46,34 @@ struct QuantJob {
 
 hipError_t launch_quantize(const QuantJob& job, hipStream_t stream);
 int max_groups_quantize();
+
+// Standalone block-16 RHT of X [rows, cols] along cols, y in fp32 (the unfused form).
+struct RhtJob {
+    const void* x;
+    int64_t rows, cols, ld;
+    QuantArgs qa;
+    float* y;
+    int64_t ldy;
+};
+hipError_t launch_rht(const RhtJob& job, hipStream_t stream);
+
+// Quality statistics of one quantization (the operand is not stored): fp64 sums over the elements of
+// (q - ref)^2, ref^2 and q * ref, where ref is the value the quantizer rounds (the fp32 RHT output, or x) and
+// q the dequantized code, and the number of codes per magnitude code 0..7. Layout of the caller's output.
+struct QuantStats {
+    double err2, ref2, cross;
+    unsigned long long hist[8];
+};
+// Same fields as QuantJob for a rowwise (transpose = 0) or transposed operand; no outputs but `stats`.
+struct StatsJob {
+    int format, rounding, rht, transpose;
+    const void* x;
+    int64_t ld;
+    int64_t qrows, red;
+    QuantArgs qa;
+    QuantStats* stats;
+};
+hipError_t launch_quant_stats(const StatsJob& job, hipStream_t stream);
 
 // Both quantized operands of one tensor X [rows, cols] (rows, cols multiples of 16) from one read: Q_r = X
 // along cols ([rows, cols]) and Q_c = X^T along rows ([cols, rows]). Already validated.

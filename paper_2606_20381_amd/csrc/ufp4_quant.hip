@@ -86,9 +86,10 @@ __device__ __forceinline__ uint32_t e2m1_code_of_level(float q) {
 
 // SR over adjacent signed E2M1 levels g_a <= v < g_b (spacing d = g_b - g_a in {0.5, 1, 2}):
 // q = g_b iff g_a + d * u/2^16 < v. For v >= 0 the bracket is [lower, upper) in magnitude, for v < 0 it
-// is (-upper, -lower] mirrored, so that a value on a level never moves.
-__device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t u16) {
-    const float vc = __builtin_fminf(__builtin_fmaxf(v, -6.0f), 6.0f);
+// is (-upper, -lower] mirrored, so that a value on a level never moves. `g` is the top level kept (the
+// grid cut at max_fpx = 2, 4 or 6 keeps the levels up to it); v is clamped to it first.
+__device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t u16, float g) {
+    const float vc = __builtin_fminf(__builtin_fmaxf(v, -g), g);
     const float a = __builtin_fabsf(vc);
     float ga, d;
     if (vc >= 0.0f) {
@@ -103,9 +104,10 @@ __device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t u16) {
     return e2m1_code_of_level(q);
 }
 
+// RTNE needs no cut: |v| <= g (1 + 2^-23) for g = 2, 4, 6 already rounds to a level <= g.
 template <int ROUND>
-__device__ __forceinline__ uint32_t e2m1_code(float v, uint32_t u16) {
-    if constexpr (ROUND == kRoundSR) return e2m1_sr(v, u16);
+__device__ __forceinline__ uint32_t e2m1_code(float v, uint32_t u16, float g) {
+    if constexpr (ROUND == kRoundSR) return e2m1_sr(v, u16, g);
     else return e2m1_rtne(v);
 }
 
@@ -146,19 +148,18 @@ __device__ __forceinline__ void rht16_unscaled(const uint32_t* w, const QuantArg
     }
 }
 
+// Scale and codes of one block from its (RHT-ed, unscaled) values y.
 template <int FMT, int ROUND, bool RHT>
-__device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
-                                              uint32_t& code_lo, uint32_t& code_hi, float& scale) {
-    float y[16];
-    rht16_unscaled<RHT>(w, qa, y);
+__device__ __forceinline__ void quant_y16(const float (&y)[16], const QuantArgs& qa, uint32_t blk, uint32_t row,
+                                          uint32_t& code_lo, uint32_t& code_hi, float& scale) {
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
-    constexpr float g = FMT == kFmtUniform ? 7.0f : 6.0f;
+    const float g = FMT == kFmtUniform ? 7.0f : qa.e2m1_g;
     // RN(amax / g) as RN(amax * c) with c = RN(1/g), corrected by one FMA residual step: equal to the correctly
     // rounded quotient for every fp32 amax when g = 7 and for every normal quotient when g = 6 (both checked
-    // over all fp32 inputs); amax = 0 gives 0.
-    constexpr float c = 1.0f / g;
+    // over all fp32 inputs); for g = 2 and 4 the product is already exact. amax = 0 gives 0.
+    const float c = FMT == kFmtUniform ? 1.0f / 7.0f : qa.e2m1_ginv;
     const float q0 = amax * c;
     const float sc = __builtin_fmaf(__builtin_fmaf(-q0, g, amax), c, q0);
     scale = RHT ? sc * 0.25f : sc;
@@ -191,13 +192,21 @@ __device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const Quan
         for (int i = 0; i < 16; ++i) {
             const float v = __fmul_rn(y[i], r);
             const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-            const uint32_t c = e2m1_code<ROUND>(v, u16);
+            const uint32_t c = e2m1_code<ROUND>(v, u16, g);
             if (i < 8) lo |= c << (4 * i);
             else hi |= c << (4 * (i - 8));
         }
         code_lo = lo;
         code_hi = hi;
     }
+}
+
+template <int FMT, int ROUND, bool RHT>
+__device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
+                                              uint32_t& code_lo, uint32_t& code_hi, float& scale) {
+    float y[16];
+    rht16_unscaled<RHT>(w, qa, y);
+    quant_y16<FMT, ROUND, RHT>(y, qa, blk, row, code_lo, code_hi, scale);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -211,11 +220,15 @@ constexpr int kRB = 16;    // tile blocks
 constexpr int kRT = 512;   // threads
 constexpr int kRI = kRR * kRB / kRT;  // blocks per thread
 
-template <int FMT, int ROUND, bool RHT>
-__global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, int64_t qrows,
+// T = uint16_t: bf16 input (the fused kernel). T = float: fp32 input quantized without a transform, the
+// second half of the unfused form (a standalone RHT writes y in fp32, see rht_rows_kernel).
+template <int FMT, int ROUND, bool RHT, typename T = uint16_t>
+__global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x, int64_t ld, int64_t qrows,
                                                          int64_t nb, QuantArgs qa, uint8_t* __restrict__ codes,
                                                          int64_t code_pld, float* __restrict__ scales,
                                                          int64_t scale_pld) {
+    constexpr int kVec = (int)sizeof(T) * kBlock / 16;  // 16-byte loads per block: 2 (bf16) or 4 (fp32)
+    static_assert(sizeof(T) == 2 || !RHT, "the fp32-input kernel applies no transform");
     __shared__ uint2 s_codes[kRB][kRR];
     __shared__ float s_scales[kRB][kRR];
     const int t = threadIdx.x;
@@ -223,16 +236,17 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restr
     const int64_t b0 = (int64_t)blockIdx.x * kRB;
 
     // item k = t + kRT q: row k / 16, block k % 16 of the tile
-    uint4 v[kRI][2];
+    uint4 v[kRI][kVec];
 #pragma unroll
     for (int q = 0; q < kRI; ++q) {
         const int k = t + kRT * q;
         const int64_t r = r0 + (k >> 4), b = b0 + (k & 15);
-        v[q][0] = v[q][1] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int c = 0; c < kVec; ++c) v[q][c] = make_uint4(0, 0, 0, 0);
         if (r < qrows && b < nb) {
             const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kBlock);
-            v[q][0] = src[0];
-            v[q][1] = src[1];
+#pragma unroll
+            for (int c = 0; c < kVec; ++c) v[q][c] = src[c];
         }
     }
 #pragma unroll
@@ -242,9 +256,21 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const uint16_t* __restr
         uint32_t lo = 0, hi = 0;
         float sc = 0.0f;
         if (r < qrows && b < nb) {
-            const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
-                                   v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
-            quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
+                                       v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
+                quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+            } else {
+                float y[16];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    y[4 * c] = __uint_as_float(v[q][c].x);
+                    y[4 * c + 1] = __uint_as_float(v[q][c].y);
+                    y[4 * c + 2] = __uint_as_float(v[q][c].z);
+                    y[4 * c + 3] = __uint_as_float(v[q][c].w);
+                }
+                quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+            }
         }
         s_codes[k & 15][k >> 4] = make_uint2(lo, hi);
         s_scales[k & 15][k >> 4] = sc;
@@ -662,15 +688,182 @@ __global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict
 // ------------------------------------------------------------------------------------------------
 // Host-side launchers
 // ------------------------------------------------------------------------------------------------
+// ------------------------------------------------------------------------------------------------
+// Quality statistics (Sec. 3.2 diagnostics). Every block is quantized as by the quantizers above, its codes
+// are dequantized in registers (q = level * s, exact in fp64) and the kernel accumulates in fp64
+// (q - ref)^2, ref^2 and q * ref, where ref is the value the quantizer rounds (the fp32 RHT output, or x),
+// and counts the codes per magnitude code; nothing else is written. One thread per block in a grid-stride
+// loop. Rowwise: consecutive threads take consecutive blocks of a row (32 contiguous bytes each).
+// Transposed: consecutive threads take consecutive operand rows (columns of X) of one block, so each of
+// the 16 row loads of a wave reads one contiguous 128-byte run.
+// ------------------------------------------------------------------------------------------------
+constexpr int kStatsThreads = 256;
+constexpr int kStatsMaxGrid = 1024;  // few workgroups: one atomic per field and workgroup
+
+template <int FMT>
+__device__ __forceinline__ float level_of_nibble(uint32_t nib) {
+    const uint32_t m = nib & 7u;
+    float lv;
+    if constexpr (FMT == kFmtUniform) lv = (float)m;
+    else lv = m <= 4u ? 0.5f * (float)m : (m == 7u ? 6.0f : (float)(m - 2u));  // 0 .5 1 1.5 2 | 3 4 | 6
+    return (nib & 8u) ? -lv : lv;
+}
+
+__global__ void stats_zero_kernel(QuantStats* out) {
+    if (threadIdx.x == 0) {
+        out->err2 = 0.0;
+        out->ref2 = 0.0;
+        out->cross = 0.0;
+    }
+    if (threadIdx.x < 8) out->hist[threadIdx.x] = 0ull;
+}
+
+template <int FMT, int ROUND, bool RHT, bool TRANS>
+__global__ __launch_bounds__(kStatsThreads) void quant_stats_kernel(const uint16_t* __restrict__ x, int64_t ld,
+                                                                    int64_t qrows, int64_t nb, QuantArgs qa,
+                                                                    QuantStats* __restrict__ out) {
+    double e2 = 0.0, r2 = 0.0, cr = 0.0;
+    uint32_t hist[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const int64_t total = qrows * nb;
+    const int64_t step = (int64_t)gridDim.x * kStatsThreads;
+    for (int64_t id = (int64_t)blockIdx.x * kStatsThreads + threadIdx.x; id < total; id += step) {
+        int64_t r, b;
+        uint32_t w[8];
+        if constexpr (!TRANS) {
+            r = id / nb;
+            b = id - r * nb;
+            const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kBlock);
+            const uint4 v0 = src[0], v1 = src[1];
+            w[0] = v0.x; w[1] = v0.y; w[2] = v0.z; w[3] = v0.w;
+            w[4] = v1.x; w[5] = v1.y; w[6] = v1.z; w[7] = v1.w;
+        } else {
+            b = id / qrows;
+            r = id - b * qrows;
+            const uint16_t* src = x + b * kBlock * ld + r;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = (uint32_t)src[(2 * j) * ld] | ((uint32_t)src[(2 * j + 1) * ld] << 16);
+        }
+        float y[16];
+        rht16_unscaled<RHT>(w, qa, y);
+        uint32_t lo, hi;
+        float sc;
+        quant_y16<FMT, ROUND, RHT>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+        const double s = (double)sc;
+        uint64_t counts = 0;  // one byte per magnitude code: at most 16 per block
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const uint32_t nib = ((i < 8 ? lo : hi) >> (4 * (i & 7))) & 15u;
+            const double q = (double)level_of_nibble<FMT>(nib) * s;  // a 4-bit level times an fp32 scale: exact
+            const double ref = RHT ? 0.25 * (double)y[i] : (double)y[i];  // y holds 4y under the RHT
+            const double d = q - ref;
+            e2 = __builtin_fma(d, d, e2);
+            r2 = __builtin_fma(ref, ref, r2);
+            cr = __builtin_fma(q, ref, cr);
+            counts += 1ull << (8 * (nib & 7u));
+        }
+#pragma unroll
+        for (int m = 0; m < 8; ++m) hist[m] += (uint32_t)(counts >> (8 * m)) & 0xFFu;
+    }
+    // wave sums, then the four waves through LDS, then one atomic per field and workgroup
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        e2 += __shfl_xor(e2, o);
+        r2 += __shfl_xor(r2, o);
+        cr += __shfl_xor(cr, o);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) hist[m] += __shfl_xor(hist[m], o);
+    }
+    __shared__ double s_sum[3][kStatsThreads / 64];
+    __shared__ uint32_t s_hist[8][kStatsThreads / 64];
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_sum[0][wave] = e2;
+        s_sum[1][wave] = r2;
+        s_sum[2][wave] = cr;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) s_hist[m][wave] = hist[m];
+    }
+    __syncthreads();
+    if (threadIdx.x < 3) {
+        double t = 0.0;
+        for (int k = 0; k < kStatsThreads / 64; ++k) t += s_sum[threadIdx.x][k];
+        atomicAdd(threadIdx.x == 0 ? &out->err2 : (threadIdx.x == 1 ? &out->ref2 : &out->cross), t);
+    } else if (threadIdx.x >= 64 && threadIdx.x < 72) {
+        const int m = threadIdx.x - 64;
+        unsigned long long t = 0;
+        for (int k = 0; k < kStatsThreads / 64; ++k) t += s_hist[m][k];
+        if (t) atomicAdd(&out->hist[m], t);
+    }
+}
+
 template <int FMT, int ROUND, bool RHT>
+static hipError_t launch_stats_t(const StatsJob& j, hipStream_t s) {
+    const int64_t nb = j.red / kBlock;
+    const int64_t total = j.qrows * nb;
+    const int64_t want = (total + kStatsThreads - 1) / kStatsThreads;
+    const unsigned grid = (unsigned)(want < kStatsMaxGrid ? want : kStatsMaxGrid);
+    if (grid == 0) return hipSuccess;
+    const uint16_t* x = static_cast<const uint16_t*>(j.x);
+    if (j.transpose) quant_stats_kernel<FMT, ROUND, RHT, true><<<grid, kStatsThreads, 0, s>>>(x, j.ld, j.qrows, nb, j.qa, j.stats);
+    else quant_stats_kernel<FMT, ROUND, RHT, false><<<grid, kStatsThreads, 0, s>>>(x, j.ld, j.qrows, nb, j.qa, j.stats);
+    return hipGetLastError();
+}
+
+template <int FMT>
+static hipError_t dispatch_stats(const StatsJob& j, hipStream_t s) {
+    if (j.rounding == kRoundSR) return j.rht ? launch_stats_t<FMT, kRoundSR, true>(j, s) : launch_stats_t<FMT, kRoundSR, false>(j, s);
+    return j.rht ? launch_stats_t<FMT, kRoundRTNE, true>(j, s) : launch_stats_t<FMT, kRoundRTNE, false>(j, s);
+}
+
+hipError_t launch_quant_stats(const StatsJob& j, hipStream_t s) {
+    stats_zero_kernel<<<1, 64, 0, s>>>(j.stats);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return j.format == kFmtE2M1 ? dispatch_stats<kFmtE2M1>(j, s) : dispatch_stats<kFmtUniform>(j, s);
+}
+
+template <int FMT, int ROUND, bool RHT, typename T = uint16_t>
 static hipError_t launch_rows_t(const QuantJob& j, hipStream_t s) {
     const int64_t nb = j.red / kBlock;
     const int64_t prows = padded_rows(j.qrows);
     if (nb == 0 || prows == 0) return hipSuccess;
     const dim3 grid((unsigned)((nb + kRB - 1) / kRB), (unsigned)(prows / kRR));
-    quant_rows_kernel<FMT, ROUND, RHT><<<grid, kRT, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, j.qrows, nb, j.qa,
-                                                           static_cast<uint8_t*>(j.codes), j.code_pld, j.scales,
-                                                           j.scale_pld);
+    quant_rows_kernel<FMT, ROUND, RHT, T><<<grid, kRT, 0, s>>>(static_cast<const T*>(j.x), j.ld, j.qrows, nb, j.qa,
+                                                              static_cast<uint8_t*>(j.codes), j.code_pld, j.scales,
+                                                              j.scale_pld);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------------
+// Unfused form (Sec. 5 Q5 compares it with the fused kernel): a standalone block-16 RHT writes y =
+// RN32(x S16 H16) in fp32 (one thread per block, 32 bytes in, 64 bytes out), then quant_rows_kernel<.., float>
+// quantizes y without a transform. The fp32 intermediate holds y exactly, so both forms give the same codes.
+// ------------------------------------------------------------------------------------------------
+constexpr int kRhtThreads = 256;
+
+__global__ __launch_bounds__(kRhtThreads) void rht_rows_kernel(const uint16_t* __restrict__ x, int64_t ld,
+                                                               int64_t rows, int64_t nb, QuantArgs qa,
+                                                               float* __restrict__ y, int64_t ldy) {
+    const int64_t b = (int64_t)blockIdx.x * kRhtThreads + threadIdx.x;
+    if (b >= nb) return;
+    for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+        const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kBlock);
+        const uint4 v0 = src[0], v1 = src[1];
+        const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        float yv[16];
+        rht16_unscaled<true>(w, qa, yv);  // 4y
+        float4* dst = reinterpret_cast<float4*>(y + r * ldy + b * kBlock);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            dst[c] = make_float4(yv[4 * c] * 0.25f, yv[4 * c + 1] * 0.25f, yv[4 * c + 2] * 0.25f, yv[4 * c + 3] * 0.25f);
+    }
+}
+
+hipError_t launch_rht(const RhtJob& j, hipStream_t s) {
+    const int64_t nb = j.cols / kBlock;
+    if (nb == 0 || j.rows == 0) return hipSuccess;
+    const dim3 grid((unsigned)((nb + kRhtThreads - 1) / kRhtThreads), (unsigned)(j.rows < 65535 ? j.rows : 65535));
+    rht_rows_kernel<<<grid, kRhtThreads, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, j.rows, nb, j.qa, j.y, j.ldy);
     return hipGetLastError();
 }
 
@@ -690,6 +883,10 @@ static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
 
 template <int FMT, int ROUND, bool RHT>
 static hipError_t dispatch_layout(const QuantJob& j, hipStream_t s) {
+    if (j.input_f32) {
+        if constexpr (RHT) return hipErrorInvalidValue;  // rejected by the API layer
+        else return launch_rows_t<FMT, ROUND, false, float>(j, s);
+    }
     if (!j.transpose) return launch_rows_t<FMT, ROUND, RHT>(j, s);
     if (j.group_off) return launch_cols_t<FMT, ROUND, RHT, true>(j, s);
     return launch_cols_t<FMT, ROUND, RHT, false>(j, s);

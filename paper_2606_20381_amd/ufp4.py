@@ -7,7 +7,9 @@ must be built (``python -m paper_2606_20381_amd.build``); without it every call 
 from __future__ import annotations
 
 import ctypes
+import math
 import os
+import struct
 from dataclasses import dataclass
 
 import torch
@@ -41,6 +43,11 @@ SIGNATURES = {
                                  _I64, _P, _I64, _P], _INT),
     "ufp4_quantize_dual": ([_INT, _P, _I64, _I64, _I64, _INT, _U32, _U32, _INT, _U32, _U32, _INT, _U64, _P, _I64, _P,
                             _I64, _P, _I64, _P, _I64, _P], _INT),
+    "ufp4_e2m1_quantize_range": ([_P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, ctypes.c_float, _P, _I64,
+                                  _P, _I64, _P], _INT),
+    "ufp4_quant_stats": ([_INT, ctypes.c_float, _P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, _P, _P], _INT),
+    "ufp4_rht": ([_P, _I64, _I64, _I64, _U32, _P, _I64, _P], _INT),
+    "ufp4_quantize_f32": ([_INT, _P, _I64, _I64, _I64, _INT, _U64, _U32, _P, _I64, _P, _I64, _P], _INT),
     "ufp4_mx_quantize": (_QUANT_ARGS, _INT),
     "ufp4_mx_gemm_fwd_y": (_GEMM_MX_ARGS, _INT),
     "ufp4_mx_gemm_bwd_dx": (_GEMM_MX_ARGS, _INT),
@@ -170,6 +177,112 @@ def e2m1_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = False
                   rounding: int = RTNE, seed: int = 0, stream_id: int = 0, out: QTensor | None = None) -> QTensor:
     """Fused (optional) RHT + E2M1 quantization (ufp4_e2m1_quantize), the comparison baseline."""
     return _quantize_call("ufp4_e2m1_quantize", E2M1, x, transpose, rht, sign_mask, rounding, seed, stream_id, out)
+
+
+def e2m1_quantize_range(x: torch.Tensor, max_fpx: float, *, transpose: bool = False, rht: bool = False,
+                        sign_mask: int = 0, rounding: int = RTNE, seed: int = 0, stream_id: int = 0,
+                        out: QTensor | None = None) -> QTensor:
+    """E2M1 quantization on the grid cut at max_fpx in {2, 4, 6} (ufp4_e2m1_quantize_range)."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    qrows, red = (cols, rows) if transpose else (rows, cols)
+    q = out if out is not None else empty_qtensor(qrows, red, E2M1, x.device)
+    st = lib().ufp4_e2m1_quantize_range(x.data_ptr(), rows, cols, x.stride(0), int(transpose), int(rht), sign_mask,
+                                        rounding, seed & 0xFFFFFFFFFFFFFFFF, stream_id, float(max_fpx),
+                                        q.codes.data_ptr(), q.code_panel_ld, q.scales.data_ptr(), q.scale_panel_ld,
+                                        _stream())
+    _check(st, "ufp4_e2m1_quantize_range")
+    return q
+
+
+def rht(x: torch.Tensor, *, sign_mask: int = 0, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Standalone block-16 RHT along the rows of x (ufp4_rht): fp32 [rows, cols]."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    y = out if out is not None else torch.empty(x.shape, dtype=torch.float32, device=x.device)
+    if y.dtype != torch.float32 or y.shape != x.shape or y.stride(1) != 1:
+        raise ValueError("out must be a row-major fp32 tensor of x's shape")
+    st = lib().ufp4_rht(x.data_ptr(), x.shape[0], x.shape[1], x.stride(0), sign_mask, y.data_ptr(), y.stride(0),
+                        _stream())
+    _check(st, "ufp4_rht")
+    return y
+
+
+def quantize_f32(x: torch.Tensor, fmt: int = UNIFORM, *, rounding: int = RTNE, seed: int = 0, stream_id: int = 0,
+                 out: QTensor | None = None) -> QTensor:
+    """Rowwise quantization of an fp32 tensor, no transform (ufp4_quantize_f32)."""
+    if x.dtype != torch.float32 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major fp32 CUDA tensor")
+    rows, cols = x.shape
+    q = out if out is not None else empty_qtensor(rows, cols, fmt, x.device)
+    st = lib().ufp4_quantize_f32(fmt, x.data_ptr(), rows, cols, x.stride(0), rounding, seed & 0xFFFFFFFFFFFFFFFF,
+                                 stream_id, q.codes.data_ptr(), q.code_panel_ld, q.scales.data_ptr(),
+                                 q.scale_panel_ld, _stream())
+    _check(st, "ufp4_quantize_f32")
+    return q
+
+
+# number of levels (magnitude buckets, zero included) of each grid: B_eff's K
+def grid_levels(fmt: int, max_fpx: float = 0.0) -> int:
+    if fmt == UNIFORM or max_fpx in (0.0, 6.0):
+        return 8
+    return {2.0: 5, 4.0: 7}[float(max_fpx)]
+
+
+@dataclass
+class QuantStats:
+    """Record of ufp4_quant_stats: fp64 sums over the elements and the magnitude-code histogram."""
+
+    err2: float
+    ref2: float
+    cross: float
+    hist: list
+    fmt: int
+    max_fpx: float
+
+    @property
+    def nmse(self) -> float:
+        return self.err2 / self.ref2 if self.ref2 > 0 else float("nan")
+
+    @property
+    def sqnr_db(self) -> float:
+        return -10.0 * math.log10(self.nmse) if self.err2 > 0 else float("inf")
+
+    @property
+    def alpha(self) -> float:
+        return self.cross / self.ref2 if self.ref2 > 0 else float("nan")
+
+    @property
+    def beff(self) -> float:
+        k = grid_levels(self.fmt, self.max_fpx)
+        n = sum(self.hist[:k])
+        ent = -sum((h / n) * math.log(h / n + 1e-12) for h in self.hist[:k]) if n else 0.0
+        return math.exp(ent) / k
+
+
+STATS_BYTES = 88  # 3 doubles + 8 uint64
+
+
+def quant_stats(x: torch.Tensor, fmt: int = UNIFORM, *, max_fpx: float = 0.0, transpose: bool = False,
+                rht: bool = True, sign_mask: int = 0, rounding: int = RTNE, seed: int = 0, stream_id: int = 0,
+                out: torch.Tensor | None = None) -> QuantStats:
+    """Quality statistics of one quantization of x (ufp4_quant_stats); synchronizes to read the record."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    rec = out if out is not None else torch.empty(STATS_BYTES // 8, dtype=torch.float64, device=x.device)
+    st = lib().ufp4_quant_stats(fmt, float(max_fpx), x.data_ptr(), rows, cols, x.stride(0), int(transpose), int(rht),
+                                sign_mask, rounding, seed & 0xFFFFFFFFFFFFFFFF, stream_id, rec.data_ptr(), _stream())
+    _check(st, "ufp4_quant_stats")
+    raw = rec.cpu().numpy().tobytes()
+    vals = struct.unpack("<3d8Q", raw[:STATS_BYTES])
+    return QuantStats(vals[0], vals[1], vals[2], list(vals[3:]), fmt, float(max_fpx))
+
+
+def delta_sqnr_db(raw: QuantStats, rotated: QuantStats) -> float:
+    """10 log10(NMSE_I / NMSE_H16) (Sec. 3.2): positive when the rotation lowers the quantization error."""
+    return 10.0 * math.log10(raw.nmse / rotated.nmse)
 
 
 def quantize_dual(x: torch.Tensor, *, fmt: int = UNIFORM, rht_rows: bool = True, rht_cols: bool = True,

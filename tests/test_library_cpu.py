@@ -191,3 +191,47 @@ def test_mx_validation(lib):
                                    None) == 2  # reduction N % 32
     assert lib.ufp4_mx_gemm_bwd_dw(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 48, 16, 16, FAKE, 16, 0,
                                    None) == 2  # reduction M % 32
+
+
+def test_quant_stats_validation(lib):
+    """ufp4_quant_stats(format, max_fpx, x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, rec)"""
+    ok = (0, 0.0, FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE)
+    cases = [
+        ((0, 4.0) + ok[2:], 1),                  # max_fpx on the uniform grid
+        ((1, 3.0) + ok[2:], 1),                  # max_fpx not in {2, 4, 6}
+        ((2,) + ok[1:], 1),                      # format enum
+        (ok[:2] + (None,) + ok[3:], 1),          # null input
+        (ok[:12] + (None,), 1),                  # null record
+        (ok[:12] + (FAKE + 4,), 3),              # record alignment
+        (ok[:4] + (24, 24) + ok[6:], 2),         # cols % 16
+        (ok[:5] + (30,) + ok[6:], 2),            # ld < cols
+        (ok[:6] + (2,) + ok[7:], 1),             # transpose flag
+        (ok[:9] + (2,) + ok[10:], 1),            # rounding enum
+    ]
+    for args, status in cases:
+        assert lib.ufp4_quant_stats(*args, None) == status, args
+
+
+def test_e2m1_range_validation(lib):
+    args = (FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0)
+    for mf in (0.0, 1.0, 3.0, 7.0):
+        assert lib.ufp4_e2m1_quantize_range(*args, mf, FAKE, 2 * 1024, FAKE, 2 * 128, None) == 1
+    assert lib.ufp4_e2m1_quantize_range(FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, 4.0, FAKE, 2048, FAKE, 256, None) == 2
+
+
+def test_unfused_validation(lib):
+    # ufp4_rht(x, rows, cols, ld, mask, y, ldy, stream)
+    assert lib.ufp4_rht(None, 16, 32, 32, 0, FAKE, 32, None) == 1
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0x10000, FAKE, 32, None) == 1
+    assert lib.ufp4_rht(FAKE, 16, 24, 24, 0, FAKE, 24, None) == 2      # cols % 16
+    assert lib.ufp4_rht(FAKE, 16, 32, 36, 0, FAKE, 32, None) == 2      # ld % 8
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 30, None) == 2      # ldy < cols
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 34, None) == 2      # ldy % 4
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE + 4, 32, None) == 3  # y alignment
+    # ufp4_quantize_f32(format, x, rows, cols, ld, rounding, seed, stream, codes, cld, scales, sld, stream)
+    assert lib.ufp4_quantize_f32(2, FAKE, 16, 32, 32, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 1
+    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 32, 2, 0, 0, FAKE, C2, FAKE, S2, None) == 1
+    assert lib.ufp4_quantize_f32(0, FAKE, 16, 24, 24, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 2
+    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 34, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 2   # ld % 4
+    assert lib.ufp4_quantize_f32(0, FAKE + 8, 16, 32, 32, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 3
+    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 32, 0, 0, 0, FAKE, C1, FAKE, S2, None) == 2   # code panel stride
