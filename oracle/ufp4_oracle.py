@@ -125,11 +125,11 @@ def sign_vector(sign_mask: int, n: int = BLOCK) -> np.ndarray:
 
 
 def _check_rht_domain(blocks: np.ndarray) -> None:
-    """Check that the fp64 evaluation of every 16-term sum is exact.
+    """Check that the fp64 evaluation of every n-term sum (n = the last axis, 16 by default) is exact.
 
     Each term is a bf16 value (8 significant bits). With frexp exponents e_max and e_min over the nonzero
-    entries of a block, the exact sum is a multiple of 2^(e_min - 8) below 2^(e_max + 4) in magnitude, so
-    it fits the 53-bit fp64 significand when e_max - e_min <= 41.
+    entries of a block, the exact sum is a multiple of 2^(e_min - 8) below 2^(e_max + log2 n) in magnitude,
+    so it fits the 53-bit fp64 significand when e_max - e_min <= 45 - log2 n (41 for n = 16).
     """
     mag = np.abs(blocks)
     nz = mag > 0
@@ -137,8 +137,9 @@ def _check_rht_domain(blocks: np.ndarray) -> None:
     e_max = np.where(nz, e, np.iinfo(np.int32).min).max(axis=-1)
     e_min = np.where(nz, e, np.iinfo(np.int32).max).min(axis=-1)
     spread = np.where(nz.any(axis=-1), e_max - e_min, 0)
-    if np.any(spread > 41):
-        raise ValueError("a block spans more than 2^41 in magnitude: the RHT sum is not exact in fp64")
+    limit = 45 - int(np.log2(blocks.shape[-1]))
+    if np.any(spread > limit):
+        raise ValueError(f"a block spans more than 2^{limit} in magnitude: the RHT sum is not exact in fp64")
 
 
 def rht_exact_f64(blocks: np.ndarray, sign_mask: int) -> np.ndarray:
@@ -164,6 +165,41 @@ def rht_blocks(blocks_f32: np.ndarray, sign_mask: int) -> np.ndarray:
     b64 = np.asarray(blocks_f32, dtype=np.float64)
     _check_rht_domain(b64)
     y = rht_exact_f64(b64, sign_mask).astype(np.float32)
+    mag = np.abs(y)
+    if np.any((mag > 0) & (mag < FP32_MIN_NORMAL)):
+        raise ValueError("an RHT output is a subnormal fp32 number: outside the supported domain")
+    return y
+
+
+# RHT blocks larger than the quantization block (the RHT block-size dimension of the E2M1 reference search,
+# Appendix search-space table: 16 / 32 / 64 / 128). The transform of each n-block is x S_n H_n with the
+# normalisation 1/sqrt(n) of the Sec. 2.2 recursion; the 16-blocks of its output are then quantized as usual.
+RHT_BLOCKS = (16, 32, 64, 128)
+
+
+def rht_norm(n: int) -> float:
+    """fp64 normalisation of the n-point RHT: RN64(sqrt(1/n)); exactly 1/4 and 1/8 for n = 16 and 64."""
+    return float(np.sqrt(1.0 / n))
+
+
+def rht_rows_n(a_f32: np.ndarray, sign_mask: int, n: int) -> np.ndarray:
+    """RHT of the n-blocks of every row of A [rows, red] (red % n == 0), as fp32.
+
+    y = RN32( RN64( S * RN64(1/sqrt(n)) ) ) with S = sum_j H_n^pm1[i,j] eps_j x_j exact in fp64 (explicit matrix
+    product, `_check_rht_domain`). For n = 16 and 64 the normalisation is a power of two and y is the correctly
+    rounded transform; for n = 32 and 128 it is the fp64-rounded product, then rounded to fp32. eps_j = -1 iff
+    bit j of the n-bit `sign_mask` is set.
+    """
+    if n not in RHT_BLOCKS:
+        raise ValueError("RHT block must be 16, 32, 64 or 128")
+    a = np.asarray(a_f32, dtype=np.float64)
+    rows, red = a.shape
+    if red % n:
+        raise ValueError("the reduction length must be a multiple of the RHT block")
+    blocks = a.reshape(rows, red // n, n)
+    _check_rht_domain(blocks)
+    s = (blocks * sign_vector(sign_mask, n)) @ hadamard_pm1(n)
+    y = (s * rht_norm(n)).astype(np.float32).reshape(rows, red)
     mag = np.abs(y)
     if np.any((mag > 0) & (mag < FP32_MIN_NORMAL)):
         raise ValueError("an RHT output is a subnormal fp32 number: outside the supported domain")
@@ -299,14 +335,16 @@ def _check_block_domain(amax: np.ndarray, g: float) -> None:
 
 
 def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0,
-                  seed: int = 0, stream: int = 0, row_ids=None, block_base: int = 0, max_fpx=None):
+                  seed: int = 0, stream: int = 0, row_ids=None, block_base: int = 0, max_fpx=None,
+                  rht_block: int = BLOCK):
     """Quantize an operand A [rows, red] along its contiguous (reduction) axis.
 
     Steps per 1x16 block B (Sec. 2.1 display; RHT of Sec. 2.2 applied first when `rht`):
       y = RHT(x) or x;  s = RN32(amax/g);  q_i = rho(y_i / s) with y_i/s taken as RN32(y_i * RN32(g/amax)).
     `row_ids` are the global row numbers used in the SR counters (default 0..rows-1); `block_base` is
     added to the block number (used for operands cut out of a longer reduction axis). `max_fpx` (E2M1
-    only) restricts the grid to the levels up to it, with g = max_fpx.
+    only) restricts the grid to the levels up to it, with g = max_fpx. `rht_block` > 16 rotates n-blocks
+    (`rht_rows_n`, with an n-bit sign mask) before the 1x16 quantization.
     Returns (signed level indices int64 [rows, red], scales fp32 [rows, red/16]).
     """
     a = np.asarray(a_f32, dtype=np.float32)
@@ -315,7 +353,10 @@ def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_ma
         raise ValueError("reduction length must be a multiple of 16")
     nb = red // BLOCK
     blocks = a.reshape(rows, nb, BLOCK)
-    y = rht_blocks(blocks, sign_mask) if rht else blocks.copy()
+    if rht and rht_block != BLOCK:
+        y = rht_rows_n(a, sign_mask, rht_block).reshape(rows, nb, BLOCK)
+    else:
+        y = rht_blocks(blocks, sign_mask) if rht else blocks.copy()
     if not np.all(np.isfinite(y)):
         raise ValueError("non-finite value after the transform")
     g = np.float32(grid_gmax(fmt, max_fpx))

@@ -662,6 +662,75 @@ def test_max_fpx_on_grid_block_is_reproduced():
 
 
 # ------------------------------------------------------------------------------------------------
+# RHT blocks of 32 / 64 / 128 (Appendix search space: RHT block size)
+# ------------------------------------------------------------------------------------------------
+
+def _rn32(fr: Fraction) -> np.float32:
+    """The fp32 number nearest to an exact rational, ties to the even significand."""
+    c = np.float32(float(fr))
+    cands = [np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))]
+    return min(cands, key=lambda v: (abs(Fraction(float(v)) - fr), int(np.float32(v).view(np.uint32)) & 1))
+
+
+def test_rht_n_matrix_is_scipys_sylvester_hadamard():
+    import scipy.linalg
+
+    for n in O.RHT_BLOCKS:
+        assert np.array_equal(O.hadamard_pm1(n), scipy.linalg.hadamard(n).astype(np.float64))
+    assert O.rht_norm(16) == 0.25 and O.rht_norm(64) == 0.125
+
+
+def test_rht_n_of_a_unit_vector_and_block_16():
+    """e_0 without signs -> every output is RN32(1/sqrt(n)); n = 16 reduces to the block-16 RHT."""
+    for n in (32, 64, 128):
+        a = np.zeros((1, n), np.float32)
+        a[0, 0] = 1.0
+        y = O.rht_rows_n(a, 0, n)
+        assert np.all(y == np.float32(1.0 / np.sqrt(n)))
+        # a sign flip on position 0 flips every output
+        assert np.all(O.rht_rows_n(a, 1, n) == -y)
+    rng = np.random.default_rng(71)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (8, 64)))
+    assert np.array_equal(O.rht_rows_n(a, 0x9A3C, 16), O.rht_blocks(a.reshape(8, 4, 16), 0x9A3C).reshape(8, 64))
+
+
+def test_rht_n_is_orthogonal_and_matches_exact_rationals():
+    """Parseval within fp32 rounding; for n = 64 (power-of-two normalisation) every output equals the exact
+    rational sum rounded once to fp32."""
+    rng = np.random.default_rng(72)
+    for n in (32, 64, 128):
+        a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (6, 2 * n)))
+        mask = int(rng.integers(0, 2 ** 62)) | (int(rng.integers(0, 2 ** 62)) << 62)
+        mask &= (1 << n) - 1
+        y = O.rht_rows_n(a, mask, n).astype(np.float64)
+        xb = a.astype(np.float64).reshape(6, 2, n)
+        yb = y.reshape(6, 2, n)
+        assert np.allclose((yb ** 2).sum(-1), (xb ** 2).sum(-1), rtol=1e-6)
+        if n == 64:
+            for r in range(2):
+                for i in (0, 5, 63):
+                    tot = sum(Fraction(float(xb[r, 0, j])) * (-1 if (mask >> j) & 1 else 1)
+                              * (-1 if bin(i & j).count("1") % 2 else 1) for j in range(n)) / 8
+                    assert _rn32(tot) == np.float32(y[r, i])
+
+
+def test_quantize_rows_with_rht_block_n():
+    """rht_block = n quantizes the 16-blocks of the n-point transform; n = 16 is the default path."""
+    rng = np.random.default_rng(73)
+    a = O.bf16_bits_to_f32(_rand_bf16_bits(rng, (10, 128)))
+    i16, s16 = O.quantize_rows(a, O.UNIFORM, O.SR, True, 0x77, 3, 0)
+    j16, t16 = O.quantize_rows(a, O.UNIFORM, O.SR, True, 0x77, 3, 0, rht_block=16)
+    assert np.array_equal(i16, j16) and np.array_equal(s16, t16)
+    for n in (32, 64, 128):
+        y = O.rht_rows_n(a, 0x123456789, n)
+        want = O.quantize_rows(y, O.UNIFORM, O.RTNE, False)
+        got = O.quantize_rows(a, O.UNIFORM, O.RTNE, True, 0x123456789, rht_block=n)
+        assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+    with pytest.raises(ValueError):
+        O.quantize_rows(a[:, :48], O.UNIFORM, O.RTNE, True, 0, rht_block=32)
+
+
+# ------------------------------------------------------------------------------------------------
 # Uniform grid with power-of-two block scales (Sec. 4: scale hierarchy chosen for the hardware)
 # ------------------------------------------------------------------------------------------------
 
