@@ -116,6 +116,23 @@ int ufp4_e2m1_quantize_range(const void *x_dev, int64_t rows, int64_t cols, int6
                              void *stream);
 
 /*
+ * ufp4_quantize_rht_block -- RHT over blocks of n = 16, 32, 64 or 128 elements along the reduction axis, then
+ * the usual 1x16 quantization of the result (the RHT block-size dimension of the paper's E2M1 reference
+ * search, Appendix; the recipe itself uses 16). Per n-block: y = RN32( RN64( S * RN64(sqrt(1/n)) ) ) with S the
+ * exact sum_j H_n[i,j] eps_j x_j (H_n the Sylvester +-1 matrix, exact when a block's nonzero |x| span at
+ * most 2^(45 - log2 n)); for n = 16 and 64 the factor is a power of two and y is correctly rounded.
+ *   rht_block        16, 32, 64 or 128; the reduction length must be a multiple of it.
+ *   sign_words_host  host array of rht_block / 16 words: eps_j = -1 iff bit (j % 16) of word j / 16 is set.
+ *   format           UFP4_FMT_UNIFORM or UFP4_FMT_E2M1 (full grid). Rowwise and plain transposed operands
+ *                    (not grouped). rht_block = 16 is ufp4_rht_quantize / ufp4_e2m1_quantize with rht = 1.
+ *   Remaining arguments as ufp4_rht_quantize. A GEMM's two operands must use the same block and signs.
+ */
+int ufp4_quantize_rht_block(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,
+                            int rht_block, const uint16_t *sign_words_host, int rounding, uint64_t seed,
+                            uint32_t stream_id, void *codes_dev, int64_t code_panel_ld, float *scales_dev,
+                            int64_t scale_panel_ld, void *stream);
+
+/*
  * ufp4_quant_stats -- quality statistics of one quantization, the sums behind the diagnostics of Sec. 3.2
  * (NMSE_A(G, T), SQNR, the operand projection alpha, the bucket entropy behind B_eff). The operand is
  * quantized exactly as ufp4_rht_quantize / ufp4_e2m1_quantize(_range) would quantize it, but nothing is

@@ -2,6 +2,7 @@
 // Declarations and the meaning of every argument are in include/ufp4.h.
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 #include "../../include/ufp4.h"
@@ -33,6 +34,8 @@ void fill_grid(float max_fpx, QuantArgs& qa) {
     const float g = max_fpx == 0.0f ? 6.0f : max_fpx;
     qa.e2m1_g = g;
     qa.e2m1_ginv = 1.0f / g;  // RN(1/g), as the kernels' constant for the uniform grid
+    qa.rht_m = 1;             // block-16 RHT unless a caller asks for a wider one
+    qa.rht_c = 0.25;
 }
 
 constexpr int64_t kMaxCodePanelLd = int64_t(1) << 29;   // bytes
@@ -68,9 +71,11 @@ int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, in
     return UFP4_OK;
 }
 
+// rht_block 16 (with sign_mask) or 32 / 64 / 128 (with the n/16 words of `sign_words`).
 int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                   uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void* codes, int64_t code_pld,
-                  float* scales, int64_t scale_pld, void* stream, float max_fpx = 0.0f) {
+                  float* scales, int64_t scale_pld, void* stream, float max_fpx = 0.0f, int rht_block = 16,
+                  const uint16_t* sign_words = nullptr) {
     if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
     if (!valid_max_fpx(format, max_fpx)) return UFP4_ERR_INVALID_ARG;
     const int64_t red = transpose ? rows : cols;
@@ -80,6 +85,7 @@ int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t
     if (st != UFP4_OK) return st;
     // rowwise: one workgroup per 32 padded rows along the grid's y dimension
     if (!transpose && padded_rows(qrows) / 32 > 65535) return UFP4_ERR_UNSUPPORTED;
+    if (rht_block != 16 && red % rht_block != 0) return UFP4_ERR_SHAPE;
     if (rows == 0 || cols == 0) return UFP4_OK;
     QuantJob j{};
     j.format = format;
@@ -96,6 +102,9 @@ int quantize_impl(int format, const void* x, int64_t rows, int64_t cols, int64_t
     j.num_groups = 1;
     fill_sign_xor(sign_mask, j.qa.sign_xor);
     fill_grid(max_fpx, j.qa);
+    j.qa.rht_m = rht_block / 16;
+    j.qa.rht_c = sqrt(1.0 / rht_block);  // correctly rounded square root of an exact power of two
+    for (int k = 0; k < rht_block / 16 && sign_words; ++k) j.qa.sign_words[k] = sign_words[k];
     j.qa.key0 = (uint32_t)seed;
     j.qa.key1 = (uint32_t)(seed >> 32);
     j.qa.stream = stream_id;
@@ -284,6 +293,20 @@ int ufp4_e2m1_quantize_range(const void* x_dev, int64_t rows, int64_t cols, int6
     if (max_fpx == 0.0f) return UFP4_ERR_INVALID_ARG;  // the full grid is ufp4_e2m1_quantize
     return quantize_impl(UFP4_FMT_E2M1, x_dev, rows, cols, ld, transpose, rht, sign_mask, rounding, seed, stream_id,
                          codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream, max_fpx);
+}
+
+int ufp4_quantize_rht_block(int format, const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,
+                            int rht_block, const uint16_t* sign_words_host, int rounding, uint64_t seed,
+                            uint32_t stream_id, void* codes_dev, int64_t code_panel_ld, float* scales_dev,
+                            int64_t scale_panel_ld, void* stream) {
+    if (rht_block != 16 && rht_block != 32 && rht_block != 64 && rht_block != 128) return UFP4_ERR_INVALID_ARG;
+    if (!sign_words_host) return UFP4_ERR_INVALID_ARG;
+    if (format != UFP4_FMT_UNIFORM && format != UFP4_FMT_E2M1) return UFP4_ERR_INVALID_ARG;
+    if (rht_block == 16)
+        return quantize_impl(format, x_dev, rows, cols, ld, transpose, 1, sign_words_host[0], rounding, seed, stream_id,
+                             codes_dev, code_panel_ld, scales_dev, scale_panel_ld, stream);
+    return quantize_impl(format, x_dev, rows, cols, ld, transpose, 1, 0, rounding, seed, stream_id, codes_dev,
+                         code_panel_ld, scales_dev, scale_panel_ld, stream, 0.0f, rht_block, sign_words_host);
 }
 
 int ufp4_quant_stats(int format, float max_fpx, const void* x_dev, int64_t rows, int64_t cols, int64_t ld,

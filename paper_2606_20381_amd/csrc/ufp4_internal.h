@@ -24,6 +24,9 @@ struct QuantArgs {
     uint32_t stream;       // Philox counter word 3
     float e2m1_g;          // E2M1 top level max_fpx (2, 4 or 6) and RN(1 / max_fpx); unused by the uniform grid
     float e2m1_ginv;
+    int32_t rht_m;          // RHT block = 16 * rht_m (1, 2, 4, 8); rht_m > 1 selects the wide-RHT kernels
+    double rht_c;           // their normalisation RN64(sqrt(1 / (16 rht_m)))
+    uint32_t sign_words[8]; // their sign mask: bits 16k .. 16k + 15 of the n-bit mask in word k
 };
 
 // One quantization request, already validated.

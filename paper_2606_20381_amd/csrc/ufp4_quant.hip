@@ -115,28 +115,33 @@ __device__ __forceinline__ uint32_t e2m1_code(float v, uint32_t u16, float g) {
 // One 16-block: eight bf16 pairs in (element 2j in the low half of w[j]), packed codes + scale out.
 // ------------------------------------------------------------------------------------------------
 // The RHT of one 16-block: y' = 4y = RN32( sum_j H16[i,j] eps_j x_j ) (see the file header), or y = x.
+// The exact sums sum_j H16pm1[i,j] eps_j x_j of one 16-block in fp64 (sx: the sign-bit XOR word per pair).
+__device__ __forceinline__ void rht16_sums(const uint32_t* w, const uint32_t* sx, double* d) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t p = w[j] ^ sx[j];  // eps_j = -1: flip the bf16 sign bit
+        d[2 * j] = (double)bf16_lo(p);
+        d[2 * j + 1] = (double)bf16_hi(p);
+    }
+    // Sylvester butterfly: after the four stages d = H16pm1 * (eps x), H16pm1[i][j] = (-1)^popcount(i&j).
+#pragma unroll
+    for (int h = 1; h < 16; h <<= 1) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            if (!(i & h)) {
+                const double a = d[i], b = d[i + h];
+                d[i] = a + b;
+                d[i + h] = a - b;
+            }
+        }
+    }
+}
+
 template <bool RHT>
 __device__ __forceinline__ void rht16_unscaled(const uint32_t* w, const QuantArgs& qa, float* y) {
     if constexpr (RHT) {
         double d[16];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint32_t p = w[j] ^ qa.sign_xor[j];  // eps_j = -1: flip the bf16 sign bit
-            d[2 * j] = (double)bf16_lo(p);
-            d[2 * j + 1] = (double)bf16_hi(p);
-        }
-        // Sylvester butterfly: after the four stages d = H16pm1 * (eps x), H16pm1[i][j] = (-1)^popcount(i&j).
-#pragma unroll
-        for (int h = 1; h < 16; h <<= 1) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                if (!(i & h)) {
-                    const double a = d[i], b = d[i + h];
-                    d[i] = a + b;
-                    d[i + h] = a - b;
-                }
-            }
-        }
+        rht16_sums(w, qa.sign_xor, d);
 #pragma unroll
         for (int i = 0; i < 16; ++i) y[i] = (float)d[i];
     } else {
@@ -146,6 +151,32 @@ __device__ __forceinline__ void rht16_unscaled(const uint32_t* w, const QuantArg
             y[2 * j + 1] = bf16_hi(w[j]);
         }
     }
+}
+
+// Block-n RHT, n = 16 m with m = 2, 4 or 8 (the RHT block larger than the quantization block). The Sylvester
+// H_n is H_m (x) H_16 (outer factor on the high index bits), so after each thread's 16-point butterfly on its
+// own 16-block -- sub-block `sub` of the n-block, with its 16 bits of the n-bit sign mask -- a butterfly over
+// the m threads that hold the n-block (lanes `lane_step` apart, the partner of stage h at lane distance
+// h * lane_step) completes the exact fp64 sums; then y = RN32(RN64(sum * RN64(sqrt(1/n)))). Every lane must
+// call this (inactive blocks with zero inputs): the exchange reads the partner lanes' registers.
+__device__ __forceinline__ void rht_wide(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t sub, int lane_step,
+                                         float (&y)[16]) {
+    const uint32_t mask = qa.sign_words[sub & (uint32_t)(qa.rht_m - 1)];  // this sub-block's 16 sign bits
+    uint32_t sx[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sx[j] = (((mask >> (2 * j)) & 1u) << 15) | (((mask >> (2 * j + 1)) & 1u) << 31);
+    double d[16];
+    rht16_sums(w, sx, d);
+    for (int h = 1; h < qa.rht_m; h <<= 1) {
+        const bool upper = (sub & (uint32_t)h) != 0u;  // this thread holds the "minus" half of the stage
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const double o = __shfl_xor(d[i], h * lane_step);
+            d[i] = upper ? o - d[i] : d[i] + o;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) y[i] = (float)(d[i] * qa.rht_c);
 }
 
 // Scale and codes of one block from its (RHT-ed, unscaled) values y.
@@ -222,7 +253,7 @@ constexpr int kRI = kRR * kRB / kRT;  // blocks per thread
 
 // T = uint16_t: bf16 input (the fused kernel). T = float: fp32 input quantized without a transform, the
 // second half of the unfused form (a standalone RHT writes y in fp32, see rht_rows_kernel).
-template <int FMT, int ROUND, bool RHT, typename T = uint16_t>
+template <int FMT, int ROUND, bool RHT, typename T = uint16_t, bool WIDE = false>
 __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x, int64_t ld, int64_t qrows,
                                                          int64_t nb, QuantArgs qa, uint8_t* __restrict__ codes,
                                                          int64_t code_pld, float* __restrict__ scales,
@@ -255,7 +286,15 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x
         const int64_t r = r0 + (k >> 4), b = b0 + (k & 15);
         uint32_t lo = 0, hi = 0;
         float sc = 0.0f;
-        if (r < qrows && b < nb) {
+        if constexpr (WIDE) {
+            // the 16 threads k .. of a tile row hold its 16 consecutive blocks: the n-block partners are lanes
+            // h apart (n-blocks are aligned: b0 is a multiple of 16, nb of m)
+            const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
+                                   v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
+            float y[16];
+            rht_wide(w, qa, (uint32_t)b, 1, y);
+            if (r < qrows && b < nb) quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+        } else if (r < qrows && b < nb) {
             if constexpr (sizeof(T) == 2) {
                 const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
                                        v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
@@ -323,7 +362,7 @@ constexpr int kXG = 64 / kXC;              // column groups per workgroup
 constexpr int kXB = 256 / kXG;             // blocks per workgroup
 static_assert(kXC == 8 || kXC == 4, "columns per thread");
 
-template <int FMT, int ROUND, bool RHT, bool GROUPED>
+template <int FMT, int ROUND, bool RHT, bool GROUPED, bool WIDE = false>
 __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restrict__ x, int64_t rows,
                                                              int64_t cols, int64_t prows, int64_t ld,
                                                              int64_t red_total, TGroups grp, QuantArgs qa,
@@ -399,7 +438,15 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
             uint32_t w[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
-            quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+            if constexpr (WIDE) {
+                // consecutive blocks of the same columns are held by threads kXG apart (t = rb * kXG + cg)
+                float y[16];
+                rht_wide(w, qa, (uint32_t)gb, kXG, y);
+                quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+                __builtin_amdgcn_sched_barrier(0);  // one column at a time: bounds the live fp64 sums
+            } else {
+                quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+            }
         }
         const int64_t P = cbase >> 7, ri = cbase & 127;  // the kXC rows lie in one panel
         uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + ri * 8);
@@ -822,15 +869,15 @@ hipError_t launch_quant_stats(const StatsJob& j, hipStream_t s) {
     return j.format == kFmtE2M1 ? dispatch_stats<kFmtE2M1>(j, s) : dispatch_stats<kFmtUniform>(j, s);
 }
 
-template <int FMT, int ROUND, bool RHT, typename T = uint16_t>
+template <int FMT, int ROUND, bool RHT, typename T = uint16_t, bool WIDE = false>
 static hipError_t launch_rows_t(const QuantJob& j, hipStream_t s) {
     const int64_t nb = j.red / kBlock;
     const int64_t prows = padded_rows(j.qrows);
     if (nb == 0 || prows == 0) return hipSuccess;
     const dim3 grid((unsigned)((nb + kRB - 1) / kRB), (unsigned)(prows / kRR));
-    quant_rows_kernel<FMT, ROUND, RHT, T><<<grid, kRT, 0, s>>>(static_cast<const T*>(j.x), j.ld, j.qrows, nb, j.qa,
-                                                              static_cast<uint8_t*>(j.codes), j.code_pld, j.scales,
-                                                              j.scale_pld);
+    quant_rows_kernel<FMT, ROUND, RHT, T, WIDE><<<grid, kRT, 0, s>>>(static_cast<const T*>(j.x), j.ld, j.qrows, nb,
+                                                                    j.qa, static_cast<uint8_t*>(j.codes), j.code_pld,
+                                                                    j.scales, j.scale_pld);
     return hipGetLastError();
 }
 
@@ -867,7 +914,7 @@ hipError_t launch_rht(const RhtJob& j, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int FMT, int ROUND, bool RHT, bool GROUPED>
+template <int FMT, int ROUND, bool RHT, bool GROUPED, bool WIDE = false>
 static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
     const int64_t prows = padded_rows(j.qrows);
     const int64_t nblk = j.red / kBlock;
@@ -875,7 +922,7 @@ static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
     if (prows == 0 || gy == 0) return hipSuccess;
     const dim3 grid((unsigned)((prows + 63) / 64), (unsigned)(gy < 65535 ? gy : 65535));
     TGroups grp{j.group_off, j.group_poff, j.num_groups};
-    quant_cols_kernel<FMT, ROUND, RHT, GROUPED><<<grid, 256, 0, s>>>(
+    quant_cols_kernel<FMT, ROUND, RHT, GROUPED, WIDE><<<grid, 256, 0, s>>>(
         static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, prows, j.ld, j.red, grp, j.qa,
         static_cast<uint8_t*>(j.codes), j.code_pld, j.scales, j.scale_pld);
     return hipGetLastError();
@@ -886,6 +933,12 @@ static hipError_t dispatch_layout(const QuantJob& j, hipStream_t s) {
     if (j.input_f32) {
         if constexpr (RHT) return hipErrorInvalidValue;  // rejected by the API layer
         else return launch_rows_t<FMT, ROUND, false, float>(j, s);
+    }
+    if (j.qa.rht_m > 1) {  // RHT block 32 / 64 / 128 (plain rowwise or transposed; checked by the API layer)
+        if constexpr (!RHT) return hipErrorInvalidValue;
+        else if (j.group_off) return hipErrorInvalidValue;
+        else if (!j.transpose) return launch_rows_t<FMT, ROUND, false, uint16_t, true>(j, s);
+        else return launch_cols_t<FMT, ROUND, false, false, true>(j, s);
     }
     if (!j.transpose) return launch_rows_t<FMT, ROUND, RHT>(j, s);
     if (j.group_off) return launch_cols_t<FMT, ROUND, RHT, true>(j, s);

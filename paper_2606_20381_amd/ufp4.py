@@ -46,6 +46,8 @@ SIGNATURES = {
     "ufp4_e2m1_quantize_range": ([_P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, ctypes.c_float, _P, _I64,
                                   _P, _I64, _P], _INT),
     "ufp4_quant_stats": ([_INT, ctypes.c_float, _P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, _P, _P], _INT),
+    "ufp4_quantize_rht_block": ([_INT, _P, _I64, _I64, _I64, _INT, _INT, _P, _INT, _U64, _U32, _P, _I64, _P, _I64, _P],
+                                _INT),
     "ufp4_rht": ([_P, _I64, _I64, _I64, _U32, _P, _I64, _P], _INT),
     "ufp4_quantize_f32": ([_INT, _P, _I64, _I64, _I64, _INT, _U64, _U32, _P, _I64, _P, _I64, _P], _INT),
     "ufp4_mx_quantize": (_QUANT_ARGS, _INT),
@@ -193,6 +195,25 @@ def e2m1_quantize_range(x: torch.Tensor, max_fpx: float, *, transpose: bool = Fa
                                         q.codes.data_ptr(), q.code_panel_ld, q.scales.data_ptr(), q.scale_panel_ld,
                                         _stream())
     _check(st, "ufp4_e2m1_quantize_range")
+    return q
+
+
+def quantize_rht_block(x: torch.Tensor, fmt: int = UNIFORM, *, rht_block: int = 16, sign_mask: int = 0,
+                       transpose: bool = False, rounding: int = RTNE, seed: int = 0, stream_id: int = 0,
+                       out: QTensor | None = None) -> QTensor:
+    """RHT over n-blocks (n = rht_block, sign_mask an n-bit integer), then 1x16 quantization
+    (ufp4_quantize_rht_block)."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D row-major bf16 CUDA tensor")
+    rows, cols = x.shape
+    qrows, red = (cols, rows) if transpose else (rows, cols)
+    q = out if out is not None else empty_qtensor(qrows, red, fmt, x.device)
+    words = (ctypes.c_uint16 * 8)(*[(sign_mask >> (16 * k)) & 0xFFFF for k in range(8)])
+    st = lib().ufp4_quantize_rht_block(fmt, x.data_ptr(), rows, cols, x.stride(0), int(transpose), rht_block,
+                                       ctypes.cast(words, ctypes.c_void_p), rounding, seed & 0xFFFFFFFFFFFFFFFF,
+                                       stream_id, q.codes.data_ptr(), q.code_panel_ld, q.scales.data_ptr(),
+                                       q.scale_panel_ld, _stream())
+    _check(st, "ufp4_quantize_rht_block")
     return q
 
 

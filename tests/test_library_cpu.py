@@ -235,3 +235,15 @@ def test_unfused_validation(lib):
     assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 34, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 2   # ld % 4
     assert lib.ufp4_quantize_f32(0, FAKE + 8, 16, 32, 32, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 3
     assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 32, 0, 0, 0, FAKE, C1, FAKE, S2, None) == 2   # code panel stride
+
+
+def test_rht_block_validation(lib):
+    words = (ctypes.c_uint16 * 8)()
+    w = ctypes.cast(words, ctypes.c_void_p)
+    base = (0, FAKE, 16, 128, 128, 0)
+    tail = (0, 0, 0, FAKE, 8 * 1024, FAKE, 8 * 128, None)
+    assert lib.ufp4_quantize_rht_block(*base, 48, w, *tail) == 1         # block size
+    assert lib.ufp4_quantize_rht_block(*base, 32, None, *tail) == 1      # no sign words
+    assert lib.ufp4_quantize_rht_block(2, *base[1:], 32, w, *tail) == 1  # format
+    assert lib.ufp4_quantize_rht_block(0, FAKE, 16, 96, 96, 0, 64, w, 0, 0, 0, FAKE, 6 * 1024, FAKE, 6 * 128,
+                                       None) == 2                        # 96 % 64
