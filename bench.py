@@ -41,6 +41,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+from paper_2606_20381_amd import recipe as R  # noqa: E402
 from paper_2606_20381_amd import ufp4 as U  # noqa: E402
 from paper_2606_20381_amd import workloads as WL  # noqa: E402
 
@@ -62,6 +63,18 @@ DUAL_BYTES_PER_ELEM = 3.5  # two-operand quantizer: 2 B in, 2 x 0.75 B out
 BYTES_PER_ELEM = {"quant": QUANT_BYTES_PER_ELEM, "quant2": DUAL_BYTES_PER_ELEM, "copy": 2.0,
                   "quantmx": 2.0 + 0.75 + 1.0 / 32}
 METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
+
+
+def gemm_family(recipe: str) -> str:
+    """Which GEMM kernel a recipe runs: mxufp4 (FP6 scaled MFMA), ufp4 (fp8 MFMA per block) or e2m1 (FP4)."""
+    if recipe == "mxufp4":
+        return "mxufp4"
+    return "ufp4" if R.RECIPES[recipe].fmt == U.UNIFORM else "e2m1"
+
+
+def gemm_peak(recipe: str) -> float:
+    """Dense MFMA peak of the GEMM's operand type: fp8 (= int8) for uniform codes, fp4/fp6 otherwise."""
+    return INT8_PEAK_TOPS if gemm_family(recipe) == "ufp4" else FP4_PEAK_TFLOPS
 
 
 class Timeline:
@@ -90,21 +103,17 @@ class Timeline:
 # kernel table: label -> ("quant", elements) or ("gemm", flops)
 # ---------------------------------------------------------------------------------------------------
 
-# Per recipe: the quantizer and, for fwd_y / bwd_dx / bwd_dw, whether the RHT is applied to that GEMM's
-# operands (Table 1: UFP4 rotates all three; the E2M1 baseline only bwd_dw's).
-RECIPES = {
-    "ufp4": (U.UNIFORM, (True, True, True), "ufp4: uniform -7..7, RHT16 on all GEMMs, SR on dY"),
-    "e2m1": (U.E2M1, (False, False, True), "e2m1 baseline: E2M1 grid, RHT16 on bwd_dw only, SR on dY"),
-    "mxufp4": (U.UNIFORM, (True, True, True),
-               "mxufp4: uniform -7..7 with power-of-two 1x32 (E8M0) scales, FP6 E2M3 codes, RHT16 on all GEMMs, "
-               "SR on dY"),
-}
+# Recipes (paper_2606_20381_amd.recipe: Table 1, the Table 2 ablations, Sec. 5 Q4 and the Appendix search
+# space) and the power-of-two-scale variant.
+RECIPE_NOTES = {name: f"{name}: {r.note}" for name, r in R.RECIPES.items()}
+RECIPE_NOTES["mxufp4"] = ("mxufp4: uniform -7..7 with power-of-two 1x32 (E8M0) scales, FP6 E2M3 codes, RHT16 on all "
+                          "GEMMs, SR on dY")
 
 
 def _quantizers(recipe: str):
-    fmt, (r_y, r_dx, r_dw), _ = RECIPES[recipe]
-    fn = U.rht_quantize if fmt == U.UNIFORM else U.e2m1_quantize
-    return fmt, fn, r_y, r_dx, r_dw
+    r = R.RECIPES[recipe]
+    fn = U.rht_quantize if r.fmt == U.UNIFORM else U.e2m1_quantize
+    return r.fmt, fn, r.rht[0], r.rht[1], r.rht[2]
 
 
 def dense_step_mx(wl, tl: Timeline):
@@ -143,57 +152,41 @@ def dense_step_mx(wl, tl: Timeline):
 
 
 def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
+    """The layer step under a recipe of paper_2606_20381_amd.recipe: six quantizations (X and W through the
+    two-operand quantizer where the recipe allows it) and the three GEMMs."""
     if recipe == "mxufp4":
         return dense_step_mx(wl, tl)
     m, s = wl.sign_mask, wl.seed
-    fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
+    r = R.RECIPES[recipe]
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
     M, K = x.shape
     N = w.shape[0]
-    q = {
-        "x": U.empty_qtensor(M, K, fmt), "w": U.empty_qtensor(N, K, fmt), "dy": U.empty_qtensor(M, N, fmt),
-        "wt": U.empty_qtensor(K, N, fmt), "dyt": U.empty_qtensor(N, M, fmt), "xt": U.empty_qtensor(K, M, fmt),
-    }
-    y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
-    dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
-    dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
+    ls = R.LayerStep(M, N, K, r, dual=dual)
+    q, src = ls.q, {"x": x, "w": w, "dy": dy}
+    pairs = [(a, b) for a, b in (("x", "xt"), ("w", "wt")) if dual and R.dual_ok(r, a, b)]
+    singles = [op for op in R.OPERANDS if not any(op in p for p in pairs)]
 
-    def quant_dy(rec):
-        tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
-                                        out=q["dy"]), rec)
-        tl.run("quant_dyt_sr", lambda: Q(dy, transpose=True, rht=r_dw, sign_mask=m, rounding=U.SR, seed=s,
-                                         stream_id=1, out=q["dyt"]), rec)
+    def label(op):
+        return "quant_" + op + ("_sr" if r.rounding(op) == U.SR else "")
 
-    def step_separate(rec):
-        tl.run("quant_x", lambda: Q(x, rht=r_y, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: Q(w, rht=r_y, sign_mask=m, out=q["w"]), rec)
-        tl.run("quant_wt", lambda: Q(w, transpose=True, rht=r_dx, sign_mask=m, out=q["wt"]), rec)
-        tl.run("quant_xt", lambda: Q(x, transpose=True, rht=r_dw, sign_mask=m, out=q["xt"]), rec)
-        quant_dy(rec)
-        gemms(rec)
+    def step(rec):
+        for a, b in pairs:
+            tl.run(f"quant_{a}_{b}", lambda a=a, b=b: U.quantize_dual(
+                src[a], fmt=r.fmt, rht_rows=r.rotated(a), rht_cols=r.rotated(b), sign_mask_rows=m, sign_mask_cols=m,
+                rounding=r.rounding(a), seed=s, stream_rows=R.LAYOUT[a][3], stream_cols=R.LAYOUT[b][3],
+                out_rows=q[a], out_cols=q[b]), rec)
+        for op in singles:
+            tl.run(label(op), lambda op=op: R.quantize_operand(src[R.LAYOUT[op][0]], op, r, m, s, out=q[op]), rec)
+        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y(q["x"], q["w"], out=ls.y), rec)
+        tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx(q["dy"], q["wt"], out=ls.dx), rec)
+        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw(q["dyt"], q["xt"], out=ls.dw), rec)
 
-    def step_dual(rec):
-        tl.run("quant_x_xt", lambda: U.quantize_dual(x, fmt=fmt, rht_rows=r_y, rht_cols=r_dw, sign_mask_rows=m,
-                                                     sign_mask_cols=m, out_rows=q["x"], out_cols=q["xt"]), rec)
-        tl.run("quant_w_wt", lambda: U.quantize_dual(w, fmt=fmt, rht_rows=r_y, rht_cols=r_dx, sign_mask_rows=m,
-                                                     sign_mask_cols=m, out_rows=q["w"], out_cols=q["wt"]), rec)
-        quant_dy(rec)
-        gemms(rec)
-
-    def gemms(rec):
-        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y(q["x"], q["w"], out=y), rec)
-        tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
-        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
-
-    kern = {"quant_dy_sr": ("quant", M * N), "quant_dyt_sr": ("quant", M * N)}
-    if dual:
-        kern.update({"quant_x_xt": ("quant2", M * K), "quant_w_wt": ("quant2", N * K)})
-    else:
-        kern.update({"quant_x": ("quant", M * K), "quant_w": ("quant", N * K), "quant_wt": ("quant", N * K),
-                     "quant_xt": ("quant", M * K)})
+    elems = {"x": M * K, "w": N * K, "dy": M * N, "wt": N * K, "dyt": M * N, "xt": M * K}
+    kern = {f"quant_{a}_{b}": ("quant2", elems[a]) for a, b in pairs}
+    kern.update({label(op): ("quant", elems[op]) for op in singles})
     kern.update({"gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
                  "gemm_bwd_dw": ("gemm", 2 * M * N * K)})
-    return (step_dual if dual else step_separate), kern
+    return step, kern
 
 
 def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
@@ -425,7 +418,7 @@ def main():
     ap.add_argument("--workload", default="dense",
                     choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "quant1g-dual",
                              "copy1g", "quality-dense", "quality-moe124b"])
-    ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPES),
+    ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPE_NOTES),
                     help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
     ap.add_argument("--quant", default="dual", choices=["dual", "separate"],
                     help="dual: X and W quantized to both operands in one pass (dY, SR, uses the single-output "
@@ -469,8 +462,8 @@ def main():
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
-        if wl.grouped and args.recipe == "mxufp4":
-            print("bench.py: the power-of-two-scale recipe has no grouped (MoE) kernels in this build", file=sys.stderr)
+        if wl.grouped and args.recipe not in ("ufp4", "e2m1"):
+            print("bench.py: grouped (MoE) layers run the ufp4 and e2m1 recipes only", file=sys.stderr)
             sys.exit(2)
         step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe, args.quant == "dual")
         wname = wl.name
@@ -540,7 +533,7 @@ def main():
         else:
             tf = work / (us * 1e-6) / 1e12
             breakdown[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1),
-                                "frac_peak": round(tf / (INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS), 4)}
+                                "frac_peak": round(tf / gemm_peak(args.recipe), 4)}
             gemm_flops += work
 
     gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
@@ -551,8 +544,8 @@ def main():
         per_launch = np.mean([kern[k][1] for k in gemm_labels])
         avg_us = np.mean([tl.mean_us(k) for k in gemm_labels])
         ach = per_launch / (avg_us * 1e-6) / 1e12
-        peak = INT8_PEAK_TOPS if args.recipe == "ufp4" else FP4_PEAK_TFLOPS  # fp6 and fp4 share the peak
-        roof = {"bound": "mfma", "kernel": GEMM_KERNEL[args.recipe],
+        peak = gemm_peak(args.recipe)
+        roof = {"bound": "mfma", "kernel": GEMM_KERNEL[gemm_family(args.recipe)],
                 "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4), "traffic": measured_traffic("gemm", wname + "/" + args.recipe)}
         if args.recipe != "mxufp4":  # the per-16 fp32 scales need one VALU FMA per output and block
@@ -587,7 +580,7 @@ def main():
         "vs_baseline": None,
         "dtype": ("fp6+f32" if args.recipe == "mxufp4" else "f32") if gemm_labels else "f64+f32",
         "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
-        "config": {"workload": wname, "recipe": RECIPES[args.recipe][2],
+        "config": {"workload": wname, "recipe": RECIPE_NOTES[args.recipe],
                    "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",
                    "wall_s": round(wall, 3)},
         "roofline": roof,

@@ -617,13 +617,31 @@ def gemm_nt_mx(a_idx, a_e8m0, b_idx, b_e8m0) -> np.ndarray:
     return dequantize_mx(a_idx, a_e8m0) @ dequantize_mx(b_idx, b_e8m0).T
 
 
+_T, _F = True, False
 RECIPES = {
     # format, RHT on (fwd_y, bwd_dx, bwd_dw), SR on dY only (Table 1)
-    "ufp4": dict(fmt=UNIFORM, rht=(True, True, True)),
-    "e2m1": dict(fmt=E2M1, rht=(False, False, True)),
+    "ufp4": dict(fmt=UNIFORM, rht=(_T, _T, _T)),
+    "e2m1": dict(fmt=E2M1, rht=(_F, _F, _T)),
     # the UFP4 recipe with 1x32 power-of-two (E8M0) scales instead of 1x16 fp32 scales
-    "mxufp4": dict(fmt=UNIFORM, rht=(True, True, True), scales="e8m0x32"),
+    "mxufp4": dict(fmt=UNIFORM, rht=(_T, _T, _T), scales="e8m0x32"),
+    # Table 2: RHT scope and SR under the uniform grid
+    "ufp4-rht-none": dict(fmt=UNIFORM, rht=(_F, _F, _F)),
+    "ufp4-rht-dw": dict(fmt=UNIFORM, rht=(_F, _F, _T)),
+    "ufp4-rht-dx-dw": dict(fmt=UNIFORM, rht=(_F, _T, _T)),
+    "ufp4-rht-y-dw": dict(fmt=UNIFORM, rht=(_T, _F, _T)),
+    "ufp4-no-sr": dict(fmt=UNIFORM, rht=(_T, _T, _T), sr=()),
+    # E2M1 variants (Sec. 5 Q4; Appendix search space)
+    "e2m1-full-rht": dict(fmt=E2M1, rht=(_T, _T, _T)),
+    "e2m1-max4": dict(fmt=E2M1, rht=(_T, _T, _T), max_fpx=4.0),
+    "e2m1-max2": dict(fmt=E2M1, rht=(_T, _T, _T), max_fpx=2.0),
+    "e2m1-sr-bwd": dict(fmt=E2M1, rht=(_F, _F, _T), sr=("dy", "dyt", "xt", "wt")),
+    # RHT block (Appendix search space); the n-bit sign mask repeats the 16-bit one in every sub-block
+    "ufp4-rht32": dict(fmt=UNIFORM, rht=(_T, _T, _T), rht_block=32),
+    "ufp4-rht64": dict(fmt=UNIFORM, rht=(_T, _T, _T), rht_block=64),
+    "ufp4-rht128": dict(fmt=UNIFORM, rht=(_T, _T, _T), rht_block=128),
 }
+# Philox stream (counter word 3) of each operand when it is rounded stochastically
+SR_STREAMS = {"dy": 0, "dyt": 1, "x": 2, "w": 3, "wt": 4, "xt": 5}
 
 
 def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 0, seed: int = 0):
@@ -650,12 +668,20 @@ def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 
         out = {"y": gemm_nt_mx(*q["x"], *q["w"]), "dx": gemm_nt_mx(*q["dy"], *q["wt"]),
                "dw": gemm_nt_mx(*q["dyt"], *q["xt"])}
         return q, out
-    q["x"] = quantize_rows(operand_rowwise(x_bits), fmt, RTNE, r_y, sign_mask)
-    q["w"] = quantize_rows(operand_rowwise(w_bits), fmt, RTNE, r_y, sign_mask)
-    q["dy"] = quantize_rows(operand_rowwise(dy_bits), fmt, SR, r_dx, sign_mask, seed, 0)
-    q["wt"] = quantize_rows(operand_colwise(w_bits), fmt, RTNE, r_dx, sign_mask)
-    q["dyt"] = quantize_rows(operand_colwise(dy_bits), fmt, SR, r_dw, sign_mask, seed, 1)
-    q["xt"] = quantize_rows(operand_colwise(x_bits), fmt, RTNE, r_dw, sign_mask)
+    sr = set(cfg.get("sr", ("dy", "dyt")))
+    n = cfg.get("rht_block", BLOCK)
+    mask = sum((sign_mask & 0xFFFF) << (16 * k) for k in range(n // BLOCK))
+
+    def quant(op, a, rht):
+        rnd = SR if op in sr else RTNE
+        return quantize_rows(a, fmt, rnd, rht, mask, seed, SR_STREAMS[op], max_fpx=cfg.get("max_fpx"), rht_block=n)
+
+    q["x"] = quant("x", operand_rowwise(x_bits), r_y)
+    q["w"] = quant("w", operand_rowwise(w_bits), r_y)
+    q["dy"] = quant("dy", operand_rowwise(dy_bits), r_dx)
+    q["wt"] = quant("wt", operand_colwise(w_bits), r_dx)
+    q["dyt"] = quant("dyt", operand_colwise(dy_bits), r_dw)
+    q["xt"] = quant("xt", operand_colwise(x_bits), r_dw)
     out = {
         "y": gemm_nt(*q["x"], *q["w"], fmt),
         "dx": gemm_nt(*q["dy"], *q["wt"], fmt),

@@ -77,13 +77,6 @@ __device__ __forceinline__ uint32_t e2m1_rtne(float v) {
     return idx | ((v < 0.0f && idx != 0u) ? 8u : 0u);
 }
 
-// E2M1 level (exact) -> magnitude code.
-__device__ __forceinline__ uint32_t e2m1_code_of_level(float q) {
-    const float m = __builtin_fabsf(q);
-    const uint32_t idx = m <= 2.0f ? (uint32_t)(2.0f * m) : (m <= 4.0f ? (uint32_t)m + 2u : 7u);
-    return idx | ((q < 0.0f && idx != 0u) ? 8u : 0u);
-}
-
 // SR over adjacent signed E2M1 levels g_a <= v < g_b (spacing d = g_b - g_a in {0.5, 1, 2}):
 // q = g_b iff g_a + d * u/2^16 < v. For v >= 0 the bracket is [lower, upper) in magnitude, for v < 0 it
 // is (-upper, -lower] mirrored, so that a value on a level never moves. `g` is the top level kept (the
@@ -91,17 +84,24 @@ __device__ __forceinline__ uint32_t e2m1_code_of_level(float q) {
 __device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t u16, float g) {
     const float vc = __builtin_fminf(__builtin_fmaxf(v, -g), g);
     const float a = __builtin_fabsf(vc);
-    float ga, d;
-    if (vc >= 0.0f) {
-        d = a < 2.0f ? 0.5f : (a < 4.0f ? 1.0f : 2.0f);
-        ga = floorf(a / d) * d;  // division by a power of two: exact
-    } else {
-        d = a <= 2.0f ? 0.5f : (a <= 4.0f ? 1.0f : 2.0f);
-        ga = -(ceilf(a / d) * d);
-    }
+    const bool pos = vc >= 0.0f;
+    // The bracket family: spacing d = 0.5 below 2 (codes 0-4), 1 below 4 (codes 4-6), 2 above (codes 6-7);
+    // for v < 0 an edge value belongs to the family below it, so that a value on a level never moves.
+    const bool s1 = pos ? a < 2.0f : a <= 2.0f;
+    const bool s2 = pos ? a < 4.0f : a <= 4.0f;
+    const float d = s1 ? 0.5f : (s2 ? 1.0f : 2.0f);
+    const float inv = s1 ? 2.0f : (s2 ? 1.0f : 0.5f);  // 1/d: (a - base) * inv is exact
+    const float base = s1 ? 0.0f : (s2 ? 2.0f : 4.0f);
+    const int base_code = s1 ? 0 : (s2 ? 4 : 6);
+    // |g_a| (v >= 0) or |g_a| of the mirrored bracket (v < 0) as base + j d, whose code is base_code + j
+    const float r = (a - base) * inv;
+    const float j = pos ? floorf(r) : ceilf(r);
+    const float mag = base + j * d;
+    const float ga = pos ? mag : -mag;
     const float t = __builtin_fmaf((float)u16 * (1.0f / 65536.0f), d, ga);
-    const float q = (t < vc) ? ga + d : ga;
-    return e2m1_code_of_level(q);
+    const int code = base_code + (int)j;
+    const int q = (t < vc) ? (pos ? code + 1 : code - 1) : code;  // g_b = g_a + d: one code up or down
+    return (uint32_t)q | ((!pos && q != 0) ? 8u : 0u);
 }
 
 // RTNE needs no cut: |v| <= g (1 + 2^-23) for g = 2, 4, 6 already rounds to a level <= g.

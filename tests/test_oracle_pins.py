@@ -542,6 +542,27 @@ def test_layer_gemms_approximate_exact_products(recipe):
     assert q["wt"][0].shape == (128, 96) and q["dyt"][0].shape == (96, 64) and q["xt"][0].shape == (128, 64)
 
 
+@pytest.mark.parametrize("recipe", [r for r in O.RECIPES if r not in ("ufp4", "e2m1", "mxufp4")])
+def test_recipe_variants(recipe):
+    """Every ablation recipe still approximates the exact products, and its operands follow its switches:
+    an operand is the plain quantization with the recipe's RHT flag, grid, rounding and stream."""
+    rng = np.random.default_rng(57)
+    x = _rand_bf16_bits(rng, (128, 128))
+    w = _rand_bf16_bits(rng, (128, 128))
+    dy = _rand_bf16_bits(rng, (128, 128))
+    q, out = O.layer_gemms(x, w, dy, recipe, sign_mask=0x2F1D, seed=3)
+    xf, wf, df = (O.bf16_bits_to_f32(t).astype(np.float64) for t in (x, w, dy))
+    for key, ref in (("y", xf @ wf.T), ("dx", df @ wf), ("dw", df.T @ xf)):
+        assert O.sqnr_db(out[key], ref) > 8.0, key
+    cfg = O.RECIPES[recipe]
+    rnd = O.SR if "dyt" in cfg.get("sr", ("dy", "dyt")) else O.RTNE
+    n = cfg.get("rht_block", 16)
+    mask = sum(0x2F1D << (16 * k) for k in range(n // 16))
+    want = O.quantize_rows(O.operand_colwise(dy), cfg["fmt"], rnd, cfg["rht"][2], mask, 3, 1,
+                           max_fpx=cfg.get("max_fpx"), rht_block=n)
+    assert np.array_equal(q["dyt"][0], want[0]) and np.array_equal(q["dyt"][1], want[1])
+
+
 def test_diagnostics_closed_forms():
     a = np.array([[1.0, 2.0], [3.0, 4.0]])
     assert O.operand_projection(0.9 * a, a) == pytest.approx(0.9)
