@@ -29,6 +29,14 @@ Readings of the paper that this oracle fixes (the paper states exact mathematics
   * Codes outside the grid are clamped (|v| can exceed g by one fp32 ulp).
   * Packing: sign-magnitude nibbles for both grids -- sign in bit 3, magnitude code in bits 0-2 (for E2M1
     this is the OCP FP4 bit pattern), zero always encoded as +0; element 2j in the low nibble of byte j.
+  * Range-restricted E2M1 (Sec. 5 Q4): the levels up to max_fpx are kept and g = max_fpx.
+  * RHT blocks of 32/64/128 (Appendix search space): the exact fp64 sum times RN64(sqrt(1/n)), rounded once to
+    fp32; the 16-blocks of the result are quantized as usual.
+  * Diagnostics (Sec. 3.2): the reference of NMSE / alpha is the tensor the quantizer rounds (the fp32 RHT
+    output, or x); B_eff counts the magnitude codes of the grid, zero included.
+  * Recipes: per-GEMM RHT flags, the set of operands rounded stochastically (streams 0 and 1 for dY and dY^T,
+    2-5 for X, W, W^T, X^T), max_fpx and the RHT block, for Table 1, Table 2's ablations, Sec. 5 Q4 and the
+    Appendix search space.
 """
 
 from __future__ import annotations
