@@ -72,3 +72,22 @@ def test_quality_of_scale_formats(cfg):
         assert row["ufp4 e8m0/32"] > row["ufp4 fp32/16"] - 6.0, name
         assert row["ufp4 fp32/16"] > 10.0, name
     assert errs["ufp4 e8m0/32"] < 2.0 * errs["ufp4 fp32/16"]
+
+
+@pytest.mark.parametrize("cfg", ["dense", "moe124b"])
+def test_rht_effect_per_grid(cfg):
+    """Sec. 3.2 diagnostics from the oracle on 256 rows of X: Delta SQNR, B_eff and alpha for the uniform grid and
+    E2M1, without and with the RHT. Sanity bounds only; on these outlier-heavy activations the rotation helps the
+    uniform grid more than E2M1 (the paper's qualitative finding)."""
+    wl = WL.dense_ffn() if cfg == "dense" else WL.moe_124b_share()
+    a = _operands(wl)["X"]
+    rows = {}
+    for name, fmt in (("uniform", O.UNIFORM), ("e2m1", O.E2M1)):
+        raw = O.quant_stats(a, fmt, O.RTNE, False, wl.sign_mask)
+        rot = O.quant_stats(a, fmt, O.RTNE, True, wl.sign_mask)
+        mr, mh = O.stats_metrics(raw, fmt), O.stats_metrics(rot, fmt)
+        rows[name] = (O.delta_sqnr_db(mr["nmse"], mh["nmse"]), mr, mh)
+        print(f"\n{wl.name} X {name}: dSQNR {rows[name][0]:+.2f} dB  B_eff {mr['beff']:.3f} -> {mh['beff']:.3f}  "
+              f"alpha {mr['alpha']:.4f} -> {mh['alpha']:.4f}")
+    assert rows["uniform"][0] > 0.0
+    assert rows["uniform"][0] > rows["e2m1"][0]
