@@ -355,7 +355,7 @@ def quality_report(wl, steps: int):
 # kernel source it was measured on
 # ---------------------------------------------------------------------------------------------------
 
-TRAFFIC_SOURCES = {"gemm": "ufp4_gemm.hip", "quant": "ufp4_quant.hip"}
+TRAFFIC_SOURCES = {"gemm": "ufp4_gemm.hip", "gemm_mx": "ufp4_gemm_mx.hip", "quant": "ufp4_quant.hip"}
 
 
 def _source_digest(name: str) -> str:
@@ -547,7 +547,8 @@ def main():
         peak = gemm_peak(args.recipe)
         roof = {"bound": "mfma", "kernel": GEMM_KERNEL[gemm_family(args.recipe)],
                 "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": measured_traffic("gemm", wname + "/" + args.recipe)}
+                "frac": round(ach / peak, 4),
+                "traffic": measured_traffic("gemm_mx" if args.recipe == "mxufp4" else "gemm", wname + "/" + args.recipe)}
         if args.recipe != "mxufp4":  # the per-16 fp32 scales need one VALU FMA per output and block
             roof["attainable"] = {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
                                   "why": "one fp32 VALU FMA per output and 16-block"}
