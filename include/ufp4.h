@@ -91,7 +91,7 @@ const char *ufp4_version(void);
  *   rht        nonzero: apply the block-16 RHT with sign_mask (bits 0..15) before quantizing.
  *   rounding   UFP4_ROUND_RTNE or UFP4_ROUND_SR (seed, stream select the Philox draws; ignored for RTNE).
  *   codes_dev, code_panel_ld, scales_dev, scale_panel_ld: Q in the panel layout above.
- * Rowwise operands (transpose = 0) of more than 2097120 rows return UFP4_ERR_UNSUPPORTED.
+ * Rowwise operands (transpose = 0) of more than 2097024 rows (16383 panels) return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_rht_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
@@ -242,7 +242,7 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
  *   + i * 8; its scale at scales_dev + p * scale_panel_ld + b * 128 + i. code_panel_ld >=
  *   3072 * red/32 and scale_panel_ld >= 128 * red/32, both multiples of 16; both pointers 16-byte aligned.
  *   Padding rows of the last panel are written as zero codes and scale byte 0. Rowwise operands of more than
- *   4194240 rows return UFP4_ERR_UNSUPPORTED.
+ *   4194176 rows (32767 panels) return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_mx_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                      uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
