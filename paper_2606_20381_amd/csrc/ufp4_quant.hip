@@ -332,10 +332,10 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x
 // Transposed (and grouped-transposed): operand A = X^T, reduction along X's rows. A thread loads a
 // 16-row x kXC-column bf16 sub-tile (one load of 2 kXC bytes per row) and quantizes its kXC column blocks
 // from registers, so no LDS transposition and no barrier is needed. It then writes the kXC consecutive
-// operand rows of its block, 8 kXC contiguous bytes of codes. A workgroup of 256 threads covers 64 columns
-// x (256 / (64 / kXC)) blocks; the threads of one block read 128 contiguous bytes of each row. (Measured:
-// 4 columns per thread performs within a few percent of 8; an LDS-transposed 128 x 64 tile was 12-20%
-// slower.)
+// operand rows of its block, 8 kXC contiguous bytes of codes. A workgroup of 256 threads covers 256 columns
+// x 8 blocks; the 32 threads of one block read 512 contiguous bytes of each row. (Measured on the 1 GiB
+// tensor: 64-column workgroups, 128 bytes per row, were 17% slower, wider ones no faster; 4 columns per
+// thread performs within a few percent of 8; an LDS-transposed 128 x 64 tile was 12-20% slower.)
 // ------------------------------------------------------------------------------------------------
 // One row's kXC consecutive bf16 (kXC / 2 dwords) with a single 16- or 8-byte load.
 template <int C>
@@ -358,8 +358,10 @@ struct TGroups {
     int32_t G;
 };
 
-constexpr int kXG = 64 / kXC;              // column groups per workgroup
-constexpr int kXB = 256 / kXG;             // blocks per workgroup
+// Column groups per workgroup. With 32 a wave reads 512 contiguous bytes of each row (two blocks of 256
+// columns); the block-n RHT kernel keeps 8 so that the m blocks of an n-block lie in one wave.
+constexpr int kXG = 64 / kXC;  // block-n RHT
+constexpr int kXGD = 32;       // otherwise
 static_assert(kXC == 8 || kXC == 4, "columns per thread");
 
 template <int FMT, int ROUND, bool RHT, bool GROUPED, bool WIDE = false>
@@ -378,14 +380,15 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         }
         __syncthreads();
     }
-    const int cg = t % kXG, rb = t / kXG;
-    const int64_t cbase = (int64_t)blockIdx.x * 64 + cg * kXC;  // first operand row of the thread
+    constexpr int XG = WIDE ? kXG : kXGD, XB = 256 / XG;  // column groups, blocks per workgroup
+    const int cg = t % XG, rb = t / XG;
+    const int64_t cbase = (int64_t)blockIdx.x * (XG * kXC) + cg * kXC;  // first operand row of the thread
     if (cbase >= prows) return;
     const int ncol = cols - cbase < kXC ? (int)(cols - cbase) : kXC;  // valid columns of the thread (<= 0: none)
     const int64_t nblk = red_total / kBlock;
     constexpr int kW = kXC / 2;  // dwords per row
 
-    for (int64_t gb = (int64_t)blockIdx.y * kXB + rb; gb < nblk; gb += (int64_t)gridDim.y * kXB) {
+    for (int64_t gb = (int64_t)blockIdx.y * XB + rb; gb < nblk; gb += (int64_t)gridDim.y * XB) {
         const int64_t P0 = gb * kBlock;
         // the 16 positions of a block lie in one group (group lengths are padded to multiples of 16): rows
         // src0 .. src0 + nvalid - 1 of X, the rest padding
@@ -463,15 +466,19 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
 // Q_c = Q(X^T) along rows (transposed), each with its own RHT flag, sign mask and SR stream; bit for bit the
 // results of the two separate kernels. rows and cols are multiples of 16.
 //
-// The lanes l and l + 32 of a wave form a pair that owns a 16 x 16 sub-tile: rows 16 gb .. 16 gb + 15,
-// columns col0 .. col0 + 15; lane l loads columns col0 .. col0 + 7 of all 16 rows, lane l + 32 the other
-// eight. Each lane first quantizes its eight column blocks as the transposed kernel does. One
+// A wave covers 256 columns x 2 row groups (512 contiguous bytes of each row it reads), a workgroup four
+// waves stacked along the rows. The lanes l and l + 32 of a wave form a pair that owns a 16 x 16 sub-tile:
+// rows 16 gb .. 16 gb + 15, columns col0 .. col0 + 15; lane l loads columns col0 .. col0 + 7 of all 16 rows,
+// lane l + 32 the other eight. Each lane first quantizes its eight column blocks as the transposed kernel does. One
 // v_permlane32_swap per dword then exchanges half of the sub-tile between the two lanes (lanes 0-31 give up
 // rows 8-15 and receive columns 8-15 of rows 0-7, lanes 32-63 the converse), after which registers v[i]
 // and v[8 + i] hold row 8h + i's full 16-column block in both lanes (h = l / 32). Each lane then quantizes
 // eight row blocks and writes them as 64 contiguous bytes (eight consecutive rows of one block).
 // Zero codes and scales fill the padding rows of both operands' last panels.
 // ------------------------------------------------------------------------------------------------
+constexpr int kDC = 16;       // 16-column chunks per wave: 512 contiguous bytes of each row
+constexpr int kDB = 32 / kDC;  // 16-row groups per wave
+
 template <int FMT, int ROUND, bool RHT_R, bool RHT_C>
 __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
                                                          int64_t ld, QuantArgs qr, QuantArgs qc,
@@ -480,14 +487,16 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
                                                          uint8_t* __restrict__ codes_c, int64_t code_pld_c,
                                                          float* __restrict__ scales_c, int64_t scale_pld_c) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int h = lane >> 5, chunk = lane & 3, rbl = (lane >> 2) & 7;
-    const int64_t col0 = (int64_t)blockIdx.x * 64 + chunk * 16;  // first column of the pair's sub-tile
-    const int64_t cbase = col0 + h * 8;                          // first column of this lane
+    const int h = lane >> 5, chunk = lane % kDC, rbl = (lane & 31) / kDC;
+    const int64_t col0 = (int64_t)blockIdx.x * (16 * kDC) + chunk * 16;  // first column of the pair's sub-tile
+    const int64_t cbase = col0 + h * 8;                                  // first column of this lane
     const bool chunk_ok = col0 < cols;  // cols % 16 == 0: the 16 columns are all real or all padding
+    if (col0 >= padded_rows(cols)) return;  // past Q_c's last panel (both lanes of the pair)
     const int64_t nblk = rows / kBlock;                 // reduction blocks of Q_c = 16-row groups of X
     const int64_t ngrp = padded_rows(rows) / kBlock;    // 16-row groups including Q_r's padding rows
 
-    for (int64_t gb = (int64_t)blockIdx.y * 32 + wave * 8 + rbl; gb < ngrp; gb += (int64_t)gridDim.y * 32) {
+    for (int64_t gb = (int64_t)blockIdx.y * (4 * kDB) + wave * kDB + rbl; gb < ngrp;
+         gb += (int64_t)gridDim.y * (4 * kDB)) {
         const int64_t r0 = gb * kBlock + h * 8;  // first Q_r row of this lane
         const int64_t Pr = r0 >> 7, rir = r0 & 127;
         const int64_t bcol = col0 / kBlock;
@@ -918,9 +927,10 @@ template <int FMT, int ROUND, bool RHT, bool GROUPED, bool WIDE = false>
 static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
     const int64_t prows = padded_rows(j.qrows);
     const int64_t nblk = j.red / kBlock;
-    const int64_t gy = (nblk + kXB - 1) / kXB;
+    constexpr int XG = WIDE ? kXG : kXGD, XB = 256 / XG;
+    const int64_t gy = (nblk + XB - 1) / XB;
     if (prows == 0 || gy == 0) return hipSuccess;
-    const dim3 grid((unsigned)((prows + 63) / 64), (unsigned)(gy < 65535 ? gy : 65535));
+    const dim3 grid((unsigned)((prows + XG * kXC - 1) / (XG * kXC)), (unsigned)(gy < 65535 ? gy : 65535));
     TGroups grp{j.group_off, j.group_poff, j.num_groups};
     quant_cols_kernel<FMT, ROUND, RHT, GROUPED, WIDE><<<grid, 256, 0, s>>>(
         static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, prows, j.ld, j.red, grp, j.qa,
@@ -959,8 +969,8 @@ hipError_t launch_quantize(const QuantJob& j, hipStream_t s) {
 
 template <int FMT, int ROUND, bool RHT_R, bool RHT_C>
 static hipError_t launch_dual_t(const DualJob& j, hipStream_t s) {
-    const int64_t gx = padded_rows(j.cols) / 64;
-    const int64_t gy = (padded_rows(j.rows) / kBlock + 31) / 32;
+    const int64_t gx = (padded_rows(j.cols) + 16 * kDC - 1) / (16 * kDC);
+    const int64_t gy = (padded_rows(j.rows) / kBlock + 4 * kDB - 1) / (4 * kDB);
     if (gx == 0 || gy == 0) return hipSuccess;
     const dim3 grid((unsigned)gx, (unsigned)(gy < 65535 ? gy : 65535));
     quant_dual_kernel<FMT, ROUND, RHT_R, RHT_C><<<grid, 256, 0, s>>>(
