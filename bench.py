@@ -589,6 +589,11 @@ def main():
         "roofline": roof,
         "breakdown": breakdown,
     }
+    if wl is not None:
+        # the step re-reads the same inputs every time: tensors that fit the 256 MB last-level cache (MALL) may
+        # be served from it, so the per-kernel quantizer rates of a layer step are cache-warm figures
+        out["breakdown_note"] = ("per-kernel means inside the timed steps; the inputs are reused across steps, so "
+                                 "tensors under the 256 MB MALL may be read warm")
     if context is not None:
         out["rht_cost"] = context
     if wl is not None:
