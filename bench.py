@@ -427,8 +427,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU layout "
-              f"is described in DESIGN.md but not run", file=sys.stderr)
+        print(f"bench.py: the hot path runs on one GPU only (asked for --gpus {args.gpus}); sharding it over "
+              f"several GPUs is a design note, not an implemented mode", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
