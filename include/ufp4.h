@@ -67,7 +67,7 @@ typedef enum {
     UFP4_ERR_INVALID_ARG = 1, /* null pointer, negative size, unknown enum value                     */
     UFP4_ERR_SHAPE = 2,       /* reduction length not a multiple of 16, leading dimension too small  */
     UFP4_ERR_ALIGN = 3,       /* pointer or leading dimension not aligned as required                 */
-    UFP4_ERR_UNSUPPORTED = 5, /* valid request this build does not implement                          */
+    UFP4_ERR_UNSUPPORTED = 5, /* valid request outside the implemented limits or variants              */
     UFP4_ERR_HIP = 6          /* kernel launch failed                                                 */
 } ufp4_status;
 
