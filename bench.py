@@ -425,6 +425,9 @@ def main():
                     help="dual: X and W quantized to both operands in one pass (dY, SR, uses the single-output "
                          "kernels, measured faster); separate: six single-output quantizations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture the layer step once in a HIP graph and time its replays (reported beside "
+                         "`value`, which stays the eagerly launched step)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the hot path runs on one GPU only (asked for --gpus {args.gpus}); sharding it over "
@@ -518,6 +521,31 @@ def main():
                                 "quantizer (4 B in, 0.75 B out); same codes as the fused kernel",
                 "paper_unfused": "unfused / fused latency 1.62x (SM90), 1.41x (SM100); Sec. 5 Q5"})
 
+    graph_ctx = None
+    if args.graph and wl is not None:
+        # the library only launches kernels (no allocation, memset or synchronization), so the whole step can be
+        # captured; replays skip the per-launch host overhead
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(False)
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(False)
+        for _ in range(max(3, args.warmup)):
+            graph.replay()
+        torch.cuda.synchronize()
+        gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gs.record()
+        for _ in range(args.steps):
+            graph.replay()
+        ge.record()
+        torch.cuda.synchronize()
+        g_ms = gs.elapsed_time(ge) / args.steps
+        graph_ctx = {"ms_per_step": round(g_ms, 4), "eager_ms_per_step": round(ms_per_step, 4),
+                     "eager_over_graph": round(ms_per_step / g_ms, 3)}
+
     breakdown = {}
     gemm_flops = 0
     quant_bytes = 0.0
@@ -596,6 +624,8 @@ def main():
                                  "tensors under the 256 MB MALL may be read warm")
     if context is not None:
         out["rht_cost"] = context
+    if graph_ctx is not None:
+        out["graph_replay"] = graph_ctx
     if wl is not None:
         out["config"]["quant"] = args.quant
     if wl is not None and not args.no_cpu_baseline and not wl.grouped:
