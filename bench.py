@@ -394,16 +394,22 @@ def cpu_baseline(wl, tokens: int = 512, recipe: str = "ufp4"):
     w = WL.bf16_bits(wl.w)
     M, K = x.shape
     N = w.shape[0]
+    times = {}
     t0 = time.perf_counter()
-    O.layer_gemms(x, w, dy, recipe, sign_mask=wl.sign_mask, seed=wl.seed)
+    O.layer_gemms(x, w, dy, recipe, sign_mask=wl.sign_mask, seed=wl.seed, times=times)
     dt = time.perf_counter() - t0
     flops = 3 * 2 * M * N * K
+    quant_elems = 2 * (M * K + N * K + M * N)  # the six operands
     blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    per_op = {k: round(v, 3) for k, v in times.items()}
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas),
         "kind": "oracle",
+        "per_op_s": per_op,
+        "quantize_GB/s": round(quant_elems * QUANT_BYTES_PER_ELEM / times["quantize"] / 1e9, 3),
+        "gemm_TFLOP/s": round(float(2 * M * N * K / np.mean([times[k] for k in ("fwd_y", "bwd_dx", "bwd_dw")])) / 1e12, 4),
         "sample": (f"whole {recipe} layer step (6 quantizations + 3 fp64 GEMMs) on {tokens} of {wl.x.shape[0]} "
                    f"tokens, full {N}x{K} weight; {dt:.1f} s; elementwise numpy on 1 thread, fp64 matmul on "
                    f"{blas} BLAS threads; host {platform.processor() or platform.machine()}, "

@@ -652,15 +652,28 @@ RECIPES = {
 SR_STREAMS = {"dy": 0, "dyt": 1, "x": 2, "w": 3, "wt": 4, "xt": 5}
 
 
-def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 0, seed: int = 0):
+def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 0, seed: int = 0,
+                times: dict | None = None):
     """Quantize the six operands of one linear layer and run fwd_y, bwd_dx and bwd_dw.
 
     X [M, K], W [N, K], dY [M, N] (bf16 bit patterns). Operands:
       fwd_y : X, W rowwise along K (RTNE)              -> Y  [M, N]
       bwd_dx: dY rowwise along N (SR, stream 0),  W^T along N (RTNE)  -> dX [M, K]
       bwd_dw: dY^T along M (SR, stream 1),       X^T along M (RTNE)  -> dW [N, K]
-    Returns a dict with the quantized operands (idx, scales) and the three fp64 outputs.
+    Returns a dict with the quantized operands (idx, scales) and the three fp64 outputs. If `times` is a dict,
+    the wall-clock seconds of the six quantizations ("quantize") and of each GEMM ("fwd_y", "bwd_dx",
+    "bwd_dw") are stored in it; this is bookkeeping only.
     """
+    import time
+
+    clock = [time.perf_counter()]
+
+    def mark(name):
+        now = time.perf_counter()
+        if times is not None:
+            times[name] = now - clock[0]
+        clock[0] = now
+
     cfg = RECIPES[recipe]
     fmt = cfg["fmt"]
     r_y, r_dx, r_dw = cfg["rht"]
@@ -673,8 +686,13 @@ def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 
         q["wt"] = Q(operand_colwise(w_bits), RTNE, r_dx, sign_mask)
         q["dyt"] = Q(operand_colwise(dy_bits), SR, r_dw, sign_mask, seed, 1)
         q["xt"] = Q(operand_colwise(x_bits), RTNE, r_dw, sign_mask)
-        out = {"y": gemm_nt_mx(*q["x"], *q["w"]), "dx": gemm_nt_mx(*q["dy"], *q["wt"]),
-               "dw": gemm_nt_mx(*q["dyt"], *q["xt"])}
+        mark("quantize")
+        out = {"y": gemm_nt_mx(*q["x"], *q["w"])}
+        mark("fwd_y")
+        out["dx"] = gemm_nt_mx(*q["dy"], *q["wt"])
+        mark("bwd_dx")
+        out["dw"] = gemm_nt_mx(*q["dyt"], *q["xt"])
+        mark("bwd_dw")
         return q, out
     sr = set(cfg.get("sr", ("dy", "dyt")))
     n = cfg.get("rht_block", BLOCK)
@@ -690,11 +708,13 @@ def layer_gemms(x_bits, w_bits, dy_bits, recipe: str = "ufp4", sign_mask: int = 
     q["wt"] = quant("wt", operand_colwise(w_bits), r_dx)
     q["dyt"] = quant("dyt", operand_colwise(dy_bits), r_dw)
     q["xt"] = quant("xt", operand_colwise(x_bits), r_dw)
-    out = {
-        "y": gemm_nt(*q["x"], *q["w"], fmt),
-        "dx": gemm_nt(*q["dy"], *q["wt"], fmt),
-        "dw": gemm_nt(*q["dyt"], *q["xt"], fmt),
-    }
+    mark("quantize")
+    out = {"y": gemm_nt(*q["x"], *q["w"], fmt)}
+    mark("fwd_y")
+    out["dx"] = gemm_nt(*q["dy"], *q["wt"], fmt)
+    mark("bwd_dx")
+    out["dw"] = gemm_nt(*q["dyt"], *q["xt"], fmt)
+    mark("bwd_dw")
     return q, out
 
 
