@@ -381,9 +381,18 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         __syncthreads();
     }
     constexpr int XG = WIDE ? kXG : kXGD, XB = 256 / XG;  // column groups, blocks per workgroup
+    // Staged stores (dense RTNE): each half-wave (32 threads, one block of 256 operand rows) puts its 2 KB of
+    // codes and 1 KB of scales in its own LDS area in output order and reads them back so that every store
+    // instruction writes 512 contiguous bytes instead of 16-byte pieces of 64-byte runs. Measured on the 1 GiB
+    // tensor: 2% faster for uniform RTNE; SR, E2M1 and the grouped form would lose more to the extra registers
+    // (past 128 VGPRs) than they gain, so they store directly.
+    constexpr bool STAGE = !WIDE && !GROUPED && FMT == kFmtUniform && ROUND == kRoundRTNE && XG == 32 && kXC == 8;
+    __shared__ uint4 s_stage[STAGE ? 8 : 1][STAGE ? 192 : 1];
     const int cg = t % XG, rb = t / XG;
     const int64_t cbase = (int64_t)blockIdx.x * (XG * kXC) + cg * kXC;  // first operand row of the thread
-    if (cbase >= prows) return;
+    // Without staging a thread past the last panel has nothing to do. With it, every thread stays: its (zero)
+    // data fills its slot of the stage and stores to panels past the end are skipped.
+    if (!STAGE && cbase >= prows) return;
     const int ncol = cols - cbase < kXC ? (int)(cols - cbase) : kXC;  // valid columns of the thread (<= 0: none)
     const int64_t nblk = red_total / kBlock;
     constexpr int kW = kXC / 2;  // dwords per row
@@ -451,13 +460,43 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
                 quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
             }
         }
-        const int64_t P = cbase >> 7, ri = cbase & 127;  // the kXC rows lie in one panel
-        uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + ri * 8);
+        if constexpr (STAGE) {
+            // half-wave area: codes of operand rows 0..255 of the block (8 bytes each, uint4 0..127), then their
+            // scales (uint4 128..191); thread cg owns rows 8 cg .. 8 cg + 7
+            uint4* st = s_stage[t >> 5];
+            const int L = t & 31;
 #pragma unroll
-        for (int q = 0; q < kXC / 2; ++q) dc[q] = make_uint4(clo[2 * q], chi[2 * q], clo[2 * q + 1], chi[2 * q + 1]);
-        float4* ds = reinterpret_cast<float4*>(scales + P * scale_pld + gb * 128 + ri);
+            for (int q = 0; q < 4; ++q) st[4 * L + q] = make_uint4(clo[2 * q], chi[2 * q], clo[2 * q + 1], chi[2 * q + 1]);
+            st[128 + 2 * L] = make_uint4(__float_as_uint(sc[0]), __float_as_uint(sc[1]), __float_as_uint(sc[2]),
+                                         __float_as_uint(sc[3]));
+            st[129 + 2 * L] = make_uint4(__float_as_uint(sc[4]), __float_as_uint(sc[5]), __float_as_uint(sc[6]),
+                                         __float_as_uint(sc[7]));
+            // the half-wave reads what its own lanes wrote: LDS operations of a wave complete in order, the wait
+            // and the compiler barrier keep the reads after the writes
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            const int64_t P0 = (int64_t)blockIdx.x * 2;  // the block's two panels
 #pragma unroll
-        for (int q = 0; q < kXC / 4; ++q) ds[q] = make_float4(sc[4 * q], sc[4 * q + 1], sc[4 * q + 2], sc[4 * q + 3]);
+            for (int q = 0; q < 4; ++q) {
+                const int64_t P = P0 + (q >> 1);
+                if (P * kPanelRows < prows)
+                    *reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + (q & 1) * 512 + 16 * L) = st[32 * q + L];
+            }
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int64_t P = P0 + q;
+                if (P * kPanelRows < prows)
+                    *reinterpret_cast<uint4*>(scales + P * scale_pld + gb * 128 + 4 * L) = st[128 + 32 * q + L];
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the next iteration's writes
+        } else {
+            const int64_t P = cbase >> 7, ri = cbase & 127;  // the kXC rows lie in one panel
+            uint4* dc = reinterpret_cast<uint4*>(codes + P * code_pld + gb * 1024 + ri * 8);
+#pragma unroll
+            for (int q = 0; q < kXC / 2; ++q) dc[q] = make_uint4(clo[2 * q], chi[2 * q], clo[2 * q + 1], chi[2 * q + 1]);
+            float4* ds = reinterpret_cast<float4*>(scales + P * scale_pld + gb * 128 + ri);
+#pragma unroll
+            for (int q = 0; q < kXC / 4; ++q) ds[q] = make_float4(sc[4 * q], sc[4 * q + 1], sc[4 * q + 2], sc[4 * q + 3]);
+        }
     }
 }
 

@@ -105,9 +105,11 @@ def test_ragged_rowwise(shape):
     _check_operand(t, "dy", O.UNIFORM, True, 0x1357, 9)
 
 
-@pytest.mark.parametrize("shape", [(272, 200), (16, 8), (128, 64), (400, 136), (48, 8)])
+@pytest.mark.parametrize("shape", [(272, 200), (16, 8), (128, 64), (400, 136), (48, 8), (272, 312), (48, 520)])
 def test_ragged_transposed(shape):
-    """Tiles of 128 reduction rows x 64 columns: several tiles, ragged tails on both axes."""
+    """Ragged tails on both axes. The transposed kernel's workgroups cover 256 operand rows (two panels): 312
+    and 520 columns give 384 and 640 padded operand rows, so the last workgroup's second panel lies past the
+    end and its stores must be skipped."""
     g = torch.Generator().manual_seed(shape[0] * 1000 + shape[1])
     t = torch.randn(*shape, generator=g).bfloat16()
     _check_operand(t, "xt", O.UNIFORM, True, 0x2468, 11)
