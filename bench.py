@@ -360,11 +360,18 @@ TRAFFIC_SOURCES = {"gemm": "ufp4_gemm.hip", "gemm_mx": "ufp4_gemm_mx.hip", "quan
 
 
 def _source_digest(name: str) -> str:
+    """sha256 of a kernel source with its comments and blank space removed: a figure measured on a kernel stays
+    valid across edits of its comments, and becomes stale with any change of the code."""
     import hashlib
+    import re
 
     path = os.path.join(ROOT, "paper_2606_20381_amd", "csrc", name)
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    with open(path, encoding="utf-8") as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)  # block comments
+    text = re.sub(r"//[^\n]*", " ", text)                # line comments (the sources have no '//' in strings)
+    code = " ".join(text.split())
+    return hashlib.sha256(code.encode()).hexdigest()
 
 
 def measured_traffic(kind: str, workload: str):

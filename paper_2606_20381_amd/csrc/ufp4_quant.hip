@@ -331,8 +331,9 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x
 // ------------------------------------------------------------------------------------------------
 // Transposed (and grouped-transposed): operand A = X^T, reduction along X's rows. A thread loads a
 // 16-row x kXC-column bf16 sub-tile (one load of 2 kXC bytes per row) and quantizes its kXC column blocks
-// from registers, so no LDS transposition and no barrier is needed. It then writes the kXC consecutive
-// operand rows of its block, 8 kXC contiguous bytes of codes. A workgroup of 256 threads covers 256 columns
+// from registers, so no LDS transposition and no barrier is needed. Its results are the kXC consecutive
+// operand rows of its block, 8 kXC contiguous bytes of codes (stored directly, or through LDS so that the
+// stores of a half-wave are contiguous; see the kernel). A workgroup of 256 threads covers 256 columns
 // x 8 blocks; the 32 threads of one block read 512 contiguous bytes of each row. (Measured on the 1 GiB
 // tensor: 64-column workgroups, 128 bytes per row, were 17% slower, wider ones no faster; 4 columns per
 // thread performs within a few percent of 8; an LDS-transposed 128 x 64 tile was 12-20% slower.)

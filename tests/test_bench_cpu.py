@@ -101,3 +101,15 @@ def test_committed_traffic_entries_name_known_sources():
         assert kind in bench.TRAFFIC_SOURCES
         for name, e in entries.items():
             assert len(e["source_sha256"]) == 64 and e["bytes_per_launch"] > 0, name
+
+
+def test_source_digest_ignores_comments_only(tmp_path, monkeypatch):
+    src = tmp_path / "paper_2606_20381_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "k.hip").write_text("// header\nint f(int a) { return a + 1; }  /* block\n comment */\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    d0 = bench._source_digest("k.hip")
+    (src / "k.hip").write_text("// another header, longer\n\nint f(int a) {   return a + 1; }\n// trailing note\n")
+    assert bench._source_digest("k.hip") == d0
+    (src / "k.hip").write_text("// header\nint f(int a) { return a + 2; }\n")
+    assert bench._source_digest("k.hip") != d0
