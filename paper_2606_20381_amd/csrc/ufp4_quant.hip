@@ -66,10 +66,18 @@ __device__ __forceinline__ uint32_t offset_to_sign_magnitude(uint32_t x) {
 }
 
 // E2M1 magnitude code of the nearest level, ties to the even code (levels 0,.5,1,1.5,2,3,4,6; the bin
-// edges are the midpoints; an edge belongs to the even-coded side).
+// edges are the midpoints; an edge belongs to the even-coded side). For a >= 1 the levels are the fp32 values
+// with one fraction bit, and the code is 2 (exponent - 126) + that bit: the significand is rounded to one
+// fraction bit, ties to even, on the bit pattern. Below 1 the levels are 0, 0.5, 1: the code is RNE(2a), read
+// off 2a + 2^23. Codes past 7 (a > 6 can only come from rounding) are cut to 7. Equal to the nearest-level
+// search for every fp32 a in [0, 8] (checked exhaustively on the host).
 __device__ __forceinline__ uint32_t e2m1_mag_rtne(float a) {
-    return (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) + (uint32_t)(a >= 1.75f) +
-           (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) + (uint32_t)(a > 5.0f);
+    const uint32_t b = __float_as_uint(a);
+    const uint32_t r = b + 0x1FFFFFu + ((b >> 22) & 1u);
+    const uint32_t hi = (r >> 22) - 252u;
+    const uint32_t lo = __float_as_uint(__builtin_fmaf(a, 2.0f, 8388608.0f)) - 0x4B000000u;
+    const uint32_t idx = a >= 1.0f ? hi : lo;
+    return idx < 7u ? idx : 7u;
 }
 
 __device__ __forceinline__ uint32_t e2m1_rtne(float v) {
