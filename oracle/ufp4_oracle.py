@@ -17,11 +17,15 @@ the product package. Inputs are numpy arrays; bf16 tensors arrive as their raw u
 
 Readings of the paper that this oracle fixes (the paper states exact mathematics only):
   * RHT arithmetic: y = RN_fp32( (1/4) * sum_j H16[i,j] * eps_j * x_j ), the exact 16-term sum rounded
-    once to fp32 ("correctly rounded"). The sum is evaluated in fp64 through an explicit 16x16 matrix
-    product; this is exact when the nonzero magnitudes of a block span at most 2^41 (checked, see
+    once to fp32 precision ("correctly rounded"; gradual underflow below 2^-126, and no overflow: a rotated
+    value past FLT_MAX keeps 24 significant bits). The sum is evaluated in fp64 through an explicit 16x16
+    matrix product; this is exact when the nonzero magnitudes of a block span at most 2^41 (checked, see
     `_check_rht_domain`).
-  * Scale and reciprocal: s = RN32(amax / g), r = RN32(g / amax), v = RN32(y * r); g = 7 (uniform) or
-    6 (E2M1). A block with amax = 0 gets s = 0 and all codes 0.
+  * Scale and reciprocal: s = RN32(amax / g), r = RN24(g / amax), v = RN32(y * r); g = 7 (uniform) or
+    6 (E2M1). RN32 is IEEE binary32 rounding with gradual underflow (a tiny block gets a subnormal scale);
+    RN24 rounds to 24 significant bits without an exponent limit, which is RN32 whenever g / amax is below
+    the fp32 overflow threshold (every amax >= g / FLT_MAX) and keeps the reciprocal finite for the few
+    normal and subnormal amax below it. A block with amax = 0 gets s = 0 and all codes 0.
   * RTNE tie rule: the level whose magnitude code is even (IEEE round-half-even on the 4-bit encoding).
   * SR: q = g_b with probability (v - g_a)/(g_b - g_a) over adjacent signed levels g_a <= v < g_b,
     realised with a 16-bit uniform draw U = u / 2^16: q = g_b iff U < (v - g_a)/(g_b - g_a).
@@ -161,22 +165,23 @@ def rht_exact_f64(blocks: np.ndarray, sign_mask: int) -> np.ndarray:
     return ((blocks * eps) @ hadamard_pm1(BLOCK)) * 0.25
 
 
-FP32_MIN_NORMAL = 2.0 ** -126
+def round_to_fp32(t: np.ndarray) -> np.ndarray:
+    """Round to nearest even onto the binary32 grid, returned as fp64: gradual underflow below 2^-126 (IEEE), and
+    no overflow -- a magnitude of 2^127 or more keeps 24 significant bits beyond the fp32 range. Only the RHT of
+    inputs near the bf16 maximum reaches past it (|y| <= 4 max|x| for block 16)."""
+    t = np.asarray(t, dtype=np.float64)
+    big = np.abs(t) >= 2.0 ** 127
+    low = np.where(big, 0.0, t).astype(np.float32).astype(np.float64)
+    high = (np.where(big, t, 0.0) * 2.0 ** -64).astype(np.float32).astype(np.float64) * 2.0 ** 64
+    return np.where(big, high, low)
 
 
 def rht_blocks(blocks_f32: np.ndarray, sign_mask: int) -> np.ndarray:
-    """RHT of bf16-valued 16-blocks, correctly rounded to fp32 (one rounding of the exact result).
-
-    Domain: besides `_check_rht_domain`, every nonzero output must be a normal fp32 number (reading of the
-    paper's silence on subnormals: scaling by the RHT's factor 1/4 is then exact in any order).
-    """
+    """RHT of bf16-valued 16-blocks, correctly rounded to fp32 precision (one rounding of the exact result,
+    `round_to_fp32`: gradual underflow, no overflow). Returned as fp64 holding those values."""
     b64 = np.asarray(blocks_f32, dtype=np.float64)
     _check_rht_domain(b64)
-    y = rht_exact_f64(b64, sign_mask).astype(np.float32)
-    mag = np.abs(y)
-    if np.any((mag > 0) & (mag < FP32_MIN_NORMAL)):
-        raise ValueError("an RHT output is a subnormal fp32 number: outside the supported domain")
-    return y
+    return round_to_fp32(rht_exact_f64(b64, sign_mask))
 
 
 # RHT blocks larger than the quantization block (the RHT block-size dimension of the E2M1 reference search,
@@ -195,8 +200,8 @@ def rht_rows_n(a_f32: np.ndarray, sign_mask: int, n: int) -> np.ndarray:
 
     y = RN32( RN64( S * RN64(1/sqrt(n)) ) ) with S = sum_j H_n^pm1[i,j] eps_j x_j exact in fp64 (explicit matrix
     product, `_check_rht_domain`). For n = 16 and 64 the normalisation is a power of two and y is the correctly
-    rounded transform; for n = 32 and 128 it is the fp64-rounded product, then rounded to fp32. eps_j = -1 iff
-    bit j of the n-bit `sign_mask` is set.
+    rounded transform; for n = 32 and 128 it is the fp64-rounded product, then rounded to fp32 precision
+    (`round_to_fp32`; fp64 result). eps_j = -1 iff bit j of the n-bit `sign_mask` is set.
     """
     if n not in RHT_BLOCKS:
         raise ValueError("RHT block must be 16, 32, 64 or 128")
@@ -207,11 +212,7 @@ def rht_rows_n(a_f32: np.ndarray, sign_mask: int, n: int) -> np.ndarray:
     blocks = a.reshape(rows, red // n, n)
     _check_rht_domain(blocks)
     s = (blocks * sign_vector(sign_mask, n)) @ hadamard_pm1(n)
-    y = (s * rht_norm(n)).astype(np.float32).reshape(rows, red)
-    mag = np.abs(y)
-    if np.any((mag > 0) & (mag < FP32_MIN_NORMAL)):
-        raise ValueError("an RHT output is a subnormal fp32 number: outside the supported domain")
-    return y
+    return round_to_fp32(s * rht_norm(n)).reshape(rows, red)
 
 
 # ---------------------------------------------------------------------------------------------------
@@ -332,14 +333,37 @@ def level_values(signed_idx: np.ndarray, fmt: int) -> np.ndarray:
 # The blockwise quantizer Q_G of Sec. 2.1, with the RHT of Sec. 2.2 in front
 # ---------------------------------------------------------------------------------------------------
 
-def _check_block_domain(amax: np.ndarray, g: float) -> None:
-    """Supported blocks: finite, and either all zero or with a scale amax/g that is a normal fp32 number."""
-    nz = amax > 0
-    r = np.float32(g) / np.where(nz, amax, np.float32(1.0))
-    if not np.all(np.isfinite(amax)) or not np.all(np.isfinite(r)):
-        raise ValueError("non-finite input, or a block amax so small that g/amax overflows fp32")
-    if np.any(nz & (amax.astype(np.float64) < g * FP32_MIN_NORMAL)):
-        raise ValueError("a block amax below g * 2^-126 (subnormal scale): outside the supported domain")
+def _check_block_domain(y: np.ndarray) -> None:
+    """Inputs must be finite (Sec. 2.1 defines the quantizer for real-valued tensors)."""
+    if not np.all(np.isfinite(y)):
+        raise ValueError("non-finite input")
+
+
+def scale_rn32(amax: np.ndarray, g: float) -> np.ndarray:
+    """s = RN32(amax / g), the IEEE binary32 quotient: gradual underflow for tiny blocks, +inf past the fp32 range.
+    amax holds fp32-precision values (fp64 array) that may exceed FLT_MAX (`round_to_fp32`); below 2^127 it is
+    an fp32 number and one binary32 division gives s. Above, RN24(amax 2^-64 / g) 2^64 is that quotient with an
+    unbounded exponent, and its cast to fp32 overflows exactly where the IEEE quotient does."""
+    a = np.asarray(amax, dtype=np.float64)
+    big = a >= 2.0 ** 127
+    low = np.where(big, 0.0, a).astype(np.float32) / np.float32(g)
+    q = (np.where(big, a, 0.0) * 2.0 ** -64).astype(np.float32) / np.float32(g)
+    with np.errstate(over="ignore"):
+        high = (q.astype(np.float64) * 2.0 ** 64).astype(np.float32)
+    return np.where(big, high, low).astype(np.float32)
+
+
+def reciprocal_rn24(g: float, amax: np.ndarray) -> np.ndarray:
+    """r = g / amax rounded to nearest even at 24 significant bits, without an exponent limit (fp64 result).
+
+    amax = m * 2^e with m in [0.5, 1) (exact); RN24(g / amax) = RN24(g / m) * 2^-e, and g / m in (g, 2g] is a
+    normal fp32 quotient, so one IEEE binary32 division gives RN24(g / m). Equal to RN32(g / amax) whenever
+    that is finite. amax = 0 gives 0.
+    """
+    a = np.asarray(amax, dtype=np.float64)
+    m, e = np.frexp(a)
+    r_m = np.float32(g) / np.where(a > 0, m, 1.0).astype(np.float32)
+    return np.where(a > 0, r_m.astype(np.float64) * np.ldexp(1.0, -e), 0.0)
 
 
 def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask: int = 0,
@@ -348,7 +372,8 @@ def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_ma
     """Quantize an operand A [rows, red] along its contiguous (reduction) axis.
 
     Steps per 1x16 block B (Sec. 2.1 display; RHT of Sec. 2.2 applied first when `rht`):
-      y = RHT(x) or x;  s = RN32(amax/g);  q_i = rho(y_i / s) with y_i/s taken as RN32(y_i * RN32(g/amax)).
+      y = RHT(x) or x;  s = RN32(amax/g);  q_i = rho(y_i / s) with y_i/s taken as RN32(y_i * RN24(g/amax))
+    (`reciprocal_rn24`).
     `row_ids` are the global row numbers used in the SR counters (default 0..rows-1); `block_base` is
     added to the block number (used for operands cut out of a longer reduction axis). `max_fpx` (E2M1
     only) restricts the grid to the levels up to it, with g = max_fpx. `rht_block` > 16 rotates n-blocks
@@ -364,16 +389,15 @@ def quantize_rows(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_ma
     if rht and rht_block != BLOCK:
         y = rht_rows_n(a, sign_mask, rht_block).reshape(rows, nb, BLOCK)
     else:
-        y = rht_blocks(blocks, sign_mask) if rht else blocks.copy()
-    if not np.all(np.isfinite(y)):
-        raise ValueError("non-finite value after the transform")
-    g = np.float32(grid_gmax(fmt, max_fpx))
-    amax = np.abs(y).max(axis=-1)  # fp32
-    _check_block_domain(amax, float(g))
+        y = rht_blocks(blocks, sign_mask) if rht else blocks.astype(np.float64)
+    _check_block_domain(y)
+    g = grid_gmax(fmt, max_fpx)
+    amax = np.abs(y).max(axis=-1)  # fp32 precision, held in fp64 (the RHT output may exceed FLT_MAX)
     nz = amax > 0
-    scale = np.where(nz, amax / g, np.float32(0.0)).astype(np.float32)
-    recip = np.where(nz, g / np.where(nz, amax, np.float32(1.0)), np.float32(0.0)).astype(np.float32)
-    v = (y * recip[..., None]).astype(np.float32)  # one fp32 multiply per element
+    scale = scale_rn32(amax, g)  # IEEE binary32: subnormal when tiny
+    recip = reciprocal_rn24(g, amax)
+    # one rounding per element: the fp64 product of two 24-bit significands is exact, then RN32
+    v = (y * recip[..., None]).astype(np.float32)
     if rounding == RTNE:
         idx = round_nearest_even(v, fmt, max_fpx)
     elif rounding == SR:
@@ -526,10 +550,11 @@ def mx_scale_exponent(amax) -> np.ndarray:
     (floor(log2 amax) minus the exponent of the element format's largest binade) with the integer levels
     -7..7 read as FP6 E2M3 numbers, whose largest binade is [4, 8). Then amax / 2^E lies in [4, 8): the
     top element may exceed the top level 7 and is clamped to it (the rounding clamps, as for the fp32
-    scales). amax = 0 gives E = -127 (E8M0 byte 0); a zero block's codes are all 0 whatever the scale."""
+    scales). E8M0 holds E >= -127 only: a block with amax < 2^-125 takes the smallest scale 2^-127 (byte 0),
+    and then amax / 2^E < 4. amax = 0 gives E = -127 too; a zero block's codes are all 0 whatever the scale."""
     a = np.asarray(amax, dtype=np.float64)
     m, e = np.frexp(a)  # a = m * 2^e with 0.5 <= m < 1, so floor(log2 a) = e - 1
-    return np.where(a > 0, e - 3, -E8M0_BIAS).astype(np.int64)
+    return np.maximum(np.where(a > 0, e - 3, -E8M0_BIAS), -E8M0_BIAS).astype(np.int64)
 
 
 def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int = 0, seed: int = 0,
@@ -547,14 +572,12 @@ def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int
         raise ValueError("reduction length must be a multiple of 32")
     n16, n32 = red // BLOCK, red // MX_BLOCK
     y16 = a.reshape(rows, n16, BLOCK)
-    y16 = rht_blocks(y16, sign_mask) if rht else y16.copy()
-    if not np.all(np.isfinite(y16)):
-        raise ValueError("non-finite value after the transform")
+    y16 = rht_blocks(y16, sign_mask) if rht else y16.astype(np.float64)
+    _check_block_domain(y16)
     y = y16.reshape(rows, n32, MX_BLOCK)
     amax = np.abs(y).max(axis=-1)
-    _check_block_domain(amax, 7.0)
     E = mx_scale_exponent(amax)
-    v = y.astype(np.float64) * np.ldexp(1.0, -E)[..., None]  # a power of two: exact
+    v = y * np.ldexp(1.0, -E)[..., None]  # a power of two: exact
     if rounding == RTNE:
         idx = round_nearest_even(v, UNIFORM)
     elif rounding == SR:
@@ -760,8 +783,8 @@ def quant_stats(a_f32: np.ndarray, fmt: int, rounding: int, rht: bool, sign_mask
     a = np.asarray(a_f32, dtype=np.float32)
     rows, red = a.shape
     blocks = a.reshape(rows, red // BLOCK, BLOCK)
-    y = rht_blocks(blocks, sign_mask) if rht else blocks
-    ref = np.asarray(y, dtype=np.float64).reshape(rows, red)
+    y = rht_blocks(blocks, sign_mask) if rht else blocks.astype(np.float64)
+    ref = y.reshape(rows, red)
     idx, sc = quantize_rows(a, fmt, rounding, rht, sign_mask, seed, stream, max_fpx=max_fpx)
     q = dequantize(idx, sc, fmt)
     return {

@@ -26,6 +26,10 @@ def _read_table(name):
     return rows
 
 
+def _bf16_blocks(vals):
+    return O.bf16_bits_to_f32(O.f32_to_bf16_bits(np.asarray(vals, dtype=np.float64).astype(np.float32)))
+
+
 def _rand_bf16_bits(rng, shape, scale=1.0):
     x = (rng.standard_normal(shape) * scale).astype(np.float32)
     return O.f32_to_bf16_bits(x)
@@ -117,23 +121,22 @@ def _round_fraction_f32(q: Fraction) -> np.float32:
 
 def test_rht_correctly_rounded_bruteforce():
     """y_i = RN32(1/4 sum_j H[i,j] eps_j x_j) against exact rational arithmetic, including blocks whose
-    magnitudes span up to 2^41 and subnormal-range results."""
+    magnitudes span up to 2^41 and results in the subnormal range (gradual underflow)."""
     rng = np.random.default_rng(11)
     blocks = []
-    for t in range(300):
+    for t in range(400):
         mant = rng.integers(-255, 256, size=16)
         spread = int(rng.integers(0, 42))
-        base = int(rng.integers(-120, 100))
+        # every fourth block lies at the bottom of the bf16 range, where sums / 4 fall below 2^-126
+        base = int(rng.integers(-133, -110)) if t % 4 == 0 else int(rng.integers(-120, 100))
         expo = base - rng.integers(0, spread + 1, size=16)
         vals = np.array([float(Fraction(int(mm)) * Fraction(2) ** int(ee - 7)) for mm, ee in zip(mant, expo)])
         if t % 7 == 0:
             vals[rng.integers(0, 16, size=5)] = 0.0
         blocks.append(O.bf16_bits_to_f32(O.f32_to_bf16_bits(vals.astype(np.float32))))
     blocks = np.array(blocks)
-    # keep only blocks inside the supported domain after the bf16 rounding (sum exact in fp64, no subnormal
-    # fp32 output)
+    # keep only blocks whose sum is exact in fp64 (the RHT domain of the oracle: nonzero magnitudes within 2^41)
     mask = 0x9E37
-    got = None
     keep = []
     for b in blocks:
         try:
@@ -142,8 +145,10 @@ def test_rht_correctly_rounded_bruteforce():
         except ValueError:
             pass
     keep = np.array(keep)
-    assert len(keep) > 250
+    assert len(keep) > 300
     got = O.rht_blocks(keep, mask)
+    mag = np.abs(got)
+    assert np.count_nonzero((mag > 0) & (mag < np.float32(2.0 ** -126))) > 200  # subnormal outputs are covered
     h = O.hadamard_pm1(16)
     eps = O.sign_vector(mask)
     for bi, b in enumerate(keep):
@@ -151,7 +156,25 @@ def test_rht_correctly_rounded_bruteforce():
         for i in range(16):
             s = sum(Fraction(int(h[i, j] * eps[j])) * xs[j] for j in range(16)) / 4
             want = _round_fraction_f32(s)
-            assert got[bi, i].view(np.uint32) == want.view(np.uint32), (bi, i)
+            assert np.float32(got[bi, i]).view(np.uint32) == want.view(np.uint32), (bi, i)
+
+
+def test_rht_outputs_past_the_fp32_range_keep_24_bits():
+    """Inputs near the bf16 maximum rotate to values beyond FLT_MAX: y is the exact value rounded to 24
+    significant bits (no overflow), checked with exact rationals."""
+    big = (2.0 - 2.0 ** -7) * 2.0 ** 127  # the largest bf16
+    b = _bf16_blocks([[big, big, -big, big, big / 3, 0.0, big / 5, big] + [big / 7] * 8,
+                      [big] * 16, [2.0 ** 125, 2.0 ** 126, -(2.0 ** 124)] + [0.0] * 13])
+    mask = 0x0F0F
+    got = O.rht_blocks(b, mask)
+    assert np.any(np.abs(got) > float(np.finfo(np.float32).max))
+    h, eps = O.hadamard_pm1(16), O.sign_vector(mask)
+    for r in range(len(b)):
+        xs = [Fraction(float(v)) for v in b[r]]
+        for i in range(16):
+            s = sum(Fraction(int(h[i, j] * eps[j])) * xs[j] for j in range(16)) / 4
+            want = _round_fraction_sig(abs(s), 24) * (1 if s > 0 else -1) if s != 0 else Fraction(0)
+            assert Fraction(float(got[r, i])) == want, (r, i)
 
 
 def test_rht_domain_is_enforced():
@@ -164,22 +187,170 @@ def test_rht_domain_is_enforced():
     O.rht_blocks(b.astype(np.float32), 0)
 
 
-def test_subnormal_outputs_and_scales_are_outside_the_domain():
-    # RHT output 2^-127 (x0 / 4): subnormal fp32 -> rejected; 2^-126 is the smallest accepted magnitude
-    b = np.zeros((1, 16), dtype=np.float32)
-    b[0, 0] = np.float32(2.0 ** -125)
-    with pytest.raises(ValueError):
-        O.rht_blocks(b, 0)
-    b[0, 0] = np.float32(2.0 ** -124)
-    assert np.all(np.abs(O.rht_blocks(b, 0)) == np.float32(2.0 ** -126))
-    # block scale amax / g must be normal: amax = 2^-124 < 7 * 2^-126 is rejected, 2^-123 accepted (g = 7)
-    a = np.zeros((1, 16), dtype=np.float32)
-    a[0, 3] = np.float32(2.0 ** -124)
-    with pytest.raises(ValueError):
-        O.quantize_rows(a, O.UNIFORM, O.RTNE, False)
-    a[0, 3] = np.float32(2.0 ** -123)
-    idx, sc = O.quantize_rows(a, O.UNIFORM, O.RTNE, False)
-    assert idx[0, 3] == 7 and sc[0, 0] == np.float32(2.0 ** -123 / 7)
+def _round_fraction_sig(q: Fraction, bits: int) -> Fraction:
+    """Round-half-even of a positive rational to `bits` significant bits, with no exponent limit."""
+    assert q > 0
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    while Fraction(2) ** e > q:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= q:
+        e += 1
+    step = Fraction(2) ** (e - bits + 1)
+    n = floor(q / step)
+    rem = q / step - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return n * step
+
+
+def _round_fp32_no_overflow(q: Fraction) -> Fraction:
+    """fp32 rounding with gradual underflow below 2^-126 and 24 significant bits (no overflow) from 2^127 up."""
+    if q == 0:
+        return Fraction(0)
+    if abs(q) >= Fraction(2) ** 127:
+        return _round_fraction_sig(abs(q), 24) * (1 if q > 0 else -1)
+    return Fraction(float(_round_fraction_f32(q)))
+
+
+def _exact_quant_block(x, fmt, rounding, rht, mask, u16):
+    """One 16-block quantized with exact rationals, step by step as Sec. 2.1 / 2.2 state it: y = RN32 of the
+    exact RHT (or x), amax, s = RN32(amax / g) with gradual underflow, r = g / amax to 24 significant bits,
+    v = RN32(y r), then the nearest level (ties to the even magnitude code) or the SR rule with the draws.
+    Returns (signed level indices, scale as fp32)."""
+    xs = [Fraction(float(v)) for v in x]
+    if rht:
+        h = O.hadamard_pm1(16)
+        eps = O.sign_vector(mask)
+        ys = [_round_fp32_no_overflow(sum(Fraction(int(h[i, j] * eps[j])) * xs[j] for j in range(16)) / 4)
+              for i in range(16)]
+    else:
+        ys = xs
+    g = Fraction(int(O.G_MAX[fmt]))
+    amax = max(abs(t) for t in ys)
+    if amax == 0:
+        return [0] * 16, np.float32(0.0)
+    q = amax / g
+    s = np.float32(np.inf) if _round_fraction_sig(q, 24) >= Fraction(2) ** 128 else _round_fraction_f32(q)
+    r = _round_fraction_sig(g / amax, 24)
+    mags = [Fraction(float(m)) for m in O.GRID_MAGNITUDES[fmt]]
+    levels = sorted({-m for m in mags} | set(mags))
+    out = []
+    for i, t in enumerate(ys):
+        v = Fraction(float(_round_fraction_f32(t * r)))
+        if rounding == O.RTNE:
+            d = [abs(abs(v) - m) for m in mags]
+            cand = [k for k, dd in enumerate(d) if dd == min(d)]
+            k = [c for c in cand if c % 2 == 0][0] if len(cand) > 1 else cand[0]
+            out.append(-k if v < 0 else k)
+        else:
+            vc = min(max(v, levels[0]), levels[-1])
+            ia = max(k for k, L in enumerate(levels) if L <= vc)
+            ga = levels[ia]
+            if ia + 1 < len(levels) and Fraction(int(u16[i]), 65536) < (vc - ga) / (levels[ia + 1] - ga):
+                ga = levels[ia + 1]
+            k = mags.index(abs(ga))
+            out.append(-k if ga < 0 else k)
+    return out, s
+
+
+def _edge_blocks():
+    """Blocks at both ends of the fp32 range (bf16 values), each a case where plain fp32 arithmetic would break:
+    amax at g * 2^-126 and one bf16 step either side (scale normal / subnormal), amax below g / FLT_MAX
+    (g / amax beyond the fp32 range), subnormal bf16 inputs, RHT outputs in the subnormal range, a normal
+    block for reference, and blocks near the bf16 maximum (RHT outputs beyond FLT_MAX)."""
+    rng = np.random.default_rng(97)
+    t = 2.0 ** -126
+    ulp = 2.0 ** -131  # bf16 step at 7 * 2^-126 = 1.75 * 2^-124
+    rows = []
+    for g in (7.0, 6.0):
+        for a in (g * t - ulp, g * t, g * t + ulp):
+            rows.append([a, -a / 3, a / 5, 0.0, -a, a / 7] + list(rng.uniform(-a, a, 10)))
+    for a in (1.5e-38, 2.0e-38, 1.0e-38, 1.2e-38):  # 7 / FLT_MAX = 2.06e-38: g / amax overflows fp32
+        rows.append([a, -a, a / 2, 0.0] + list(rng.uniform(-a, a, 12)))
+    for a in (9.2e-41, 3e-40, 1e-39, 5e-39):  # subnormal bf16 inputs (and subnormal RHT outputs)
+        rows.append(list(rng.uniform(-a, a, 16)))
+    rows.append([2.0 ** -124, 2.0 ** -125, -(2.0 ** -127), 2.0 ** -130] + [0.0] * 12)  # sums / 4 below 2^-126
+    rows.append([2.0 ** -100, 2.0 ** -127, 2.0 ** -133] + list(rng.uniform(-1e-36, 1e-36, 13)))
+    rows.append(list(rng.standard_normal(16)))
+    big = (2.0 - 2.0 ** -7) * 2.0 ** 127  # the largest bf16: RHT outputs and E2M1 scales past FLT_MAX
+    rows.append([big] * 16)
+    rows.append([big, -big, big / 2, 0.0] + list(rng.uniform(-big, big, 12)))
+    rows.append(list(rng.uniform(-1, 1, 16) * 2.0 ** 120))
+    return _bf16_blocks(rows)
+
+
+@pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
+@pytest.mark.parametrize("rounding", [O.RTNE, O.SR])
+@pytest.mark.parametrize("rht", [False, True])
+def test_quantizer_full_domain_against_exact_rationals(fmt, rounding, rht):
+    """The whole finite bf16 range: tiny blocks (subnormal scales and RHT outputs, g / amax past FLT_MAX) and
+    random blocks from 2^-133 to 2^120, every code and scale against `_exact_quant_block`."""
+    rng = np.random.default_rng(101 + 4 * fmt + 2 * rounding + rht)
+    rand = []
+    for _ in range(60):
+        base = int(rng.integers(-133, 121))
+        e = base - rng.integers(0, 30, size=16)
+        m = rng.integers(-255, 256, size=16)
+        rand.append([float(Fraction(int(mm)) * Fraction(2) ** int(ee - 7)) for mm, ee in zip(m, e)])
+    a = np.concatenate([_edge_blocks(), _bf16_blocks(rand)])
+    a = a[np.isfinite(a).all(axis=1)]
+    mask, seed = 0x6A09, 12345
+    idx, sc = O.quantize_rows(a, fmt, rounding, rht, mask, seed=seed, stream=3)
+    u = O.sr_draws(np.zeros((len(a), 1), np.int64), np.arange(len(a))[:, None], seed, 3)[:, 0]
+    for r in range(len(a)):
+        want, s = _exact_quant_block(a[r], fmt, rounding, rht, mask, u[r])
+        assert list(idx[r]) == want, r
+        assert sc[r, 0].view(np.uint32) == s.view(np.uint32), r
+    assert np.any((sc > 0) & (sc < np.float32(2.0 ** -126)))  # subnormal scales occur
+
+
+def test_reciprocal_is_rn24_and_equals_fp32_division_where_finite():
+    rng = np.random.default_rng(103)
+    amax = np.concatenate([np.abs(rng.standard_normal(2000) * 10.0 ** rng.integers(-37, 38, 2000)),
+                           [2.0 ** -149, 1e-45, 1e-40, 1.5e-38, 2.0e-38, 2.06e-38, 2.1e-38, 7 * 2.0 ** -126]])
+    amax = amax.astype(np.float32)
+    amax = amax[amax > 0]
+    for g in (7.0, 6.0, 4.0, 2.0):
+        r = O.reciprocal_rn24(g, amax)
+        for a, got in zip(amax.tolist(), r.tolist()):
+            assert Fraction(got) == _round_fraction_sig(Fraction(int(g)) / Fraction(a), 24), (g, a)
+        with np.errstate(over="ignore"):
+            f32 = np.float32(g) / amax
+        fin = np.isfinite(f32)
+        assert np.array_equal(r[fin], f32[fin].astype(np.float64))
+        assert not fin.all()  # the range contains amax below g / FLT_MAX
+
+
+def test_tiny_block_codes_match_the_normal_block_they_scale():
+    """RN commutes with powers of two: away from subnormal y and scale, a block scaled by 2^k has the same
+    codes; scaling a normal block down to amax = 1.5e-38 (g / amax beyond FLT_MAX) keeps its codes."""
+    rng = np.random.default_rng(107)
+    base = _bf16_blocks(rng.standard_normal((8, 16)) * 4)
+    for k in (-100, -120, -124):
+        small = (base.astype(np.float64) * 2.0 ** k).astype(np.float32)
+        assert np.array_equal(small.astype(np.float64) * 2.0 ** -k, base.astype(np.float64))  # exact scaling
+        for fmt in (O.UNIFORM, O.E2M1):
+            i0, s0 = O.quantize_rows(base, fmt, O.RTNE, False)
+            i1, s1 = O.quantize_rows(small, fmt, O.RTNE, False)
+            assert np.array_equal(i0, i1), (k, fmt)
+            if k > -120:
+                assert np.array_equal(s1.astype(np.float64), s0.astype(np.float64) * 2.0 ** k)
+
+
+def test_mx_tiny_blocks_take_the_smallest_scale():
+    """E8M0 stops at 2^-127: a block with amax < 2^-125 keeps byte 0 and its codes are RTNE(y * 2^127)."""
+    rng = np.random.default_rng(109)
+    a = _bf16_blocks(rng.uniform(-1, 1, (4, 32)) * np.array([[1e-38], [3e-39], [1e-40], [2.0 ** -124]]))
+    idx, e8 = O.quantize_rows_mx(a, O.RTNE, False)
+    assert np.all(e8[:3] == 0)
+    for r in range(3):
+        for i in range(32):
+            v = Fraction(float(a[r, i])) * Fraction(2) ** 127
+            lo = floor(v)
+            k = lo + 1 if v - lo > Fraction(1, 2) or (v - lo == Fraction(1, 2) and lo % 2) else lo
+            assert idx[r, i] == max(-7, min(7, k))
+    codes, e = _mx_reference_block(a[3])
+    assert list(idx[3]) == codes and e8[3, 0] == e
 
 
 # ------------------------------------------------------------------------------------------------
