@@ -35,10 +35,13 @@
  *      write rows past `rows` in the last panel as zero codes and zero scales. Panel strides above 2^29
  *      bytes (codes) or 2^27 floats (scales) return UFP4_ERR_UNSUPPORTED.
  *  - Quantizer arithmetic, per 16-block x (bf16):
- *      y_i  = RN_fp32( 1/4 * sum_j H16[i,j] * eps_j * x_j )  with the exact sum (rht != 0), else y = x;
- *             H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
- *             Exact when the nonzero |x_j| of a block span at most 2^41.
- *      amax = max |y_i|;  s = RN(amax/g);  r = RN(g/amax);  v_i = RN(y_i * r);  amax == 0 -> s = 0, codes 0.
+ *      y_i  = the exact 1/4 * sum_j H16[i,j] * eps_j * x_j  rounded once to fp32 precision (rht != 0), else
+ *             y = x; H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
+ *             Rounding: to nearest even, with gradual underflow below 2^-126 and no overflow (an output past
+ *             FLT_MAX keeps 24 significant bits). Exact when the nonzero |x_j| of a block span at most 2^41.
+ *      amax = max |y_i|;  s = RN32(amax/g) (IEEE: subnormal for a tiny block, +inf past the fp32 range);
+ *      r = g/amax rounded to 24 significant bits without an exponent limit (= RN32(g/amax) whenever that is
+ *      finite);  v_i = RN32(y_i * r);  amax == 0 -> s = 0, codes 0.
  *      RTNE (Sec. 2.1): nearest level, ties to the level with the even magnitude code.
  *      SR   (Sec. 2.1): adjacent signed levels g_a <= v < g_b; q = g_b iff u/2^16 < (v - g_a)/(g_b - g_a),
  *             u a 16-bit Philox4x32-10 draw: key = (seed lo32, seed hi32), counter = (block, row, half,
@@ -164,7 +167,7 @@ int ufp4_quant_stats(int format, float max_fpx, const void *x_dev, int64_t rows,
  * ufp4_rht_quantize(x, rht = 1) (rowwise) bit for bit.
  *
  * ufp4_rht -- y = RN_fp32( x S_16 H_16 ) for every 16-block along the rows of x (Sec. 2.2; the arithmetic
- *   of the quantizer's transform, see the conventions above). x_dev bf16 [rows, cols] (cols % 16 == 0, ld as
+ *   of the quantizer's transform, see the conventions above; +-inf past FLT_MAX). x_dev bf16 [rows, cols] (cols % 16 == 0, ld as
  *   for the quantizers); y_dev fp32 [rows, cols] with leading dimension ldy (ldy >= cols, ldy % 4 == 0,
  *   16-byte aligned). sign_mask as for ufp4_rht_quantize.
  */
@@ -175,7 +178,7 @@ int ufp4_rht(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t
  * ufp4_quantize_f32 -- rowwise quantization of an fp32 tensor without a transform (the second half of the
  *   unfused form): operand A = X [rows, cols] along cols, the arithmetic of ufp4_rht_quantize with rht = 0
  *   applied to fp32 values. format UFP4_FMT_UNIFORM or UFP4_FMT_E2M1 (full grid); ld >= cols, ld % 4 == 0,
- *   x_dev 16-byte aligned. Inputs must be finite with every nonzero block amax at least g * 2^-126.
+ *   x_dev 16-byte aligned. Inputs must be finite.
  *   Remaining arguments as ufp4_rht_quantize.
  */
 int ufp4_quantize_f32(int format, const float *x_dev, int64_t rows, int64_t cols, int64_t ld, int rounding,
@@ -229,8 +232,9 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
  * 1x32 block that gfx950's scaled matrix-core instruction applies itself.
  *
  * ufp4_mx_quantize -- fused RHT + quantization with power-of-two scales. Per 1x32 block along the reduction
- *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = floor(log2 amax |y|) - 2 (the OCP
- *   Microscaling shared-exponent rule, the levels read as FP6 E2M3 numbers); v = y * 2^-E (exact, |v| < 8);
+ *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = max(floor(log2 amax |y|) - 2, -127)
+ *   (the OCP Microscaling shared-exponent rule, the levels read as FP6 E2M3 numbers; E8M0 stops at 2^-127);
+ *   v = RN32(y * 2^-E) (|v| < 8);
  *   codes -7..7 by RTNE or SR (same rules and Philox draws, the counters numbering 16-blocks), |v| > 7
  *   clamped to the top level. Arguments as ufp4_rht_quantize, except:
  *     red % 32 == 0 (cols when transpose = 0, rows when transpose = 1);

@@ -561,10 +561,10 @@ def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int
                      stream: int = 0, row_ids=None):
     """Quantize an operand A [rows, red] (red % 32 == 0) along its contiguous axis with power-of-two scales.
 
-    Per 1x32 block: y = RHT16(x) on each half (or x); E = mx_scale_exponent(amax |y|); v = y * 2^-E (exact,
-    |v| < 8); codes -7..7 by RTNE or SR with the draws of the two 16-blocks it contains (the SR counters
-    number 16-blocks, as in `quantize_rows`), |v| > 7 clamped to the top level. Returns (signed codes int64
-    [rows, red], E8M0 bytes uint8 [rows, red/32]).
+    Per 1x32 block: y = RHT16(x) on each half (or x); E = mx_scale_exponent(amax |y|); v = RN32(y * 2^-E) (|v| <
+    8; a power of two, so exact unless below 2^-126); codes -7..7 by RTNE or SR with the draws of the two
+    16-blocks it contains (the SR counters number 16-blocks, as in `quantize_rows`), |v| > 7 clamped to the top
+    level. Returns (signed codes int64 [rows, red], E8M0 bytes uint8 [rows, red/32]).
     """
     a = np.asarray(a_f32, dtype=np.float32)
     rows, red = a.shape
@@ -577,7 +577,7 @@ def quantize_rows_mx(a_f32: np.ndarray, rounding: int, rht: bool, sign_mask: int
     y = y16.reshape(rows, n32, MX_BLOCK)
     amax = np.abs(y).max(axis=-1)
     E = mx_scale_exponent(amax)
-    v = y * np.ldexp(1.0, -E)[..., None]  # a power of two: exact
+    v = (y * np.ldexp(1.0, -E)[..., None]).astype(np.float32)  # RN32: exact but below 2^-126 (as v of the 1x16 path)
     if rounding == RTNE:
         idx = round_nearest_even(v, UNIFORM)
     elif rounding == SR:

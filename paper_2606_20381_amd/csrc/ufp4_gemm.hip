@@ -1,32 +1,20 @@
-// Block-scaled 4-bit NT GEMM on CDNA4 int8 MFMA (Sec. 2.2: Y_hat = Q(XH') Q(WH')^T; the three training
+// Block-scaled 4-bit NT GEMM on CDNA4 matrix cores (Sec. 2.2: Y_hat = Q(XH') Q(WH')^T; the three training
 // GEMMs fwd_y, bwd_dx, bwd_dw all take this form once both operands are stored reduction-contiguous).
 //
 //   C[i, j] = sum_b  sA[i,b] * sB[j,b] * D_b[i, j],   D_b[i, j] = sum_{k in block b} A[i,k] * B[j,k]
 //
-// Every 16-element K-block has its own fp32 scale on both sides, so D_b is formed per block by one
-// v_mfma_i32_32x32x16_i8 (K = 16 exactly) and folded into an fp32 accumulator by the VALU:
-// acc += float(D_b) * (sA * sB). Codes are expanded to int8 through byte-permute tables: uniform codes to k,
-// E2M1 codes to 2 * level (exact in int8; the factor 4 on D_b is undone at the end).
-//
-// Work split: 128 x 128 output tile per workgroup, 4 waves in 2 x 2, each wave 64 x 64 = 2 x 2 MFMA
-// tiles. K is staged through LDS 8 blocks (128 codes) at a time, double-buffered: the next stage's
-// global loads are in flight while the current one is computed. LDS holds codes as planes
-// [block][half][row] (one dword = 8 codes per row and half), so the MFMA operand reads of a half-wave
-// are 32 consecutive dwords; scales as planes [block][row].
+// Every 16-element K-block has its own fp32 scale on both sides, so D_b is formed per block by one MFMA with
+// K = 16 (the integer codes made exact fp8 numbers; E2M1 codes as FP4) and folded into an fp32 accumulator
+// with the scale product of the block: acc += D_b * (sA * sB). The design is described at gemm_f32_kernel.
 //
 // Grouped (MoE) problems: ragged M (fwd_y, bwd_dx: token rows split into groups) resolves its group
 // from the tile index with a wave-wide prefix sum over the group sizes; ragged K (bwd_dw: the reduction
 // runs over each group's padded token range) takes the group from the grid's z index.
 
-#include <cstdlib>
-#include <cstring>
-
 #include "ufp4_device.h"
 #include "ufp4_internal.h"
 
 namespace ufp4 {
-
-typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128;
 static_assert(BM == kPanelRows && BN == kPanelRows, "a dense tile is one operand panel");
@@ -40,62 +28,6 @@ __device__ __forceinline__ int64_t scale_off(int row0, int row, int64_t kb, int6
     const int r = row0 + row;
     return (int64_t)(r / kPanelRows) * pld + kb * kPanelBlockScales + (r % kPanelRows);
 }
-constexpr int SKB = 8;         // K-blocks per LDS stage
-constexpr int CPL = BM + 2;    // dwords per code plane (row stride offset of 2 banks between planes)
-constexpr int SPL = BM + 4;    // floats per scale plane
-static_assert(BM == BN, "one plane stride for both operands");
-
-struct alignas(16) GemmSmem {
-    uint32_t a[2][SKB * 2 * CPL];
-    uint32_t b[2][SKB * 2 * CPL];
-    float as[2][SKB * SPL];
-    float bs[2][SKB * SPL];
-    int32_t grp[2];
-};
-
-// Per-byte sign masks: byte i of the result is 0xFF when bit 7 of byte i of x is set, else 0x00. The byte
-// permute's selectors 8..11 replicate bits 15, 31, 47 and 63 of {x << 8, x}, i.e. bits 15, 31, 7, 23 of x.
-__device__ __forceinline__ uint32_t byte_sign_mask(uint32_t x) {
-    return __builtin_amdgcn_perm(x << 8, x, 0x090B080Au);
-}
-
-// 4 uniform sign-magnitude nibbles, one per byte (low 4 bits) -> 4 int8 holding the code k.
-__device__ __forceinline__ uint32_t uniform_bytes_to_i8(uint32_t nib) {
-    const uint32_t mag = nib & 0x07070707u;
-    const uint32_t neg = __builtin_amdgcn_perm(0xF9FAFBFCu, 0xFDFEFF00u, mag);  // 0 -1 -2 .. -7
-    const uint32_t m = byte_sign_mask(nib << 4);
-    return (neg & m) | (mag & ~m);
-}
-
-// 8 packed uniform codes (one dword) -> 8 int8 lanes (even codes first, then odd).
-__device__ __forceinline__ long expand_uniform(uint32_t d) {
-    const uint32_t lo = uniform_bytes_to_i8(d & 0x0F0F0F0Fu);
-    const uint32_t hi = uniform_bytes_to_i8((d >> 4) & 0x0F0F0F0Fu);
-    return (long)(((uint64_t)hi << 32) | lo);
-}
-
-// 4 E2M1 nibbles, one per byte (low 4 bits) -> 4 int8 holding 2 * level.
-__device__ __forceinline__ uint32_t e2m1_bytes_to_i8x2(uint32_t nib) {
-    const uint32_t sel = nib & 0x07070707u;
-    // magnitudes * 2: 0 1 2 3 4 6 8 12 and their negations
-    const uint32_t pos = __builtin_amdgcn_perm(0x0C080604u, 0x03020100u, sel);
-    const uint32_t neg = __builtin_amdgcn_perm(0xF4F8FAFCu, 0xFDFEFF00u, sel);
-    const uint32_t m = ((nib >> 3) & 0x01010101u) * 0xFFu;
-    return (pos & ~m) | (neg & m);
-}
-
-__device__ __forceinline__ long expand_e2m1(uint32_t d) {
-    const uint32_t lo = e2m1_bytes_to_i8x2(d & 0x0F0F0F0Fu);
-    const uint32_t hi = e2m1_bytes_to_i8x2((d >> 4) & 0x0F0F0F0Fu);
-    return (long)(((uint64_t)hi << 32) | lo);
-}
-
-template <int FMT>
-__device__ __forceinline__ long expand(uint32_t d) {
-    if constexpr (FMT == kFmtUniform) return expand_uniform(d);
-    else return expand_e2m1(d);
-}
-
 struct GemmArgs {
     GemmJob j;
 };
@@ -146,33 +78,6 @@ __device__ bool resolve_ragged_m(const GemmJob& j, int32_t* grp, int64_t t, int&
     g_out = grp[0];
     local_tile = grp[1];
     return g_out >= 0;
-}
-
-// Write a workgroup's 128 x 128 fp32 accumulator tile (four waves, 2 x 2 MFMA tiles of 32 x 32 each; output
-// row of register i in lane l: 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32), scaled by `mul`.
-template <int OUT>
-__device__ __forceinline__ void store_tile(const GemmJob& j, const Tile& tl, const float (&acc)[2][2][16], float mul,
-                                           int wm, int wn, int h, int l32) {
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            const int col = wn * 64 + b * 32 + l32;
-            if (col >= tl.nrows) continue;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = wm * 64 + a * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                if (row >= tl.mrows) continue;
-                const float v = acc[a][b][i] * mul;
-                const int64_t off = tl.c_off + (int64_t)row * j.ldc + col;
-                if constexpr (OUT == kOutF32) {
-                    static_cast<float*>(j.c)[off] = v;
-                } else {
-                    static_cast<uint16_t*>(j.c)[off] = (uint16_t)f32_to_bf16_bits(v);
-                }
-            }
-        }
-    }
 }
 
 // Grid position of a workgroup: tile column, tile row (ragged-M: global m-tile index) and group (ragged-K).
@@ -235,122 +140,8 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos,
     return true;
 }
 
-template <int FMT, int OUT>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs args) {
-    __shared__ GemmSmem sm;
-    const GemmJob& j = args.j;
-    const int tid = threadIdx.x;
-
-    Tile tl;
-    if (!resolve_tile(j, sm.grp, grid_pos(), tl)) return;
-
-    // ---- main loop ----------------------------------------------------------------------------
-    const int lane = tid & 63, h = lane >> 5, l32 = lane & 31;
-    const int wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-
-    float acc[2][2][16];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.0f;
-
-    uint2 ra[4], rb[4];
-    float rsa[4], rsb[4];
-    const int64_t nstages = (tl.nkb + SKB - 1) / SKB;
-
-    auto load_stage = [&](int64_t s) {
-        const int64_t ks = s * SKB;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = tid + 256 * q;
-            const int row = e >> 3, kb = e & 7;
-            const bool kok = ks + kb < tl.nkb;
-            const bool aok = kok && row < tl.mrows, bok = kok && row < tl.nrows;
-            ra[q] = aok ? *reinterpret_cast<const uint2*>(tl.a + code_off(tl.a_row0, row, ks + kb, j.a_pld))
-                        : make_uint2(0, 0);
-            rsa[q] = aok ? tl.as[scale_off(tl.a_row0, row, ks + kb, j.as_pld)] : 0.0f;
-            rb[q] = bok ? *reinterpret_cast<const uint2*>(tl.b + code_off(tl.b_row0, row, ks + kb, j.b_pld))
-                        : make_uint2(0, 0);
-            rsb[q] = bok ? tl.bs[scale_off(tl.b_row0, row, ks + kb, j.bs_pld)] : 0.0f;
-        }
-    };
-    auto store_stage = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = tid + 256 * q;
-            const int row = e >> 3, kb = e & 7;
-            sm.a[buf][(kb * 2 + 0) * CPL + row] = ra[q].x;
-            sm.a[buf][(kb * 2 + 1) * CPL + row] = ra[q].y;
-            sm.b[buf][(kb * 2 + 0) * CPL + row] = rb[q].x;
-            sm.b[buf][(kb * 2 + 1) * CPL + row] = rb[q].y;
-            sm.as[buf][kb * SPL + row] = rsa[q];
-            sm.bs[buf][kb * SPL + row] = rsb[q];
-        }
-    };
-
-    if (nstages > 0) {
-        load_stage(0);
-        store_stage(0);
-    }
-    __syncthreads();
-
-    for (int64_t s = 0; s < nstages; ++s) {
-        const int buf = (int)(s & 1);
-        if (s + 1 < nstages) load_stage(s + 1);
-        const int64_t left = tl.nkb - s * SKB;
-        const int kbn = (int)(left < SKB ? left : SKB);
-#pragma unroll
-        for (int kb = 0; kb < SKB; ++kb) {
-            if (kb < kbn) {
-                long aop[2], bop[2];
-#pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2) {
-                    aop[t2] = expand<FMT>(sm.a[buf][(kb * 2 + h) * CPL + wm * 64 + t2 * 32 + l32]);
-                    bop[t2] = expand<FMT>(sm.b[buf][(kb * 2 + h) * CPL + wn * 64 + t2 * 32 + l32]);
-                }
-                v16i d[2][2];
-#pragma unroll
-                for (int a = 0; a < 2; ++a)
-#pragma unroll
-                    for (int b = 0; b < 2; ++b) {
-                        const v16i z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-                        d[a][b] = __builtin_amdgcn_mfma_i32_32x32x16_i8(aop[a], bop[b], z, 0, 0, 0);
-                    }
-                float sb[2];
-#pragma unroll
-                for (int b = 0; b < 2; ++b) sb[b] = sm.bs[buf][kb * SPL + wn * 64 + b * 32 + l32];
-#pragma unroll
-                for (int a = 0; a < 2; ++a) {
-                    float sa[16];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const float4 v =
-                            *reinterpret_cast<const float4*>(&sm.as[buf][kb * SPL + wm * 64 + a * 32 + 8 * q + 4 * h]);
-                        sa[4 * q + 0] = v.x;
-                        sa[4 * q + 1] = v.y;
-                        sa[4 * q + 2] = v.z;
-                        sa[4 * q + 3] = v.w;
-                    }
-#pragma unroll
-                    for (int b = 0; b < 2; ++b)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            acc[a][b][i] = __builtin_fmaf((float)d[a][b][i], sa[i] * sb[b], acc[a][b][i]);
-                }
-            }
-        }
-        if (s + 1 < nstages) store_stage(buf ^ 1);
-        __syncthreads();
-    }
-
-    constexpr float kUndo = FMT == kFmtUniform ? 1.0f : 0.25f;
-    store_tile<OUT>(j, tl, acc, kUndo, wm, wn, h, l32);
-}
-
 // ================================================================================================
-// fp32-output variant (the default).
+// The kernel.
 //
 // The per-block dot product D_b comes out of an MFMA already in fp32 and a second MFMA forms the outer
 // product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and block:
@@ -618,16 +409,6 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     }
 }
 
-// UFP4_GEMM_MFMA=i8 selects the int8-MFMA kernel (cvt + scale product + fma per output and block) instead of
-// the default fp32-output kernel; both compute the same sums exactly up to fp32 accumulation order.
-static bool use_i8_mfma() {
-    static const bool v = [] {
-        const char* e = getenv("UFP4_GEMM_MFMA");
-        return e != nullptr && strcmp(e, "i8") == 0;
-    }();
-    return v;
-}
-
 template <int FMT, int OUT>
 static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
     dim3 grid((unsigned)((j.N + BN - 1) / BN), 1, 1);
@@ -639,11 +420,7 @@ static hipError_t launch_t(const GemmJob& j, hipStream_t s) {
     }
     if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
     GemmArgs args{j};
-    if (use_i8_mfma()) {
-        gemm_kernel<FMT, OUT><<<grid, 256, 0, s>>>(args);
-    } else {
-        gemm_f32_kernel<FMT, OUT><<<grid, 64 * kWaves2, 0, s>>>(args);
-    }
+    gemm_f32_kernel<FMT, OUT><<<grid, 64 * kWaves2, 0, s>>>(args);
     return hipGetLastError();
 }
 

@@ -5,9 +5,17 @@
 //   y    = RN32( x S_16 H_16 )            exact 16-term sum in fp64 (Sylvester butterfly), one rounding
 //   s    = RN32(amax / g),  r = RN32(g / amax),  v = RN32(y * r)
 //   code = RTNE(v) or SR(v; Philox draw)  onto the grid, clamped to +-g
-// The RHT's factor 1/4 is a power of two: the kernel keeps y' = 4y = RN32(unscaled sum), so amax' = 4 amax,
-// RN32(g / amax') = RN32(g / amax) / 4 and y' * RN32(g / amax') = y * r exactly, and s = RN32(amax' / g) / 4.
-// These identities hold while y and s are normal fp32 numbers, the supported input domain.
+// y is rounded with gradual underflow and without overflow (24 significant bits past FLT_MAX); s is the IEEE
+// quotient (subnormal for tiny blocks, +inf past the fp32 range); r has 24 significant bits and no exponent
+// limit (equal to RN32(g / amax) wherever that is finite).
+//
+// Fast path. The RHT's factor 1/4 is a power of two: the kernel keeps y' = 4y = RN32(unscaled sum), so amax' =
+// 4 amax, RN32(g / amax') = r / 4, y' * RN32(g / amax') = y * r exactly, and s = RN32(amax' / g) / 4. For bf16
+// inputs y' = 4y holds for every output (a sum below 2^-124 is a multiple of 2^-133 with at most 9 significant
+// bits, so both it and a quarter of it are exact fp32 numbers); with amax' in [2^-121, 2^127) (or 0) the
+// quotients are normal and these identities are exact (s by the FMA-corrected product, r by an IEEE division). Any other block takes the exact path (`quant_core`),
+// which rescales the block by a power of two before the reciprocal. Real data never leaves the fast range; the
+// check costs three instructions per block.
 //
 // Two input layouts: rowwise (reduction axis contiguous, one thread per block, 32-byte loads) and
 // transposed (reduction axis strided: each thread loads a 16-row x 8-column sub-tile and builds its eight
@@ -165,10 +173,11 @@ __device__ __forceinline__ void rht16_unscaled(const uint32_t* w, const QuantArg
 // H_n is H_m (x) H_16 (outer factor on the high index bits), so after each thread's 16-point butterfly on its
 // own 16-block -- sub-block `sub` of the n-block, with its 16 bits of the n-bit sign mask -- a butterfly over
 // the m threads that hold the n-block (lanes `lane_step` apart, the partner of stage h at lane distance
-// h * lane_step) completes the exact fp64 sums; then y = RN32(RN64(sum * RN64(sqrt(1/n)))). Every lane must
-// call this (inactive blocks with zero inputs): the exchange reads the partner lanes' registers.
+// h * lane_step) completes the exact fp64 sums; then t = RN64(sum * RN64(sqrt(1/n))), whose rounding to fp32
+// precision is y (`quant_wide`). Every lane must call this (inactive blocks with zero inputs): the exchange
+// reads the partner lanes' registers.
 __device__ __forceinline__ void rht_wide(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t sub, int lane_step,
-                                         float (&y)[16]) {
+                                         double (&t)[16]) {
     const uint32_t mask = qa.sign_words[sub & (uint32_t)(qa.rht_m - 1)];  // this sub-block's 16 sign bits
     uint32_t sx[8];
 #pragma unroll
@@ -184,25 +193,69 @@ __device__ __forceinline__ void rht_wide(const uint32_t (&w)[8], const QuantArgs
         }
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) y[i] = (float)(d[i] * qa.rht_c);
+    for (int i = 0; i < 16; ++i) t[i] = d[i] * qa.rht_c;
 }
 
-// Scale and codes of one block from its (RHT-ed, unscaled) values y.
-template <int FMT, int ROUND, bool RHT>
-__device__ __forceinline__ void quant_y16(const float (&y)[16], const QuantArgs& qa, uint32_t blk, uint32_t row,
-                                          uint32_t& code_lo, uint32_t& code_hi, float& scale) {
+// The fast path's amax range (see the file header), [2^-121, 2^127), as fp32 bit patterns.
+constexpr uint32_t kFastLoBits = 0x03000000u;
+constexpr uint32_t kFastEndBits = 0x7F000000u;
+
+// amax (>= 0) outside {0} and [2^-121, 2^127) (infinity included): the block needs the exact path.
+__device__ __forceinline__ bool needs_exact(float amax) {
+    const uint32_t b = __float_as_uint(amax);
+    return b - kFastLoBits >= kFastEndBits - kFastLoBits && b != 0u;
+}
+
+// Exact path (see the file header), for a block whose amax is outside the fast range: the block is rescaled in
+// place by 2^64 (tiny) or 2^-64 (huge), and the fast arithmetic then runs on it. The power of two is exact on
+// every element whose v can be nonzero, the reciprocal of the scaled amax is a normal fp32 number with the same
+// 24-bit significand as g / amax, and (y_i 2^Q) r' is the same real product as y_i r, so one rounding still gives
+// v_i. Only the stored scale is taken separately: s = RN32(amax / g) is one IEEE division of amax, an fp32
+// number (for the folded RHT amax = amax' / 4 exactly). A folded or wide RHT output past FLT_MAX overflows y to
+// infinity; then `exact_t` supplies the fp64 values t_i whose rounding to 24 bits is y_i, and the block is taken
+// at 2^-64 (and s = RN32(amax 2^-64 / g) 2^64, +inf where amax / g is past the fp32 range).
+//
+// EXACT = false leaves the exact path out (its branch costs registers in the two-operand kernel): the result is
+// then valid only when the function returns false, and the caller redoes the block with EXACT = true otherwise.
+template <int FMT, int ROUND, bool FOLD, bool OVF, bool EXACT, typename TFn>
+__device__ __forceinline__ bool quant_core(float (&y)[16], TFn&& exact_t, const QuantArgs& qa, uint32_t blk,
+                                           uint32_t row, uint32_t& code_lo, uint32_t& code_hi, float& scale) {
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
     const float g = FMT == kFmtUniform ? 7.0f : qa.e2m1_g;
+    const bool exact = needs_exact(amax);
+    float s_exact = 0.0f;
+    if (EXACT && __builtin_expect(exact, 0)) {
+        if (OVF && !(amax <= 0x1.fffffep127f)) {
+            double t[16];
+            exact_t(t);
+            amax = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                y[i] = (float)(t[i] * 0x1p-64);  // y_i 2^-64: normal here, or too small to matter
+                amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
+            }
+            s_exact = __fmul_rn(amax / g, 0x1p64f);
+        } else {
+            s_exact = (FOLD ? __fmul_rn(amax, 0.25f) : amax) / g;  // IEEE: subnormal for a tiny block
+            const float q = amax < 1.0f ? 0x1p64f : 0x1p-64f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) y[i] = __fmul_rn(y[i], q);
+            amax = __fmul_rn(amax, q);
+        }
+    }
     // RN(amax / g) as RN(amax * c) with c = RN(1/g), corrected by one FMA residual step: equal to the correctly
-    // rounded quotient for every fp32 amax when g = 7 and for every normal quotient when g = 6 (both checked
-    // over all fp32 inputs); for g = 2 and 4 the product is already exact. amax = 0 gives 0.
+    // rounded quotient for every fp32 amax when g = 7 and for every normal quotient when g = 6 (both checked over
+    // all fp32 inputs); for g = 2 and 4 the product is already exact. amax = 0 gives 0.
     const float c = FMT == kFmtUniform ? 1.0f / 7.0f : qa.e2m1_ginv;
     const float q0 = amax * c;
     const float sc = __builtin_fmaf(__builtin_fmaf(-q0, g, amax), c, q0);
-    scale = RHT ? sc * 0.25f : sc;
+    scale = EXACT && exact ? s_exact : (FOLD ? sc * 0.25f : sc);
     const float r = amax > 0.0f ? g / amax : 0.0f;  // IEEE division; zero block: all v = 0, codes 0
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = __fmul_rn(y[i], r);
 
     uint32_t u[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if constexpr (ROUND == kRoundSR) {
@@ -212,40 +265,94 @@ __device__ __forceinline__ void quant_y16(const float (&y)[16], const QuantArgs&
         u[4] = p1.x; u[5] = p1.y; u[6] = p1.z; u[7] = p1.w;
     }
     if constexpr (FMT == kFmtUniform) {
-        uint32_t t[16];
+        uint32_t tt[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float v = __fmul_rn(y[i], r);
             if constexpr (ROUND == kRoundSR) {
                 const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);  // exact: an integer plus the constant
+                tt[i] = __float_as_uint(uniform_sr_level(v[i], u16) + kMagic8);  // exact: an integer plus the constant
             } else {
-                t[i] = __float_as_uint(v + kMagic8);  // the rounding itself
+                tt[i] = __float_as_uint(v[i] + kMagic8);  // the rounding itself
             }
         }
-        code_lo = offset_to_sign_magnitude(pack_nibbles(t));
-        code_hi = offset_to_sign_magnitude(pack_nibbles(t + 8));
+        code_lo = offset_to_sign_magnitude(pack_nibbles(tt));
+        code_hi = offset_to_sign_magnitude(pack_nibbles(tt + 8));
     } else {
         uint32_t lo = 0, hi = 0;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float v = __fmul_rn(y[i], r);
             const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-            const uint32_t c = e2m1_code<ROUND>(v, u16, g);
+            const uint32_t c = e2m1_code<ROUND>(v[i], u16, g);
             if (i < 8) lo |= c << (4 * i);
             else hi |= c << (4 * (i - 8));
         }
         code_lo = lo;
         code_hi = hi;
     }
+    return exact;
 }
 
-template <int FMT, int ROUND, bool RHT>
-__device__ __forceinline__ void quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
+// Values y given directly (no transform, or a transform already applied); finite, so they cannot overflow.
+template <int FMT, int ROUND>
+__device__ __forceinline__ void quant_y16(float (&y)[16], const QuantArgs& qa, uint32_t blk, uint32_t row,
+                                          uint32_t& code_lo, uint32_t& code_hi, float& scale) {
+    quant_core<FMT, ROUND, false, false, true>(y, [](double (&)[16]) {}, qa, blk, row, code_lo, code_hi, scale);
+}
+
+// The fp64 values y_i of the block-16 RHT before rounding (exact sums / 4), recomputed from the input words. The
+// empty asm makes the words opaque, so the compiler recomputes the sums here instead of keeping the fast path's
+// 32 registers of them alive until this rare branch.
+__device__ __forceinline__ void rht16_exact(const uint32_t (&w)[8], const QuantArgs& qa, double (&t)[16]) {
+    uint32_t wc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        wc[j] = w[j];
+        asm volatile("" : "+v"(wc[j]));
+    }
+    rht16_sums(wc, qa.sign_xor, t);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t[i] *= 0.25;  // exact in fp64
+}
+
+// Makes a register tile opaque to the compiler in place (see the two-operand kernel's fix-up).
+template <int R, int C>
+__device__ __forceinline__ void opaque(uint32_t (&a)[R][C]) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+#pragma unroll
+        for (int j = 0; j < C; ++j) asm volatile("" : "+v"(a[i][j]));
+    }
+}
+
+// One 16-block of bf16 pairs w (element 2j in the low half of w[j]), with the block-16 RHT when RHT. With EXACT
+// = false the result is valid only if this returns false (see `quant_core`).
+template <int FMT, int ROUND, bool RHT, bool EXACT = true>
+__device__ __forceinline__ bool quant_block16(const uint32_t (&w)[8], const QuantArgs& qa, uint32_t blk, uint32_t row,
                                               uint32_t& code_lo, uint32_t& code_hi, float& scale) {
     float y[16];
     rht16_unscaled<RHT>(w, qa, y);
-    quant_y16<FMT, ROUND, RHT>(y, qa, blk, row, code_lo, code_hi, scale);
+    if constexpr (RHT) {
+        return quant_core<FMT, ROUND, true, true, EXACT>(y, [&](double (&t)[16]) { rht16_exact(w, qa, t); }, qa, blk,
+                                                        row, code_lo, code_hi, scale);
+    } else {
+        return quant_core<FMT, ROUND, false, false, EXACT>(y, [](double (&)[16]) {}, qa, blk, row, code_lo, code_hi,
+                                                          scale);
+    }
+}
+
+// One block after a wider RHT (`rht_wide`): y = RN32(t), and t itself if that overflows.
+template <int FMT, int ROUND>
+__device__ __forceinline__ void quant_wide(const double (&t)[16], const QuantArgs& qa, uint32_t blk, uint32_t row,
+                                           uint32_t& code_lo, uint32_t& code_hi, float& scale) {
+    float y[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) y[i] = (float)t[i];
+    quant_core<FMT, ROUND, false, true, true>(
+        y, [&](double (&tt)[16]) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) tt[i] = t[i];
+        },
+        qa, blk, row, code_lo, code_hi, scale);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -299,9 +406,9 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x
             // h apart (n-blocks are aligned: b0 is a multiple of 16, nb of m)
             const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
                                    v[q][1].x, v[q][1].y, v[q][1].z, v[q][1].w};
-            float y[16];
-            rht_wide(w, qa, (uint32_t)b, 1, y);
-            if (r < qrows && b < nb) quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+            double tw[16];
+            rht_wide(w, qa, (uint32_t)b, 1, tw);
+            if (r < qrows && b < nb) quant_wide<FMT, ROUND>(tw, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
         } else if (r < qrows && b < nb) {
             if constexpr (sizeof(T) == 2) {
                 const uint32_t w[8] = {v[q][0].x, v[q][0].y, v[q][0].z, v[q][0].w,
@@ -316,7 +423,7 @@ __global__ __launch_bounds__(kRT) void quant_rows_kernel(const T* __restrict__ x
                     y[4 * c + 2] = __uint_as_float(v[q][c].z);
                     y[4 * c + 3] = __uint_as_float(v[q][c].w);
                 }
-                quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+                quant_y16<FMT, ROUND>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
             }
         }
         s_codes[k & 15][k >> 4] = make_uint2(lo, hi);
@@ -453,6 +560,7 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         // and a +0 scale, the padding value, so every block is quantized unconditionally.
         uint32_t clo[kXC], chi[kXC];
         float sc[kXC];
+        uint32_t redo = 0;  // blocks outside the fast range (block-16 RHT or none), redone below
 #pragma unroll
         for (int q = 0; q < kXC; ++q) {
             const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;  // high or low bf16 of each dword
@@ -461,12 +569,32 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
             for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
             if constexpr (WIDE) {
                 // consecutive blocks of the same columns are held by threads kXG apart (t = rb * kXG + cg)
-                float y[16];
-                rht_wide(w, qa, (uint32_t)gb, kXG, y);
-                quant_y16<FMT, ROUND, false>(y, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+                double tw[16];
+                rht_wide(w, qa, (uint32_t)gb, kXG, tw);
+                quant_wide<FMT, ROUND>(tw, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
                 __builtin_amdgcn_sched_barrier(0);  // one column at a time: bounds the live fp64 sums
             } else {
-                quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+                if (quant_block16<FMT, ROUND, RHT, false>(w, qa, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q],
+                                                          sc[q]))
+                    redo |= 1u << q;
+            }
+        }
+        // Rare: blocks outside the fast range are quantized again by the exact path. Kept out of the loop above,
+        // where its branch would cost registers on every block; the inputs and the row are made opaque so that the
+        // compiler recomputes here instead of keeping the loop's sums and draws alive.
+        if (!WIDE && __builtin_expect(__builtin_amdgcn_ballot_w64(redo != 0u) != 0, 0)) {
+            opaque(v);
+            uint32_t row0 = (uint32_t)cbase;
+            asm volatile("" : "+v"(row0));
+#pragma unroll
+            for (int q = 0; q < kXC; ++q) {
+                if (redo & (1u << q)) {
+                    const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+                    uint32_t w[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
+                    quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)gb, row0 + q, clo[q], chi[q], sc[q]);
+                }
             }
         }
         if constexpr (STAGE) {
@@ -572,13 +700,16 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
         {
             uint32_t clo[8], chi[8];
             float sc[8];
+            uint32_t redo = 0;  // blocks outside the fast range, redone below
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
                 uint32_t w[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
-                quant_block16<FMT, ROUND, RHT_C>(w, qc, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q], sc[q]);
+                if (quant_block16<FMT, ROUND, RHT_C, false>(w, qc, (uint32_t)gb, (uint32_t)(cbase + q), clo[q], chi[q],
+                                                            sc[q]))
+                    redo |= 1u << q;
             }
             const int64_t P = cbase >> 7, ri = cbase & 127;
             uint4* dc = reinterpret_cast<uint4*>(codes_c + P * code_pld_c + gb * 1024 + ri * 8);
@@ -587,6 +718,31 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
             float4* ds = reinterpret_cast<float4*>(scales_c + P * scale_pld_c + gb * 128 + ri);
             ds[0] = make_float4(sc[0], sc[1], sc[2], sc[3]);
             ds[1] = make_float4(sc[4], sc[5], sc[6], sc[7]);
+            // Rare: blocks outside the fast range are quantized again by the exact path and stored over the fast
+            // results (the same thread wrote them: program order keeps the second store last). Kept out of the loop
+            // above, where its branch would cost registers on every block.
+            if (__builtin_expect(__builtin_amdgcn_ballot_w64(redo != 0u) != 0, 0)) {
+                // inputs and row made opaque: otherwise the compiler reuses the loop's words, sums and draws here
+                // and keeps them all alive through the loop
+                opaque(v);
+                uint32_t row0 = (uint32_t)cbase;
+                asm volatile("" : "+v"(row0));
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (redo & (1u << q)) {
+                        const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+                        uint32_t w[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
+                        uint32_t lo, hi;
+                        float s1;
+                        quant_block16<FMT, ROUND, RHT_C>(w, qc, (uint32_t)gb, row0 + q, lo, hi, s1);
+                        *reinterpret_cast<uint2*>(codes_c + P * code_pld_c + gb * 1024 + (ri + q) * 8) = make_uint2(lo, hi);
+                        scales_c[P * scale_pld_c + gb * 128 + ri + q] = s1;
+                    }
+                }
+            }
         }
         if (!chunk_ok) continue;  // no Q_r block for padding columns (the partner lane takes the same branch)
         __builtin_amdgcn_sched_barrier(0);  // keep the two phases apart: their temporaries would add up
@@ -602,10 +758,12 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
         }
         uint32_t rlo[8], rhi[8];
         float rs[8];
+        uint32_t redo = 0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const uint32_t w[8] = {v[i][0], v[i][1], v[i][2], v[i][3], v[8 + i][0], v[8 + i][1], v[8 + i][2], v[8 + i][3]};
-            quant_block16<FMT, ROUND, RHT_R>(w, qr, (uint32_t)bcol, (uint32_t)(r0 + i), rlo[i], rhi[i], rs[i]);
+            if (quant_block16<FMT, ROUND, RHT_R, false>(w, qr, (uint32_t)bcol, (uint32_t)(r0 + i), rlo[i], rhi[i], rs[i]))
+                redo |= 1u << i;
         }
         uint4* dc = reinterpret_cast<uint4*>(codes_r + Pr * code_pld_r + bcol * 1024 + rir * 8);
 #pragma unroll
@@ -613,6 +771,23 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
         float4* ds = reinterpret_cast<float4*>(scales_r + Pr * scale_pld_r + bcol * 128 + rir);
         ds[0] = make_float4(rs[0], rs[1], rs[2], rs[3]);
         ds[1] = make_float4(rs[4], rs[5], rs[6], rs[7]);
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(redo != 0u) != 0, 0)) {  // as for Q_c above
+            opaque(v);
+            uint32_t row0 = (uint32_t)r0;
+            asm volatile("" : "+v"(row0));
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (redo & (1u << i)) {
+                    const uint32_t w[8] = {v[i][0], v[i][1], v[i][2], v[i][3],
+                                           v[8 + i][0], v[8 + i][1], v[8 + i][2], v[8 + i][3]};
+                    uint32_t lo, hi;
+                    float s1;
+                    quant_block16<FMT, ROUND, RHT_R>(w, qr, (uint32_t)bcol, row0 + i, lo, hi, s1);
+                    *reinterpret_cast<uint2*>(codes_r + Pr * code_pld_r + bcol * 1024 + (rir + i) * 8) = make_uint2(lo, hi);
+                    scales_r[Pr * scale_pld_r + bcol * 128 + rir + i] = s1;
+                }
+            }
+        }
     }
 }
 
@@ -657,13 +832,42 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(y[i]));
-    // amax = 1.f * 2^(eb - 127): E = floor(log2 amax) - 2 = eb - 129 (the OCP shared-exponent rule with the
-    // levels read as E2M3 numbers), so amax * 2^-E lies in [4, 8)
-    const uint32_t ab = __float_as_uint(amax);
-    const int e8 = (int)(ab >> 23) - 2;  // E + 127 for this amax
-    // y' = 4y with the RHT: the scale of y is 2^(E - 2); v = y' * 2^-E either way (exact, a power of two)
-    e8m0 = amax > 0.0f ? (uint32_t)(RHT ? e8 - 2 : e8) : 0u;
-    const float mult = amax > 0.0f ? __uint_as_float((uint32_t)(254 - e8) << 23) : 0.0f;
+    // floor(log2 amax) = (exponent field of amax) - 127 - P, with P = 2 for the folded RHT (y' = 4y) and P = 0
+    // otherwise; the exact path (as for the fp32 scales) rescales a block outside the fast range in place by
+    // 2^+-64 and adds it to P, so that amax is a normal number. E8M0 holds E >= -127: a tiny block takes the
+    // smallest scale. v = y 2^-E is one multiplication by a power of two, exact but below 2^-126.
+    int P = RHT ? 2 : 0;
+    if (__builtin_expect(needs_exact(amax), 0)) {
+        if (RHT && !(amax <= 0x1.fffffep127f)) {  // a rotated value past FLT_MAX: the fp64 sums at 2^-64
+            amax = 0.0f;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t wh[8] = {w[8 * h], w[8 * h + 1], w[8 * h + 2], w[8 * h + 3],
+                                        w[8 * h + 4], w[8 * h + 5], w[8 * h + 6], w[8 * h + 7]};
+                double t[16];
+                rht16_exact(wh, qa, t);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    y[16 * h + i] = (float)(t[i] * 0x1p-64);
+                    amax = __builtin_fmaxf(amax, __builtin_fabsf(y[16 * h + i]));
+                }
+            }
+            P = -64;
+        } else {
+            const float q = amax < 1.0f ? 0x1p64f : 0x1p-64f;
+#pragma unroll
+            for (int i = 0; i < 32; ++i) y[i] = __fmul_rn(y[i], q);
+            P += amax < 1.0f ? 64 : -64;
+            amax = __fmul_rn(amax, q);
+        }
+    }
+    const int fl = (int)(__float_as_uint(amax) >> 23) - 127 - P;  // floor(log2 amax)
+    const int E = fl - 2 > -127 ? fl - 2 : -127;
+    e8m0 = amax > 0.0f ? (uint32_t)(E + 127) : 0u;
+    const float mult = amax > 0.0f ? __uint_as_float((uint32_t)(127 - P - E) << 23) : 0.0f;  // 2^(-P-E), normal
+    float v[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) v[i] = __fmul_rn(y[i], mult);
     uint32_t p[4];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -677,12 +881,12 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
         uint32_t t[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float v = y[16 * h + i] * mult;  // |v| < 8: the top level 7 is the clamp
+            const float vi = v[16 * h + i];  // |v| < 8: the top level 7 is the clamp
             if constexpr (ROUND == kRoundSR) {
                 const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-                t[i] = __float_as_uint(uniform_sr_level(v, u16) + kMagic8);  // clamps itself
+                t[i] = __float_as_uint(uniform_sr_level(vi, u16) + kMagic8);  // clamps itself
             } else {
-                t[i] = __float_as_uint(__builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f) + kMagic8);
+                t[i] = __float_as_uint(__builtin_fminf(__builtin_fmaxf(vi, -7.0f), 7.0f) + kMagic8);
             }
         }
         p[2 * h] = offset_to_sign_magnitude(pack_nibbles(t));
@@ -847,22 +1051,37 @@ __global__ __launch_bounds__(kStatsThreads) void quant_stats_kernel(const uint16
 #pragma unroll
             for (int j = 0; j < 8; ++j) w[j] = (uint32_t)src[(2 * j) * ld] | ((uint32_t)src[(2 * j + 1) * ld] << 16);
         }
-        float y[16];
-        rht16_unscaled<RHT>(w, qa, y);
         uint32_t lo, hi;
         float sc;
-        quant_y16<FMT, ROUND, RHT>(y, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+        quant_block16<FMT, ROUND, RHT>(w, qa, (uint32_t)b, (uint32_t)r, lo, hi, sc);
+        // ref = y: a quarter of y' under the RHT, unless y' overflowed (a rotated value past FLT_MAX: then the
+        // fp64 sums give y with 24 significant bits)
+        float y[16];
+        rht16_unscaled<RHT>(w, qa, y);
+        double ref[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) ref[i] = RHT ? 0.25 * (double)y[i] : (double)y[i];
+        if (RHT) {
+            float ym = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) ym = __builtin_fmaxf(ym, __builtin_fabsf(y[i]));
+            if (__builtin_expect(!(ym <= 0x1.fffffep127f), 0)) {
+                double t[16];
+                rht16_exact(w, qa, t);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) ref[i] = (double)(float)(t[i] * 0x1p-64) * 0x1p64;
+            }
+        }
         const double s = (double)sc;
         uint64_t counts = 0;  // one byte per magnitude code: at most 16 per block
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             const uint32_t nib = ((i < 8 ? lo : hi) >> (4 * (i & 7))) & 15u;
             const double q = (double)level_of_nibble<FMT>(nib) * s;  // a 4-bit level times an fp32 scale: exact
-            const double ref = RHT ? 0.25 * (double)y[i] : (double)y[i];  // y holds 4y under the RHT
-            const double d = q - ref;
+            const double d = q - ref[i];
             e2 = __builtin_fma(d, d, e2);
-            r2 = __builtin_fma(ref, ref, r2);
-            cr = __builtin_fma(q, ref, cr);
+            r2 = __builtin_fma(ref[i], ref[i], r2);
+            cr = __builtin_fma(q, ref[i], cr);
             counts += 1ull << (8 * (nib & 7u));
         }
 #pragma unroll
@@ -954,12 +1173,14 @@ __global__ __launch_bounds__(kRhtThreads) void rht_rows_kernel(const uint16_t* _
         const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kBlock);
         const uint4 v0 = src[0], v1 = src[1];
         const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        double d[16];
+        rht16_sums(w, qa.sign_xor, d);
         float yv[16];
-        rht16_unscaled<true>(w, qa, yv);  // 4y
+#pragma unroll
+        for (int i = 0; i < 16; ++i) yv[i] = (float)(d[i] * 0.25);  // y = RN32(sum / 4); +-inf past FLT_MAX
         float4* dst = reinterpret_cast<float4*>(y + r * ldy + b * kBlock);
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            dst[c] = make_float4(yv[4 * c] * 0.25f, yv[4 * c + 1] * 0.25f, yv[4 * c + 2] * 0.25f, yv[4 * c + 3] * 0.25f);
+        for (int c = 0; c < 4; ++c) dst[c] = make_float4(yv[4 * c], yv[4 * c + 1], yv[4 * c + 2], yv[4 * c + 3]);
     }
 }
 

@@ -37,7 +37,7 @@ def test_standalone_rht_is_correctly_rounded(shape):
         y = U.rht(t.cuda(), sign_mask=mask).cpu().numpy()
         a = O.bf16_bits_to_f32(WL.bf16_bits(t))
         want = O.rht_blocks(a.reshape(shape[0], -1, 16), mask).reshape(shape)
-        assert np.array_equal(y.view(np.uint32), want.view(np.uint32)), f"{shape} mask={mask:#x}"
+        assert np.array_equal(y.view(np.uint32), want.astype(np.float32).view(np.uint32)), f"{shape} mask={mask:#x}"
 
 
 @pytest.mark.parametrize("shape", SHAPES)
@@ -85,7 +85,7 @@ def test_strided_buffers():
     y = ybuf[:, 4:68]
     U.rht(x, sign_mask=0x1234, out=y)
     want = O.rht_blocks(O.bf16_bits_to_f32(WL.bf16_bits(x.cpu())).reshape(64, 4, 16), 0x1234).reshape(64, 64)
-    assert np.array_equal(y.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), want.astype(np.float32).view(np.uint32))
     assert torch.isnan(ybuf[:, :4]).all() and torch.isnan(ybuf[:, 68:]).all()
     q = U.quantize_f32(y, O.UNIFORM)
     ref = U.rht_quantize(x, rht=True, sign_mask=0x1234)
