@@ -197,8 +197,8 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     x, dy = wl.x.cuda(), wl.dy.cuda()
     w2 = wl.w.reshape(E * N, K).cuda()
     M = x.shape[0]
-    off, poff, red = U.group_offsets(wl.counts)
-    eoff, epoff, ered = U.group_offsets([N] * E)
+    off, red = U.group_offsets(wl.counts)
+    eoff, ered = U.group_offsets([N] * E)
     q = {
         "x": U.empty_qtensor(M, K, fmt), "w": U.empty_qtensor(E * N, K, fmt), "dy": U.empty_qtensor(M, N, fmt),
         "wt": U.empty_qtensor(K, E * N, fmt), "dyt": U.empty_qtensor(N, red, fmt), "xt": U.empty_qtensor(K, red, fmt),
@@ -214,17 +214,17 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
                                                          sign_mask_cols=m, out_rows=q["w"], out_cols=q["wt"]), rec)
         else:
             tl.run("quant_w", lambda: Q(w2, rht=r_y, sign_mask=m, out=q["w"]), rec)
-            tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, epoff, ered, fmt=fmt, rht=r_dx, sign_mask=m,
+            tl.run("quant_wt", lambda: U.quantize_grouped_t(w2, eoff, ered, fmt=fmt, rht=r_dx, sign_mask=m,
                                                             out=q["wt"]), rec)
         tl.run("quant_dy_sr", lambda: Q(dy, rht=r_dx, sign_mask=m, rounding=U.SR, seed=s, stream_id=0,
                                         out=q["dy"]), rec)
-        tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
+        tl.run("quant_dyt_sr", lambda: U.quantize_grouped_t(dy, off, red, fmt=fmt, rht=r_dw, sign_mask=m,
                                                             rounding=U.SR, seed=s, stream_id=1, out=q["dyt"]), rec)
-        tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, poff, red, fmt=fmt, rht=r_dw, sign_mask=m,
+        tl.run("quant_xt", lambda: U.quantize_grouped_t(x, off, red, fmt=fmt, rht=r_dw, sign_mask=m,
                                                         out=q["xt"]), rec)
-        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y_grouped(q["x"], q["w"], off, N, out=y), rec)
+        tl.run("gemm_fwd_y", lambda: U.gemm_fwd_y_grouped(q["x"], q["w"], off, out=y), rec)
         tl.run("gemm_bwd_dx", lambda: U.gemm_bwd_dx_grouped(q["dy"], q["wt"], off, out=dx), rec)
-        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw_grouped(q["dyt"], q["xt"], poff, out=dw), rec)
+        tl.run("gemm_bwd_dw", lambda: U.gemm_bwd_dw_grouped(q["dyt"], q["xt"], off, out=dw), rec)
 
     flops = 2 * M * N * K
     kern = {"quant_x": ("quant", M * K)}
@@ -312,21 +312,22 @@ def quality_report(wl, steps: int):
            "dY^T (bwd_dw)": (dy, True, U.SR, 1), "X^T (bwd_dw)": (x, True, U.RTNE, 0)}
     table = {}
     for gname, fmt, mf in QUALITY_GRIDS:
-        rows = {}
+        rows, stats = {}, {}
         for oname, (t, tr, rnd, st) in ops.items():
-            r = {}
+            r, recs = {}, {}
             for rht in (False, True):
                 q = U.quant_stats(t, fmt, max_fpx=mf, transpose=tr, rht=rht, sign_mask=wl.sign_mask, rounding=rnd,
                                   seed=wl.seed, stream_id=st)
+                recs[rht] = q
                 r["rht" if rht else "raw"] = {"nmse": q.nmse, "sqnr_db": round(q.sqnr_db, 3),
                                               "alpha": round(q.alpha, 6), "beff": round(q.beff, 4)}
-                r["_nmse_" + ("rht" if rht else "raw")] = q.nmse
-            r["delta_sqnr_db"] = round(10.0 * np.log10(r.pop("_nmse_raw") / r.pop("_nmse_rht")), 3)
-            rows[oname] = r
+            r["delta_sqnr_db"] = round(U.delta_sqnr_db(recs[False], recs[True]), 3)
+            rows[oname], stats[oname] = r, recs
         eta = {}
         for gemm, (a, b) in {"fwd_y": ("X (fwd_y)", "W (fwd_y)"), "bwd_dx": ("dY (bwd_dx)", "W^T (bwd_dx)"),
                              "bwd_dw": ("dY^T (bwd_dw)", "X^T (bwd_dw)")}.items():
-            eta[gemm] = {k: round(rows[a][k]["alpha"] * rows[b][k]["alpha"], 6) for k in ("raw", "rht")}
+            eta[gemm] = {("rht" if k else "raw"): round(U.gemm_attenuation(stats[a][k], stats[b][k]), 6)
+                         for k in (False, True)}
         table[gname] = {"operands": rows, "eta": eta}
     # timing of the statistics kernel (uniform grid, RHT, X rowwise)
     rec = torch.empty(U.STATS_BYTES // 8, dtype=torch.float64, device="cuda")

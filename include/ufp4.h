@@ -15,25 +15,26 @@
  * Conventions shared by every call
  * --------------------------------
  *  - All pointers named *_dev are device pointers (HBM). Host pointers are named *_host. The caller owns
- *    every buffer; the library allocates, frees and synchronizes nothing.
+ *    every buffer; the library allocates, frees and synchronizes nothing, and keeps no state between calls.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls are asynchronous on it.
  *  - bf16 tensors are row-major with a leading dimension `ld` in elements (ld >= cols, ld % 8 == 0,
  *    base 16-byte aligned).
  *  - A quantized operand Q is [rows, red] (red % 16 == 0, nkb = red/16 blocks of 16 along the reduction
- *    axis), stored in panels: rows 128p .. 128p+127 form panel p, and within a panel the data of block b
- *    of all 128 rows is contiguous -- the order in which the GEMMs stage K-blocks.
- *      codes : panel p at codes_dev + p * code_panel_ld bytes; block b of row 128p + i at
- *              + b * 1024 + i * 8 (8 bytes). Element 2j of the block is the low nibble of byte j. Each
- *              nibble is sign-magnitude: sign in bit 3, magnitude code in bits 0-2, zero always +0.
- *              Uniform grid: magnitude |k| of the code k in -7..7. E2M1: index of the magnitude in
- *              0, .5, 1, 1.5, 2, 3, 4, 6 (the OCP FP4 bit pattern).
- *      scales: fp32; panel p at scales_dev + p * scale_panel_ld floats; block b of row 128p + i at
- *              + b * 128 + i. Block b of row r dequantizes as level(code) * scale. Uniform grid:
- *              s = RN(amax/7); E2M1: s = RN(amax/6).
- *      code_panel_ld >= 1024 * nkb and a multiple of 16, scale_panel_ld >= 128 * nkb and a multiple of 4;
- *      both base pointers 16-byte aligned; buffers hold ceil(rows / 128) whole panels. The quantizers
- *      write rows past `rows` in the last panel as zero codes and zero scales. Panel strides above 2^29
- *      bytes (codes) or 2^27 floats (scales) return UFP4_ERR_UNSUPPORTED.
+ *    axis), described by a ufp4_qtensor (below) and stored in panels: rows 128p .. 128p+127 form panel p, and
+ *    within a panel the data of block b of all 128 rows is contiguous -- the order in which the GEMMs stage
+ *    K-blocks.
+ *      codes : panel p at codes + p * code_panel_ld bytes; block b of row 128p + i at + b * 1024 + i * 8
+ *              (8 bytes). Element 2j of the block is the low nibble of byte j. Each nibble is sign-magnitude:
+ *              sign in bit 3, magnitude code in bits 0-2, zero always +0. Uniform grid: magnitude |k| of the
+ *              code k in -7..7. E2M1: index of the magnitude in 0, .5, 1, 1.5, 2, 3, 4, 6 (the OCP FP4 bit
+ *              pattern).
+ *      scales: fp32; panel p at scales + p * scale_panel_ld floats; block b of row 128p + i at + b * 128 + i.
+ *              Block b of row r dequantizes as level(code) * scale.
+ *      code_panel_ld >= 1024 * nkb and a multiple of 16, scale_panel_ld >= 128 * nkb and a multiple of 4; both
+ *      base pointers 16-byte aligned; the buffers hold `panels` >= ceil(rows / 128) whole panels
+ *      (ufp4_qtensor_bytes gives the minimal layout). The quantizers write rows past `rows` in the last panel
+ *      as zero codes and zero scales. Panel strides above 2^29 bytes (codes) or 2^27 floats (scales) return
+ *      UFP4_ERR_UNSUPPORTED.
  *  - Quantizer arithmetic, per 16-block x (bf16):
  *      y_i  = the exact 1/4 * sum_j H16[i,j] * eps_j * x_j  rounded once to fp32 precision (rht != 0), else
  *             y = x; H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
@@ -41,7 +42,7 @@
  *             FLT_MAX keeps 24 significant bits). Exact when the nonzero |x_j| of a block span at most 2^41.
  *      amax = max |y_i|;  s = RN32(amax/g) (IEEE: subnormal for a tiny block, +inf past the fp32 range);
  *      r = g/amax rounded to 24 significant bits without an exponent limit (= RN32(g/amax) whenever that is
- *      finite);  v_i = RN32(y_i * r);  amax == 0 -> s = 0, codes 0.
+ *      finite);  v_i = RN32(y_i * r);  amax == 0 -> s = 0, codes 0.  Uniform grid g = 7, E2M1 g = 6.
  *      RTNE (Sec. 2.1): nearest level, ties to the level with the even magnitude code.
  *      SR   (Sec. 2.1): adjacent signed levels g_a <= v < g_b; q = g_b iff u/2^16 < (v - g_a)/(g_b - g_a),
  *             u a 16-bit Philox4x32-10 draw: key = (seed lo32, seed hi32), counter = (block, row, half,
@@ -49,7 +50,8 @@
  *             `block` is the block index along the reduction axis, `row` the operand row.
  *      |v| beyond the top level is clamped to it.
  *  - GEMMs: C[i, j] = sum_b sA[i,b] sB[j,b] sum_{k in block b} level(A[i,k]) level(B[j,k]) with fp32
- *    accumulation; output fp32 or bf16 (RNE), row-major with leading dimension ldc (elements).
+ *    accumulation; output fp32 or bf16 (RNE), row-major with leading dimension ldc (elements). The output
+ *    buffer must hold the product; the library cannot see its size.
  *
  * Errors: every call validates its arguments on the host before launching anything and returns
  * UFP4_OK or an error code (no launch happens on error). Device faults surface at the caller's next
@@ -67,22 +69,66 @@ extern "C" {
 
 typedef enum {
     UFP4_OK = 0,
-    UFP4_ERR_INVALID_ARG = 1, /* null pointer, negative size, unknown enum value                     */
-    UFP4_ERR_SHAPE = 2,       /* reduction length not a multiple of 16, leading dimension too small  */
-    UFP4_ERR_ALIGN = 3,       /* pointer or leading dimension not aligned as required                 */
-    UFP4_ERR_UNSUPPORTED = 5, /* valid request outside the implemented limits or variants              */
-    UFP4_ERR_HIP = 6          /* kernel launch failed                                                 */
+    UFP4_ERR_INVALID_ARG = 1, /* null pointer, negative size, unknown enum value                          */
+    UFP4_ERR_SHAPE = 2,       /* reduction length not a multiple of 16, leading dimension or buffer too small */
+    UFP4_ERR_ALIGN = 3,       /* pointer or leading dimension not aligned as required                      */
+    UFP4_ERR_MISMATCH = 4,    /* the operands of a GEMM were quantized differently: grid, RHT block or sign */
+                              /* mask, or reduction length (Sec. 2.2 needs the same H' on both operands)     */
+    UFP4_ERR_UNSUPPORTED = 5, /* valid request outside the implemented limits or variants                   */
+    UFP4_ERR_HIP = 6          /* kernel launch failed                                                      */
 } ufp4_status;
 
-enum { UFP4_FMT_UNIFORM = 0, UFP4_FMT_E2M1 = 1 };
+enum { UFP4_FMT_UNIFORM = 0, UFP4_FMT_E2M1 = 1, UFP4_FMT_UNIFORM_MX32 = 2 };
 enum { UFP4_ROUND_RTNE = 0, UFP4_ROUND_SR = 1 };
 enum { UFP4_OUT_F32 = 0, UFP4_OUT_BF16 = 1 };
+
+/*
+ * A quantized operand Q(A H') [rows, red] (Sec. 2.1: codes plus block scales). The caller sets the storage
+ * fields and passes the descriptor to a quantizer, which checks that the operand fits them and records what it
+ * wrote; the GEMMs read both and refuse operand pairs whose grid, RHT block, RHT signs or reduction length
+ * differ (UFP4_ERR_MISMATCH): the rotation cancels in the product only when both operands carry the same H'
+ * along the shared axis (Sec. 2.2).
+ */
+typedef struct {
+    /* storage, set by the caller */
+    void *codes;             /* device; panel layout above (UFP4_FMT_UNIFORM_MX32: see ufp4_mx_quantize) */
+    void *scales;            /* device; fp32, or E8M0 bytes for UFP4_FMT_UNIFORM_MX32                   */
+    int64_t code_panel_ld;   /* bytes from one panel of codes to the next                               */
+    int64_t scale_panel_ld;  /* scale elements (floats, or bytes for E8M0) from one panel to the next   */
+    int64_t panels;          /* whole panels the two buffers hold                                        */
+    /* contents, written by the quantizer */
+    int64_t rows;            /* operand rows                                                             */
+    int64_t red;             /* reduction length                                                         */
+    int32_t format;          /* UFP4_FMT_*                                                               */
+    int32_t rht_block;       /* RHT along the reduction axis: 0 (none), 16, 32, 64 or 128                */
+    uint16_t sign_words[8];  /* its signs: eps_j = -1 iff bit (j % 16) of word j / 16; unused words 0    */
+    float max_fpx;           /* E2M1 grid cut at 2 or 4 (Sec. 5 Q4); 0 for the full grid                 */
+    int32_t rounding;        /* UFP4_ROUND_* used (recorded only)                                        */
+} ufp4_qtensor;
 
 /* Human-readable name of a status code (static string). */
 const char *ufp4_status_string(int status);
 
 /* Library version, "major.minor.patch". */
 const char *ufp4_version(void);
+
+/*
+ * ufp4_qtensor_bytes -- the minimal storage of a [rows, red] operand of `format` (UFP4_FMT_*): panel count, panel
+ * strides (code_panel_ld bytes; scale_panel_ld floats, or bytes for UFP4_FMT_UNIFORM_MX32) and the two buffer
+ * sizes in bytes. Any output pointer may be NULL. red must be a multiple of 16 (32 for UFP4_FMT_UNIFORM_MX32);
+ * an empty operand still has one panel. Host only.
+ */
+int ufp4_qtensor_bytes(int format, int64_t rows, int64_t red, int64_t *panels, int64_t *code_panel_ld,
+                       int64_t *scale_panel_ld, size_t *codes_bytes, size_t *scales_bytes);
+
+/*
+ * ufp4_grouped_reduction -- the reduction axis of a grouped transposed operand (bwd_dw of a MoE layer): each
+ * group's tokens zero-padded to a multiple of 16, groups concatenated. From host token offsets off_0 = 0 <=
+ * ... <= off_G: red_total = sum_g 16 ceil((off_{g+1} - off_g) / 16), and, if padded_offsets_host is not NULL,
+ * the G + 1 padded offsets pad_0 = 0, pad_{g+1} = pad_g + 16 ceil((off_{g+1} - off_g) / 16). Host only.
+ */
+int ufp4_grouped_reduction(const int64_t *group_offsets_host, int32_t num_groups, int64_t *padded_offsets_host,
+                           int64_t *red_total);
 
 /*
  * ufp4_rht_quantize -- fused RHT + uniform-grid quantization of one GEMM operand (Sec. 2.1, Sec. 2.2;
@@ -92,19 +138,19 @@ const char *ufp4_version(void);
  *   transpose  0: operand A = X, reduction along cols (cols % 16 == 0); Q is [rows, cols].
  *              1: operand A = X^T, reduction along rows (rows % 16 == 0); Q is [cols, rows].
  *   rht        nonzero: apply the block-16 RHT with sign_mask (bits 0..15) before quantizing.
- *   rounding   UFP4_ROUND_RTNE or UFP4_ROUND_SR (seed, stream select the Philox draws; ignored for RTNE).
- *   codes_dev, code_panel_ld, scales_dev, scale_panel_ld: Q in the panel layout above.
+ *   rounding   UFP4_ROUND_RTNE or UFP4_ROUND_SR (seed, stream_id select the Philox draws; ignored for RTNE).
+ *   out        storage set by the caller; its contents fields are written.
  * Rowwise operands (transpose = 0) of more than 2097024 rows (16383 panels) return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_rht_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
-                      uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
-                      int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld, void *stream);
+                      uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                      void *stream);
 
 /* ufp4_e2m1_quantize -- the same operation on the E2M1 grid (g = 6, levels 0, .5, 1, 1.5, 2, 3, 4, 6),
  * the comparison baseline of Table 1. Arguments as ufp4_rht_quantize. */
 int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
-                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
-                       int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld, void *stream);
+                       uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                       void *stream);
 
 /*
  * ufp4_e2m1_quantize_range -- ufp4_e2m1_quantize on the E2M1 grid cut at max_fpx (Sec. 5 Q4, the
@@ -115,15 +161,15 @@ int ufp4_e2m1_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld
  */
 int ufp4_e2m1_quantize_range(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
                              uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, float max_fpx,
-                             void *codes_dev, int64_t code_panel_ld, float *scales_dev, int64_t scale_panel_ld,
-                             void *stream);
+                             ufp4_qtensor *out, void *stream);
 
 /*
  * ufp4_quantize_rht_block -- RHT over blocks of n = 16, 32, 64 or 128 elements along the reduction axis, then
  * the usual 1x16 quantization of the result (the RHT block-size dimension of the paper's E2M1 reference
- * search, Appendix; the recipe itself uses 16). Per n-block: y = RN32( RN64( S * RN64(sqrt(1/n)) ) ) with S the
- * exact sum_j H_n[i,j] eps_j x_j (H_n the Sylvester +-1 matrix, exact when a block's nonzero |x| span at
- * most 2^(45 - log2 n)); for n = 16 and 64 the factor is a power of two and y is correctly rounded.
+ * search, Appendix; the recipe itself uses 16). Per n-block: y = the fp32 rounding (as above) of
+ * RN64( S * RN64(sqrt(1/n)) ) with S the exact sum_j H_n[i,j] eps_j x_j (H_n the Sylvester +-1 matrix, exact when a
+ * block's nonzero |x| span at most 2^(45 - log2 n)); for n = 16 and 64 the factor is a power of two and y is
+ * correctly rounded.
  *   rht_block        16, 32, 64 or 128; the reduction length must be a multiple of it.
  *   sign_words_host  host array of rht_block / 16 words: eps_j = -1 iff bit (j % 16) of word j / 16 is set.
  *   format           UFP4_FMT_UNIFORM or UFP4_FMT_E2M1 (full grid). Rowwise and plain transposed operands
@@ -132,22 +178,20 @@ int ufp4_e2m1_quantize_range(const void *x_dev, int64_t rows, int64_t cols, int6
  */
 int ufp4_quantize_rht_block(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,
                             int rht_block, const uint16_t *sign_words_host, int rounding, uint64_t seed,
-                            uint32_t stream_id, void *codes_dev, int64_t code_panel_ld, float *scales_dev,
-                            int64_t scale_panel_ld, void *stream);
+                            uint32_t stream_id, ufp4_qtensor *out, void *stream);
 
 /*
  * ufp4_quant_stats -- quality statistics of one quantization, the sums behind the diagnostics of Sec. 3.2
  * (NMSE_A(G, T), SQNR, the operand projection alpha, the bucket entropy behind B_eff). The operand is
  * quantized exactly as ufp4_rht_quantize / ufp4_e2m1_quantize(_range) would quantize it, but nothing is
- * stored except the record below. For every element, ref is the value the quantizer rounds (the fp32 RHT
- * output y when rht != 0, else x) and q = level(code) * scale its dequantized value.
+ * stored except the record below. For every element, ref is the value the quantizer rounds (the RHT output
+ * y when rht != 0, else x) and q = level(code) * scale its dequantized value.
  *
  *   format, max_fpx  UFP4_FMT_UNIFORM with max_fpx = 0, or UFP4_FMT_E2M1 with max_fpx 0 (full grid), 2, 4, 6.
  *   stats_dev        device pointer (8-byte aligned) to one ufp4_quant_stats_t record, overwritten (zero for
- *                    an empty operand, whose x_dev may be NULL). fp64 sums are accumulated with atomics: their last bits may
- *                    differ between calls; the counts are exact.
- *   Other arguments as ufp4_rht_quantize. NMSE = err2 / ref2, alpha = cross / ref2, bucket fractions
- *   p_m = hist[m] / (rows * cols).
+ *                    an empty operand, whose x_dev may be NULL). fp64 sums are accumulated with atomics: their
+ *                    last bits may differ between calls; the counts are exact.
+ *   Other arguments as ufp4_rht_quantize. ufp4_quant_metrics turns the record into the Sec. 3.2 metrics.
  */
 typedef struct {
     double err2;           /* sum of (q - ref)^2 */
@@ -161,15 +205,45 @@ int ufp4_quant_stats(int format, float max_fpx, const void *x_dev, int64_t rows,
                      ufp4_quant_stats_t *stats_dev, void *stream);
 
 /*
+ * ufp4_quant_metrics -- the Sec. 3.2 diagnostics of one quantization from its ufp4_quant_stats_t record (host
+ * copy): NMSE = err2 / ref2, SQNR = -10 log10 NMSE (dB; +inf when err2 = 0), the operand projection alpha =
+ * cross / ref2 (NaN for an all-zero operand), and the bucket statistics over the K magnitude levels of the
+ * grid, zero included (K = 8; the E2M1 grid cut at max_fpx 2 or 4 has K = 5 or 7): p_m = hist[m] / sum, the
+ * entropy E = -sum_m p_m log(p_m + 1e-12) and B_eff = exp(E) / K. format and max_fpx as in ufp4_quant_stats.
+ * Host only.
+ */
+typedef struct {
+    double nmse;
+    double sqnr_db;
+    double alpha;
+    double entropy;
+    double beff;
+} ufp4_quant_metrics_t;
+
+int ufp4_quant_metrics(const ufp4_quant_stats_t *stats_host, int format, float max_fpx,
+                       ufp4_quant_metrics_t *metrics_host);
+
+/*
+ * ufp4_rotation_gain -- Sec. 3.2's Delta SQNR of a rotation, 10 log10(NMSE without RHT / NMSE with RHT) in dB
+ * (positive when the rotation lowers the quantization error), from the metrics of the two quantizations of
+ * one operand; and the attenuation of a GEMM's coherent signal, eta = alpha_A * alpha_B, from the metrics of
+ * its two operands. Either output pointer may be NULL. Host only.
+ */
+int ufp4_rotation_gain(const ufp4_quant_metrics_t *raw_host, const ufp4_quant_metrics_t *rotated_host,
+                       double *delta_sqnr_db);
+int ufp4_gemm_attenuation(const ufp4_quant_metrics_t *a_host, const ufp4_quant_metrics_t *b_host, double *eta);
+
+/*
  * The unfused form of RHT + quantization (Sec. 5 Q5 measures it against the fused kernel): a standalone
  * transform that writes the rotated tensor, then a plain quantization of it. The intermediate is fp32, which
- * holds y exactly, so ufp4_quantize_f32(ufp4_rht(x)) produces the same codes and scales as
+ * holds y exactly (unless a rotated value passes FLT_MAX, which only inputs within a factor 4 of the bf16
+ * maximum produce), so ufp4_quantize_f32(ufp4_rht(x)) produces the same codes and scales as
  * ufp4_rht_quantize(x, rht = 1) (rowwise) bit for bit.
  *
  * ufp4_rht -- y = RN_fp32( x S_16 H_16 ) for every 16-block along the rows of x (Sec. 2.2; the arithmetic
- *   of the quantizer's transform, see the conventions above; +-inf past FLT_MAX). x_dev bf16 [rows, cols] (cols % 16 == 0, ld as
- *   for the quantizers); y_dev fp32 [rows, cols] with leading dimension ldy (ldy >= cols, ldy % 4 == 0,
- *   16-byte aligned). sign_mask as for ufp4_rht_quantize.
+ *   of the quantizer's transform, see the conventions above; +-inf past FLT_MAX). x_dev bf16 [rows, cols]
+ *   (cols % 16 == 0, ld as for the quantizers); y_dev fp32 [rows, cols] with leading dimension ldy (ldy >= cols,
+ *   ldy % 4 == 0, 16-byte aligned). sign_mask as for ufp4_rht_quantize.
  */
 int ufp4_rht(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t sign_mask, float *y_dev,
              int64_t ldy, void *stream);
@@ -178,31 +252,31 @@ int ufp4_rht(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t
  * ufp4_quantize_f32 -- rowwise quantization of an fp32 tensor without a transform (the second half of the
  *   unfused form): operand A = X [rows, cols] along cols, the arithmetic of ufp4_rht_quantize with rht = 0
  *   applied to fp32 values. format UFP4_FMT_UNIFORM or UFP4_FMT_E2M1 (full grid); ld >= cols, ld % 4 == 0,
- *   x_dev 16-byte aligned. Inputs must be finite.
- *   Remaining arguments as ufp4_rht_quantize.
+ *   x_dev 16-byte aligned; inputs finite. rht, sign_mask: the block-16 RHT the input already carries (from
+ *   ufp4_rht), recorded in `out` for the GEMMs' operand check; they do not change the arithmetic. Remaining
+ *   arguments as ufp4_rht_quantize.
  */
-int ufp4_quantize_f32(int format, const float *x_dev, int64_t rows, int64_t cols, int64_t ld, int rounding,
-                      uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_panel_ld, float *scales_dev,
-                      int64_t scale_panel_ld, void *stream);
+int ufp4_quantize_f32(int format, const float *x_dev, int64_t rows, int64_t cols, int64_t ld, int rht,
+                      uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                      void *stream);
 
 /*
  * ufp4_quantize_grouped_t -- transposed quantization of an expert-grouped tensor (MoE), either grid.
  *
  *   x_dev              bf16 [rows, cols] (ld elements); rows are split into num_groups consecutive groups.
  *   group_offsets_dev  int64 [num_groups + 1] device array, 0 = off_0 <= ... <= off_G = rows.
- *   padded_offsets_dev int64 [num_groups + 1] device array, pad_0 = 0, pad_{g+1} = pad_g +
- *                      16 * ceil((off_{g+1} - off_g) / 16): the group's column range in Q.
- *   Q is [cols, red_total] with red_total = pad_G; group g's block of Q is X[off_g:off_{g+1}]^T with its
- *   reduction (token) axis zero-padded to a multiple of 16. Block numbers in the SR counters count along
- *   the padded concatenated axis. Used for bwd_dw's dY^T and X^T and, with equal groups, for the
- *   per-expert W^T of bwd_dx.
- *   red_total          pad_G as known to the caller (sizes the output); must match the device array.
+ *   red_total          reduction length of Q, at least pad_G (ufp4_grouped_reduction) when the offsets are known
+ *                      on the host, else any bound such as rows + 15 * num_groups; blocks past pad_G are zero.
+ *   Q is [cols, red_total]: group g's block of Q is X[off_g:off_{g+1}]^T with its reduction (token) axis
+ *   zero-padded to a multiple of 16, at reduction positions pad_g .. pad_{g+1} (the padded offsets are computed
+ *   on the device from the token offsets). Block numbers in the SR counters count along the padded
+ *   concatenated axis. Used for bwd_dw's dY^T and X^T and, with equal groups, for the per-expert W^T of bwd_dx.
+ *   num_groups up to 1024.
  */
 int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld,
-                            const int64_t *group_offsets_dev, const int64_t *padded_offsets_dev,
-                            int32_t num_groups, int64_t red_total, int rht, uint32_t sign_mask, int rounding,
-                            uint64_t seed, uint32_t stream_id, void *codes_dev, int64_t code_panel_ld,
-                            float *scales_dev, int64_t scale_panel_ld, void *stream);
+                            const int64_t *group_offsets_dev, int32_t num_groups, int64_t red_total, int rht,
+                            uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                            void *stream);
 
 /*
  * ufp4_quantize_dual -- both quantized operands of one tensor from a single read of it (either grid):
@@ -217,14 +291,12 @@ int ufp4_quantize_grouped_t(int format, const void *x_dev, int64_t rows, int64_t
  *   x_dev              bf16 [rows, cols], leading dimension ld; rows % 16 == 0 and cols % 16 == 0.
  *   rht_rows, sign_mask_rows, stream_rows   RHT and SR stream of Q_r; *_cols the same for Q_c.
  *   rounding, seed     as ufp4_rht_quantize, for both outputs.
- *   codes_r_dev ... scale_panel_ld_r   Q_r in the panel layout (reduction cols); *_c: Q_c (reduction rows).
- * The two outputs must not overlap each other or the input.
+ *   out_rows, out_cols Q_r and Q_c. The two outputs must not overlap each other or the input.
  */
 int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int rht_rows,
                        uint32_t sign_mask_rows, uint32_t stream_rows, int rht_cols, uint32_t sign_mask_cols,
-                       uint32_t stream_cols, int rounding, uint64_t seed, void *codes_r_dev, int64_t code_panel_ld_r,
-                       float *scales_r_dev, int64_t scale_panel_ld_r, void *codes_c_dev, int64_t code_panel_ld_c,
-                       float *scales_c_dev, int64_t scale_panel_ld_c, void *stream);
+                       uint32_t stream_cols, int rounding, uint64_t seed, ufp4_qtensor *out_rows,
+                       ufp4_qtensor *out_cols, void *stream);
 
 /*
  * Power-of-two block scales. The paper leaves the scale hierarchy open (Sec. 4: single-level, two-level or
@@ -234,43 +306,37 @@ int ufp4_quantize_dual(int format, const void *x_dev, int64_t rows, int64_t cols
  * ufp4_mx_quantize -- fused RHT + quantization with power-of-two scales. Per 1x32 block along the reduction
  *   axis: y = RHT16 of each half as in ufp4_rht_quantize (or y = x); E = max(floor(log2 amax |y|) - 2, -127)
  *   (the OCP Microscaling shared-exponent rule, the levels read as FP6 E2M3 numbers; E8M0 stops at 2^-127);
- *   v = RN32(y * 2^-E) (|v| < 8);
- *   codes -7..7 by RTNE or SR (same rules and Philox draws, the counters numbering 16-blocks), |v| > 7
- *   clamped to the top level. Arguments as ufp4_rht_quantize, except:
- *     red % 32 == 0 (cols when transpose = 0, rows when transpose = 1);
+ *   v = RN32(y * 2^-E) (|v| < 8); codes -7..7 by RTNE or SR (same rules and Philox draws, the counters numbering
+ *   16-blocks), |v| > 7 clamped to the top level. Arguments as ufp4_rht_quantize, except:
+ *     red % 32 == 0 (cols when transpose = 0, rows when transpose = 1); out->format becomes
+ *     UFP4_FMT_UNIFORM_MX32;
  *     codes: FP6 E2M3 numbers (the integers -7..7 are exact), 32 per block in 24 bytes, element j in bits
  *            6j .. 6j + 5 of the block's little-endian 192-bit string;
- *     scales_dev: uint8 E8M0 bytes E + 127 (0 for an all-zero block).
+ *     scales: uint8 E8M0 bytes E + 127 (0 for an all-zero block).
  *   Layout (panels of 128 rows, 32-blocks): the 24 code bytes of block b of row 128p + i are three 8-byte
- *   units, unit u (bytes 8u .. 8u + 7 of the string) at codes_dev + p * code_panel_ld + b * 3072 + u * 1024
- *   + i * 8; its scale at scales_dev + p * scale_panel_ld + b * 128 + i. code_panel_ld >=
- *   3072 * red/32 and scale_panel_ld >= 128 * red/32, both multiples of 16; both pointers 16-byte aligned.
+ *   units, unit u (bytes 8u .. 8u + 7 of the string) at codes + p * code_panel_ld + b * 3072 + u * 1024
+ *   + i * 8; its scale at scales + p * scale_panel_ld + b * 128 + i. code_panel_ld >= 3072 * red/32 and
+ *   scale_panel_ld >= 128 * red/32, both multiples of 16; both pointers 16-byte aligned.
  *   Padding rows of the last panel are written as zero codes and scale byte 0. Rowwise operands of more than
  *   4194176 rows (32767 panels) return UFP4_ERR_UNSUPPORTED.
  */
 int ufp4_mx_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose, int rht,
-                     uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, void *codes_dev,
-                     int64_t code_panel_ld, void *scales_dev, int64_t scale_panel_ld, void *stream);
+                     uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                     void *stream);
 
 /*
- * ufp4_mx_gemm_fwd_y / _bwd_dx / _bwd_dw -- the three passes (shapes and operand roles as the ufp4_gemm_*
- *   calls below) on operands from ufp4_mx_quantize: C[i, j] = sum_k A[i,k] 2^(eA - 127) B[j,k] 2^(eB - 127)
- *   with the scales of each element's 32-block, accumulated in fp32 by the matrix core; output fp32 or bf16
- *   (RNE) with leading dimension ldc. K % 32 == 0. Outputs of 2^31 or more 128 x 128 tiles return
- *   UFP4_ERR_UNSUPPORTED.
+ * ufp4_mx_gemm_fwd_y / _bwd_dx / _bwd_dw -- the three passes (operand roles as the ufp4_gemm_* calls below) on
+ *   operands from ufp4_mx_quantize: C[i, j] = sum_k A[i,k] 2^(eA - 127) B[j,k] 2^(eB - 127) with the scales of
+ *   each element's 32-block, accumulated in fp32 by the matrix core; output fp32 or bf16 (RNE) with leading
+ *   dimension ldc. Outputs of 2^31 or more 128 x 128 tiles return UFP4_ERR_UNSUPPORTED; operands that are not
+ *   UFP4_FMT_UNIFORM_MX32 or differ in RHT block, signs or reduction length return UFP4_ERR_MISMATCH.
  */
-int ufp4_mx_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_panel_ld, const void *x_scales_dev,
-                       int64_t x_scale_panel_ld, const void *w_codes_dev, int64_t w_code_panel_ld,
-                       const void *w_scales_dev, int64_t w_scale_panel_ld, int64_t M, int64_t N, int64_t K, void *y_dev,
-                       int64_t ldc, int out_dtype, void *stream);
-int ufp4_mx_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_panel_ld, const void *dy_scales_dev,
-                        int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
-                        const void *wt_scales_dev, int64_t wt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
-                        void *dx_dev, int64_t ldc, int out_dtype, void *stream);
-int ufp4_mx_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const void *dyt_scales_dev,
-                        int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
-                        const void *xt_scales_dev, int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
-                        void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_mx_gemm_fwd_y(const ufp4_qtensor *x, const ufp4_qtensor *w, void *y_dev, int64_t ldc, int out_dtype,
+                       void *stream);
+int ufp4_mx_gemm_bwd_dx(const ufp4_qtensor *dy, const ufp4_qtensor *wt, void *dx_dev, int64_t ldc, int out_dtype,
+                        void *stream);
+int ufp4_mx_gemm_bwd_dw(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, void *dw_dev, int64_t ldc, int out_dtype,
+                        void *stream);
 
 /*
  * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that
@@ -280,53 +346,40 @@ int ufp4_mx_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, co
  *   ufp4_gemm_bwd_dx: dX [M, K] = Q(dY H')  [M, N] . Q(W^T H') [K, N]^T
  *   ufp4_gemm_bwd_dw: dW [N, K] = Q(dY^T H')[N, M] . Q(X^T H') [K, M]^T
  *
- * Arguments: (a_codes, a_scales) is the left operand, (b_codes, b_scales) the right one, each in the panel
- * layout with its panel strides (code_panel_ld bytes, scale_panel_ld floats); `format` is the grid both
- * operands were quantized to
- * (UFP4_FMT_UNIFORM or UFP4_FMT_E2M1); out_dtype UFP4_OUT_F32 or UFP4_OUT_BF16; out_dev row-major with
- * leading dimension ldc (elements). Both operands must come from quantizations with the same rht
- * setting and sign mask (the library cannot check this).
+ * The shapes come from the descriptors (output rows = left operand's rows, columns = right operand's rows).
+ * Both operands must be UFP4_FMT_UNIFORM or both UFP4_FMT_E2M1 with the same rht_block, sign words and
+ * reduction length, else UFP4_ERR_MISMATCH. out_dtype UFP4_OUT_F32 or UFP4_OUT_BF16; out_dev row-major with
+ * leading dimension ldc (elements).
  */
-int ufp4_gemm_fwd_y(const void *x_codes_dev, int64_t x_code_panel_ld, const float *x_scales_dev, int64_t x_scale_panel_ld,
-                    const void *w_codes_dev, int64_t w_code_panel_ld, const float *w_scales_dev, int64_t w_scale_panel_ld,
-                    int64_t M, int64_t N, int64_t K, int format, void *y_dev, int64_t ldc, int out_dtype,
+int ufp4_gemm_fwd_y(const ufp4_qtensor *x, const ufp4_qtensor *w, void *y_dev, int64_t ldc, int out_dtype,
                     void *stream);
-int ufp4_gemm_bwd_dx(const void *dy_codes_dev, int64_t dy_code_panel_ld, const float *dy_scales_dev,
-                     int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
-                     const float *wt_scales_dev, int64_t wt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
-                     int format, void *dx_dev, int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dw(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const float *dyt_scales_dev,
-                     int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
-                     const float *xt_scales_dev, int64_t xt_scale_panel_ld, int64_t M, int64_t N, int64_t K,
-                     int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dx(const ufp4_qtensor *dy, const ufp4_qtensor *wt, void *dx_dev, int64_t ldc, int out_dtype,
+                     void *stream);
+int ufp4_gemm_bwd_dw(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, void *dw_dev, int64_t ldc, int out_dtype,
+                     void *stream);
 
 /*
- * Grouped (MoE) forms: num_groups experts, token rows expert-contiguous.
+ * Grouped (MoE) forms: num_groups experts, token rows expert-contiguous, group_offsets_dev the int64 token
+ * offsets [num_groups + 1] on the device (0 = off_0 <= ... <= off_G).
  *
- *   fwd_y : Y_g  [m_g, N] = Qx[off_g:off_{g+1}, :K] . Qw[g*N:(g+1)*N, :K]^T        (Y  [M_total, N])
- *   bwd_dx: dX_g [m_g, K] = Qdy[off_g:off_{g+1}, :N] . Qwt[:K, g*N:(g+1)*N]^T       (dX [M_total, K])
- *           where Qwt [K, G*N] is the grouped-transposed quantization of W [G*N, K] with equal groups.
- *   bwd_dw: dW_g [N, K]  = Qdyt[:N, pad_g:pad_{g+1}] . Qxt[:K, pad_g:pad_{g+1}]^T   (dW [G, N, K])
+ *   fwd_y : Y_g  [m_g, N] = Qx[off_g:off_{g+1}, :K] . Qw[g*N:(g+1)*N, :K]^T         (Y  [M_total, N])
+ *           Qx [M_total, K]; Qw [G*N, K] (its rows a multiple of num_groups).
+ *   bwd_dx: dX_g [m_g, K] = Qdy[off_g:off_{g+1}, :N] . Qwt[:K, g*N:(g+1)*N]^T        (dX [M_total, K])
+ *           Qdy [M_total, N]; Qwt [K, G*N] is the grouped-transposed quantization of W [G*N, K] with equal
+ *           groups (its reduction length must be num_groups times Qdy's).
+ *   bwd_dw: dW_g [N, K]  = Qdyt[:N, pad_g:pad_{g+1}] . Qxt[:K, pad_g:pad_{g+1}]^T    (dW [G, N, K], each
+ *           [N, K] with leading dimension ldc, groups N * ldc apart). Qdyt [N, R], Qxt [K, R] from
+ *           ufp4_quantize_grouped_t on the same offsets; the padded offsets pad_g are computed on the device.
  *
- * group_offsets_dev / padded_offsets_dev as in ufp4_quantize_grouped_t; M_total = off_G; red_total = pad_G is
- * the reduction length of Qdyt and Qxt. Offsets are read on the device: rows past M_total and reduction
- * positions past red_total are ignored, groups with no tokens give dW_g = 0.
+ * Offsets are read on the device: rows past M_total and reduction positions past R are ignored, groups with
+ * no tokens give dW_g = 0. Operand checks as for the dense calls. num_groups up to 65535.
  */
-int ufp4_gemm_fwd_y_grouped(const void *x_codes_dev, int64_t x_code_panel_ld, const float *x_scales_dev,
-                            int64_t x_scale_panel_ld, const void *w_codes_dev, int64_t w_code_panel_ld,
-                            const float *w_scales_dev, int64_t w_scale_panel_ld, const int64_t *group_offsets_dev,
-                            int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format, void *y_dev,
-                            int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dx_grouped(const void *dy_codes_dev, int64_t dy_code_panel_ld, const float *dy_scales_dev,
-                             int64_t dy_scale_panel_ld, const void *wt_codes_dev, int64_t wt_code_panel_ld,
-                             const float *wt_scales_dev, int64_t wt_scale_panel_ld, const int64_t *group_offsets_dev,
-                             int32_t num_groups, int64_t M_total, int64_t N, int64_t K, int format,
-                             void *dx_dev, int64_t ldc, int out_dtype, void *stream);
-int ufp4_gemm_bwd_dw_grouped(const void *dyt_codes_dev, int64_t dyt_code_panel_ld, const float *dyt_scales_dev,
-                             int64_t dyt_scale_panel_ld, const void *xt_codes_dev, int64_t xt_code_panel_ld,
-                             const float *xt_scales_dev, int64_t xt_scale_panel_ld,
-                             const int64_t *padded_offsets_dev, int32_t num_groups, int64_t red_total, int64_t N,
-                             int64_t K, int format, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_fwd_y_grouped(const ufp4_qtensor *x, const ufp4_qtensor *w, const int64_t *group_offsets_dev,
+                            int32_t num_groups, void *y_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dx_grouped(const ufp4_qtensor *dy, const ufp4_qtensor *wt, const int64_t *group_offsets_dev,
+                             int32_t num_groups, void *dx_dev, int64_t ldc, int out_dtype, void *stream);
+int ufp4_gemm_bwd_dw_grouped(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, const int64_t *group_offsets_dev,
+                             int32_t num_groups, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
 
 #ifdef __cplusplus
 }

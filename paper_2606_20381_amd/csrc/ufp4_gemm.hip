@@ -87,9 +87,28 @@ struct TilePos {
 };
 __device__ __forceinline__ TilePos grid_pos() { return {(int64_t)blockIdx.x, (int64_t)blockIdx.y, (int)blockIdx.z}; }
 
+// Padded start of group g along a ragged-K reduction: sum over h < g of the token counts rounded up to multiples
+// of 16 (each group's tokens were zero-padded so; ufp4_quantize_grouped_t lays them out the same way). Wave 0
+// sums, the result goes through LDS; every thread of the workgroup must call this.
+__device__ int64_t padded_start(const int64_t* off, int g, int64_t* slot) {
+    const int tid = threadIdx.x;
+    if (tid < 64) {
+        int64_t sum = 0;
+        for (int h = tid; h < g; h += 64) {
+            const int64_t c = off[h + 1] - off[h];
+            sum += (c > 0 ? c + 15 : 0) / 16 * 16;
+        }
+#pragma unroll
+        for (int d = 32; d > 0; d >>= 1) sum += __shfl_xor(sum, d, 64);
+        if (tid == 0) *slot = sum;
+    }
+    __syncthreads();
+    return *slot;
+}
+
 // Resolve the workgroup's output tile (dense, ragged-M group or ragged-K group). Returns false when the
 // workgroup has nothing to do (a ragged-M tile index past the last group); all threads agree.
-__device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos, Tile& tl) {
+__device__ bool resolve_tile(const GemmJob& j, int32_t* grp, int64_t* pad, const TilePos& pos, Tile& tl) {
     const int64_t tn = pos.tn;
     if (j.mode == kGemmRaggedM) {
         int g;
@@ -119,8 +138,11 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, const TilePos& pos,
         if (j.mode == kGemmRaggedK) {
             const int g = pos.g;
             // the group's padded token range, clamped to the operands' reduction length
-            const int64_t p0 = j.offsets[g] < j.red_total ? j.offsets[g] : j.red_total;
-            const int64_t p1 = j.offsets[g + 1] < j.red_total ? j.offsets[g + 1] : j.red_total;
+            const int64_t c = j.offsets[g + 1] - j.offsets[g];
+            const int64_t q0 = padded_start(j.offsets, g, pad);
+            const int64_t q1 = q0 + (c > 0 ? c + 15 : 0) / 16 * 16;
+            const int64_t p0 = q0 < j.red_total ? q0 : j.red_total;
+            const int64_t p1 = q1 < j.red_total ? q1 : j.red_total;
             kb0 = p0 / 16;
             tl.nkb = p1 > p0 ? (p1 - p0) / 16 : 0;
             c_base = (int64_t)g * j.M * j.ldc;
@@ -214,6 +236,7 @@ struct alignas(16) GemmSmem2 {
     uint2 as[2][SKB2 * 2 * PL2];
     uint2 bs[2][SKB2 * 2 * PL2];
     int32_t grp[2];
+    int64_t pad;
 };
 
 template <int FMT>
@@ -271,7 +294,7 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     const int tid = threadIdx.x;
 
     Tile tl;
-    if (!resolve_tile(j, sm.grp, grid_pos(), tl)) return;
+    if (!resolve_tile(j, sm.grp, &sm.pad, grid_pos(), tl)) return;
     // the buffer resources below must live in SGPRs
     tl.a = uniform_ptr(tl.a);
     tl.b = uniform_ptr(tl.b);

@@ -37,8 +37,7 @@ struct QuantJob {
     int64_t xrows, ld;  // X rows and leading dimension (elements)
     int64_t qrows;      // rows of the quantized operand
     int64_t red;        // reduction length of the quantized operand (padded total when grouped)
-    const int64_t* group_off;   // grouped transposed only (device), else nullptr
-    const int64_t* group_poff;  // grouped transposed only (device)
+    const int64_t* group_off;   // grouped transposed only: token offsets [G+1] (device), else nullptr
     int32_t num_groups;
     QuantArgs qa;
     void* codes;
@@ -155,7 +154,7 @@ struct GemmJob {
     void* c;
     int64_t ldc;  // elements
     // grouped
-    const int64_t* offsets;  // ragged-M: token offsets [G+1]; ragged-K: padded offsets [G+1]
+    const int64_t* offsets;  // token offsets [G+1] (ragged-K pads each group's count to a multiple of 16)
     int32_t G;
     int64_t b_group_rows;  // ragged-M: B rows advanced per group (fwd_y: N)
     int64_t b_group_kb;    // ragged-M: B reduction blocks advanced per group (bwd_dx: N/16)

@@ -469,8 +469,7 @@ constexpr int kXC = 8;                     // columns (operand rows) per thread
 constexpr int kMaxGroupsLds = 1024;
 
 struct TGroups {
-    const int64_t* off;   // token offsets [G+1] (device), nullptr for a dense tensor
-    const int64_t* poff;  // padded offsets [G+1] (device)
+    const int64_t* off;  // token offsets [G+1] (device), nullptr for a dense tensor
     int32_t G;
 };
 
@@ -490,9 +489,33 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
     __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
     const int t = threadIdx.x;
     if constexpr (GROUPED) {
-        for (int g = t; g <= grp.G; g += 256) {
-            s_off[g] = grp.off[g];
-            s_poff[g] = grp.poff[g];
+        // token offsets, and the padded offsets: group lengths rounded up to multiples of 16, prefix-summed
+        // (thread t owns groups 4t .. 4t + 3; the 256 partial sums are scanned in place in s_poff)
+        for (int g = t; g <= grp.G; g += 256) s_off[g] = grp.off[g];
+        if (t == 0) s_poff[0] = 0;
+        __syncthreads();
+        int64_t part[4], run = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int g = 4 * t + k;
+            const int64_t c = g < grp.G ? s_off[g + 1] - s_off[g] : 0;
+            run += (c > 0 ? c + 15 : 0) / 16 * 16;
+            part[k] = run;
+        }
+        s_poff[t + 1] = run;
+        __syncthreads();
+        for (int d = 1; d < 256; d <<= 1) {  // inclusive scan of the 256 partial sums at s_poff[1 ..]
+            const int64_t o = t >= d ? s_poff[t + 1 - d] : 0;
+            __syncthreads();
+            s_poff[t + 1] += o;
+            __syncthreads();
+        }
+        const int64_t base = s_poff[t];  // exclusive prefix of thread t (s_poff[0] is 0)
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int g = 4 * t + k;
+            if (g < grp.G) s_poff[g + 1] = base + part[k];
         }
         __syncthreads();
     }
@@ -1200,7 +1223,7 @@ static hipError_t launch_cols_t(const QuantJob& j, hipStream_t s) {
     const int64_t gy = (nblk + XB - 1) / XB;
     if (prows == 0 || gy == 0) return hipSuccess;
     const dim3 grid((unsigned)((prows + XG * kXC - 1) / (XG * kXC)), (unsigned)(gy < 65535 ? gy : 65535));
-    TGroups grp{j.group_off, j.group_poff, j.num_groups};
+    TGroups grp{j.group_off, j.num_groups};
     quant_cols_kernel<FMT, ROUND, RHT, GROUPED, WIDE><<<grid, 256, 0, s>>>(
         static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, prows, j.ld, j.red, grp, j.qa,
         static_cast<uint8_t*>(j.codes), j.code_pld, j.scales, j.scale_pld);

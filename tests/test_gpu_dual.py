@@ -173,10 +173,8 @@ def test_dual_empty_and_invalid_calls():
     x = torch.zeros(32, 48, dtype=torch.bfloat16, device="cuda")
     qr, qc = U.empty_qtensor(32, 48), U.empty_qtensor(48, 32)
     qr.codes.fill_(0xAB)
-    args = lambda rows, cols, ld, rnd=0: (0, x.data_ptr(), rows, cols, ld, 1, 0, 0, 1, 0, 1, rnd, 0,
-                                          qr.codes.data_ptr(), qr.code_panel_ld, qr.scales.data_ptr(),
-                                          qr.scale_panel_ld, qc.codes.data_ptr(), qc.code_panel_ld,
-                                          qc.scales.data_ptr(), qc.scale_panel_ld, None)
+    args = lambda rows, cols, ld, rnd=0: (0, x.data_ptr(), rows, cols, ld, 1, 0, 0, 1, 0, 1, rnd, 0, qr.ref(),
+                                          qc.ref(), None)
     assert lib.ufp4_quantize_dual(*args(0, 48, 48)) == 0  # empty: nothing written
     assert lib.ufp4_quantize_dual(*args(32, 0, 48)) == 0
     torch.cuda.synchronize()
@@ -184,6 +182,8 @@ def test_dual_empty_and_invalid_calls():
     assert lib.ufp4_quantize_dual(*args(24, 48, 48)) == 2  # rows % 16
     assert lib.ufp4_quantize_dual(*args(32, 40, 48)) == 2  # cols % 16
     assert lib.ufp4_quantize_dual(*args(32, 48, 48, rnd=3)) == 1
+    assert lib.ufp4_quantize_dual(0, x.data_ptr(), 32, 48, 48, 1, 0, 0, 1, 0, 1, 0, 0, qr.ref(), qr.ref(),
+                                  None) == 1  # one descriptor for both outputs
 
 
 def test_dual_transposed_equals_equal_group_transpose():
@@ -192,11 +192,11 @@ def test_dual_transposed_equals_equal_group_transpose():
     E, N, K = 6, 176, 256
     g = torch.Generator().manual_seed(23)
     w = (torch.randn(E * N, K, generator=g) * 0.02).bfloat16().cuda()
-    eoff, epoff, ered = U.group_offsets([N] * E)
+    eoff, ered = U.group_offsets([N] * E)
     for fmt in (O.UNIFORM, O.E2M1):
         _, qc = U.quantize_dual(w, fmt=fmt, rht_rows=True, rht_cols=True, sign_mask_rows=0x3C3C,
                                 sign_mask_cols=0x3C3C)
-        qg = U.quantize_grouped_t(w, eoff, epoff, ered, fmt=fmt, rht=True, sign_mask=0x3C3C)
+        qg = U.quantize_grouped_t(w, eoff, ered, fmt=fmt, rht=True, sign_mask=0x3C3C)
         torch.cuda.synchronize()
         assert torch.equal(qc.codes, qg.codes)
         assert torch.equal(qc.scales.view(torch.int32), qg.scales.view(torch.int32))

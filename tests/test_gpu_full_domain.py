@@ -133,9 +133,9 @@ def test_grouped_transposed(fmt, rounding):
     a = _edge_rows()
     x = np.ascontiguousarray(a.T)  # tokens x channels: operand row c is a's row c
     counts = [5, 20, 0, 39]
-    off, poff, red = U.group_offsets(counts)
+    off, red = U.group_offsets(counts)
     print(f"full-domain grouped fmt={fmt} rnd={rounding}", flush=True)
-    q = U.quantize_grouped_t(_dev(x), off, poff, red, fmt=fmt, rht=True, sign_mask=0x6A09, rounding=rounding,
+    q = U.quantize_grouped_t(_dev(x), off, red, fmt=fmt, rht=True, sign_mask=0x6A09, rounding=rounding,
                              seed=24, stream_id=1)
     idx, sc, _ = P.oracle_operand_grouped(O.f32_to_bf16_bits(x), counts, fmt, rounding, True, 0x6A09, 24, 1)
     _check(q, idx, sc, fmt, "grouped transposed")

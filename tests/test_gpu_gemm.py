@@ -154,22 +154,21 @@ def _grouped_case(x, w, dy, counts, mask, seed, fmt=O.UNIFORM, rows_per_group=No
     E, N, K = w.shape
     w2 = w.reshape(E * N, K)
     xb, w2b, dyb = WL.bf16_bits(x), WL.bf16_bits(w2), WL.bf16_bits(dy)
-    off, poff, red_total = U.group_offsets(counts)
+    off, red_total = U.group_offsets(counts)
     offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
-    poffs = poff.cpu().numpy()
     xd, w2d, dyd = x.cuda(), w2.cuda(), dy.cuda()
     quant = U.rht_quantize if fmt == O.UNIFORM else U.e2m1_quantize
     xq = quant(xd, rht=True, sign_mask=mask)
     wq = quant(w2d, rht=True, sign_mask=mask)
     dyq = quant(dyd, rht=True, sign_mask=mask, rounding=U.SR, seed=seed, stream_id=0)
-    eq, epoff, ered = U.group_offsets([N] * E)
-    wtq = U.quantize_grouped_t(w2d, eq, epoff, ered, fmt=fmt, rht=True, sign_mask=mask)
-    dytq = U.quantize_grouped_t(dyd, off, poff, red_total, fmt=fmt, rht=True, sign_mask=mask, rounding=U.SR,
+    eq, ered = U.group_offsets([N] * E)
+    wtq = U.quantize_grouped_t(w2d, eq, ered, fmt=fmt, rht=True, sign_mask=mask)
+    dytq = U.quantize_grouped_t(dyd, off, red_total, fmt=fmt, rht=True, sign_mask=mask, rounding=U.SR,
                                 seed=seed, stream_id=1)
-    xtq = U.quantize_grouped_t(xd, off, poff, red_total, fmt=fmt, rht=True, sign_mask=mask)
-    y = U.gemm_fwd_y_grouped(xq, wq, off, N, out_dtype=out_dtype)
+    xtq = U.quantize_grouped_t(xd, off, red_total, fmt=fmt, rht=True, sign_mask=mask)
+    y = U.gemm_fwd_y_grouped(xq, wq, off, out_dtype=out_dtype)
     dx = U.gemm_bwd_dx_grouped(dyq, wtq, off, out_dtype=out_dtype)
-    dw = U.gemm_bwd_dw_grouped(dytq, xtq, poff, out_dtype=out_dtype)
+    dw = U.gemm_bwd_dw_grouped(dytq, xtq, off, out_dtype=out_dtype)
     torch.cuda.synchronize()
     tol = TOL[out_dtype]
     rng = rng or np.random.default_rng(0)
@@ -194,8 +193,9 @@ def _grouped_case(x, w, dy, counts, mask, seed, fmt=O.UNIFORM, rows_per_group=No
         err = P.rel_fro(dxn[np.ix_(rows, kc)], O.gemm_nt(ia, sa, it[:, sl], st[:, g * N // 16:(g + 1) * N // 16], fmt))
         assert err <= tol, ("bwd_dx", g, err)
     # bwd_dw: dW_g = Qdyt[nc, pad_g:pad_g+1] Qxt[kc, pad_g:pad_g+1]^T
-    ida, sda, _ = P.oracle_operand_grouped(dyb, counts, fmt, O.SR, True, mask, seed, 1, nc)
+    ida, sda, poffs = P.oracle_operand_grouped(dyb, counts, fmt, O.SR, True, mask, seed, 1, nc)
     ixa, sxa, _ = P.oracle_operand_grouped(xb, counts, fmt, O.RTNE, True, mask, seed, 0, kc)
+    assert poffs[-1] == red_total
     dwn = P.to_numpy(dw)
     for g in range(len(counts)):
         cs = slice(int(poffs[g]), int(poffs[g + 1]))

@@ -130,7 +130,8 @@ def test_panel_layout_padding_and_strides(fmt):
         nkb = red // 16
         codes = torch.full((2, nkb * 1024 + 96), 0xAB, dtype=torch.uint8, device="cuda")
         scales = torch.full((2, nkb * 128 + 12), -5.0, dtype=torch.float32, device="cuda")
-        q = U.QTensor(codes, scales, fmt, qrows, red)
+        q = U.QTensor(codes, scales, U.QDesc(codes=codes.data_ptr(), scales=scales.data_ptr(),
+                                             code_panel_ld=codes.stride(0), scale_panel_ld=scales.stride(0), panels=2))
         print(f"panel layout fmt={fmt} layout={layout}", flush=True)
         fn(src.cuda(), transpose=(layout == "cols"), rht=True, sign_mask=0x1111, rounding=O.RTNE, seed=1, out=q)
         torch.cuda.synchronize()
@@ -173,21 +174,19 @@ def test_empty_and_invalid_calls():
     x = torch.zeros(32, 32, dtype=torch.bfloat16, device="cuda")
     q = U.empty_qtensor(32, 32)
     s = torch.cuda.current_stream().cuda_stream
-    # empty tensor: no launch, OK
-    assert L.ufp4_rht_quantize(x.data_ptr(), 0, 32, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
-                               q.scales.data_ptr(), q.scale_panel_ld, s) == 0
+    call = lambda *a: L.ufp4_rht_quantize(*a, q.ref(), s)
+    # empty tensor: no launch, OK, and the descriptor records the empty operand
+    assert call(x.data_ptr(), 0, 32, 32, 0, 1, 0, 0, 0, 0) == 0
+    assert (q.rows, q.red, q.rht_block) == (0, 32, 16)
     # reduction length not a multiple of 16
-    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 24, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
-                               q.scales.data_ptr(), q.scale_panel_ld, s) == 2
-    # code panel stride too small
-    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 32, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), 8,
-                               q.scales.data_ptr(), q.scale_panel_ld, s) == 2
+    assert call(x.data_ptr(), 32, 24, 32, 0, 1, 0, 0, 0, 0) == 2
     # misaligned input
-    assert L.ufp4_rht_quantize(x.data_ptr() + 2, 32, 16, 32, 0, 1, 0, 0, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
-                               q.scales.data_ptr(), q.scale_panel_ld, s) == 3
+    assert call(x.data_ptr() + 2, 32, 16, 32, 0, 1, 0, 0, 0, 0) == 3
     # bad enum
-    assert L.ufp4_rht_quantize(x.data_ptr(), 32, 32, 32, 0, 1, 0, 7, 0, 0, q.codes.data_ptr(), q.code_panel_ld,
-                               q.scales.data_ptr(), q.scale_panel_ld, s) == 1
+    assert call(x.data_ptr(), 32, 32, 32, 0, 1, 0, 7, 0, 0) == 1
+    # code panel stride too small
+    q.desc.code_panel_ld = 8
+    assert call(x.data_ptr(), 32, 32, 32, 0, 1, 0, 0, 0, 0) == 2
     torch.cuda.synchronize()
 
 
@@ -250,8 +249,8 @@ def test_1gib_quantizer_tensor_sampled():
 
 def _check_grouped(t_cpu, counts, fmt, rounding, rht, mask, seed, stream, rows=None):
     bits = WL.bf16_bits(t_cpu)
-    off, poff, red_total = U.group_offsets(counts)
-    q = U.quantize_grouped_t(t_cpu.cuda(), off, poff, red_total, fmt=fmt, rht=rht, sign_mask=mask,
+    off, red_total = U.group_offsets(counts)
+    q = U.quantize_grouped_t(t_cpu.cuda(), off, red_total, fmt=fmt, rht=rht, sign_mask=mask,
                              rounding=rounding, seed=seed, stream_id=stream)
     gc, gs = P.gpu_rows(q, rows)
     idx, sc, po = P.oracle_operand_grouped(bits, counts, fmt, rounding, rht, mask, seed, stream, rows)

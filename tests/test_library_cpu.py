@@ -1,9 +1,13 @@
-"""CPU checks of the C ABI library: it loads, exports every function include/ufp4.h declares, and rejects
-bad arguments on the host before any GPU call (no compute runs here)."""
+"""CPU checks of the C ABI library: it loads, exports every function include/ufp4.h declares, computes its host-side
+arithmetic (layout sizes, grouped padding, Sec. 3.2 metrics), and rejects bad arguments -- including GEMM operands
+quantized differently -- on the host before any GPU call. Every call below either is host-only or fails validation,
+so nothing is launched."""
 
 import ctypes
+import math
 import os
 import re
+import struct
 
 import pytest
 
@@ -11,6 +15,8 @@ from paper_2606_20381_amd import ufp4 as U
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ufp4.h")
+
+OK, INVALID, SHAPE, ALIGN, MISMATCH, UNSUPPORTED = 0, 1, 2, 3, 4, 5
 
 
 def _declared():
@@ -29,8 +35,9 @@ def lib():
 def test_header_declares_the_boundary():
     names = _declared()
     for required in ("ufp4_rht_quantize", "ufp4_e2m1_quantize", "ufp4_gemm_fwd_y", "ufp4_gemm_bwd_dx",
-                     "ufp4_gemm_bwd_dw"):
+                     "ufp4_gemm_bwd_dw", "ufp4_qtensor_bytes", "ufp4_grouped_reduction", "ufp4_quant_metrics"):
         assert required in names
+    assert "UFP4_ERR_MISMATCH = 4" in open(HEADER).read()
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -43,120 +50,324 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings(lib):
     assert lib.ufp4_status_string(0) == b"ok"
     assert lib.ufp4_status_string(3).startswith(b"misaligned")
-    assert lib.ufp4_version() == b"0.1.0"
+    assert lib.ufp4_status_string(4).startswith(b"operands quantized differently")
+    assert lib.ufp4_version() == b"0.2.0"
 
 
 FAKE = 1 << 20  # a 1 MiB-aligned non-null address that is never dereferenced: every call below fails validation
 
 
-# panel strides for one and two 16-blocks of reduction
-C1, S1, C2, S2 = 1024, 128, 2048, 256
+def _desc(rows=16, red=32, fmt=U.UNIFORM, rht_block=16, mask=0, codes=FAKE, scales=FAKE, cld=None, sld=None,
+          panels=1):
+    """A descriptor as a quantizer would leave it (storage at FAKE, minimal strides unless given)."""
+    mx = fmt == U.UNIFORM_MX32
+    nkb = red // (32 if mx else 16)
+    d = U.QDesc(codes=codes, scales=scales, code_panel_ld=cld if cld is not None else max(16, nkb * (3072 if mx else 1024)),
+                scale_panel_ld=sld if sld is not None else max(16 if mx else 4, nkb * 128), panels=panels, rows=rows,
+                red=red, format=fmt, rht_block=rht_block)
+    for k in range(8):
+        d.sign_words[k] = (mask >> (16 * k)) & 0xFFFF if k < rht_block // 16 else 0
+    return d
 
 
-@pytest.mark.parametrize("args,status", [
-    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream_id, codes, code_panel_ld, scales,
-    #  scale_panel_ld)
-    ((None, 16, 16, 16, 0, 1, 0, 0, 0, 0, FAKE, C1, FAKE, S1), 1),          # null input
-    ((FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # cols % 16
-    ((FAKE, 24, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # transposed: rows % 16
-    ((FAKE, 16, 32, 30, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # ld < cols
-    ((FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 2),          # ld % 8
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C1, FAKE, S2), 2),          # code panel stride < 1024 nkb
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S1), 2),          # scale panel stride < 128 nkb
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2 + 8, FAKE, S2), 3),      # code panel stride % 16
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2 + 2), 3),      # scale panel stride % 4
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE + 8, C2, FAKE, S2), 3),      # codes alignment
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE + 4, S2), 3),      # scales alignment
-    ((FAKE + 2, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 3),      # input alignment
-    ((FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, C2, FAKE, S2), 1),          # rounding enum
-    ((FAKE, 16, 32, 32, 2, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 1),          # transpose flag
-    ((FAKE, 16, 32, 32, 0, 1, 0x10000, 0, 0, 0, FAKE, C2, FAKE, S2), 1),    # sign mask > 16 bits
-    ((FAKE, -1, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, S2), 1),          # negative size
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 1 << 30, FAKE, S2), 5),     # code panel stride > 2^29
-    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C2, FAKE, 1 << 28), 5),     # scale panel stride > 2^27
+R = ctypes.byref
+
+
+# ------------------------------------------------------------------------------------------------
+# host-side arithmetic
+# ------------------------------------------------------------------------------------------------
+
+def test_qtensor_bytes(lib):
+    p, c, s = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    cb, sb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.ufp4_qtensor_bytes(0, 200, 48, R(p), R(c), R(s), R(cb), R(sb)) == OK
+    # 200 rows -> 2 panels; 3 blocks of 16: 3 x 128 x 8 code bytes and 3 x 128 fp32 scales per panel
+    assert (p.value, c.value, s.value, cb.value, sb.value) == (2, 3072, 384, 6144, 3072)
+    assert lib.ufp4_qtensor_bytes(2, 129, 64, R(p), R(c), R(s), R(cb), R(sb)) == OK  # power-of-two scales
+    assert (p.value, c.value, s.value, cb.value, sb.value) == (2, 2 * 3072, 256, 12288, 512)
+    assert lib.ufp4_qtensor_bytes(0, 0, 0, R(p), R(c), R(s), None, None) == OK  # empty: one minimal panel
+    assert (p.value, c.value, s.value) == (1, 16, 4)
+    assert lib.ufp4_qtensor_bytes(0, 16, 24, None, None, None, None, None) == SHAPE
+    assert lib.ufp4_qtensor_bytes(2, 16, 48, None, None, None, None, None) == SHAPE
+    assert lib.ufp4_qtensor_bytes(3, 16, 32, None, None, None, None, None) == INVALID
+    assert lib.ufp4_qtensor_bytes(0, -1, 32, None, None, None, None, None) == INVALID
+
+
+def _grouped(lib, offsets):
+    arr = (ctypes.c_int64 * len(offsets))(*offsets)
+    pad = (ctypes.c_int64 * len(offsets))()
+    red = ctypes.c_int64()
+    st = lib.ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(offsets) - 1,
+                                    ctypes.cast(pad, ctypes.c_void_p), R(red))
+    return st, list(pad), red.value
+
+
+def test_grouped_reduction(lib):
+    # counts 0, 1, 16, 17, 33: each rounded up to a multiple of 16 (Sec. 2.2 needs whole RHT blocks per group)
+    st, pad, red = _grouped(lib, [0, 0, 1, 17, 34, 67])
+    assert st == OK and pad == [0, 0, 16, 32, 64, 112] and red == 112
+    assert _grouped(lib, [0, 5, 3])[0] == INVALID      # decreasing offsets
+    assert _grouped(lib, [2, 5])[0] == INVALID         # first offset not 0
+    assert lib.ufp4_grouped_reduction(None, 1, None, None) == INVALID
+
+
+def _metrics(lib, err2, ref2, cross, hist, fmt=0, max_fpx=0.0):
+    rec = ctypes.create_string_buffer(struct.pack("<3d8Q", err2, ref2, cross, *hist), 88)
+    m = U.Metrics()
+    assert lib.ufp4_quant_metrics(rec, fmt, max_fpx, R(m)) == OK
+    return m
+
+
+def test_quant_metrics_closed_forms(lib):
+    m = _metrics(lib, 1.0, 100.0, 99.0, [10, 10, 10, 10, 10, 10, 10, 10])
+    assert m.nmse == 0.01 and m.sqnr_db == pytest.approx(20.0) and m.alpha == 0.99
+    assert m.beff == pytest.approx(1.0, abs=1e-9)  # all 8 buckets equally used
+    m = _metrics(lib, 0.0, 4.0, 4.0, [5, 0, 0, 0, 0, 0, 0, 3])
+    assert m.sqnr_db == math.inf and m.alpha == 1.0
+    p = [5 / 8, 3 / 8]
+    assert m.entropy == pytest.approx(-sum(q * math.log(q + 1e-12) for q in p))
+    assert m.beff == pytest.approx(math.exp(m.entropy) / 8)
+    # E2M1 cut at 2 has K = 5 levels (0, .5, 1, 1.5, 2): the sixth bucket and up are not counted
+    m = _metrics(lib, 1.0, 2.0, 1.0, [1, 1, 1, 1, 1, 7, 7, 7], fmt=1, max_fpx=2.0)
+    assert m.beff == pytest.approx(1.0, abs=1e-9)
+    m = _metrics(lib, 0.0, 0.0, 0.0, [0] * 8)  # an all-zero operand
+    assert math.isnan(m.nmse) and math.isnan(m.alpha)
+    raw, rot = _metrics(lib, 2.0, 100.0, 99.0, [1] * 8), _metrics(lib, 1.0, 100.0, 98.0, [1] * 8)
+    out = ctypes.c_double()
+    assert lib.ufp4_rotation_gain(R(raw), R(rot), R(out)) == OK
+    assert out.value == pytest.approx(10 * math.log10(2.0))
+    assert lib.ufp4_gemm_attenuation(R(raw), R(rot), R(out)) == OK
+    assert out.value == pytest.approx(0.99 * 0.98)
+    rec = ctypes.create_string_buffer(88)
+    assert lib.ufp4_quant_metrics(rec, 0, 4.0, R(U.Metrics())) == INVALID  # max_fpx on the uniform grid
+    assert lib.ufp4_quant_metrics(None, 0, 0.0, R(U.Metrics())) == INVALID
+
+
+# ------------------------------------------------------------------------------------------------
+# quantizer validation
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("args,dkw,status", [
+    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream_id), descriptor storage
+    ((None, 16, 16, 16, 0, 1, 0, 0, 0, 0), {}, INVALID),            # null input
+    ((FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0), {}, SHAPE),              # cols % 16
+    ((FAKE, 24, 16, 16, 1, 1, 0, 0, 0, 0), {}, SHAPE),              # transposed: rows % 16
+    ((FAKE, 16, 32, 30, 0, 1, 0, 0, 0, 0), {}, SHAPE),              # ld < cols
+    ((FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0), {}, SHAPE),              # ld % 8
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(cld=1024), SHAPE),  # code panel stride < 1024 nkb
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(sld=128), SHAPE),   # scale panel stride < 128 nkb
+    ((FAKE, 200, 32, 32, 0, 1, 0, 0, 0, 0), dict(panels=1), SHAPE),  # 200 rows need 2 panels
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(cld=2048 + 8), ALIGN),  # code panel stride % 16
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(sld=256 + 2), ALIGN),   # scale panel stride % 4
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(codes=FAKE + 8), ALIGN),  # codes alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(scales=FAKE + 4), ALIGN),  # scales alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(codes=None), INVALID),  # no code buffer
+    ((FAKE + 2, 16, 32, 32, 0, 1, 0, 0, 0, 0), {}, ALIGN),          # input alignment
+    ((FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0), {}, INVALID),            # rounding enum
+    ((FAKE, 16, 32, 32, 2, 1, 0, 0, 0, 0), {}, INVALID),            # transpose flag
+    ((FAKE, 16, 32, 32, 0, 1, 0x10000, 0, 0, 0), {}, INVALID),      # sign mask > 16 bits
+    ((FAKE, -1, 32, 32, 0, 1, 0, 0, 0, 0), {}, INVALID),            # negative size
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(cld=1 << 30), UNSUPPORTED),  # code panel stride > 2^29
+    ((FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0), dict(sld=1 << 28), UNSUPPORTED),  # scale panel stride > 2^27
 ])
-def test_quantize_validation(lib, args, status):
+def test_quantize_validation(lib, args, dkw, status):
     for fn in (lib.ufp4_rht_quantize, lib.ufp4_e2m1_quantize):
-        assert fn(*args, None) == status
+        d = _desc(rows=0, red=0, **dkw)
+        d.code_panel_ld = dkw.get("cld", 2048)
+        d.scale_panel_ld = dkw.get("sld", 256)
+        assert fn(*args, R(d), None) == status
+    assert lib.ufp4_rht_quantize(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, None, None) == INVALID  # no descriptor
 
 
-@pytest.mark.parametrize("args,status", [
-    # (a, a_panel_ld, as, as_panel_ld, b, b_panel_ld, bs, bs_panel_ld, M, N, K, fmt, c, ldc, out)
-    ((None, C1, FAKE, S1, FAKE, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 1),
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 24, 0, FAKE, 16, 0), 2),      # K % 16
-    ((FAKE, C1, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 0), 2),      # A panel stride < 1024 K/16
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S1, 16, 16, 32, 0, FAKE, 16, 0), 2),      # B scale stride < 128 K/16
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 8, 0), 2),       # ldc < N
-    ((FAKE, C1 + 8, FAKE, S1, FAKE, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 3),  # A panel stride % 16
-    ((FAKE, C1, FAKE, S1, FAKE + 4, C1, FAKE, S1, 16, 16, 16, 0, FAKE, 16, 0), 3),  # B codes alignment
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 3, FAKE, 16, 0), 1),      # format enum
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 5), 1),      # out dtype enum
-    ((FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 16, 32, 0, FAKE + 1, 16, 0), 3),  # output alignment
-    ((FAKE, C2, FAKE, S2, FAKE, 1 << 30, FAKE, S2, 16, 16, 32, 0, FAKE, 16, 0), 5), # B panel stride > 2^29
-])
-def test_gemm_validation(lib, args, status):
-    # the dense entry points map (M, N, K) onto (rows_a, rows_b, reduction) differently; pick the layout each
-    # expects so the same failure shows up
-    assert lib.ufp4_gemm_fwd_y(*args, None) == status
-
-
-def test_gemm_validation_per_pass_layout(lib):
-    # bwd_dx: dY [M, N] . Wt [K, N]^T -> dX [M, K]; the reduction is N
-    assert lib.ufp4_gemm_bwd_dx(FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 16, 24, 16, 0, FAKE, 16, 0, None) == 2
-    # bwd_dw: dYt [N, M] . Xt [K, M]^T -> dW [N, K]; the reduction is M
-    assert lib.ufp4_gemm_bwd_dw(FAKE, C2, FAKE, S2, FAKE, C2, FAKE, S2, 24, 16, 16, 0, FAKE, 16, 0, None) == 2
-
-
-def _dual_args(rows=32, cols=48, ld=48, fmt=0, rht_r=1, mask_r=0, rht_c=1, mask_c=0, rnd=0, x=FAKE, cr=FAKE,
-               cr_ld=3 * 1024, sr=FAKE, sr_ld=3 * 128, cc=FAKE, cc_ld=2 * 1024, sc=FAKE, sc_ld=2 * 128):
-    # (fmt, x, rows, cols, ld, rht_r, mask_r, stream_r, rht_c, mask_c, stream_c, rounding, seed,
-    #  codes_r, code_panel_ld_r, scales_r, scale_panel_ld_r, codes_c, ..., stream)
-    return (fmt, x, rows, cols, ld, rht_r, mask_r, 0, rht_c, mask_c, 1, rnd, 0, cr, cr_ld, sr, sr_ld, cc, cc_ld, sc,
-            sc_ld, None)
+def _dual(lib, rows=32, cols=48, ld=48, fmt=0, rht_r=1, mask_r=0, rht_c=1, mask_c=0, rnd=0, x=FAKE, dr=None, dc=None):
+    dr = dr or _desc(cld=3 * 1024, sld=3 * 128)
+    dc = dc or _desc(cld=2 * 1024, sld=2 * 128)
+    return lib.ufp4_quantize_dual(fmt, x, rows, cols, ld, rht_r, mask_r, 0, rht_c, mask_c, 1, rnd, 0, R(dr), R(dc),
+                                  None)
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(x=None), 1),                          # null input
-    (dict(cc=None), 1),                         # null transposed codes
-    (dict(fmt=2), 1),                           # format enum
-    (dict(rnd=2), 1),                           # rounding enum
-    (dict(rht_c=3), 1),                         # rht flag
-    (dict(mask_r=0x10000), 1),                  # sign mask > 16 bits
-    (dict(rows=-16), 1),                        # negative size
-    (dict(rows=24), 2),                         # rows % 16 (the transposed output's reduction)
-    (dict(cols=40, ld=40), 2),                  # cols % 16 (the rowwise output's reduction)
-    (dict(ld=40), 2),                           # ld < cols
-    (dict(ld=52), 2),                           # ld % 8
-    (dict(cr_ld=2 * 1024), 2),                  # rowwise code panel stride < 1024 cols/16
-    (dict(sc_ld=128), 2),                       # transposed scale panel stride < 128 rows/16
-    (dict(cc_ld=2 * 1024 + 8), 3),              # panel stride % 16
-    (dict(x=FAKE + 2), 3),                      # input alignment
-    (dict(sr=FAKE + 4), 3),                     # scales alignment
-    (dict(cc_ld=1 << 30), 5),                   # panel stride > 2^29
+    (dict(x=None), INVALID),                                # null input
+    (dict(dc=_desc(codes=None)), INVALID),                  # null transposed codes
+    (dict(fmt=2), INVALID),                                 # format enum
+    (dict(rnd=2), INVALID),                                 # rounding enum
+    (dict(rht_c=3), INVALID),                               # rht flag
+    (dict(mask_r=0x10000), INVALID),                        # sign mask > 16 bits
+    (dict(rows=-16), INVALID),                              # negative size
+    (dict(rows=24), SHAPE),                                 # rows % 16 (the transposed output's reduction)
+    (dict(cols=40, ld=40), SHAPE),                          # cols % 16 (the rowwise output's reduction)
+    (dict(ld=40), SHAPE),                                   # ld < cols
+    (dict(ld=52), SHAPE),                                   # ld % 8
+    (dict(dr=_desc(cld=2 * 1024, sld=3 * 128)), SHAPE),     # rowwise code panel stride < 1024 cols/16
+    (dict(dc=_desc(cld=2 * 1024, sld=128)), SHAPE),         # transposed scale panel stride < 128 rows/16
+    (dict(dc=_desc(cld=2 * 1024 + 8, sld=256)), ALIGN),     # panel stride % 16
+    (dict(x=FAKE + 2), ALIGN),                              # input alignment
+    (dict(dr=_desc(scales=FAKE + 4, cld=3 * 1024, sld=3 * 128)), ALIGN),  # scales alignment
+    (dict(dc=_desc(cld=1 << 30, sld=256)), UNSUPPORTED),    # panel stride > 2^29
 ])
 def test_dual_validation(lib, kw, status):
-    assert lib.ufp4_quantize_dual(*_dual_args(**kw)) == status
+    assert _dual(lib, **kw) == status
 
 
-def test_grouped_validation(lib):
-    # null offsets
-    assert lib.ufp4_quantize_grouped_t(0, FAKE, 32, 16, 16, None, FAKE, 2, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
-                                       None) == 1
-    # too many groups for one launch
-    assert lib.ufp4_quantize_grouped_t(0, FAKE, 32, 16, 16, FAKE, FAKE, 5000, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
-                                       None) == 5
-    # padded total smaller than the rows
-    assert lib.ufp4_quantize_grouped_t(0, FAKE, 64, 16, 16, FAKE, FAKE, 2, 32, 1, 0, 0, 0, 0, FAKE, 16, FAKE, 2,
-                                       None) == 2
-    assert lib.ufp4_gemm_fwd_y_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, None, 2, 16, 16, 16, 0, FAKE, 16, 0,
-                                       None) == 1
-    assert lib.ufp4_gemm_bwd_dx_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, FAKE, 0, 16, 16, 16, 0, FAKE, 16, 0,
-                                        None) == 1
-    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, 8, FAKE, 1, FAKE, 8, FAKE, 1, FAKE, 2, 32, 16, 16, 3, FAKE, 16, 0,
-                                        None) == 1
-    # red_total wider than the operands' panels
-    assert lib.ufp4_gemm_bwd_dw_grouped(FAKE, C1, FAKE, S1, FAKE, C1, FAKE, S1, FAKE, 2, 32, 16, 16, 0, FAKE, 16,
-                                        0, None) == 2
+def test_grouped_quantizer_validation(lib):
+    d = _desc(cld=2 * 1024, sld=2 * 128)
+    q = lib.ufp4_quantize_grouped_t
+    # (format, x, rows, cols, ld, offsets, G, red_total, rht, mask, rounding, seed, stream, out)
+    assert q(0, FAKE, 32, 16, 16, None, 2, 32, 1, 0, 0, 0, 0, R(d), None) == INVALID      # null offsets
+    assert q(0, FAKE, 32, 16, 16, FAKE, 5000, 32, 1, 0, 0, 0, 0, R(d), None) == UNSUPPORTED  # too many groups
+    assert q(0, FAKE, 64, 16, 16, FAKE, 2, 32, 1, 0, 0, 0, 0, R(d), None) == SHAPE         # red_total < rows
+    assert q(0, FAKE, 32, 16, 16, FAKE, 2, 48, 1, 0, 0, 0, 0, R(d), None) == SHAPE         # 3 blocks, room for 2
+
+
+def test_mx_quantizer_validation(lib):
+    C32, S32 = 3072, 128  # panel strides for one 32-block
+    q = lib.ufp4_mx_quantize
+
+    def d(cld=2 * C32, sld=2 * S32, **kw):
+        return R(_desc(fmt=U.UNIFORM_MX32, cld=cld, sld=sld, **kw))
+
+    assert q(FAKE, 16, 48, 48, 0, 1, 0, 0, 0, 0, d(), None) == SHAPE             # cols % 32
+    assert q(FAKE, 48, 16, 16, 1, 1, 0, 0, 0, 0, d(), None) == SHAPE             # transposed: rows % 32
+    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, d(cld=C32), None) == SHAPE      # code stride < 3072 nkb
+    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, d(sld=S32), None) == SHAPE      # scale stride < 128 nkb
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, d(sld=S32 + 4), None) == ALIGN  # scale stride % 16
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, d(scales=FAKE + 8), None) == ALIGN  # scales alignment
+    assert q(None, 16, 32, 32, 0, 1, 0, 0, 0, 0, d(), None) == INVALID           # null input
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, d(), None) == INVALID           # rounding enum
+    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, d(cld=1 << 30), None) == UNSUPPORTED  # stride > 2^29
+
+
+def test_quant_stats_validation(lib):
+    """ufp4_quant_stats(format, max_fpx, x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, rec)"""
+    ok = (0, 0.0, FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE)
+    cases = [
+        ((0, 4.0) + ok[2:], INVALID),            # max_fpx on the uniform grid
+        ((1, 3.0) + ok[2:], INVALID),            # max_fpx not in {2, 4, 6}
+        ((2,) + ok[1:], INVALID),                # format enum
+        (ok[:2] + (None,) + ok[3:], INVALID),    # null input
+        (ok[:12] + (None,), INVALID),            # null record
+        (ok[:12] + (FAKE + 4,), ALIGN),          # record alignment
+        (ok[:4] + (24, 24) + ok[6:], SHAPE),     # cols % 16
+        (ok[:5] + (30,) + ok[6:], SHAPE),        # ld < cols
+        (ok[:6] + (2,) + ok[7:], INVALID),       # transpose flag
+        (ok[:9] + (2,) + ok[10:], INVALID),      # rounding enum
+    ]
+    for args, status in cases:
+        assert lib.ufp4_quant_stats(*args, None) == status, args
+
+
+def test_e2m1_range_validation(lib):
+    args = (FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0)
+    for mf in (0.0, 1.0, 3.0, 7.0):
+        assert lib.ufp4_e2m1_quantize_range(*args, mf, R(_desc(fmt=1)), None) == INVALID
+    assert lib.ufp4_e2m1_quantize_range(FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, 4.0, R(_desc(fmt=1)), None) == SHAPE
+
+
+def test_unfused_validation(lib):
+    # ufp4_rht(x, rows, cols, ld, mask, y, ldy, stream)
+    assert lib.ufp4_rht(None, 16, 32, 32, 0, FAKE, 32, None) == INVALID
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0x10000, FAKE, 32, None) == INVALID
+    assert lib.ufp4_rht(FAKE, 16, 24, 24, 0, FAKE, 24, None) == SHAPE      # cols % 16
+    assert lib.ufp4_rht(FAKE, 16, 32, 36, 0, FAKE, 32, None) == SHAPE      # ld % 8
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 30, None) == SHAPE      # ldy < cols
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 34, None) == SHAPE      # ldy % 4
+    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE + 4, 32, None) == ALIGN  # y alignment
+    # ufp4_quantize_f32(format, x, rows, cols, ld, rht, mask, rounding, seed, stream, out, stream)
+    f = lib.ufp4_quantize_f32
+    assert f(2, FAKE, 16, 32, 32, 0, 0, 0, 0, 0, R(_desc()), None) == INVALID     # format
+    assert f(0, FAKE, 16, 32, 32, 0, 0, 2, 0, 0, R(_desc()), None) == INVALID     # rounding
+    assert f(0, FAKE, 16, 32, 32, 2, 0, 0, 0, 0, R(_desc()), None) == INVALID     # rht flag
+    assert f(0, FAKE, 16, 24, 24, 0, 0, 0, 0, 0, R(_desc()), None) == SHAPE       # cols % 16
+    assert f(0, FAKE, 16, 32, 34, 0, 0, 0, 0, 0, R(_desc()), None) == SHAPE       # ld % 4
+    assert f(0, FAKE + 8, 16, 32, 32, 0, 0, 0, 0, 0, R(_desc()), None) == ALIGN   # input alignment
+    assert f(0, FAKE, 16, 32, 32, 0, 0, 0, 0, 0, R(_desc(cld=1024)), None) == SHAPE  # code panel stride
+
+
+def test_rht_block_validation(lib):
+    words = (ctypes.c_uint16 * 8)()
+    w = ctypes.cast(words, ctypes.c_void_p)
+    base = (0, FAKE, 16, 128, 128, 0)
+    d = R(_desc(red=128))
+    assert lib.ufp4_quantize_rht_block(*base, 48, w, 0, 0, 0, d, None) == INVALID          # block size
+    assert lib.ufp4_quantize_rht_block(*base, 32, None, 0, 0, 0, d, None) == INVALID       # no sign words
+    assert lib.ufp4_quantize_rht_block(2, *base[1:], 32, w, 0, 0, 0, d, None) == INVALID   # format
+    assert lib.ufp4_quantize_rht_block(0, FAKE, 16, 96, 96, 0, 64, w, 0, 0, 0, R(_desc(red=96)), None) == SHAPE  # 96 % 64
+
+
+# ------------------------------------------------------------------------------------------------
+# GEMM validation: operands and output
+# ------------------------------------------------------------------------------------------------
+
+GEMMS = ("ufp4_gemm_fwd_y", "ufp4_gemm_bwd_dx", "ufp4_gemm_bwd_dw")
+
+
+@pytest.mark.parametrize("name", GEMMS)
+@pytest.mark.parametrize("a,b,status", [
+    (dict(), dict(fmt=U.E2M1), MISMATCH),                      # grids differ
+    (dict(rht_block=16), dict(rht_block=0), MISMATCH),         # one operand rotated, the other not
+    (dict(mask=0x1234), dict(mask=0x1235), MISMATCH),          # different signs: different H'
+    (dict(rht_block=32, mask=0x1), dict(rht_block=32, mask=0x10001), MISMATCH),  # second word of the signs
+    (dict(rht_block=16, mask=0x1), dict(rht_block=32, mask=0x1), MISMATCH),      # different RHT blocks
+    (dict(red=32), dict(red=48, cld=3072, sld=384), MISMATCH),  # reduction lengths differ
+    (dict(fmt=U.UNIFORM_MX32), dict(fmt=U.UNIFORM_MX32), MISMATCH),  # power-of-two scales: the mx calls
+    (dict(fmt=7), dict(fmt=7), INVALID),                       # unknown format
+    (dict(rht_block=24), dict(rht_block=24), INVALID),         # unknown RHT block
+    (dict(codes=None), dict(), INVALID),                       # no codes
+    (dict(rows=200), dict(), SHAPE),                           # 200 rows in one panel
+    (dict(cld=1024), dict(), SHAPE),                           # code stride < 1024 nkb
+    (dict(), dict(scales=FAKE + 4), ALIGN),                    # scales alignment
+    (dict(), dict(cld=1 << 30), UNSUPPORTED),                  # panel stride > 2^29
+])
+def test_gemm_operand_checks(lib, name, a, b, status):
+    assert getattr(lib, name)(R(_desc(**a)), R(_desc(**b)), FAKE, 16, 0, None) == status
+
+
+@pytest.mark.parametrize("name", GEMMS)
+def test_gemm_signs_ignored_without_rht(lib, name):
+    """With no RHT the sign words carry nothing: operands that differ only there pass the operand checks (the
+    output check after them fails here, so nothing is launched)."""
+    a, b = _desc(rht_block=0), _desc(rht_block=0)
+    a.sign_words[0], b.sign_words[0] = 1, 2
+    assert getattr(lib, name)(R(a), R(b), FAKE, 8, 0, None) == SHAPE
+
+
+@pytest.mark.parametrize("name", GEMMS)
+def test_gemm_output_checks(lib, name):
+    f = getattr(lib, name)
+    assert f(R(_desc()), R(_desc()), None, 16, 0, None) == INVALID        # no output
+    assert f(R(_desc()), R(_desc()), FAKE, 8, 0, None) == SHAPE           # ldc < N
+    assert f(R(_desc()), R(_desc()), FAKE + 1, 16, 0, None) == ALIGN      # output alignment
+    assert f(R(_desc()), R(_desc()), FAKE, 16, 5, None) == INVALID        # out dtype enum
+    assert f(None, R(_desc()), FAKE, 16, 0, None) == INVALID              # no operand
+
+
+def test_mx_gemm_operand_checks(lib):
+    mx = dict(fmt=U.UNIFORM_MX32)
+    g = lib.ufp4_mx_gemm_fwd_y
+    assert g(R(_desc()), R(_desc()), FAKE, 16, 0, None) == MISMATCH                     # 1x16 operands
+    assert g(R(_desc(**mx)), R(_desc(red=64, **mx)), FAKE, 16, 0, None) == MISMATCH     # reductions differ
+    assert g(R(_desc(mask=3, **mx)), R(_desc(mask=5, **mx)), FAKE, 16, 0, None) == MISMATCH
+    assert g(R(_desc(**mx)), R(_desc(**mx)), FAKE, 8, 0, None) == SHAPE                 # ldc < N
+    assert g(R(_desc(**mx)), R(_desc(**mx)), FAKE, 16, 4, None) == INVALID              # out dtype
+    assert g(R(_desc(red=48, **mx)), R(_desc(red=48, **mx)), FAKE, 16, 0, None) == SHAPE  # K % 32
+    for name in ("ufp4_mx_gemm_bwd_dx", "ufp4_mx_gemm_bwd_dw"):
+        assert getattr(lib, name)(R(_desc()), R(_desc(**mx)), FAKE, 16, 0, None) == MISMATCH
+
+
+def test_grouped_gemm_checks(lib):
+    fy, fx, fw = lib.ufp4_gemm_fwd_y_grouped, lib.ufp4_gemm_bwd_dx_grouped, lib.ufp4_gemm_bwd_dw_grouped
+    # (a, b, offsets, G, c, ldc, out, stream)
+    for f in (fy, fx, fw):
+        assert f(R(_desc()), R(_desc()), None, 2, FAKE, 16, 0, None) == INVALID          # null offsets
+        assert f(R(_desc()), R(_desc()), FAKE, 0, FAKE, 16, 0, None) == INVALID          # no groups
+        assert f(R(_desc()), R(_desc(fmt=1)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH    # grids differ
+        assert f(R(_desc(mask=1)), R(_desc(mask=2)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fy(R(_desc()), R(_desc(rows=15)), FAKE, 2, FAKE, 16, 0, None) == SHAPE        # 15 rows of W in 2 groups
+    assert fy(R(_desc()), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH  # K differs
+    # bwd_dx: W^T's reduction must be G times dY's
+    assert fx(R(_desc(red=32)), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fw(R(_desc()), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fw(R(_desc()), R(_desc()), FAKE, 70000, FAKE, 16, 0, None) == UNSUPPORTED     # groups > 65535
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
@@ -166,84 +377,10 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
         U.lib()
 
 
-def test_mx_validation(lib):
-    # (x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, codes, code_pld, scales, scale_pld)
-    C32, S32 = 3072, 128  # panel strides for one 32-block
-    q = lib.ufp4_mx_quantize
-    assert q(FAKE, 16, 48, 48, 0, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, 2 * S32, None) == 2   # cols % 32
-    assert q(FAKE, 48, 16, 16, 1, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, 2 * S32, None) == 2   # transposed: rows % 32
-    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, 2 * S32, None) == 2       # code stride < 3072 nkb
-    assert q(FAKE, 16, 64, 64, 0, 1, 0, 0, 0, 0, FAKE, 2 * C32, FAKE, S32, None) == 2       # scale stride < 128 nkb
-    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, S32 + 4, None) == 3       # scale stride % 16
-    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE + 8, S32, None) == 3       # scales alignment
-    assert q(None, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, C32, FAKE, S32, None) == 1           # null input
-    assert q(FAKE, 16, 32, 32, 0, 1, 0, 2, 0, 0, FAKE, C32, FAKE, S32, None) == 1           # rounding enum
-    assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE, 1 << 30, FAKE, S32, None) == 5       # stride > 2^29
-    g = lib.ufp4_mx_gemm_fwd_y
-    # (a, a_pld, as, as_pld, b, b_pld, bs, bs_pld, M, N, K, c, ldc, out)
-    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 48, FAKE, 16, 0, None) == 2  # K % 32
-    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 64, FAKE, 16, 0, None) == 2  # strides < 2 blocks
-    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 8, 0, None) == 2   # ldc < N
-    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 16, 4, None) == 1  # out dtype
-    assert g(None, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE, 16, 0, None) == 1  # null operand
-    assert g(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 16, 32, FAKE + 2, 16, 0, None) == 3  # out alignment
-    assert lib.ufp4_mx_gemm_bwd_dx(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 16, 48, 16, FAKE, 16, 0,
-                                   None) == 2  # reduction N % 32
-    assert lib.ufp4_mx_gemm_bwd_dw(FAKE, C32, FAKE, S32, FAKE, C32, FAKE, S32, 48, 16, 16, FAKE, 16, 0,
-                                   None) == 2  # reduction M % 32
-
-
-def test_quant_stats_validation(lib):
-    """ufp4_quant_stats(format, max_fpx, x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, rec)"""
-    ok = (0, 0.0, FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE)
-    cases = [
-        ((0, 4.0) + ok[2:], 1),                  # max_fpx on the uniform grid
-        ((1, 3.0) + ok[2:], 1),                  # max_fpx not in {2, 4, 6}
-        ((2,) + ok[1:], 1),                      # format enum
-        (ok[:2] + (None,) + ok[3:], 1),          # null input
-        (ok[:12] + (None,), 1),                  # null record
-        (ok[:12] + (FAKE + 4,), 3),              # record alignment
-        (ok[:4] + (24, 24) + ok[6:], 2),         # cols % 16
-        (ok[:5] + (30,) + ok[6:], 2),            # ld < cols
-        (ok[:6] + (2,) + ok[7:], 1),             # transpose flag
-        (ok[:9] + (2,) + ok[10:], 1),            # rounding enum
-    ]
-    for args, status in cases:
-        assert lib.ufp4_quant_stats(*args, None) == status, args
-
-
-def test_e2m1_range_validation(lib):
-    args = (FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0)
-    for mf in (0.0, 1.0, 3.0, 7.0):
-        assert lib.ufp4_e2m1_quantize_range(*args, mf, FAKE, 2 * 1024, FAKE, 2 * 128, None) == 1
-    assert lib.ufp4_e2m1_quantize_range(FAKE, 16, 24, 24, 0, 1, 0, 0, 0, 0, 4.0, FAKE, 2048, FAKE, 256, None) == 2
-
-
-def test_unfused_validation(lib):
-    # ufp4_rht(x, rows, cols, ld, mask, y, ldy, stream)
-    assert lib.ufp4_rht(None, 16, 32, 32, 0, FAKE, 32, None) == 1
-    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0x10000, FAKE, 32, None) == 1
-    assert lib.ufp4_rht(FAKE, 16, 24, 24, 0, FAKE, 24, None) == 2      # cols % 16
-    assert lib.ufp4_rht(FAKE, 16, 32, 36, 0, FAKE, 32, None) == 2      # ld % 8
-    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 30, None) == 2      # ldy < cols
-    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE, 34, None) == 2      # ldy % 4
-    assert lib.ufp4_rht(FAKE, 16, 32, 32, 0, FAKE + 4, 32, None) == 3  # y alignment
-    # ufp4_quantize_f32(format, x, rows, cols, ld, rounding, seed, stream, codes, cld, scales, sld, stream)
-    assert lib.ufp4_quantize_f32(2, FAKE, 16, 32, 32, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 1
-    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 32, 2, 0, 0, FAKE, C2, FAKE, S2, None) == 1
-    assert lib.ufp4_quantize_f32(0, FAKE, 16, 24, 24, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 2
-    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 34, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 2   # ld % 4
-    assert lib.ufp4_quantize_f32(0, FAKE + 8, 16, 32, 32, 0, 0, 0, FAKE, C2, FAKE, S2, None) == 3
-    assert lib.ufp4_quantize_f32(0, FAKE, 16, 32, 32, 0, 0, 0, FAKE, C1, FAKE, S2, None) == 2   # code panel stride
-
-
-def test_rht_block_validation(lib):
-    words = (ctypes.c_uint16 * 8)()
-    w = ctypes.cast(words, ctypes.c_void_p)
-    base = (0, FAKE, 16, 128, 128, 0)
-    tail = (0, 0, 0, FAKE, 8 * 1024, FAKE, 8 * 128, None)
-    assert lib.ufp4_quantize_rht_block(*base, 48, w, *tail) == 1         # block size
-    assert lib.ufp4_quantize_rht_block(*base, 32, None, *tail) == 1      # no sign words
-    assert lib.ufp4_quantize_rht_block(2, *base[1:], 32, w, *tail) == 1  # format
-    assert lib.ufp4_quantize_rht_block(0, FAKE, 16, 96, 96, 0, 64, w, 0, 0, 0, FAKE, 6 * 1024, FAKE, 6 * 128,
-                                       None) == 2                        # 96 % 64
+def test_binding_descriptor_layout_matches_the_header():
+    """The ctypes mirror of ufp4_qtensor: field order and offsets as the header declares them (88 bytes)."""
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct \{(.*?)\} ufp4_qtensor;", src, re.S).group(1)
+    names = re.findall(r"\b(\w+)(?:\[\d+\])?;", body)
+    assert names == [f[0] for f in U.QDesc._fields_]
+    assert ctypes.sizeof(U.QDesc) == 88 and U.QDesc.sign_words.offset == 64
