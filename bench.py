@@ -7,14 +7,19 @@ the two-operand quantizer (one read, both operands) and dY through the two singl
 SR); --quant separate uses six single-output calls. Inputs are resident in HBM before the timed region; every
 output buffer is allocated before it, so the timed loop only launches kernels.
 
+The default workload is the square 16384^3 layer, the largest that the paper's configurations put on one GPU.
+
 Prints one JSON line. `value` is the step's GEMM work (3 x 2MNK) divided by the step time, in TFLOP/s;
 `breakdown` has every kernel's average duration and its own GB/s (algorithmic bytes: 2.75 per element for a
 single-output quantizer, 3.5 for the two-operand one) or TFLOP/s (GEMMs); `roofline` is for the GEMM kernel,
-the dominant one; `cpu_baseline` times the CPU oracle on a bounded sample of the same layer.
+the dominant one; `cpu_baseline` times the CPU oracle on a bounded sample of the same layer (a block of tokens
+and of W's rows). For a layer workload under the ufp4 recipe the line also carries, untimed by `value`:
+`e2m1_step`, the same step under the E2M1 baseline recipe of Table 1 on the same inputs, and
+`quantizer_1gib`, every quantizer kernel on a 1 GiB bf16 tensor (Sec. 5 Q5).
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup W] [--quant dual|separate]
-                       [--workload dense|tiny|moe7.9b|moe124b|square|quant1g|quant1g-t|quant1g-dual|copy1g|
-                                   quality-dense|quality-moe124b]
+                       [--workload square|dense|tiny|moe7.9b|moe124b|quant1g|quant1g-t|quant1g-dual|copy1g|
+                                   quality-dense|quality-moe124b] [--no-compare] [--no-cpu-baseline]
 
 The quant1g workloads time one quantizer on a 1 GiB bf16 tensor; they also time the same kernel without the
 RHT (plain block quantization) and report the ratio, the quantity the paper gives for its own fused kernel.
@@ -71,6 +76,14 @@ def gemm_family(recipe: str) -> str:
     if recipe == "mxufp4":
         return "mxufp4"
     return "ufp4" if R.RECIPES[recipe].fmt == U.UNIFORM else "e2m1"
+
+
+# The arithmetic each GEMM family computes in: 4-bit codes times per-block scales, fp32 accumulation.
+ARITH = {
+    "ufp4": "int4xf32",   # integer codes -7..7 (as exact fp8 e4m3 values on the fp8 MFMA), fp32 1x16 scales
+    "e2m1": "fp4xf32",    # E2M1 codes on the FP4 MFMA, fp32 1x16 scales
+    "mxufp4": "int4xe8m0",  # integer codes -7..7 (as FP6 E2M3 values), power-of-two 1x32 scales in the MFMA
+}
 
 
 def gemm_peak(recipe: str) -> float:
@@ -293,6 +306,74 @@ def quant1g_step(tl: Timeline, mode: str):
 
 
 # ---------------------------------------------------------------------------------------------------
+# extras of a layer run: the E2M1 baseline step on the same inputs, every quantizer on a 1 GiB tensor
+# ---------------------------------------------------------------------------------------------------
+
+def time_steps(step, steps: int, warmup: int, warm_seconds: float = 0.0) -> float:
+    """`warmup` untimed calls (more until `warm_seconds` have passed), then `steps` calls between two events on
+    the current stream: ms per call."""
+    n, t0 = 0, time.perf_counter()
+    while n < warmup or time.perf_counter() - t0 < warm_seconds:
+        step(False)
+        n += 1
+        if n % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        step(True)
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def e2m1_comparison(wl, steps: int, warmup: int, dual: bool) -> dict:
+    """The same layer step under the E2M1 recipe of Table 1 (RHT on bwd_dw only, SR on dY), same inputs."""
+    tl = Timeline()
+    step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, "e2m1", dual)
+    ms = time_steps(step, steps, warmup)
+    gemms, flops, qus = {}, 0, 0.0
+    for label, (kind, work) in kern.items():
+        us = tl.mean_us(label)
+        if kind == "gemm":
+            tf = work / (us * 1e-6) / 1e12
+            gemms[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
+            flops += work
+        else:
+            qus += us
+    return {"recipe": RECIPE_NOTES["e2m1"], "kernel": GEMM_KERNEL["e2m1"], "ms_per_step": round(ms, 4),
+            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 3), "gemms": gemms, "quant_all_us": round(qus, 2)}
+
+
+def quantizer_1gib(steps: int, warmup: int) -> dict:
+    """Each quantizer kernel on the 1 GiB bf16 tensor [32768, 16384] (Sec. 5 Q5's measurement): RHT16, both
+    roundings, rowwise, transposed and both operands in one pass, and the E2M1 grid."""
+    t = WL.quantizer_tensor().cuda()
+    rows, cols = t.shape
+    qr, qc = U.empty_qtensor(rows, cols), U.empty_qtensor(cols, rows)
+    er = U.empty_qtensor(rows, cols, U.E2M1)
+    m = 0x6A09
+    cases = {
+        "rows_rtne": (lambda: U.rht_quantize(t, sign_mask=m, out=qr), "quant"),
+        "cols_rtne": (lambda: U.rht_quantize(t, transpose=True, sign_mask=m, out=qc), "quant"),
+        "rows_sr": (lambda: U.rht_quantize(t, sign_mask=m, rounding=U.SR, seed=7, out=qr), "quant"),
+        "cols_sr": (lambda: U.rht_quantize(t, transpose=True, sign_mask=m, rounding=U.SR, seed=7, stream_id=1,
+                                           out=qc), "quant"),
+        "dual_rtne": (lambda: U.quantize_dual(t, sign_mask_rows=m, sign_mask_cols=m, out_rows=qr, out_cols=qc),
+                      "quant2"),
+        "rows_e2m1_rtne": (lambda: U.e2m1_quantize(t, rht=True, sign_mask=m, out=er), "quant"),
+    }
+    out = {}
+    for label, (fn, kind) in cases.items():
+        us = time_steps(lambda rec, fn=fn: fn(), steps, warmup, WARMUP_SECONDS) * 1e3
+        gbps = rows * cols * BYTES_PER_ELEM[kind] / (us * 1e-6) / 1e9
+        out[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
+    del t, qr, qc, er
+    return out
+
+
+# ---------------------------------------------------------------------------------------------------
 # quality diagnostics (Sec. 3.2) on the layer's tensors at full size, from ufp4_quant_stats
 # ---------------------------------------------------------------------------------------------------
 
@@ -393,21 +474,25 @@ def measured_traffic(kind: str, workload: str):
 # CPU oracle baseline: the same layer step on a bounded sample of tokens
 # ---------------------------------------------------------------------------------------------------
 
-def cpu_baseline(wl, tokens: int = 512, recipe: str = "ufp4"):
+def cpu_baseline(wl, tokens: int = 1024, wrows: int = 1024, recipe: str = "ufp4"):
+    """The oracle's layer step (six quantizations, three fp64 GEMMs) on the first `tokens` rows of X and dY and
+    the first `wrows` rows of W (dY's matching columns): the same arithmetic per element as the full layer, on
+    a sample that fits a few seconds of host time. The rate is per sampled work."""
     from oracle import ufp4_oracle as O
     from threadpoolctl import threadpool_info
 
-    x = WL.bf16_bits(wl.x[:tokens].contiguous())
-    dy = WL.bf16_bits(wl.dy[:tokens].contiguous())
-    w = WL.bf16_bits(wl.w)
-    M, K = x.shape
-    N = w.shape[0]
+    M_full, K = wl.x.shape
+    N_full = wl.w.shape[0]
+    m, n = min(tokens, M_full), min(wrows, N_full)
+    x = WL.bf16_bits(wl.x[:m].contiguous())
+    dy = WL.bf16_bits(wl.dy[:m, :n].contiguous())
+    w = WL.bf16_bits(wl.w[:n].contiguous())
     times = {}
     t0 = time.perf_counter()
     O.layer_gemms(x, w, dy, recipe, sign_mask=wl.sign_mask, seed=wl.seed, times=times)
     dt = time.perf_counter() - t0
-    flops = 3 * 2 * M * N * K
-    quant_elems = 2 * (M * K + N * K + M * N)  # the six operands
+    flops = 3 * 2 * m * n * K
+    quant_elems = 2 * (m * K + n * K + m * n)  # the six operands
     blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     per_op = {k: round(v, 3) for k, v in times.items()}
     return {
@@ -417,12 +502,17 @@ def cpu_baseline(wl, tokens: int = 512, recipe: str = "ufp4"):
         "kind": "oracle",
         "per_op_s": per_op,
         "quantize_GB/s": round(quant_elems * QUANT_BYTES_PER_ELEM / times["quantize"] / 1e9, 3),
-        "gemm_TFLOP/s": round(float(2 * M * N * K / np.mean([times[k] for k in ("fwd_y", "bwd_dx", "bwd_dw")])) / 1e12, 4),
-        "sample": (f"whole {recipe} layer step (6 quantizations + 3 fp64 GEMMs) on {tokens} of {wl.x.shape[0]} "
-                   f"tokens, full {N}x{K} weight; {dt:.1f} s; elementwise numpy on 1 thread, fp64 matmul on "
-                   f"{blas} BLAS threads; host {platform.processor() or platform.machine()}, "
-                   f"os.cpu_count()={os.cpu_count()}"),
+        "gemm_TFLOP/s": round(float(2 * m * n * K / np.mean([times[k] for k in ("fwd_y", "bwd_dx", "bwd_dw")])) / 1e12, 4),
+        "sample": (f"whole {recipe} layer step (6 quantizations + 3 fp64 GEMMs) on {m} of {M_full} tokens and {n} "
+                   f"of {N_full} output features (X [{m}, {K}], W [{n}, {K}], dY [{m}, {n}]); {dt:.1f} s; "
+                   f"elementwise numpy on 1 thread, fp64 matmul on {blas} BLAS threads; host "
+                   f"{platform.processor() or platform.machine()}, os.cpu_count()={os.cpu_count()}"),
     }
+
+
+def progress(msg: str) -> None:
+    """A line on stderr per finished stage (the JSON result is the only stdout line)."""
+    print(f"bench.py: {msg}", file=sys.stderr, flush=True)
 
 
 def main():
@@ -430,8 +520,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: steps for WARMUP_SECONDS)")
-    ap.add_argument("--workload", default="dense",
-                    choices=["dense", "tiny", "moe7.9b", "moe124b", "square", "quant1g", "quant1g-t", "quant1g-dual",
+    ap.add_argument("--workload", default="square",
+                    choices=["square", "dense", "tiny", "moe7.9b", "moe124b", "quant1g", "quant1g-t", "quant1g-dual",
                              "copy1g", "quality-dense", "quality-moe124b"])
     ap.add_argument("--recipe", default="ufp4", choices=sorted(RECIPE_NOTES),
                     help="ufp4 (the method) or e2m1 (the comparison baseline of Table 1)")
@@ -439,6 +529,8 @@ def main():
                     help="dual: X and W quantized to both operands in one pass (dY, SR, uses the single-output "
                          "kernels, measured faster); separate: six single-output quantizations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip the E2M1 step and the 1 GiB quantizer runs that a ufp4 layer run carries")
     ap.add_argument("--graph", action="store_true",
                     help="also capture the layer step once in a HIP graph and time its replays (reported beside "
                          "`value`, which stays the eagerly launched step)")
@@ -486,6 +578,7 @@ def main():
         step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe, args.quant == "dual")
         wname = wl.name
     torch.cuda.synchronize()
+    progress(f"inputs of '{wname}' resident; warming up")
 
     if args.warmup is None:
         # whole untimed steps until the clock has settled
@@ -534,6 +627,16 @@ def main():
                 "unfused_form": "standalone RHT writing fp32 y (2 B in, 4 B out per element), then the fp32-input "
                                 "quantizer (4 B in, 0.75 B out); same codes as the fused kernel",
                 "paper_unfused": "unfused / fused latency 1.62x (SM90), 1.41x (SM100); Sec. 5 Q5"})
+
+    progress(f"timed {args.steps} steps: {ms_per_step:.3f} ms per step")
+
+    extras = {}
+    if wl is not None and args.recipe == "ufp4" and not args.no_compare:
+        extras["e2m1_step"] = e2m1_comparison(wl, args.steps, args.warmup, args.quant == "dual")
+        extras["e2m1_step"]["ufp4_over_e2m1_speed"] = round(extras["e2m1_step"]["ms_per_step"] / ms_per_step, 3)
+        progress("E2M1 step timed")
+        extras["quantizer_1gib"] = quantizer_1gib(args.steps, 5)
+        progress("1 GiB quantizers timed")
 
     graph_ctx = None
     if args.graph and wl is not None:
@@ -623,7 +726,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": ("fp6+f32" if args.recipe == "mxufp4" else "f32") if gemm_labels else "f64+f32",
+        "dtype": ARITH[gemm_family(args.recipe)] if gemm_labels else "bf16->int4xf32",
         "data": "synthetic (seeded, shapes and distributions of the workload; no real tensors)",
         "config": {"workload": wname, "recipe": RECIPE_NOTES[args.recipe],
                    "outputs": "Y bf16, dX bf16, dW fp32" if gemm_labels else "codes + fp32 scales",
@@ -640,9 +743,11 @@ def main():
         out["rht_cost"] = context
     if graph_ctx is not None:
         out["graph_replay"] = graph_ctx
+    out.update(extras)
     if wl is not None:
         out["config"]["quant"] = args.quant
     if wl is not None and not args.no_cpu_baseline and not wl.grouped:
+        progress("timing the CPU oracle on a sample of the layer")
         out["cpu_baseline"] = cpu_baseline(wl, recipe=args.recipe)
     print(json.dumps(out), flush=True)
 
