@@ -53,10 +53,12 @@ from paper_2606_20381_amd import workloads as WL  # noqa: E402
 HBM_PEAK_GBPS = 8000.0
 INT8_PEAK_TOPS = 5000.0  # dense int8 / fp8 MFMA, MI355X
 FP4_PEAK_TFLOPS = 10100.0  # dense fp4 MFMA (the E2M1 baseline's block products)
-# Bound of the per-16-block fp32-scale GEMM kernel: per 32x32 output tile and 16-block two MFMAs of 32 cycles each
-# (block product, scale outer product) = 64 cycles for 32*32*16*2 ops, i.e. 512 ops per cycle per SIMD, at
-# 256 CUs x 4 SIMDs x 2.4 GHz.
-ATTAINABLE_TOPS = 32 * 32 * 16 * 2 / 64 * 256 * 4 * 2.4e9 / 1e12
+# Bound of the per-16-block fp32-scale GEMM kernel, per 32x32 output tile and 16-block: two MFMAs of 32 cycles
+# each (block product, scale outer product) occupy the matrix core 64 cycles, and the SIMD issues them and the
+# 16 fp32 FMAs (acc += D_b * (sA sB)_b) through its VALU port at one wave64 instruction per 4 cycles: at least
+# 18 issue slots = 72 cycles for 32*32*16*2 ops. 256 CUs x 4 SIMDs at 2.4 GHz.
+MFMA_BOUND_TOPS = 32 * 32 * 16 * 2 / 64 * 256 * 4 * 2.4e9 / 1e12
+ATTAINABLE_TOPS = 32 * 32 * 16 * 2 / (4 * (2 + 16)) * 256 * 4 * 2.4e9 / 1e12
 GEMM_KERNEL = {
     "mxufp4": "gemm_mx_kernel (scaled f8f6f4 MFMA 32x32x64, FP6 E2M3 operands, E8M0 scales applied in the matrix core)",
     "ufp4": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
@@ -697,8 +699,9 @@ def main():
                 "traffic": measured_traffic("gemm_mx" if args.recipe == "mxufp4" else "gemm", wname + "/" + args.recipe)}
         if args.recipe != "mxufp4":  # per-16 fp32 scales: a scale outer product per tile and block
             roof["attainable"] = {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
-                                  "why": "two 32-cycle MFMAs per 32x32 tile and 16-block (block product and "
-                                         "scale outer product)"}
+                                  "why": "per 32x32 tile and 16-block: 2 MFMAs (64 matrix-core cycles) and 16 fp32 "
+                                         "FMAs, 18 VALU issue slots of 4 cycles = 72 cycles; the matrix cores alone "
+                                         f"would allow {MFMA_BOUND_TOPS:.1f}"}
     else:
         value = quant_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"

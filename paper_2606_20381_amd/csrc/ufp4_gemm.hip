@@ -85,7 +85,24 @@ struct TilePos {
     int64_t tn, tm;
     int g;
 };
-__device__ __forceinline__ TilePos grid_pos() { return {(int64_t)blockIdx.x, (int64_t)blockIdx.y, (int)blockIdx.z}; }
+
+// Workgroups are dealt to the 8 XCDs round robin (linear index L to XCD L % 8), each XCD with its own L2. On a
+// single-problem grid the first 8 * floor(T / 8) workgroups are renumbered so that XCD k gets the contiguous
+// range of tiles [k T/8, (k + 1) T/8); tiles are ordered in bands of kBandRows tile rows, column by column
+// within a band, so the workgroups resident on one XCD share a few panels of A and of B instead of every XCD
+// streaming every panel. The map is a bijection of the grid, so every tile is still computed exactly once.
+constexpr int64_t kBandRows = 8;
+__device__ __forceinline__ TilePos grid_pos() {
+    if (gridDim.z != 1 || gridDim.y == 1) return {(int64_t)blockIdx.x, (int64_t)blockIdx.y, (int)blockIdx.z};
+    const int64_t gx = gridDim.x, gy = gridDim.y, T = gx * gy, per = T / 8;
+    const int64_t L = (int64_t)blockIdx.y * gx + blockIdx.x;
+    const int64_t t = L < 8 * per ? (L % 8) * per + L / 8 : L;
+    const int64_t band = t / (kBandRows * gx);
+    const int64_t first = band * kBandRows;
+    const int64_t rows = gy - first < kBandRows ? gy - first : kBandRows;
+    const int64_t r = t - band * kBandRows * gx;
+    return {r / rows, first + r % rows, 0};
+}
 
 // Padded start of group g along a ragged-K reduction: sum over h < g of the token counts rounded up to multiples
 // of 16 (each group's tokens were zero-padded so; ufp4_quantize_grouped_t lays them out the same way). Wave 0
