@@ -53,12 +53,11 @@ from paper_2606_20381_amd import workloads as WL  # noqa: E402
 HBM_PEAK_GBPS = 8000.0
 INT8_PEAK_TOPS = 5000.0  # dense int8 / fp8 MFMA, MI355X
 FP4_PEAK_TFLOPS = 10100.0  # dense fp4 MFMA (the E2M1 baseline's block products)
-# Bound of the per-16-block fp32-scale GEMM kernel, per 32x32 output tile and 16-block: two MFMAs of 32 cycles
-# each (block product, scale outer product) occupy the matrix core 64 cycles, and the SIMD issues them and the
-# 16 fp32 FMAs (acc += D_b * (sA sB)_b) through its VALU port at one wave64 instruction per 4 cycles: at least
-# 18 issue slots = 72 cycles for 32*32*16*2 ops. 256 CUs x 4 SIMDs at 2.4 GHz.
-MFMA_BOUND_TOPS = 32 * 32 * 16 * 2 / 64 * 256 * 4 * 2.4e9 / 1e12
-ATTAINABLE_TOPS = 32 * 32 * 16 * 2 / (4 * (2 + 16)) * 256 * 4 * 2.4e9 / 1e12
+# Bound of the per-16-block fp32-scale GEMM kernel: per 32x32 output tile and 16-block two MFMAs of 32 cycles each
+# (block product, scale outer product) keep the matrix core busy 64 cycles (the counter SQ_VALU_MFMA_BUSY_CYCLES
+# reads exactly that) for 32*32*16*2 ops, i.e. 512 ops per cycle per SIMD, at 256 CUs x 4 SIMDs x 2.4 GHz. The 16
+# fp32 FMAs per tile-block (acc += D_b * (sA sB)_b) run on the VALU beside the MFMAs; the bound assumes they hide.
+ATTAINABLE_TOPS = 32 * 32 * 16 * 2 / 64 * 256 * 4 * 2.4e9 / 1e12
 GEMM_KERNEL = {
     "mxufp4": "gemm_mx_kernel (scaled f8f6f4 MFMA 32x32x64, FP6 E2M3 operands, E8M0 scales applied in the matrix core)",
     "ufp4": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
@@ -265,28 +264,30 @@ def copy1g_step(tl: Timeline):
     return step, {"copy": ("copy", t.numel() * t.element_size())}
 
 
-def quant1g_step(tl: Timeline, mode: str):
+def quant1g_step(tl: Timeline, mode: str, sr: bool = False):
     """One quantizer on a 1 GiB bf16 tensor: rowwise (reduction along its 16384 columns), transposed (operand
-    X^T, reduction along its 32768 rows) or both operands in one pass. Returns (step, kernel table, plain step):
-    the plain step runs the same kernel without the RHT."""
+    X^T, reduction along its 32768 rows) or both operands in one pass, rounding RTNE or SR. Returns (step, kernel
+    table, plain step, unfused step): the plain step runs the same kernel without the RHT."""
     t = WL.quantizer_tensor().cuda()
     R, C = t.shape
+    rnd, rname = (U.SR, "sr") if sr else (U.RTNE, "rtne")
     if mode == "dual":
         qr, qc = U.empty_qtensor(R, C), U.empty_qtensor(C, R)
 
         def run(rht):
             return U.quantize_dual(t, rht_rows=rht, rht_cols=rht, sign_mask_rows=0x6A09, sign_mask_cols=0x6A09,
-                                   out_rows=qr, out_cols=qc)
+                                   rounding=rnd, seed=7, stream_rows=0, stream_cols=1, out_rows=qr, out_cols=qc)
 
-        label, kind = "quant_dual_rtne", "quant2"
+        label, kind = "quant_dual_" + rname, "quant2"
     else:
         transpose = mode == "cols"
         q = U.empty_qtensor(C, R) if transpose else U.empty_qtensor(R, C)
 
         def run(rht):
-            return U.rht_quantize(t, transpose=transpose, rht=rht, sign_mask=0x6A09, out=q)
+            return U.rht_quantize(t, transpose=transpose, rht=rht, sign_mask=0x6A09, rounding=rnd, seed=7,
+                                  stream_id=int(transpose), out=q)
 
-        label, kind = ("quant_cols_rtne" if transpose else "quant_rows_rtne"), "quant"
+        label, kind = ("quant_cols_" if transpose else "quant_rows_") + rname, "quant"
 
     def step(rec):
         tl.run(label, lambda: run(True), rec)
@@ -295,7 +296,7 @@ def quant1g_step(tl: Timeline, mode: str):
         tl.run(label + "_plain", lambda: run(False), rec)
 
     unfused = None
-    if mode == "rows":
+    if mode == "rows" and not sr:
         # the unfused form: standalone RHT into an fp32 tensor, then the fp32-input quantizer (same codes)
         y = torch.empty((R, C), dtype=torch.float32, device="cuda")
         qu = U.empty_qtensor(R, C)
@@ -530,6 +531,8 @@ def main():
     ap.add_argument("--quant", default="dual", choices=["dual", "separate"],
                     help="dual: X and W quantized to both operands in one pass (dY, SR, uses the single-output "
                          "kernels, measured faster); separate: six single-output quantizations")
+    ap.add_argument("--rounding", default="rtne", choices=["rtne", "sr"],
+                    help="rounding of the quant1g workloads (the layer step rounds dY stochastically, the rest RTNE)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip the E2M1 step and the 1 GiB quantizer runs that a ufp4 layer run carries")
@@ -566,9 +569,9 @@ def main():
     plain = unfused = None
     if args.workload in ("quant1g", "quant1g-t", "quant1g-dual"):
         mode = {"quant1g": "rows", "quant1g-t": "cols", "quant1g-dual": "dual"}[args.workload]
-        step, kern, plain, unfused = quant1g_step(tl, mode)
+        step, kern, plain, unfused = quant1g_step(tl, mode, args.rounding == "sr")
         what = {"rows": "rowwise", "cols": "transposed", "dual": "rowwise + transposed in one pass"}[mode]
-        wname = f"standalone quantizer: 32768x16384 bf16 (1 GiB), {what} RTNE with RHT"
+        wname = f"standalone quantizer: 32768x16384 bf16 (1 GiB), {what} {args.rounding.upper()} with RHT"
     elif args.workload == "copy1g":
         step, kern = copy1g_step(tl)
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
@@ -699,9 +702,8 @@ def main():
                 "traffic": measured_traffic("gemm_mx" if args.recipe == "mxufp4" else "gemm", wname + "/" + args.recipe)}
         if args.recipe != "mxufp4":  # per-16 fp32 scales: a scale outer product per tile and block
             roof["attainable"] = {"peak": round(ATTAINABLE_TOPS, 1), "frac": round(ach / ATTAINABLE_TOPS, 4),
-                                  "why": "per 32x32 tile and 16-block: 2 MFMAs (64 matrix-core cycles) and 16 fp32 "
-                                         "FMAs, 18 VALU issue slots of 4 cycles = 72 cycles; the matrix cores alone "
-                                         f"would allow {MFMA_BOUND_TOPS:.1f}"}
+                                  "why": "two 32-cycle MFMAs per 32x32 tile and 16-block (block product and "
+                                         "scale outer product); the 16 fp32 FMAs per tile-block hidden beside them"}
     else:
         value = quant_bytes / (ms_per_step * 1e-3) / 1e9
         unit = "GB/s"
@@ -710,6 +712,8 @@ def main():
         per_launch = kern[label][1] * BYTES_PER_ELEM[kern[label][0]]
         ach = per_launch / (us * 1e-6) / 1e9
         kname = {"quant_rows_rtne": "quant_rows_kernel", "quant_cols_rtne": "quant_cols_kernel",
+                 "quant_rows_sr": "quant_rows_kernel", "quant_cols_sr": "quant_cols_kernel",
+                 "quant_dual_sr": "quant_dual_kernel",
                  "quant_dual_rtne": "quant_dual_kernel"}.get(label, "copy")
         roof = {"bound": "hbm", "kernel": kname, "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),

@@ -68,12 +68,9 @@ def test_group_offsets_pad_each_group_to_16():
 
 
 def test_roofline_constants():
-    # per 32 x 32 tile and 16-block: two 32-cycle MFMAs (64 matrix-core cycles) and 18 VALU issue slots (2 MFMA +
-    # 16 FMA) of 4 cycles; 1024 SIMDs at 2.4 GHz
-    assert bench.MFMA_BOUND_TOPS == pytest.approx(32768 / 64 * 1024 * 2.4e9 / 1e12)
-    assert bench.MFMA_BOUND_TOPS == pytest.approx(1258.29, abs=0.01)
-    assert bench.ATTAINABLE_TOPS == pytest.approx(32768 / 72 * 1024 * 2.4e9 / 1e12)
-    assert bench.ATTAINABLE_TOPS == pytest.approx(1118.48, abs=0.01)
+    # two 32-cycle MFMAs per 32 x 32 tile and 16-block: 32768 ops per 64 cycles per SIMD, 1024 SIMDs at 2.4 GHz
+    assert bench.ATTAINABLE_TOPS == pytest.approx(32768 / 64 * 1024 * 2.4e9 / 1e12)
+    assert bench.ATTAINABLE_TOPS == pytest.approx(1258.29, abs=0.01)
     assert bench.QUANT_BYTES_PER_ELEM == 2 + 0.5 + 0.25  # bf16 in, 4-bit code and a fp32 scale per 16 out
     assert bench.DUAL_BYTES_PER_ELEM == 2 + 2 * (0.5 + 0.25)
     # the 1 GiB quantizer tensor at the HBM peak: 1.476 GB in 184.5 us; 70% of the peak is 264 us
