@@ -437,23 +437,25 @@ def quantize_both(t_bits: np.ndarray, fmt: int, rounding: int, rht_rows: bool, r
             quantize_rows(operand_colwise(t_bits), fmt, rounding, rht_cols, sign_mask_cols, seed, stream_cols))
 
 
-def pad16(n: int) -> int:
-    return -(-int(n) // BLOCK) * BLOCK
+def pad16(n: int, block: int = BLOCK) -> int:
+    """n rounded up to a multiple of `block` (16: one quantization block; 32 for power-of-two scales)."""
+    return -(-int(n) // block) * block
 
 
-def operand_colwise_grouped(t_bits: np.ndarray, counts) -> tuple[np.ndarray, np.ndarray]:
+def operand_colwise_grouped(t_bits: np.ndarray, counts, block: int = BLOCK) -> tuple[np.ndarray, np.ndarray]:
     """Transposed operand of a grouped (MoE) tensor whose rows are split into consecutive groups.
 
     Group g owns rows [off_g, off_g + counts[g]) of T. Its block of A is T[group]^T with the reduction
-    axis (the group's tokens) zero-padded to a multiple of 16; the padded groups are concatenated along
-    the reduction axis. Zero padding keeps every group's GEMM unchanged ((XH')(WH')^T = XW^T).
-    Returns (A [cols, sum pad16(counts)], padded offsets [G+1]).
+    axis (the group's tokens) zero-padded to a multiple of `block` (the quantization block along that axis: 16,
+    or 32 for power-of-two scales, so that no block straddles two groups); the padded groups are concatenated
+    along the reduction axis. Zero padding keeps every group's GEMM unchanged ((XH')(WH')^T = XW^T).
+    Returns (A [cols, sum of padded counts], padded offsets [G+1]).
     """
     t = bf16_bits_to_f32(t_bits)
     counts = [int(c) for c in counts]
     if sum(counts) != t.shape[0]:
         raise ValueError("group counts do not cover the rows")
-    pads = [pad16(c) for c in counts]
+    pads = [pad16(c, block) for c in counts]
     poff = np.concatenate([[0], np.cumsum(pads)]).astype(np.int64)
     a = np.zeros((t.shape[1], int(poff[-1])), dtype=np.float32)
     off = 0

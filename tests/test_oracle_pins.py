@@ -1043,3 +1043,36 @@ def test_mx_gemm_special_cases():
             want = sum(Fraction(int(a[i, k])) * Fraction(2) ** (int(ea[i, k // 32]) - 127) * int(b[j, k])
                        * Fraction(2) ** (int(eb[j, k // 32]) - 127) for k in range(64))
             assert c[i, j] == float(want)
+
+
+def test_grouped_padding_to_32_for_power_of_two_scales():
+    """With power-of-two 1x32 scales the token axis is padded per group to a multiple of 32: the padded lengths,
+    no 32-block straddling two groups, zero padding, and per-group products unchanged by it."""
+    rng = np.random.default_rng(48)
+    counts = [5, 16, 33, 0, 19, 32]
+    mtot = sum(counts)
+    x = _rand_bf16_bits(rng, (mtot, 64))
+    dy = _rand_bf16_bits(rng, (mtot, 32))
+    ax, poff = O.operand_colwise_grouped(x, counts, block=32)
+    ad, _ = O.operand_colwise_grouped(dy, counts, block=32)
+    assert list(np.diff(poff)) == [32, 32, 64, 0, 32, 32] and all(p % 32 == 0 for p in poff)
+    xf, df = O.bf16_bits_to_f32(x).astype(np.float64), O.bf16_bits_to_f32(dy).astype(np.float64)
+    off = 0
+    for gi, c in enumerate(counts):
+        lo, hi = int(poff[gi]), int(poff[gi + 1])
+        assert not np.any(ax[:, lo + c:hi]) and not np.any(ad[:, lo + c:hi])  # the padding is zero
+        assert np.array_equal(ax[:, lo:lo + c], O.bf16_bits_to_f32(x)[off:off + c].T)
+        ref = df[off:off + c].T @ xf[off:off + c]
+        assert np.allclose(ad[:, lo:hi].astype(np.float64) @ ax[:, lo:hi].T.astype(np.float64), ref, rtol=0, atol=1e-12)
+        off += c
+    # quantized along the padded axis, a group's blocks hold only its own tokens: its product equals the one of
+    # the group quantized alone (same values and the same draws up to the block numbering)
+    idx, e8 = O.quantize_rows_mx(ax, O.RTNE, True, 0x1234)
+    for gi, c in enumerate(counts):
+        lo, hi = int(poff[gi]), int(poff[gi + 1])
+        if hi == lo:
+            continue
+        alone = np.zeros((ax.shape[0], hi - lo), dtype=np.float32)
+        alone[:, :c] = ax[:, lo:lo + c]
+        i2, e2 = O.quantize_rows_mx(alone, O.RTNE, True, 0x1234)
+        assert np.array_equal(idx[:, lo:hi], i2) and np.array_equal(e8[:, lo // 32:hi // 32], e2)
