@@ -205,6 +205,8 @@ def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
 
 
 def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
+    if recipe == "mxufp4":
+        return moe_step_mx(wl, tl)
     m, s = wl.sign_mask, wl.seed
     fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     E, N, K = wl.w.shape
@@ -250,6 +252,47 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
         "quant_dy_sr": ("quant", M * N), "quant_dyt_sr": ("quant", M * N), "quant_xt": ("quant", M * K),
         "gemm_fwd_y": ("gemm", flops), "gemm_bwd_dx": ("gemm", flops), "gemm_bwd_dw": ("gemm", flops),
     })
+    return step, kern
+
+
+def moe_step_mx(wl, tl: Timeline):
+    """The expert layer step with power-of-two 1x32 scales: X and dY in the grouped-rows form (each expert's rows
+    from a panel boundary) for the ragged-M passes, X^T and dY^T with each expert's tokens padded to 32 for
+    bwd_dw, W and W^T plain; RHT16 everywhere, SR on dY."""
+    m, s = wl.sign_mask, wl.seed
+    E, N, K = wl.w.shape
+    x, dy = wl.x.cuda(), wl.dy.cuda()
+    w2 = wl.w.reshape(E * N, K).cuda()
+    M = x.shape[0]
+    off, prow = U.group_offsets(wl.counts, block=128)
+    _, red32 = U.group_offsets(wl.counts, block=32)
+    Q = U.empty_qtensor_mx
+    q = {"x": Q(prow, K), "w": Q(E * N, K), "dy": Q(prow, N), "wt": Q(K, E * N), "dyt": Q(N, red32),
+         "xt": Q(K, red32)}
+    y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
+    dw = torch.empty(E, N, K, dtype=torch.float32, device="cuda")
+    G = U.mx_quantize_grouped
+
+    def step(rec):
+        tl.run("quant_x", lambda: G(x, off, prow, transpose=False, sign_mask=m, out=q["x"]), rec)
+        tl.run("quant_w", lambda: U.mx_quantize(w2, sign_mask=m, out=q["w"]), rec)
+        tl.run("quant_dy_sr", lambda: G(dy, off, prow, transpose=False, sign_mask=m, rounding=U.SR, seed=s,
+                                        stream_id=0, out=q["dy"]), rec)
+        tl.run("quant_wt", lambda: U.mx_quantize(w2, transpose=True, sign_mask=m, out=q["wt"]), rec)
+        tl.run("quant_dyt_sr", lambda: G(dy, off, red32, transpose=True, sign_mask=m, rounding=U.SR, seed=s,
+                                         stream_id=1, out=q["dyt"]), rec)
+        tl.run("quant_xt", lambda: G(x, off, red32, transpose=True, sign_mask=m, out=q["xt"]), rec)
+        tl.run("gemm_fwd_y", lambda: U.mx_gemm_fwd_y_grouped(q["x"], q["w"], off, M, out=y), rec)
+        tl.run("gemm_bwd_dx", lambda: U.mx_gemm_bwd_dx_grouped(q["dy"], q["wt"], off, M, out=dx), rec)
+        tl.run("gemm_bwd_dw", lambda: U.mx_gemm_bwd_dw_grouped(q["dyt"], q["xt"], off, out=dw), rec)
+
+    flops = 2 * M * N * K
+    kern = {
+        "quant_x": ("quantmx", M * K), "quant_w": ("quantmx", E * N * K), "quant_dy_sr": ("quantmx", M * N),
+        "quant_wt": ("quantmx", E * N * K), "quant_dyt_sr": ("quantmx", M * N), "quant_xt": ("quantmx", M * K),
+        "gemm_fwd_y": ("gemm", flops), "gemm_bwd_dx": ("gemm", flops), "gemm_bwd_dw": ("gemm", flops),
+    }
     return step, kern
 
 
@@ -577,8 +620,8 @@ def main():
         wname = "calibration: device copy of a 1 GiB bf16 tensor (read 1 GiB + write 1 GiB)"
     else:
         wl = WL.CONFIGS[args.workload]()
-        if wl.grouped and args.recipe not in ("ufp4", "e2m1"):
-            print("bench.py: grouped (MoE) layers run the ufp4 and e2m1 recipes only", file=sys.stderr)
+        if wl.grouped and args.recipe not in ("ufp4", "e2m1", "mxufp4"):
+            print("bench.py: grouped (MoE) layers run the ufp4, e2m1 and mxufp4 recipes only", file=sys.stderr)
             sys.exit(2)
         step, kern = (moe_step if wl.grouped else dense_step)(wl, tl, args.recipe, args.quant == "dual")
         wname = wl.name

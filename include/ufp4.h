@@ -81,6 +81,12 @@ typedef enum {
 enum { UFP4_FMT_UNIFORM = 0, UFP4_FMT_E2M1 = 1, UFP4_FMT_UNIFORM_MX32 = 2 };
 enum { UFP4_ROUND_RTNE = 0, UFP4_ROUND_SR = 1 };
 enum { UFP4_OUT_F32 = 0, UFP4_OUT_BF16 = 1 };
+/* How a quantized operand's rows and reduction axis relate to the tensor it came from (ufp4_qtensor.layout):
+ * PLAIN: row i and reduction position k are the tensor's; GROUPED_ROWS: the rows of expert groups, each group
+ * starting on a panel boundary (ufp4_mx_quantize_grouped, transpose 0); GROUPED_RED: the reduction axis is the
+ * groups' tokens, each group zero-padded to a multiple of the quantization block (ufp4_quantize_grouped_t,
+ * ufp4_mx_quantize_grouped with transpose 1). */
+enum { UFP4_LAYOUT_PLAIN = 0, UFP4_LAYOUT_GROUPED_ROWS = 1, UFP4_LAYOUT_GROUPED_RED = 2 };
 
 /*
  * A quantized operand Q(A H') [rows, red] (Sec. 2.1: codes plus block scales). The caller sets the storage
@@ -104,6 +110,8 @@ typedef struct {
     uint16_t sign_words[8];  /* its signs: eps_j = -1 iff bit (j % 16) of word j / 16; unused words 0    */
     float max_fpx;           /* E2M1 grid cut at 2 or 4 (Sec. 5 Q4); 0 for the full grid                 */
     int32_t rounding;        /* UFP4_ROUND_* used (recorded only)                                        */
+    int32_t layout;          /* UFP4_LAYOUT_*                                                            */
+    int32_t reserved;        /* 0                                                                        */
 } ufp4_qtensor;
 
 /* Human-readable name of a status code (static string). */
@@ -122,13 +130,16 @@ int ufp4_qtensor_bytes(int format, int64_t rows, int64_t red, int64_t *panels, i
                        int64_t *scale_panel_ld, size_t *codes_bytes, size_t *scales_bytes);
 
 /*
- * ufp4_grouped_reduction -- the reduction axis of a grouped transposed operand (bwd_dw of a MoE layer): each
- * group's tokens zero-padded to a multiple of 16, groups concatenated. From host token offsets off_0 = 0 <=
- * ... <= off_G: red_total = sum_g 16 ceil((off_{g+1} - off_g) / 16), and, if padded_offsets_host is not NULL,
- * the G + 1 padded offsets pad_0 = 0, pad_{g+1} = pad_g + 16 ceil((off_{g+1} - off_g) / 16). Host only.
+ * ufp4_grouped_reduction -- the padded axis of a grouped operand: each group's tokens zero-padded to a multiple
+ * of `block`, groups concatenated. block 16: the reduction of ufp4_quantize_grouped_t (bwd_dw of a MoE layer);
+ * 32: that of ufp4_mx_quantize_grouped with transpose 1; 128: the rows of ufp4_mx_quantize_grouped with
+ * transpose 0 (each group on whole panels). From host token offsets off_0 = 0 <= ... <= off_G: total = sum_g
+ * block ceil((off_{g+1} - off_g) / block), and, if padded_offsets_host is not NULL, the G + 1 padded offsets
+ * pad_0 = 0, pad_{g+1} = pad_g + block ceil((off_{g+1} - off_g) / block). Host only; other blocks return
+ * UFP4_ERR_INVALID_ARG.
  */
-int ufp4_grouped_reduction(const int64_t *group_offsets_host, int32_t num_groups, int64_t *padded_offsets_host,
-                           int64_t *red_total);
+int ufp4_grouped_reduction(const int64_t *group_offsets_host, int32_t num_groups, int32_t block,
+                           int64_t *padded_offsets_host, int64_t *total);
 
 /*
  * ufp4_rht_quantize -- fused RHT + uniform-grid quantization of one GEMM operand (Sec. 2.1, Sec. 2.2;
@@ -337,6 +348,48 @@ int ufp4_mx_gemm_bwd_dx(const ufp4_qtensor *dy, const ufp4_qtensor *wt, void *dx
                         void *stream);
 int ufp4_mx_gemm_bwd_dw(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, void *dw_dev, int64_t ldc, int out_dtype,
                         void *stream);
+
+/*
+ * Grouped (MoE) operands and GEMMs with power-of-two scales. The GEMM stages whole 128-row panels, so an expert's
+ * rows must start on a panel boundary: the ragged-M passes take A from the grouped-rows form below.
+ *
+ * ufp4_mx_quantize_grouped -- ufp4_mx_quantize over G groups of X's rows (device token offsets off_0 = 0 <= ...
+ *   <= off_G <= rows, up to 1024 groups).
+ *     transpose 0 (grouped rows; A of the grouped fwd_y and bwd_dx): Q is [padded_total, cols], cols % 32 == 0;
+ *       group g's rows are X[off_g .. off_{g+1}) starting at row P_g = sum_{h<g} 128 ceil((off_{h+1} - off_h) /
+ *       128), each quantized as ufp4_mx_quantize quantizes it (its SR counters use its row of X), the rows that
+ *       pad a group to whole panels and any rows past the last group zero. padded_total >= P_G
+ *       (ufp4_grouped_reduction with block 128).
+ *     transpose 1 (grouped reduction; both operands of the grouped bwd_dw): Q is [cols, padded_total], the
+ *       reduction axis being each group's tokens zero-padded to a multiple of 32 (no 32-block straddles two
+ *       groups), groups concatenated; block numbers in the SR counters count along this axis. padded_total =
+ *       ufp4_grouped_reduction with block 32.
+ *   Other arguments and the storage as ufp4_mx_quantize; out->layout records the form.
+ */
+int ufp4_mx_quantize_grouped(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,
+                             const int64_t *group_offsets_dev, int32_t num_groups, int64_t padded_total, int rht,
+                             uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor *out,
+                             void *stream);
+
+/*
+ * ufp4_mx_gemm_fwd_y_grouped -- Y[off_g .. off_{g+1}) = Q(X_g H') Q(W_g H')^T per group: x in grouped-rows form
+ *   [*, K], w plain [G * N, K] (group g's weight rows g N .. g N + N - 1; N % 128 == 0), y [m_total, N] row-major
+ *   with ldc >= N, m_total the rows of X (outputs past it are not written).
+ * ufp4_mx_gemm_bwd_dx_grouped -- dX[off_g .. off_{g+1}) = Q(dY_g H') Q(W_g^T H')^T: dy in grouped-rows form [*, N]
+ *   (N % 32 == 0), wt plain [K, G * N] (group g reduces over its positions g N .. g N + N - 1), dx [m_total, K].
+ * ufp4_mx_gemm_bwd_dw_grouped -- dW[g] = Q(dY_g^T H') Q(X_g^T H')^T: dyt [N, R] and xt [K, R] in grouped-reduction
+ *   form with the same offsets (R = the padded token axis), dw [G, N, K] (group g at dw + g N ldc; a group
+ *   without tokens gets zeros). Up to 65535 groups.
+ *   Operand forms other than these return UFP4_ERR_MISMATCH, as do the checks of the ungrouped calls.
+ */
+int ufp4_mx_gemm_fwd_y_grouped(const ufp4_qtensor *x, const ufp4_qtensor *w, const int64_t *group_offsets_dev,
+                               int32_t num_groups, int64_t m_total, void *y_dev, int64_t ldc, int out_dtype,
+                               void *stream);
+int ufp4_mx_gemm_bwd_dx_grouped(const ufp4_qtensor *dy, const ufp4_qtensor *wt, const int64_t *group_offsets_dev,
+                                int32_t num_groups, int64_t m_total, void *dx_dev, int64_t ldc, int out_dtype,
+                                void *stream);
+int ufp4_mx_gemm_bwd_dw_grouped(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, const int64_t *group_offsets_dev,
+                                int32_t num_groups, void *dw_dev, int64_t ldc, int out_dtype, void *stream);
 
 /*
  * Block-scaled 4-bit GEMMs (Sec. 2.2). All three passes are NT products of two quantized operands that

@@ -12,7 +12,7 @@
 using namespace ufp4;
 
 static_assert(sizeof(ufp4_quant_stats_t) == sizeof(QuantStats), "statistics record layout");
-static_assert(sizeof(ufp4_qtensor) == 88, "descriptor layout (mirrored by the Python binding)");
+static_assert(sizeof(ufp4_qtensor) == 96, "descriptor layout (mirrored by the Python binding)");
 
 namespace {
 
@@ -66,7 +66,7 @@ int check_storage(const ufp4_qtensor* q, int format, int64_t rows, int64_t red) 
 
 // What a quantizer wrote into `q`.
 void record(ufp4_qtensor* q, int format, int64_t rows, int64_t red, int rht_block, const uint16_t* words,
-            float max_fpx, int rounding) {
+            float max_fpx, int rounding, int layout = UFP4_LAYOUT_PLAIN) {
     q->rows = rows;
     q->red = red;
     q->format = format;
@@ -74,6 +74,8 @@ void record(ufp4_qtensor* q, int format, int64_t rows, int64_t red, int rht_bloc
     for (int k = 0; k < 8; ++k) q->sign_words[k] = (words && k < rht_block / 16) ? words[k] : 0;
     q->max_fpx = max_fpx == 6.0f ? 0.0f : max_fpx;
     q->rounding = rounding;
+    q->layout = layout;
+    q->reserved = 0;
 }
 
 // Checks shared by the bf16-input quantizers: the input tensor and the operand's storage.
@@ -227,9 +229,30 @@ int mx_gemm_impl(const ufp4_qtensor* a, const ufp4_qtensor* b, void* c, int64_t 
     j.M = a->rows;
     j.N = b->rows;
     j.nkb = a->red / 32;
+    j.a_rows = a->rows;
+    j.b_rows = b->rows;
     j.c = c;
     j.ldc = ldc;
+    j.mode = kGemmDense;
     return status_of(launch_gemm_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+MxGemmJob mx_job(const ufp4_qtensor* a, const ufp4_qtensor* b, void* c, int64_t ldc, int out_dtype) {
+    MxGemmJob j{};
+    j.out_dtype = out_dtype;
+    j.a = static_cast<const uint8_t*>(a->codes);
+    j.a_pld = a->code_panel_ld;
+    j.as = static_cast<const uint8_t*>(a->scales);
+    j.as_pld = a->scale_panel_ld;
+    j.b = static_cast<const uint8_t*>(b->codes);
+    j.b_pld = b->code_panel_ld;
+    j.bs = static_cast<const uint8_t*>(b->scales);
+    j.bs_pld = b->scale_panel_ld;
+    j.a_rows = a->rows;
+    j.b_rows = b->rows;
+    j.c = c;
+    j.ldc = ldc;
+    return j;
 }
 
 int grid_levels(int format, float max_fpx) {
@@ -255,7 +278,7 @@ const char* ufp4_status_string(int status) {
     }
 }
 
-const char* ufp4_version(void) { return "0.2.0"; }
+const char* ufp4_version(void) { return "0.3.0"; }
 
 int ufp4_qtensor_bytes(int format, int64_t rows, int64_t red, int64_t* panels, int64_t* code_panel_ld,
                        int64_t* scale_panel_ld, size_t* codes_bytes, size_t* scales_bytes) {
@@ -278,19 +301,20 @@ int ufp4_qtensor_bytes(int format, int64_t rows, int64_t red, int64_t* panels, i
     return UFP4_OK;
 }
 
-int ufp4_grouped_reduction(const int64_t* group_offsets_host, int32_t num_groups, int64_t* padded_offsets_host,
-                           int64_t* red_total) {
+int ufp4_grouped_reduction(const int64_t* group_offsets_host, int32_t num_groups, int32_t block,
+                           int64_t* padded_offsets_host, int64_t* total) {
     if (!group_offsets_host || num_groups < 1) return UFP4_ERR_INVALID_ARG;
+    if (block != 16 && block != 32 && block != 128) return UFP4_ERR_INVALID_ARG;
     if (group_offsets_host[0] != 0) return UFP4_ERR_INVALID_ARG;
     int64_t pad = 0;
     if (padded_offsets_host) padded_offsets_host[0] = 0;
     for (int32_t g = 0; g < num_groups; ++g) {
         const int64_t cnt = group_offsets_host[g + 1] - group_offsets_host[g];
         if (cnt < 0) return UFP4_ERR_INVALID_ARG;
-        pad += ceil_div(cnt, 16) * 16;  // the group's tokens zero-padded to a multiple of 16
+        pad += ceil_div(cnt, block) * block;  // the group's tokens zero-padded to a multiple of the block
         if (padded_offsets_host) padded_offsets_host[g + 1] = pad;
     }
-    if (red_total) *red_total = pad;
+    if (total) *total = pad;
     return UFP4_OK;
 }
 
@@ -467,7 +491,7 @@ int ufp4_quantize_grouped_t(int format, const void* x_dev, int64_t rows, int64_t
     const int st = check_quant_common(format, x_dev, rows, cols, ld, rht, sign_mask, rounding, out, cols, red_total);
     if (st != UFP4_OK) return st;
     const uint16_t mask16 = (uint16_t)sign_mask;
-    record(out, format, cols, red_total, rht ? 16 : 0, &mask16, 0.0f, rounding);
+    record(out, format, cols, red_total, rht ? 16 : 0, &mask16, 0.0f, rounding, UFP4_LAYOUT_GROUPED_RED);
     if (red_total == 0 || cols == 0) return UFP4_OK;
     QuantJob j{};
     j.format = format;
@@ -574,6 +598,129 @@ int ufp4_mx_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, 
     j.scales = out->scales;
     j.scale_pld = out->scale_panel_ld;
     return status_of(launch_quantize_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_quantize_grouped(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,
+                             const int64_t* group_offsets_dev, int32_t num_groups, int64_t padded_total, int rht,
+                             uint32_t sign_mask, int rounding, uint64_t seed, uint32_t stream_id, ufp4_qtensor* out,
+                             void* stream) {
+    if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
+    if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
+    if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
+    if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0 || padded_total < 0) return UFP4_ERR_INVALID_ARG;
+    if (!x_dev || !group_offsets_dev) return UFP4_ERR_INVALID_ARG;
+    if (num_groups < 1) return UFP4_ERR_INVALID_ARG;
+    if (num_groups > max_groups_quantize()) return UFP4_ERR_UNSUPPORTED;
+    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    // transpose 0: [padded_total, cols], groups of rows on whole panels; transpose 1: [cols, padded_total]
+    const int64_t qrows = transpose ? cols : padded_total;
+    const int64_t red = transpose ? padded_total : cols;
+    if (transpose ? padded_total < rows : padded_total % kPanelRows != 0) return UFP4_ERR_SHAPE;
+    const int st = check_storage(out, UFP4_FMT_UNIFORM_MX32, qrows, red);
+    if (st != UFP4_OK) return st;
+    if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    if (!transpose && padded_rows(qrows) / 64 > 65535) return UFP4_ERR_UNSUPPORTED;
+    const uint16_t mask16 = (uint16_t)sign_mask;
+    record(out, UFP4_FMT_UNIFORM_MX32, qrows, red, rht ? 16 : 0, &mask16, 0.0f, rounding,
+           transpose ? UFP4_LAYOUT_GROUPED_RED : UFP4_LAYOUT_GROUPED_ROWS);
+    if (qrows == 0 || red == 0) return UFP4_OK;
+    MxQuantJob j{};
+    j.rounding = rounding;
+    j.rht = rht;
+    j.transpose = transpose;
+    j.x = x_dev;
+    j.xrows = rows;
+    j.ld = ld;
+    j.qrows = qrows;
+    j.red = red;
+    j.group_off = group_offsets_dev;
+    j.num_groups = num_groups;
+    fill_sign_xor(sign_mask, j.qa.sign_xor);
+    j.qa.key0 = (uint32_t)seed;
+    j.qa.key1 = (uint32_t)(seed >> 32);
+    j.qa.stream = stream_id;
+    j.codes = out->codes;
+    j.code_pld = out->code_panel_ld;
+    j.scales = out->scales;
+    j.scale_pld = out->scale_panel_ld;
+    return status_of(launch_quantize_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_gemm_fwd_y_grouped(const ufp4_qtensor* x, const ufp4_qtensor* w, const int64_t* group_offsets_dev,
+                               int32_t num_groups, int64_t m_total, void* y_dev, int64_t ldc, int out_dtype,
+                               void* stream) {
+    if (!group_offsets_dev || num_groups < 1 || m_total < 0) return UFP4_ERR_INVALID_ARG;
+    int st = check_operands(x, w, true);
+    if (st != UFP4_OK) return st;
+    if (x->layout != UFP4_LAYOUT_GROUPED_ROWS || w->layout != UFP4_LAYOUT_PLAIN) return UFP4_ERR_MISMATCH;
+    if (x->red != w->red) return UFP4_ERR_MISMATCH;
+    if (w->rows % num_groups != 0) return UFP4_ERR_SHAPE;
+    const int64_t N = w->rows / num_groups;
+    if (N % kPanelRows != 0) return UFP4_ERR_UNSUPPORTED;  // each group's weight rows start on a panel
+    st = check_output(y_dev, ldc, N, out_dtype);
+    if (st != UFP4_OK) return st;
+    if (m_total == 0 || N == 0 || x->rows == 0) return UFP4_OK;
+    MxGemmJob j = mx_job(x, w, y_dev, ldc, out_dtype);
+    j.mode = kGemmRaggedM;
+    j.M = m_total;
+    j.N = N;
+    j.nkb = x->red / 32;
+    j.offsets = group_offsets_dev;
+    j.G = num_groups;
+    j.m_tiles = ceil_div(x->rows, 256) + num_groups;
+    j.b_group_rows = N;
+    j.b_group_kb = 0;
+    if (j.m_tiles * ceil_div(N, 256) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    return status_of(launch_gemm_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_gemm_bwd_dx_grouped(const ufp4_qtensor* dy, const ufp4_qtensor* wt, const int64_t* group_offsets_dev,
+                                int32_t num_groups, int64_t m_total, void* dx_dev, int64_t ldc, int out_dtype,
+                                void* stream) {
+    if (!group_offsets_dev || num_groups < 1 || m_total < 0) return UFP4_ERR_INVALID_ARG;
+    int st = check_operands(dy, wt, true);
+    if (st != UFP4_OK) return st;
+    if (dy->layout != UFP4_LAYOUT_GROUPED_ROWS || wt->layout != UFP4_LAYOUT_PLAIN) return UFP4_ERR_MISMATCH;
+    if (wt->red != dy->red * num_groups) return UFP4_ERR_MISMATCH;
+    st = check_output(dx_dev, ldc, wt->rows, out_dtype);
+    if (st != UFP4_OK) return st;
+    if (m_total == 0 || wt->rows == 0 || dy->rows == 0) return UFP4_OK;
+    MxGemmJob j = mx_job(dy, wt, dx_dev, ldc, out_dtype);
+    j.mode = kGemmRaggedM;
+    j.M = m_total;
+    j.N = wt->rows;
+    j.nkb = dy->red / 32;
+    j.offsets = group_offsets_dev;
+    j.G = num_groups;
+    j.m_tiles = ceil_div(dy->rows, 256) + num_groups;
+    j.b_group_rows = 0;
+    j.b_group_kb = dy->red / 32;
+    if (j.m_tiles * ceil_div(j.N, 256) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    return status_of(launch_gemm_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_gemm_bwd_dw_grouped(const ufp4_qtensor* dyt, const ufp4_qtensor* xt, const int64_t* group_offsets_dev,
+                                int32_t num_groups, void* dw_dev, int64_t ldc, int out_dtype, void* stream) {
+    if (!group_offsets_dev || num_groups < 1) return UFP4_ERR_INVALID_ARG;
+    if (num_groups > 65535) return UFP4_ERR_UNSUPPORTED;
+    int st = check_operands(dyt, xt, true);
+    if (st != UFP4_OK) return st;
+    if (dyt->layout != UFP4_LAYOUT_GROUPED_RED || xt->layout != UFP4_LAYOUT_GROUPED_RED) return UFP4_ERR_MISMATCH;
+    if (dyt->red != xt->red) return UFP4_ERR_MISMATCH;
+    st = check_output(dw_dev, ldc, xt->rows, out_dtype);
+    if (st != UFP4_OK) return st;
+    if (dyt->rows == 0 || xt->rows == 0) return UFP4_OK;
+    if (ceil_div(dyt->rows, 256) * ceil_div(xt->rows, 256) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    MxGemmJob j = mx_job(dyt, xt, dw_dev, ldc, out_dtype);
+    j.mode = kGemmRaggedK;
+    j.M = dyt->rows;
+    j.N = xt->rows;
+    j.nkb = dyt->red / 32;
+    j.offsets = group_offsets_dev;
+    j.G = num_groups;
+    return status_of(launch_gemm_mx(j, static_cast<hipStream_t>(stream)));
 }
 
 int ufp4_mx_gemm_fwd_y(const ufp4_qtensor* x, const ufp4_qtensor* w, void* y_dev, int64_t ldc, int out_dtype,

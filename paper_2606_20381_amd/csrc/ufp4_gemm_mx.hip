@@ -80,32 +80,139 @@ __device__ __forceinline__ void tile_of(int64_t L, int64_t gy, int64_t gx, int64
     tn = r / rows;
 }
 
+constexpr int64_t kMxBlock32 = 32;  // reduction values per scale block
+
+// Wave-uniform copy (SGPRs) of a value the compiler cannot prove uniform, e.g. one read back from LDS.
+__device__ __forceinline__ int64_t uniform_i64_mx(int64_t v) {
+    const uint64_t u = (uint64_t)v;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Ragged-M: the group and local tile of global m-tile t, with the group's padded row start (a multiple of 128)
+// and its token rows. Wave 0 prefix-sums the per-group tile counts ceil(m_g / 256) and padded lengths
+// pad128(m_g), 64 groups at a time; the result goes through LDS. Every thread calls this; false past the last tile.
+struct MxGroupTile {
+    int64_t g, lt, prow0, trow0, rows;
+};
+__device__ bool resolve_mx_ragged_m(const MxGemmJob& j, int64_t t, int64_t* slot, MxGroupTile& r) {
+    const int tid = threadIdx.x;
+    if (tid == 0) slot[0] = -1;
+    __syncthreads();
+    if (tid < 64) {
+        int64_t tbase = 0, pbase = 0;
+        for (int g0 = 0; g0 < j.G; g0 += 64) {
+            const int g = g0 + tid;
+            int64_t m = 0;
+            if (g < j.G) m = j.offsets[g + 1] - j.offsets[g];
+            if (m < 0) m = 0;
+            const int64_t cnt = (m + kMxTile - 1) / kMxTile, pad = (m + 127) / 128 * 128;
+            int64_t ti = cnt, pi = pad;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int64_t vt = __shfl_up(ti, d, 64), vp = __shfl_up(pi, d, 64);
+                if (tid >= d) {
+                    ti += vt;
+                    pi += vp;
+                }
+            }
+            const int64_t te = tbase + ti - cnt;  // first global tile of group g
+            if (cnt > 0 && te <= t && t < te + cnt) {
+                slot[0] = g;
+                slot[1] = t - te;
+                slot[2] = pbase + pi - pad;
+                slot[3] = m;
+            }
+            tbase += __shfl(ti, 63, 64);
+            pbase += __shfl(pi, 63, 64);
+        }
+    }
+    __syncthreads();
+    r.g = slot[0];
+    if (r.g < 0) return false;
+    r.lt = slot[1];
+    r.prow0 = slot[2] + r.lt * kMxTile;
+    r.trow0 = j.offsets[r.g] + r.lt * kMxTile;
+    r.rows = slot[3] - r.lt * kMxTile;
+    return true;
+}
+
+// Padded start of group g along a ragged reduction (token counts rounded up to 32, summed over h < g) and the
+// group's padded length, by wave 0 through LDS; every thread calls this.
+__device__ void mx_padded_range(const int64_t* off, int g, int64_t* slot, int64_t& start, int64_t& len) {
+    const int tid = threadIdx.x;
+    if (tid < 64) {
+        int64_t sum = 0;
+        for (int h = tid; h < g; h += 64) {
+            const int64_t c = off[h + 1] - off[h];
+            sum += (c > 0 ? c + kMxBlock32 - 1 : 0) / kMxBlock32 * kMxBlock32;
+        }
+#pragma unroll
+        for (int d = 32; d > 0; d >>= 1) sum += __shfl_xor(sum, d, 64);
+        if (tid == 0) slot[0] = sum;
+    }
+    __syncthreads();
+    start = slot[0];
+    const int64_t c = off[g + 1] - off[g];
+    len = (c > 0 ? c + kMxBlock32 - 1 : 0) / kMxBlock32 * kMxBlock32;
+}
+
 template <int OUT>
 __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
     // three separate LDS objects (not an array): the compiler then knows that loads in flight into one buffer
     // do not alias reads of another and does not make the reads wait for them
     __shared__ MxStageSmem sm0, sm1, sm2;
+    __shared__ int64_t s_slot[4];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: load addresses stay scalar
     const int h = lane >> 5, l32 = lane & 31;
     const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows wm * 128 .. + 127, cols wn * 64 .. + 63
     int64_t tm, tn;
-    tile_of(blockIdx.x, (j.M + kMxTile - 1) / kMxTile, (j.N + kMxTile - 1) / kMxTile, tm, tn);
+    const int64_t gy = j.mode == kGemmRaggedM ? j.m_tiles : (j.M + kMxTile - 1) / kMxTile;
+    tile_of(blockIdx.x, gy, (j.N + kMxTile - 1) / kMxTile, tm, tn);
+    // What the tile covers: A panels from pa0, B panels from pb0, reduction blocks from a_kb0 / b_kb0 (nkb of
+    // them), output rows out_row0 .. out_row0 + mrows - 1 (token rows for ragged-M) of the problem at c_base.
+    int64_t pa0 = 2 * tm, pb0 = 2 * tn, a_kb0 = 0, b_kb0 = 0, nkb64 = j.nkb;
+    int64_t out_row0 = tm * kMxTile, mrows = j.M - tm * kMxTile, c_base = 0;
+    if (j.mode == kGemmRaggedM) {
+        MxGroupTile r;
+        if (!resolve_mx_ragged_m(j, tm, s_slot, r)) return;  // the whole workgroup agrees
+        pa0 = r.prow0 / 128;
+        out_row0 = r.trow0;
+        mrows = r.rows < j.M - r.trow0 ? r.rows : j.M - r.trow0;  // token rows past the output are not stored
+        pb0 = (r.g * j.b_group_rows) / 128 + 2 * tn;
+        b_kb0 = r.g * j.b_group_kb;
+    } else if (j.mode == kGemmRaggedK) {
+        int64_t start, len;
+        mx_padded_range(j.offsets, (int)blockIdx.y, s_slot, start, len);
+        a_kb0 = b_kb0 = start / kMxBlock32;
+        nkb64 = len / kMxBlock32;
+        if (a_kb0 + nkb64 > j.nkb) nkb64 = j.nkb - a_kb0 > 0 ? j.nkb - a_kb0 : 0;  // clamped to the operands
+        c_base = (int64_t)blockIdx.y * j.M * j.ldc;
+    }
+    pa0 = uniform_i64_mx(pa0);
+    pb0 = uniform_i64_mx(pb0);
+    a_kb0 = uniform_i64_mx(a_kb0);
+    b_kb0 = uniform_i64_mx(b_kb0);
+    nkb64 = uniform_i64_mx(nkb64);
     // The tile's two panels of each operand. A panel past the operand's last one (a tile over the edge) is
     // replaced by the last panel: those rows only feed outputs that are not stored.
-    const int64_t pa_last = (j.M - 1) / 128, pb_last = (j.N - 1) / 128;
-    const int64_t pa1 = 2 * tm + 1 < pa_last ? 2 * tm + 1 : pa_last;
-    const int64_t pb1 = 2 * tn + 1 < pb_last ? 2 * tn + 1 : pb_last;
-    const uint8_t* const ga0 = j.a + 2 * tm * j.a_pld;
-    const uint8_t* const ga1 = j.a + pa1 * j.a_pld;
-    const uint8_t* const gb0 = j.b + 2 * tn * j.b_pld;
-    const uint8_t* const gb1 = j.b + pb1 * j.b_pld;
+    const int64_t pa_last = (j.a_rows - 1) / 128, pb_last = (j.b_rows - 1) / 128;
+    if (pa0 > pa_last) pa0 = pa_last;  // only for offsets inconsistent with the operand: wrong values, no fault
+    if (pb0 > pb_last) pb0 = pb_last;
+    const int64_t pa1 = pa0 + 1 < pa_last ? pa0 + 1 : pa_last;
+    const int64_t pb1 = pb0 + 1 < pb_last ? pb0 + 1 : pb_last;
+    const uint8_t* const ga0 = j.a + pa0 * j.a_pld + a_kb0 * 3072;
+    const uint8_t* const ga1 = j.a + pa1 * j.a_pld + a_kb0 * 3072;
+    const uint8_t* const gb0 = j.b + pb0 * j.b_pld + b_kb0 * 3072;
+    const uint8_t* const gb1 = j.b + pb1 * j.b_pld + b_kb0 * 3072;
     // this wave's scale run: chunks 16 w .. 16 w + 15 of [A panel 0, A panel 1, B panel 0, B panel 1] x 32
     const int sop = wave >> 2, sp = (wave >> 1) & 1;
-    const uint8_t* const gs = sop == 0 ? j.as + (sp ? pa1 : 2 * tm) * j.as_pld : j.bs + (sp ? pb1 : 2 * tn) * j.bs_pld;
-    const int64_t M = j.M, N = j.N, ldc = j.ldc;
+    const uint8_t* const gs = sop == 0 ? j.as + (sp ? pa1 : pa0) * j.as_pld + a_kb0 * 128
+                                       : j.bs + (sp ? pb1 : pb0) * j.bs_pld + b_kb0 * 128;
+    const int64_t N = j.N, ldc = j.ldc;
     void* const cptr = j.c;
-    const int nkb = (int)j.nkb;
+    const int nkb = (int)nkb64;
     const int nst = (nkb + kMxStageBlocks - 1) / kMxStageBlocks;
     const int kb_last = nkb - 1;
 
@@ -189,12 +296,13 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 
     // Epilogue: lane (l32, h) holds rows 8q + 4h + t (q, t < 4) of column l32 of each 32 x 32 tile; a store
     // instruction writes two runs of 32 consecutive outputs. Tiles inside the output skip the bounds tests.
-    const bool inside = (tm + 1) * kMxTile <= M && (tn + 1) * kMxTile <= N;
+    const bool inside = mrows >= kMxTile && (tn + 1) * kMxTile <= N;
     auto store = [&](int64_t row, int64_t col, float v) {
+        const int64_t off = c_base + row * ldc + col;
         if constexpr (OUT == kOutF32) {
-            static_cast<float*>(cptr)[row * ldc + col] = v;
+            static_cast<float*>(cptr)[off] = v;
         } else {
-            static_cast<uint16_t*>(cptr)[row * ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
+            static_cast<uint16_t*>(cptr)[off] = __builtin_bit_cast(uint16_t, (__bf16)v);  // RNE
         }
     };
 #pragma unroll
@@ -202,15 +310,15 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const int64_t col = tn * kMxTile + wn * 64 + b * 32 + l32;
-            const int64_t row0 = tm * kMxTile + wm * 128 + a * 32 + 4 * h;
+            const int64_t lr0 = wm * 128 + a * 32 + 4 * h;  // tile row of acc element 0
             if (inside) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) store(row0 + 8 * (i >> 2) + (i & 3), col, acc[a][b][i]);
+                for (int i = 0; i < 16; ++i) store(out_row0 + lr0 + 8 * (i >> 2) + (i & 3), col, acc[a][b][i]);
             } else if (col < N) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int64_t row = row0 + 8 * (i >> 2) + (i & 3);
-                    if (row < M) store(row, col, acc[a][b][i]);
+                    const int64_t lr = lr0 + 8 * (i >> 2) + (i & 3);
+                    if (lr < mrows) store(out_row0 + lr, col, acc[a][b][i]);
                 }
             }
         }
@@ -218,9 +326,10 @@ __global__ __launch_bounds__(kMxThreads) void gemm_mx_kernel(MxGemmJob j) {
 }
 
 hipError_t launch_gemm_mx(const MxGemmJob& j, hipStream_t s) {
-    const int64_t tiles = ((j.N + kMxTile - 1) / kMxTile) * ((j.M + kMxTile - 1) / kMxTile);
+    const int64_t gy = j.mode == kGemmRaggedM ? j.m_tiles : (j.M + kMxTile - 1) / kMxTile;
+    const int64_t tiles = ((j.N + kMxTile - 1) / kMxTile) * gy;
     if (tiles == 0) return hipSuccess;
-    const dim3 grid((unsigned)tiles);
+    const dim3 grid((unsigned)tiles, j.mode == kGemmRaggedK ? (unsigned)j.G : 1u);
     if (j.out_dtype == kOutBF16) gemm_mx_kernel<kOutBF16><<<grid, kMxThreads, 0, s>>>(j);
     else gemm_mx_kernel<kOutF32><<<grid, kMxThreads, 0, s>>>(j);
     return hipGetLastError();

@@ -96,6 +96,8 @@ struct DualJob {
 
 hipError_t launch_quantize_dual(const DualJob& job, hipStream_t stream);
 
+enum GemmMode { kGemmDense = 0, kGemmRaggedM = 1, kGemmRaggedK = 2 };
+
 // Power-of-two block scales: the uniform grid with one E8M0 scale per 1x32 block and FP6 E2M3 codes.
 // Operand [rows, red] (red % 32 == 0) in panels of 128 rows; within a panel, 32-block b of all 128 rows is
 // contiguous: codes 128 x 24 bytes at b * 3072, scales 128 bytes at b * 128.
@@ -108,6 +110,11 @@ struct MxQuantJob {
     int64_t xrows, ld;  // X rows and leading dimension (elements)
     int64_t qrows;      // rows of the quantized operand
     int64_t red;        // its reduction length (multiple of 32)
+    // grouped: token offsets [G+1] on the device, else nullptr. Rowwise: groups of rows, each starting on a panel
+    // boundary (qrows = the padded row count); transposed: the reduction axis padded to 32 per group (red = its
+    // padded length)
+    const int64_t* group_off;
+    int32_t num_groups;
     QuantArgs qa;
     void* codes;
     int64_t code_pld;  // bytes between panels
@@ -128,15 +135,25 @@ struct MxGemmJob {
     int64_t b_pld;
     const uint8_t* bs;
     int64_t bs_pld;
-    int64_t M, N, nkb;  // rows of A, rows of B, 32-blocks of the reduction
+    int64_t M, N, nkb;  // rows of A, rows of B (ragged-M: per group), 32-blocks of the reduction
+    int64_t a_rows, b_rows;  // rows stored in the A and B operands (their last panels)
     void* c;
     int64_t ldc;
+    // grouped (mode kGemmRaggedM / kGemmRaggedK of GemmMode below): token offsets [G+1] on the device.
+    // Ragged-M: A holds each group's rows from a panel boundary (row sum_{h<g} pad128(m_h)); B advances by
+    // b_group_rows rows (fwd_y) or b_group_kb 32-blocks of the reduction (bwd_dx) per group; C rows are token rows.
+    // Ragged-K: both operands' reduction is the token axis padded to 32 per group; C holds one [M, N] per group.
+    int mode;
+    const int64_t* offsets;
+    int32_t G;
+    int64_t m_tiles;       // ragged-M: bound on the number of 256-row tiles over all groups
+    int64_t b_group_rows;
+    int64_t b_group_kb;
 };
 
 hipError_t launch_gemm_mx(const MxGemmJob& job, hipStream_t stream);
 
 // Block-scaled NT GEMM: C[i, j] = sum_b sA[i,b] sB[j,b] sum_{k in b} A[i,k] B[j,k] over `nkb` 16-blocks.
-enum GemmMode { kGemmDense = 0, kGemmRaggedM = 1, kGemmRaggedK = 2 };
 
 struct GemmJob {
     int format, out_dtype, mode;

@@ -473,6 +473,52 @@ struct TGroups {
     int32_t G;
 };
 
+// The token offsets of up to kMaxGroupsLds groups into s_off, and into s_poff the padded offsets: group lengths
+// rounded up to multiples of PAD, prefix-summed (thread t owns groups 4t .. 4t + 3; the 256 partial sums are
+// scanned in place). Every thread of a 256-thread workgroup calls this; it ends with a barrier.
+template <int PAD>
+__device__ __forceinline__ void load_group_offsets(const TGroups& grp, int64_t* s_off, int64_t* s_poff) {
+    const int t = threadIdx.x;
+    for (int g = t; g <= grp.G; g += 256) s_off[g] = grp.off[g];
+    if (t == 0) s_poff[0] = 0;
+    __syncthreads();
+    int64_t part[4], run = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int g = 4 * t + k;
+        const int64_t c = g < grp.G ? s_off[g + 1] - s_off[g] : 0;
+        run += (c > 0 ? c + PAD - 1 : 0) / PAD * PAD;
+        part[k] = run;
+    }
+    s_poff[t + 1] = run;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {  // inclusive scan of the 256 partial sums at s_poff[1 ..]
+        const int64_t o = t >= d ? s_poff[t + 1 - d] : 0;
+        __syncthreads();
+        s_poff[t + 1] += o;
+        __syncthreads();
+    }
+    const int64_t base = s_poff[t];  // exclusive prefix of thread t (s_poff[0] is 0)
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int g = 4 * t + k;
+        if (g < grp.G) s_poff[g + 1] = base + part[k];
+    }
+    __syncthreads();
+}
+
+// Last group g with s_poff[g] <= P (G >= 1).
+__device__ __forceinline__ int find_group(const int64_t* s_poff, int G, int64_t P) {
+    int lo = 0, hi = G - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_poff[mid] <= P) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
 // Column groups per workgroup. With 32 a wave reads 512 contiguous bytes of each row (two blocks of 256
 // columns); the block-n RHT kernel keeps 8 so that the m blocks of an n-block lie in one wave.
 constexpr int kXG = 64 / kXC;  // block-n RHT
@@ -488,37 +534,7 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
     __shared__ int64_t s_off[GROUPED ? kMaxGroupsLds + 1 : 1];
     __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
     const int t = threadIdx.x;
-    if constexpr (GROUPED) {
-        // token offsets, and the padded offsets: group lengths rounded up to multiples of 16, prefix-summed
-        // (thread t owns groups 4t .. 4t + 3; the 256 partial sums are scanned in place in s_poff)
-        for (int g = t; g <= grp.G; g += 256) s_off[g] = grp.off[g];
-        if (t == 0) s_poff[0] = 0;
-        __syncthreads();
-        int64_t part[4], run = 0;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int g = 4 * t + k;
-            const int64_t c = g < grp.G ? s_off[g + 1] - s_off[g] : 0;
-            run += (c > 0 ? c + 15 : 0) / 16 * 16;
-            part[k] = run;
-        }
-        s_poff[t + 1] = run;
-        __syncthreads();
-        for (int d = 1; d < 256; d <<= 1) {  // inclusive scan of the 256 partial sums at s_poff[1 ..]
-            const int64_t o = t >= d ? s_poff[t + 1 - d] : 0;
-            __syncthreads();
-            s_poff[t + 1] += o;
-            __syncthreads();
-        }
-        const int64_t base = s_poff[t];  // exclusive prefix of thread t (s_poff[0] is 0)
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int g = 4 * t + k;
-            if (g < grp.G) s_poff[g + 1] = base + part[k];
-        }
-        __syncthreads();
-    }
+    if constexpr (GROUPED) load_group_offsets<kBlock>(grp, s_off, s_poff);
     constexpr int XG = WIDE ? kXG : kXGD, XB = 256 / XG;  // column groups, blocks per workgroup
     // Staged stores (dense RTNE): each half-wave (32 threads, one block of 256 operand rows) puts its 2 KB of
     // codes and 1 KB of scales in its own LDS area in output order and reads them back so that every store
@@ -542,12 +558,7 @@ __global__ __launch_bounds__(256) void quant_cols_kernel(const uint16_t* __restr
         // src0 .. src0 + nvalid - 1 of X, the rest padding
         int64_t src0, nvalid;
         if constexpr (GROUPED) {
-            int lo = 0, hi = grp.G - 1;  // last group with poff[g] <= P0
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (s_poff[mid] <= P0) lo = mid;
-                else hi = mid - 1;
-            }
+            const int lo = find_group(s_poff, grp.G, P0);
             const int64_t local0 = P0 - s_poff[lo];
             src0 = s_off[lo] + local0;
             nvalid = (s_off[lo + 1] - s_off[lo]) - local0;
@@ -934,26 +945,41 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
 // Rowwise: wave w of a workgroup takes 32-block blockIdx.x * 4 + w of 64 consecutive operand rows (lane =
 // row), so the four waves read 256 contiguous bytes of each row and every wave writes three runs of 64 x 8
 // bytes of codes and 64 scale bytes. Rows past the operand's last one (panel padding) get zeros.
-template <int ROUND, bool RHT>
-__global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict__ x, int64_t ld, int64_t qrows,
-                                                      int64_t nb32, QuantArgs qa, uint8_t* __restrict__ codes,
-                                                      int64_t code_pld, uint8_t* __restrict__ scales,
-                                                      int64_t scale_pld) {
+// GROWS (grouped rows, for the ragged-M GEMMs): the operand holds the groups of X's rows one after another, each
+// starting on a panel boundary (group g at row sum_{h<g} pad128(m_h)); a row is quantized exactly as in the plain
+// operand (its SR counters use its row of X), and the rows that pad a group to whole panels are zeros. The 64
+// rows of a workgroup lie in one group's padded range, since groups start at multiples of 128.
+template <int ROUND, bool RHT, bool GROWS>
+__global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict__ x, int64_t xrows, int64_t ld,
+                                                      int64_t qrows, int64_t nb32, TGroups grp, QuantArgs qa,
+                                                      uint8_t* __restrict__ codes, int64_t code_pld,
+                                                      uint8_t* __restrict__ scales, int64_t scale_pld) {
+    __shared__ int64_t s_off[GROWS ? kMaxGroupsLds + 1 : 1];
+    __shared__ int64_t s_poff[GROWS ? kMaxGroupsLds + 1 : 1];
+    if constexpr (GROWS) load_group_offsets<kPanelRows>(grp, s_off, s_poff);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t b = (int64_t)blockIdx.x * 4 + wave;
     if (b >= nb32) return;
-    const int64_t r = (int64_t)blockIdx.y * 64 + lane;
+    const int64_t r = (int64_t)blockIdx.y * 64 + lane;  // operand row
+    int64_t src = r;                                    // row of X
+    bool valid = r < qrows;
+    if constexpr (GROWS) {
+        const int g = find_group(s_poff, grp.G, (int64_t)blockIdx.y * 64);
+        const int64_t local = r - s_poff[g];
+        src = s_off[g] + local;
+        valid = valid && local < s_off[g + 1] - s_off[g] && src >= 0 && src < xrows;
+    }
     uint32_t out[6] = {0, 0, 0, 0, 0, 0};
     uint32_t e8 = 0;
-    if (r < qrows) {
-        const uint4* src = reinterpret_cast<const uint4*>(x + r * ld + b * kMxBlock);
+    if (valid) {
+        const uint4* srcp = reinterpret_cast<const uint4*>(x + src * ld + b * kMxBlock);
         uint32_t w[16];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const uint4 l = src[q];
+            const uint4 l = srcp[q];
             w[4 * q] = l.x; w[4 * q + 1] = l.y; w[4 * q + 2] = l.z; w[4 * q + 3] = l.w;
         }
-        quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * b), (uint32_t)r, out, e8);
+        quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * b), (uint32_t)src, out, e8);
     }
     const int64_t P = r >> 7, ri = r & 127;
     uint8_t* dc = codes + P * code_pld + b * 3072 + ri * 8;  // three planes of 8-byte units
@@ -966,21 +992,39 @@ __global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict
 // column blocks from registers; sixteen threads cover 64 columns, a workgroup 16 row blocks. The four
 // operand rows of a block leave as three runs of 32 bytes of codes and one word of scales. Columns past `cols`
 // (panel padding) hold zeros and quantize to zero codes and scale byte 0.
-template <int ROUND, bool RHT>
+// GROUPED (the ragged reduction of bwd_dw): the reduction axis is X's rows split into groups, each group's tokens
+// zero-padded to a multiple of 32 (a 32-block never straddles two groups); blocks are numbered along the padded
+// axis, of length red_total.
+template <int ROUND, bool RHT, bool GROUPED>
 __global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
-                                                      int64_t ld, QuantArgs qa, uint8_t* __restrict__ codes,
-                                                      int64_t code_pld, uint8_t* __restrict__ scales,
-                                                      int64_t scale_pld) {
+                                                      int64_t ld, int64_t red_total, TGroups grp, QuantArgs qa,
+                                                      uint8_t* __restrict__ codes, int64_t code_pld,
+                                                      uint8_t* __restrict__ scales, int64_t scale_pld) {
+    __shared__ int64_t s_off[GROUPED ? kMaxGroupsLds + 1 : 1];
+    __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
+    if constexpr (GROUPED) load_group_offsets<kMxBlock>(grp, s_off, s_poff);
     const int t = threadIdx.x, cg = t & 15, rb = t >> 4;
     const int64_t cbase = (int64_t)blockIdx.x * 64 + cg * 4;
     const int ncol = cols - cbase < 4 ? (int)(cols - cbase) : 4;
-    const int64_t nblk = rows / kMxBlock;
+    const int64_t nblk = red_total / kMxBlock;
     for (int64_t gb = (int64_t)blockIdx.y * 16 + rb; gb < nblk; gb += (int64_t)gridDim.y * 16) {
+        // rows src0 .. src0 + nvalid - 1 of X feed this block, the rest is padding
+        int64_t src0 = gb * kMxBlock, nvalid = kMxBlock;
+        if constexpr (GROUPED) {
+            const int64_t P0 = gb * kMxBlock;
+            const int g = find_group(s_poff, grp.G, P0);
+            const int64_t local0 = P0 - s_poff[g];
+            src0 = s_off[g] + local0;
+            nvalid = (s_off[g + 1] - s_off[g]) - local0;
+        }
+        if (src0 + nvalid > rows) nvalid = rows - src0;  // offsets beyond X are treated as padding
+        if (src0 < 0 || nvalid < 0) nvalid = 0;
+        if (nvalid > kMxBlock) nvalid = kMxBlock;
         uint32_t v[kMxBlock][2];
-        if (ncol == 4) {
+        if (ncol == 4 && nvalid == kMxBlock) {
 #pragma unroll
             for (int j = 0; j < kMxBlock; ++j) {
-                const uint2 l = *reinterpret_cast<const uint2*>(x + (gb * kMxBlock + j) * ld + cbase);
+                const uint2 l = *reinterpret_cast<const uint2*>(x + (src0 + j) * ld + cbase);
                 v[j][0] = l.x;
                 v[j][1] = l.y;
             }
@@ -988,10 +1032,12 @@ __global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict
 #pragma unroll
             for (int j = 0; j < kMxBlock; ++j) {
                 v[j][0] = v[j][1] = 0;
-                const uint16_t* src = x + (gb * kMxBlock + j) * ld + cbase;
+                if (j < nvalid) {
+                    const uint16_t* src = x + (src0 + j) * ld + cbase;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
+                    for (int k = 0; k < 4; ++k)
+                        if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
+                }
             }
         }
         uint32_t out[4][6], e8[4];
@@ -1283,30 +1329,36 @@ static hipError_t dispatch_dual_fmt(const DualJob& j, hipStream_t s) {
     return j.rounding == kRoundSR ? dispatch_dual_rht<FMT, kRoundSR>(j, s) : dispatch_dual_rht<FMT, kRoundRTNE>(j, s);
 }
 
-template <int ROUND, bool RHT>
+template <int ROUND, bool RHT, bool GR>
 static hipError_t launch_mx_t(const MxQuantJob& j, hipStream_t s) {
     const int64_t prows = padded_rows(j.qrows);
+    const TGroups grp{j.group_off, j.num_groups};
     if (!j.transpose) {
         const int64_t nb32 = j.red / kMxBlock;
         const dim3 grid((unsigned)((nb32 + 3) / 4), (unsigned)(prows / 64));
         if (grid.x == 0 || grid.y == 0) return hipSuccess;
-        mx_rows_kernel<ROUND, RHT><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.ld, j.qrows, nb32, j.qa,
-                                                        static_cast<uint8_t*>(j.codes), j.code_pld,
-                                                        static_cast<uint8_t*>(j.scales), j.scale_pld);
+        mx_rows_kernel<ROUND, RHT, GR><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.ld, j.qrows,
+                                                            nb32, grp, j.qa, static_cast<uint8_t*>(j.codes),
+                                                            j.code_pld, static_cast<uint8_t*>(j.scales), j.scale_pld);
     } else {
         const int64_t gy = (j.red / kMxBlock + 15) / 16;
         const dim3 grid((unsigned)(prows / 64), (unsigned)(gy < 65535 ? gy : 65535));
         if (grid.x == 0 || grid.y == 0) return hipSuccess;
-        mx_cols_kernel<ROUND, RHT><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, j.ld,
-                                                        j.qa, static_cast<uint8_t*>(j.codes), j.code_pld,
-                                                        static_cast<uint8_t*>(j.scales), j.scale_pld);
+        mx_cols_kernel<ROUND, RHT, GR><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, j.ld,
+                                                            j.red, grp, j.qa, static_cast<uint8_t*>(j.codes),
+                                                            j.code_pld, static_cast<uint8_t*>(j.scales), j.scale_pld);
     }
     return hipGetLastError();
 }
 
+template <int ROUND, bool RHT>
+static hipError_t launch_mx_g(const MxQuantJob& j, hipStream_t s) {
+    return j.group_off ? launch_mx_t<ROUND, RHT, true>(j, s) : launch_mx_t<ROUND, RHT, false>(j, s);
+}
+
 hipError_t launch_quantize_mx(const MxQuantJob& j, hipStream_t s) {
-    if (j.rounding == kRoundSR) return j.rht ? launch_mx_t<kRoundSR, true>(j, s) : launch_mx_t<kRoundSR, false>(j, s);
-    return j.rht ? launch_mx_t<kRoundRTNE, true>(j, s) : launch_mx_t<kRoundRTNE, false>(j, s);
+    if (j.rounding == kRoundSR) return j.rht ? launch_mx_g<kRoundSR, true>(j, s) : launch_mx_g<kRoundSR, false>(j, s);
+    return j.rht ? launch_mx_g<kRoundRTNE, true>(j, s) : launch_mx_g<kRoundRTNE, false>(j, s);
 }
 
 hipError_t launch_quantize_dual(const DualJob& j, hipStream_t s) {

@@ -40,10 +40,13 @@ class QDesc(ctypes.Structure):
 
     _fields_ = [("codes", _P), ("scales", _P), ("code_panel_ld", _I64), ("scale_panel_ld", _I64), ("panels", _I64),
                 ("rows", _I64), ("red", _I64), ("format", _I32), ("rht_block", _I32),
-                ("sign_words", ctypes.c_uint16 * 8), ("max_fpx", _F), ("rounding", _I32)]
+                ("sign_words", ctypes.c_uint16 * 8), ("max_fpx", _F), ("rounding", _I32), ("layout", _I32),
+                ("reserved", _I32)]
 
 
-assert ctypes.sizeof(QDesc) == 88
+assert ctypes.sizeof(QDesc) == 96
+# ufp4_qtensor.layout
+LAYOUT_PLAIN, LAYOUT_GROUPED_ROWS, LAYOUT_GROUPED_RED = 0, 1, 2
 
 
 class Metrics(ctypes.Structure):
@@ -61,7 +64,7 @@ SIGNATURES = {
     "ufp4_status_string": ([_INT], ctypes.c_char_p),
     "ufp4_version": ([], ctypes.c_char_p),
     "ufp4_qtensor_bytes": ([_INT, _I64, _I64, _P, _P, _P, _P, _P], _INT),
-    "ufp4_grouped_reduction": ([_P, _I32, _P, _P], _INT),
+    "ufp4_grouped_reduction": ([_P, _I32, _I32, _P, _P], _INT),
     "ufp4_rht_quantize": (_QUANT_ARGS, _INT),
     "ufp4_e2m1_quantize": (_QUANT_ARGS, _INT),
     "ufp4_e2m1_quantize_range": ([_P, _I64, _I64, _I64, _INT, _INT, _U32, _INT, _U64, _U32, _F, _Q, _P], _INT),
@@ -80,6 +83,11 @@ SIGNATURES = {
     "ufp4_mx_gemm_fwd_y": (_GEMM_ARGS, _INT),
     "ufp4_mx_gemm_bwd_dx": (_GEMM_ARGS, _INT),
     "ufp4_mx_gemm_bwd_dw": (_GEMM_ARGS, _INT),
+    "ufp4_mx_quantize_grouped": ([_P, _I64, _I64, _I64, _INT, _P, _I32, _I64, _INT, _U32, _INT, _U64, _U32, _Q, _P],
+                                 _INT),
+    "ufp4_mx_gemm_fwd_y_grouped": ([_Q, _Q, _P, _I32, _I64, _P, _I64, _INT, _P], _INT),
+    "ufp4_mx_gemm_bwd_dx_grouped": ([_Q, _Q, _P, _I32, _I64, _P, _I64, _INT, _P], _INT),
+    "ufp4_mx_gemm_bwd_dw_grouped": (_GEMM_G_ARGS, _INT),
     "ufp4_gemm_fwd_y": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dx": (_GEMM_ARGS, _INT),
     "ufp4_gemm_bwd_dw": (_GEMM_ARGS, _INT),
@@ -152,6 +160,7 @@ class QTensor:
     code_panel_ld = property(lambda self: self.desc.code_panel_ld)
     scale_panel_ld = property(lambda self: self.desc.scale_panel_ld)
     panels = property(lambda self: self.desc.panels)
+    layout = property(lambda self: self.desc.layout)
 
     @property
     def sign_mask(self) -> int:
@@ -363,26 +372,27 @@ def mx_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = True, s
 # grouped (MoE) operands
 # ---------------------------------------------------------------------------------------------------
 
-def group_offsets(counts, device="cuda"):
-    """(token offsets as an int64 tensor [G + 1] on `device`, the padded reduction length of the grouped
-    transposed operands from ufp4_grouped_reduction)."""
+def group_offsets(counts, device="cuda", block: int = 16):
+    """(token offsets as an int64 tensor [G + 1] on `device`, the padded length of the grouped axis from
+    ufp4_grouped_reduction: `block` 16 for the grouped transposed operands, 32 for their power-of-two-scale form,
+    128 for the grouped rows of the power-of-two-scale ragged-M passes)."""
     off = [0]
     for c in counts:
         off.append(off[-1] + int(c))
     arr = (ctypes.c_int64 * len(off))(*off)
     red = _I64()
-    _check(lib().ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(off) - 1, None, ctypes.byref(red)),
-           "ufp4_grouped_reduction")
+    _check(lib().ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(off) - 1, block, None,
+                                        ctypes.byref(red)), "ufp4_grouped_reduction")
     return torch.tensor(off, dtype=torch.int64, device=device), red.value
 
 
-def padded_offsets(offsets_host) -> list:
-    """The padded offsets of the grouped transposed operands (ufp4_grouped_reduction), from host token offsets."""
+def padded_offsets(offsets_host, block: int = 16) -> list:
+    """The padded offsets of a grouped axis (ufp4_grouped_reduction), from host token offsets."""
     off = [int(v) for v in offsets_host]
     arr = (ctypes.c_int64 * len(off))(*off)
     pad = (ctypes.c_int64 * len(off))()
-    _check(lib().ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(off) - 1, ctypes.cast(pad, ctypes.c_void_p),
-                                        None), "ufp4_grouped_reduction")
+    _check(lib().ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(off) - 1, block,
+                                        ctypes.cast(pad, ctypes.c_void_p), None), "ufp4_grouped_reduction")
     return list(pad)
 
 
@@ -494,4 +504,56 @@ def gemm_bwd_dw_grouped(dytq: QTensor, xtq: QTensor, offsets: torch.Tensor, out_
     token offsets are those the grouped operands were quantized with."""
     G = _offsets(offsets)
     return _gemm_grouped("ufp4_gemm_bwd_dw_grouped", dytq, xtq, offsets,
+                         _out((G, dytq.rows, xtq.rows), out_dtype, dytq.codes.device, out))
+
+
+# ---------------------------------------------------------------------------------------------------
+# grouped (MoE) operands and GEMMs with power-of-two 1x32 scales
+# ---------------------------------------------------------------------------------------------------
+
+def mx_quantize_grouped(x: torch.Tensor, offsets: torch.Tensor, padded_total: int, *, transpose: bool, rht: bool = True,
+                        sign_mask: int = 0, rounding: int = RTNE, seed: int = 0, stream_id: int = 0,
+                        out: QTensor | None = None) -> QTensor:
+    """ufp4_mx_quantize_grouped: transpose False gives the grouped-rows operand [padded_total, cols] (each group of
+    X's rows from a panel boundary; padded_total from group_offsets(..., block=128)), True the grouped-reduction
+    operand [cols, padded_total] (each group's tokens padded to 32; block=32)."""
+    _bf16_2d(x)
+    rows, cols = x.shape
+    G = _offsets(offsets)
+    qrows, red = (cols, padded_total) if transpose else (padded_total, cols)
+    q = out if out is not None else empty_qtensor(qrows, red, UNIFORM_MX32, x.device)
+    st = lib().ufp4_mx_quantize_grouped(x.data_ptr(), rows, cols, x.stride(0), int(transpose), offsets.data_ptr(), G,
+                                        padded_total, int(rht), sign_mask, rounding, seed & 0xFFFFFFFFFFFFFFFF,
+                                        stream_id, q.ref(), _stream())
+    _check(st, "ufp4_mx_quantize_grouped")
+    return q
+
+
+def _mx_gemm_ragged_m(name, a: QTensor, b: QTensor, offsets: torch.Tensor, m_total: int, c: torch.Tensor):
+    st = getattr(lib(), name)(a.ref(), b.ref(), offsets.data_ptr(), _offsets(offsets), m_total, c.data_ptr(),
+                              c.stride(-2), _odt(c), _stream())
+    _check(st, name)
+    return c
+
+
+def mx_gemm_fwd_y_grouped(xq: QTensor, wq: QTensor, offsets: torch.Tensor, m_total: int, out_dtype=torch.float32,
+                          out=None) -> torch.Tensor:
+    """Y [m_total, N] per group from the grouped-rows X and W [G*N, K] (ufp4_mx_gemm_fwd_y_grouped)."""
+    n = wq.rows // _offsets(offsets)
+    return _mx_gemm_ragged_m("ufp4_mx_gemm_fwd_y_grouped", xq, wq, offsets, m_total,
+                             _out((m_total, n), out_dtype, xq.codes.device, out))
+
+
+def mx_gemm_bwd_dx_grouped(dyq: QTensor, wtq: QTensor, offsets: torch.Tensor, m_total: int, out_dtype=torch.float32,
+                           out=None) -> torch.Tensor:
+    """dX [m_total, K] per group from the grouped-rows dY and W^T [K, G*N] (ufp4_mx_gemm_bwd_dx_grouped)."""
+    return _mx_gemm_ragged_m("ufp4_mx_gemm_bwd_dx_grouped", dyq, wtq, offsets, m_total,
+                             _out((m_total, wtq.rows), out_dtype, dyq.codes.device, out))
+
+
+def mx_gemm_bwd_dw_grouped(dytq: QTensor, xtq: QTensor, offsets: torch.Tensor, out_dtype=torch.float32,
+                           out=None) -> torch.Tensor:
+    """dW [G, N, K] from the grouped-reduction dY^T and X^T (ufp4_mx_gemm_bwd_dw_grouped)."""
+    G = _offsets(offsets)
+    return _gemm_grouped("ufp4_mx_gemm_bwd_dw_grouped", dytq, xtq, offsets,
                          _out((G, dytq.rows, xtq.rows), out_dtype, dytq.codes.device, out))

@@ -51,20 +51,20 @@ def test_status_strings(lib):
     assert lib.ufp4_status_string(0) == b"ok"
     assert lib.ufp4_status_string(3).startswith(b"misaligned")
     assert lib.ufp4_status_string(4).startswith(b"operands quantized differently")
-    assert lib.ufp4_version() == b"0.2.0"
+    assert lib.ufp4_version() == b"0.3.0"
 
 
 FAKE = 1 << 20  # a 1 MiB-aligned non-null address that is never dereferenced: every call below fails validation
 
 
 def _desc(rows=16, red=32, fmt=U.UNIFORM, rht_block=16, mask=0, codes=FAKE, scales=FAKE, cld=None, sld=None,
-          panels=1):
+          panels=1, layout=0):
     """A descriptor as a quantizer would leave it (storage at FAKE, minimal strides unless given)."""
     mx = fmt == U.UNIFORM_MX32
     nkb = red // (32 if mx else 16)
     d = U.QDesc(codes=codes, scales=scales, code_panel_ld=cld if cld is not None else max(16, nkb * (3072 if mx else 1024)),
                 scale_panel_ld=sld if sld is not None else max(16 if mx else 4, nkb * 128), panels=panels, rows=rows,
-                red=red, format=fmt, rht_block=rht_block)
+                red=red, format=fmt, rht_block=rht_block, layout=layout)
     for k in range(8):
         d.sign_words[k] = (mask >> (16 * k)) & 0xFFFF if k < rht_block // 16 else 0
     return d
@@ -93,11 +93,11 @@ def test_qtensor_bytes(lib):
     assert lib.ufp4_qtensor_bytes(0, -1, 32, None, None, None, None, None) == INVALID
 
 
-def _grouped(lib, offsets):
+def _grouped(lib, offsets, block=16):
     arr = (ctypes.c_int64 * len(offsets))(*offsets)
     pad = (ctypes.c_int64 * len(offsets))()
     red = ctypes.c_int64()
-    st = lib.ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(offsets) - 1,
+    st = lib.ufp4_grouped_reduction(ctypes.cast(arr, ctypes.c_void_p), len(offsets) - 1, block,
                                     ctypes.cast(pad, ctypes.c_void_p), R(red))
     return st, list(pad), red.value
 
@@ -106,9 +106,13 @@ def test_grouped_reduction(lib):
     # counts 0, 1, 16, 17, 33: each rounded up to a multiple of 16 (Sec. 2.2 needs whole RHT blocks per group)
     st, pad, red = _grouped(lib, [0, 0, 1, 17, 34, 67])
     assert st == OK and pad == [0, 0, 16, 32, 64, 112] and red == 112
+    # power-of-two scales: whole 32-blocks along the reduction, whole 128-row panels for grouped rows
+    assert _grouped(lib, [0, 0, 1, 17, 34, 67], 32)[1:] == ([0, 0, 32, 64, 96, 160], 160)
+    assert _grouped(lib, [0, 0, 1, 129, 300], 128)[1:] == ([0, 0, 128, 256, 512], 512)
     assert _grouped(lib, [0, 5, 3])[0] == INVALID      # decreasing offsets
     assert _grouped(lib, [2, 5])[0] == INVALID         # first offset not 0
-    assert lib.ufp4_grouped_reduction(None, 1, None, None) == INVALID
+    assert _grouped(lib, [0, 5], 24)[0] == INVALID     # padding block
+    assert lib.ufp4_grouped_reduction(None, 1, 16, None, None) == INVALID
 
 
 def _metrics(lib, err2, ref2, cross, hist, fmt=0, max_fpx=0.0):
@@ -383,4 +387,53 @@ def test_binding_descriptor_layout_matches_the_header():
     body = re.search(r"typedef struct \{(.*?)\} ufp4_qtensor;", src, re.S).group(1)
     names = re.findall(r"\b(\w+)(?:\[\d+\])?;", body)
     assert names == [f[0] for f in U.QDesc._fields_]
-    assert ctypes.sizeof(U.QDesc) == 88 and U.QDesc.sign_words.offset == 64
+    assert ctypes.sizeof(U.QDesc) == 96 and U.QDesc.sign_words.offset == 64 and U.QDesc.layout.offset == 88
+
+
+def test_mx_grouped_quantizer_validation(lib):
+    q = lib.ufp4_mx_quantize_grouped
+    mx = dict(fmt=U.UNIFORM_MX32)
+    # (x, rows, cols, ld, transpose, offsets, G, padded_total, rht, mask, rounding, seed, stream, out, stream)
+    rows_out = _desc(rows=256, red=64, cld=2 * 3072, sld=2 * 128, panels=2, **mx)
+    assert q(FAKE, 200, 64, 64, 0, None, 2, 256, 1, 0, 0, 0, 0, R(rows_out), None) == INVALID   # no offsets
+    assert q(FAKE, 200, 64, 64, 0, FAKE, 0, 256, 1, 0, 0, 0, 0, R(rows_out), None) == INVALID   # no groups
+    assert q(FAKE, 200, 64, 64, 0, FAKE, 2000, 256, 1, 0, 0, 0, 0, R(rows_out), None) == UNSUPPORTED
+    assert q(FAKE, 200, 64, 64, 0, FAKE, 2, 200, 1, 0, 0, 0, 0, R(rows_out), None) == SHAPE  # not whole panels
+    assert q(FAKE, 200, 64, 64, 0, FAKE, 2, 384, 1, 0, 0, 0, 0, R(rows_out), None) == SHAPE  # 3 panels, room for 2
+    assert q(FAKE, 200, 48, 48, 0, FAKE, 2, 256, 1, 0, 0, 0, 0, R(rows_out), None) == SHAPE  # cols % 32
+    assert q(FAKE, 200, 64, 64, 2, FAKE, 2, 256, 1, 0, 0, 0, 0, R(rows_out), None) == INVALID   # transpose flag
+    assert q(FAKE + 8, 200, 64, 64, 0, FAKE, 2, 256, 1, 0, 0, 0, 0, R(rows_out), None) == ALIGN
+    red_out = _desc(rows=64, red=256, cld=8 * 3072, sld=8 * 128, **mx)
+    assert q(FAKE, 300, 64, 64, 1, FAKE, 2, 256, 1, 0, 0, 0, 0, R(red_out), None) == SHAPE   # padded < rows
+    assert q(FAKE, 200, 64, 64, 1, FAKE, 2, 240, 1, 0, 0, 0, 0, R(red_out), None) == SHAPE   # 240 % 32
+    assert q(FAKE, 200, 64, 64, 1, FAKE, 2, 288, 1, 0, 0, 0, 0, R(red_out), None) == SHAPE   # 9 blocks, room for 8
+
+
+def test_mx_grouped_gemm_checks(lib):
+    mx = dict(fmt=U.UNIFORM_MX32)
+    gr = dict(layout=U.LAYOUT_GROUPED_ROWS, **mx)
+    gk = dict(layout=U.LAYOUT_GROUPED_RED, **mx)
+    fy, fx, fw = lib.ufp4_mx_gemm_fwd_y_grouped, lib.ufp4_mx_gemm_bwd_dx_grouped, lib.ufp4_mx_gemm_bwd_dw_grouped
+    w = _desc(rows=256, red=32, panels=2, **mx)  # two groups of 128 weight rows
+    # (a, b, offsets, G, m_total, c, ldc, out, stream)
+    assert fy(R(_desc(**gr)), R(w), None, 2, 16, FAKE, 128, 0, None) == INVALID        # no offsets
+    assert fy(R(_desc(**gr)), R(w), FAKE, 2, -1, FAKE, 128, 0, None) == INVALID        # negative rows
+    assert fy(R(_desc(**mx)), R(w), FAKE, 2, 16, FAKE, 128, 0, None) == MISMATCH       # X not in grouped rows
+    assert fy(R(_desc(**gr)), R(_desc(rows=256, red=32, panels=2, **gr)), FAKE, 2, 16, FAKE, 128, 0, None) == MISMATCH
+    assert fy(R(_desc(**gr)), R(_desc(rows=256, red=32, panels=2)), FAKE, 2, 16, FAKE, 128, 0, None) == MISMATCH  # 1x16
+    assert fy(R(_desc(red=64, cld=2 * 3072, sld=256, **gr)), R(w), FAKE, 2, 16, FAKE, 128, 0, None) == MISMATCH
+    assert fy(R(_desc(**gr)), R(_desc(rows=96, red=32, **mx)), FAKE, 2, 16, FAKE, 48, 0, None) == UNSUPPORTED  # N=48
+    assert fy(R(_desc(**gr)), R(_desc(rows=255, red=32, panels=2, **mx)), FAKE, 2, 16, FAKE, 128, 0, None) == SHAPE
+    assert fy(R(_desc(**gr)), R(w), FAKE, 2, 16, FAKE, 64, 0, None) == SHAPE            # ldc < N
+    assert fy(R(_desc(mask=1, **gr)), R(_desc(rows=256, red=32, panels=2, mask=2, **mx)), FAKE, 2, 16, FAKE, 128, 0,
+              None) == MISMATCH                                                          # other signs
+    wt = _desc(rows=64, red=64, cld=2 * 3072, sld=256, **mx)  # W^T [K, G*N] with N = 32, G = 2
+    assert fx(R(_desc(**mx)), R(wt), FAKE, 2, 16, FAKE, 64, 0, None) == MISMATCH         # dY not in grouped rows
+    assert fx(R(_desc(**gr)), R(_desc(rows=64, red=96, cld=3 * 3072, sld=384, **mx)), FAKE, 2, 16, FAKE, 64, 0,
+              None) == MISMATCH                                                          # W^T red != G * N
+    assert fx(R(_desc(**gr)), R(wt), FAKE, 2, 16, FAKE, 32, 0, None) == SHAPE             # ldc < K
+    # bwd_dw: both operands grouped along the reduction
+    assert fw(R(_desc(**gk)), R(_desc(**mx)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fw(R(_desc(**gk)), R(_desc(red=64, cld=2 * 3072, sld=256, **gk)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fw(R(_desc(**gk)), R(_desc(**gk)), FAKE, 70000, FAKE, 16, 0, None) == UNSUPPORTED
+    assert fw(R(_desc(**gk)), R(_desc(**gk)), FAKE, 2, FAKE, 8, 0, None) == SHAPE          # ldc < K
