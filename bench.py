@@ -68,7 +68,8 @@ WARMUP_SECONDS = 0.5
 QUANT_BYTES_PER_ELEM = 2.75  # 2 B bf16 in, 0.5 B codes + 0.25 B scale out
 DUAL_BYTES_PER_ELEM = 3.5  # two-operand quantizer: 2 B in, 2 x 0.75 B out
 BYTES_PER_ELEM = {"quant": QUANT_BYTES_PER_ELEM, "quant2": DUAL_BYTES_PER_ELEM, "copy": 2.0,
-                  "quantmx": 2.0 + 0.75 + 1.0 / 32}
+                  "quantmx": 2.0 + 0.75 + 1.0 / 32,  # power-of-two scales: 0.75 B FP6 codes + 1/32 B E8M0 out
+                  "quant2mx": 2.0 + 2 * (0.75 + 1.0 / 32)}
 METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline)"
 
 
@@ -131,9 +132,10 @@ def _quantizers(recipe: str):
     return r.fmt, fn, r.rht[0], r.rht[1], r.rht[2]
 
 
-def dense_step_mx(wl, tl: Timeline):
-    """The layer step with power-of-two 1x32 scales: six quantizations (RHT16 everywhere, SR on dY) and the
-    three passes on the scaled FP6 matrix-core instruction."""
+def dense_step_mx(wl, tl: Timeline, dual: bool = True):
+    """The layer step with power-of-two 1x32 scales: six quantizations (RHT16 everywhere, SR on dY; X and W
+    through the two-operand quantizer unless `dual` is off) and the three passes on the scaled FP6 matrix-core
+    instruction."""
     m, s = wl.sign_mask, wl.seed
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
     M, K = x.shape
@@ -144,25 +146,35 @@ def dense_step_mx(wl, tl: Timeline):
     dx = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
     dw = torch.empty(N, K, dtype=torch.float32, device="cuda")
     Q = U.mx_quantize
+    src = {"x": x, "w": w}
 
     def step(rec):
-        tl.run("quant_x", lambda: Q(x, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: Q(w, sign_mask=m, out=q["w"]), rec)
+        for a in ("x", "w"):
+            if dual:
+                tl.run(f"quant_{a}_{a}t", lambda a=a: U.mx_quantize_dual(
+                    src[a], sign_mask_rows=m, sign_mask_cols=m, out_rows=q[a], out_cols=q[a + "t"]), rec)
+            else:
+                tl.run(f"quant_{a}", lambda a=a: Q(src[a], sign_mask=m, out=q[a]), rec)
+                tl.run(f"quant_{a}t", lambda a=a: Q(src[a], transpose=True, sign_mask=m, out=q[a + "t"]), rec)
         tl.run("quant_dy_sr", lambda: Q(dy, sign_mask=m, rounding=U.SR, seed=s, stream_id=0, out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: Q(w, transpose=True, sign_mask=m, out=q["wt"]), rec)
         tl.run("quant_dyt_sr", lambda: Q(dy, transpose=True, sign_mask=m, rounding=U.SR, seed=s, stream_id=1,
                                          out=q["dyt"]), rec)
-        tl.run("quant_xt", lambda: Q(x, transpose=True, sign_mask=m, out=q["xt"]), rec)
         tl.run("gemm_fwd_y", lambda: U.mx_gemm_fwd_y(q["x"], q["w"], out=y), rec)
         tl.run("gemm_bwd_dx", lambda: U.mx_gemm_bwd_dx(q["dy"], q["wt"], out=dx), rec)
         tl.run("gemm_bwd_dw", lambda: U.mx_gemm_bwd_dw(q["dyt"], q["xt"], out=dw), rec)
 
-    kern = {
-        "quant_x": ("quantmx", M * K), "quant_w": ("quantmx", N * K), "quant_dy_sr": ("quantmx", M * N),
-        "quant_wt": ("quantmx", N * K), "quant_dyt_sr": ("quantmx", M * N), "quant_xt": ("quantmx", M * K),
+    elems = {"x": M * K, "w": N * K}
+    kern = {}
+    for a in ("x", "w"):
+        if dual:
+            kern[f"quant_{a}_{a}t"] = ("quant2mx", elems[a])
+        else:
+            kern.update({f"quant_{a}": ("quantmx", elems[a]), f"quant_{a}t": ("quantmx", elems[a])})
+    kern.update({
+        "quant_dy_sr": ("quantmx", M * N), "quant_dyt_sr": ("quantmx", M * N),
         "gemm_fwd_y": ("gemm", 2 * M * N * K), "gemm_bwd_dx": ("gemm", 2 * M * N * K),
         "gemm_bwd_dw": ("gemm", 2 * M * N * K),
-    }
+    })
     return step, kern
 
 
@@ -170,7 +182,7 @@ def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     """The layer step under a recipe of paper_2606_20381_amd.recipe: six quantizations (X and W through the
     two-operand quantizer where the recipe allows it) and the three GEMMs."""
     if recipe == "mxufp4":
-        return dense_step_mx(wl, tl)
+        return dense_step_mx(wl, tl, dual)
     m, s = wl.sign_mask, wl.seed
     r = R.RECIPES[recipe]
     x, w, dy = (t.cuda() for t in (wl.x, wl.w, wl.dy))
@@ -206,7 +218,7 @@ def dense_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
 
 def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     if recipe == "mxufp4":
-        return moe_step_mx(wl, tl)
+        return moe_step_mx(wl, tl, dual)
     m, s = wl.sign_mask, wl.seed
     fmt, Q, r_y, r_dx, r_dw = _quantizers(recipe)
     E, N, K = wl.w.shape
@@ -255,10 +267,11 @@ def moe_step(wl, tl: Timeline, recipe: str = "ufp4", dual: bool = True):
     return step, kern
 
 
-def moe_step_mx(wl, tl: Timeline):
+def moe_step_mx(wl, tl: Timeline, dual: bool = True):
     """The expert layer step with power-of-two 1x32 scales: X and dY in the grouped-rows form (each expert's rows
     from a panel boundary) for the ragged-M passes, X^T and dY^T with each expert's tokens padded to 32 for
-    bwd_dw, W and W^T plain; RHT16 everywhere, SR on dY."""
+    bwd_dw, W and W^T plain (from the two-operand quantizer unless `dual` is off: W^T's expert groups are N
+    rows each, N % 32 == 0, so the plain transposed operand is the grouped one); RHT16 everywhere, SR on dY."""
     m, s = wl.sign_mask, wl.seed
     E, N, K = wl.w.shape
     x, dy = wl.x.cuda(), wl.dy.cuda()
@@ -276,10 +289,14 @@ def moe_step_mx(wl, tl: Timeline):
 
     def step(rec):
         tl.run("quant_x", lambda: G(x, off, prow, transpose=False, sign_mask=m, out=q["x"]), rec)
-        tl.run("quant_w", lambda: U.mx_quantize(w2, sign_mask=m, out=q["w"]), rec)
+        if dual:
+            tl.run("quant_w_wt", lambda: U.mx_quantize_dual(w2, sign_mask_rows=m, sign_mask_cols=m, out_rows=q["w"],
+                                                            out_cols=q["wt"]), rec)
+        else:
+            tl.run("quant_w", lambda: U.mx_quantize(w2, sign_mask=m, out=q["w"]), rec)
+            tl.run("quant_wt", lambda: U.mx_quantize(w2, transpose=True, sign_mask=m, out=q["wt"]), rec)
         tl.run("quant_dy_sr", lambda: G(dy, off, prow, transpose=False, sign_mask=m, rounding=U.SR, seed=s,
                                         stream_id=0, out=q["dy"]), rec)
-        tl.run("quant_wt", lambda: U.mx_quantize(w2, transpose=True, sign_mask=m, out=q["wt"]), rec)
         tl.run("quant_dyt_sr", lambda: G(dy, off, red32, transpose=True, sign_mask=m, rounding=U.SR, seed=s,
                                          stream_id=1, out=q["dyt"]), rec)
         tl.run("quant_xt", lambda: G(x, off, red32, transpose=True, sign_mask=m, out=q["xt"]), rec)
@@ -288,11 +305,15 @@ def moe_step_mx(wl, tl: Timeline):
         tl.run("gemm_bwd_dw", lambda: U.mx_gemm_bwd_dw_grouped(q["dyt"], q["xt"], off, out=dw), rec)
 
     flops = 2 * M * N * K
-    kern = {
-        "quant_x": ("quantmx", M * K), "quant_w": ("quantmx", E * N * K), "quant_dy_sr": ("quantmx", M * N),
-        "quant_wt": ("quantmx", E * N * K), "quant_dyt_sr": ("quantmx", M * N), "quant_xt": ("quantmx", M * K),
+    kern = {"quant_x": ("quantmx", M * K)}
+    if dual:
+        kern["quant_w_wt"] = ("quant2mx", E * N * K)
+    else:
+        kern.update({"quant_w": ("quantmx", E * N * K), "quant_wt": ("quantmx", E * N * K)})
+    kern.update({
+        "quant_dy_sr": ("quantmx", M * N), "quant_dyt_sr": ("quantmx", M * N), "quant_xt": ("quantmx", M * K),
         "gemm_fwd_y": ("gemm", flops), "gemm_bwd_dx": ("gemm", flops), "gemm_bwd_dw": ("gemm", flops),
-    }
+    })
     return step, kern
 
 
@@ -394,11 +415,13 @@ def e2m1_comparison(wl, steps: int, warmup: int, dual: bool) -> dict:
 
 def quantizer_1gib(steps: int, warmup: int) -> dict:
     """Each quantizer kernel on the 1 GiB bf16 tensor [32768, 16384] (Sec. 5 Q5's measurement): RHT16, both
-    roundings, rowwise, transposed and both operands in one pass, and the E2M1 grid."""
+    roundings, rowwise, transposed and both operands in one pass, the E2M1 grid, and the power-of-two-scale
+    quantizers (rowwise, transposed, both in one pass)."""
     t = WL.quantizer_tensor().cuda()
     rows, cols = t.shape
     qr, qc = U.empty_qtensor(rows, cols), U.empty_qtensor(cols, rows)
     er = U.empty_qtensor(rows, cols, U.E2M1)
+    mr, mc = U.empty_qtensor_mx(rows, cols), U.empty_qtensor_mx(cols, rows)
     m = 0x6A09
     cases = {
         "rows_rtne": (lambda: U.rht_quantize(t, sign_mask=m, out=qr), "quant"),
@@ -409,13 +432,17 @@ def quantizer_1gib(steps: int, warmup: int) -> dict:
         "dual_rtne": (lambda: U.quantize_dual(t, sign_mask_rows=m, sign_mask_cols=m, out_rows=qr, out_cols=qc),
                       "quant2"),
         "rows_e2m1_rtne": (lambda: U.e2m1_quantize(t, rht=True, sign_mask=m, out=er), "quant"),
+        "mx_rows_rtne": (lambda: U.mx_quantize(t, sign_mask=m, out=mr), "quantmx"),
+        "mx_cols_rtne": (lambda: U.mx_quantize(t, transpose=True, sign_mask=m, out=mc), "quantmx"),
+        "mx_dual_rtne": (lambda: U.mx_quantize_dual(t, sign_mask_rows=m, sign_mask_cols=m, out_rows=mr,
+                                                    out_cols=mc), "quant2mx"),
     }
     out = {}
     for label, (fn, kind) in cases.items():
         us = time_steps(lambda rec, fn=fn: fn(), steps, warmup, WARMUP_SECONDS) * 1e3
         gbps = rows * cols * BYTES_PER_ELEM[kind] / (us * 1e-6) / 1e9
         out[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
-    del t, qr, qc, er
+    del t, qr, qc, er, mr, mc
     return out
 
 
@@ -720,7 +747,7 @@ def main():
             gbps = 2 * work / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += 2 * work
-        elif kind in ("quant", "quant2", "quantmx"):
+        elif kind in ("quant", "quant2", "quantmx", "quant2mx"):
             gbps = work * BYTES_PER_ELEM[kind] / (us * 1e-6) / 1e9
             breakdown[label] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
             quant_bytes += work * BYTES_PER_ELEM[kind]
@@ -731,7 +758,8 @@ def main():
             gemm_flops += work
 
     gemm_labels = [k for k, (kind, _) in kern.items() if kind == "gemm"]
-    quant_labels = [k for k, (kind, _) in kern.items() if kind in ("quant", "quant2", "quantmx", "copy")]
+    quant_kinds = ("quant", "quant2", "quantmx", "quant2mx", "copy")
+    quant_labels = [k for k, (kind, _) in kern.items() if kind in quant_kinds]
     if gemm_labels:
         value = gemm_flops / (ms_per_step * 1e-3) / 1e12
         unit = "TFLOP/s"

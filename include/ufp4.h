@@ -336,6 +336,20 @@ int ufp4_mx_quantize(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, 
                      void *stream);
 
 /*
+ * ufp4_mx_quantize_dual -- both power-of-two-scale operands of one tensor from a single read of it: Q_r =
+ *   Q(X H') [rows, cols] along cols and Q_c = Q(X^T H') [cols, rows] along rows, the pair the two GEMMs of a
+ *   training step on X need (Sec. 2.2); equal, bit for bit, to ufp4_mx_quantize with transpose 0 and 1 and
+ *   these arguments. rows % 32 == 0 and cols % 32 == 0; 2^31 rows or columns or more return
+ *   UFP4_ERR_UNSUPPORTED. Each output has its own RHT flag, sign mask and SR stream; rounding and seed
+ *   serve both. The outputs must not overlap each other or the input; the same descriptor for both returns
+ *   UFP4_ERR_INVALID_ARG. Storage, padding rows and errors as ufp4_mx_quantize.
+ */
+int ufp4_mx_quantize_dual(const void *x_dev, int64_t rows, int64_t cols, int64_t ld, int rht_rows,
+                          uint32_t sign_mask_rows, uint32_t stream_rows, int rht_cols, uint32_t sign_mask_cols,
+                          uint32_t stream_cols, int rounding, uint64_t seed, ufp4_qtensor *out_rows,
+                          ufp4_qtensor *out_cols, void *stream);
+
+/*
  * ufp4_mx_gemm_fwd_y / _bwd_dx / _bwd_dw -- the three passes (operand roles as the ufp4_gemm_* calls below) on
  *   operands from ufp4_mx_quantize: C[i, j] = sum_k A[i,k] 2^(eA - 127) B[j,k] 2^(eB - 127) with the scales of
  *   each element's 32-block, accumulated in fp32 by the matrix core; output fp32 or bf16 (RNE) with leading

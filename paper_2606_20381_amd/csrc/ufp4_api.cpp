@@ -576,7 +576,8 @@ int ufp4_mx_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, 
     const int st = check_storage(out, UFP4_FMT_UNIFORM_MX32, qrows, red);
     if (st != UFP4_OK) return st;
     if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
-    if (!transpose && padded_rows(qrows) / 64 > 65535) return UFP4_ERR_UNSUPPORTED;  // one workgroup row per 64
+    if (!transpose && padded_rows(qrows) / 64 > 65535) return UFP4_ERR_UNSUPPORTED;
+    if (mx_tile_count(rows, cols, !transpose, transpose != 0) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     const uint16_t mask16 = (uint16_t)sign_mask;
     record(out, UFP4_FMT_UNIFORM_MX32, qrows, red, rht ? 16 : 0, &mask16, 0.0f, rounding);
     if (rows == 0 || cols == 0) return UFP4_OK;
@@ -598,6 +599,52 @@ int ufp4_mx_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, 
     j.scales = out->scales;
     j.scale_pld = out->scale_panel_ld;
     return status_of(launch_quantize_mx(j, static_cast<hipStream_t>(stream)));
+}
+
+int ufp4_mx_quantize_dual(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int rht_rows,
+                          uint32_t sign_mask_rows, uint32_t stream_rows, int rht_cols, uint32_t sign_mask_cols,
+                          uint32_t stream_cols, int rounding, uint64_t seed, ufp4_qtensor* out_rows,
+                          ufp4_qtensor* out_cols, void* stream) {
+    // Q_r = X [rows, cols] along cols; Q_c = X^T [cols, rows] along rows
+    if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
+    if ((rht_rows != 0 && rht_rows != 1) || (rht_cols != 0 && rht_cols != 1)) return UFP4_ERR_INVALID_ARG;
+    if (sign_mask_rows > 0xFFFFu || sign_mask_cols > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0 || !x_dev) return UFP4_ERR_INVALID_ARG;
+    if (out_rows == out_cols) return UFP4_ERR_INVALID_ARG;
+    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    int st = check_storage(out_rows, UFP4_FMT_UNIFORM_MX32, rows, cols);
+    if (st == UFP4_OK) st = check_storage(out_cols, UFP4_FMT_UNIFORM_MX32, cols, rows);
+    if (st != UFP4_OK) return st;
+    if (rows >= (int64_t(1) << 31) || cols >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
+    if (mx_tile_count(rows, cols, true, true) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;  // 1-D grid
+    const uint16_t mr = (uint16_t)sign_mask_rows, mc = (uint16_t)sign_mask_cols;
+    record(out_rows, UFP4_FMT_UNIFORM_MX32, rows, cols, rht_rows ? 16 : 0, &mr, 0.0f, rounding);
+    record(out_cols, UFP4_FMT_UNIFORM_MX32, cols, rows, rht_cols ? 16 : 0, &mc, 0.0f, rounding);
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    MxDualJob j{};
+    j.rounding = rounding;
+    j.rht_r = rht_rows;
+    j.rht_c = rht_cols;
+    j.x = x_dev;
+    j.rows = rows;
+    j.cols = cols;
+    j.ld = ld;
+    fill_sign_xor(sign_mask_rows, j.qr.sign_xor);
+    fill_sign_xor(sign_mask_cols, j.qc.sign_xor);
+    j.qr.key0 = j.qc.key0 = (uint32_t)seed;
+    j.qr.key1 = j.qc.key1 = (uint32_t)(seed >> 32);
+    j.qr.stream = stream_rows;
+    j.qc.stream = stream_cols;
+    j.codes_r = out_rows->codes;
+    j.code_pld_r = out_rows->code_panel_ld;
+    j.scales_r = out_rows->scales;
+    j.scale_pld_r = out_rows->scale_panel_ld;
+    j.codes_c = out_cols->codes;
+    j.code_pld_c = out_cols->code_panel_ld;
+    j.scales_c = out_cols->scales;
+    j.scale_pld_c = out_cols->scale_panel_ld;
+    return status_of(launch_quantize_mx_dual(j, static_cast<hipStream_t>(stream)));
 }
 
 int ufp4_mx_quantize_grouped(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, int transpose,

@@ -124,6 +124,26 @@ struct MxQuantJob {
 
 hipError_t launch_quantize_mx(const MxQuantJob& job, hipStream_t stream);
 
+// Both operands with power-of-two scales from one read of X [rows, cols] (rows and cols multiples of 32).
+struct MxDualJob {
+    int rounding, rht_r, rht_c;
+    const void* x;
+    int64_t rows, cols, ld;
+    QuantArgs qr, qc;  // per output: signs, SR stream
+    void* codes_r;
+    int64_t code_pld_r;
+    void* scales_r;
+    int64_t scale_pld_r;
+    void* codes_c;
+    int64_t code_pld_c;
+    void* scales_c;
+    int64_t scale_pld_c;
+};
+
+hipError_t launch_quantize_mx_dual(const MxDualJob& job, hipStream_t stream);
+// Workgroups of the power-of-two-scale tile kernel (32 x 256 tiles) for the outputs asked for.
+int64_t mx_tile_count(int64_t rows, int64_t cols, bool rows_out, bool cols_out);
+
 // NT GEMM on two such operands: C[i, j] = sum_k A[i,k] 2^(eA[i,k/32]-127) B[j,k] 2^(eB[j,k/32]-127).
 struct MxGemmJob {
     int out_dtype;

@@ -54,7 +54,7 @@ __device__ __forceinline__ float uniform_sr_level(float v, uint32_t u16) {
     const float vc = __builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f);
     const float lo = floorf(vc);
     const float t = __builtin_fmaf((float)u16, 1.0f / 65536.0f, lo);
-    return (t < vc) ? lo + 1.0f : lo;
+    return lo + ((t < vc) ? 1.0f : 0.0f);  // a zero level comes out as +0
 }
 
 // Eight words whose bits 0-3 hold a nibble and bits 4-21 are clear (higher bits arbitrary) -> one dword,
@@ -836,23 +836,8 @@ __global__ __launch_bounds__(256) void quant_dual_kernel(const uint16_t* __restr
 // consecutive rows' units are contiguous (conflict-free 8-byte LDS reads in the GEMM).
 // ------------------------------------------------------------------------------------------------
 constexpr int kMxBlock = 32;
-
-// Sign-magnitude nibbles of 8 consecutive codes (nibble i = code i) -> E2M3 bytes: b0 = codes 0-3, b1 = 4-7.
-// E2M3 magnitudes of 0..7 are 0, 8, 16, 20, 24, 26, 28, 30 (a byte-permute lookup); the sign goes to bit 5.
-__device__ __forceinline__ void sm_nibbles_to_e2m3(uint32_t p, uint32_t& b0, uint32_t& b1) {
-    const uint32_t ev = p & 0x0F0F0F0Fu;         // nibbles 0, 2, 4, 6
-    const uint32_t od = (p >> 4) & 0x0F0F0F0Fu;  // nibbles 1, 3, 5, 7
-    const uint32_t n0 = __builtin_amdgcn_perm(od, ev, 0x05010400u);  // nibbles 0 1 2 3, one per byte
-    const uint32_t n1 = __builtin_amdgcn_perm(od, ev, 0x07030602u);  // nibbles 4 5 6 7
-    b0 = __builtin_amdgcn_perm(0x1E1C1A18u, 0x14100800u, n0 & 0x07070707u) | ((n0 & 0x08080808u) << 2);
-    b1 = __builtin_amdgcn_perm(0x1E1C1A18u, 0x14100800u, n1 & 0x07070707u) | ((n1 & 0x08080808u) << 2);
-}
-
-// Four 6-bit values, one per byte -> 24 bits c0 | c1 << 6 | c2 << 12 | c3 << 18.
-__device__ __forceinline__ uint32_t pack6x4(uint32_t b) {
-    const uint32_t p = (b & 0x003F003Fu) | ((b >> 2) & 0x0FC00FC0u);
-    return (p & 0xFFFu) | ((p >> 4) & 0xFFF000u);
-}
+typedef float fp6_v16 __attribute__((ext_vector_type(16)));
+typedef uint32_t fp6_u6 __attribute__((ext_vector_type(6)));
 
 // One 32-block: sixteen bf16 pairs in (element 2j in the low half of w[j]); 24 bytes of E2M3 codes and the
 // E8M0 scale byte out. `blk16` numbers the block's first 16-block along the reduction axis (the SR counters
@@ -899,10 +884,10 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
     const int E = fl - 2 > -127 ? fl - 2 : -127;
     e8m0 = amax > 0.0f ? (uint32_t)(E + 127) : 0u;
     const float mult = amax > 0.0f ? __uint_as_float((uint32_t)(127 - P - E) << 23) : 0.0f;  // 2^(-P-E), normal
-    float v[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i) v[i] = __fmul_rn(y[i], mult);
-    uint32_t p[4];
+    // levels as floats (integers -7..7, zero as +0), even elements in `ev`, odd ones in `od`: the E2M3
+    // conversion instruction packs ev[i] at bits 12i and od[i] at bits 12i + 6 of its 192-bit result, and an
+    // integer of magnitude <= 7 is exact in E2M3, so its rounding and the scale operand 1.0 change nothing
+    fp6_v16 ev, od;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         uint32_t u[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -912,34 +897,23 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
             u[0] = p0.x; u[1] = p0.y; u[2] = p0.z; u[3] = p0.w;
             u[4] = p1.x; u[5] = p1.y; u[6] = p1.z; u[7] = p1.w;
         }
-        uint32_t t[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float vi = v[16 * h + i];  // |v| < 8: the top level 7 is the clamp
+            const float vi = __fmul_rn(y[16 * h + i], mult);  // |v| < 8: the top level 7 is the clamp
+            float lv;
             if constexpr (ROUND == kRoundSR) {
                 const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-                t[i] = __float_as_uint(uniform_sr_level(vi, u16) + kMagic8);  // clamps itself
+                lv = uniform_sr_level(vi, u16);
             } else {
-                t[i] = __float_as_uint(__builtin_fminf(__builtin_fmaxf(vi, -7.0f), 7.0f) + kMagic8);
+                lv = __builtin_rintf(__builtin_fminf(__builtin_fmaxf(vi, -7.0f), 7.0f)) + 0.0f;
             }
+            if (i & 1) od[8 * h + (i >> 1)] = lv;
+            else ev[8 * h + (i >> 1)] = lv;
         }
-        p[2 * h] = offset_to_sign_magnitude(pack_nibbles(t));
-        p[2 * h + 1] = offset_to_sign_magnitude(pack_nibbles(t + 8));
     }
-    uint32_t g[8];
+    const fp6_u6 c = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev, od, 1.0f);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        uint32_t b0, b1;
-        sm_nibbles_to_e2m3(p[k], b0, b1);
-        g[2 * k] = pack6x4(b0);
-        g[2 * k + 1] = pack6x4(b1);
-    }
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {  // four 24-bit groups -> three words
-        out[3 * k] = g[4 * k] | (g[4 * k + 1] << 24);
-        out[3 * k + 1] = (g[4 * k + 1] >> 8) | (g[4 * k + 2] << 16);
-        out[3 * k + 2] = (g[4 * k + 2] >> 16) | (g[4 * k + 3] << 8);
-    }
+    for (int k = 0; k < 6; ++k) out[k] = c[k];
 }
 
 // Rowwise: wave w of a workgroup takes 32-block blockIdx.x * 4 + w of 64 consecutive operand rows (lane =
@@ -1329,10 +1303,145 @@ static hipError_t dispatch_dual_fmt(const DualJob& j, hipStream_t s) {
     return j.rounding == kRoundSR ? dispatch_dual_rht<FMT, kRoundSR>(j, s) : dispatch_dual_rht<FMT, kRoundRTNE>(j, s);
 }
 
+// Power-of-two-scale operands of X [rows, cols] (rows % 32 == 0 for Q_c, cols % 32 == 0 for Q_r) by
+// 32 x 256 tiles of X: Q_r [rows, cols] along cols (DO_R) and Q_c [cols, rows] along rows (DO_C), one or both
+// from a single read. Thread t loads 64 contiguous bytes of tile row t / 8, which are one 32-block of that row,
+// and quantizes it for Q_r from its registers; for Q_c it leaves the words in LDS and, after one barrier, reads
+// column t of the tile (32 values, one block of Q_c's row c0 + t) as bf16 pairs. Q_c's stores are consecutive
+// operand rows (coalesced); Q_r's are 8-byte units of eight rows per block. Workgroup L takes row tile
+// L / n_ctiles and column tile L % n_ctiles (consecutive workgroups read adjacent spans of the same rows). Row
+// tiles past the last row, or column tiles past the last column, write only the zero padding rows of the last
+// panels.
+template <int ROUND, bool RHTR, bool RHTC, bool DO_R, bool DO_C>
+__global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                      int64_t ld, uint32_t n_ctiles, QuantArgs qr, QuantArgs qc,
+                                                      uint8_t* __restrict__ codes_r, int64_t cpld_r,
+                                                      uint8_t* __restrict__ scales_r, int64_t spld_r,
+                                                      uint8_t* __restrict__ codes_c, int64_t cpld_c,
+                                                      uint8_t* __restrict__ scales_c, int64_t spld_c) {
+    constexpr int kTW = 256 / 2 + 4;  // LDS words per tile row (16 bytes of padding)
+    __shared__ uint4 tile4[DO_C ? 32 * kTW / 4 : 1];
+    uint32_t* const tile = reinterpret_cast<uint32_t*>(tile4);
+    const int t = threadIdx.x, lr = t >> 3, lb = t & 7;
+    const uint32_t tr = blockIdx.x / n_ctiles, tc = blockIdx.x - tr * n_ctiles;
+    const int64_t r0 = (int64_t)tr * 32, c0 = (int64_t)tc * 256;
+    // --- the row block: row r0 + lr, columns c0 + 32 lb .. + 31
+    const int64_t gr = r0 + lr, gc = c0 + 32 * lb;
+    uint32_t w[16];
+    const bool in = gr < rows && gc + 32 <= cols;  // a 32-block all inside, else (cols % 32 == 0) all outside
+    if (in) {
+        const uint4* src = reinterpret_cast<const uint4*>(x + gr * ld + gc);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint4 l = src[q];
+            w[4 * q] = l.x; w[4 * q + 1] = l.y; w[4 * q + 2] = l.z; w[4 * q + 3] = l.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) w[i] = 0;
+        if (DO_C && !DO_R && gr < rows && gc < cols) {  // Q_c alone allows any column count: a partial block
+            const uint16_t* src = x + gr * ld;
+            for (int i = 0; i < 16; ++i) {
+                const int64_t k = gc + 2 * i;
+                const uint32_t lo = k < cols ? src[k] : 0u, hi = k + 1 < cols ? src[k + 1] : 0u;
+                w[i] = lo | (hi << 16);
+            }
+        }
+    }
+    if constexpr (DO_C) {
+        uint4* const trow = reinterpret_cast<uint4*>(tile + lr * kTW + 16 * lb);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) trow[q] = make_uint4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
+    }
+    if constexpr (DO_R) {
+        if (gr < padded_rows(rows) && gc < cols) {  // a row of Q_r (padding rows of the last panel get zeros)
+            uint32_t out[6] = {0, 0, 0, 0, 0, 0};
+            uint32_t e8 = 0;
+            const int64_t b = gc / kMxBlock;
+            if (in) quant_block32_mx<ROUND, RHTR>(w, qr, (uint32_t)(2 * b), (uint32_t)gr, out, e8);
+            const int64_t P = gr >> 7, ri = gr & 127;
+            uint8_t* dc = codes_r + P * cpld_r + b * 3072 + ri * 8;
+#pragma unroll
+            for (int q = 0; q < 3; ++q)
+                *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
+            scales_r[P * spld_r + b * 128 + ri] = (uint8_t)e8;
+        }
+    }
+    if constexpr (DO_C) {
+        __syncthreads();
+        // --- the column block: column c0 + t, rows r0 .. r0 + 31 (block r0 / 32 of Q_c's row c0 + t)
+        const int64_t cc = c0 + t;
+        if (r0 < rows && cc < padded_rows(cols)) {
+            uint32_t out[6] = {0, 0, 0, 0, 0, 0};
+            uint32_t e8 = 0;
+            if (cc < cols) {
+                const uint32_t sel = (t & 1) ? 0x07060302u : 0x05040100u;
+                uint32_t v[16];
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    v[j] = __builtin_amdgcn_perm(tile[(2 * j + 1) * kTW + (t >> 1)], tile[2 * j * kTW + (t >> 1)], sel);
+                quant_block32_mx<ROUND, RHTC>(v, qc, (uint32_t)(2 * (r0 / kMxBlock)), (uint32_t)cc, out, e8);
+            }
+            const int64_t P = cc >> 7, ri = cc & 127, b = r0 / kMxBlock;
+            uint8_t* dc = codes_c + P * cpld_c + b * 3072 + ri * 8;
+#pragma unroll
+            for (int q = 0; q < 3; ++q)
+                *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
+            scales_c[P * spld_c + b * 128 + ri] = (uint8_t)e8;
+        }
+    }
+}
+
+// Tile counts of mx_tile_kernel's grid: Q_r needs the row tiles of its padded rows and the column tiles of the
+// columns; Q_c the row tiles of the rows and the column tiles of its padded rows.
+template <int ROUND, bool RHTR, bool RHTC, bool DO_R, bool DO_C>
+static hipError_t launch_mx_tiles(const void* x, int64_t rows, int64_t cols, int64_t ld, const QuantArgs& qr,
+                                  const QuantArgs& qc, void* codes_r, int64_t cpld_r, void* scales_r, int64_t spld_r,
+                                  void* codes_c, int64_t cpld_c, void* scales_c, int64_t spld_c, hipStream_t s) {
+    const int64_t n_rt = (DO_R ? padded_rows(rows) : rows) / 32;
+    const int64_t n_ct = ((DO_C ? padded_rows(cols) : cols) + 255) / 256;
+    if (n_rt == 0 || n_ct == 0) return hipSuccess;
+    mx_tile_kernel<ROUND, RHTR, RHTC, DO_R, DO_C><<<dim3((unsigned)(n_rt * n_ct)), 256, 0, s>>>(
+        static_cast<const uint16_t*>(x), rows, cols, ld, (uint32_t)n_ct, qr, qc, static_cast<uint8_t*>(codes_r),
+        cpld_r, static_cast<uint8_t*>(scales_r), spld_r, static_cast<uint8_t*>(codes_c), cpld_c,
+        static_cast<uint8_t*>(scales_c), spld_c);
+    return hipGetLastError();
+}
+
+int64_t mx_tile_count(int64_t rows, int64_t cols, bool do_r, bool do_c) {
+    return ((do_r ? padded_rows(rows) : rows) / 32) * (((do_c ? padded_rows(cols) : cols) + 255) / 256);
+}
+
+template <int ROUND, bool RHTR, bool RHTC>
+static hipError_t launch_mx_dual_t(const MxDualJob& j, hipStream_t s) {
+    return launch_mx_tiles<ROUND, RHTR, RHTC, true, true>(j.x, j.rows, j.cols, j.ld, j.qr, j.qc, j.codes_r,
+                                                          j.code_pld_r, j.scales_r, j.scale_pld_r, j.codes_c,
+                                                          j.code_pld_c, j.scales_c, j.scale_pld_c, s);
+}
+
+template <int ROUND>
+static hipError_t launch_mx_dual_r(const MxDualJob& j, hipStream_t s) {
+    if (j.rht_r) return j.rht_c ? launch_mx_dual_t<ROUND, true, true>(j, s) : launch_mx_dual_t<ROUND, true, false>(j, s);
+    return j.rht_c ? launch_mx_dual_t<ROUND, false, true>(j, s) : launch_mx_dual_t<ROUND, false, false>(j, s);
+}
+
+hipError_t launch_quantize_mx_dual(const MxDualJob& j, hipStream_t s) {
+    return j.rounding == kRoundSR ? launch_mx_dual_r<kRoundSR>(j, s) : launch_mx_dual_r<kRoundRTNE>(j, s);
+}
+
 template <int ROUND, bool RHT, bool GR>
 static hipError_t launch_mx_t(const MxQuantJob& j, hipStream_t s) {
     const int64_t prows = padded_rows(j.qrows);
     const TGroups grp{j.group_off, j.num_groups};
+    if constexpr (!GR) {  // plain operands: the tile kernel with one output
+        if (!j.transpose)
+            return launch_mx_tiles<ROUND, RHT, false, true, false>(j.x, j.xrows, j.red, j.ld, j.qa, j.qa, j.codes,
+                                                                   j.code_pld, j.scales, j.scale_pld, nullptr, 0,
+                                                                   nullptr, 0, s);
+        return launch_mx_tiles<ROUND, false, RHT, false, true>(j.x, j.red, j.qrows, j.ld, j.qa, j.qa, nullptr, 0,
+                                                               nullptr, 0, j.codes, j.code_pld, j.scales, j.scale_pld,
+                                                               s);
+    }
     if (!j.transpose) {
         const int64_t nb32 = j.red / kMxBlock;
         const dim3 grid((unsigned)((nb32 + 3) / 4), (unsigned)(prows / 64));

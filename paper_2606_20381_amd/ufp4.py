@@ -80,6 +80,8 @@ SIGNATURES = {
     "ufp4_quantize_dual": ([_INT, _P, _I64, _I64, _I64, _INT, _U32, _U32, _INT, _U32, _U32, _INT, _U64, _Q, _Q, _P],
                            _INT),
     "ufp4_mx_quantize": (_QUANT_ARGS, _INT),
+    "ufp4_mx_quantize_dual": ([_P, _I64, _I64, _I64, _INT, _U32, _U32, _INT, _U32, _U32, _INT, _U64, _Q, _Q, _P],
+                              _INT),
     "ufp4_mx_gemm_fwd_y": (_GEMM_ARGS, _INT),
     "ufp4_mx_gemm_bwd_dx": (_GEMM_ARGS, _INT),
     "ufp4_mx_gemm_bwd_dw": (_GEMM_ARGS, _INT),
@@ -366,6 +368,23 @@ def mx_quantize(x: torch.Tensor, *, transpose: bool = False, rht: bool = True, s
     """Fused RHT + uniform-grid quantization with power-of-two 1x32 scales (ufp4_mx_quantize)."""
     return _quantize_call("ufp4_mx_quantize", UNIFORM_MX32, x, transpose, rht, sign_mask, rounding, seed, stream_id,
                           out)
+
+
+def mx_quantize_dual(x: torch.Tensor, *, rht_rows: bool = True, rht_cols: bool = True, sign_mask_rows: int = 0,
+                     sign_mask_cols: int = 0, rounding: int = RTNE, seed: int = 0, stream_rows: int = 0,
+                     stream_cols: int = 0, out_rows: QTensor | None = None,
+                     out_cols: QTensor | None = None) -> tuple[QTensor, QTensor]:
+    """Both power-of-two-scale operands of x [rows, cols] from one read (ufp4_mx_quantize_dual): (Q_r [rows, cols]
+    along cols, Q_c [cols, rows] along rows)."""
+    _bf16_2d(x)
+    rows, cols = x.shape
+    qr = out_rows if out_rows is not None else empty_qtensor_mx(rows, cols, x.device)
+    qc = out_cols if out_cols is not None else empty_qtensor_mx(cols, rows, x.device)
+    st = lib().ufp4_mx_quantize_dual(x.data_ptr(), rows, cols, x.stride(0), int(rht_rows), sign_mask_rows,
+                                     stream_rows, int(rht_cols), sign_mask_cols, stream_cols, rounding,
+                                     seed & 0xFFFFFFFFFFFFFFFF, qr.ref(), qc.ref(), _stream())
+    _check(st, "ufp4_mx_quantize_dual")
+    return qr, qc
 
 
 # ---------------------------------------------------------------------------------------------------

@@ -241,6 +241,33 @@ def test_mx_quantizer_validation(lib):
     assert q(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, d(cld=1 << 30), None) == UNSUPPORTED  # stride > 2^29
 
 
+def test_mx_dual_validation(lib):
+    C32, S32 = 3072, 128
+    q = lib.ufp4_mx_quantize_dual
+
+    def d(rows=64, red=64, **kw):
+        return _desc(rows=rows, red=red, fmt=U.UNIFORM_MX32, **kw)
+
+    dr, dc = d(), d()
+
+    def call(x=FAKE, rows=64, cols=64, ld=64, rht_r=1, rht_c=1, mr=0, mc=0, rnd=0, out_r=None, out_c=None):
+        return q(x, rows, cols, ld, rht_r, mr, 0, rht_c, mc, 1, rnd, 0, R(out_r or dr), R(out_c or dc), None)
+
+    assert call(rows=48, out_c=d(red=48, cld=2 * C32, sld=2 * S32)) == SHAPE  # rows % 32 (Q_c's reduction)
+    assert call(cols=48, ld=48) == SHAPE                                     # cols % 32 (Q_r's reduction)
+    assert call(ld=56) == SHAPE                                              # ld < cols
+    assert call(cols=32, ld=36) == SHAPE                                     # ld % 8
+    assert call(x=FAKE + 2) == ALIGN
+    assert call(x=None) == INVALID
+    assert call(rnd=2) == INVALID
+    assert call(rht_c=2) == INVALID
+    assert call(mr=0x10000) == INVALID
+    assert call(rows=-32) == INVALID
+    assert call(out_r=d(cld=C32)) == SHAPE                                   # code stride < 3072 nkb
+    assert call(out_c=d(cld=2 * C32 + 8)) == ALIGN                           # code stride % 16
+    assert q(FAKE, 64, 64, 64, 1, 0, 0, 1, 0, 1, 0, 0, R(dr), R(dr), None) == INVALID  # one descriptor for both
+
+
 def test_quant_stats_validation(lib):
     """ufp4_quant_stats(format, max_fpx, x, rows, cols, ld, transpose, rht, mask, rounding, seed, stream, rec)"""
     ok = (0, 0.0, FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, FAKE)
