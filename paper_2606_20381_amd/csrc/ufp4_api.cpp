@@ -669,6 +669,8 @@ int ufp4_mx_quantize_grouped(const void* x_dev, int64_t rows, int64_t cols, int6
     if (st != UFP4_OK) return st;
     if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     if (!transpose && padded_rows(qrows) / 64 > 65535) return UFP4_ERR_UNSUPPORTED;
+    // grid y: chunks of four 256-column tiles of X (its padded columns for the transposed form)
+    if (((transpose ? padded_rows(cols) : cols) + 1023) / 1024 > 65535) return UFP4_ERR_UNSUPPORTED;
     const uint16_t mask16 = (uint16_t)sign_mask;
     record(out, UFP4_FMT_UNIFORM_MX32, qrows, red, rht ? 16 : 0, &mask16, 0.0f, rounding,
            transpose ? UFP4_LAYOUT_GROUPED_RED : UFP4_LAYOUT_GROUPED_ROWS);

@@ -474,32 +474,42 @@ struct TGroups {
 };
 
 // The token offsets of up to kMaxGroupsLds groups into s_off, and into s_poff the padded offsets: group lengths
-// rounded up to multiples of PAD, prefix-summed (thread t owns groups 4t .. 4t + 3; the 256 partial sums are
-// scanned in place). Every thread of a 256-thread workgroup calls this; it ends with a barrier.
+// rounded up to multiples of PAD, prefix-summed. Thread t owns groups 4t .. 4t + 3 (read straight from global
+// memory); the 256 partial sums are scanned with wave shuffles and one exchange of the four wave totals, so the
+// whole call costs two barriers. Every thread of a 256-thread workgroup calls this; it ends with a barrier.
 template <int PAD>
 __device__ __forceinline__ void load_group_offsets(const TGroups& grp, int64_t* s_off, int64_t* s_poff) {
-    const int t = threadIdx.x;
-    for (int g = t; g <= grp.G; g += 256) s_off[g] = grp.off[g];
-    if (t == 0) s_poff[0] = 0;
-    __syncthreads();
+    __shared__ int64_t s_wave[4];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    int64_t o[5];
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+        const int g = 4 * t + k;
+        o[k] = g <= grp.G ? grp.off[g] : 0;
+    }
     int64_t part[4], run = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int g = 4 * t + k;
-        const int64_t c = g < grp.G ? s_off[g + 1] - s_off[g] : 0;
+        const int64_t c = g < grp.G ? o[k + 1] - o[k] : 0;
         run += (c > 0 ? c + PAD - 1 : 0) / PAD * PAD;
         part[k] = run;
+        if (g < grp.G) s_off[g] = o[k];
     }
-    s_poff[t + 1] = run;
-    __syncthreads();
-    for (int d = 1; d < 256; d <<= 1) {  // inclusive scan of the 256 partial sums at s_poff[1 ..]
-        const int64_t o = t >= d ? s_poff[t + 1 - d] : 0;
-        __syncthreads();
-        s_poff[t + 1] += o;
-        __syncthreads();
+    if (t == 0) {
+        s_off[grp.G] = grp.off[grp.G];
+        s_poff[0] = 0;
     }
-    const int64_t base = s_poff[t];  // exclusive prefix of thread t (s_poff[0] is 0)
+    int64_t incl = run;  // inclusive scan over the wave
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t v = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += v;
+    }
+    if (lane == 63) s_wave[wave] = incl;
     __syncthreads();
+    int64_t base = incl - run;
+    for (int w = 0; w < wave; ++w) base += s_wave[w];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int g = 4 * t + k;
@@ -916,126 +926,6 @@ __device__ __forceinline__ void quant_block32_mx(const uint32_t (&w)[16], const 
     for (int k = 0; k < 6; ++k) out[k] = c[k];
 }
 
-// Rowwise: wave w of a workgroup takes 32-block blockIdx.x * 4 + w of 64 consecutive operand rows (lane =
-// row), so the four waves read 256 contiguous bytes of each row and every wave writes three runs of 64 x 8
-// bytes of codes and 64 scale bytes. Rows past the operand's last one (panel padding) get zeros.
-// GROWS (grouped rows, for the ragged-M GEMMs): the operand holds the groups of X's rows one after another, each
-// starting on a panel boundary (group g at row sum_{h<g} pad128(m_h)); a row is quantized exactly as in the plain
-// operand (its SR counters use its row of X), and the rows that pad a group to whole panels are zeros. The 64
-// rows of a workgroup lie in one group's padded range, since groups start at multiples of 128.
-template <int ROUND, bool RHT, bool GROWS>
-__global__ __launch_bounds__(256) void mx_rows_kernel(const uint16_t* __restrict__ x, int64_t xrows, int64_t ld,
-                                                      int64_t qrows, int64_t nb32, TGroups grp, QuantArgs qa,
-                                                      uint8_t* __restrict__ codes, int64_t code_pld,
-                                                      uint8_t* __restrict__ scales, int64_t scale_pld) {
-    __shared__ int64_t s_off[GROWS ? kMaxGroupsLds + 1 : 1];
-    __shared__ int64_t s_poff[GROWS ? kMaxGroupsLds + 1 : 1];
-    if constexpr (GROWS) load_group_offsets<kPanelRows>(grp, s_off, s_poff);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t b = (int64_t)blockIdx.x * 4 + wave;
-    if (b >= nb32) return;
-    const int64_t r = (int64_t)blockIdx.y * 64 + lane;  // operand row
-    int64_t src = r;                                    // row of X
-    bool valid = r < qrows;
-    if constexpr (GROWS) {
-        const int g = find_group(s_poff, grp.G, (int64_t)blockIdx.y * 64);
-        const int64_t local = r - s_poff[g];
-        src = s_off[g] + local;
-        valid = valid && local < s_off[g + 1] - s_off[g] && src >= 0 && src < xrows;
-    }
-    uint32_t out[6] = {0, 0, 0, 0, 0, 0};
-    uint32_t e8 = 0;
-    if (valid) {
-        const uint4* srcp = reinterpret_cast<const uint4*>(x + src * ld + b * kMxBlock);
-        uint32_t w[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const uint4 l = srcp[q];
-            w[4 * q] = l.x; w[4 * q + 1] = l.y; w[4 * q + 2] = l.z; w[4 * q + 3] = l.w;
-        }
-        quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * b), (uint32_t)src, out, e8);
-    }
-    const int64_t P = r >> 7, ri = r & 127;
-    uint8_t* dc = codes + P * code_pld + b * 3072 + ri * 8;  // three planes of 8-byte units
-#pragma unroll
-    for (int q = 0; q < 3; ++q) *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
-    scales[P * scale_pld + b * 128 + ri] = (uint8_t)e8;
-}
-
-// Transposed: a thread loads 32 rows x 4 columns of X (one 8-byte load per row) and quantizes the four
-// column blocks from registers; sixteen threads cover 64 columns, a workgroup 16 row blocks. The four
-// operand rows of a block leave as three runs of 32 bytes of codes and one word of scales. Columns past `cols`
-// (panel padding) hold zeros and quantize to zero codes and scale byte 0.
-// GROUPED (the ragged reduction of bwd_dw): the reduction axis is X's rows split into groups, each group's tokens
-// zero-padded to a multiple of 32 (a 32-block never straddles two groups); blocks are numbered along the padded
-// axis, of length red_total.
-template <int ROUND, bool RHT, bool GROUPED>
-__global__ __launch_bounds__(256) void mx_cols_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
-                                                      int64_t ld, int64_t red_total, TGroups grp, QuantArgs qa,
-                                                      uint8_t* __restrict__ codes, int64_t code_pld,
-                                                      uint8_t* __restrict__ scales, int64_t scale_pld) {
-    __shared__ int64_t s_off[GROUPED ? kMaxGroupsLds + 1 : 1];
-    __shared__ int64_t s_poff[GROUPED ? kMaxGroupsLds + 1 : 1];
-    if constexpr (GROUPED) load_group_offsets<kMxBlock>(grp, s_off, s_poff);
-    const int t = threadIdx.x, cg = t & 15, rb = t >> 4;
-    const int64_t cbase = (int64_t)blockIdx.x * 64 + cg * 4;
-    const int ncol = cols - cbase < 4 ? (int)(cols - cbase) : 4;
-    const int64_t nblk = red_total / kMxBlock;
-    for (int64_t gb = (int64_t)blockIdx.y * 16 + rb; gb < nblk; gb += (int64_t)gridDim.y * 16) {
-        // rows src0 .. src0 + nvalid - 1 of X feed this block, the rest is padding
-        int64_t src0 = gb * kMxBlock, nvalid = kMxBlock;
-        if constexpr (GROUPED) {
-            const int64_t P0 = gb * kMxBlock;
-            const int g = find_group(s_poff, grp.G, P0);
-            const int64_t local0 = P0 - s_poff[g];
-            src0 = s_off[g] + local0;
-            nvalid = (s_off[g + 1] - s_off[g]) - local0;
-        }
-        if (src0 + nvalid > rows) nvalid = rows - src0;  // offsets beyond X are treated as padding
-        if (src0 < 0 || nvalid < 0) nvalid = 0;
-        if (nvalid > kMxBlock) nvalid = kMxBlock;
-        uint32_t v[kMxBlock][2];
-        if (ncol == 4 && nvalid == kMxBlock) {
-#pragma unroll
-            for (int j = 0; j < kMxBlock; ++j) {
-                const uint2 l = *reinterpret_cast<const uint2*>(x + (src0 + j) * ld + cbase);
-                v[j][0] = l.x;
-                v[j][1] = l.y;
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < kMxBlock; ++j) {
-                v[j][0] = v[j][1] = 0;
-                if (j < nvalid) {
-                    const uint16_t* src = x + (src0 + j) * ld + cbase;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        if (k < ncol) v[j][k >> 1] |= (uint32_t)src[k] << (16 * (k & 1));
-                }
-            }
-        }
-        uint32_t out[4][6], e8[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
-            uint32_t w[16];
-#pragma unroll
-            for (int j = 0; j < 16; ++j) w[j] = __builtin_amdgcn_perm(v[2 * j + 1][q >> 1], v[2 * j][q >> 1], sel);
-            quant_block32_mx<ROUND, RHT>(w, qa, (uint32_t)(2 * gb), (uint32_t)(cbase + q), out[q], e8[q]);
-        }
-        const int64_t P = cbase >> 7, ri = cbase & 127;
-        uint8_t* dc = codes + P * code_pld + gb * 3072 + ri * 8;  // per plane, 4 rows x 8 bytes = 32 bytes
-#pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            uint4* d = reinterpret_cast<uint4*>(dc + q * 1024);
-            d[0] = make_uint4(out[0][2 * q], out[0][2 * q + 1], out[1][2 * q], out[1][2 * q + 1]);
-            d[1] = make_uint4(out[2][2 * q], out[2][2 * q + 1], out[3][2 * q], out[3][2 * q + 1]);
-        }
-        *reinterpret_cast<uint32_t*>(scales + P * scale_pld + gb * 128 + ri) =
-            e8[0] | (e8[1] << 8) | (e8[2] << 16) | (e8[3] << 24);
-    }
-}
-
 // ------------------------------------------------------------------------------------------------
 // Host-side launchers
 // ------------------------------------------------------------------------------------------------
@@ -1303,47 +1193,50 @@ static hipError_t dispatch_dual_fmt(const DualJob& j, hipStream_t s) {
     return j.rounding == kRoundSR ? dispatch_dual_rht<FMT, kRoundSR>(j, s) : dispatch_dual_rht<FMT, kRoundRTNE>(j, s);
 }
 
-// Power-of-two-scale operands of X [rows, cols] (rows % 32 == 0 for Q_c, cols % 32 == 0 for Q_r) by
-// 32 x 256 tiles of X: Q_r [rows, cols] along cols (DO_R) and Q_c [cols, rows] along rows (DO_C), one or both
-// from a single read. Thread t loads 64 contiguous bytes of tile row t / 8, which are one 32-block of that row,
-// and quantizes it for Q_r from its registers; for Q_c it leaves the words in LDS and, after one barrier, reads
-// column t of the tile (32 values, one block of Q_c's row c0 + t) as bf16 pairs. Q_c's stores are consecutive
-// operand rows (coalesced); Q_r's are 8-byte units of eight rows per block. Workgroup L takes row tile
-// L / n_ctiles and column tile L % n_ctiles (consecutive workgroups read adjacent spans of the same rows). Row
-// tiles past the last row, or column tiles past the last column, write only the zero padding rows of the last
-// panels.
+// Power-of-two-scale operands of X [rows, cols] by 32 x 256 tiles of X: Q_r along cols (DO_R; cols % 32 == 0)
+// and Q_c = X^T along rows (DO_C; 32 tile rows per reduction block), one or both from a single read. Thread t
+// loads 64 contiguous bytes of tile row t / 8 (the X row `src`, or zeros where src < 0), which are one 32-block of
+// that row, and quantizes it for Q_r from its registers as row `qr_row` (SR counters: row src); for Q_c it
+// leaves the words in LDS and, after one barrier, reads column t of the tile (32 values, block `qc_blk` of Q_c's
+// row c0 + t) as bf16 pairs. Q_c's stores are consecutive operand rows (coalesced); Q_r's are 8-byte units of
+// eight rows per block. Rows of Q_r below qr_prows past the data, and Q_c rows past the last column, are written
+// as zero padding.
+struct MxTileOut {
+    uint8_t* codes_r;
+    int64_t cpld_r;
+    uint8_t* scales_r;
+    int64_t spld_r;
+    uint8_t* codes_c;
+    int64_t cpld_c;
+    uint8_t* scales_c;
+    int64_t spld_c;
+};
+
 template <int ROUND, bool RHTR, bool RHTC, bool DO_R, bool DO_C>
-__global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
-                                                      int64_t ld, uint32_t n_ctiles, QuantArgs qr, QuantArgs qc,
-                                                      uint8_t* __restrict__ codes_r, int64_t cpld_r,
-                                                      uint8_t* __restrict__ scales_r, int64_t spld_r,
-                                                      uint8_t* __restrict__ codes_c, int64_t cpld_c,
-                                                      uint8_t* __restrict__ scales_c, int64_t spld_c) {
+__device__ __forceinline__ void mx_tile(const uint16_t* __restrict__ x, int64_t cols, int64_t ld, int64_t src,
+                                        int64_t qr_row, int64_t qr_prows, int64_t qc_blk, int64_t c0,
+                                        const QuantArgs& qr, const QuantArgs& qc, const MxTileOut& o,
+                                        uint32_t* tile) {
     constexpr int kTW = 256 / 2 + 4;  // LDS words per tile row (16 bytes of padding)
-    __shared__ uint4 tile4[DO_C ? 32 * kTW / 4 : 1];
-    uint32_t* const tile = reinterpret_cast<uint32_t*>(tile4);
     const int t = threadIdx.x, lr = t >> 3, lb = t & 7;
-    const uint32_t tr = blockIdx.x / n_ctiles, tc = blockIdx.x - tr * n_ctiles;
-    const int64_t r0 = (int64_t)tr * 32, c0 = (int64_t)tc * 256;
-    // --- the row block: row r0 + lr, columns c0 + 32 lb .. + 31
-    const int64_t gr = r0 + lr, gc = c0 + 32 * lb;
+    const int64_t gc = c0 + 32 * lb;
     uint32_t w[16];
-    const bool in = gr < rows && gc + 32 <= cols;  // a 32-block all inside, else (cols % 32 == 0) all outside
+    const bool in = src >= 0 && gc + 32 <= cols;
     if (in) {
-        const uint4* src = reinterpret_cast<const uint4*>(x + gr * ld + gc);
+        const uint4* sp = reinterpret_cast<const uint4*>(x + src * ld + gc);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const uint4 l = src[q];
+            const uint4 l = sp[q];
             w[4 * q] = l.x; w[4 * q + 1] = l.y; w[4 * q + 2] = l.z; w[4 * q + 3] = l.w;
         }
     } else {
 #pragma unroll
         for (int i = 0; i < 16; ++i) w[i] = 0;
-        if (DO_C && !DO_R && gr < rows && gc < cols) {  // Q_c alone allows any column count: a partial block
-            const uint16_t* src = x + gr * ld;
+        if (DO_C && !DO_R && src >= 0 && gc < cols) {  // Q_c alone allows any column count: a partial block
+            const uint16_t* sp = x + src * ld;
             for (int i = 0; i < 16; ++i) {
                 const int64_t k = gc + 2 * i;
-                const uint32_t lo = k < cols ? src[k] : 0u, hi = k + 1 < cols ? src[k + 1] : 0u;
+                const uint32_t lo = k < cols ? sp[k] : 0u, hi = k + 1 < cols ? sp[k + 1] : 0u;
                 w[i] = lo | (hi << 16);
             }
         }
@@ -1354,24 +1247,23 @@ __global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict
         for (int q = 0; q < 4; ++q) trow[q] = make_uint4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
     }
     if constexpr (DO_R) {
-        if (gr < padded_rows(rows) && gc < cols) {  // a row of Q_r (padding rows of the last panel get zeros)
+        if (qr_row < qr_prows && gc < cols) {
             uint32_t out[6] = {0, 0, 0, 0, 0, 0};
             uint32_t e8 = 0;
             const int64_t b = gc / kMxBlock;
-            if (in) quant_block32_mx<ROUND, RHTR>(w, qr, (uint32_t)(2 * b), (uint32_t)gr, out, e8);
-            const int64_t P = gr >> 7, ri = gr & 127;
-            uint8_t* dc = codes_r + P * cpld_r + b * 3072 + ri * 8;
+            if (in) quant_block32_mx<ROUND, RHTR>(w, qr, (uint32_t)(2 * b), (uint32_t)src, out, e8);
+            const int64_t P = qr_row >> 7, ri = qr_row & 127;
+            uint8_t* dc = o.codes_r + P * o.cpld_r + b * 3072 + ri * 8;
 #pragma unroll
             for (int q = 0; q < 3; ++q)
                 *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
-            scales_r[P * spld_r + b * 128 + ri] = (uint8_t)e8;
+            o.scales_r[P * o.spld_r + b * 128 + ri] = (uint8_t)e8;
         }
     }
     if constexpr (DO_C) {
         __syncthreads();
-        // --- the column block: column c0 + t, rows r0 .. r0 + 31 (block r0 / 32 of Q_c's row c0 + t)
         const int64_t cc = c0 + t;
-        if (r0 < rows && cc < padded_rows(cols)) {
+        if (qc_blk >= 0 && cc < padded_rows(cols)) {
             uint32_t out[6] = {0, 0, 0, 0, 0, 0};
             uint32_t e8 = 0;
             if (cc < cols) {
@@ -1380,15 +1272,71 @@ __global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict
 #pragma unroll
                 for (int j = 0; j < 16; ++j)
                     v[j] = __builtin_amdgcn_perm(tile[(2 * j + 1) * kTW + (t >> 1)], tile[2 * j * kTW + (t >> 1)], sel);
-                quant_block32_mx<ROUND, RHTC>(v, qc, (uint32_t)(2 * (r0 / kMxBlock)), (uint32_t)cc, out, e8);
+                quant_block32_mx<ROUND, RHTC>(v, qc, (uint32_t)(2 * qc_blk), (uint32_t)cc, out, e8);
             }
-            const int64_t P = cc >> 7, ri = cc & 127, b = r0 / kMxBlock;
-            uint8_t* dc = codes_c + P * cpld_c + b * 3072 + ri * 8;
+            const int64_t P = cc >> 7, ri = cc & 127;
+            uint8_t* dc = o.codes_c + P * o.cpld_c + qc_blk * 3072 + ri * 8;
 #pragma unroll
             for (int q = 0; q < 3; ++q)
                 *reinterpret_cast<uint2*>(dc + q * 1024) = make_uint2(out[2 * q], out[2 * q + 1]);
-            scales_c[P * spld_c + b * 128 + ri] = (uint8_t)e8;
+            o.scales_c[P * o.spld_c + qc_blk * 128 + ri] = (uint8_t)e8;
         }
+    }
+}
+
+constexpr int kMxTileWords = 32 * (256 / 2 + 4);
+
+// Plain operands: workgroup L takes row tile L / n_ctiles and column tile L % n_ctiles (consecutive workgroups
+// read adjacent spans of the same rows).
+template <int ROUND, bool RHTR, bool RHTC, bool DO_R, bool DO_C>
+__global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                      int64_t ld, uint32_t n_ctiles, QuantArgs qr, QuantArgs qc,
+                                                      MxTileOut o) {
+    __shared__ uint4 tile4[DO_C ? kMxTileWords / 4 : 1];
+    const uint32_t tr = blockIdx.x / n_ctiles, tc = blockIdx.x - tr * n_ctiles;
+    const int64_t r0 = (int64_t)tr * 32, gr = r0 + (threadIdx.x >> 3);
+    mx_tile<ROUND, RHTR, RHTC, DO_R, DO_C>(x, cols, ld, gr < rows ? gr : -1, gr, padded_rows(rows),
+                                           r0 < rows ? r0 / kMxBlock : -1, (int64_t)tc * 256, qr, qc, o,
+                                           reinterpret_cast<uint32_t*>(tile4));
+}
+
+// Grouped operands: workgroup (tr, y) takes tile row tr of the operand's grouped axis and column tiles
+// kMxColChunk y .. kMxColChunk (y + 1) - 1, so that reading the group offsets is shared by a few tiles. GROWS
+// (Q_r in grouped-rows form, for the ragged-M GEMMs): operand rows in panels, group g's rows X[off_g ..
+// off_{g+1}) from row P_g = sum_{h<g} pad128(m_h), the rest zero; a tile's 32 rows lie in one group's padded
+// range. Otherwise (Q_c with a grouped reduction, for bwd_dw): the reduction axis is each group's tokens padded
+// to 32, so the tile's 32 positions are rows src0 .. src0 + nvalid - 1 of X and zero padding.
+constexpr uint32_t kMxColChunk = 4;
+
+template <int ROUND, bool RHT, bool GROWS>
+__global__ __launch_bounds__(256) void mx_tile_grouped_kernel(const uint16_t* __restrict__ x, int64_t xrows,
+                                                              int64_t cols, int64_t ld, uint32_t n_ctiles,
+                                                              int64_t qr_prows, TGroups grp, QuantArgs qa,
+                                                              MxTileOut o) {
+    __shared__ int64_t s_off[kMaxGroupsLds + 1];
+    __shared__ int64_t s_poff[kMaxGroupsLds + 1];
+    __shared__ uint4 tile4[GROWS ? 1 : kMxTileWords / 4];
+    load_group_offsets<GROWS ? kPanelRows : kMxBlock>(grp, s_off, s_poff);
+    const int lr = threadIdx.x >> 3;
+    const int64_t r0 = (int64_t)blockIdx.x * 32;
+    const int g = find_group(s_poff, grp.G, r0);
+    const int64_t cnt = s_off[g + 1] - s_off[g];
+    int64_t src = -1;
+    if constexpr (GROWS) {
+        const int64_t local = r0 + lr - s_poff[g], sr = s_off[g] + local;
+        if (local < cnt && sr >= 0 && sr < xrows) src = sr;
+    } else {
+        const int64_t local0 = r0 - s_poff[g], src0 = s_off[g] + local0;
+        int64_t nvalid = cnt - local0;
+        if (src0 + nvalid > xrows) nvalid = xrows - src0;  // offsets beyond X are treated as padding
+        if (src0 < 0 || nvalid < 0) nvalid = 0;
+        if (lr < nvalid) src = src0 + lr;
+    }
+    const uint32_t tc_end = min(n_ctiles, (blockIdx.y + 1) * kMxColChunk);
+    for (uint32_t tc = blockIdx.y * kMxColChunk; tc < tc_end; ++tc) {
+        mx_tile<ROUND, RHT, RHT, GROWS, !GROWS>(x, cols, ld, src, r0 + lr, qr_prows, GROWS ? -1 : r0 / kMxBlock,
+                                                (int64_t)tc * 256, qa, qa, o, reinterpret_cast<uint32_t*>(tile4));
+        if constexpr (!GROWS) __syncthreads();  // the tile's column reads before the next tile's writes
     }
 }
 
@@ -1396,15 +1344,12 @@ __global__ __launch_bounds__(256) void mx_tile_kernel(const uint16_t* __restrict
 // columns; Q_c the row tiles of the rows and the column tiles of its padded rows.
 template <int ROUND, bool RHTR, bool RHTC, bool DO_R, bool DO_C>
 static hipError_t launch_mx_tiles(const void* x, int64_t rows, int64_t cols, int64_t ld, const QuantArgs& qr,
-                                  const QuantArgs& qc, void* codes_r, int64_t cpld_r, void* scales_r, int64_t spld_r,
-                                  void* codes_c, int64_t cpld_c, void* scales_c, int64_t spld_c, hipStream_t s) {
+                                  const QuantArgs& qc, const MxTileOut& o, hipStream_t s) {
     const int64_t n_rt = (DO_R ? padded_rows(rows) : rows) / 32;
     const int64_t n_ct = ((DO_C ? padded_rows(cols) : cols) + 255) / 256;
     if (n_rt == 0 || n_ct == 0) return hipSuccess;
     mx_tile_kernel<ROUND, RHTR, RHTC, DO_R, DO_C><<<dim3((unsigned)(n_rt * n_ct)), 256, 0, s>>>(
-        static_cast<const uint16_t*>(x), rows, cols, ld, (uint32_t)n_ct, qr, qc, static_cast<uint8_t*>(codes_r),
-        cpld_r, static_cast<uint8_t*>(scales_r), spld_r, static_cast<uint8_t*>(codes_c), cpld_c,
-        static_cast<uint8_t*>(scales_c), spld_c);
+        static_cast<const uint16_t*>(x), rows, cols, ld, (uint32_t)n_ct, qr, qc, o);
     return hipGetLastError();
 }
 
@@ -1414,9 +1359,10 @@ int64_t mx_tile_count(int64_t rows, int64_t cols, bool do_r, bool do_c) {
 
 template <int ROUND, bool RHTR, bool RHTC>
 static hipError_t launch_mx_dual_t(const MxDualJob& j, hipStream_t s) {
-    return launch_mx_tiles<ROUND, RHTR, RHTC, true, true>(j.x, j.rows, j.cols, j.ld, j.qr, j.qc, j.codes_r,
-                                                          j.code_pld_r, j.scales_r, j.scale_pld_r, j.codes_c,
-                                                          j.code_pld_c, j.scales_c, j.scale_pld_c, s);
+    const MxTileOut o{static_cast<uint8_t*>(j.codes_r), j.code_pld_r, static_cast<uint8_t*>(j.scales_r),
+                      j.scale_pld_r, static_cast<uint8_t*>(j.codes_c), j.code_pld_c,
+                      static_cast<uint8_t*>(j.scales_c), j.scale_pld_c};
+    return launch_mx_tiles<ROUND, RHTR, RHTC, true, true>(j.x, j.rows, j.cols, j.ld, j.qr, j.qc, o, s);
 }
 
 template <int ROUND>
@@ -1431,33 +1377,31 @@ hipError_t launch_quantize_mx_dual(const MxDualJob& j, hipStream_t s) {
 
 template <int ROUND, bool RHT, bool GR>
 static hipError_t launch_mx_t(const MxQuantJob& j, hipStream_t s) {
-    const int64_t prows = padded_rows(j.qrows);
-    const TGroups grp{j.group_off, j.num_groups};
-    if constexpr (!GR) {  // plain operands: the tile kernel with one output
+    uint8_t* const c = static_cast<uint8_t*>(j.codes);
+    uint8_t* const sc = static_cast<uint8_t*>(j.scales);
+    const MxTileOut o = j.transpose ? MxTileOut{nullptr, 0, nullptr, 0, c, j.code_pld, sc, j.scale_pld}
+                                    : MxTileOut{c, j.code_pld, sc, j.scale_pld, nullptr, 0, nullptr, 0};
+    if constexpr (!GR) {  // the tile kernel with one output
         if (!j.transpose)
-            return launch_mx_tiles<ROUND, RHT, false, true, false>(j.x, j.xrows, j.red, j.ld, j.qa, j.qa, j.codes,
-                                                                   j.code_pld, j.scales, j.scale_pld, nullptr, 0,
-                                                                   nullptr, 0, s);
-        return launch_mx_tiles<ROUND, false, RHT, false, true>(j.x, j.red, j.qrows, j.ld, j.qa, j.qa, nullptr, 0,
-                                                               nullptr, 0, j.codes, j.code_pld, j.scales, j.scale_pld,
-                                                               s);
-    }
-    if (!j.transpose) {
-        const int64_t nb32 = j.red / kMxBlock;
-        const dim3 grid((unsigned)((nb32 + 3) / 4), (unsigned)(prows / 64));
-        if (grid.x == 0 || grid.y == 0) return hipSuccess;
-        mx_rows_kernel<ROUND, RHT, GR><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.ld, j.qrows,
-                                                            nb32, grp, j.qa, static_cast<uint8_t*>(j.codes),
-                                                            j.code_pld, static_cast<uint8_t*>(j.scales), j.scale_pld);
+            return launch_mx_tiles<ROUND, RHT, false, true, false>(j.x, j.xrows, j.red, j.ld, j.qa, j.qa, o, s);
+        return launch_mx_tiles<ROUND, false, RHT, false, true>(j.x, j.red, j.qrows, j.ld, j.qa, j.qa, o, s);
     } else {
-        const int64_t gy = (j.red / kMxBlock + 15) / 16;
-        const dim3 grid((unsigned)(prows / 64), (unsigned)(gy < 65535 ? gy : 65535));
-        if (grid.x == 0 || grid.y == 0) return hipSuccess;
-        mx_cols_kernel<ROUND, RHT, GR><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(j.x), j.xrows, j.qrows, j.ld,
-                                                            j.red, grp, j.qa, static_cast<uint8_t*>(j.codes),
-                                                            j.code_pld, static_cast<uint8_t*>(j.scales), j.scale_pld);
+        // grouped rows: Q_r [qrows, cols] with qrows the padded total; grouped reduction: Q_c [cols, red] with
+        // red the padded token total; one workgroup per 32 positions of the grouped axis
+        const int64_t cols = j.transpose ? j.qrows : j.red;
+        const int64_t n_rt = (j.transpose ? j.red : j.qrows) / 32;
+        const int64_t n_ct = ((j.transpose ? padded_rows(cols) : cols) + 255) / 256;
+        if (n_rt == 0 || n_ct == 0) return hipSuccess;
+        const TGroups grp{j.group_off, j.num_groups};
+        const dim3 grid((unsigned)n_rt, (unsigned)((n_ct + kMxColChunk - 1) / kMxColChunk));
+        if (j.transpose)
+            mx_tile_grouped_kernel<ROUND, RHT, false><<<grid, 256, 0, s>>>(
+                static_cast<const uint16_t*>(j.x), j.xrows, cols, j.ld, (uint32_t)n_ct, 0, grp, j.qa, o);
+        else
+            mx_tile_grouped_kernel<ROUND, RHT, true><<<grid, 256, 0, s>>>(
+                static_cast<const uint16_t*>(j.x), j.xrows, cols, j.ld, (uint32_t)n_ct, j.qrows, grp, j.qa, o);
+        return hipGetLastError();
     }
-    return hipGetLastError();
 }
 
 template <int ROUND, bool RHT>
