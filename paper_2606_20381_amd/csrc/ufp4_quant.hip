@@ -57,6 +57,16 @@ __device__ __forceinline__ float uniform_sr_level(float v, uint32_t u16) {
     return lo + ((t < vc) ? 1.0f : 0.0f);  // a zero level comes out as +0
 }
 
+// The same decision with the offset nibble as the result: lo + kMagic8 holds nibble lo + 8 in bits 0-3 (bits
+// 4-21 clear), and the step up is added to that bit pattern as an integer (lo + 8 + 1 <= 15: no carry leaves
+// the nibble, since lo = 7 only when the clamped v is 7, which never rounds up).
+__device__ __forceinline__ uint32_t uniform_sr_offset(float v, uint32_t u16) {
+    const float vc = __builtin_fminf(__builtin_fmaxf(v, -7.0f), 7.0f);
+    const float lo = floorf(vc);
+    const float t = __builtin_fmaf((float)u16, 1.0f / 65536.0f, lo);
+    return __float_as_uint(lo + kMagic8) + ((t < vc) ? 1u : 0u);
+}
+
 // Eight words whose bits 0-3 hold a nibble and bits 4-21 are clear (higher bits arbitrary) -> one dword,
 // element i in bits 4i .. 4i+3. Shifts by 12 and more push the arbitrary bits out of the word.
 __device__ __forceinline__ uint32_t pack_nibbles(const uint32_t* t) {
@@ -270,7 +280,7 @@ __device__ __forceinline__ bool quant_core(float (&y)[16], TFn&& exact_t, const 
         for (int i = 0; i < 16; ++i) {
             if constexpr (ROUND == kRoundSR) {
                 const uint32_t u16 = (i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu);
-                tt[i] = __float_as_uint(uniform_sr_level(v[i], u16) + kMagic8);  // exact: an integer plus the constant
+                tt[i] = uniform_sr_offset(v[i], u16);
             } else {
                 tt[i] = __float_as_uint(v[i] + kMagic8);  // the rounding itself
             }
