@@ -439,7 +439,10 @@ int ufp4_gemm_bwd_dw(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, void *dw_d
  *           ufp4_quantize_grouped_t on the same offsets; the padded offsets pad_g are computed on the device.
  *
  * Offsets are read on the device: rows past M_total and reduction positions past R are ignored, groups with
- * no tokens give dW_g = 0. Operand checks as for the dense calls. num_groups up to 65535.
+ * no tokens give dW_g = 0. Operand checks as for the dense calls; besides, fwd_y takes plain operands, bwd_dx a
+ * plain Qdy and a plain or grouped-transposed Qwt (the same bytes: N is a multiple of 16), bwd_dw two
+ * grouped-transposed operands (UFP4_LAYOUT_GROUPED_RED); other forms return UFP4_ERR_MISMATCH. num_groups up to
+ * 65535.
  */
 int ufp4_gemm_fwd_y_grouped(const ufp4_qtensor *x, const ufp4_qtensor *w, const int64_t *group_offsets_dev,
                             int32_t num_groups, void *y_dev, int64_t ldc, int out_dtype, void *stream);

@@ -213,7 +213,7 @@ int mx_gemm_impl(const ufp4_qtensor* a, const ufp4_qtensor* b, void* c, int64_t 
     if (a->red != b->red) return UFP4_ERR_MISMATCH;
     st = check_output(c, ldc, b->rows, out_dtype);
     if (st != UFP4_OK) return st;
-    // one workgroup per 128 x 128 output tile on a one-dimensional grid
+    // one workgroup per 256 x 256 output tile on a one-dimensional grid (the count of 128 x 128 tiles bounds it)
     if (ceil_div(a->rows, 128) * ceil_div(b->rows, 128) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     if (a->rows == 0 || b->rows == 0) return UFP4_OK;
     MxGemmJob j{};
@@ -807,6 +807,7 @@ int ufp4_gemm_fwd_y_grouped(const ufp4_qtensor* x, const ufp4_qtensor* w, const 
     if (!group_offsets_dev || num_groups < 1) return UFP4_ERR_INVALID_ARG;
     int st = check_operands(x, w, false);
     if (st != UFP4_OK) return st;
+    if (x->layout != UFP4_LAYOUT_PLAIN || w->layout != UFP4_LAYOUT_PLAIN) return UFP4_ERR_MISMATCH;
     if (x->red != w->red) return UFP4_ERR_MISMATCH;
     if (w->rows % num_groups != 0) return UFP4_ERR_SHAPE;
     const int64_t N = w->rows / num_groups;
@@ -827,6 +828,9 @@ int ufp4_gemm_bwd_dx_grouped(const ufp4_qtensor* dy, const ufp4_qtensor* wt, con
     // A = dY [M_total, N]; B = W^T [K, G*N], group g uses reduction columns [g*N, (g+1)*N)
     int st = check_operands(dy, wt, false);
     if (st != UFP4_OK) return st;
+    // dY's reduction (N) is a multiple of 16, so W^T's equal groups need no padding: its grouped-transposed
+    // and plain transposed forms coincide and both are accepted
+    if (dy->layout != UFP4_LAYOUT_PLAIN || wt->layout == UFP4_LAYOUT_GROUPED_ROWS) return UFP4_ERR_MISMATCH;
     if (wt->red != dy->red * num_groups) return UFP4_ERR_MISMATCH;
     st = check_output(dx_dev, ldc, wt->rows, out_dtype);
     if (st != UFP4_OK) return st;
@@ -846,6 +850,8 @@ int ufp4_gemm_bwd_dw_grouped(const ufp4_qtensor* dyt, const ufp4_qtensor* xt, co
     // A = dY^T [N, R], B = X^T [K, R]; group g reduces over [pad_g, pad_{g+1}) of that axis
     int st = check_operands(dyt, xt, false);
     if (st != UFP4_OK) return st;
+    // the kernel reduces each group over its tokens padded to 16, the layout ufp4_quantize_grouped_t writes
+    if (dyt->layout != UFP4_LAYOUT_GROUPED_RED || xt->layout != UFP4_LAYOUT_GROUPED_RED) return UFP4_ERR_MISMATCH;
     if (dyt->red != xt->red) return UFP4_ERR_MISMATCH;
     st = check_output(dw_dev, ldc, xt->rows, out_dtype);
     if (st != UFP4_OK) return st;

@@ -397,8 +397,15 @@ def test_grouped_gemm_checks(lib):
     assert fy(R(_desc()), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH  # K differs
     # bwd_dx: W^T's reduction must be G times dY's
     assert fx(R(_desc(red=32)), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
-    assert fw(R(_desc()), R(_desc(red=48, cld=3072, sld=384)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    g = dict(layout=2)  # grouped-transposed operands, as bwd_dw takes them
+    assert fw(R(_desc(**g)), R(_desc(red=48, cld=3072, sld=384, **g)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
     assert fw(R(_desc()), R(_desc()), FAKE, 70000, FAKE, 16, 0, None) == UNSUPPORTED     # groups > 65535
+    # operand forms: bwd_dw pads each group's tokens to 16, so plain operands are refused; fwd_y and dY take plain
+    assert fw(R(_desc()), R(_desc()), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fw(R(_desc(**g)), R(_desc()), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fy(R(_desc(**g)), R(_desc()), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fy(R(_desc()), R(_desc(**g)), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
+    assert fx(R(_desc(red=16, **g)), R(_desc()), FAKE, 2, FAKE, 16, 0, None) == MISMATCH
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
