@@ -515,26 +515,6 @@ def gemm_nt(a_idx, a_scales, b_idx, b_scales, fmt: int) -> np.ndarray:
     return dequantize(a_idx, a_scales, fmt) @ dequantize(b_idx, b_scales, fmt).T
 
 
-def gemm_nt_grouped(a_idx, a_scales, b_idx, b_scales, fmt: int, a_rows=None, b_rows=None,
-                    red_cols=None) -> list[np.ndarray]:
-    """Per-group NT GEMMs. Each of `a_rows`, `b_rows`, `red_cols` is a list of (start, stop) pairs or
-    None (whole axis); group g multiplies A[a_rows[g], red_cols[g]] by B[b_rows[g], red_cols[g]]^T."""
-    da = dequantize(a_idx, a_scales, fmt)
-    db = dequantize(b_idx, b_scales, fmt)
-    n = max(len(x) for x in (a_rows, b_rows, red_cols) if x is not None)
-    out = []
-    for g in range(n):
-        ar = slice(*a_rows[g]) if a_rows is not None else slice(None)
-        br = slice(*b_rows[g]) if b_rows is not None else slice(None)
-        rc = slice(*red_cols[g]) if red_cols is not None else slice(None)
-        out.append(da[ar, rc] @ db[br, rc].T)
-    return out
-
-
-# ---------------------------------------------------------------------------------------------------
-# One linear layer's three quantized GEMMs under a recipe (Sec. 4, Table 1; Sec. 2.2 closing sentence)
-# ---------------------------------------------------------------------------------------------------
-
 # ---------------------------------------------------------------------------------------------------
 # The uniform grid with power-of-two block scales (Sec. 4: the scale hierarchy is orthogonal to the grid
 # and may follow the hardware). Quantization blocks of 32 along the reduction axis share one scale 2^E
@@ -649,6 +629,10 @@ def gemm_nt_mx(a_idx, a_e8m0, b_idx, b_e8m0) -> np.ndarray:
     """C = deq(A) @ deq(B)^T in fp64 for operands with power-of-two block scales."""
     return dequantize_mx(a_idx, a_e8m0) @ dequantize_mx(b_idx, b_e8m0).T
 
+
+# ---------------------------------------------------------------------------------------------------
+# One linear layer's three quantized GEMMs under a recipe (Sec. 4, Table 1; Sec. 2.2 closing sentence)
+# ---------------------------------------------------------------------------------------------------
 
 _T, _F = True, False
 RECIPES = {
