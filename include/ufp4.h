@@ -18,7 +18,8 @@
  *    every buffer; the library allocates, frees and synchronizes nothing, and keeps no state between calls.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls are asynchronous on it.
  *  - bf16 tensors are row-major with a leading dimension `ld` in elements (ld >= cols, ld % 8 == 0,
- *    base 16-byte aligned).
+ *    base 16-byte aligned). A tensor with no element (rows or cols 0), input or GEMM output, is never
+ *    accessed: its pointer may be NULL and its leading dimension is not checked.
  *  - A quantized operand Q is [rows, red] (red % 16 == 0, nkb = red/16 blocks of 16 along the reduction
  *    axis), described by a ufp4_qtensor (below) and stored in panels: rows 128p .. 128p+127 form panel p, and
  *    within a panel the data of block b of all 128 rows is contiguous -- the order in which the GEMMs stage

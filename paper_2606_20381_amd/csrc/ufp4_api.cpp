@@ -78,6 +78,17 @@ void record(ufp4_qtensor* q, int format, int64_t rows, int64_t red, int rht_bloc
     q->reserved = 0;
 }
 
+// An input tensor [rows, cols] with leading dimension ld (elements, a multiple of ld_mult) at x. An empty tensor
+// (rows or cols 0) is read by nobody: it may have no storage and any leading dimension.
+int check_input(const void* x, int64_t rows, int64_t cols, int64_t ld, int64_t ld_mult) {
+    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    if (rows == 0 || cols == 0) return UFP4_OK;
+    if (!x) return UFP4_ERR_INVALID_ARG;
+    if (ld < cols || ld % ld_mult != 0) return UFP4_ERR_SHAPE;
+    if (!aligned(x, 16)) return UFP4_ERR_ALIGN;
+    return UFP4_OK;
+}
+
 // Checks shared by the bf16-input quantizers: the input tensor and the operand's storage.
 int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, int64_t ld, int rht, uint32_t sign_mask,
                        int rounding, const ufp4_qtensor* out, int64_t qrows, int64_t red) {
@@ -86,9 +97,8 @@ int check_quant_common(int format, const void* x, int64_t rows, int64_t cols, in
     if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
     if (rows < 0 || cols < 0 || red < 0 || qrows < 0) return UFP4_ERR_INVALID_ARG;
-    if (!x) return UFP4_ERR_INVALID_ARG;
-    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x, 16)) return UFP4_ERR_ALIGN;
+    const int si = check_input(x, rows, cols, ld, 8);
+    if (si != UFP4_OK) return si;
     const int st = check_storage(out, format, qrows, red);
     if (st != UFP4_OK) return st;
     if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
@@ -163,8 +173,10 @@ int check_operands(const ufp4_qtensor* a, const ufp4_qtensor* b, bool mx) {
     return UFP4_OK;
 }
 
-int check_output(const void* c, int64_t ldc, int64_t c_cols, int out_dtype) {
+// The output (c_cols columns per row, leading dimension ldc); an empty output may have no storage.
+int check_output(const void* c, int64_t ldc, int64_t c_cols, int out_dtype, bool empty) {
     if (out_dtype != UFP4_OUT_F32 && out_dtype != UFP4_OUT_BF16) return UFP4_ERR_INVALID_ARG;
+    if (empty) return UFP4_OK;
     if (!c) return UFP4_ERR_INVALID_ARG;
     if (ldc < c_cols) return UFP4_ERR_SHAPE;
     if (!aligned(c, out_dtype == UFP4_OUT_F32 ? 4 : 2)) return UFP4_ERR_ALIGN;
@@ -200,7 +212,7 @@ int gemm_dense(const ufp4_qtensor* a, const ufp4_qtensor* b, void* c, int64_t ld
     int st = check_operands(a, b, false);
     if (st != UFP4_OK) return st;
     if (a->red != b->red) return UFP4_ERR_MISMATCH;
-    st = check_output(c, ldc, b->rows, out_dtype);
+    st = check_output(c, ldc, b->rows, out_dtype, a->rows == 0 || b->rows == 0);
     if (st != UFP4_OK) return st;
     if (a->rows == 0 || b->rows == 0) return UFP4_OK;
     const GemmJob j = make_job(kGemmDense, a, b, a->rows, b->rows, a->red / 16, c, ldc, out_dtype);
@@ -211,7 +223,7 @@ int mx_gemm_impl(const ufp4_qtensor* a, const ufp4_qtensor* b, void* c, int64_t 
     int st = check_operands(a, b, true);
     if (st != UFP4_OK) return st;
     if (a->red != b->red) return UFP4_ERR_MISMATCH;
-    st = check_output(c, ldc, b->rows, out_dtype);
+    st = check_output(c, ldc, b->rows, out_dtype, a->rows == 0 || b->rows == 0);
     if (st != UFP4_OK) return st;
     // one workgroup per 256 x 256 output tile on a one-dimensional grid (the count of 128 x 128 tiles bounds it)
     if (ceil_div(a->rows, 128) * ceil_div(b->rows, 128) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
@@ -362,14 +374,14 @@ int ufp4_quant_stats(int format, float max_fpx, const void* x_dev, int64_t rows,
     if (transpose != 0 && transpose != 1) return UFP4_ERR_INVALID_ARG;
     if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
-    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
+    if (!stats_dev) return UFP4_ERR_INVALID_ARG;
+    const int si = check_input(x_dev, rows, cols, ld, 8);
+    if (si != UFP4_OK) return si;
     const bool empty = rows == 0 || cols == 0;
-    if ((!x_dev && !empty) || !stats_dev) return UFP4_ERR_INVALID_ARG;  // an empty operand may have no storage
-    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
     const int64_t red = transpose ? rows : cols;
     const int64_t qrows = transpose ? cols : rows;
     if (red % 16 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16) || !aligned(stats_dev, 8)) return UFP4_ERR_ALIGN;
+    if (!aligned(stats_dev, 8)) return UFP4_ERR_ALIGN;
     if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     StatsJob j{};
     j.format = format;
@@ -425,9 +437,10 @@ int ufp4_rht(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, uint32_t
              void* stream) {
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
     if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
-    if (!x_dev || !y_dev) return UFP4_ERR_INVALID_ARG;
-    if (cols % 16 != 0 || ld < cols || ld % 8 != 0 || ldy < cols || ldy % 4 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16) || !aligned(y_dev, 16)) return UFP4_ERR_ALIGN;
+    if (cols % 16 != 0) return UFP4_ERR_SHAPE;
+    int si = check_input(x_dev, rows, cols, ld, 8);
+    if (si == UFP4_OK) si = check_input(y_dev, rows, cols, ldy, 4);  // the output, checked like an input
+    if (si != UFP4_OK) return si;
     if (cols / 16 / 256 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
     if (rows == 0 || cols == 0) return UFP4_OK;
     RhtJob j{};
@@ -450,9 +463,9 @@ int ufp4_quantize_f32(int format, const float* x_dev, int64_t rows, int64_t cols
     if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
     if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
-    if (!x_dev) return UFP4_ERR_INVALID_ARG;
-    if (cols % 16 != 0 || ld < cols || ld % 4 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    if (cols % 16 != 0) return UFP4_ERR_SHAPE;
+    const int si = check_input(x_dev, rows, cols, ld, 4);
+    if (si != UFP4_OK) return si;
     const int st = check_storage(out, format, rows, cols);
     if (st != UFP4_OK) return st;
     if (rows >= (int64_t(1) << 31) || padded_rows(rows) / 32 > 65535) return UFP4_ERR_UNSUPPORTED;
@@ -567,12 +580,10 @@ int ufp4_mx_quantize(const void* x_dev, int64_t rows, int64_t cols, int64_t ld, 
     if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
     if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
-    if (rows < 0 || cols < 0) return UFP4_ERR_INVALID_ARG;
-    if (!x_dev) return UFP4_ERR_INVALID_ARG;
+    const int si = check_input(x_dev, rows, cols, ld, 8);
+    if (si != UFP4_OK) return si;
     const int64_t red = transpose ? rows : cols;
     const int64_t qrows = transpose ? cols : rows;
-    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
     const int st = check_storage(out, UFP4_FMT_UNIFORM_MX32, qrows, red);
     if (st != UFP4_OK) return st;
     if (qrows >= (int64_t(1) << 31) || red / 16 >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
@@ -609,10 +620,9 @@ int ufp4_mx_quantize_dual(const void* x_dev, int64_t rows, int64_t cols, int64_t
     if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
     if ((rht_rows != 0 && rht_rows != 1) || (rht_cols != 0 && rht_cols != 1)) return UFP4_ERR_INVALID_ARG;
     if (sign_mask_rows > 0xFFFFu || sign_mask_cols > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
-    if (rows < 0 || cols < 0 || !x_dev) return UFP4_ERR_INVALID_ARG;
     if (out_rows == out_cols) return UFP4_ERR_INVALID_ARG;
-    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    const int si = check_input(x_dev, rows, cols, ld, 8);
+    if (si != UFP4_OK) return si;
     int st = check_storage(out_rows, UFP4_FMT_UNIFORM_MX32, rows, cols);
     if (st == UFP4_OK) st = check_storage(out_cols, UFP4_FMT_UNIFORM_MX32, cols, rows);
     if (st != UFP4_OK) return st;
@@ -655,12 +665,11 @@ int ufp4_mx_quantize_grouped(const void* x_dev, int64_t rows, int64_t cols, int6
     if (rounding != UFP4_ROUND_RTNE && rounding != UFP4_ROUND_SR) return UFP4_ERR_INVALID_ARG;
     if (rht != 0 && rht != 1) return UFP4_ERR_INVALID_ARG;
     if (sign_mask > 0xFFFFu) return UFP4_ERR_INVALID_ARG;
-    if (rows < 0 || cols < 0 || padded_total < 0) return UFP4_ERR_INVALID_ARG;
-    if (!x_dev || !group_offsets_dev) return UFP4_ERR_INVALID_ARG;
+    if (padded_total < 0 || !group_offsets_dev) return UFP4_ERR_INVALID_ARG;
     if (num_groups < 1) return UFP4_ERR_INVALID_ARG;
     if (num_groups > max_groups_quantize()) return UFP4_ERR_UNSUPPORTED;
-    if (ld < cols || ld % 8 != 0) return UFP4_ERR_SHAPE;
-    if (!aligned(x_dev, 16)) return UFP4_ERR_ALIGN;
+    const int si = check_input(x_dev, rows, cols, ld, 8);
+    if (si != UFP4_OK) return si;
     // transpose 0: [padded_total, cols], groups of rows on whole panels; transpose 1: [cols, padded_total]
     const int64_t qrows = transpose ? cols : padded_total;
     const int64_t red = transpose ? padded_total : cols;
@@ -708,7 +717,7 @@ int ufp4_mx_gemm_fwd_y_grouped(const ufp4_qtensor* x, const ufp4_qtensor* w, con
     if (w->rows % num_groups != 0) return UFP4_ERR_SHAPE;
     const int64_t N = w->rows / num_groups;
     if (N % kPanelRows != 0) return UFP4_ERR_UNSUPPORTED;  // each group's weight rows start on a panel
-    st = check_output(y_dev, ldc, N, out_dtype);
+    st = check_output(y_dev, ldc, N, out_dtype, m_total == 0 || N == 0);
     if (st != UFP4_OK) return st;
     if (m_total == 0 || N == 0 || x->rows == 0) return UFP4_OK;
     MxGemmJob j = mx_job(x, w, y_dev, ldc, out_dtype);
@@ -733,7 +742,7 @@ int ufp4_mx_gemm_bwd_dx_grouped(const ufp4_qtensor* dy, const ufp4_qtensor* wt, 
     if (st != UFP4_OK) return st;
     if (dy->layout != UFP4_LAYOUT_GROUPED_ROWS || wt->layout != UFP4_LAYOUT_PLAIN) return UFP4_ERR_MISMATCH;
     if (wt->red != dy->red * num_groups) return UFP4_ERR_MISMATCH;
-    st = check_output(dx_dev, ldc, wt->rows, out_dtype);
+    st = check_output(dx_dev, ldc, wt->rows, out_dtype, m_total == 0 || wt->rows == 0);
     if (st != UFP4_OK) return st;
     if (m_total == 0 || wt->rows == 0 || dy->rows == 0) return UFP4_OK;
     MxGemmJob j = mx_job(dy, wt, dx_dev, ldc, out_dtype);
@@ -758,7 +767,7 @@ int ufp4_mx_gemm_bwd_dw_grouped(const ufp4_qtensor* dyt, const ufp4_qtensor* xt,
     if (st != UFP4_OK) return st;
     if (dyt->layout != UFP4_LAYOUT_GROUPED_RED || xt->layout != UFP4_LAYOUT_GROUPED_RED) return UFP4_ERR_MISMATCH;
     if (dyt->red != xt->red) return UFP4_ERR_MISMATCH;
-    st = check_output(dw_dev, ldc, xt->rows, out_dtype);
+    st = check_output(dw_dev, ldc, xt->rows, out_dtype, dyt->rows == 0 || xt->rows == 0);
     if (st != UFP4_OK) return st;
     if (dyt->rows == 0 || xt->rows == 0) return UFP4_OK;
     if (ceil_div(dyt->rows, 256) * ceil_div(xt->rows, 256) >= (int64_t(1) << 31)) return UFP4_ERR_UNSUPPORTED;
@@ -811,7 +820,7 @@ int ufp4_gemm_fwd_y_grouped(const ufp4_qtensor* x, const ufp4_qtensor* w, const 
     if (x->red != w->red) return UFP4_ERR_MISMATCH;
     if (w->rows % num_groups != 0) return UFP4_ERR_SHAPE;
     const int64_t N = w->rows / num_groups;
-    st = check_output(y_dev, ldc, N, out_dtype);
+    st = check_output(y_dev, ldc, N, out_dtype, x->rows == 0 || N == 0);
     if (st != UFP4_OK) return st;
     if (x->rows == 0 || N == 0) return UFP4_OK;
     GemmJob j = make_job(kGemmRaggedM, x, w, x->rows, N, x->red / 16, y_dev, ldc, out_dtype);
@@ -832,7 +841,7 @@ int ufp4_gemm_bwd_dx_grouped(const ufp4_qtensor* dy, const ufp4_qtensor* wt, con
     // and plain transposed forms coincide and both are accepted
     if (dy->layout != UFP4_LAYOUT_PLAIN || wt->layout == UFP4_LAYOUT_GROUPED_ROWS) return UFP4_ERR_MISMATCH;
     if (wt->red != dy->red * num_groups) return UFP4_ERR_MISMATCH;
-    st = check_output(dx_dev, ldc, wt->rows, out_dtype);
+    st = check_output(dx_dev, ldc, wt->rows, out_dtype, dy->rows == 0 || wt->rows == 0);
     if (st != UFP4_OK) return st;
     if (dy->rows == 0 || wt->rows == 0) return UFP4_OK;
     GemmJob j = make_job(kGemmRaggedM, dy, wt, dy->rows, wt->rows, dy->red / 16, dx_dev, ldc, out_dtype);
@@ -853,7 +862,7 @@ int ufp4_gemm_bwd_dw_grouped(const ufp4_qtensor* dyt, const ufp4_qtensor* xt, co
     // the kernel reduces each group over its tokens padded to 16, the layout ufp4_quantize_grouped_t writes
     if (dyt->layout != UFP4_LAYOUT_GROUPED_RED || xt->layout != UFP4_LAYOUT_GROUPED_RED) return UFP4_ERR_MISMATCH;
     if (dyt->red != xt->red) return UFP4_ERR_MISMATCH;
-    st = check_output(dw_dev, ldc, xt->rows, out_dtype);
+    st = check_output(dw_dev, ldc, xt->rows, out_dtype, dyt->rows == 0 || xt->rows == 0);
     if (st != UFP4_OK) return st;
     if (dyt->rows == 0 || xt->rows == 0) return UFP4_OK;
     GemmJob j = make_job(kGemmRaggedK, dyt, xt, dyt->rows, xt->rows, 0, dw_dev, ldc, out_dtype);

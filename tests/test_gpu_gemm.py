@@ -103,6 +103,34 @@ def test_zero_operand_and_output_stride():
     assert torch.all(o[:, :40] == 0) and torch.all(o[:, 40:] == 7.0)
 
 
+@pytest.mark.parametrize("kind", ["uniform", "e2m1", "mx"])
+def test_empty_gemm_shapes(kind):
+    """M = 0 and N = 0 give empty outputs; a zero-length reduction gives C = 0 (the kernels run no K-stage and
+    still store every output, over a prefilled buffer)."""
+    quant = {"uniform": U.rht_quantize, "e2m1": U.e2m1_quantize, "mx": U.mx_quantize}[kind]
+    gemm = U.mx_gemm_fwd_y if kind == "mx" else U.gemm_fwd_y
+    bf = dict(dtype=torch.bfloat16, device="cuda")
+    for m, n, k in [(0, 40, 64), (70, 0, 64), (0, 0, 0), (300, 130, 0)]:
+        print(f"empty gemm {kind} {m}x{n}x{k}", flush=True)
+        xq, wq = quant(torch.randn(m, k, **bf)), quant(torch.randn(n, k, **bf))
+        for odt in (torch.float32, torch.bfloat16):
+            out = torch.full((m, n), 7.0, dtype=odt, device="cuda")
+            y = gemm(xq, wq, out=out)
+            torch.cuda.synchronize()
+            assert y.shape == (m, n) and torch.all(y == 0)
+
+
+def test_empty_reduction_grouped():
+    """Grouped fwd_y over a zero-length reduction: every token row of every group is 0."""
+    bf = dict(dtype=torch.bfloat16, device="cuda")
+    off, _ = U.group_offsets([5, 0, 130])
+    xq, wq = U.rht_quantize(torch.randn(135, 0, **bf)), U.rht_quantize(torch.randn(3 * 32, 0, **bf))
+    out = torch.full((135, 32), 7.0, device="cuda")
+    U.gemm_fwd_y_grouped(xq, wq, off, out=out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0)
+
+
 def test_gemm_deterministic():
     wl = WL.tiny()
     xq = U.rht_quantize(wl.x.cuda(), sign_mask=wl.sign_mask)

@@ -183,6 +183,29 @@ def test_quantize_validation(lib, args, dkw, status):
     assert lib.ufp4_rht_quantize(FAKE, 16, 32, 32, 0, 1, 0, 0, 0, 0, None, None) == INVALID  # no descriptor
 
 
+def test_empty_tensors_need_no_storage(lib):
+    """A tensor with no element is never accessed: a NULL pointer and any leading dimension are accepted (as
+    torch hands them over for empty tensors), the call returns OK without launching, and the descriptor
+    records the empty operand. Non-empty tensors still need both."""
+    for fn in (lib.ufp4_rht_quantize, lib.ufp4_e2m1_quantize, lib.ufp4_mx_quantize):
+        mx = dict(fmt=U.UNIFORM_MX32) if fn is lib.ufp4_mx_quantize else {}
+        for rows, cols, ld, transpose in [(0, 64, 64, 0), (70, 0, 1, 0), (0, 0, 1, 1), (0, 64, 64, 1)]:
+            d = _desc(rows=7, red=128, **mx)  # storage for any of the shapes
+            assert fn(None, rows, cols, ld, transpose, 1, 0, 0, 0, 0, R(d), None) == OK
+            assert (d.rows, d.red) == ((cols, rows) if transpose else (rows, cols))
+        assert fn(None, 16, 32 if mx else 16, 32, 0, 1, 0, 0, 0, 0, R(_desc(**mx)), None) == INVALID
+        assert fn(FAKE, 16, 32, 36, 0, 1, 0, 0, 0, 0, R(_desc(**mx)), None) == SHAPE  # ld % 8 still checked
+    assert _dual(lib, rows=0, x=None, ld=1) == OK
+    assert lib.ufp4_rht(None, 0, 32, 32, 0, None, 1, None) == OK
+    assert lib.ufp4_quantize_f32(0, None, 0, 32, 1, 1, 0, 0, 0, 0, R(_desc()), None) == OK
+    # a GEMM whose output has no element: NULL output, OK, no launch
+    assert lib.ufp4_gemm_fwd_y(R(_desc(rows=0)), R(_desc(rows=40)), None, 40, 0, None) == OK
+    assert lib.ufp4_gemm_fwd_y(R(_desc(rows=16)), R(_desc(rows=0)), None, 0, 1, None) == OK
+    mx = dict(fmt=U.UNIFORM_MX32)
+    assert lib.ufp4_mx_gemm_fwd_y(R(_desc(rows=0, **mx)), R(_desc(rows=40, **mx)), None, 40, 0, None) == OK
+    assert lib.ufp4_gemm_fwd_y(R(_desc(rows=16)), R(_desc(rows=40)), None, 40, 0, None) == INVALID  # not empty
+
+
 def _dual(lib, rows=32, cols=48, ld=48, fmt=0, rht_r=1, mask_r=0, rht_c=1, mask_c=0, rnd=0, x=FAKE, dr=None, dc=None):
     dr = dr or _desc(cld=3 * 1024, sld=3 * 128)
     dc = dc or _desc(cld=2 * 1024, sld=2 * 128)
