@@ -18,9 +18,9 @@ the product package. Inputs are numpy arrays; bf16 tensors arrive as their raw u
 Readings of the paper that this oracle fixes (the paper states exact mathematics only):
   * RHT arithmetic: y = RN_fp32( (1/4) * sum_j H16[i,j] * eps_j * x_j ), the exact 16-term sum rounded
     once to fp32 precision ("correctly rounded"; gradual underflow below 2^-126, and no overflow: a rotated
-    value past FLT_MAX keeps 24 significant bits). The sum is evaluated in fp64 through an explicit 16x16
-    matrix product; this is exact when the nonzero magnitudes of a block span at most 2^41 (checked, see
-    `_check_rht_domain`).
+    value past FLT_MAX keeps 24 significant bits), for every finite bf16 block. The sum is evaluated in fp64
+    through an explicit 16x16 matrix product, which is exact when the nonzero magnitudes of a block span at
+    most 2^41 (`_fp64_sums_exact`); the other blocks are summed with Python integers and rounded once.
   * Scale and reciprocal: s = RN32(amax / g), r = RN24(g / amax), v = RN32(y * r); g = 7 (uniform) or
     6 (E2M1). RN32 is IEEE binary32 rounding with gradual underflow (a tiny block gets a subnormal scale);
     RN24 rounds to 24 significant bits without an exponent limit, which is RN32 whenever g / amax is below
@@ -44,6 +44,9 @@ Readings of the paper that this oracle fixes (the paper states exact mathematics
 """
 
 from __future__ import annotations
+
+from fractions import Fraction
+import math
 
 import numpy as np
 
@@ -136,8 +139,8 @@ def sign_vector(sign_mask: int, n: int = BLOCK) -> np.ndarray:
     return np.array([-1.0 if (int(sign_mask) >> j) & 1 else 1.0 for j in range(n)])
 
 
-def _check_rht_domain(blocks: np.ndarray) -> None:
-    """Check that the fp64 evaluation of every n-term sum (n = the last axis, 16 by default) is exact.
+def _fp64_sums_exact(blocks: np.ndarray) -> np.ndarray:
+    """Per block (last axis, n entries): whether the fp64 evaluation of every n-term signed sum is exact.
 
     Each term is a bf16 value (8 significant bits). With frexp exponents e_max and e_min over the nonzero
     entries of a block, the exact sum is a multiple of 2^(e_min - 8) below 2^(e_max + log2 n) in magnitude,
@@ -149,16 +152,46 @@ def _check_rht_domain(blocks: np.ndarray) -> None:
     e_max = np.where(nz, e, np.iinfo(np.int32).min).max(axis=-1)
     e_min = np.where(nz, e, np.iinfo(np.int32).max).min(axis=-1)
     spread = np.where(nz.any(axis=-1), e_max - e_min, 0)
-    limit = 45 - int(np.log2(blocks.shape[-1]))
-    if np.any(spread > limit):
-        raise ValueError(f"a block spans more than 2^{limit} in magnitude: the RHT sum is not exact in fp64")
+    return spread <= 45 - int(np.log2(blocks.shape[-1]))
+
+
+def _exact_signed_sums(block: np.ndarray, eps: np.ndarray) -> tuple[list[int], int]:
+    """The n sums sum_j H_n^pm1[i,j] eps_j x_j of one n-block exactly: integers m_i with sum_i = m_i * 2^e.
+
+    Every x_j is a binary fraction p_j / 2^k_j (float.as_integer_ratio); over the common denominator 2^k the
+    terms are integers and the sums are plain integer sums.
+    """
+    n = block.shape[-1]
+    h = hadamard_pm1(n)
+    ratios = [float(v).as_integer_ratio() for v in block]
+    den = max(q for _, q in ratios)
+    ints = [p * (den // q) for p, q in ratios]
+    sums = [sum(int(h[i, j]) * int(eps[j]) * ints[j] for j in range(n)) for i in range(n)]
+    return sums, -(den.bit_length() - 1)
+
+
+def _round_int_to_fp32(m: int, e: int) -> float:
+    """m * 2^e rounded onto the fp32 grid as `round_to_fp32` rounds: to nearest even, gradual underflow (the
+    quantum never below 2^-149), and 24 significant bits with no exponent limit at the top. Returned as fp64."""
+    if m == 0:
+        return 0.0
+    sign = -1.0 if m < 0 else 1.0
+    m = abs(m)
+    q = max(e + m.bit_length() - 24, -149)  # weight of the last kept bit
+    if q > e:
+        sh = q - e
+        keep, rest, half = m >> sh, m & ((1 << sh) - 1), 1 << (sh - 1)
+        if rest > half or (rest == half and keep & 1):
+            keep += 1
+        m, e = keep, q
+    return sign * math.ldexp(m, e)
 
 
 def rht_exact_f64(blocks: np.ndarray, sign_mask: int) -> np.ndarray:
     """Unrounded RHT of 16-element row blocks: each row vector x becomes x S_16 H_16 (Sec. 2.2).
 
     `blocks` has shape [..., 16]. H_16 is symmetric, so (x S H)_i = (1/4) sum_j H16pm1[i,j] eps_j x_j.
-    Evaluated as an explicit matrix product in fp64; exact under `_check_rht_domain`.
+    Evaluated as an explicit matrix product in fp64; exact where `_fp64_sums_exact` holds.
     """
     blocks = np.asarray(blocks, dtype=np.float64)
     eps = sign_vector(sign_mask)
@@ -178,10 +211,17 @@ def round_to_fp32(t: np.ndarray) -> np.ndarray:
 
 def rht_blocks(blocks_f32: np.ndarray, sign_mask: int) -> np.ndarray:
     """RHT of bf16-valued 16-blocks, correctly rounded to fp32 precision (one rounding of the exact result,
-    `round_to_fp32`: gradual underflow, no overflow). Returned as fp64 holding those values."""
+    `round_to_fp32`: gradual underflow, no overflow). Returned as fp64 holding those values. Blocks whose fp64
+    sums could round (nonzero magnitudes spanning more than 2^41) are summed exactly with integers."""
     b64 = np.asarray(blocks_f32, dtype=np.float64)
-    _check_rht_domain(b64)
-    return round_to_fp32(rht_exact_f64(b64, sign_mask))
+    y = round_to_fp32(rht_exact_f64(b64, sign_mask))
+    wide = ~_fp64_sums_exact(b64)
+    if wide.any():
+        eps = sign_vector(sign_mask)
+        for idx in zip(*np.nonzero(wide)):
+            sums, e = _exact_signed_sums(b64[idx], eps)
+            y[idx] = [_round_int_to_fp32(m, e - 2) for m in sums]  # the factor 1/4 of the 16-point RHT
+    return y
 
 
 # RHT blocks larger than the quantization block (the RHT block-size dimension of the E2M1 reference search,
@@ -198,10 +238,11 @@ def rht_norm(n: int) -> float:
 def rht_rows_n(a_f32: np.ndarray, sign_mask: int, n: int) -> np.ndarray:
     """RHT of the n-blocks of every row of A [rows, red] (red % n == 0), as fp32.
 
-    y = RN32( RN64( S * RN64(1/sqrt(n)) ) ) with S = sum_j H_n^pm1[i,j] eps_j x_j exact in fp64 (explicit matrix
-    product, `_check_rht_domain`). For n = 16 and 64 the normalisation is a power of two and y is the correctly
-    rounded transform; for n = 32 and 128 it is the fp64-rounded product, then rounded to fp32 precision
-    (`round_to_fp32`; fp64 result). eps_j = -1 iff bit j of the n-bit `sign_mask` is set.
+    y = RN32( RN64( S * RN64(1/sqrt(n)) ) ) with S = sum_j H_n^pm1[i,j] eps_j x_j the exact sum (an explicit fp64
+    matrix product where `_fp64_sums_exact` holds, integers elsewhere). For n = 16 and 64 the normalisation is a
+    power of two and y is the correctly rounded transform; for n = 32 and 128 it is the correctly rounded fp64
+    product, then rounded to fp32 precision (`round_to_fp32`; fp64 result). eps_j = -1 iff bit j of the n-bit
+    `sign_mask` is set.
     """
     if n not in RHT_BLOCKS:
         raise ValueError("RHT block must be 16, 32, 64 or 128")
@@ -210,9 +251,17 @@ def rht_rows_n(a_f32: np.ndarray, sign_mask: int, n: int) -> np.ndarray:
     if red % n:
         raise ValueError("the reduction length must be a multiple of the RHT block")
     blocks = a.reshape(rows, red // n, n)
-    _check_rht_domain(blocks)
-    s = (blocks * sign_vector(sign_mask, n)) @ hadamard_pm1(n)
-    return round_to_fp32(s * rht_norm(n)).reshape(rows, red)
+    eps = sign_vector(sign_mask, n)
+    c = rht_norm(n)
+    y = round_to_fp32(((blocks * eps) @ hadamard_pm1(n)) * c)
+    wide = ~_fp64_sums_exact(blocks)
+    for idx in zip(*np.nonzero(wide)):
+        sums, e = _exact_signed_sums(blocks[idx], eps)
+        if n in (16, 64):  # c = 2^-2 or 2^-3: one rounding of the exact transform
+            y[idx] = [_round_int_to_fp32(m, e + int(math.log2(c))) for m in sums]
+        else:  # the exact product S * c rounded to fp64 (Fraction -> float rounds correctly), then to fp32
+            y[idx] = round_to_fp32(np.array([float(Fraction(m) * Fraction(2) ** e * Fraction(c)) for m in sums]))
+    return y.reshape(rows, red)
 
 
 # ---------------------------------------------------------------------------------------------------
