@@ -40,7 +40,9 @@
  *      y_i  = the exact 1/4 * sum_j H16[i,j] * eps_j * x_j  rounded once to fp32 precision (rht != 0), else
  *             y = x; H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
  *             Rounding: to nearest even, with gradual underflow below 2^-126 and no overflow (an output past
- *             FLT_MAX keeps 24 significant bits). Exact when the nonzero |x_j| of a block span at most 2^41.
+ *             FLT_MAX keeps 24 significant bits). The kernels sum in fp64: exact when the nonzero |x_j| of a
+ *             block span at most 2^41; a block spanning more may lose its smallest terms (y then need not be
+ *             the correctly rounded value).
  *      amax = max |y_i|;  s = RN32(amax/g) (IEEE: subnormal for a tiny block, +inf past the fp32 range);
  *      r = g/amax rounded to 24 significant bits without an exponent limit (= RN32(g/amax) whenever that is
  *      finite);  v_i = RN32(y_i * r);  amax == 0 -> s = 0, codes 0.  Uniform grid g = 7, E2M1 g = 6.
