@@ -52,7 +52,7 @@ from paper_2606_20381_amd import workloads as WL  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
 INT8_PEAK_TOPS = 5000.0  # dense int8 / fp8 MFMA, MI355X
-FP4_PEAK_TFLOPS = 10100.0  # dense fp4 MFMA (the E2M1 baseline's block products)
+FP4_PEAK_TFLOPS = 10100.0  # dense fp4 / fp6 MFMA (the power-of-two-scale GEMM's FP6 operands)
 # Bound of the per-16-block fp32-scale GEMM kernel: per 32x32 output tile and 16-block two MFMAs of 32 cycles each
 # (block product, scale outer product) keep the matrix core busy 64 cycles (the counter SQ_VALU_MFMA_BUSY_CYCLES
 # reads exactly that) for 32*32*16*2 ops, i.e. 512 ops per cycle per SIMD, at 256 CUs x 4 SIMDs x 2.4 GHz. The 16
@@ -61,7 +61,8 @@ ATTAINABLE_TOPS = 32 * 32 * 16 * 2 / 64 * 256 * 4 * 2.4e9 / 1e12
 GEMM_KERNEL = {
     "mxufp4": "gemm_mx_kernel (scaled f8f6f4 MFMA 32x32x64, FP6 E2M3 operands, E8M0 scales applied in the matrix core)",
     "ufp4": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
-    "e2m1": "gemm_f32_kernel (FP4 f8f6f4 MFMA per K-block + bf16 MFMA 32x32x8 scale outer product + fp32 FMA)",
+    "e2m1": "gemm_f32_kernel (fp8 MFMA 32x32x16 per K-block on the E2M1 levels as e4m3 + bf16 MFMA 32x32x8 scale "
+            "outer product + fp32 FMA)",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 WARMUP_SECONDS = 0.5
@@ -74,7 +75,7 @@ METRIC = "RHT+quantize GB/s and 4-bit fwd_y/bwd_dx/bwd_dw TFLOP/s (% of roofline
 
 
 def gemm_family(recipe: str) -> str:
-    """Which GEMM kernel a recipe runs: mxufp4 (FP6 scaled MFMA), ufp4 (fp8 MFMA per block) or e2m1 (FP4)."""
+    """Which GEMM kernel a recipe runs: mxufp4 (FP6 scaled MFMA), ufp4 or e2m1 (fp8 MFMA per block)."""
     if recipe == "mxufp4":
         return "mxufp4"
     return "ufp4" if R.RECIPES[recipe].fmt == U.UNIFORM else "e2m1"
@@ -83,14 +84,15 @@ def gemm_family(recipe: str) -> str:
 # The arithmetic each GEMM family computes in: 4-bit codes times per-block scales, fp32 accumulation.
 ARITH = {
     "ufp4": "int4xf32",   # integer codes -7..7 (as exact fp8 e4m3 values on the fp8 MFMA), fp32 1x16 scales
-    "e2m1": "fp4xf32",    # E2M1 codes on the FP4 MFMA, fp32 1x16 scales
+    "e2m1": "fp4xf32",    # E2M1 codes (as exact fp8 e4m3 values on the fp8 MFMA), fp32 1x16 scales
     "mxufp4": "int4xe8m0",  # integer codes -7..7 (as FP6 E2M3 values), power-of-two 1x32 scales in the MFMA
 }
 
 
 def gemm_peak(recipe: str) -> float:
-    """Dense MFMA peak of the GEMM's operand type: fp8 (= int8) for uniform codes, fp4/fp6 otherwise."""
-    return INT8_PEAK_TOPS if gemm_family(recipe) == "ufp4" else FP4_PEAK_TFLOPS
+    """Dense MFMA peak of the GEMM's operand type: fp8 (= int8) for both per-16 grids, fp6 (the fp4 rate) for the
+    power-of-two-scale GEMM."""
+    return FP4_PEAK_TFLOPS if gemm_family(recipe) == "mxufp4" else INT8_PEAK_TOPS
 
 
 class Timeline:
@@ -405,7 +407,7 @@ def e2m1_comparison(wl, steps: int, warmup: int, dual: bool) -> dict:
         us = tl.mean_us(label)
         if kind == "gemm":
             tf = work / (us * 1e-6) / 1e12
-            gemms[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
+            gemms[label] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac_peak": round(tf / gemm_peak("e2m1"), 4)}
             flops += work
         else:
             qus += us

@@ -4,8 +4,8 @@
 //   C[i, j] = sum_b  sA[i,b] * sB[j,b] * D_b[i, j],   D_b[i, j] = sum_{k in block b} A[i,k] * B[j,k]
 //
 // Every 16-element K-block has its own fp32 scale on both sides, so D_b is formed per block by one MFMA with
-// K = 16 (the integer codes made exact fp8 numbers; E2M1 codes as FP4) and folded into an fp32 accumulator
-// with the scale product of the block: acc += D_b * (sA * sB). The design is described at gemm_f32_kernel.
+// K = 16 (the codes of either grid made exact fp8 numbers) and folded into an fp32 accumulator with the scale
+// product of the block: acc += D_b * (sA * sB). The design is described at gemm_f32_kernel.
 //
 // Grouped (MoE) problems: ragged M (fwd_y, bwd_dx: token rows split into groups) resolves its group
 // from the tile index with a wave-wide prefix sum over the group sizes; ragged K (bwd_dw: the reduction
@@ -186,9 +186,9 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, int64_t* pad, const
 // product sA[:, b] x sB[:, b] in the same register layout, so the VALU does one FMA per output and block:
 // acc += D_b * (sA sB)_b.
 //
-//  * D_b: uniform codes become fp8 e4m3 subnormals (code k -> k * 2^-9, exact) while a stage is copied into
-//    LDS and go through v_mfma_f32_32x32x16_fp8_fp8; E2M1 codes go straight into the scaled f8f6f4 MFMA as
-//    FP4 operands (neutral E8M0 scales), the 16 codes of a block occupying 16 of its 64 K slots.
+//  * D_b: the codes become fp8 e4m3 numbers while a stage is copied into LDS and go through
+//    v_mfma_f32_32x32x16_fp8_fp8 (K = 16, one block): uniform code k -> the subnormal k * 2^-9, E2M1 level
+//    -> the same value as an e4m3 normal (every level 0, 0.5, ..., 6 is one); both exact, so D_b is exact.
 //  * (sA sB)_b: every fp32 scale is split exactly into three bf16 pieces s = s0 + s1 + s2 (top, middle and
 //    low 8 significand bits) when staged, and stored directly as the operand of a v_mfma_f32_32x32x8_bf16
 //    whose 8 K slots hold eight of the nine piece products (all but s2 * s2', below 2^-30 sA sB). Products
@@ -199,7 +199,6 @@ __device__ bool resolve_tile(const GemmJob& j, int32_t* grp, int64_t* pad, const
 // ================================================================================================
 
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef int v8i __attribute__((ext_vector_type(8)));
 typedef short v4s __attribute__((ext_vector_type(4)));
 
 constexpr int SKB2 = 4;       // K-blocks per LDS stage
@@ -212,6 +211,16 @@ constexpr int PL2 = BM + 1;   // 8-byte entries per LDS plane (one plane per blo
 __device__ __forceinline__ uint2 uniform_to_e4m3(uint32_t d) {
     const uint32_t lo = (d & 0x07070707u) | ((d << 4) & 0x80808080u);
     const uint32_t hi = ((d >> 4) & 0x07070707u) | (d & 0x80808080u);
+    return make_uint2(lo, hi);
+}
+
+// 8 E2M1 codes (sign-magnitude nibbles, magnitude = index of 0, 0.5, 1, 1.5, 2, 3, 4, 6) -> 8 fp8 e4m3 bytes of
+// the same values: a byte-select table (v_perm_b32 picks byte m of {0x4C484440, 0x3C383000} for magnitude m:
+// 0x00 0x30 0x38 0x3C 0x40 0x44 0x48 0x4C = 0, 0.5, 1, 1.5, 2, 3, 4, 6 in e4m3) and the sign in bit 7; even and
+// odd codes split as for the uniform grid.
+__device__ __forceinline__ uint2 e2m1_to_e4m3(uint32_t d) {
+    const uint32_t lo = __builtin_amdgcn_perm(0x4C484440u, 0x3C383000u, d & 0x07070707u) | ((d << 4) & 0x80808080u);
+    const uint32_t hi = __builtin_amdgcn_perm(0x4C484440u, 0x3C383000u, (d >> 4) & 0x07070707u) | (d & 0x80808080u);
     return make_uint2(lo, hi);
 }
 
@@ -246,8 +255,8 @@ __device__ __forceinline__ ScaleOp scale_op_b(float s) {
 }
 
 struct alignas(16) GemmSmem2 {
-    // plane (block * 2 + half) holds one 8-byte entry per row: codes (fp8 bytes for uniform, 8 FP4 codes in
-    // .x for E2M1) and outer-product scale operands
+    // plane (block * 2 + half) holds one 8-byte entry per row: codes (8 e4m3 bytes) and outer-product scale
+    // operands
     uint2 a[2][SKB2 * 2 * PL2];
     uint2 b[2][SKB2 * 2 * PL2];
     uint2 as[2][SKB2 * 2 * PL2];
@@ -256,19 +265,12 @@ struct alignas(16) GemmSmem2 {
     int64_t pad;
 };
 
-template <int FMT>
+// D_b of one 32 x 32 tile from the e4m3 bytes of a block (8 per lane: its K-half of the 16 codes).
 __device__ __forceinline__ v16f block_dot(uint2 a, uint2 b) {
     const v16f z = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-    if constexpr (FMT == kFmtUniform) {
-        const long av = (long)(((uint64_t)a.y << 32) | a.x);
-        const long bv = (long)(((uint64_t)b.y << 32) | b.x);
-        return __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(av, bv, z, 0, 0, 0);
-    } else {
-        const v8i av = {(int)a.x, 0, 0, 0, 0, 0, 0, 0};
-        const v8i bv = {(int)b.x, 0, 0, 0, 0, 0, 0, 0};
-        // A and B as FP4 E2M1 (format 4), E8M0 scales 127 = 2^0
-        return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, z, 4, 4, 0, 127, 0, 127);
-    }
+    const long av = (long)(((uint64_t)a.y << 32) | a.x);
+    const long bv = (long)(((uint64_t)b.y << 32) | b.x);
+    return __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(av, bv, z, 0, 0, 0);
 }
 
 __device__ __forceinline__ v16f scale_outer(uint2 a, uint2 b) {
@@ -366,7 +368,7 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
     };
     auto conv = [](uint32_t d) -> uint2 {
         if constexpr (FMT == kFmtUniform) return uniform_to_e4m3(d);
-        else return make_uint2(d, 0u);
+        else return e2m1_to_e4m3(d);
     };
     auto put = [&](int buf, const StageRegs& r) {
         uint2* cp = st_a ? sm.a[buf] : sm.b[buf];
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(512, 2) void gemm_f32_kernel(GemmArgs args) {
 #pragma unroll
                 for (int a = 0; a < 2; ++a) {
                     const int ra = pl + wm * 64 + a * 32 + l32;
-                    const v16f d = block_dot<FMT>(sm.a[buf][ra], bc);
+                    const v16f d = block_dot(sm.a[buf][ra], bc);
                     const v16f w = scale_outer(sm.as[buf][ra], bw);
 #pragma unroll
                     for (int i = 0; i < 16; ++i) acc[a][i] = __builtin_fmaf(d[i], w[i], acc[a][i]);
