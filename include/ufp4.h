@@ -41,8 +41,9 @@
  *             y = x; H16[i,j] = (-1)^popcount(i & j) (Sylvester, Sec. 2.2); eps_j = -1 iff bit j of sign_mask.
  *             Rounding: to nearest even, with gradual underflow below 2^-126 and no overflow (an output past
  *             FLT_MAX keeps 24 significant bits). The kernels sum in fp64: exact when the nonzero |x_j| of a
- *             block span at most 2^41; a block spanning more may lose its smallest terms (y then need not be
- *             the correctly rounded value).
+ *             block span at most 2^41; a block spanning more may lose its smallest terms, an error below
+ *             2^-46 max|x_j| before the rounding to fp32 (y then need not be the correctly rounded value; a
+ *             code may move to an adjacent level and a scale by an ulp where such a y decides them).
  *      amax = max |y_i|;  s = RN32(amax/g) (IEEE: subnormal for a tiny block, +inf past the fp32 range);
  *      r = g/amax rounded to 24 significant bits without an exponent limit (= RN32(g/amax) whenever that is
  *      finite);  v_i = RN32(y_i * r);  amax == 0 -> s = 0, codes 0.  Uniform grid g = 7, E2M1 g = 6.
