@@ -248,9 +248,9 @@ def test_grouped_small(counts, fmt):
     _grouped_case(x, w, dy, counts, 0x5A5A, 11, fmt=fmt)
 
 
-@pytest.mark.parametrize("cfg", ["moe7.9b", "moe124b"])
-def test_moe_layer_sampled(cfg):
+@pytest.mark.parametrize("cfg,fmt", [("moe7.9b", O.UNIFORM), ("moe124b", O.UNIFORM), ("moe7.9b", O.E2M1)])
+def test_moe_layer_sampled(cfg, fmt):
     wl = WL.CONFIGS[cfg]()
-    print(f"{cfg} counts={wl.counts[:4]}.. total={sum(wl.counts)}", flush=True)
-    _grouped_case(wl.x, wl.w, wl.dy, wl.counts, wl.sign_mask, wl.seed, rows_per_group=8, cols=np.arange(24),
-                  rng=np.random.default_rng(4))
+    print(f"{cfg} fmt {fmt} counts={wl.counts[:4]}.. total={sum(wl.counts)}", flush=True)
+    _grouped_case(wl.x, wl.w, wl.dy, wl.counts, wl.sign_mask, wl.seed, fmt=fmt, rows_per_group=8,
+                  cols=np.arange(24), rng=np.random.default_rng(4))

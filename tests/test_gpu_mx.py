@@ -211,3 +211,26 @@ def test_mx_dense_ffn_sampled():
         got = c[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")].cpu().numpy()
         want = _oracle_pass(bits, pas, wl.sign_mask, wl.seed, rows, cols)
         assert P.rel_fro(got, want) <= 1e-5, pas
+
+
+def test_mx_square_sampled():
+    """The 16384^3 layer at full size with the output types of the timed layer step (Y and dX bf16, dW fp32):
+    sampled operand rows bit-exact, sampled rows x columns of each pass against the oracle."""
+    wl = WL.square()
+    bits = P.layer_bits(wl)
+    rng = np.random.default_rng(6)
+    q = _layer((wl.x, wl.w, wl.dy), wl.sign_mask, wl.seed)
+    for name, (layout, rnd, st) in P.OPERANDS.items():
+        rows = P.sample(q[name].rows, 8, rng)
+        idx, e8 = _oracle_mx(bits[P.SOURCE[name]], layout, rnd, True, wl.sign_mask, wl.seed, st, rows)
+        _assert_mx_equal(q[name], idx, e8, rows, f"square {name}")
+    out = {"fwd_y": torch.bfloat16, "bwd_dx": torch.bfloat16, "bwd_dw": torch.float32}
+    for pas, (a, b, fn) in PASSES.items():
+        print(f"mx square {pas}", flush=True)
+        c = fn(q[a], q[b], out_dtype=out[pas])
+        rows = P.sample(c.shape[0], 8, rng)
+        cols = P.sample(c.shape[1], 32, rng)
+        got = P.to_numpy(c[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")])
+        del c
+        want = _oracle_pass(bits, pas, wl.sign_mask, wl.seed, rows, cols)
+        assert P.rel_fro(got, want) <= TOL[out[pas]], pas
