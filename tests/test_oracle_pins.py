@@ -1101,3 +1101,94 @@ def test_grouped_padding_to_32_for_power_of_two_scales():
         alone[:, :c] = ax[:, lo:lo + c]
         i2, e2 = O.quantize_rows_mx(alone, O.RTNE, True, 0x1234)
         assert np.array_equal(idx[:, lo:hi], i2) and np.array_equal(e8[:, lo // 32:hi // 32], e2)
+
+
+# ------------------------------------------------------------------------------------------------
+# binary32 rounding, the scale quotient and the 4-bit code patterns, against their definitions
+# ------------------------------------------------------------------------------------------------
+
+def _rn24_exact(q: Fraction, subnormal_floor: bool = True) -> Fraction:
+    """Round-half-even of an exact rational to 24 significant bits, on the binary32 grid below 2^-126 (gradual
+    underflow) when `subnormal_floor`, with no upper exponent limit (the caller decides what overflows)."""
+    if q == 0:
+        return Fraction(0)
+    sign = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    ulp_e = max(e - 23, -149) if subnormal_floor else e - 23
+    scaled = a / Fraction(2) ** ulp_e
+    n = floor(scaled)
+    rem = scaled - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sign * Fraction(n) * Fraction(2) ** ulp_e
+
+
+def test_round_to_fp32_against_exact_rounding():
+    """RN onto the binary32 grid: ties to even in the normal range, gradual underflow with ties below 2^-126,
+    and 24 significant bits kept past FLT_MAX (the RHT's largest outputs), against integer rounding."""
+    vals = [1 + 2.0 ** -24, 1 + 3 * 2.0 ** -24, 1 + 2.0 ** -24 + 2.0 ** -60, -(1 + 2.0 ** -24),
+            2.0 ** -150, 3 * 2.0 ** -150, 2.0 ** -150 + 2.0 ** -200, 5 * 2.0 ** -151, -(2.0 ** -149) * 1.5,
+            2.0 ** -126 - 2.0 ** -150, 2.0 ** -126 - 2.0 ** -151,
+            (2 - 2.0 ** -24) * 2.0 ** 127, (2 - 2.0 ** -23) * 2.0 ** 127, 2.0 ** 128 * (1 + 2.0 ** -24),
+            3.9 * 2.0 ** 127, -(2.0 ** 129) * (1 + 3 * 2.0 ** -25), 0.0]
+    rng = np.random.default_rng(12)
+    mant = rng.integers(1 << 52, 1 << 53, size=300).astype(np.float64) * 2.0 ** -52
+    expo = rng.integers(-160, 130, size=300)
+    vals += list(np.where(rng.random(300) < 0.5, -1, 1) * mant * np.exp2(expo.astype(np.float64)))
+    got = O.round_to_fp32(np.array(vals))
+    for v, g in zip(vals, got):
+        want = _rn24_exact(Fraction(float(v)))
+        assert Fraction(float(g)) == want, (v, float(g), float(want))
+
+
+@pytest.mark.parametrize("g", [7.0, 6.0, 4.0, 2.0])
+def test_scale_quotient_against_exact_division(g):
+    """s = RN32(amax/g) as IEEE binary32: subnormal for tiny amax, +inf where the rounded quotient reaches
+    2^128, for amax from the smallest bf16 subnormal up to the RHT's largest output (4x the bf16 maximum)."""
+    rng = np.random.default_rng(int(g))
+    bf16_max = (2 - 2.0 ** -7) * 2.0 ** 127
+    amax = [2.0 ** -133, 3 * 2.0 ** -133, 7 * 2.0 ** -126, 7 * 2.0 ** -126 * (1 - 2.0 ** -23), 1.0, 7.0, 6.0,
+            bf16_max, 4 * bf16_max, g * (2 - 2.0 ** -24) * 2.0 ** 127, g * (2 - 2.0 ** -23) * 2.0 ** 127]
+    m = rng.integers(1 << 23, 1 << 24, size=200).astype(np.float64) * 2.0 ** -23
+    e = rng.integers(-133, 129, size=200).astype(np.float64)
+    amax = np.array(amax + list(m * np.exp2(e)))
+    amax = O.round_to_fp32(amax)  # amax is an fp32-precision value, possibly past FLT_MAX
+    got = O.scale_rn32(amax, g)
+    assert got.dtype == np.float32
+    for a, s in zip(amax, got):
+        q = _rn24_exact(Fraction(float(a)) / Fraction(g))
+        if q >= Fraction(2) ** 128:
+            assert np.isinf(s) and s > 0, (a, s)
+        else:
+            assert Fraction(float(s)) == q, (a, float(s), float(q))
+
+
+def test_e2m1_nibbles_are_the_ocp_fp4_encoding():
+    """Every E2M1 nibble decodes, by the OCP FP4 definition (sign bit 3, exponent bits 2-1 with bias 1,
+    mantissa bit 0; exponent 0 is subnormal), to the level the oracle assigns to it; codes re-encode to the same
+    nibble, except -0 which the quantizer never emits (zero is +0)."""
+    nib = np.arange(16, dtype=np.uint8)
+    idx = O.nibbles_to_idx(nib, O.E2M1)
+    got = O.level_values(idx, O.E2M1)
+    for n in range(16):
+        s, ex, mt = (n >> 3) & 1, (n >> 1) & 3, n & 1
+        mag = mt * 0.5 if ex == 0 else (1 + mt / 2) * 2.0 ** (ex - 1)
+        assert got[n] == (-mag if s else mag), n
+    back = O.code_nibbles(idx, O.E2M1)
+    assert np.array_equal(back, np.where(nib == 8, 0, nib))
+
+
+def test_grid_top_levels_and_block_padding():
+    """g of each grid (Sec. 2.1: the largest level; Sec. 5 Q4's cut E2M1 grids) and the padding helper against
+    brute force."""
+    assert O.grid_gmax(O.UNIFORM) == 7.0 and O.grid_gmax(O.E2M1) == 6.0
+    assert O.grid_gmax(O.E2M1, 4) == 4.0 and O.grid_gmax(O.E2M1, 2) == 2.0
+    for block in (16, 32):
+        for n in range(0, 200):
+            want = next(m for m in range(0, n + block + 1, block) if m >= n)
+            assert O.pad16(n, block) == want
