@@ -114,3 +114,30 @@ def test_wide_span_blocks_two_operand_kernel():
         gc, gs = P.gpu_rows(q)
         idx, sc = P.oracle_operand(t, name, O.UNIFORM, O.RTNE, True, MASK, 0, 0)
         _assert_within_one_level(gc, gs, idx, sc, O.UNIFORM, f"two-operand {name}")
+
+
+@pytest.mark.parametrize("layout", ["rows", "cols"])
+@pytest.mark.parametrize("rounding", [O.RTNE, O.SR])
+def test_wide_span_blocks_power_of_two_scales(layout, rounding):
+    """The same blocks through the power-of-two-scale quantizer (two RHT16 halves per 1x32 block): a scale
+    exponent may move by one where a rounded output crosses a power of two; where it does not, every code stays
+    within one level of the exact transform's, and every dequantized value within two steps of the coarser grid."""
+    bits = _wide_tensor()
+    if layout == "cols":
+        bits = np.ascontiguousarray(bits.T)
+    q = U.mx_quantize(_device(bits), transpose=(layout == "cols"), rht=True, sign_mask=MASK, rounding=rounding,
+                      seed=11, stream_id=0)
+    gi = O.unpack_fp6(q.codes_rows().cpu().numpy())
+    ge = q.scales_rows().cpu().numpy().astype(np.int64)
+    a = O.bf16_bits_to_f32(bits) if layout == "rows" else np.ascontiguousarray(O.bf16_bits_to_f32(bits).T)
+    idx, e8 = O.quantize_rows_mx(a, rounding, True, MASK, 11, 0)
+    e8 = e8.astype(np.int64)
+    assert np.abs(ge - e8).max() <= 1, "a scale exponent more than one from the oracle's"
+    same = np.repeat(ge == e8, O.MX_BLOCK, axis=1)
+    assert np.abs(gi - idx)[same].max(initial=0) <= 1, "a code more than one level from the oracle's"
+    step = np.exp2(np.repeat(np.maximum(ge, e8), O.MX_BLOCK, axis=1).astype(np.float64) - 127)
+    deq_g = gi * np.exp2(np.repeat(ge, O.MX_BLOCK, axis=1).astype(np.float64) - 127)
+    deq_o = idx * np.exp2(np.repeat(e8, O.MX_BLOCK, axis=1).astype(np.float64) - 127)
+    assert np.all(np.abs(deq_g - deq_o) <= 2 * step)
+    print(f"power-of-two {layout} rounding {rounding}: {int((gi != idx).sum())} of {gi.size} codes and "
+          f"{int((ge != e8).sum())} of {ge.size} exponents differ from the exact transform's", flush=True)
