@@ -549,7 +549,7 @@ def measured_traffic(kind: str, workload: str):
 # CPU oracle baseline: the same layer step on a bounded sample of tokens
 # ---------------------------------------------------------------------------------------------------
 
-def cpu_baseline(wl, tokens: int = 1024, wrows: int = 1024, recipe: str = "ufp4"):
+def cpu_baseline(wl, tokens: int = 1280, wrows: int = 1280, recipe: str = "ufp4"):
     """The oracle's layer step (six quantizations, three fp64 GEMMs) on the first `tokens` rows of X and dY and
     the first `wrows` rows of W (dY's matching columns): the same arithmetic per element as the full layer, on
     a sample that fits a few seconds of host time. The rate is per sampled work."""
