@@ -442,8 +442,8 @@ int ufp4_gemm_bwd_dw(const ufp4_qtensor *dyt, const ufp4_qtensor *xt, void *dw_d
  *           [N, K] with leading dimension ldc, groups N * ldc apart). Qdyt [N, R], Qxt [K, R] from
  *           ufp4_quantize_grouped_t on the same offsets; the padded offsets pad_g are computed on the device.
  *
- * Offsets are read on the device: rows past M_total and reduction positions past R are ignored, groups with
- * no tokens give dW_g = 0. Operand checks as for the dense calls; besides, fwd_y takes plain operands, bwd_dx a
+ * Offsets are read on the device: rows past M_total and reduction positions past R are ignored, output rows
+ * past off_G (fwd_y, bwd_dx) are not written, groups with no tokens give dW_g = 0. Operand checks as for the dense calls; besides, fwd_y takes plain operands, bwd_dx a
  * plain Qdy and a plain or grouped-transposed Qwt (the same bytes: N is a multiple of 16), bwd_dw two
  * grouped-transposed operands (UFP4_LAYOUT_GROUPED_RED); other forms return UFP4_ERR_MISMATCH. num_groups up to
  * 65535.

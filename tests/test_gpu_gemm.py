@@ -237,6 +237,28 @@ def _grouped_case(x, w, dy, counts, mask, seed, fmt=O.UNIFORM, rows_per_group=No
             assert err <= tol, ("bwd_dw", g, err)
 
 
+def test_grouped_offsets_past_and_short_of_the_rows():
+    """Offsets are read on the device: a last offset beyond M_total computes exactly the rows that exist (the
+    same bytes as the offsets that end at M_total), and output rows past a last offset below M_total are not
+    written."""
+    g = torch.Generator().manual_seed(21)
+    E, N, K, M = 3, 48, 64, 200
+    x = torch.randn(M, K, generator=g).bfloat16().cuda()
+    w = (torch.randn(E * N, K, generator=g) * 0.05).bfloat16().cuda()
+    xq, wq = U.rht_quantize(x, sign_mask=0x1234), U.rht_quantize(w, sign_mask=0x1234)
+    dev = dict(dtype=torch.int64, device="cuda")
+    ref = U.gemm_fwd_y_grouped(xq, wq, torch.tensor([0, 60, 160, 200], **dev))
+    y = torch.full((M, N), 7.0, device="cuda")
+    U.gemm_fwd_y_grouped(xq, wq, torch.tensor([0, 60, 160, 1000], **dev), out=y)
+    torch.cuda.synchronize()
+    assert torch.equal(y, ref)
+    y = torch.full((M, N), 7.0, device="cuda")
+    U.gemm_fwd_y_grouped(xq, wq, torch.tensor([0, 60, 100, 150], **dev), out=y)
+    ref2 = U.gemm_fwd_y_grouped(xq, wq, torch.tensor([0, 60, 100, 200], **dev))
+    torch.cuda.synchronize()
+    assert torch.equal(y[:150], ref2[:150]) and torch.all(y[150:] == 7.0)
+
+
 @pytest.mark.parametrize("counts", [[5, 16, 33, 0, 19], [300, 0, 7], [129, 127, 250, 1]])
 @pytest.mark.parametrize("fmt", [O.UNIFORM, O.E2M1])
 def test_grouped_small(counts, fmt):
